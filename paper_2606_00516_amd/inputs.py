@@ -1,0 +1,344 @@
+"""Seeded synthetic inputs for one decoder-layer step over a token batch.
+
+This module only draws numbers and lays them out; it performs none of the
+layer arithmetic.  Both the HIP path (through the binding) and the CPU oracle
+consume what it produces, so it is the one piece of code they share.
+
+Workload shapes follow the per-iteration batch that the paper's scheduler
+forms (Sec. 3.1 "Timing Model": prefill rows and decode rows of requests whose
+KV is preserved; App. A.1: at most B rows per iteration under chunked
+prefill).  Layer shapes are Llama-style decoders (tiny, 8B-shaped,
+70B-shaped).  Readings of points the paper leaves open (seeds, gains, RoPE
+theta for the larger shapes, length-draw rules) are listed with each helper.
+
+Everything bf16 is held as torch.bfloat16 tensors; ``bits()`` gives the raw
+uint16 patterns the oracle works on.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import List, Optional, Sequence
+
+import numpy as np
+import torch
+
+PAGE_SIZE = 16
+BASE_SEED = 0
+
+
+@dataclasses.dataclass(frozen=True)
+class LayerShape:
+    name: str
+    hidden: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    ffn: int
+    rope_theta: float
+    rms_eps: float = 1e-5
+    page_size: int = PAGE_SIZE
+
+    @property
+    def group(self) -> int:
+        return self.n_q_heads // self.n_kv_heads
+
+    @property
+    def qkv_rows(self) -> int:
+        return (self.n_q_heads + 2 * self.n_kv_heads) * self.head_dim
+
+    def weight_bytes(self) -> int:
+        d, f = self.hidden, self.ffn
+        n = self.qkv_rows * d + d * self.n_q_heads * self.head_dim + 2 * f * d + d * f + 2 * d
+        return 2 * n
+
+
+# Tiny layer: hidden 256, GQA 4/2, head_dim 64, SwiGLU 688, RoPE theta 1e4.
+TINY = LayerShape("tiny", 256, 4, 2, 64, 688, 1e4)
+# Llama-3-8B-shaped layer.  RoPE theta 5e5 follows the Llama-3 convention
+# (the workload description does not state it).
+L8B = LayerShape("llama3-8b", 4096, 32, 8, 128, 14336, 5e5)
+# Llama-3-70B-shaped layer, same theta reading.
+L70B = LayerShape("llama3-70b", 8192, 64, 8, 128, 28672, 5e5)
+
+SHAPES = {s.name: s for s in (TINY, L8B, L70B)}
+
+
+def seeds(base: int = BASE_SEED) -> dict:
+    """Four independent integer seeds: weights, kv, batch, x."""
+    children = np.random.SeedSequence(base).spawn(4)
+    names = ("weights", "kv", "batch", "x")
+    return {n: int(c.generate_state(1, dtype=np.uint64)[0] & 0x7FFFFFFFFFFFFFFF)
+            for n, c in zip(names, children)}
+
+
+def _gen(device, seed: int) -> torch.Generator:
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    return g
+
+
+def bits(t: torch.Tensor) -> np.ndarray:
+    """Raw bf16 bit patterns of a bf16 tensor as a uint16 numpy array."""
+    assert t.dtype == torch.bfloat16
+    return t.detach().contiguous().cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+# ----------------------------------------------------------------------------
+# weights
+# ----------------------------------------------------------------------------
+
+def make_weights(shape: LayerShape, seed: Optional[int] = None, device="cpu",
+                 proj_std: float = 0.02) -> dict:
+    """Layer weights in the [out, in] layout, bf16.
+
+    Projections ~ N(0, proj_std), 0.02 by default; a larger spread makes the
+    attention scores peaky, which some self-checks need.  Norm gains ~ 1 + 0.1 N(0, 1): a gain of exactly
+    one would hide a dropped gain, and N(0, 0.02) gains would shrink the
+    residual stream fifty-fold.
+    w_qkv rows: q heads, then k heads, then v heads.  w_gate_up rows: gate then up.
+    """
+    if seed is None:
+        seed = seeds()["weights"]
+    g = _gen(device, seed)
+    d, hd = shape.hidden, shape.head_dim
+    f = shape.ffn
+
+    def proj(rows, cols):
+        w = torch.empty(rows, cols, dtype=torch.bfloat16, device=device)
+        # chunked draw keeps the fp32 temporary small for 70B-sized matrices
+        step = max(1, (1 << 26) // cols)
+        for r0 in range(0, rows, step):
+            r1 = min(rows, r0 + step)
+            w[r0:r1] = (torch.randn(r1 - r0, cols, generator=g, device=device) * proj_std).to(torch.bfloat16)
+        return w
+
+    def gain():
+        return (1.0 + 0.1 * torch.randn(d, generator=g, device=device)).to(torch.bfloat16)
+
+    return {
+        "attn_norm": gain(),
+        "w_qkv": proj(shape.qkv_rows, d),
+        "w_o": proj(d, shape.n_q_heads * hd),
+        "mlp_norm": gain(),
+        "w_gate_up": proj(2 * f, d),
+        "w_down": proj(d, f),
+    }
+
+
+# ----------------------------------------------------------------------------
+# batches
+# ----------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class Batch:
+    """One step's requests.
+
+    context_lens[i]: tokens already in the cache before the step.
+    chunk_lens[i]:  new rows this step (1 for a decode request).
+    Rows of request i are contiguous and requests are in list order.
+    """
+    context_lens: np.ndarray
+    chunk_lens: np.ndarray
+    label: str = ""
+
+    @property
+    def num_seqs(self) -> int:
+        return int(self.context_lens.shape[0])
+
+    @property
+    def num_tokens(self) -> int:
+        return int(self.chunk_lens.sum())
+
+    @property
+    def row_offsets(self) -> np.ndarray:
+        return np.concatenate([[0], np.cumsum(self.chunk_lens)]).astype(np.int64)
+
+    @property
+    def num_decode(self) -> int:
+        return int((self.chunk_lens == 1).sum())
+
+    def subset(self, idx: Sequence[int]) -> "Batch":
+        idx = np.asarray(idx, dtype=np.int64)
+        return Batch(self.context_lens[idx].copy(), self.chunk_lens[idx].copy(), self.label + "[subset]")
+
+    def concat(self, other: "Batch") -> "Batch":
+        return Batch(np.concatenate([self.context_lens, other.context_lens]),
+                     np.concatenate([self.chunk_lens, other.chunk_lens]),
+                     self.label + "+" + other.label)
+
+
+def _uniform_int(rng, lo, hi, n):
+    """Inclusive discrete uniform on [lo, hi]."""
+    return rng.integers(lo, hi + 1, size=n).astype(np.int32)
+
+
+def batch_decode(n: int, ctx_lo: int, ctx_hi: int, rng) -> Batch:
+    c = _uniform_int(rng, ctx_lo, ctx_hi, n)
+    return Batch(c, np.ones(n, dtype=np.int32), f"decode{n}")
+
+
+def batch_tiny(seed: Optional[int] = None, mode: str = "mixed") -> Batch:
+    """4 decode requests with contexts U{64..256} plus one 128-token prefill
+    chunk with no prior prefix.  mode: 'decode' | 'prefill' | 'mixed'."""
+    rng = np.random.default_rng(seeds()["batch"] if seed is None else seed)
+    dec = batch_decode(4, 64, 256, rng)
+    pre = Batch(np.zeros(1, np.int32), np.full(1, 128, np.int32), "prefill128")
+    return {"decode": dec, "prefill": pre, "mixed": dec.concat(pre)}[mode]
+
+
+def batch_8b_decode(seed: Optional[int] = None) -> Batch:
+    """64 decode requests, contexts U{512..4096}."""
+    rng = np.random.default_rng(seeds()["batch"] if seed is None else seed)
+    return batch_decode(64, 512, 4096, rng)
+
+
+def batch_8b_prefill(seed: Optional[int] = None, cap: int = 8192) -> Batch:
+    """8 prompts, lengths U{256..2048}, walked in order and cut so the total is
+    at most ``cap`` (a prompt that would overflow is truncated to the remainder,
+    later ones are dropped); no prior KV."""
+    rng = np.random.default_rng(seeds()["batch"] if seed is None else seed)
+    lens = _uniform_int(rng, 256, 2048, 8)
+    out, left = [], cap
+    for L in lens:
+        if left <= 0:
+            break
+        take = int(min(L, left))
+        out.append(take)
+        left -= take
+    n = np.asarray(out, np.int32)
+    return Batch(np.zeros_like(n), n, "prefill8")
+
+
+def batch_mixed_budget(r: float, budget: int, rng, dec_ctx=(1024, 8192),
+                       chunk=(256, 1024), prefix=(0, 2048)) -> Batch:
+    """Mixed step at a fixed token budget B and decode share r.
+
+    n_d = round(r B) decode rows (one per request) come first; prefill chunks
+    drawn from U{chunk} fill the remaining B - n_d rows, the last one cut to
+    what is left, each with a prior prefix drawn from U{prefix}.
+    """
+    n_d = int(round(r * budget))
+    dec = batch_decode(n_d, dec_ctx[0], dec_ctx[1], rng) if n_d else Batch(np.zeros(0, np.int32), np.zeros(0, np.int32))
+    left = budget - n_d
+    cl, pl = [], []
+    while left > 0:
+        L = int(min(rng.integers(chunk[0], chunk[1] + 1), left))
+        cl.append(L)
+        pl.append(int(rng.integers(prefix[0], prefix[1] + 1)))
+        left -= L
+    pre = Batch(np.asarray(pl, np.int32), np.asarray(cl, np.int32), "prefill")
+    b = dec.concat(pre) if n_d else pre
+    b.label = f"mb_r{r:.2f}_B{budget}"
+    return b
+
+
+def batch_8b_mixed(r: float, budget: int = 2048, seed: Optional[int] = None, **kw) -> Batch:
+    """The 8B-shaped mixed sweep point at decode share r (budget 2048)."""
+    s = seeds()["batch"] if seed is None else seed
+    rng = np.random.default_rng([s, int(round(r * 1000)), budget])
+    return batch_mixed_budget(r, budget, rng, **kw)
+
+
+# ----------------------------------------------------------------------------
+# paged KV pool
+# ----------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class KVPool:
+    k_cache: torch.Tensor          # [num_pages, n_kv, page, hd] bf16
+    v_cache: torch.Tensor
+    block_tables: torch.Tensor     # [num_seqs, max_pages_per_seq] int32 (-1 = unused)
+    num_pages: int
+    max_pages_per_seq: int
+
+    def clone(self) -> "KVPool":
+        return KVPool(self.k_cache.clone(), self.v_cache.clone(), self.block_tables.clone(),
+                      self.num_pages, self.max_pages_per_seq)
+
+    def to(self, device) -> "KVPool":
+        return KVPool(self.k_cache.to(device), self.v_cache.to(device), self.block_tables.to(device),
+                      self.num_pages, self.max_pages_per_seq)
+
+
+def pages_needed(batch: Batch, page: int = PAGE_SIZE) -> np.ndarray:
+    return (batch.context_lens.astype(np.int64) + batch.chunk_lens + page - 1) // page
+
+
+def make_block_tables(batch: Batch, spare_pages: int, seed: int, page: int = PAGE_SIZE,
+                      max_pages_per_seq: Optional[int] = None):
+    """A seeded permutation of the pool's page ids dealt out, in order, to the
+    (request, logical page) pairs; no page is shared.  Returns (tables, pool)."""
+    need = pages_needed(batch, page)
+    total = int(need.sum())
+    pool = total + spare_pages
+    rng = np.random.default_rng(seed)
+    perm = rng.permutation(pool).astype(np.int32)
+    mp = int(need.max()) if max_pages_per_seq is None else max_pages_per_seq
+    assert mp >= int(need.max()) if batch.num_seqs else True
+    bt = np.full((batch.num_seqs, max(mp, 1)), -1, np.int32)
+    k = 0
+    for i, n in enumerate(need):
+        bt[i, :n] = perm[k:k + n]
+        k += n
+    return bt, pool
+
+
+def make_kv_pool(shape: LayerShape, batch: Batch, seed: Optional[int] = None, device="cpu",
+                 spare_pages: int = 0, poison: bool = True,
+                 max_pages_per_seq: Optional[int] = None) -> KVPool:
+    """Paged bf16 K/V pool holding each request's prior context.
+
+    Prior positions (< context_len) hold bf16 N(0, 1).  With ``poison`` every
+    other slot (spare pages, the slots the step will append to, and slots past
+    the end of each request) holds bf16 NaN, so any read outside the block
+    table or past a request's length shows up as NaN in the output.
+    """
+    if seed is None:
+        seed = seeds()["kv"]
+    bt, pool = make_block_tables(batch, spare_pages, seed, shape.page_size, max_pages_per_seq)
+    nkv, P, hd = shape.n_kv_heads, shape.page_size, shape.head_dim
+    g = _gen(device, seed)
+    fill = float("nan") if poison else 0.0
+    kc = torch.full((pool, nkv, P, hd), fill, dtype=torch.bfloat16, device=device)
+    vc = torch.full((pool, nkv, P, hd), fill, dtype=torch.bfloat16, device=device)
+    bt_t = torch.from_numpy(bt).to(device)
+    for i in range(batch.num_seqs):
+        c = int(batch.context_lens[i])
+        if c == 0:
+            continue
+        npg = (c + P - 1) // P
+        pages = bt_t[i, :npg].long()
+        kvals = torch.randn(npg * P, nkv, hd, generator=g, device=device).to(torch.bfloat16)
+        vvals = torch.randn(npg * P, nkv, hd, generator=g, device=device).to(torch.bfloat16)
+        if poison and c % P:
+            kvals[c:] = float("nan")
+            vvals[c:] = float("nan")
+        # [npg*P, nkv, hd] -> [npg, nkv, P, hd]
+        kc[pages] = kvals.view(npg, P, nkv, hd).permute(0, 2, 1, 3)
+        vc[pages] = vvals.view(npg, P, nkv, hd).permute(0, 2, 1, 3)
+    return KVPool(kc, vc, bt_t, pool, bt.shape[1])
+
+
+def make_x(shape: LayerShape, num_tokens: int, seed: Optional[int] = None, device="cpu") -> torch.Tensor:
+    """Activations entering the layer: bf16 N(0, 1), [num_tokens, hidden]."""
+    if seed is None:
+        seed = seeds()["x"]
+    g = _gen(device, seed)
+    return torch.randn(num_tokens, shape.hidden, generator=g, device=device).to(torch.bfloat16)
+
+
+def relabel_pages(pool: KVPool, seed: int) -> KVPool:
+    """The same logical cache under a different physical page numbering."""
+    rng = np.random.default_rng(seed)
+    perm = torch.from_numpy(rng.permutation(pool.num_pages).astype(np.int64))
+    inv = torch.empty_like(perm)
+    inv[perm] = torch.arange(pool.num_pages)
+    kc = torch.empty_like(pool.k_cache)
+    vc = torch.empty_like(pool.v_cache)
+    kc[perm.to(kc.device)] = pool.k_cache
+    vc[perm.to(vc.device)] = pool.v_cache
+    bt = pool.block_tables.clone().long()
+    m = bt >= 0
+    bt[m] = perm.to(bt.device)[bt[m]]
+    return KVPool(kc, vc, bt.to(torch.int32), pool.num_pages, pool.max_pages_per_seq)

@@ -1,0 +1,433 @@
+"""Pins for the CPU oracle, against things other than the oracle itself:
+torch / transformers library routines, closed forms, brute force on tiny
+inputs, and invariances the definition fixes.  CPU only."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import layer as L
+from paper_2606_00516_amd import inputs as gen
+from tests._cases import make_case, oracle_cfg, tiny_case
+
+RNG = np.random.default_rng(1234)
+
+
+def maxrel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return float(np.max(np.abs(a - b)) / max(np.max(np.abs(b)), 1e-30))
+
+
+# ---------------------------------------------------------------- bf16 format
+
+def test_bf16_rounding_matches_torch():
+    x = np.concatenate([
+        RNG.standard_normal(100000).astype(np.float32) * 10.0,
+        # exact ties between two bf16 neighbours, both parities
+        ((np.arange(2000, dtype=np.uint32) << 16) | 0x8000).view(np.float32),
+        np.array([0.0, -0.0, np.inf, -np.inf, 3.0e38, -3.0e38, 1e-40], np.float32),
+    ])
+    ours = L.f32_to_bf16_bits(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
+    nan_bits = L.f32_to_bf16_bits(np.array([np.nan], np.float32))
+    assert np.isnan(L.bf16_bits_to_f32(nan_bits)).all()
+
+
+def test_bf16_widening_is_exact():
+    b = RNG.integers(0, 1 << 16, 50000).astype(np.uint16)
+    f = L.bf16_bits_to_f32(b)
+    ref = torch.from_numpy(b.view(np.int16)).view(torch.bfloat16).float().numpy()
+    ok = ~np.isnan(ref)
+    assert np.array_equal(f[ok].view(np.uint32), ref[ok].view(np.uint32))
+    assert np.isnan(f[~ok]).all()
+
+
+# ---------------------------------------------------------------- elementwise
+
+def test_rmsnorm_matches_torch_and_scale_invariance():
+    x = RNG.standard_normal((7, 256))
+    g = 1 + 0.1 * RNG.standard_normal(256)
+    ours = L.rmsnorm(x, g, 1e-5)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(x), (256,), torch.from_numpy(g), eps=1e-5).numpy()
+    assert maxrel(ours, ref) < 1e-12
+    # unit gain: output rms is 1 up to the eps term; scale invariant
+    u = L.rmsnorm(x * 1e3, np.ones(256), 1e-5)
+    assert np.allclose(np.sqrt(np.mean(u ** 2, axis=-1)), 1.0, atol=1e-9)
+    assert maxrel(u, L.rmsnorm(x, np.ones(256), 0.0)) < 1e-9
+
+
+def test_silu_matches_torch():
+    z = RNG.standard_normal(1000) * 6
+    ref = torch.nn.functional.silu(torch.from_numpy(z)).numpy()
+    assert maxrel(L.silu(z), ref) < 1e-14
+    assert L.silu(np.zeros(3))[0] == 0.0
+
+
+@pytest.mark.parametrize("hd,theta", [(64, 1e4), (128, 5e5)])
+def test_rope_identities(hd, theta):
+    u = RNG.standard_normal((3, hd))
+    # position 0 is the identity
+    assert np.array_equal(L.rope(u, 0, theta), u)
+    # complex-rotation form: pair (t, t + hd/2) is the complex number a + ib
+    # multiplied by exp(i pos omega_t), omega_t = theta^(-2t/hd)
+    pos = 937
+    half = hd // 2
+    z = (u[:, :half] + 1j * u[:, half:]) * np.exp(1j * pos * theta ** (-2.0 * np.arange(half) / hd))
+    ref = np.concatenate([z.real, z.imag], axis=-1)
+    assert maxrel(L.rope(u, pos, theta), ref) < 1e-12
+    # norm preserving, and q(m).k(n) depends on m - n only
+    assert np.allclose(np.linalg.norm(L.rope(u, pos, theta), axis=-1), np.linalg.norm(u, axis=-1))
+    q, k = RNG.standard_normal(hd), RNG.standard_normal(hd)
+    d1 = L.rope(q[None], 50, theta)[0] @ L.rope(k[None], 20, theta)[0]
+    d2 = L.rope(q[None], 1030, theta)[0] @ L.rope(k[None], 1000, theta)[0]
+    assert abs(d1 - d2) < 1e-9 * (1 + abs(d1))
+    # vectorised over rows equals per-row
+    rows = RNG.standard_normal((4, 2, hd))
+    ps = np.array([0, 5, 17, 4000])
+    vec = L.rope(rows, ps, theta)
+    for i, p in enumerate(ps):
+        assert np.array_equal(vec[i], L.rope(rows[i], p, theta))
+
+
+# ---------------------------------------------------------------- attention
+
+def test_softmax_rows_sum_to_one_and_mask_zero():
+    # With V = identity, attention returns the probability row itself.
+    n, Lk, G = 5, 12, 2
+    q = RNG.standard_normal((n, 2 * G, Lk)).astype(np.float64) * 3
+    K = RNG.standard_normal((Lk, 2, Lk))
+    V = np.broadcast_to(np.eye(Lk)[:, None, :], (Lk, 2, Lk)).copy()
+    pos = np.array([0, 3, 7, 10, 11])
+    P = L.causal_attention_seq(q, K, V, pos, G)
+    assert np.allclose(P.sum(-1), 1.0, atol=1e-12)
+    assert (P >= 0).all()
+    for j, p in enumerate(pos):
+        assert (P[j, :, p + 1:] == 0).all()
+    # single-query form agrees
+    p1 = L.attend_one(q[2, 1], K[: pos[2] + 1, 0, :], V[: pos[2] + 1, 0, :])
+    assert np.allclose(p1.sum(), 1.0, atol=1e-12)
+    assert np.allclose(p1, P[2, 1], atol=1e-12)
+
+
+def test_attention_vs_torch_sdpa_bruteforce():
+    # dense causal attention with GQA by torch's library kernel, fp64
+    n, c, nq, nkv, hd = 9, 13, 4, 2, 16
+    q = RNG.standard_normal((n, nq, hd))
+    K = RNG.standard_normal((c + n, nkv, hd))
+    V = RNG.standard_normal((c + n, nkv, hd))
+    pos = c + np.arange(n)
+    ours = L.causal_attention_seq(q, K, V, pos, nq // nkv)
+    mask = torch.from_numpy(np.arange(c + n)[None, :] <= pos[:, None])
+    tq = torch.from_numpy(q).permute(1, 0, 2)[None]
+    tk = torch.from_numpy(K).permute(1, 0, 2)[None]
+    tv = torch.from_numpy(V).permute(1, 0, 2)[None]
+    ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask, enable_gqa=True)
+    ref = ref[0].permute(1, 0, 2).numpy()
+    assert maxrel(ours, ref) < 1e-12
+    # explicit O(n^2) loop with a mask matrix
+    brute = np.zeros_like(q)
+    for j in range(n):
+        for h in range(nq):
+            g = h // (nq // nkv)
+            s = np.array([q[j, h] @ K[t, g] / np.sqrt(hd) if t <= pos[j] else -np.inf for t in range(c + n)])
+            w = np.exp(s - s.max())
+            w /= w.sum()
+            brute[j, h] = w @ V[:, g]
+    assert maxrel(ours, brute) < 1e-12
+
+
+def test_equal_keys_give_mean_of_values():
+    q = RNG.standard_normal((4, 8))
+    K = np.tile(RNG.standard_normal((1, 2, 8)), (6, 1, 1))
+    V = RNG.standard_normal((6, 2, 8))
+    out = L.causal_attention_seq(q[None], K, V, np.array([5]), 2)[0]
+    for h in range(4):
+        assert np.allclose(out[h], V[:, h // 2].mean(0), atol=1e-12)
+
+
+def test_paged_gather_identity_and_relabelling():
+    shape = gen.TINY
+    b = gen.batch_tiny(mode="decode")
+    pool = gen.make_kv_pool(shape, b, spare_pages=2, poison=False)
+    kc = gen.bits(pool.k_cache)
+    bt = pool.block_tables.numpy()
+    # identity layout: a request whose pages are 0..n-1 reads the pool as one
+    # contiguous [pos, head, dim] array
+    npg = 5
+    ident = np.arange(npg)
+    dense = L.gather_positions(kc, ident, npg * 16, 16)
+    ref = L.bf16_bits_to_f32(kc[:npg]).transpose(0, 2, 1, 3).reshape(npg * 16, shape.n_kv_heads, -1)
+    assert np.array_equal(dense, ref)
+    # relabelled physical pages give the same logical sequence
+    pool2 = gen.relabel_pages(pool, seed=9)
+    kc2, bt2 = gen.bits(pool2.k_cache), pool2.block_tables.numpy()
+    for i in range(b.num_seqs):
+        n = int(b.context_lens[i])
+        assert np.array_equal(L.gather_positions(kc, bt[i], n, 16), L.gather_positions(kc2, bt2[i], n, 16))
+
+
+# ---------------------------------------------------------------- whole layer
+
+def _hf_layer(shape, w_bits):
+    from transformers import LlamaConfig
+    from transformers.models.llama.modeling_llama import LlamaDecoderLayer, LlamaRotaryEmbedding
+    cfg = LlamaConfig(hidden_size=shape.hidden, intermediate_size=shape.ffn,
+                      num_attention_heads=shape.n_q_heads, num_key_value_heads=shape.n_kv_heads,
+                      head_dim=shape.head_dim, rms_norm_eps=shape.rms_eps, rope_theta=shape.rope_theta,
+                      attention_bias=False, mlp_bias=False)
+    cfg._attn_implementation = "sdpa"  # the eager path takes its softmax in fp32
+    layer = LlamaDecoderLayer(cfg, layer_idx=0).double()
+    rot = LlamaRotaryEmbedding(cfg).double()
+    # the library forms its frequencies in fp32; recompute them in fp64
+    hd = shape.head_dim
+    rot.inv_freq = shape.rope_theta ** (-torch.arange(0, hd, 2, dtype=torch.float64) / hd)
+    f = lambda k: torch.from_numpy(L.bf16_bits_to_f32(w_bits[k]).astype(np.float64))  # noqa: E731
+    nq, nkv, hd, ff = shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn
+    qkv, gu = f("w_qkv"), f("w_gate_up")
+    # the library's RMSNorm module computes in fp32; use torch's in fp64
+    layer.input_layernorm = torch.nn.RMSNorm(shape.hidden, eps=shape.rms_eps, dtype=torch.float64)
+    layer.post_attention_layernorm = torch.nn.RMSNorm(shape.hidden, eps=shape.rms_eps, dtype=torch.float64)
+    with torch.no_grad():
+        layer.self_attn.q_proj.weight.copy_(qkv[: nq * hd])
+        layer.self_attn.k_proj.weight.copy_(qkv[nq * hd:(nq + nkv) * hd])
+        layer.self_attn.v_proj.weight.copy_(qkv[(nq + nkv) * hd:])
+        layer.self_attn.o_proj.weight.copy_(f("w_o"))
+        layer.mlp.gate_proj.weight.copy_(gu[:ff])
+        layer.mlp.up_proj.weight.copy_(gu[ff:])
+        layer.mlp.down_proj.weight.copy_(f("w_down"))
+        layer.input_layernorm.weight.copy_(f("attn_norm"))
+        layer.post_attention_layernorm.weight.copy_(f("mlp_norm"))
+    return layer, rot
+
+
+class _Bf16Cache:
+    """Minimal KV cache for the library layer: holds a request's prior K/V and
+    stores each appended K/V rounded to bf16 (through fp32), as a bf16 paged
+    cache does; returns everything stored so far."""
+
+    def __init__(self, k_prior, v_prior):
+        self.k, self.v = k_prior, v_prior            # [1, n_kv, c, hd] fp64
+
+    def update(self, k, v, layer_idx, cache_kwargs=None):
+        rnd = lambda t: t.float().to(torch.bfloat16).double()  # noqa: E731
+        self.k = torch.cat([self.k, rnd(k)], dim=2)
+        self.v = torch.cat([self.v, rnd(v)], dim=2)
+        return self.k, self.v
+
+
+def _hf_reference(shape, o, seq):
+    """The library decoder layer in fp64 on request ``seq`` of an oracle input
+    set: returns (h1 - x, y - h1, y) for that request's rows."""
+    layer, rot = _hf_layer(shape, o["w_bits"])
+    c, n = int(o["context_lens"][seq]), int(o["chunk_lens"][seq])
+    r0 = int(np.sum(o["chunk_lens"][:seq]))
+    bt = o["block_tables"][seq]
+    pos = np.arange(c)
+    kp = L.bf16_bits_to_f32(o["k_cache"][bt[pos // 16], :, pos % 16, :]).astype(np.float64)
+    vp = L.bf16_bits_to_f32(o["v_cache"][bt[pos // 16], :, pos % 16, :]).astype(np.float64)
+    cache = _Bf16Cache(torch.from_numpy(kp).permute(1, 0, 2)[None], torch.from_numpy(vp).permute(1, 0, 2)[None])
+    x = torch.from_numpy(L.bf16_bits_to_f32(o["x_bits"][r0:r0 + n]).astype(np.float64))[None]
+    p = torch.arange(c, c + n)[None]
+    mask = torch.zeros(n, c + n, dtype=torch.float64)
+    mask[torch.arange(c + n)[None, :] > (c + torch.arange(n))[:, None]] = float("-inf")
+    # the library's rotary module forms angles in fp32; give the layer fp64
+    # cos/sin in its own (duplicated-halves) format instead
+    ang = p[0].double()[:, None] * rot.inv_freq[None, :]
+    emb = torch.cat([ang, ang], dim=-1)[None]
+    pe = (emb.cos(), emb.sin())
+    with torch.no_grad():
+        a = layer.input_layernorm(x)
+        attn_branch = layer.self_attn(a, attention_mask=mask[None, None], position_ids=p,
+                                      position_embeddings=pe, past_key_values=cache)[0]
+        h1 = x + attn_branch
+        mlp_branch = layer.mlp(layer.post_attention_layernorm(h1))
+    return attn_branch[0].numpy(), mlp_branch[0].numpy(), (h1 + mlp_branch)[0].numpy()
+
+
+# A prompt chunk with a paged prior prefix, and decode rows, against the
+# library decoder layer in fp64.  Projections N(0, 0.2) make the softmax
+# peaky so that RoPE, GQA and masking mistakes move the attention branch.
+_HF_BATCH = gen.Batch(np.array([40, 0, 77], np.int32), np.array([56, 33, 1], np.int32))
+
+
+@pytest.mark.parametrize("mode", ["batched", "exact"])
+def test_layer_matches_transformers_llama_layer(mode):
+    shape = gen.TINY
+    case = make_case(shape, _HF_BATCH, weights=gen.make_weights(shape, proj_std=0.2))
+    (y, inter), o = case.run_oracle(mode=mode, dtype=np.float64, intermediates=True)
+    o0 = case.oracle_inputs()
+    x = L.bf16_bits_to_f32(o0["x_bits"]).astype(np.float64)
+    off = _HF_BATCH.row_offsets
+    for i in range(_HF_BATCH.num_seqs):
+        rows = slice(off[i], off[i + 1])
+        attn_b, mlp_b, y_ref = _hf_reference(shape, o0, i)
+        assert maxrel(inter["h1"][rows] - x[rows], attn_b) < 1e-9
+        assert maxrel(y[rows] - inter["h1"][rows], mlp_b) < 1e-9
+        assert maxrel(y[rows], y_ref) < 1e-9
+
+
+def test_planted_mistakes_are_caught():
+    # Each mistake planted in a copy of the oracle's arithmetic moves the
+    # attention branch far outside the 1e-9 bound used above.
+    shape = gen.TINY
+    case = make_case(shape, _HF_BATCH, weights=gen.make_weights(shape, proj_std=0.2))
+    o0 = case.oracle_inputs()
+    x = L.bf16_bits_to_f32(o0["x_bits"]).astype(np.float64)
+    refs = [_hf_reference(shape, o0, i)[0] for i in range(_HF_BATCH.num_seqs)]
+    good_rope, good_cas = L.rope, L.causal_attention_seq
+
+    def interleaved(u, pos, theta):
+        hd = u.shape[-1]
+        perm = np.concatenate([np.arange(0, hd, 2), np.arange(1, hd, 2)])
+        return good_rope(u[..., perm], pos, theta)[..., np.argsort(perm)]
+
+    def gqa_modulo(q, K, V, positions, group):
+        # q head h -> kv head h % n_kv instead of h // G
+        nkv = K.shape[1]
+        idx = np.array([(h % nkv) * group + h // nkv for h in range(q.shape[1])])
+        out = good_cas(q[:, np.argsort(idx)], K, V, positions, group)
+        return out[:, idx]
+
+    def off_by_one_mask(q, K, V, positions, group):
+        return good_cas(q, K, V, np.asarray(positions) - 1 + (np.asarray(positions) == 0), group)
+
+    for name, patch in (("rope", ("rope", interleaved)), ("gqa", ("causal_attention_seq", gqa_modulo)),
+                        ("mask", ("causal_attention_seq", off_by_one_mask))):
+        setattr(L, patch[0], patch[1])
+        try:
+            W = oracle.prepare_weights(o0["w_bits"], o0["cfg"], np.float64)
+            y, inter = oracle.layer_step(o0["cfg"], W, o0["k_cache"].copy(), o0["v_cache"].copy(),
+                                         o0["block_tables"], o0["context_lens"], o0["chunk_lens"],
+                                         o0["x_bits"], intermediates=True)
+        finally:
+            L.rope, L.causal_attention_seq = good_rope, good_cas
+        off = _HF_BATCH.row_offsets
+        worst = max(maxrel(inter["h1"][off[i]:off[i + 1]] - x[off[i]:off[i + 1]], refs[i])
+                    for i in range(_HF_BATCH.num_seqs))
+        assert worst > 1e-3, name
+
+
+def test_single_token_no_context_reads_its_own_value():
+    # c = 0, n = 1: softmax over one key is exactly 1, so o_h = bf16(v_{h//G})
+    shape = gen.TINY
+    batch = gen.Batch(np.zeros(3, np.int32), np.ones(3, np.int32))
+    case = make_case(shape, batch)
+    (y, inter), _ = case.run_oracle(mode="exact", intermediates=True)
+    G = shape.group
+    v_bf = L.bf16_bits_to_f32(L.f32_to_bf16_bits(inter["v"]))
+    attn = inter["attn"].reshape(3, shape.n_q_heads, shape.head_dim)
+    for h in range(shape.n_q_heads):
+        assert np.array_equal(attn[:, h], v_bf[:, h // G])
+
+
+def test_exact_and_batched_modes_agree():
+    case = tiny_case("mixed")
+    y_e, _ = case.run_oracle(mode="exact")
+    y_b, _ = case.run_oracle(mode="batched")
+    assert np.isfinite(y_e).all()
+    assert maxrel(y_b, y_e) < 1e-5
+
+
+def test_cache_writes_only_new_slots():
+    case = tiny_case("mixed")
+    y, o = case.run_oracle()
+    before_k = gen.bits(case.pool.k_cache)
+    after_k = o["k_cache"]
+    bt = o["block_tables"]
+    written = set()
+    for i, (c, n) in enumerate(zip(case.batch.context_lens, case.batch.chunk_lens)):
+        for p in range(c, c + n):
+            written.add((int(bt[i][p // 16]), p % 16))
+    changed = set()
+    diff = ~((before_k == after_k) | (np.isnan(L.bf16_bits_to_f32(before_k)) & np.isnan(L.bf16_bits_to_f32(after_k))))
+    for pg, h, s, d in zip(*np.nonzero(diff)):
+        changed.add((int(pg), int(s)))
+    assert changed <= written
+    # every written slot holds finite values now (poison overwritten)
+    for pg, s in written:
+        assert np.isfinite(L.bf16_bits_to_f32(after_k[pg, :, s, :])).all()
+
+
+def test_batch_invariance_exact_mode():
+    # each request's rows are bitwise the same alone, in an EB batch, in the
+    # MB batch, and with the batch order reversed
+    shape = gen.TINY
+    mixed = gen.batch_tiny(mode="mixed")
+    case = make_case(shape, mixed)
+    y_mb, o = case.run_oracle(mode="exact")
+    off = mixed.row_offsets
+    W = oracle.prepare_weights(o["w_bits"], o["cfg"])
+    x_bits = gen.bits(case.x)
+    for order in (list(range(mixed.num_seqs)), list(reversed(range(mixed.num_seqs))), [4], [0, 2]):
+        sub = mixed.subset(order)
+        xs = np.concatenate([x_bits[off[i]:off[i + 1]] for i in order])
+        kc, vc = gen.bits(case.pool.k_cache).copy(), gen.bits(case.pool.v_cache).copy()
+        bt = case.pool.block_tables.numpy()[order]
+        y = oracle.layer_step(o["cfg"], W, kc, vc, bt, sub.context_lens, sub.chunk_lens, xs, mode="exact")
+        so = sub.row_offsets
+        for k, i in enumerate(order):
+            assert np.array_equal(y[so[k]:so[k + 1]], y_mb[off[i]:off[i + 1]])
+
+
+def test_page_relabelling_invariance():
+    case = tiny_case("mixed")
+    y1, _ = case.run_oracle(mode="batched")
+    case.pool = gen.relabel_pages(case.pool, seed=77)
+    y2, _ = case.run_oracle(mode="batched")
+    assert np.array_equal(y1, y2)
+
+
+def test_causality_future_rows_do_not_leak():
+    shape = gen.TINY
+    batch = gen.Batch(np.array([20], np.int32), np.array([40], np.int32))
+    case = make_case(shape, batch)
+    y1, o = case.run_oracle(mode="exact")
+    x2 = case.x.clone()
+    x2[25:] = x2[25:] * -3.0 + 1.0
+    case.x = x2
+    y2, _ = case.run_oracle(mode="exact")
+    assert np.array_equal(y1[:25], y2[:25])
+    assert not np.array_equal(y1[25:], y2[25:])
+
+
+def test_two_chunks_equal_one_chunk_and_decode_equals_prefill_row():
+    # prefill of n rows in one chunk vs two chunks where the second reads the
+    # first's bf16 K/V as its prefix; and a decode step on top of a c-token
+    # prefill equals row c of a (c+1)-token prefill.  Exact mode, bitwise.
+    shape = gen.TINY
+    n1, n2 = 37, 28
+    one = gen.Batch(np.zeros(1, np.int32), np.array([n1 + n2], np.int32))
+    case = make_case(shape, one, poison=True)
+    y_one, o = case.run_oracle(mode="exact")
+    W = oracle.prepare_weights(o["w_bits"], o["cfg"])
+    xb = gen.bits(case.x)
+    kc, vc = gen.bits(case.pool.k_cache).copy(), gen.bits(case.pool.v_cache).copy()
+    bt = case.pool.block_tables.numpy()
+    cfg = o["cfg"]
+    ya = oracle.layer_step(cfg, W, kc, vc, bt, [0], [n1], xb[:n1], mode="exact")
+    yb = oracle.layer_step(cfg, W, kc, vc, bt, [n1], [n2], xb[n1:], mode="exact")
+    assert np.array_equal(ya, y_one[:n1])
+    assert np.array_equal(yb, y_one[n1:])
+    kc, vc = gen.bits(case.pool.k_cache).copy(), gen.bits(case.pool.v_cache).copy()
+    c = n1 + n2 - 1
+    oracle.layer_step(cfg, W, kc, vc, bt, [0], [c], xb[:c], mode="exact")
+    yd = oracle.layer_step(cfg, W, kc, vc, bt, [c], [1], xb[c:c + 1], mode="exact")
+    assert np.array_equal(yd[0], y_one[c])
+
+
+def test_poisoned_slots_never_read():
+    case = tiny_case("mixed")
+    y, _ = case.run_oracle(mode="batched")
+    assert np.isfinite(y).all()
+
+
+def test_subset_equals_full_batch():
+    case = tiny_case("mixed")
+    y_all, _ = case.run_oracle(mode="batched")
+    y_sub, _ = case.run_oracle(mode="batched", seqs=[1, 4])
+    off = case.batch.row_offsets
+    for i in (1, 4):
+        assert np.array_equal(y_sub[off[i]:off[i + 1]], y_all[off[i]:off[i + 1]])
+    assert np.isnan(y_sub[off[0]:off[1]]).all()
