@@ -1,0 +1,189 @@
+/*
+ * eb_layer.h — C ABI of libeb.so: one transformer decoder-layer step over a
+ * token batch on an MI355X (gfx950), in exclusive-decode, exclusive-prefill
+ * and mixed batch modes.
+ *
+ * What a step is.  The paper prices one iteration of the serving loop as
+ * T_iter = alpha + beta * n_tok over a batch of n_tok rows whose decode share
+ * is r = n_decode / n_tok (Sec. 1); exclusive batching runs prefill and decode
+ * rows in separate iterations, mixed batching puts them in one (Sec. 1,
+ * Sec. 3.1 "Timing Model").  Requests keep their KV cache between iterations
+ * (Sec. 3.1 "System Model"), every iteration handles at most B rows under
+ * chunked prefill (App. A.1), and the cache is paged (Sec. 4.1
+ * "Implementation").  A decode request streams its whole cached context in
+ * attention (App. A.2, "Effect of decode context length").  One call here is
+ * one layer of such an iteration: for every request i with c_i tokens already
+ * cached and n_i new rows,
+ *
+ *   a = RMSNorm(x) g1;  q,k,v = a Wqkv^T;  RoPE(q,k) at pos = c_i + j;
+ *   append k,v (bf16) at pos;  o = causal GQA attention over keys 0..pos;
+ *   h1 = x + o Wo^T;  m = SiLU(RMSNorm(h1) g2 Wg^T) * (RMSNorm(h1) g2 Wu^T);
+ *   y = h1 + m Wd^T.
+ *
+ * Conventions shared by every entry point.
+ *  - bf16 data are passed as raw 16-bit patterns (uint16 storage), row-major,
+ *    contiguous.  Arithmetic is fp32 with bf16 inputs and outputs.
+ *  - Pointers named *_host are host memory; every other data pointer is
+ *    device memory of the current HIP device.  The caller owns all memory.
+ *  - `stream` is a hipStream_t passed as void* (NULL = default stream).  Calls
+ *    only enqueue work on it and return without waiting; buffers must stay
+ *    alive until the stream has finished the work.
+ *  - Every check runs before anything is enqueued: on a non-EB_OK return no
+ *    work was launched and no byte of device memory was written.  The
+ *    message for the last failure on the calling thread is eb_last_error().
+ *  - Supported shapes: head_dim in {64, 128}; n_q_heads a multiple of
+ *    n_kv_heads with n_q_heads / n_kv_heads in {1, 2, 4, 8}; page_size 16;
+ *    hidden and ffn multiples of 8.  Anything else is EB_ERR_CONFIG.
+ *  - A handle is not thread-safe; separate handles are independent.
+ */
+#ifndef EB_LAYER_H
+#define EB_LAYER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum eb_status {
+  EB_OK = 0,
+  EB_ERR_NULL = -1,      /* a required pointer is NULL */
+  EB_ERR_CONFIG = -2,    /* unsupported layer shape */
+  EB_ERR_BATCH = -3,     /* lengths inconsistent (n_i = 0, sum n_i != num_tokens, negative c_i, ...) */
+  EB_ERR_MODE = -4,      /* batch not allowed by the entry point's mode */
+  EB_ERR_PAGES = -5,     /* block table too short or holding ids outside [0, num_pages) or shared */
+  EB_ERR_WORKSPACE = -6, /* workspace NULL or smaller than eb_workspace_bytes() */
+  EB_ERR_LIMITS = -7,    /* batch larger than the handle was created for */
+  EB_ERR_HIP = -8        /* a HIP runtime call or kernel launch failed */
+} eb_status;
+
+typedef enum eb_mode {
+  EB_MODE_DECODE = 0,  /* exclusive decode: every n_i == 1 */
+  EB_MODE_PREFILL = 1, /* exclusive prefill: every n_i >= 1, any c_i */
+  EB_MODE_MIXED = 2    /* mixed: any n_i >= 1, decode and prefill rows in one step */
+} eb_mode;
+
+typedef enum eb_epilogue {
+  EB_EPI_STORE = 0,    /* out = bf16(A W^T) */
+  EB_EPI_RESIDUAL = 1, /* out = bf16(A W^T + residual) */
+  EB_EPI_SILU_MUL = 2  /* W holds [gate; up] (2F rows): out[:, f] = bf16(SiLU(g_f) * u_f), F = N / 2 */
+} eb_epilogue;
+
+/* Layer shape.  rms_eps: RMSNorm epsilon; rope_theta: RoPE base. */
+typedef struct eb_layer_config {
+  int32_t hidden, n_q_heads, n_kv_heads, head_dim, ffn, page_size;
+  float rms_eps, rope_theta;
+} eb_layer_config;
+
+/* Device pointers to bf16 weights in the [out, in] layout:
+ *   attn_norm, mlp_norm  [hidden]
+ *   w_qkv     [(n_q + 2 n_kv) head_dim, hidden], rows q heads, k heads, v heads
+ *   w_o       [hidden, n_q head_dim]
+ *   w_gate_up [2 ffn, hidden], rows gate then up
+ *   w_down    [hidden, ffn] */
+typedef struct eb_layer_weights {
+  const void *attn_norm, *w_qkv, *w_o, *mlp_norm, *w_gate_up, *w_down;
+} eb_layer_weights;
+
+/* Paged KV cache (device).  k_cache, v_cache: bf16 [num_pages, n_kv_heads,
+ * page_size, head_dim].  block_tables: int32 [num_seqs, max_pages_per_seq];
+ * logical page j of request i is physical page block_tables[i][j].  Entries
+ * past a request's last needed page are never read.  The library never
+ * allocates or frees pages. */
+typedef struct eb_kv_cache {
+  void *k_cache, *v_cache;
+  int32_t num_pages;
+  const int32_t *block_tables;
+  int32_t max_pages_per_seq;
+} eb_kv_cache;
+
+/* One step's requests.  context_lens_host[i] = c_i, tokens already cached
+ * before the step; chunk_lens_host[i] = n_i >= 1, new rows.  Rows of request
+ * i are x rows off_i .. off_i + n_i - 1 with off_i = n_0 + ... + n_{i-1}.
+ * num_tokens must equal the sum of n_i.  Both arrays are HOST memory. */
+typedef struct eb_batch {
+  int32_t num_seqs, num_tokens;
+  const int32_t *context_lens_host, *chunk_lens_host;
+} eb_batch;
+
+typedef struct eb_handle eb_handle;
+
+/* Create a handle for one layer shape on the current HIP device, sized for at
+ * most max_seqs requests and max_tokens rows per step.  Allocates small
+ * pinned host staging buffers.  Errors: EB_ERR_NULL, EB_ERR_CONFIG,
+ * EB_ERR_LIMITS (max_seqs or max_tokens < 1), EB_ERR_HIP. */
+eb_status eb_create(const eb_layer_config *cfg, int32_t max_seqs, int32_t max_tokens, eb_handle **out);
+
+/* Release a handle (waits for nothing: the caller synchronises first). */
+void eb_destroy(eb_handle *h);
+
+/* Bytes of device workspace a step over `batch` needs in `mode` (256-byte
+ * aligned base required).  Returns 0 if the batch is invalid for the mode. */
+size_t eb_workspace_bytes(const eb_handle *h, const eb_batch *batch, eb_mode mode);
+
+/* The three step entry points.  x: bf16 [num_tokens, hidden] (input rows),
+ * y: bf16 [num_tokens, hidden] (output; must not alias x).  Writes y, the
+ * workspace and exactly the cache slots of positions c_i .. c_i + n_i - 1;
+ * every other cache byte is left unchanged.  The block-table pages for all
+ * positions < c_i + n_i must exist (checked on the host by eb_validate;
+ * device block tables are not read back here).
+ *   decode : every n_i == 1 (EB_ERR_MODE otherwise)
+ *   prefill: any n_i >= 1
+ *   mixed  : any n_i >= 1; decode and prefill attention share one launch. */
+eb_status eb_layer_step_decode(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv,
+                               const eb_batch *batch, const void *x, void *y, void *ws, size_t ws_bytes,
+                               void *stream);
+eb_status eb_layer_step_prefill(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv,
+                                const eb_batch *batch, const void *x, void *y, void *ws, size_t ws_bytes,
+                                void *stream);
+eb_status eb_layer_step_mixed(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv,
+                              const eb_batch *batch, const void *x, void *y, void *ws, size_t ws_bytes,
+                              void *stream);
+
+/* Host-only check of a step's inputs (no GPU needed): shape support, lengths,
+ * mode constraints, and block-table contents (ids in [0, num_pages) for every
+ * needed logical page, no physical page used twice).  block_tables_host is
+ * int32 [num_seqs, max_pages_per_seq] in host memory. */
+eb_status eb_validate(const eb_layer_config *cfg, const eb_batch *batch, const int32_t *block_tables_host,
+                      int32_t num_pages, int32_t max_pages_per_seq, eb_mode mode);
+
+const char *eb_status_str(eb_status s);
+const char *eb_last_error(void); /* thread-local message of the last failure */
+
+/* ---- single operations of the step, same conventions (for parity tests) ---- */
+
+/* out[r] = bf16(x[r] / sqrt(mean(x[r]^2) + eps) * gamma), rows x hidden. */
+eb_status eb_op_rmsnorm(const eb_handle *h, const void *x, const void *gamma, void *out, int32_t rows,
+                        void *stream);
+
+/* out = epilogue(A W^T): A bf16 [M, K], W bf16 [N, K], out bf16 [M, N] (or
+ * [M, N/2] for EB_EPI_SILU_MUL), residual bf16 [M, N] (EB_EPI_RESIDUAL only).
+ * ws: device scratch of at least eb_op_gemm_workspace_bytes(M, N, K). */
+size_t eb_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
+eb_status eb_op_gemm(const void *A, const void *W, void *out, const void *residual, int32_t M, int32_t N,
+                     int32_t K, eb_epilogue epi, void *ws, size_t ws_bytes, void *stream);
+
+/* RoPE on the q and k heads of qkv (bf16 [num_tokens, (n_q + 2 n_kv) head_dim],
+ * the QKV projection output) at pos = c_i + j; q is rotated in place, the
+ * rotated k and the v heads are written to the cache. */
+eb_status eb_op_rope_kv_append(eb_handle *h, void *qkv, const eb_kv_cache *kv, const eb_batch *batch,
+                               void *ws, size_t ws_bytes, void *stream);
+
+/* Attention of every row over keys 0..pos of its request, reading rotated q
+ * from qkv and keys/values from the cache (already appended); out bf16
+ * [num_tokens, n_q head_dim].  mode selects the launch plan exactly as the
+ * step entry points do. */
+eb_status eb_op_attention(eb_handle *h, const void *qkv, const eb_kv_cache *kv, const eb_batch *batch,
+                          void *out, void *ws, size_t ws_bytes, eb_mode mode, void *stream);
+
+/* Dense copy of every request's cached positions 0 .. c_i + n_i - 1 through
+ * its block table: out_k, out_v bf16 [sum_i (c_i + n_i), n_kv_heads,
+ * head_dim], requests in order.  Pure paging: bit-exact. */
+eb_status eb_op_gather_kv(eb_handle *h, const eb_kv_cache *kv, const eb_batch *batch, void *out_k,
+                          void *out_v, void *ws, size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EB_LAYER_H */

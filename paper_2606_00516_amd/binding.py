@@ -1,0 +1,282 @@
+"""ctypes binding of libeb.so (C ABI in include/eb_layer.h).
+
+Argument marshalling only: torch tensors become device pointers, numpy
+length arrays become host pointers, the current torch stream becomes the
+hipStream_t.  Every computation runs in the library's HIP kernels.  Loading
+raises if the library has not been built; nothing here falls back to another
+implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libeb.so")
+
+EB_OK = 0
+STATUS = {0: "EB_OK", -1: "EB_ERR_NULL", -2: "EB_ERR_CONFIG", -3: "EB_ERR_BATCH", -4: "EB_ERR_MODE",
+          -5: "EB_ERR_PAGES", -6: "EB_ERR_WORKSPACE", -7: "EB_ERR_LIMITS", -8: "EB_ERR_HIP"}
+MODES = {"decode": 0, "prefill": 1, "mixed": 2}
+EPILOGUES = {"store": 0, "residual": 1, "silu_mul": 2}
+
+# every symbol include/eb_layer.h declares
+SYMBOLS = ("eb_create", "eb_destroy", "eb_workspace_bytes", "eb_layer_step_decode", "eb_layer_step_prefill",
+           "eb_layer_step_mixed", "eb_validate", "eb_status_str", "eb_last_error", "eb_op_rmsnorm",
+           "eb_op_gemm_workspace_bytes", "eb_op_gemm", "eb_op_rope_kv_append", "eb_op_attention",
+           "eb_op_gather_kv")
+
+
+class EbError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class LayerConfig(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")]
+
+
+class KvCache(ctypes.Structure):
+    _fields_ = [("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p), ("num_pages", ctypes.c_int32),
+                ("block_tables", ctypes.c_void_p), ("max_pages_per_seq", ctypes.c_int32)]
+
+
+class Batch(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("num_tokens", ctypes.c_int32),
+                ("context_lens_host", ctypes.c_void_p), ("chunk_lens_host", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libeb.so (raises if it is missing)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build() (hipcc, gfx950)")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I32, SZ, VP = ctypes.POINTER, ctypes.c_int32, ctypes.c_size_t, ctypes.c_void_p
+    sig = {
+        "eb_create": (I32, [P(LayerConfig), I32, I32, P(VP)]),
+        "eb_destroy": (None, [VP]),
+        "eb_workspace_bytes": (SZ, [VP, P(Batch), I32]),
+        "eb_validate": (I32, [P(LayerConfig), P(Batch), VP, I32, I32, I32]),
+        "eb_status_str": (ctypes.c_char_p, [I32]),
+        "eb_last_error": (ctypes.c_char_p, []),
+        "eb_op_rmsnorm": (I32, [VP, VP, VP, VP, I32, VP]),
+        "eb_op_gemm_workspace_bytes": (SZ, [I32, I32, I32]),
+        "eb_op_gemm": (I32, [VP, VP, VP, VP, I32, I32, I32, I32, VP, SZ, VP]),
+        "eb_op_rope_kv_append": (I32, [VP, VP, P(KvCache), P(Batch), VP, SZ, VP]),
+        "eb_op_attention": (I32, [VP, VP, P(KvCache), P(Batch), VP, VP, SZ, I32, VP]),
+        "eb_op_gather_kv": (I32, [VP, P(KvCache), P(Batch), VP, VP, VP, SZ, VP]),
+    }
+    for name in ("eb_layer_step_decode", "eb_layer_step_prefill", "eb_layer_step_mixed"):
+        sig[name] = (I32, [VP, P(LayerWeights), P(KvCache), P(Batch), VP, VP, VP, SZ, VP])
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != EB_OK:
+        raise EbError(status, lib().eb_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def config_of(shape) -> LayerConfig:
+    """LayerConfig from any object with the layer-shape attributes."""
+    return LayerConfig(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn,
+                       getattr(shape, "page_size", 16), float(shape.rms_eps), float(shape.rope_theta))
+
+
+class HostBatch:
+    """Holds the host int32 length arrays alive for the duration of a call."""
+
+    def __init__(self, context_lens, chunk_lens):
+        self.ctx = np.ascontiguousarray(context_lens, dtype=np.int32)
+        self.chk = np.ascontiguousarray(chunk_lens, dtype=np.int32)
+        self.c = Batch(len(self.ctx), int(self.chk.sum()), self.ctx.ctypes.data, self.chk.ctypes.data)
+
+
+def kv_struct(k_cache: torch.Tensor, v_cache: torch.Tensor, block_tables: torch.Tensor) -> KvCache:
+    assert k_cache.dtype == torch.bfloat16 and v_cache.dtype == torch.bfloat16
+    assert block_tables.dtype == torch.int32 and block_tables.dim() == 2
+    return KvCache(_ptr(k_cache), _ptr(v_cache), int(k_cache.shape[0]), _ptr(block_tables),
+                   int(block_tables.shape[1]))
+
+
+def weights_struct(w: dict) -> LayerWeights:
+    return LayerWeights(*[_ptr(w[k]) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")])
+
+
+class Handle:
+    """eb_create / eb_destroy."""
+
+    def __init__(self, shape, max_seqs: int, max_tokens: int):
+        self.shape = shape
+        self.cfg = config_of(shape)
+        h = ctypes.c_void_p()
+        _check(lib().eb_create(ctypes.byref(self.cfg), int(max_seqs), int(max_tokens), ctypes.byref(h)))
+        self.h = h
+
+    def close(self):
+        if getattr(self, "h", None) is not None and self.h.value:
+            lib().eb_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def eb_workspace_bytes(h: Handle, context_lens, chunk_lens, mode: str) -> int:
+    hb = HostBatch(context_lens, chunk_lens)
+    return int(lib().eb_workspace_bytes(h.h, ctypes.byref(hb.c), MODES[mode]))
+
+
+def alloc_workspace(nbytes: int, device="cuda") -> torch.Tensor:
+    # torch's caching allocator returns 256-byte (or better) aligned blocks
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def _step(name, h: Handle, weights: dict, k_cache, v_cache, block_tables, context_lens, chunk_lens,
+          x: torch.Tensor, y: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, stream=None):
+    hb = HostBatch(context_lens, chunk_lens)
+    mode = {"eb_layer_step_decode": "decode", "eb_layer_step_prefill": "prefill",
+            "eb_layer_step_mixed": "mixed"}[name]
+    if y is None:
+        y = torch.empty_like(x)
+    if ws is None:
+        ws = alloc_workspace(lib().eb_workspace_bytes(h.h, ctypes.byref(hb.c), MODES[mode]), x.device)
+    kv = kv_struct(k_cache, v_cache, block_tables)
+    w = weights_struct(weights)
+    _check(getattr(lib(), name)(h.h, ctypes.byref(w), ctypes.byref(kv), ctypes.byref(hb.c), _ptr(x), _ptr(y),
+                                _ptr(ws), ws.numel(), _stream(stream)))
+    return y
+
+
+def eb_layer_step_decode(h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x, y=None, ws=None,
+                         stream=None):
+    return _step("eb_layer_step_decode", h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x,
+                 y, ws, stream)
+
+
+def eb_layer_step_prefill(h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x, y=None, ws=None,
+                          stream=None):
+    return _step("eb_layer_step_prefill", h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x,
+                 y, ws, stream)
+
+
+def eb_layer_step_mixed(h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x, y=None, ws=None,
+                        stream=None):
+    return _step("eb_layer_step_mixed", h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x,
+                 y, ws, stream)
+
+
+def eb_validate(shape, context_lens, chunk_lens, block_tables_host: np.ndarray, num_pages: int, mode: str) -> int:
+    """Host-only validation; returns the status code (0 = EB_OK)."""
+    cfg = config_of(shape)
+    hb = HostBatch(context_lens, chunk_lens)
+    bt = np.ascontiguousarray(block_tables_host, dtype=np.int32)
+    mp = bt.shape[1] if bt.ndim == 2 else 0
+    return int(lib().eb_validate(ctypes.byref(cfg), ctypes.byref(hb.c), bt.ctypes.data if bt.size else None,
+                                 int(num_pages), int(mp), MODES.get(mode, mode) if isinstance(mode, str) else mode))
+
+
+def eb_last_error() -> str:
+    return lib().eb_last_error().decode()
+
+
+def eb_status_str(status: int) -> str:
+    return lib().eb_status_str(int(status)).decode()
+
+
+def eb_op_rmsnorm(h: Handle, x: torch.Tensor, gamma: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+    out = torch.empty_like(x) if out is None else out
+    _check(lib().eb_op_rmsnorm(h.h, _ptr(x), _ptr(gamma), _ptr(out), int(x.shape[0]), _stream(stream)))
+    return out
+
+
+def eb_op_gemm(A: torch.Tensor, W: torch.Tensor, epilogue: str = "store", residual: Optional[torch.Tensor] = None,
+               out: Optional[torch.Tensor] = None, stream=None):
+    M, K = A.shape
+    N = W.shape[0]
+    ncol = N // 2 if epilogue == "silu_mul" else N
+    out = torch.empty(M, ncol, dtype=torch.bfloat16, device=A.device) if out is None else out
+    nb = int(lib().eb_op_gemm_workspace_bytes(M, N, K))
+    ws = alloc_workspace(nb, A.device)
+    _check(lib().eb_op_gemm(_ptr(A), _ptr(W), _ptr(out), _ptr(residual), M, N, K, EPILOGUES[epilogue], _ptr(ws),
+                            ws.numel(), _stream(stream)))
+    return out
+
+
+def _op_ws(h, hb, mode="mixed", device="cuda"):
+    return alloc_workspace(lib().eb_workspace_bytes(h.h, ctypes.byref(hb.c), MODES[mode]), device)
+
+
+def eb_op_rope_kv_append(h: Handle, qkv: torch.Tensor, k_cache, v_cache, block_tables, context_lens, chunk_lens,
+                         stream=None):
+    hb = HostBatch(context_lens, chunk_lens)
+    ws = _op_ws(h, hb, device=qkv.device)
+    kv = kv_struct(k_cache, v_cache, block_tables)
+    _check(lib().eb_op_rope_kv_append(h.h, _ptr(qkv), ctypes.byref(kv), ctypes.byref(hb.c), _ptr(ws), ws.numel(),
+                                      _stream(stream)))
+    return qkv
+
+
+def eb_op_attention(h: Handle, qkv: torch.Tensor, k_cache, v_cache, block_tables, context_lens, chunk_lens,
+                    mode: str = "mixed", out: Optional[torch.Tensor] = None, stream=None):
+    hb = HostBatch(context_lens, chunk_lens)
+    s = h.shape
+    T = int(hb.chk.sum())
+    out = torch.empty(T, s.n_q_heads * s.head_dim, dtype=torch.bfloat16, device=qkv.device) if out is None else out
+    ws = _op_ws(h, hb, mode if mode in MODES else "mixed", qkv.device)
+    kv = kv_struct(k_cache, v_cache, block_tables)
+    _check(lib().eb_op_attention(h.h, _ptr(qkv), ctypes.byref(kv), ctypes.byref(hb.c), _ptr(out), _ptr(ws),
+                                 ws.numel(), MODES[mode], _stream(stream)))
+    return out
+
+
+def eb_op_gather_kv(h: Handle, k_cache, v_cache, block_tables, context_lens, chunk_lens, stream=None):
+    hb = HostBatch(context_lens, chunk_lens)
+    s = h.shape
+    total = int((hb.ctx.astype(np.int64) + hb.chk).sum())
+    ok = torch.empty(total, s.n_kv_heads, s.head_dim, dtype=torch.bfloat16, device=k_cache.device)
+    ov = torch.empty_like(ok)
+    ws = _op_ws(h, hb, device=k_cache.device)
+    kv = kv_struct(k_cache, v_cache, block_tables)
+    _check(lib().eb_op_gather_kv(h.h, ctypes.byref(kv), ctypes.byref(hb.c), _ptr(ok), _ptr(ov), _ptr(ws), ws.numel(),
+                                 _stream(stream)))
+    return ok, ov

@@ -1,0 +1,442 @@
+// C ABI of libeb.so: handle, workspace carve-up, validation and the launch
+// sequence of one decoder-layer step on the caller's stream.
+#include <hip/hip_runtime.h>
+#include <string.h>
+
+#include <string>
+
+#include "../../include/eb_layer.h"
+#include "eb_internal.h"
+#include "host_plan.h"
+
+using namespace eb;
+
+namespace {
+
+thread_local std::string g_err;
+
+eb_status fail(eb_status s, const std::string &msg) {
+  g_err = msg;
+  return s;
+}
+
+constexpr int kRing = 4;  // pinned staging slots per handle
+
+size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
+
+Shape shape_of(const eb_layer_config &c) {
+  return Shape{c.hidden, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn, c.rms_eps, c.rope_theta};
+}
+
+// Byte offsets of everything a step keeps in the caller's workspace.
+struct WsLayout {
+  size_t meta = 0, act = 0, qkv = 0, attn = 0, h1 = 0, mlp = 0, part_o = 0, part_ml = 0, gemm = 0, total = 0;
+};
+
+WsLayout layout_for(const Shape &s, const HostPlan &p, bool full_step) {
+  WsLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  const size_t T = (size_t)p.T;
+  L.meta = take(p.blob.size() * sizeof(int32_t));
+  L.part_o = take((size_t)p.total_splits * s.nkv * s.group() * s.hd * sizeof(float));
+  L.part_ml = take((size_t)p.total_splits * s.nkv * s.group() * 2 * sizeof(float));
+  if (full_step) {
+    L.act = take(T * s.hidden * 2);
+    L.qkv = take(T * s.qkv_cols() * 2);
+    L.attn = take(T * s.nq * s.hd * 2);
+    L.h1 = take(T * s.hidden * 2);
+    L.mlp = take(T * s.ffn * 2);
+    size_t g = 0;
+    const int M = p.T;
+    const GemmPlan plans[4] = {plan_gemm(M, s.qkv_cols(), s.hidden, EPI_STORE),
+                               plan_gemm(M, s.hidden, s.nq * s.hd, EPI_RESIDUAL),
+                               plan_gemm(M, 2 * s.ffn, s.hidden, EPI_SILU_MUL),
+                               plan_gemm(M, s.hidden, s.ffn, EPI_RESIDUAL)};
+    for (const auto &gp : plans) g = gp.ws_bytes > g ? gp.ws_bytes : g;
+    L.gemm = take(g);
+  }
+  L.total = off;
+  return L;
+}
+
+DevMeta meta_at(const HostPlan &p, const int32_t *dev) {
+  DevMeta m;
+  m.seq_ctx = dev + p.o_ctx;
+  m.seq_len = dev + p.o_len;
+  m.seq_row = dev + p.o_row;
+  m.row_seq = dev + p.o_row_seq;
+  m.row_pos = dev + p.o_row_pos;
+  m.dec_seq = dev + p.o_dec_seq;
+  m.dec_split_off = dev + p.o_dec_off;
+  m.comb_list = dev + p.o_comb;
+  m.tile_seq = dev + p.o_tseq;
+  m.tile_qb = dev + p.o_tqb;
+  m.gather_off = dev + p.o_goff;
+  m.S = p.S;
+  m.T = p.T;
+  m.n_dec = p.n_dec;
+  m.total_splits = p.total_splits;
+  m.n_comb = p.n_comb;
+  m.n_tiles = p.n_tiles;
+  return m;
+}
+
+eb_status hip_fail(hipError_t e, const char *what) {
+  return fail(EB_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+}  // namespace
+
+struct eb_handle {
+  eb_layer_config cfg;
+  Shape shape;
+  int32_t max_seqs, max_tokens;
+  int device;
+  size_t slot_cap;  // int32 elements per pinned slot
+  int32_t *pinned[kRing];
+  hipEvent_t ev[kRing];
+  bool used[kRing];
+  int next;
+};
+
+namespace {
+
+// Copy a plan's metadata into the workspace through the next pinned slot,
+// asynchronously on the stream.
+eb_status stage_meta(eb_handle *h, const HostPlan &p, void *ws, const WsLayout &L, hipStream_t st) {
+  const int k = h->next;
+  h->next = (h->next + 1) % kRing;
+  if (p.blob.size() > h->slot_cap) return fail(EB_ERR_LIMITS, "step metadata exceeds the handle's staging buffer");
+  if (h->used[k]) {
+    hipError_t e = hipEventSynchronize(h->ev[k]);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  }
+  memcpy(h->pinned[k], p.blob.data(), p.blob.size() * sizeof(int32_t));
+  hipError_t e = hipMemcpyAsync(static_cast<char *>(ws) + L.meta, h->pinned[k], p.blob.size() * sizeof(int32_t),
+                                hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(metadata)");
+  e = hipEventRecord(h->ev[k], st);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
+  h->used[k] = true;
+  return EB_OK;
+}
+
+eb_status check_kv(const eb_kv_cache *kv) {
+  if (!kv) return fail(EB_ERR_NULL, "kv is NULL");
+  if (!kv->k_cache || !kv->v_cache || !kv->block_tables) return fail(EB_ERR_NULL, "kv cache or block table is NULL");
+  if (kv->num_pages <= 0 || kv->max_pages_per_seq <= 0)
+    return fail(EB_ERR_PAGES, "num_pages and max_pages_per_seq must be positive");
+  return EB_OK;
+}
+
+eb_status check_common(const eb_handle *h, const eb_batch *b, eb_mode mode, int32_t max_pages) {
+  if (!h) return fail(EB_ERR_NULL, "handle is NULL");
+  std::string err;
+  eb_status s = check_batch(h->cfg, b, max_pages, mode, err);
+  if (s != EB_OK) return fail(s, err);
+  if (b->num_seqs > h->max_seqs || b->num_tokens > h->max_tokens)
+    return fail(EB_ERR_LIMITS, "batch larger than the handle's max_seqs / max_tokens");
+  return EB_OK;
+}
+
+eb_status check_ws(void *ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return EB_OK;
+  if (!ws) return fail(EB_ERR_WORKSPACE, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(EB_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < need)
+    return fail(EB_ERR_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes, got " +
+                                      std::to_string(ws_bytes));
+  return EB_OK;
+}
+
+KV kv_of(const eb_kv_cache *kv) {
+  return KV{static_cast<uint16_t *>(kv->k_cache), static_cast<uint16_t *>(kv->v_cache), kv->block_tables,
+            kv->num_pages, kv->max_pages_per_seq};
+}
+
+eb_status run_step(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv, const eb_batch *b, const void *x,
+                   void *y, void *ws, size_t ws_bytes, void *stream, eb_mode mode) {
+  if (!h) return fail(EB_ERR_NULL, "handle is NULL");
+  if (!w || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm || !w->w_gate_up || !w->w_down)
+    return fail(EB_ERR_NULL, "a weight pointer is NULL");
+  eb_status s = check_kv(kv);
+  if (s != EB_OK) return s;
+  s = check_common(h, b, mode, kv->max_pages_per_seq);
+  if (s != EB_OK) return s;
+  if (b->num_tokens == 0) return EB_OK;
+  if (!x || !y) return fail(EB_ERR_NULL, "x or y is NULL");
+  if (x == y) return fail(EB_ERR_BATCH, "y must not alias x");
+  HostPlan p;
+  build_plan(h->cfg, *b, p);
+  const Shape &sh = h->shape;
+  const WsLayout L = layout_for(sh, p, true);
+  s = check_ws(ws, ws_bytes, L.total);
+  if (s != EB_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char *base = static_cast<char *>(ws);
+  s = stage_meta(h, p, ws, L, st);
+  if (s != EB_OK) return s;
+  const DevMeta m = meta_at(p, reinterpret_cast<const int32_t *>(base + L.meta));
+  const KV kvd = kv_of(kv);
+  uint16_t *act = reinterpret_cast<uint16_t *>(base + L.act);
+  uint16_t *qkv = reinterpret_cast<uint16_t *>(base + L.qkv);
+  uint16_t *attn = reinterpret_cast<uint16_t *>(base + L.attn);
+  uint16_t *h1 = reinterpret_cast<uint16_t *>(base + L.h1);
+  uint16_t *mlp = reinterpret_cast<uint16_t *>(base + L.mlp);
+  float *part_o = reinterpret_cast<float *>(base + L.part_o);
+  float *part_ml = reinterpret_cast<float *>(base + L.part_ml);
+  void *gws = base + L.gemm;
+  const uint16_t *xin = static_cast<const uint16_t *>(x);
+  uint16_t *yout = static_cast<uint16_t *>(y);
+  const int T = p.T;
+  hipError_t e;
+#define EB_TRY(call, what)                 \
+  if ((e = (call)) != hipSuccess) {        \
+    return hip_fail(e, what);              \
+  }
+  EB_TRY(launch_rmsnorm(xin, static_cast<const uint16_t *>(w->attn_norm), act, T, sh.hidden, sh.eps, st), "rmsnorm1");
+  EB_TRY(launch_gemm(plan_gemm(T, sh.qkv_cols(), sh.hidden, EPI_STORE), act, static_cast<const uint16_t *>(w->w_qkv),
+                     qkv, nullptr, T, sh.qkv_cols(), sh.hidden, EPI_STORE, gws, st),
+         "qkv gemm");
+  EB_TRY(launch_rope_append(sh, qkv, kvd, m, st), "rope/kv append");
+  const int kind = mode == EB_MODE_DECODE ? 0 : (mode == EB_MODE_PREFILL ? 1 : 2);
+  EB_TRY(launch_attention(sh, qkv, kvd, m, attn, part_o, part_ml, kind, st), "attention");
+  EB_TRY(launch_gemm(plan_gemm(T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL), attn, static_cast<const uint16_t *>(w->w_o),
+                     h1, xin, T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, gws, st),
+         "o gemm");
+  EB_TRY(launch_rmsnorm(h1, static_cast<const uint16_t *>(w->mlp_norm), act, T, sh.hidden, sh.eps, st), "rmsnorm2");
+  EB_TRY(launch_gemm(plan_gemm(T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL), act,
+                     static_cast<const uint16_t *>(w->w_gate_up), mlp, nullptr, T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL,
+                     gws, st),
+         "gate/up gemm");
+  EB_TRY(launch_gemm(plan_gemm(T, sh.hidden, sh.ffn, EPI_RESIDUAL), mlp, static_cast<const uint16_t *>(w->w_down), yout,
+                     h1, T, sh.hidden, sh.ffn, EPI_RESIDUAL, gws, st),
+         "down gemm");
+#undef EB_TRY
+  return EB_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *eb_status_str(eb_status s) {
+  switch (s) {
+    case EB_OK: return "EB_OK";
+    case EB_ERR_NULL: return "EB_ERR_NULL";
+    case EB_ERR_CONFIG: return "EB_ERR_CONFIG";
+    case EB_ERR_BATCH: return "EB_ERR_BATCH";
+    case EB_ERR_MODE: return "EB_ERR_MODE";
+    case EB_ERR_PAGES: return "EB_ERR_PAGES";
+    case EB_ERR_WORKSPACE: return "EB_ERR_WORKSPACE";
+    case EB_ERR_LIMITS: return "EB_ERR_LIMITS";
+    case EB_ERR_HIP: return "EB_ERR_HIP";
+  }
+  return "unknown status";
+}
+
+const char *eb_last_error(void) { return g_err.c_str(); }
+
+eb_status eb_create(const eb_layer_config *cfg, int32_t max_seqs, int32_t max_tokens, eb_handle **out) {
+  if (!out) return fail(EB_ERR_NULL, "out is NULL");
+  *out = nullptr;
+  std::string err;
+  eb_status s = check_config(cfg, err);
+  if (s != EB_OK) return fail(s, err);
+  if (max_seqs < 1 || max_tokens < 1) return fail(EB_ERR_LIMITS, "max_seqs and max_tokens must be >= 1");
+  eb_handle *h = new eb_handle();
+  h->cfg = *cfg;
+  h->shape = shape_of(*cfg);
+  h->max_seqs = max_seqs;
+  h->max_tokens = max_tokens;
+  h->next = 0;
+  hipError_t e = hipGetDevice(&h->device);
+  if (e != hipSuccess) {
+    delete h;
+    return hip_fail(e, "hipGetDevice");
+  }
+  h->slot_cap = plan_capacity(max_seqs, max_tokens, cfg->n_q_heads / cfg->n_kv_heads);
+  for (int k = 0; k < kRing; ++k) {
+    h->pinned[k] = nullptr;
+    h->ev[k] = nullptr;
+    h->used[k] = false;
+  }
+  for (int k = 0; k < kRing; ++k) {
+    e = hipHostMalloc(reinterpret_cast<void **>(&h->pinned[k]), h->slot_cap * sizeof(int32_t), hipHostMallocDefault);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev[k], hipEventDisableTiming);
+    if (e != hipSuccess) {
+      eb_destroy(h);
+      return hip_fail(e, "pinned staging allocation");
+    }
+  }
+  *out = h;
+  return EB_OK;
+}
+
+void eb_destroy(eb_handle *h) {
+  if (!h) return;
+  for (int k = 0; k < kRing; ++k) {
+    if (h->ev[k]) {
+      if (h->used[k]) (void)hipEventSynchronize(h->ev[k]);
+      (void)hipEventDestroy(h->ev[k]);
+    }
+    if (h->pinned[k]) (void)hipHostFree(h->pinned[k]);
+  }
+  delete h;
+}
+
+size_t eb_workspace_bytes(const eb_handle *h, const eb_batch *batch, eb_mode mode) {
+  if (!h) return 0;
+  std::string err;
+  if (check_batch(h->cfg, batch, -1, mode, err) != EB_OK) return 0;
+  HostPlan p;
+  build_plan(h->cfg, *batch, p);
+  return layout_for(h->shape, p, true).total;
+}
+
+eb_status eb_layer_step_decode(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv, const eb_batch *batch,
+                               const void *x, void *y, void *ws, size_t ws_bytes, void *stream) {
+  return run_step(h, w, kv, batch, x, y, ws, ws_bytes, stream, EB_MODE_DECODE);
+}
+
+eb_status eb_layer_step_prefill(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv, const eb_batch *batch,
+                                const void *x, void *y, void *ws, size_t ws_bytes, void *stream) {
+  return run_step(h, w, kv, batch, x, y, ws, ws_bytes, stream, EB_MODE_PREFILL);
+}
+
+eb_status eb_layer_step_mixed(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv, const eb_batch *batch,
+                              const void *x, void *y, void *ws, size_t ws_bytes, void *stream) {
+  return run_step(h, w, kv, batch, x, y, ws, ws_bytes, stream, EB_MODE_MIXED);
+}
+
+eb_status eb_validate(const eb_layer_config *cfg, const eb_batch *batch, const int32_t *block_tables_host,
+                      int32_t num_pages, int32_t max_pages_per_seq, eb_mode mode) {
+  std::string err;
+  eb_status s = check_config(cfg, err);
+  if (s != EB_OK) return fail(s, err);
+  if (max_pages_per_seq <= 0 || num_pages <= 0)
+    return fail(EB_ERR_PAGES, "num_pages and max_pages_per_seq must be positive");
+  s = check_batch(*cfg, batch, max_pages_per_seq, mode, err);
+  if (s != EB_OK) return fail(s, err);
+  s = check_tables(*cfg, *batch, block_tables_host, num_pages, max_pages_per_seq, err);
+  if (s != EB_OK) return fail(s, err);
+  return EB_OK;
+}
+
+// ---------------------------------------------------------------------------
+// single operations
+// ---------------------------------------------------------------------------
+eb_status eb_op_rmsnorm(const eb_handle *h, const void *x, const void *gamma, void *out, int32_t rows, void *stream) {
+  if (!h) return fail(EB_ERR_NULL, "handle is NULL");
+  if (rows < 0) return fail(EB_ERR_BATCH, "rows must be >= 0");
+  if (rows == 0) return EB_OK;
+  if (!x || !gamma || !out) return fail(EB_ERR_NULL, "x, gamma or out is NULL");
+  hipError_t e = launch_rmsnorm(static_cast<const uint16_t *>(x), static_cast<const uint16_t *>(gamma),
+                                static_cast<uint16_t *>(out), rows, h->shape.hidden, h->shape.eps,
+                                static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? EB_OK : hip_fail(e, "rmsnorm");
+}
+
+size_t eb_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
+  if (M <= 0 || N <= 0 || K <= 0) return 0;
+  size_t g = 0;
+  for (int epi = 0; epi < 3; ++epi) {
+    const size_t b = plan_gemm(M, N, K, epi).ws_bytes;
+    g = b > g ? b : g;
+  }
+  return g;
+}
+
+eb_status eb_op_gemm(const void *A, const void *W, void *out, const void *residual, int32_t M, int32_t N, int32_t K,
+                     eb_epilogue epi, void *ws, size_t ws_bytes, void *stream) {
+  if (M < 0 || N <= 0 || K <= 0) return fail(EB_ERR_CONFIG, "M must be >= 0, N and K > 0");
+  if (K % 8) return fail(EB_ERR_CONFIG, "K must be a multiple of 8");
+  if (epi != EB_EPI_STORE && epi != EB_EPI_RESIDUAL && epi != EB_EPI_SILU_MUL)
+    return fail(EB_ERR_CONFIG, "unknown epilogue");
+  if (epi == EB_EPI_SILU_MUL && N % 2) return fail(EB_ERR_CONFIG, "SiLU epilogue needs an even N");
+  if (M == 0) return EB_OK;
+  if (!A || !W || !out) return fail(EB_ERR_NULL, "A, W or out is NULL");
+  if (epi == EB_EPI_RESIDUAL && !residual) return fail(EB_ERR_NULL, "residual is NULL");
+  const GemmPlan p = plan_gemm(M, N, K, (int)epi);
+  eb_status s = check_ws(ws, ws_bytes, p.ws_bytes);
+  if (s != EB_OK) return s;
+  hipError_t e = launch_gemm(p, static_cast<const uint16_t *>(A), static_cast<const uint16_t *>(W),
+                             static_cast<uint16_t *>(out), static_cast<const uint16_t *>(residual), M, N, K, (int)epi,
+                             ws, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? EB_OK : hip_fail(e, "gemm");
+}
+
+eb_status eb_op_rope_kv_append(eb_handle *h, void *qkv, const eb_kv_cache *kv, const eb_batch *batch, void *ws,
+                               size_t ws_bytes, void *stream) {
+  eb_status s = check_kv(kv);
+  if (s != EB_OK) return s;
+  s = check_common(h, batch, EB_MODE_MIXED, kv->max_pages_per_seq);
+  if (s != EB_OK) return s;
+  if (batch->num_tokens == 0) return EB_OK;
+  if (!qkv) return fail(EB_ERR_NULL, "qkv is NULL");
+  HostPlan p;
+  build_plan(h->cfg, *batch, p);
+  const WsLayout L = layout_for(h->shape, p, false);
+  s = check_ws(ws, ws_bytes, L.total);
+  if (s != EB_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  s = stage_meta(h, p, ws, L, st);
+  if (s != EB_OK) return s;
+  const DevMeta m = meta_at(p, reinterpret_cast<const int32_t *>(static_cast<char *>(ws) + L.meta));
+  hipError_t e = launch_rope_append(h->shape, static_cast<uint16_t *>(qkv), kv_of(kv), m, st);
+  return e == hipSuccess ? EB_OK : hip_fail(e, "rope/kv append");
+}
+
+eb_status eb_op_attention(eb_handle *h, const void *qkv, const eb_kv_cache *kv, const eb_batch *batch, void *out,
+                          void *ws, size_t ws_bytes, eb_mode mode, void *stream) {
+  eb_status s = check_kv(kv);
+  if (s != EB_OK) return s;
+  s = check_common(h, batch, mode, kv->max_pages_per_seq);
+  if (s != EB_OK) return s;
+  if (batch->num_tokens == 0) return EB_OK;
+  if (!qkv || !out) return fail(EB_ERR_NULL, "qkv or out is NULL");
+  HostPlan p;
+  build_plan(h->cfg, *batch, p);
+  const WsLayout L = layout_for(h->shape, p, false);
+  s = check_ws(ws, ws_bytes, L.total);
+  if (s != EB_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  s = stage_meta(h, p, ws, L, st);
+  if (s != EB_OK) return s;
+  char *base = static_cast<char *>(ws);
+  const DevMeta m = meta_at(p, reinterpret_cast<const int32_t *>(base + L.meta));
+  const int kind = mode == EB_MODE_DECODE ? 0 : (mode == EB_MODE_PREFILL ? 1 : 2);
+  hipError_t e = launch_attention(h->shape, static_cast<const uint16_t *>(qkv), kv_of(kv), m,
+                                  static_cast<uint16_t *>(out), reinterpret_cast<float *>(base + L.part_o),
+                                  reinterpret_cast<float *>(base + L.part_ml), kind, st);
+  return e == hipSuccess ? EB_OK : hip_fail(e, "attention");
+}
+
+eb_status eb_op_gather_kv(eb_handle *h, const eb_kv_cache *kv, const eb_batch *batch, void *out_k, void *out_v,
+                          void *ws, size_t ws_bytes, void *stream) {
+  eb_status s = check_kv(kv);
+  if (s != EB_OK) return s;
+  s = check_common(h, batch, EB_MODE_MIXED, kv->max_pages_per_seq);
+  if (s != EB_OK) return s;
+  if (batch->num_seqs == 0) return EB_OK;
+  if (!out_k || !out_v) return fail(EB_ERR_NULL, "out_k or out_v is NULL");
+  HostPlan p;
+  build_plan(h->cfg, *batch, p);
+  const WsLayout L = layout_for(h->shape, p, false);
+  s = check_ws(ws, ws_bytes, L.total);
+  if (s != EB_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  s = stage_meta(h, p, ws, L, st);
+  if (s != EB_OK) return s;
+  const DevMeta m = meta_at(p, reinterpret_cast<const int32_t *>(static_cast<char *>(ws) + L.meta));
+  hipError_t e = launch_gather_kv(h->shape, kv_of(kv), m, static_cast<uint16_t *>(out_k),
+                                  static_cast<uint16_t *>(out_v), st);
+  return e == hipSuccess ? EB_OK : hip_fail(e, "gather");
+}
+
+}  // extern "C"

@@ -1,0 +1,80 @@
+// Device helpers shared by the gfx950 kernels: bf16 conversion, wavefront
+// reductions, MFMA operand types.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define EB_DEV __device__ __forceinline__
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+// bf16 bits <-> fp32.  Widening is exact; narrowing rounds to nearest even,
+// NaN maps to a quiet NaN.
+EB_DEV float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+EB_DEV float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+EB_DEV float bf16_to_f32(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+EB_DEV uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+EB_DEV uint32_t pack_bf16x2(float lo, float hi) { return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16); }
+
+// DPP row controls (a "row" is 16 lanes).
+#define EB_DPP_QUAD_XOR1 0xB1   // quad_perm [1,0,3,2]
+#define EB_DPP_QUAD_XOR2 0x4E   // quad_perm [2,3,0,1]
+#define EB_DPP_ROW_HALF_MIRROR 0x141
+#define EB_DPP_ROW_MIRROR 0x140
+
+template <int CTRL>
+EB_DEV float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+
+// Sum over aligned groups of LANES lanes (LANES in {8, 16}); every lane of the
+// group receives the group sum.  Stays inside a 16-lane DPP row.
+template <int LANES>
+EB_DEV float group_sum(float v) {
+  static_assert(LANES == 8 || LANES == 16, "group size");
+  v += dpp_f32<EB_DPP_QUAD_XOR1>(v);
+  v += dpp_f32<EB_DPP_QUAD_XOR2>(v);
+  v += dpp_f32<EB_DPP_ROW_HALF_MIRROR>(v);
+  if (LANES == 16) v += dpp_f32<EB_DPP_ROW_MIRROR>(v);
+  return v;
+}
+
+EB_DEV float shfl_xor_f32(float v, int mask) { return __shfl_xor(v, mask, 64); }
+
+EB_DEV float wave_max(float v) {
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  return v;
+}
+EB_DEV float wave_sum(float v) {
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
+  return v;
+}
+
+EB_DEV u32x4_t ld_u32x4(const void *p) { return *reinterpret_cast<const u32x4_t *>(p); }
+EB_DEV void st_u32x4(void *p, u32x4_t v) { *reinterpret_cast<u32x4_t *>(p) = v; }
+
+// Non-temporal 16-byte global load (streamed data read exactly once).
+EB_DEV u32x4_t ld_stream_u32x4(const void *p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+}
+
+EB_DEV bf16x8_t as_bf16x8(u32x4_t v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+// D = A B + C on one 16x16x32 bf16 tile.  Operand layout (lane l):
+//   A: row l % 16, k = 8 (l / 16) .. + 7      B: col l % 16, same k
+//   C/D: rows 4 (l / 16) .. + 3, col l % 16
+EB_DEV f32x4_t mfma16x16x32(u32x4_t a, u32x4_t b, f32x4_t c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+
+EB_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+constexpr float kLog2e = 1.4426950408889634f;

@@ -1,0 +1,70 @@
+// Internal interfaces between the host planner/launcher and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace eb {
+
+// Decode attention splits a request's keys into fixed chunks of this many
+// pages (tokens = pages * 16).  The count depends only on the request's own
+// length, so its result is the same in any batch.
+constexpr int kDecodePagesPerSplit = 32;
+constexpr int kPageSize = 16;
+
+// Prefill attention tiles: query positions per tile for a GQA group size
+// (must agree with PrefillTraits in the attention kernels).
+inline int prefill_bq(int group) { return group >= 8 ? 16 : (group == 1 ? 64 : 32); }
+
+// Per-step metadata in device memory (all int32), produced by the planner.
+struct DevMeta {
+  const int32_t *seq_ctx;       // [S] tokens cached before the step
+  const int32_t *seq_len;       // [S] new rows
+  const int32_t *seq_row;       // [S+1] first row of each request
+  const int32_t *row_seq;       // [T] request of each row
+  const int32_t *row_pos;       // [T] absolute position of each row
+  const int32_t *dec_seq;       // [D] request index of each decode request
+  const int32_t *dec_split_off; // [D+1] prefix sum of split counts
+  const int32_t *comb_list;     // [C] decode indices with >= 2 splits
+  const int32_t *tile_seq;      // [NT] prefill tiles, longest first
+  const int32_t *tile_qb;       // [NT] query block of each tile
+  const int32_t *gather_off;    // [S+1] prefix sum of (c + n)
+  int32_t S, T, n_dec, total_splits, n_comb, n_tiles;
+};
+
+struct KV {
+  uint16_t *k, *v;
+  const int32_t *bt;
+  int32_t num_pages, max_pages;
+};
+
+struct Shape {
+  int32_t hidden, nq, nkv, hd, ffn;
+  float eps, theta;
+  int32_t qkv_cols() const { return (nq + 2 * nkv) * hd; }
+  int32_t group() const { return nq / nkv; }
+};
+
+// ---- launchers (each returns the launch error) ----
+hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gamma, uint16_t *out, int rows, int d, float eps,
+                          hipStream_t st);
+hipError_t launch_rope_append(const Shape &s, uint16_t *qkv, const KV &kv, const DevMeta &m, hipStream_t st);
+hipError_t launch_gather_kv(const Shape &s, const KV &kv, const DevMeta &m, uint16_t *out_k, uint16_t *out_v,
+                            hipStream_t st);
+
+// attention: kind 0 = decode only, 1 = prefill only, 2 = mixed single launch
+hipError_t launch_attention(const Shape &s, const uint16_t *qkv, const KV &kv, const DevMeta &m, uint16_t *out,
+                            float *part_o, float *part_ml, int kind, hipStream_t st);
+
+// GEMM planning shared by the op entry and the step.
+enum GemmEpi { EPI_STORE = 0, EPI_RESIDUAL = 1, EPI_SILU_MUL = 2 };
+struct GemmPlan {
+  int kind;      // 0 = skinny weight-streaming, 1 = LDS-tiled
+  int splits;    // split-K factor (skinny only)
+  size_t ws_bytes;
+};
+GemmPlan plan_gemm(int M, int N, int K, int epi);
+hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, uint16_t *out,
+                       const uint16_t *residual, int M, int N, int K, int epi, void *ws, hipStream_t st);
+
+}  // namespace eb

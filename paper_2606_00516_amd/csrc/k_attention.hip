@@ -1,0 +1,526 @@
+// Paged attention for one step: split-K decode attention with a log-sum-exp
+// combine, LDS-tiled causal prefill attention on bf16 MFMA, and a mixed
+// launch that runs both kinds of work items in one grid.
+//
+// Cache layout: [page][kv head][16 slots][head_dim] bf16, so one (page, kv
+// head) block is 16 * head_dim * 2 bytes, contiguous.  Query head h reads kv
+// head h / G; a work item owns one kv head and serves all G of its query
+// heads, so each cached byte is read once per item.
+#include <math.h>
+
+#include "device_common.h"
+#include "eb_internal.h"
+
+namespace eb {
+
+constexpr float kNegInf = -__builtin_inff();
+
+// ===========================================================================
+// Decode: one work item = (decode request, split of 32 pages, kv head), 4
+// wavefronts.  Wave w streams pages w, w+4, ... of the split.  Lane layout
+// over a 16 x HD page block: each 16-byte load instruction covers 1 KiB, lane
+// l holding 8 dims of one token; LPT = HD/8 lanes share a token.  Scores are
+// reduced over those lanes with DPP; each lane keeps its own running
+// (max, sum, output) over the tokens it sees, and the partial states are
+// merged at the end (shuffles within the wave, LDS across waves).
+// ===========================================================================
+template <int HD, int G>
+struct DecodeTraits {
+  static constexpr int LPT = HD / 8;   // lanes per token
+  static constexpr int TG = 64 / LPT;  // tokens per load instruction
+  static constexpr int NLD = HD / 32;  // load instructions per page block = tokens per lane per page
+  static constexpr int LDS_BYTES = 4 * G * (HD + 2) * 4;
+};
+
+// Merge running softmax state (m, l, o) with another one.
+template <int N>
+__device__ __forceinline__ void lse_merge(float &m, float &l, float *o, float m2, float l2, const float *o2) {
+  const float mx = fmaxf(m, m2);
+  const float a = (m == kNegInf) ? 0.f : fast_exp2(m - mx);
+  const float b = (m2 == kNegInf) ? 0.f : fast_exp2(m2 - mx);
+  l = l * a + l2 * b;
+#pragma unroll
+  for (int i = 0; i < N; ++i) o[i] = o[i] * a + o2[i] * b;
+  m = mx;
+}
+
+template <int HD, int G>
+__device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV &kv,
+                                            const DevMeta &md, int item, int kh, uint16_t *__restrict__ out,
+                                            float *__restrict__ part_o, float *__restrict__ part_ml, float *lds) {
+  using Tr = DecodeTraits<HD, G>;
+  constexpr int LPT = Tr::LPT, TG = Tr::TG, NLD = Tr::NLD;
+  constexpr int SPLIT = kDecodePagesPerSplit * kPageSize;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int cols = (nq + 2 * nkv) * HD;
+
+  // locate the decode request owning this split
+  int lo = 0, hi = md.n_dec - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (md.dec_split_off[mid] <= item) lo = mid; else hi = mid - 1;
+  }
+  const int d = lo;
+  const int s0 = md.dec_split_off[d];
+  const int split = item - s0;
+  const int nsplit = md.dec_split_off[d + 1] - s0;
+  const int seq = md.dec_seq[d];
+  const int nkeys = md.seq_ctx[seq] + 1;
+  const int row = md.seq_row[seq];
+  const int k0 = split * SPLIT;
+  const int k1 = min(nkeys, k0 + SPLIT);
+  const int pg0 = k0 / kPageSize, pg1 = (k1 + kPageSize - 1) / kPageSize;
+  const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
+
+  // queries of the G heads, this lane's 8 dims, pre-scaled for exp2
+  const int dq = (lane % LPT) * 8;
+  const float qscale = kLog2e / sqrtf((float)HD);
+  float q[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    u32x4_t w = ld_u32x4(qkv + (size_t)row * cols + (kh * G + h) * HD + dq);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      q[h][2 * i] = bf16_lo(w[i]) * qscale;
+      q[h][2 * i + 1] = bf16_hi(w[i]) * qscale;
+    }
+  }
+  float mrun[G], lrun[G], o[G][8];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    mrun[h] = kNegInf;
+    lrun[h] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[h][i] = 0.f;
+  }
+
+  auto load_page = [&](int p, u32x4_t *kr, u32x4_t *vr) {
+    const int phys = bt[p];
+    if (phys >= 0 && phys < kv.num_pages) {
+      const size_t base = ((size_t)phys * nkv + kh) * kPageSize * HD + lane * 8;
+#pragma unroll
+      for (int j = 0; j < NLD; ++j) {
+        kr[j] = ld_stream_u32x4(kv.k + base + j * 512);
+        vr[j] = ld_stream_u32x4(kv.v + base + j * 512);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NLD; ++j) kr[j] = vr[j] = u32x4_t{0, 0, 0, 0};
+    }
+  };
+
+  u32x4_t kc[NLD], vc[NLD], kn[NLD], vn[NLD];
+#pragma unroll
+  for (int j = 0; j < NLD; ++j) kc[j] = vc[j] = kn[j] = vn[j] = u32x4_t{0, 0, 0, 0};
+  int p = pg0 + wave;
+  if (p < pg1) load_page(p, kc, vc);
+  for (; p < pg1; p += 4) {
+    const int pn = p + 4;
+    if (pn < pg1) load_page(pn, kn, vn);
+    // token of load j in this lane
+    bool valid[NLD];
+#pragma unroll
+    for (int j = 0; j < NLD; ++j) {
+      const int t = p * kPageSize + j * TG + lane / LPT;
+      valid[j] = (t >= k0) && (t < k1);
+      if (!valid[j]) vc[j] = u32x4_t{0, 0, 0, 0};
+    }
+    float kf[NLD][8];
+#pragma unroll
+    for (int j = 0; j < NLD; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        kf[j][2 * i] = bf16_lo(kc[j][i]);
+        kf[j][2 * i + 1] = bf16_hi(kc[j][i]);
+      }
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float s[NLD];
+      float mx = mrun[h];
+#pragma unroll
+      for (int j = 0; j < NLD; ++j) {
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc = fmaf(q[h][i], kf[j][i], acc);
+        acc = group_sum<LPT>(acc);
+        s[j] = valid[j] ? acc : kNegInf;
+        mx = fmaxf(mx, s[j]);
+      }
+      const float alpha = (mrun[h] == kNegInf) ? 0.f : fast_exp2(mrun[h] - mx);
+      float l = lrun[h] * alpha;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o[h][i] *= alpha;
+#pragma unroll
+      for (int j = 0; j < NLD; ++j) {
+        const float pj = (s[j] == kNegInf) ? 0.f : fast_exp2(s[j] - mx);
+        l += pj;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          o[h][2 * i] = fmaf(pj, bf16_lo(vc[j][i]), o[h][2 * i]);
+          o[h][2 * i + 1] = fmaf(pj, bf16_hi(vc[j][i]), o[h][2 * i + 1]);
+        }
+      }
+      lrun[h] = l;
+      mrun[h] = mx;
+    }
+#pragma unroll
+    for (int j = 0; j < NLD; ++j) {
+      kc[j] = kn[j];
+      vc[j] = vn[j];
+    }
+  }
+
+  // merge the token groups of this wave (lanes with equal lane % LPT)
+#pragma unroll
+  for (int mask = LPT; mask < 64; mask <<= 1) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      float o2[8];
+      const float m2 = shfl_xor_f32(mrun[h], mask);
+      const float l2 = shfl_xor_f32(lrun[h], mask);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) o2[i] = shfl_xor_f32(o[h][i], mask);
+      lse_merge<8>(mrun[h], lrun[h], o[h], m2, l2, o2);
+    }
+  }
+  // across the 4 waves through LDS: [wave][h][HD] outputs, then [wave][h][2]
+  float *lo_ = lds;
+  float *lml = lds + 4 * G * HD;
+  if (lane < LPT) {
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) lo_[(wave * G + h) * HD + dq + i] = o[h][i];
+      if (lane == 0) {
+        lml[(wave * G + h) * 2] = mrun[h];
+        lml[(wave * G + h) * 2 + 1] = lrun[h];
+      }
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < G * HD; e += blockDim.x) {
+    const int h = e / HD, dim = e - h * HD;
+    float mx = kNegInf;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) mx = fmaxf(mx, lml[(w * G + h) * 2]);
+    float L = 0.f, O = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const float mw = lml[(w * G + h) * 2];
+      const float a = (mw == kNegInf) ? 0.f : fast_exp2(mw - mx);
+      L += a * lml[(w * G + h) * 2 + 1];
+      O += a * lo_[(w * G + h) * HD + dim];
+    }
+    const int qh = kh * G + h;
+    if (nsplit == 1) {
+      out[(size_t)row * nq * HD + qh * HD + dim] = (uint16_t)f32_to_bf16_bits(O / L);
+    } else {
+      const size_t slot = ((size_t)item * nkv + kh) * G + h;
+      part_o[slot * HD + dim] = O;
+      if (dim == 0) {
+        part_ml[slot * 2] = mx;
+        part_ml[slot * 2 + 1] = L;
+      }
+    }
+  }
+  __syncthreads();
+}
+
+// Combine the splits of one decode request for one query head:
+// o = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s with M = max_s m_s, the
+// max and both sums reduced across the wavefront.
+template <int HD, int G>
+__global__ __launch_bounds__(64) void k_decode_combine(DevMeta md, const float *__restrict__ part_o,
+                                                       const float *__restrict__ part_ml, uint16_t *__restrict__ out,
+                                                       int nq, int nkv) {
+  const int d = md.comb_list[blockIdx.x];
+  const int qh = blockIdx.y;
+  const int kh = qh / G, h = qh - kh * G;
+  const int lane = threadIdx.x;
+  const int s0 = md.dec_split_off[d], ns = md.dec_split_off[d + 1] - s0;
+  const int row = md.seq_row[md.dec_seq[d]];
+  auto slot = [&](int s) { return ((size_t)(s0 + s) * nkv + kh) * G + h; };
+  float mx = kNegInf;
+  for (int s = lane; s < ns; s += 64) mx = fmaxf(mx, part_ml[slot(s) * 2]);
+  mx = wave_max(mx);
+  float den = 0.f;
+  for (int s = lane; s < ns; s += 64) {
+    const float ms = part_ml[slot(s) * 2];
+    den += (ms == kNegInf) ? 0.f : fast_exp2(ms - mx) * part_ml[slot(s) * 2 + 1];
+  }
+  den = wave_sum(den);
+  for (int dim = lane; dim < HD; dim += 64) {
+    float acc = 0.f;
+    for (int s = 0; s < ns; ++s) {
+      const float ms = part_ml[slot(s) * 2];
+      const float a = (ms == kNegInf) ? 0.f : fast_exp2(ms - mx);
+      acc += a * part_o[slot(s) * HD + dim];
+    }
+    out[(size_t)row * nq * HD + qh * HD + dim] = (uint16_t)f32_to_bf16_bits(acc / den);
+  }
+}
+
+// ===========================================================================
+// Prefill: one work item = (request, block of BQ query positions, kv head):
+// G heads x BQ positions = 16-row blocks shared out over 4 wavefronts.  Keys
+// and values stream through LDS in tiles of 64 positions gathered from 4
+// pages.  Scores are formed transposed, S^T = K Q^T, with the 16x16x32 bf16
+// MFMA, so a lane holds one query column and the row max needs only two
+// cross-lane steps; P^T stays in registers as the B operand of O^T = V^T P^T
+// (keys permuted consistently on both operands), with V^T staged in LDS.
+// ===========================================================================
+template <int HD, int G>
+struct PrefillTraits {
+  static constexpr int BQ = (G >= 8) ? 16 : ((G == 1) ? 64 : 32);
+  static constexpr int RB_TOTAL = G * BQ / 16;  // 16-row blocks per item
+  static constexpr int RB = RB_TOTAL / 4;       // per wavefront
+  static constexpr int KT = 64;                 // keys per tile
+  static constexpr int KS_STRIDE = HD + 8;      // bf16 elements per K row in LDS
+  static constexpr int VT_STRIDE = KT + 4;      // bf16 elements per V^T row in LDS
+  static constexpr int LDS_BYTES = (KT * KS_STRIDE + HD * VT_STRIDE) * 2;
+  static_assert(RB_TOTAL % 4 == 0 && RB >= 1, "row blocks");
+};
+
+template <int HD, int G>
+__device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV &kv,
+                                             const DevMeta &md, int tile, int kh, uint16_t *__restrict__ out,
+                                             uint16_t *lds) {
+  using Tr = PrefillTraits<HD, G>;
+  constexpr int BQ = Tr::BQ, RB = Tr::RB, KT = Tr::KT, KSS = Tr::KS_STRIDE, VTS = Tr::VT_STRIDE;
+  constexpr int NKS = HD / 32;  // k-steps of the QK^T product
+  constexpr int NOB = HD / 16;  // 16-dim output blocks
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int cols = (nq + 2 * nkv) * HD;
+  const int seq = md.tile_seq[tile];
+  const int qb = md.tile_qb[tile];
+  const int c = md.seq_ctx[seq];
+  const int n = md.seq_len[seq];
+  const int row0 = md.seq_row[seq];
+  const int q_lo = qb * BQ;                 // first query (chunk-relative)
+  const int q_hi = min(n, q_lo + BQ);       // one past the last
+  const int kend = c + q_hi;                // keys needed: 0 .. kend-1
+  const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
+  const int npages = (c + n + kPageSize - 1) / kPageSize;
+  uint16_t *Ks = lds;
+  uint16_t *Vt = lds + KT * KSS;
+  const float qscale = kLog2e / sqrtf((float)HD);
+  const int lq = lane & 15;   // query column of this lane inside a 16-row block
+  const int lg = lane >> 4;   // lane group 0..3
+
+  // row blocks of this wave: rb = wave + 4 i -> (head, 16-query sub-block)
+  u32x4_t qreg[RB][NKS];
+  int qpos[RB];
+  bool qok[RB];
+#pragma unroll
+  for (int i = 0; i < RB; ++i) {
+    const int rb = wave + 4 * i;
+    const int h = rb % G, sub = rb / G;
+    const int qrel = q_lo + sub * 16 + lq;
+    qok[i] = qrel < q_hi;
+    qpos[i] = c + qrel;
+    const uint16_t *src = qkv + (size_t)(row0 + qrel) * cols + (kh * G + h) * HD + lg * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qreg[i][ks] = qok[i] ? ld_u32x4(src + ks * 32) : u32x4_t{0, 0, 0, 0};
+  }
+  f32x4_t oacc[RB][NOB];
+  float mrun[RB], lrun[RB];
+#pragma unroll
+  for (int i = 0; i < RB; ++i) {
+    mrun[i] = kNegInf;
+    lrun[i] = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) oacc[i][ob] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
+  const int min_qpos = c + q_lo;
+  const int ntiles = (kend + KT - 1) / KT;
+  for (int t = 0; t < ntiles; ++t) {
+    const int k0 = t * KT;
+    // ---- stage K (row-major) and V^T into LDS; keys >= c + n are zero ----
+    for (int u = threadIdx.x; u < KT * (HD / 8); u += 256) {
+      const int key = u / (HD / 8), dc = u - key * (HD / 8);
+      const int kp = k0 + key;
+      u32x4_t w = {0, 0, 0, 0};
+      if (kp < c + n) {
+        const int pg = kp / kPageSize;
+        const int phys = pg < npages ? bt[pg] : -1;
+        if (phys >= 0 && phys < kv.num_pages)
+          w = ld_u32x4(kv.k + (((size_t)phys * nkv + kh) * kPageSize + kp % kPageSize) * HD + dc * 8);
+      }
+      st_u32x4(Ks + key * KSS + dc * 8, w);
+    }
+    for (int u = threadIdx.x; u < (KT / 2) * (HD / 8); u += 256) {
+      const int kpair = u / (HD / 8), dc = u - kpair * (HD / 8);
+      u32x4_t w[2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int kp = k0 + 2 * kpair + e;
+        w[e] = u32x4_t{0, 0, 0, 0};
+        if (kp < c + n) {
+          const int pg = kp / kPageSize;
+          const int phys = pg < npages ? bt[pg] : -1;
+          if (phys >= 0 && phys < kv.num_pages)
+            w[e] = ld_u32x4(kv.v + (((size_t)phys * nkv + kh) * kPageSize + kp % kPageSize) * HD + dc * 8);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t lo0 = w[0][i] & 0xFFFFu, hi0 = w[0][i] >> 16;
+        const uint32_t lo1 = w[1][i] & 0xFFFFu, hi1 = w[1][i] >> 16;
+        *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * i) * VTS + 2 * kpair) = lo0 | (lo1 << 16);
+        *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * i + 1) * VTS + 2 * kpair) = hi0 | (hi1 << 16);
+      }
+    }
+    __syncthreads();
+    const bool need_mask = (k0 + KT - 1) > min_qpos;
+#pragma unroll
+    for (int i = 0; i < RB; ++i) {
+      // S^T block kb: keys k0 + 16 kb + 4 lg + j, query column lq
+      f32x4_t s[4];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        s[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+          const u32x4_t a = ld_u32x4(Ks + (kb * 16 + lq) * KSS + ks * 32 + lg * 8);
+          s[kb] = mfma16x16x32(a, qreg[i][ks], s[kb]);
+        }
+      }
+      float mx = mrun[i];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float v = s[kb][j] * qscale;
+          if (need_mask || !qok[i]) {
+            const int kp = k0 + kb * 16 + lg * 4 + j;
+            if (kp > qpos[i] || !qok[i]) v = kNegInf;
+          }
+          s[kb][j] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, shfl_xor_f32(mx, 16));
+      mx = fmaxf(mx, shfl_xor_f32(mx, 32));
+      const float alpha = (mrun[i] == kNegInf) ? 0.f : fast_exp2(mrun[i] - mx);
+      const bool live = mx != kNegInf;
+      float l = lrun[i] * alpha;
+      uint32_t pk[4][2];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        float p4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          p4[j] = (live && s[kb][j] != kNegInf) ? fast_exp2(s[kb][j] - mx) : 0.f;
+          l += p4[j];
+        }
+        pk[kb][0] = pack_bf16x2(p4[0], p4[1]);
+        pk[kb][1] = pack_bf16x2(p4[2], p4[3]);
+      }
+      lrun[i] = l;
+      mrun[i] = mx;
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) {
+        f32x4_t acc = oacc[i][ob] * alpha;
+#pragma unroll
+        for (int ks2 = 0; ks2 < 2; ++ks2) {
+          // B (P^T): keys {4 lg .. +3} of block 2 ks2, then of block 2 ks2 + 1
+          const u32x4_t b = {pk[2 * ks2][0], pk[2 * ks2][1], pk[2 * ks2 + 1][0], pk[2 * ks2 + 1][1]};
+          // A (V^T): dim ob*16 + lq, the same keys
+          const uint16_t *vrow = Vt + (ob * 16 + lq) * VTS + ks2 * 32 + lg * 4;
+          const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vrow);
+          const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vrow + 16);
+          const u32x4_t a = {a0[0], a0[1], a1[0], a1[1]};
+          acc = mfma16x16x32(a, b, acc);
+        }
+        oacc[i][ob] = acc;
+      }
+    }
+    __syncthreads();
+  }
+  // normalise and store: lane holds dims ob*16 + 4 lg + j of query lq
+#pragma unroll
+  for (int i = 0; i < RB; ++i) {
+    float l = lrun[i];
+    l += shfl_xor_f32(l, 16);
+    l += shfl_xor_f32(l, 32);
+    if (!qok[i]) continue;
+    const int rb = wave + 4 * i;
+    const int h = rb % G, sub = rb / G;
+    const int qrel = q_lo + sub * 16 + lq;
+    const float inv = 1.0f / l;
+    uint16_t *dst = out + (size_t)(row0 + qrel) * nq * HD + (kh * G + h) * HD + lg * 4;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) {
+      u32x2_t w = {pack_bf16x2(oacc[i][ob][0] * inv, oacc[i][ob][1] * inv),
+                   pack_bf16x2(oacc[i][ob][2] * inv, oacc[i][ob][3] * inv)};
+      *reinterpret_cast<u32x2_t *>(dst + ob * 16) = w;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// kernels
+// ---------------------------------------------------------------------------
+template <int HD, int G>
+__global__ __launch_bounds__(256) void k_decode(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
+                                                float *part_o, float *part_ml) {
+  __shared__ float lds[DecodeTraits<HD, G>::LDS_BYTES / 4];
+  decode_item<HD, G>(qkv, nq, nkv, kv, md, blockIdx.x, blockIdx.y, out, part_o, part_ml, lds);
+}
+
+template <int HD, int G>
+__global__ __launch_bounds__(256) void k_prefill(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
+                                                 uint16_t *out) {
+  __shared__ __attribute__((aligned(16))) uint16_t lds[PrefillTraits<HD, G>::LDS_BYTES / 2];
+  prefill_item<HD, G>(qkv, nq, nkv, kv, md, blockIdx.x, blockIdx.y, out, lds);
+}
+
+// One grid for a mixed step: items [0, n_tiles) are prefill tiles (longest
+// first), the rest decode splits; every block branches uniformly on its kind.
+template <int HD, int G>
+__global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
+                                               float *part_o, float *part_ml) {
+  constexpr int PB = PrefillTraits<HD, G>::LDS_BYTES, DB = DecodeTraits<HD, G>::LDS_BYTES;
+  __shared__ __attribute__((aligned(16))) uint16_t lds[(PB > DB ? PB : DB) / 2];
+  const int b = blockIdx.x;
+  if (b < md.n_tiles)
+    prefill_item<HD, G>(qkv, nq, nkv, kv, md, b, blockIdx.y, out, lds);
+  else
+    decode_item<HD, G>(qkv, nq, nkv, kv, md, b - md.n_tiles, blockIdx.y, out, part_o, part_ml,
+                       reinterpret_cast<float *>(lds));
+}
+
+template <int HD, int G>
+static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const KV &kv, const DevMeta &m,
+                                     uint16_t *out, float *part_o, float *part_ml, int kind, hipStream_t st) {
+  const int nkv = s.nkv, nq = s.nq;
+  const bool has_dec = m.n_dec > 0, has_pf = m.n_tiles > 0;
+  if (kind == 2 && has_dec && has_pf) {
+    hipLaunchKernelGGL((k_mixed<HD, G>), dim3(m.n_tiles + m.total_splits, nkv), dim3(256), 0, st, qkv, nq, nkv, kv, m,
+                       out, part_o, part_ml);
+  } else {
+    if (has_pf) hipLaunchKernelGGL((k_prefill<HD, G>), dim3(m.n_tiles, nkv), dim3(256), 0, st, qkv, nq, nkv, kv, m, out);
+    if (has_dec)
+      hipLaunchKernelGGL((k_decode<HD, G>), dim3(m.total_splits, nkv), dim3(256), 0, st, qkv, nq, nkv, kv, m, out,
+                         part_o, part_ml);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (m.n_comb > 0)
+    hipLaunchKernelGGL((k_decode_combine<HD, G>), dim3(m.n_comb, nq), dim3(64), 0, st, m, part_o, part_ml, out, nq, nkv);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention(const Shape &s, const uint16_t *qkv, const KV &kv, const DevMeta &m, uint16_t *out,
+                            float *part_o, float *part_ml, int kind, hipStream_t st) {
+  const int G = s.group();
+#define EB_ATT_CASE(HD_, G_) \
+  if (s.hd == HD_ && G == G_) return launch_attention_t<HD_, G_>(s, qkv, kv, m, out, part_o, part_ml, kind, st);
+  EB_ATT_CASE(128, 1) EB_ATT_CASE(128, 2) EB_ATT_CASE(128, 4) EB_ATT_CASE(128, 8)
+  EB_ATT_CASE(64, 1) EB_ATT_CASE(64, 2) EB_ATT_CASE(64, 4) EB_ATT_CASE(64, 8)
+#undef EB_ATT_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace eb

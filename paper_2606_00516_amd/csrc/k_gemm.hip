@@ -1,0 +1,363 @@
+// Projection GEMMs of the layer: out = epilogue(A W^T), A [M, K] activations,
+// W [N, K] weights, both K-contiguous bf16, fp32 accumulation on the
+// 16x16x32 bf16 MFMA.
+//
+//  * skinny: M <= 64 rows per tile (decode-sized batches).  The product is
+//    bound by streaming W from HBM once, so each wavefront loads MFMA operand
+//    fragments straight from global memory (no LDS staging); the 4 waves of a
+//    block split K and reduce through LDS; blocks may further split K, with a
+//    small reduction kernel applying the epilogue.
+//  * tiled: larger M.  128x128 output tiles, K tiles of 64 double-buffered in
+//    LDS, 4 waves each owning a 64x64 sub-tile.
+//
+// Epilogues: store; + residual; SiLU(gate) * up.  For SiLU the columns are
+// processed in groups of 64 = 32 gate rows of W followed by the 32 matching
+// up rows (gate rows 0..F-1, up rows F..2F-1 of W), so that every lane holds
+// a gate accumulator and its up partner.
+#include "device_common.h"
+#include "eb_internal.h"
+
+namespace eb {
+
+// W row feeding logical column c of the product (or -1 if none).
+__device__ __forceinline__ int w_row_of(int c, int N, int epi) {
+  if (epi != EPI_SILU_MUL) return c < N ? c : -1;
+  const int F = N >> 1;
+  const int g = c >> 6, w = c & 63;
+  const int f = g * 32 + (w & 31);
+  if (f >= F) return -1;
+  return w < 32 ? f : F + f;
+}
+
+// Number of logical product columns for an epilogue.
+__host__ __device__ static inline int logical_cols(int N, int epi) {
+  if (epi != EPI_SILU_MUL) return N;
+  const int F = N / 2;
+  return ((F + 31) / 32) * 64;
+}
+
+__device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
+
+// ===========================================================================
+// skinny
+// ===========================================================================
+constexpr int SK_BN = 64;     // logical columns per block
+constexpr int SK_BM = 64;     // rows per block
+constexpr int SK_UNROLL = 2;  // k-steps of 32 per loop trip per wave
+
+__global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict__ A, const uint16_t *__restrict__ W,
+                                                     uint16_t *__restrict__ out, const uint16_t *__restrict__ res,
+                                                     float *__restrict__ part, int M, int N, int K, int epi,
+                                                     int ksteps_per_split) {
+  __shared__ float red[SK_BM][SK_BN + 4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int n0 = blockIdx.x * SK_BN;
+  const int split = blockIdx.y;
+  const int m0 = blockIdx.z * SK_BM;
+  const int nsteps = K / 32 + ((K & 31) ? 1 : 0);
+  const int ks_begin = split * ksteps_per_split;
+  const int ks_end = min(nsteps, ks_begin + ksteps_per_split);
+  const int lr = lane & 15, lk = (lane >> 4) * 8;
+
+  // operand row pointers (nullptr = zero row)
+  const uint16_t *arow[4];
+  const uint16_t *wrow[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int m = m0 + b * 16 + lr;
+    arow[b] = m < M ? A + (size_t)m * K : nullptr;
+    const int wr = w_row_of(n0 + b * 16 + lr, N, epi);
+    wrow[b] = wr >= 0 ? W + (size_t)wr * K : nullptr;
+  }
+  f32x4_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  auto load = [&](int ks, u32x4_t *a, u32x4_t *b) {
+    const int k = ks * 32 + lk;
+    const bool kin = (ks < ks_end) && (k < K);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      a[i] = (kin && arow[i]) ? ld_u32x4(arow[i] + k) : u32x4_t{0, 0, 0, 0};
+      b[i] = (kin && wrow[i]) ? ld_stream_u32x4(wrow[i] + k) : u32x4_t{0, 0, 0, 0};
+    }
+  };
+  // wave w takes k-steps ks_begin + w, + 4, ...; SK_UNROLL of them per trip,
+  // with the next trip's operands loaded before this trip's MFMAs
+  u32x4_t ca[SK_UNROLL][4], cb[SK_UNROLL][4], na[SK_UNROLL][4], nb[SK_UNROLL][4];
+  int ks = ks_begin + wave;
+#pragma unroll
+  for (int u = 0; u < SK_UNROLL; ++u) load(ks + 4 * u, ca[u], cb[u]);
+  for (; ks < ks_end; ks += 4 * SK_UNROLL) {
+    const int nks = ks + 4 * SK_UNROLL;
+#pragma unroll
+    for (int u = 0; u < SK_UNROLL; ++u) load(nks + 4 * u, na[u], nb[u]);
+#pragma unroll
+    for (int u = 0; u < SK_UNROLL; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(ca[u][i], cb[u][j], acc[i][j]);
+#pragma unroll
+    for (int u = 0; u < SK_UNROLL; ++u)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        ca[u][i] = na[u][i];
+        cb[u][i] = nb[u][i];
+      }
+  }
+  // reduce the 4 waves' accumulators in LDS, in wave order (deterministic)
+  for (int w = 0; w < 4; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float &dst = red[i * 16 + (lane >> 4) * 4 + e][j * 16 + lr];
+            dst = (w == 0) ? acc[i][j][e] : dst + acc[i][j][e];
+          }
+    }
+    __syncthreads();
+  }
+  // 256 threads x 16 columns: row t/4, columns (t%4)*16 .. +16
+  const int r = threadIdx.x >> 2, cq = (threadIdx.x & 3) * 16;
+  const int m = m0 + r;
+  if (m >= M) return;
+  float v[16];
+#pragma unroll
+  for (int c = 0; c < 16; ++c) v[c] = red[r][cq + c];
+  const int ncols = logical_cols(N, epi);
+  if (part) {  // split-K partial, logical column space
+    float *dst = part + ((size_t)split * M + m) * ncols + n0 + cq;
+#pragma unroll
+    for (int c = 0; c < 16; ++c)
+      if (n0 + cq + c < ncols) dst[c] = v[c];
+    return;
+  }
+  if (epi == EPI_SILU_MUL) {
+    // columns cq..cq+15 of the 64-group: gate if cq < 32, the matching up
+    // values sit in columns cq+32..; threads with cq < 32 finish the group
+    if (cq >= 32) return;
+    const int F = N >> 1;
+    const int f0 = (n0 >> 1) + cq;
+#pragma unroll
+    for (int c = 0; c < 16; ++c) {
+      const float g = v[c];
+      const float u = red[r][cq + 32 + c];
+      if (f0 + c < F) out[(size_t)m * F + f0 + c] = (uint16_t)f32_to_bf16_bits(silu_f(g) * u);
+    }
+    return;
+  }
+#pragma unroll
+  for (int c = 0; c < 16; ++c) {
+    const int n = n0 + cq + c;
+    if (n < N) {
+      float x = v[c];
+      if (epi == EPI_RESIDUAL) x += bf16_to_f32(res[(size_t)m * N + n]);
+      out[(size_t)m * N + n] = (uint16_t)f32_to_bf16_bits(x);
+    }
+  }
+}
+
+// Sum split-K partials (logical column space) and apply the epilogue.
+__global__ __launch_bounds__(256) void k_gemm_splitk_epilogue(const float *__restrict__ part, int splits,
+                                                              uint16_t *__restrict__ out,
+                                                              const uint16_t *__restrict__ res, int M, int N,
+                                                              int epi) {
+  const int ncols = logical_cols(N, epi);
+  const int outc = epi == EPI_SILU_MUL ? N / 2 : N;
+  const long total = (long)M * outc;
+  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
+    const int m = (int)(idx / outc), n = (int)(idx - (long)m * outc);
+    if (epi == EPI_SILU_MUL) {
+      const int gcol = (n / 32) * 64 + (n & 31);
+      float g = 0.f, u = 0.f;
+      for (int s = 0; s < splits; ++s) {
+        g += part[((size_t)s * M + m) * ncols + gcol];
+        u += part[((size_t)s * M + m) * ncols + gcol + 32];
+      }
+      out[(size_t)m * outc + n] = (uint16_t)f32_to_bf16_bits(silu_f(g) * u);
+    } else {
+      float x = 0.f;
+      for (int s = 0; s < splits; ++s) x += part[((size_t)s * M + m) * ncols + n];
+      if (epi == EPI_RESIDUAL) x += bf16_to_f32(res[(size_t)m * N + n]);
+      out[(size_t)m * N + n] = (uint16_t)f32_to_bf16_bits(x);
+    }
+  }
+}
+
+// ===========================================================================
+// tiled
+// ===========================================================================
+constexpr int TL_BM = 128, TL_BN = 128, TL_BK = 64, TL_LDK = TL_BK + 8;
+
+__global__ __launch_bounds__(256) void k_gemm_tiled(const uint16_t *__restrict__ A, const uint16_t *__restrict__ W,
+                                                    uint16_t *__restrict__ out, const uint16_t *__restrict__ res,
+                                                    int M, int N, int K, int epi, int tiles_m, int tiles_n) {
+  __shared__ __attribute__((aligned(16))) uint16_t sA[2][TL_BM * TL_LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t sB[2][TL_BN * TL_LDK];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  // tile order: column-major over M inside groups of 8 N tiles, so that
+  // consecutive blocks share the same A rows and a small band of W rows
+  const int bid = blockIdx.x;
+  const int group = 8;
+  const int per_group = group * tiles_m;
+  const int gidx = bid / per_group;
+  const int first_n = gidx * group;
+  const int gsz = min(group, tiles_n - first_n);
+  const int inb = bid - gidx * per_group;
+  const int tn = first_n + inb % gsz;
+  const int tm = inb / gsz;
+  const int m0 = tm * TL_BM, n0 = tn * TL_BN;
+  const int nk = (K + TL_BK - 1) / TL_BK;
+
+  // global -> register staging: 4 chunks of 16 B for A and for W per thread
+  const int ldr = threadIdx.x >> 3;        // row 0..31 within a pass
+  const int ldc = (threadIdx.x & 7) * 8;   // k offset
+  const uint16_t *ga[4];
+  const uint16_t *gb[4];
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int m = m0 + p * 32 + ldr;
+    ga[p] = m < M ? A + (size_t)m * K : nullptr;
+    const int wr = w_row_of(n0 + p * 32 + ldr, N, epi);
+    gb[p] = wr >= 0 ? W + (size_t)wr * K : nullptr;
+  }
+  u32x4_t ra[4], rb[4];
+  auto gload = [&](int kt) {
+    const int k = kt * TL_BK + ldc;
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      ra[p] = (ga[p] && k < K) ? ld_u32x4(ga[p] + k) : u32x4_t{0, 0, 0, 0};
+      rb[p] = (gb[p] && k < K) ? ld_u32x4(gb[p] + k) : u32x4_t{0, 0, 0, 0};
+    }
+  };
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      st_u32x4(&sA[buf][(p * 32 + ldr) * TL_LDK + ldc], ra[p]);
+      st_u32x4(&sB[buf][(p * 32 + ldr) * TL_LDK + ldc], rb[p]);
+    }
+  };
+  f32x4_t acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int lr = lane & 15, lk = (lane >> 4) * 8;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) gload(kt + 1);
+#pragma unroll
+    for (int kk = 0; kk < TL_BK; kk += 32) {
+      u32x4_t a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = ld_u32x4(&sA[buf][(wm * 64 + i * 16 + lr) * TL_LDK + kk + lk]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = ld_u32x4(&sB[buf][(wn * 64 + j * 16 + lr) * TL_LDK + kk + lk]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(a[i], b[j], acc[i][j]);
+    }
+    if (kt + 1 < nk) sstore(buf ^ 1);
+    __syncthreads();
+  }
+  // epilogue straight from the accumulator layout: lane holds rows
+  // 4 (lane/16) + e, column lane % 16 of each 16x16 block
+  const int cbase = n0 + wn * 64;
+  if (epi == EPI_SILU_MUL) {
+    const int F = N >> 1;
+    const int f0 = cbase >> 1;  // 64-group -> 32 ffn columns
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + e;
+          const int f = f0 + j * 16 + lr;
+          if (m < M && f < F)
+            out[(size_t)m * F + f] = (uint16_t)f32_to_bf16_bits(silu_f(acc[i][j][e]) * acc[i][j + 2][e]);
+        }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = m0 + wm * 64 + i * 16 + (lane >> 4) * 4 + e;
+        const int n = cbase + j * 16 + lr;
+        if (m < M && n < N) {
+          float x = acc[i][j][e];
+          if (epi == EPI_RESIDUAL) x += bf16_to_f32(res[(size_t)m * N + n]);
+          out[(size_t)m * N + n] = (uint16_t)f32_to_bf16_bits(x);
+        }
+      }
+}
+
+// ===========================================================================
+// planning and launch
+// ===========================================================================
+static int skinny_splits(int M, int N, int K) {
+  const int ncol_tiles = (N + SK_BN - 1) / SK_BN;
+  const int mt = (M + SK_BM - 1) / SK_BM;
+  const int nsteps = (K + 31) / 32;
+  int splits = 1;
+  // aim for >= 768 blocks (3 per CU) without going below 8 k-steps per wave
+  while (ncol_tiles * mt * splits < 768 && nsteps / (splits * 2) >= 4 * 8) splits *= 2;
+  return splits;
+}
+
+GemmPlan plan_gemm(int M, int N, int K, int epi) {
+  GemmPlan p{};
+  if (M <= 64) {
+    p.kind = 0;
+    const int ncols = logical_cols(N, epi);
+    p.splits = skinny_splits(M, ncols, K);
+    p.ws_bytes = p.splits > 1 ? (size_t)p.splits * M * ncols * sizeof(float) : 0;
+  } else {
+    p.kind = 1;
+    p.splits = 1;
+    p.ws_bytes = 0;
+  }
+  return p;
+}
+
+hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, uint16_t *out, const uint16_t *res,
+                       int M, int N, int K, int epi, void *ws, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  const int ncols = logical_cols(N, epi);
+  if (p.kind == 0) {
+    const int nsteps = (K + 31) / 32;
+    const int splits = p.splits;
+    const int per = (nsteps + splits - 1) / splits;
+    float *part = splits > 1 ? reinterpret_cast<float *>(ws) : nullptr;
+    dim3 grid((ncols + SK_BN - 1) / SK_BN, splits, (M + SK_BM - 1) / SK_BM);
+    hipLaunchKernelGGL(k_gemm_skinny, grid, dim3(256), 0, st, A, W, out, res, part, M, N, K, epi, per);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || splits == 1) return e;
+    const int outc = epi == EPI_SILU_MUL ? N / 2 : N;
+    const long total = (long)M * outc;
+    const int blocks = (int)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
+    hipLaunchKernelGGL(k_gemm_splitk_epilogue, dim3(blocks), dim3(256), 0, st, part, splits, out, res, M, N, epi);
+    return hipGetLastError();
+  }
+  const int tiles_m = (M + TL_BM - 1) / TL_BM, tiles_n = (ncols + TL_BN - 1) / TL_BN;
+  hipLaunchKernelGGL(k_gemm_tiled, dim3(tiles_m * tiles_n), dim3(256), 0, st, A, W, out, res, M, N, K, epi, tiles_m,
+                     tiles_n);
+  return hipGetLastError();
+}
+
+}  // namespace eb

@@ -1,0 +1,155 @@
+// RMSNorm, RoPE + paged KV append, and the dense KV gather probe.
+#include "device_common.h"
+#include "eb_internal.h"
+
+namespace eb {
+
+// ---------------------------------------------------------------------------
+// RMSNorm: out = bf16(x / sqrt(mean(x^2) + eps) * gamma).  One wavefront per
+// row, 16-byte accesses; the second pass re-reads the row from cache.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t *__restrict__ x, const uint16_t *__restrict__ g,
+                                                 uint16_t *__restrict__ out, int rows, int d, float eps) {
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const uint16_t *xr = x + (size_t)row * d;
+  uint16_t *orow = out + (size_t)row * d;
+  const int nch = d >> 3;
+  float ss = 0.f;
+  for (int c = lane; c < nch; c += 64) {
+    u32x4_t v = ld_u32x4(xr + c * 8);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float a = bf16_lo(v[i]), b = bf16_hi(v[i]);
+      ss += a * a + b * b;
+    }
+  }
+  ss = wave_sum(ss);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  for (int c = lane; c < nch; c += 64) {
+    u32x4_t v = ld_u32x4(xr + c * 8);
+    u32x4_t gv = ld_u32x4(g + c * 8);
+    u32x4_t o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      o[i] = pack_bf16x2(bf16_lo(v[i]) * inv * bf16_lo(gv[i]), bf16_hi(v[i]) * inv * bf16_hi(gv[i]));
+    st_u32x4(orow + c * 8, o);
+  }
+}
+
+hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gamma, uint16_t *out, int rows, int d, float eps,
+                          hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_rmsnorm, dim3((rows + 3) / 4), dim3(256), 0, st, x, gamma, out, rows, d, eps);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// RoPE (rotate-half pairs (t, t + hd/2), frequency theta^(-2t/hd), angle
+// formed in fp64) on the q and k heads of one QKV row, q rotated in place,
+// rotated k and v stored at the row's slot of its request's paged cache.
+// One block per row.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv, uint16_t *__restrict__ kc,
+                                                     uint16_t *__restrict__ vc, const int32_t *__restrict__ bt,
+                                                     int num_pages, int max_pages, DevMeta m, int nq, int nkv,
+                                                     int hd, double log2_theta) {
+  __shared__ float cs[64], sn[64];
+  const int r = blockIdx.x;
+  const int seq = m.row_seq[r];
+  const int pos = m.row_pos[r];
+  const int half = hd >> 1;
+  for (int t = threadIdx.x; t < half; t += blockDim.x) {
+    const double inv_freq = exp2(-(2.0 * t / hd) * log2_theta);
+    double s, c;
+    sincos((double)pos * inv_freq, &s, &c);
+    cs[t] = (float)c;
+    sn[t] = (float)s;
+  }
+  __syncthreads();
+  const int cols = (nq + 2 * nkv) * hd;
+  uint16_t *row = qkv + (size_t)r * cols;
+  const int page = bt[(size_t)seq * max_pages + pos / kPageSize];
+  const bool page_ok = page >= 0 && page < num_pages;
+  const int slot = pos % kPageSize;
+  // q and k: one thread per rotation pair
+  const int pairs = (nq + nkv) * half;
+  for (int i = threadIdx.x; i < pairs; i += blockDim.x) {
+    const int h = i / half, t = i - h * half;
+    const float a = bf16_to_f32(row[h * hd + t]);
+    const float b = bf16_to_f32(row[h * hd + t + half]);
+    const float c = cs[t], s = sn[t];
+    const uint16_t ra = (uint16_t)f32_to_bf16_bits(a * c - b * s);
+    const uint16_t rb = (uint16_t)f32_to_bf16_bits(a * s + b * c);
+    if (h < nq) {
+      row[h * hd + t] = ra;
+      row[h * hd + t + half] = rb;
+    } else if (page_ok) {
+      const int kh = h - nq;
+      uint16_t *dst = kc + (((size_t)page * nkv + kh) * kPageSize + slot) * hd;
+      dst[t] = ra;
+      dst[t + half] = rb;
+    }
+  }
+  // v: plain copy
+  if (page_ok) {
+    const uint16_t *vsrc = row + (nq + nkv) * hd;
+    for (int i = threadIdx.x; i < nkv * hd; i += blockDim.x) {
+      const int kh = i / hd, dd = i - kh * hd;
+      vc[(((size_t)page * nkv + kh) * kPageSize + slot) * hd + dd] = vsrc[i];
+    }
+  }
+}
+
+hipError_t launch_rope_append(const Shape &s, uint16_t *qkv, const KV &kv, const DevMeta &m, hipStream_t st) {
+  if (m.T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_rope_append, dim3(m.T), dim3(256), 0, st, qkv, kv.k, kv.v, kv.bt, kv.num_pages, kv.max_pages,
+                     m, s.nq, s.nkv, s.hd, log2((double)s.theta));
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Dense gather of cached positions through the block tables (bit-exact
+// paging probe).  One thread per (position, kv head, 16-byte chunk).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_gather_kv(const uint16_t *__restrict__ kc, const uint16_t *__restrict__ vc,
+                                                   const int32_t *__restrict__ bt, int num_pages, int max_pages,
+                                                   DevMeta m, int nkv, int hd, uint16_t *__restrict__ ok,
+                                                   uint16_t *__restrict__ ov) {
+  const int chunks = hd / 8;
+  const long total = (long)m.gather_off[m.S] * nkv * chunks;
+  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
+    const int c = (int)(idx % chunks);
+    const long pk = idx / chunks;
+    const int kh = (int)(pk % nkv);
+    const int gp = (int)(pk / nkv);
+    int lo = 0, hi = m.S - 1;
+    while (lo < hi) {  // last request whose gather offset is <= gp
+      const int mid = (lo + hi + 1) >> 1;
+      if (m.gather_off[mid] <= gp) lo = mid; else hi = mid - 1;
+    }
+    const int seq = lo;
+    const int p = gp - m.gather_off[seq];
+    const int page = bt[(size_t)seq * max_pages + p / kPageSize];
+    u32x4_t kv4 = {0, 0, 0, 0}, vv4 = {0, 0, 0, 0};
+    if (page >= 0 && page < num_pages) {
+      const size_t src = (((size_t)page * nkv + kh) * kPageSize + p % kPageSize) * hd + c * 8;
+      kv4 = ld_u32x4(kc + src);
+      vv4 = ld_u32x4(vc + src);
+    }
+    const size_t dst = ((size_t)gp * nkv + kh) * hd + c * 8;
+    st_u32x4(ok + dst, kv4);
+    st_u32x4(ov + dst, vv4);
+  }
+}
+
+hipError_t launch_gather_kv(const Shape &s, const KV &kv, const DevMeta &m, uint16_t *out_k, uint16_t *out_v,
+                            hipStream_t st) {
+  if (m.S <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_gather_kv, dim3(1024), dim3(256), 0, st, kv.k, kv.v, kv.bt, kv.num_pages, kv.max_pages, m,
+                     s.nkv, s.hd, out_k, out_v);
+  return hipGetLastError();
+}
+
+}  // namespace eb
