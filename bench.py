@@ -1,0 +1,263 @@
+#!/usr/bin/env python
+"""Benchmark of one decoder-layer step on one MI355X.
+
+Default workload: the Llama-3-8B-shaped layer, pure-decode exclusive step, 64
+decode requests with contexts uniform in 512..4096, paged bf16 KV (page 16,
+seeded random block tables).  A step is the whole layer (RMSNorm, QKV GEMM,
+RoPE + KV append, split-K decode attention + combine, O GEMM + residual,
+RMSNorm, gate/up GEMM + SiLU*mul, down GEMM + residual) through the C ABI,
+with every input resident in HBM before the timed region.
+
+Prints one JSON line.  Other workloads: --workload prefill8b (8 prompts,
+lengths 256..2048 capped at 8192 tokens), mixed8b --r R (2048-token step at
+decode share R), copy (a plain device copy of known size, used to calibrate
+the HBM byte counters).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "step latency vs decode share; decode HBM GB/s; prefill MFMA TFLOP/s"
+HBM_PEAK_GBPS = 8000.0
+BF16_PEAK_TFLOPS = 2516.6
+ATTN_SRC = os.path.join(ROOT, "paper_2606_00516_amd", "csrc", "k_attention.hip")
+GEMM_SRC = os.path.join(ROOT, "paper_2606_00516_amd", "csrc", "k_gemm.hip")
+COUNTERS = os.path.join(ROOT, "profiles", "hbm_counters.json")
+
+
+def sha_of(path: str) -> str:
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="decode8b", choices=["decode8b", "prefill8b", "mixed8b", "copy"])
+    ap.add_argument("--r", type=float, default=0.5, help="decode share for mixed8b")
+    ap.add_argument("--budget", type=int, default=2048, help="token budget for mixed8b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--json-out", default=None)
+    return ap.parse_args()
+
+
+# ----------------------------------------------------------------------------
+# algorithmic work of a step (each byte / flop counted once)
+# ----------------------------------------------------------------------------
+
+def step_work(shape, batch):
+    """Bytes and FLOPs a step must move / compute at minimum."""
+    import numpy as np
+    nkv, hd, nq, d = shape.n_kv_heads, shape.head_dim, shape.n_q_heads, shape.hidden
+    c = batch.context_lens.astype(np.int64)
+    n = batch.chunk_lens.astype(np.int64)
+    dec = n == 1
+    kv_bytes_dec = int(((c[dec] + 1) * nkv * hd * 4).sum())
+    kv_bytes_pf = int(((c[~dec] + n[~dec]) * nkv * hd * 4).sum())
+    T = int(n.sum())
+    w_bytes = shape.weight_bytes()
+    act_bytes = T * d * 2 * 2
+    gemm_flops = 2 * T * (shape.qkv_rows * d + d * nq * hd + 2 * shape.ffn * d + d * shape.ffn)
+    attn_flops_dec = int((4 * nq * hd * (c[dec] + 1)).sum())
+    attn_flops_pf = int((4 * nq * hd * (n[~dec] * c[~dec] + n[~dec] * (n[~dec] + 1) // 2)).sum())
+    return dict(T=T, kv_bytes_decode=kv_bytes_dec, kv_bytes_prefill=kv_bytes_pf, weight_bytes=w_bytes,
+                act_bytes=act_bytes, gemm_flops=gemm_flops, attn_flops_decode=attn_flops_dec,
+                attn_flops_prefill=attn_flops_pf)
+
+
+def workload(args):
+    from paper_2606_00516_amd import inputs as gen
+    if args.workload == "decode8b":
+        return "llama3-8b-layer decode EB: 64 requests, ctx U[512,4096], page 16", gen.L8B, gen.batch_8b_decode(), \
+            "decode"
+    if args.workload == "prefill8b":
+        return "llama3-8b-layer prefill EB: 8 prompts U[256,2048] capped at 8192 tokens", gen.L8B, \
+            gen.batch_8b_prefill(), "prefill"
+    b = gen.batch_8b_mixed(args.r, args.budget)
+    return (f"llama3-8b-layer MB: {args.budget}-token step, decode share {args.r:.2f}, decode ctx U[1024,8192], "
+            f"chunks U[256,1024] with prefix U[0,2048]"), gen.L8B, b, "mixed"
+
+
+# ----------------------------------------------------------------------------
+# CPU oracle baseline
+# ----------------------------------------------------------------------------
+
+def cpu_baseline(shape, batch, w, pool, x, mode, target_s):
+    """The oracle as it is, on the host's cores, over as many requests of the
+    same workload as fit in about ``target_s`` seconds."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2606_00516_amd import inputs as gen
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    cfg = oracle.LayerCfg(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn,
+                          shape.page_size, shape.rms_eps, shape.rope_theta)
+    W = oracle.prepare_weights({k: gen.bits(v) for k, v in w.items()}, cfg)
+    need = gen.pages_needed(batch)
+    bt_host = pool.block_tables.cpu().numpy()
+    off = batch.row_offsets
+    xb = gen.bits(x)
+    done, spent, rows, kv_bytes = [], 0.0, 0, 0
+    order = np.argsort(batch.chunk_lens, kind="stable")     # cheapest requests first
+    for i in order:
+        ids = torch.as_tensor(bt_host[i, :need[i]].astype(np.int64), device=pool.k_cache.device)
+        kb = gen.bits(pool.k_cache.index_select(0, ids)).copy()
+        vb = gen.bits(pool.v_cache.index_select(0, ids)).copy()
+        bt = np.arange(need[i], dtype=np.int32)[None]
+        xs = xb[off[i]:off[i + 1]]
+        t0 = time.perf_counter()
+        oracle.layer_step(cfg, W, kb, vb, bt, batch.context_lens[i:i + 1], batch.chunk_lens[i:i + 1], xs)
+        spent += time.perf_counter() - t0
+        done.append(int(i))
+        rows += int(batch.chunk_lens[i])
+        c, n = int(batch.context_lens[i]), int(batch.chunk_lens[i])
+        kv_bytes += (c + n) * shape.n_kv_heads * shape.head_dim * 4
+        if spent >= target_s:
+            break
+    # one oracle call per request re-reads the weights each time; count them once
+    gbps = (kv_bytes + shape.weight_bytes()) / spent / 1e9
+    return {"value": round(gbps, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+            "tokens_per_s": round(rows / spent, 3), "seconds": round(spent, 2),
+            "sample": f"{len(done)} of {batch.num_seqs} requests ({rows} rows) of the same workload, fp32 numpy "
+                      f"oracle in batched mode, one request per call"}
+
+
+# ----------------------------------------------------------------------------
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported (the layer step has no "
+              f"multi-GPU path; data-parallel replicas would each run this same single-GPU step)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2606_00516_amd import binding as B
+    from paper_2606_00516_amd import inputs as gen
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    if args.workload == "copy":
+        n = 1 << 30
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / args.steps
+        print(json.dumps({"workload": "copy", "bytes_read": n, "bytes_written": n, "ms": dt * 1e3,
+                          "GBps": 2 * n / dt / 1e9}))
+        return
+
+    label, shape, batch, mode = workload(args)
+    step_fn = {"decode": B.eb_layer_step_decode, "prefill": B.eb_layer_step_prefill,
+               "mixed": B.eb_layer_step_mixed}[mode]
+    # inputs generated on the GPU and left resident in HBM
+    w = gen.make_weights(shape, device=dev)
+    pool = gen.make_kv_pool(shape, batch, device=dev)
+    x = gen.make_x(shape, batch.num_tokens, device=dev)
+    y = torch.empty_like(x)
+    h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
+    ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
+    call = lambda: step_fn(h, w, pool.k_cache, pool.v_cache, pool.block_tables, batch.context_lens,  # noqa: E731
+                           batch.chunk_lens, x, y=y, ws=ws)
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        call()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / args.steps * 1e3
+
+    # per-stage durations: HIP events the library records around each stage on
+    # the stream it launches on, over a second pass of the same steps
+    B.eb_profile(h, True)
+    acc = {}
+    for _ in range(args.steps):
+        call()
+        for k, v in B.eb_profile_read(h).items():
+            acc[k] = acc.get(k, 0.0) + v
+    B.eb_profile(h, False)
+    stages = {k: v / args.steps for k, v in acc.items()}
+    torch.cuda.synchronize()
+
+    wk = step_work(shape, batch)
+    step_bytes = wk["kv_bytes_decode"] + wk["kv_bytes_prefill"] + wk["weight_bytes"] + wk["act_bytes"]
+    step_flops = wk["gemm_flops"] + wk["attn_flops_decode"] + wk["attn_flops_prefill"]
+    gemm_ms = sum(v for k, v in stages.items() if k.endswith("gemm"))
+    attn_ms = stages.get("attention", 0.0) + stages.get("attention_combine", 0.0)
+
+    if mode == "decode":
+        unit = "GB/s"
+        value = step_bytes / (ms / 1e3) / 1e9
+        a_ms = stages["attention"]
+        achieved = wk["kv_bytes_decode"] / (a_ms / 1e3) / 1e9
+        roof = {"kernel": "k_decode (split-K paged decode attention)", "bound": "hbm",
+                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "avg_launch_ms": round(a_ms, 5),
+                "bytes_per_launch": wk["kv_bytes_decode"], "traffic": None}
+    else:
+        unit = "TFLOP/s"
+        value = step_flops / (ms / 1e3) / 1e12
+        g_ms = stages["gate_up_gemm"]
+        fl = 2 * wk["T"] * 2 * shape.ffn * shape.hidden
+        achieved = fl / (g_ms / 1e3) / 1e12
+        roof = {"kernel": "k_gemm_tiled (gate/up projection + SiLU*mul)", "bound": "mfma",
+                "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "avg_launch_ms": round(g_ms, 5),
+                "flops_per_launch": fl, "traffic": None}
+    # HBM traffic from committed counter runs, only if the kernel is unchanged
+    try:
+        cnt = json.load(open(COUNTERS))
+        key = "decode_attention_8b" if mode == "decode" else None
+        ent = cnt.get(key) if key else None
+        if ent and ent.get("source_sha") == sha_of(ATTN_SRC):
+            roof["traffic"] = ent["bytes_per_dispatch"]
+    except (OSError, ValueError):
+        pass
+
+    line = {
+        "metric": METRIC, "value": round(value, 3), "unit": unit, "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": label, "num_tokens": wk["T"], "num_requests": batch.num_seqs,
+                   "decode_share": round(batch.num_decode / max(wk["T"], 1), 4), "parallelism": "single-gpu"},
+        "tokens_per_s": round(wk["T"] / (ms / 1e3), 1),
+        "step_bytes": step_bytes, "step_flops": step_flops,
+        "stage_ms": {k: round(v, 5) for k, v in stages.items()},
+        "gemm_ms": round(gemm_ms, 5), "attention_ms": round(attn_ms, 5),
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(shape, batch, w, pool, x, mode, args.cpu_seconds)
+    out = json.dumps(line)
+    print(out)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(out + "\n")
+
+
+if __name__ == "__main__":
+    main()

@@ -148,6 +148,17 @@ eb_status eb_layer_step_mixed(eb_handle *h, const eb_layer_weights *w, const eb_
 eb_status eb_validate(const eb_layer_config *cfg, const eb_batch *batch, const int32_t *block_tables_host,
                       int32_t num_pages, int32_t max_pages_per_seq, eb_mode mode);
 
+/* Per-stage timing.  With eb_profile(h, 1) every step records HIP events
+ * around each stage on its stream (a few microseconds of overhead per
+ * stage); eb_profile_read() waits for the last step recorded on h and
+ * writes the duration in ms of up to `cap` stages into ms[] (host), in
+ * launch order, returning how many it wrote (0 if no profiled step has run,
+ * -1 on a HIP error).  Stage names: eb_profile_stage_name(i) (NULL past the
+ * last).  Stages a step does not need read 0. */
+eb_status eb_profile(eb_handle *h, int32_t enable);
+int32_t eb_profile_read(eb_handle *h, float *ms, int32_t cap);
+const char *eb_profile_stage_name(int32_t i);
+
 const char *eb_status_str(eb_status s);
 const char *eb_last_error(void); /* thread-local message of the last failure */
 

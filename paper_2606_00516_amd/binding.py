@@ -28,7 +28,7 @@ EPILOGUES = {"store": 0, "residual": 1, "silu_mul": 2}
 SYMBOLS = ("eb_create", "eb_destroy", "eb_workspace_bytes", "eb_layer_step_decode", "eb_layer_step_prefill",
            "eb_layer_step_mixed", "eb_validate", "eb_status_str", "eb_last_error", "eb_op_rmsnorm",
            "eb_op_gemm_workspace_bytes", "eb_op_gemm", "eb_op_rope_kv_append", "eb_op_attention",
-           "eb_op_gather_kv")
+           "eb_op_gather_kv", "eb_profile", "eb_profile_read", "eb_profile_stage_name")
 
 
 class EbError(RuntimeError):
@@ -82,6 +82,9 @@ def lib() -> ctypes.CDLL:
         "eb_op_rope_kv_append": (I32, [VP, VP, P(KvCache), P(Batch), VP, SZ, VP]),
         "eb_op_attention": (I32, [VP, VP, P(KvCache), P(Batch), VP, VP, SZ, I32, VP]),
         "eb_op_gather_kv": (I32, [VP, P(KvCache), P(Batch), VP, VP, VP, SZ, VP]),
+        "eb_profile": (I32, [VP, I32]),
+        "eb_profile_read": (I32, [VP, P(ctypes.c_float), I32]),
+        "eb_profile_stage_name": (ctypes.c_char_p, [I32]),
     }
     for name in ("eb_layer_step_decode", "eb_layer_step_prefill", "eb_layer_step_mixed"):
         sig[name] = (I32, [VP, P(LayerWeights), P(KvCache), P(Batch), VP, VP, VP, SZ, VP])
@@ -280,3 +283,16 @@ def eb_op_gather_kv(h: Handle, k_cache, v_cache, block_tables, context_lens, chu
     _check(lib().eb_op_gather_kv(h.h, ctypes.byref(kv), ctypes.byref(hb.c), _ptr(ok), _ptr(ov), _ptr(ws), ws.numel(),
                                  _stream(stream)))
     return ok, ov
+
+
+def eb_profile(h: Handle, enable: bool = True):
+    _check(lib().eb_profile(h.h, 1 if enable else 0))
+
+
+def eb_profile_read(h: Handle) -> dict:
+    """Stage name -> ms of the last profiled step on this handle."""
+    buf = (ctypes.c_float * 32)()
+    n = lib().eb_profile_read(h.h, buf, 32)
+    if n < 0:
+        raise EbError(-8, "eb_profile_read failed")
+    return {lib().eb_profile_stage_name(i).decode(): float(buf[i]) for i in range(n)}

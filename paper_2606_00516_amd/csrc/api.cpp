@@ -22,6 +22,11 @@ eb_status fail(eb_status s, const std::string &msg) {
 
 constexpr int kRing = 4;  // pinned staging slots per handle
 
+// Stages of a step, in launch order (names returned by eb_profile_stage_name).
+constexpr int kStages = 9;
+const char *const kStageNames[kStages] = {"rmsnorm_1", "qkv_gemm", "rope_kv_append", "attention", "attention_combine",
+                                          "o_gemm", "rmsnorm_2", "gate_up_gemm", "down_gemm"};
+
 size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
 
 Shape shape_of(const eb_layer_config &c) {
@@ -102,6 +107,10 @@ struct eb_handle {
   hipEvent_t ev[kRing];
   bool used[kRing];
   int next;
+  // per-stage timing of the last step (eb_profile)
+  bool prof;
+  bool prof_valid;
+  hipEvent_t pev[2 * kStages];
 };
 
 namespace {
@@ -195,29 +204,41 @@ eb_status run_step(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *k
   uint16_t *yout = static_cast<uint16_t *>(y);
   const int T = p.T;
   hipError_t e;
-#define EB_TRY(call, what)                 \
-  if ((e = (call)) != hipSuccess) {        \
-    return hip_fail(e, what);              \
-  }
-  EB_TRY(launch_rmsnorm(xin, static_cast<const uint16_t *>(w->attn_norm), act, T, sh.hidden, sh.eps, st), "rmsnorm1");
-  EB_TRY(launch_gemm(plan_gemm(T, sh.qkv_cols(), sh.hidden, EPI_STORE), act, static_cast<const uint16_t *>(w->w_qkv),
-                     qkv, nullptr, T, sh.qkv_cols(), sh.hidden, EPI_STORE, gws, st),
-         "qkv gemm");
-  EB_TRY(launch_rope_append(sh, qkv, kvd, m, st), "rope/kv append");
+  h->prof_valid = false;
+  auto mark = [&](int i) -> hipError_t { return h->prof ? hipEventRecord(h->pev[i], st) : hipSuccess; };
+#define EB_STAGE(idx, call, what)                                       \
+  if ((e = mark(2 * (idx))) != hipSuccess) return hip_fail(e, "hipEventRecord"); \
+  if ((e = (call)) != hipSuccess) return hip_fail(e, what);              \
+  if ((e = mark(2 * (idx) + 1)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  EB_STAGE(0, launch_rmsnorm(xin, static_cast<const uint16_t *>(w->attn_norm), act, T, sh.hidden, sh.eps, st),
+           "rmsnorm1");
+  EB_STAGE(1,
+           launch_gemm(plan_gemm(T, sh.qkv_cols(), sh.hidden, EPI_STORE), act,
+                       static_cast<const uint16_t *>(w->w_qkv), qkv, nullptr, T, sh.qkv_cols(), sh.hidden, EPI_STORE,
+                       gws, st),
+           "qkv gemm");
+  EB_STAGE(2, launch_rope_append(sh, qkv, kvd, m, st), "rope/kv append");
   const int kind = mode == EB_MODE_DECODE ? 0 : (mode == EB_MODE_PREFILL ? 1 : 2);
-  EB_TRY(launch_attention(sh, qkv, kvd, m, attn, part_o, part_ml, kind, st), "attention");
-  EB_TRY(launch_gemm(plan_gemm(T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL), attn, static_cast<const uint16_t *>(w->w_o),
-                     h1, xin, T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, gws, st),
-         "o gemm");
-  EB_TRY(launch_rmsnorm(h1, static_cast<const uint16_t *>(w->mlp_norm), act, T, sh.hidden, sh.eps, st), "rmsnorm2");
-  EB_TRY(launch_gemm(plan_gemm(T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL), act,
-                     static_cast<const uint16_t *>(w->w_gate_up), mlp, nullptr, T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL,
-                     gws, st),
-         "gate/up gemm");
-  EB_TRY(launch_gemm(plan_gemm(T, sh.hidden, sh.ffn, EPI_RESIDUAL), mlp, static_cast<const uint16_t *>(w->w_down), yout,
-                     h1, T, sh.hidden, sh.ffn, EPI_RESIDUAL, gws, st),
-         "down gemm");
-#undef EB_TRY
+  EB_STAGE(3, launch_attention(sh, qkv, kvd, m, attn, part_o, part_ml, kind, st, 1), "attention");
+  EB_STAGE(4, launch_attention(sh, qkv, kvd, m, attn, part_o, part_ml, kind, st, 2), "attention combine");
+  EB_STAGE(5,
+           launch_gemm(plan_gemm(T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL), attn,
+                       static_cast<const uint16_t *>(w->w_o), h1, xin, T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, gws,
+                       st),
+           "o gemm");
+  EB_STAGE(6, launch_rmsnorm(h1, static_cast<const uint16_t *>(w->mlp_norm), act, T, sh.hidden, sh.eps, st),
+           "rmsnorm2");
+  EB_STAGE(7,
+           launch_gemm(plan_gemm(T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL), act,
+                       static_cast<const uint16_t *>(w->w_gate_up), mlp, nullptr, T, 2 * sh.ffn, sh.hidden,
+                       EPI_SILU_MUL, gws, st),
+           "gate/up gemm");
+  EB_STAGE(8,
+           launch_gemm(plan_gemm(T, sh.hidden, sh.ffn, EPI_RESIDUAL), mlp, static_cast<const uint16_t *>(w->w_down),
+                       yout, h1, T, sh.hidden, sh.ffn, EPI_RESIDUAL, gws, st),
+           "down gemm");
+#undef EB_STAGE
+  h->prof_valid = h->prof;
   return EB_OK;
 }
 
@@ -261,6 +282,9 @@ eb_status eb_create(const eb_layer_config *cfg, int32_t max_seqs, int32_t max_to
     return hip_fail(e, "hipGetDevice");
   }
   h->slot_cap = plan_capacity(max_seqs, max_tokens, cfg->n_q_heads / cfg->n_kv_heads);
+  h->prof = false;
+  h->prof_valid = false;
+  for (int i = 0; i < 2 * kStages; ++i) h->pev[i] = nullptr;
   for (int k = 0; k < kRing; ++k) {
     h->pinned[k] = nullptr;
     h->ev[k] = nullptr;
@@ -287,6 +311,8 @@ void eb_destroy(eb_handle *h) {
     }
     if (h->pinned[k]) (void)hipHostFree(h->pinned[k]);
   }
+  for (int i = 0; i < 2 * kStages; ++i)
+    if (h->pev[i]) (void)hipEventDestroy(h->pev[i]);
   delete h;
 }
 
@@ -327,6 +353,33 @@ eb_status eb_validate(const eb_layer_config *cfg, const eb_batch *batch, const i
   if (s != EB_OK) return fail(s, err);
   return EB_OK;
 }
+
+eb_status eb_profile(eb_handle *h, int32_t enable) {
+  if (!h) return fail(EB_ERR_NULL, "handle is NULL");
+  if (enable && !h->pev[0]) {
+    for (int i = 0; i < 2 * kStages; ++i) {
+      hipError_t e = hipEventCreate(&h->pev[i]);
+      if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+    }
+  }
+  h->prof = enable != 0;
+  h->prof_valid = false;
+  return EB_OK;
+}
+
+int32_t eb_profile_read(eb_handle *h, float *ms, int32_t cap) {
+  if (!h || !h->prof_valid) return 0;
+  if (hipEventSynchronize(h->pev[2 * kStages - 1]) != hipSuccess) return -1;
+  const int n = cap < kStages ? cap : kStages;
+  for (int i = 0; i < n; ++i) {
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, h->pev[2 * i], h->pev[2 * i + 1]) != hipSuccess) return -1;
+    ms[i] = t;
+  }
+  return n;
+}
+
+const char *eb_profile_stage_name(int32_t i) { return (i >= 0 && i < kStages) ? kStageNames[i] : nullptr; }
 
 // ---------------------------------------------------------------------------
 // single operations

@@ -52,9 +52,10 @@ hipError_t launch_rope_append(const Shape &s, uint16_t *qkv, const KV &kv, const
 hipError_t launch_gather_kv(const Shape &s, const KV &kv, const DevMeta &m, uint16_t *out_k, uint16_t *out_v,
                             hipStream_t st);
 
-// attention: kind 0 = decode only, 1 = prefill only, 2 = mixed single launch
+// attention: kind 0 = decode only, 1 = prefill only, 2 = mixed single launch;
+// parts: 1 = the attention kernel(s), 2 = the decode split combine, 3 = both
 hipError_t launch_attention(const Shape &s, const uint16_t *qkv, const KV &kv, const DevMeta &m, uint16_t *out,
-                            float *part_o, float *part_ml, int kind, hipStream_t st);
+                            float *part_o, float *part_ml, int kind, hipStream_t st, int parts = 3);
 
 // GEMM planning shared by the op entry and the step.
 enum GemmEpi { EPI_STORE = 0, EPI_RESIDUAL = 1, EPI_SILU_MUL = 2 };

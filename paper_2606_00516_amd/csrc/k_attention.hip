@@ -493,10 +493,13 @@ __global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int 
 
 template <int HD, int G>
 static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const KV &kv, const DevMeta &m,
-                                     uint16_t *out, float *part_o, float *part_ml, int kind, hipStream_t st) {
+                                     uint16_t *out, float *part_o, float *part_ml, int kind, int parts,
+                                     hipStream_t st) {
   const int nkv = s.nkv, nq = s.nq;
   const bool has_dec = m.n_dec > 0, has_pf = m.n_tiles > 0;
-  if (kind == 2 && has_dec && has_pf) {
+  if (!(parts & 1)) {
+    // combine only
+  } else if (kind == 2 && has_dec && has_pf) {
     hipLaunchKernelGGL((k_mixed<HD, G>), dim3(m.n_tiles + m.total_splits, nkv), dim3(256), 0, st, qkv, nq, nkv, kv, m,
                        out, part_o, part_ml);
   } else {
@@ -507,16 +510,16 @@ static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const 
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (m.n_comb > 0)
+  if ((parts & 2) && m.n_comb > 0)
     hipLaunchKernelGGL((k_decode_combine<HD, G>), dim3(m.n_comb, nq), dim3(64), 0, st, m, part_o, part_ml, out, nq, nkv);
   return hipGetLastError();
 }
 
 hipError_t launch_attention(const Shape &s, const uint16_t *qkv, const KV &kv, const DevMeta &m, uint16_t *out,
-                            float *part_o, float *part_ml, int kind, hipStream_t st) {
+                            float *part_o, float *part_ml, int kind, hipStream_t st, int parts) {
   const int G = s.group();
 #define EB_ATT_CASE(HD_, G_) \
-  if (s.hd == HD_ && G == G_) return launch_attention_t<HD_, G_>(s, qkv, kv, m, out, part_o, part_ml, kind, st);
+  if (s.hd == HD_ && G == G_) return launch_attention_t<HD_, G_>(s, qkv, kv, m, out, part_o, part_ml, kind, parts, st);
   EB_ATT_CASE(128, 1) EB_ATT_CASE(128, 2) EB_ATT_CASE(128, 4) EB_ATT_CASE(128, 8)
   EB_ATT_CASE(64, 1) EB_ATT_CASE(64, 2) EB_ATT_CASE(64, 4) EB_ATT_CASE(64, 8)
 #undef EB_ATT_CASE

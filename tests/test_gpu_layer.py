@@ -33,7 +33,7 @@ def run_gpu(case: Case, mode: str, handle=None):
 def test_tiny_step_vs_oracle(mode):
     case = tiny_case(mode)
     y, d, bk, bv = run_gpu(case, mode)
-    (ref, _), o = case.run_oracle(mode="batched")
+    ref, o = case.run_oracle(mode="batched")
     assert np.isfinite(y).all()
     assert maxrel(y, ref) < TOL
     errs = per_request_maxrel(y, ref, case.batch.row_offsets)
@@ -44,13 +44,17 @@ def test_tiny_step_vs_oracle(mode):
 
 
 def test_tiny_step_sharp_attention():
-    # projections N(0, 0.2): peaky softmax, so attention errors are not hidden
-    # by near-uniform weights
+    # Projections N(0, 0.08) give attention scores of standard deviation ~1.6
+    # (q, k entries ~ 0.08 * sqrt(256)), so the softmax is far from uniform
+    # and attention errors are not averaged away.  Much larger spreads make
+    # the step ill-conditioned for bf16 intermediates: with scores of ~10 a
+    # 2^-9 rounding of q alone moves single probabilities by several percent.
     shape = gen.TINY
-    case = make_case(shape, gen.batch_tiny(mode="mixed"), weights=gen.make_weights(shape, proj_std=0.2))
+    case = make_case(shape, gen.batch_tiny(mode="mixed"), weights=gen.make_weights(shape, proj_std=0.08))
     y, d, bk, bv = run_gpu(case, "mixed")
-    (ref, inter), o = case.run_oracle(mode="batched", intermediates=True)
+    ref, o = case.run_oracle(mode="batched")
     errs = per_request_maxrel(y, ref, case.batch.row_offsets)
+    print("per-request max-rel", errs)
     assert max(errs) < TOL, errs
 
 
@@ -167,6 +171,7 @@ def _sampled_parity(shape, batch, w, Wo, mode, sample, tol=TOL):
     ref = oracle.layer_step(oracle_cfg(shape), Wo, kb, vb, bt, sub.context_lens, sub.chunk_lens, xs)
     so = sub.row_offsets
     errs = [maxrel(y[off[i]:off[i + 1]], ref[so[k]:so[k + 1]]) for k, i in enumerate(sample)]
+    print(f"{mode} {batch.label}: sampled requests {list(sample)} max-rel {errs}")
     assert max(errs) < tol, errs
     return errs
 
