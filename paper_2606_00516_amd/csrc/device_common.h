@@ -7,6 +7,7 @@
 #define EB_DEV __device__ __forceinline__
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
@@ -66,6 +67,21 @@ EB_DEV u32x4_t ld_stream_u32x4(const void *p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
 }
 
+// Raw buffer access: a descriptor over [base, base + bytes); loads past the
+// end return zero without touching memory, so a wave-uniform "no data"
+// case needs no branch.  (Word 3 of the descriptor as gfx9 requires.)
+typedef __amdgpu_buffer_rsrc_t buf_rsrc_t;
+EB_DEV buf_rsrc_t make_rsrc(const void *base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, bytes, 0x00020000);
+}
+// 16-byte load at byte offset `off`; AUX = 2 marks data read exactly once
+// (non-temporal).
+constexpr int kAuxNT = 2;
+template <int AUX = 0>
+EB_DEV u32x4_t buf_ld_u32x4(buf_rsrc_t r, int off) {
+  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX));
+}
+
 EB_DEV bf16x8_t as_bf16x8(u32x4_t v) { return __builtin_bit_cast(bf16x8_t, v); }
 
 // D = A B + C on one 16x16x32 bf16 tile.  Operand layout (lane l):
@@ -73,6 +89,13 @@ EB_DEV bf16x8_t as_bf16x8(u32x4_t v) { return __builtin_bit_cast(bf16x8_t, v); }
 //   C/D: rows 4 (l / 16) .. + 3, col l % 16
 EB_DEV f32x4_t mfma16x16x32(u32x4_t a, u32x4_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+
+// c + a.lo * b.lo + a.hi * b.hi on bf16 pairs packed in 32-bit words.  (The
+// words arrive as plain values: bit-casting a vector element in place has
+// been seen to read element 0 instead.)
+EB_DEV float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c, false);
 }
 
 EB_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }

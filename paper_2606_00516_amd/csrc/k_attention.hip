@@ -44,15 +44,81 @@ __device__ __forceinline__ void lse_merge(float &m, float &l, float *o, float m2
   m = mx;
 }
 
+// Page buffers a wavefront keeps in flight while it works on another page
+// (three named register sets, rotated by hand so they stay in registers).
+template <int HD, int NLD>
+__device__ __forceinline__ void decode_load_page(u32x4_t (&k)[NLD], u32x4_t (&v)[NLD], const KV kv,
+                                                 const int32_t *bt, int p, int pg1, int nkv, int kh, int lane) {
+  // page p of the split is wave-uniform; past the end (or a bad table
+  // entry) the descriptors cover zero bytes and the loads return zero
+  const int phys = p < pg1 ? bt[p] : -1;
+  const bool ok = phys >= 0 && phys < kv.num_pages;
+  const size_t off = ok ? ((size_t)phys * nkv + kh) * kPageSize * HD : 0;
+  const int bytes = ok ? kPageSize * HD * 2 : 0;
+  const buf_rsrc_t rk = make_rsrc(kv.k + off, bytes);
+  const buf_rsrc_t rv = make_rsrc(kv.v + off, bytes);
+#pragma unroll
+  for (int j = 0; j < NLD; ++j) {
+    k[j] = buf_ld_u32x4<kAuxNT>(rk, lane * 16 + j * 1024);
+    v[j] = buf_ld_u32x4<kAuxNT>(rv, lane * 16 + j * 1024);
+  }
+}
+
+// Online-softmax update of one lane's (max, sum, output) state with the
+// tokens of one page it holds.
 template <int HD, int G>
-__device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV &kv,
-                                            const DevMeta &md, int item, int kh, uint16_t *__restrict__ out,
+__device__ __forceinline__ void decode_page_update(const u32x4_t (&k)[HD / 32], const u32x4_t (&v)[HD / 32],
+                                                   const u32x4_t (&qw)[G], float (&mrun)[G], float (&lrun)[G],
+                                                   float (&o)[G][8], int p, int k1, int lane, float qscale) {
+  constexpr int LPT = HD / 8, TG = 64 / LPT, NLD = HD / 32;
+  bool valid[NLD];
+#pragma unroll
+  for (int j = 0; j < NLD; ++j) valid[j] = p * kPageSize + j * TG + lane / LPT < k1;
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    float sc[NLD];
+    float mx = mrun[h];
+#pragma unroll
+    for (int j = 0; j < NLD; ++j) {
+      float acc = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        acc = dot2_bf16(qw[h][i], k[j][i], acc);
+      acc = group_sum<LPT>(acc) * qscale;
+      sc[j] = valid[j] ? acc : kNegInf;
+      mx = fmaxf(mx, sc[j]);
+    }
+    const float alpha = (mrun[h] == kNegInf) ? 0.f : fast_exp2(mrun[h] - mx);
+    float l = lrun[h] * alpha;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[h][i] *= alpha;
+#pragma unroll
+    for (int j = 0; j < NLD; ++j) {
+      // masked tokens: probability 0, value never read (may be NaN poison)
+      const float pj = valid[j] ? fast_exp2(sc[j] - mx) : 0.f;
+      l += pj;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t w = valid[j] ? v[j][i] : 0u;
+        o[h][2 * i] = fmaf(pj, bf16_lo(w), o[h][2 * i]);
+        o[h][2 * i + 1] = fmaf(pj, bf16_hi(w), o[h][2 * i + 1]);
+      }
+    }
+    lrun[h] = l;
+    mrun[h] = mx;
+  }
+}
+
+template <int HD, int G>
+__device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
+                                            const DevMeta md, int item, int kh, uint16_t *__restrict__ out,
                                             float *__restrict__ part_o, float *__restrict__ part_ml, float *lds) {
   using Tr = DecodeTraits<HD, G>;
-  constexpr int LPT = Tr::LPT, TG = Tr::TG, NLD = Tr::NLD;
+  constexpr int LPT = Tr::LPT, NLD = Tr::NLD;
   constexpr int SPLIT = kDecodePagesPerSplit * kPageSize;
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  // wave index made visibly uniform, so page addressing stays scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int cols = (nq + 2 * nkv) * HD;
 
   // locate the decode request owning this split
@@ -73,19 +139,13 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
   const int pg0 = k0 / kPageSize, pg1 = (k1 + kPageSize - 1) / kPageSize;
   const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
 
-  // queries of the G heads, this lane's 8 dims, pre-scaled for exp2
+  // queries of the G heads, this lane's 8 dims, as bf16 pairs (loaded
+  // first: the page loads issued after them then stay in flight)
   const int dq = (lane % LPT) * 8;
   const float qscale = kLog2e / sqrtf((float)HD);
-  float q[G][8];
+  u32x4_t qw[G];
 #pragma unroll
-  for (int h = 0; h < G; ++h) {
-    u32x4_t w = ld_u32x4(qkv + (size_t)row * cols + (kh * G + h) * HD + dq);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      q[h][2 * i] = bf16_lo(w[i]) * qscale;
-      q[h][2 * i + 1] = bf16_hi(w[i]) * qscale;
-    }
-  }
+  for (int h = 0; h < G; ++h) qw[h] = ld_u32x4(qkv + (size_t)row * cols + (kh * G + h) * HD + dq);
   float mrun[G], lrun[G], o[G][8];
 #pragma unroll
   for (int h = 0; h < G; ++h) {
@@ -95,81 +155,44 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
     for (int i = 0; i < 8; ++i) o[h][i] = 0.f;
   }
 
-  auto load_page = [&](int p, u32x4_t *kr, u32x4_t *vr) {
-    const int phys = bt[p];
-    if (phys >= 0 && phys < kv.num_pages) {
-      const size_t base = ((size_t)phys * nkv + kh) * kPageSize * HD + lane * 8;
-#pragma unroll
-      for (int j = 0; j < NLD; ++j) {
-        kr[j] = ld_stream_u32x4(kv.k + base + j * 512);
-        vr[j] = ld_stream_u32x4(kv.v + base + j * 512);
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < NLD; ++j) kr[j] = vr[j] = u32x4_t{0, 0, 0, 0};
+  // Wave w streams pages w, w+4, ... through a ring of page buffers (three
+  // for G <= 2, two for larger groups, whose accumulators need the
+  // registers), rotated in straight-line code; pages past the split's end
+  // load as zeros without memory traffic and are masked out.
+  const int pfirst = pg0 + wave;
+  u32x4_t ka[NLD], va[NLD], kb[NLD], vb[NLD], kc[NLD], vc[NLD];
+  // scheduling barriers keep page loads and page updates in program order,
+  // so the wait before an update covers only that page's loads
+#define EB_LOAD(K_, V_, P_)                                                  \
+  decode_load_page<HD, NLD>(K_, V_, kv, bt, P_, pg1, nkv, kh, lane);         \
+  __builtin_amdgcn_sched_barrier(0);
+#define EB_UPDATE(K_, V_, P_)                                                \
+  decode_page_update<HD, G>(K_, V_, qw, mrun, lrun, o, P_, k1, lane, qscale); \
+  __builtin_amdgcn_sched_barrier(0);
+  EB_LOAD(ka, va, pfirst)
+  EB_LOAD(kb, vb, pfirst + 4)
+  if constexpr (G <= 2) {
+    EB_LOAD(kc, vc, pfirst + 8)
+    for (int p = pfirst; p < pg1; p += 12) {
+      EB_UPDATE(ka, va, p)
+      EB_LOAD(ka, va, p + 12)
+      EB_UPDATE(kb, vb, p + 4)
+      EB_LOAD(kb, vb, p + 16)
+      EB_UPDATE(kc, vc, p + 8)
+      EB_LOAD(kc, vc, p + 20)
     }
-  };
-
-  u32x4_t kc[NLD], vc[NLD], kn[NLD], vn[NLD];
-#pragma unroll
-  for (int j = 0; j < NLD; ++j) kc[j] = vc[j] = kn[j] = vn[j] = u32x4_t{0, 0, 0, 0};
-  int p = pg0 + wave;
-  if (p < pg1) load_page(p, kc, vc);
-  for (; p < pg1; p += 4) {
-    const int pn = p + 4;
-    if (pn < pg1) load_page(pn, kn, vn);
-    // token of load j in this lane
-    bool valid[NLD];
-#pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      const int t = p * kPageSize + j * TG + lane / LPT;
-      valid[j] = (t >= k0) && (t < k1);
-      if (!valid[j]) vc[j] = u32x4_t{0, 0, 0, 0};
-    }
-    float kf[NLD][8];
-#pragma unroll
-    for (int j = 0; j < NLD; ++j)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        kf[j][2 * i] = bf16_lo(kc[j][i]);
-        kf[j][2 * i + 1] = bf16_hi(kc[j][i]);
-      }
-#pragma unroll
-    for (int h = 0; h < G; ++h) {
-      float s[NLD];
-      float mx = mrun[h];
-#pragma unroll
-      for (int j = 0; j < NLD; ++j) {
-        float acc = 0.f;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc = fmaf(q[h][i], kf[j][i], acc);
-        acc = group_sum<LPT>(acc);
-        s[j] = valid[j] ? acc : kNegInf;
-        mx = fmaxf(mx, s[j]);
-      }
-      const float alpha = (mrun[h] == kNegInf) ? 0.f : fast_exp2(mrun[h] - mx);
-      float l = lrun[h] * alpha;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) o[h][i] *= alpha;
-#pragma unroll
-      for (int j = 0; j < NLD; ++j) {
-        const float pj = (s[j] == kNegInf) ? 0.f : fast_exp2(s[j] - mx);
-        l += pj;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          o[h][2 * i] = fmaf(pj, bf16_lo(vc[j][i]), o[h][2 * i]);
-          o[h][2 * i + 1] = fmaf(pj, bf16_hi(vc[j][i]), o[h][2 * i + 1]);
-        }
-      }
-      lrun[h] = l;
-      mrun[h] = mx;
-    }
-#pragma unroll
-    for (int j = 0; j < NLD; ++j) {
-      kc[j] = kn[j];
-      vc[j] = vn[j];
+  } else {
+    (void)kc;
+    (void)vc;
+    for (int p = pfirst; p < pg1; p += 8) {
+      EB_UPDATE(ka, va, p)
+      EB_LOAD(ka, va, p + 8)
+      EB_UPDATE(kb, vb, p + 4)
+      EB_LOAD(kb, vb, p + 12)
     }
   }
+#undef EB_LOAD
+#undef EB_UPDATE
 
   // merge the token groups of this wave (lanes with equal lane % LPT)
 #pragma unroll
@@ -283,8 +306,8 @@ struct PrefillTraits {
 };
 
 template <int HD, int G>
-__device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV &kv,
-                                             const DevMeta &md, int tile, int kh, uint16_t *__restrict__ out,
+__device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
+                                             const DevMeta md, int tile, int kh, uint16_t *__restrict__ out,
                                              uint16_t *lds) {
   using Tr = PrefillTraits<HD, G>;
   constexpr int BQ = Tr::BQ, RB = Tr::RB, KT = Tr::KT, KSS = Tr::KS_STRIDE, VTS = Tr::VT_STRIDE;

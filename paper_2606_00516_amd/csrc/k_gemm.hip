@@ -43,14 +43,42 @@ __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)
 // ===========================================================================
 constexpr int SK_BN = 64;     // logical columns per block
 constexpr int SK_BM = 64;     // rows per block
-constexpr int SK_UNROLL = 2;  // k-steps of 32 per loop trip per wave
+
+// One k-step (32 deep) of operand fragments for a 64 x 64 block: 4 row
+// blocks of A, 4 column blocks of W (16 x 32 each, 16 bytes per lane).
+struct SkinnyFrags {
+  u32x4_t a[4], b[4];
+};
+
+// Offsets are byte offsets into A / W; a fragment outside the matrix (row
+// past the end, k past K, k-step past the split) gets an offset past the
+// descriptor's range and loads as zero without memory traffic.
+__device__ __forceinline__ void skinny_load(SkinnyFrags &f, buf_rsrc_t ra, buf_rsrc_t rw, const uint32_t (&aoff)[4],
+                                            const uint32_t (&woff)[4], int ks, int ks_end, int lk, int K) {
+  const int k = ks * 32 + lk;
+  const bool kin = ks < ks_end && k < K;
+  const uint32_t kb = (uint32_t)k * 2u;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f.a[i] = buf_ld_u32x4<0>(ra, (int)(kin ? aoff[i] + kb : 0xFFFFFFF0u));
+    f.b[i] = buf_ld_u32x4<kAuxNT>(rw, (int)(kin ? woff[i] + kb : 0xFFFFFFF0u));
+  }
+}
+
+__device__ __forceinline__ void skinny_mma(f32x4_t (&acc)[4][4], const SkinnyFrags &f) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(f.a[i], f.b[j], acc[i][j]);
+}
 
 __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict__ A, const uint16_t *__restrict__ W,
                                                      uint16_t *__restrict__ out, const uint16_t *__restrict__ res,
                                                      float *__restrict__ part, int M, int N, int K, int epi,
                                                      int ksteps_per_split) {
   __shared__ float red[SK_BM][SK_BN + 4];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n0 = blockIdx.x * SK_BN;
   const int split = blockIdx.y;
   const int m0 = blockIdx.z * SK_BM;
@@ -58,55 +86,56 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
   const int ks_begin = split * ksteps_per_split;
   const int ks_end = min(nsteps, ks_begin + ksteps_per_split);
   const int lr = lane & 15, lk = (lane >> 4) * 8;
+  const int wrows = epi == EPI_SILU_MUL ? N : N;  // rows of W
 
-  // operand row pointers (nullptr = zero row)
-  const uint16_t *arow[4];
-  const uint16_t *wrow[4];
+  // byte offsets of this lane's operand rows (0xFFFFFFF0 = none)
+  uint32_t aoff[4], woff[4];
 #pragma unroll
   for (int b = 0; b < 4; ++b) {
     const int m = m0 + b * 16 + lr;
-    arow[b] = m < M ? A + (size_t)m * K : nullptr;
+    aoff[b] = m < M ? (uint32_t)m * (uint32_t)K * 2u : 0xFFFFFFF0u;
     const int wr = w_row_of(n0 + b * 16 + lr, N, epi);
-    wrow[b] = wr >= 0 ? W + (size_t)wr * K : nullptr;
+    woff[b] = wr >= 0 ? (uint32_t)wr * (uint32_t)K * 2u : 0xFFFFFFF0u;
   }
+  const buf_rsrc_t ra = make_rsrc(A, (int)min((size_t)M * K * 2, (size_t)0x7FFFFFFF));
+  const buf_rsrc_t rw = make_rsrc(W, (int)min((size_t)wrows * K * 2, (size_t)0x7FFFFFFF));
   f32x4_t acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  auto load = [&](int ks, u32x4_t *a, u32x4_t *b) {
-    const int k = ks * 32 + lk;
-    const bool kin = (ks < ks_end) && (k < K);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      a[i] = (kin && arow[i]) ? ld_u32x4(arow[i] + k) : u32x4_t{0, 0, 0, 0};
-      b[i] = (kin && wrow[i]) ? ld_stream_u32x4(wrow[i] + k) : u32x4_t{0, 0, 0, 0};
-    }
-  };
-  // wave w takes k-steps ks_begin + w, + 4, ...; SK_UNROLL of them per trip,
-  // with the next trip's operands loaded before this trip's MFMAs
-  u32x4_t ca[SK_UNROLL][4], cb[SK_UNROLL][4], na[SK_UNROLL][4], nb[SK_UNROLL][4];
-  int ks = ks_begin + wave;
-#pragma unroll
-  for (int u = 0; u < SK_UNROLL; ++u) load(ks + 4 * u, ca[u], cb[u]);
-  for (; ks < ks_end; ks += 4 * SK_UNROLL) {
-    const int nks = ks + 4 * SK_UNROLL;
-#pragma unroll
-    for (int u = 0; u < SK_UNROLL; ++u) load(nks + 4 * u, na[u], nb[u]);
-#pragma unroll
-    for (int u = 0; u < SK_UNROLL; ++u)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(ca[u][i], cb[u][j], acc[i][j]);
-#pragma unroll
-    for (int u = 0; u < SK_UNROLL; ++u)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        ca[u][i] = na[u][i];
-        cb[u][i] = nb[u][i];
-      }
+  // wave w takes k-steps ks_begin + w, + 4, ...; four k-steps of fragments
+  // in flight, rotated in straight-line code (scheduling barriers keep each
+  // load group and each MFMA group in program order, so the wait before an
+  // MFMA group covers only its own fragments)
+  SkinnyFrags f0, f1, f2, f3;
+  const int ks0 = ks_begin + wave;
+  skinny_load(f0, ra, rw, aoff, woff, ks0, ks_end, lk, K);
+  __builtin_amdgcn_sched_barrier(0);
+  skinny_load(f1, ra, rw, aoff, woff, ks0 + 4, ks_end, lk, K);
+  __builtin_amdgcn_sched_barrier(0);
+  skinny_load(f2, ra, rw, aoff, woff, ks0 + 8, ks_end, lk, K);
+  __builtin_amdgcn_sched_barrier(0);
+  skinny_load(f3, ra, rw, aoff, woff, ks0 + 12, ks_end, lk, K);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int ks = ks0; ks < ks_end; ks += 16) {
+    skinny_mma(acc, f0);
+    __builtin_amdgcn_sched_barrier(0);
+    skinny_load(f0, ra, rw, aoff, woff, ks + 16, ks_end, lk, K);
+    __builtin_amdgcn_sched_barrier(0);
+    skinny_mma(acc, f1);
+    __builtin_amdgcn_sched_barrier(0);
+    skinny_load(f1, ra, rw, aoff, woff, ks + 20, ks_end, lk, K);
+    __builtin_amdgcn_sched_barrier(0);
+    skinny_mma(acc, f2);
+    __builtin_amdgcn_sched_barrier(0);
+    skinny_load(f2, ra, rw, aoff, woff, ks + 24, ks_end, lk, K);
+    __builtin_amdgcn_sched_barrier(0);
+    skinny_mma(acc, f3);
+    __builtin_amdgcn_sched_barrier(0);
+    skinny_load(f3, ra, rw, aoff, woff, ks + 28, ks_end, lk, K);
+    __builtin_amdgcn_sched_barrier(0);
   }
   // reduce the 4 waves' accumulators in LDS, in wave order (deterministic)
   for (int w = 0; w < 4; ++w) {
@@ -315,8 +344,9 @@ static int skinny_splits(int M, int N, int K) {
   const int mt = (M + SK_BM - 1) / SK_BM;
   const int nsteps = (K + 31) / 32;
   int splits = 1;
-  // aim for >= 768 blocks (3 per CU) without going below 8 k-steps per wave
-  while (ncol_tiles * mt * splits < 768 && nsteps / (splits * 2) >= 4 * 8) splits *= 2;
+  // aim for about 2 blocks per CU (512) without going below 16 k-steps per
+  // wave (the 4-deep operand ring needs a few trips to pay off)
+  while (ncol_tiles * mt * splits * 2 <= 512 && nsteps / (splits * 2) >= 4 * 16) splits *= 2;
   return splits;
 }
 
