@@ -224,7 +224,7 @@ def main():
         g_ms = stages["gate_up_gemm"]
         fl = 2 * wk["T"] * 2 * shape.ffn * shape.hidden
         achieved = fl / (g_ms / 1e3) / 1e12
-        roof = {"kernel": "k_gemm_tiled (gate/up projection + SiLU*mul)", "bound": "mfma",
+        roof = {"kernel": "k_gemm_big (gate/up projection + SiLU*mul, 256x256 tiles)", "bound": "mfma",
                 "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "avg_launch_ms": round(g_ms, 5),
                 "flops_per_launch": fl, "traffic": None}

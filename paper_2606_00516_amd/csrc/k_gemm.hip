@@ -337,6 +337,158 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const uint16_t *__restrict__
 }
 
 // ===========================================================================
+// big: 256 x 256 output tiles for large M (prefill-sized batches).  K tiles
+// of 64 stream into a double-buffered LDS ring straight from global memory
+// (buffer loads with an LDS destination: no register round trip).  8 waves
+// (2 along M x 4 along N) each own a 128 x 64 sub-tile held in accumulation
+// registers.  The product is formed transposed, C^T = W A^T, so that each
+// lane's accumulators hold 4 consecutive output columns of one row and the
+// epilogue stores 8 bytes at a time.  LDS rows are 128 bytes (64 bf16 of
+// K); the 16-byte chunk c of row r sits at chunk c ^ ((r >> 1) & 7), which
+// makes the MFMA operand reads of 16 consecutive rows conflict free.
+// Requires K % 64 == 0, N % 8 == 0 and both operands under 2 GiB (32-bit
+// offsets).
+// ===========================================================================
+constexpr int BG_BM = 256, BG_BN = 256, BG_BK = 64;
+constexpr int BG_THREADS = 512;
+constexpr int BG_TILE_BYTES = 256 * BG_BK * 2;  // one operand tile: 32 KiB
+
+__device__ __forceinline__ int bg_swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+
+__global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restrict__ A,
+                                                         const uint16_t *__restrict__ W, uint16_t *__restrict__ out,
+                                                         const uint16_t *__restrict__ res, int M, int N, int K,
+                                                         int epi, int tiles_m, int tiles_n, int per_xcd) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t bg_lds[];  // [2][A tile | W tile]
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave >> 2, wn = wave & 3;  // 128 rows of M, 64 columns of N
+  // XCD-aware tile order: blocks are dealt round-robin to the 8 XCDs, so
+  // block b works on tile (b % 8) * per_xcd + b / 8: each XCD walks its own
+  // contiguous run of the (grouped) tile order and its L2 keeps the shared
+  // A and W panels.
+  const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (t >= tiles_m * tiles_n) return;
+  const int group = 8;
+  const int per_group = group * tiles_m;
+  const int gidx = t / per_group;
+  const int first_n = gidx * group;
+  const int gsz = min(group, tiles_n - first_n);
+  const int inb = t - gidx * per_group;
+  const int tn = first_n + inb % gsz;
+  const int tm = inb / gsz;
+  const int m0 = tm * BG_BM, n0 = tn * BG_BN;
+  const int nk = K / BG_BK;
+
+  const buf_rsrc_t ra = make_rsrc(A, (int)min((size_t)M * K * 2, (size_t)0x7FFFFFFF));
+  const buf_rsrc_t rw = make_rsrc(W, (int)min((size_t)N * K * 2, (size_t)0x7FFFFFFF));
+  // DMA: wave w moves LDS rows [32 w, 32 w + 32) of both tiles, 8 rows
+  // (1 KiB) per instruction; lane l fills row 8 i + l / 8, physical chunk
+  // l % 8 with logical chunk bg_swz(row, l % 8).  Rows outside the operands
+  // point 2 GiB in, past every descriptor's range, so they load zeros.
+  uint32_t aoff[4], woff[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = wave * 32 + i * 8 + (lane >> 3);
+    const int c = bg_swz(row, lane & 7);
+    const int m = m0 + row;
+    aoff[i] = m < M ? ((uint32_t)m * (uint32_t)K + (uint32_t)(c * 8)) * 2u : 0x80000000u;
+    const int wr = w_row_of(n0 + row, N, epi);
+    woff[i] = wr >= 0 ? ((uint32_t)wr * (uint32_t)K + (uint32_t)(c * 8)) * 2u : 0x80000000u;
+  }
+  typedef __attribute__((address_space(3))) void lds_void;
+  auto dma = [&](int kt, int buf) {
+    uint8_t *base = bg_lds + buf * 2 * BG_TILE_BYTES + wave * 32 * 128;
+    const uint32_t kb = (uint32_t)kt * BG_BK * 2u;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(base + i * 1024), 16, aoff[i] + kb, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void *)(base + BG_TILE_BYTES + i * 1024), 16, woff[i] + kb,
+                                               0, 0, 0);
+    }
+  };
+
+  f32x4_t acc[4][8];  // [W block jn][A block im]: rows n, cols m
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int lr = lane & 15, lg = lane >> 4;
+  dma(0, 0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) dma(kt + 1, buf ^ 1);
+    const uint8_t *sa = bg_lds + buf * 2 * BG_TILE_BYTES;
+    const uint8_t *sw = sa + BG_TILE_BYTES;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      u32x4_t af[8], wf[4];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int r = wm * 128 + i * 16 + lr;
+        af[i] = *reinterpret_cast<const u32x4_t *>(sa + r * 128 + bg_swz(r, ks * 4 + lg) * 16);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = wn * 64 + j * 16 + lr;
+        wf[j] = *reinterpret_cast<const u32x4_t *>(sw + r * 128 + bg_swz(r, ks * 4 + lg) * 16);
+      }
+#pragma unroll
+      for (int jn = 0; jn < 4; ++jn)
+#pragma unroll
+        for (int im = 0; im < 8; ++im) acc[jn][im] = mfma16x16x32(wf[jn], af[im], acc[jn][im]);
+    }
+    __syncthreads();
+  }
+
+  // epilogue: lane holds out[m][n .. n+3] with m = m0 + wm*128 + 16 im + lr,
+  // n = n0 + wn*64 + 16 jn + 4 lg (N and F are multiples of 4, so a group of
+  // 4 columns is either wholly inside or wholly outside)
+  if (epi == EPI_SILU_MUL) {
+    // the wave's 64 columns are one [32 gate | 32 up] group: blocks jn and
+    // jn + 2 pair up
+    const int F = N >> 1;
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj) {
+      const int f = ((n0 + wn * 64) >> 1) + jj * 16 + lg * 4;
+#pragma unroll
+      for (int im = 0; im < 8; ++im) {
+        const int m = m0 + wm * 128 + im * 16 + lr;
+        if (m < M && f < F) {
+          const f32x4_t gv = acc[jj][im], uv = acc[jj + 2][im];
+          u32x2_t w = {pack_bf16x2(silu_f(gv[0]) * uv[0], silu_f(gv[1]) * uv[1]),
+                       pack_bf16x2(silu_f(gv[2]) * uv[2], silu_f(gv[3]) * uv[3])};
+          *reinterpret_cast<u32x2_t *>(out + (size_t)m * F + f) = w;
+        }
+      }
+    }
+    return;
+  }
+#pragma unroll
+  for (int jn = 0; jn < 4; ++jn) {
+    const int n = n0 + wn * 64 + jn * 16 + lg * 4;
+#pragma unroll
+    for (int im = 0; im < 8; ++im) {
+      const int m = m0 + wm * 128 + im * 16 + lr;
+      if (m < M && n < N) {
+        f32x4_t v = acc[jn][im];
+        if (epi == EPI_RESIDUAL) {
+          const u32x2_t r = *reinterpret_cast<const u32x2_t *>(res + (size_t)m * N + n);
+          v[0] += bf16_lo(r[0]);
+          v[1] += bf16_hi(r[0]);
+          v[2] += bf16_lo(r[1]);
+          v[3] += bf16_hi(r[1]);
+        }
+        u32x2_t w = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        *reinterpret_cast<u32x2_t *>(out + (size_t)m * N + n) = w;
+      }
+    }
+  }
+}
+
+// ===========================================================================
 // planning and launch
 // ===========================================================================
 static int skinny_splits(int M, int N, int K) {
@@ -358,7 +510,11 @@ GemmPlan plan_gemm(int M, int N, int K, int epi) {
     p.splits = skinny_splits(M, ncols, K);
     p.ws_bytes = p.splits > 1 ? (size_t)p.splits * M * ncols * sizeof(float) : 0;
   } else {
-    p.kind = 1;
+    const int ncols = logical_cols(N, epi);
+    const bool fits = (size_t)M * K * 2 < ((size_t)1 << 31) && (size_t)N * K * 2 < ((size_t)1 << 31);
+    // 256 x 256 tiles once the grid covers at least half the CUs
+    const long big_tiles = (long)((M + BG_BM - 1) / BG_BM) * ((ncols + BG_BN - 1) / BG_BN);
+    p.kind = (K % BG_BK == 0 && N % 8 == 0 && fits && M >= 256 && big_tiles >= 128) ? 2 : 1;
     p.splits = 1;
     p.ws_bytes = 0;
   }
@@ -382,6 +538,13 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, 
     const long total = (long)M * outc;
     const int blocks = (int)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
     hipLaunchKernelGGL(k_gemm_splitk_epilogue, dim3(blocks), dim3(256), 0, st, part, splits, out, res, M, N, epi);
+    return hipGetLastError();
+  }
+  if (p.kind == 2) {
+    const int tm = (M + BG_BM - 1) / BG_BM, tn = (ncols + BG_BN - 1) / BG_BN;
+    const int per_xcd = (tm * tn + 7) / 8;
+    hipLaunchKernelGGL(k_gemm_big, dim3(8 * per_xcd), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A, W, out, res, M, N, K, epi,
+                       tm, tn, per_xcd);
     return hipGetLastError();
   }
   const int tiles_m = (M + TL_BM - 1) / TL_BM, tiles_n = (ncols + TL_BN - 1) / TL_BN;

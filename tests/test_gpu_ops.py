@@ -25,7 +25,9 @@ def _bf(shape, seed, scale=1.0):
 # ---------------------------------------------------------------- GEMM
 
 @pytest.mark.parametrize("M,N,K", [(1, 256, 256), (4, 512, 256), (64, 1376, 256), (37, 256, 688), (64, 6144, 4096),
-                                   (130, 512, 256), (256, 688, 264), (512, 1024, 512), (300, 1376, 256)])
+                                   (130, 512, 256), (256, 688, 264), (512, 1024, 512), (300, 1376, 256),
+                                   # 256 x 256 LDS-streamed tiles: aligned, and ragged in M, N and F
+                                   (1024, 8192, 1024), (1000, 8200, 512), (2048, 6144, 4096)])
 @pytest.mark.parametrize("epi", ["store", "residual", "silu_mul"])
 def test_gemm(M, N, K, epi):
     A = _bf((M, K), 1)
