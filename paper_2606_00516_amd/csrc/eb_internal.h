@@ -14,7 +14,7 @@ constexpr int kPageSize = 16;
 
 // Prefill attention tiles: query positions per tile for a GQA group size
 // (must agree with PrefillTraits in the attention kernels).
-inline int prefill_bq(int group) { return group >= 8 ? 16 : (group == 1 ? 64 : 32); }
+inline int prefill_bq(int group) { return 128 / group; }
 
 // Per-step metadata in device memory (all int32), produced by the planner.
 struct DevMeta {

@@ -9,7 +9,7 @@ namespace {
 constexpr int kPagesPerSplit = 32;  // must match kDecodePagesPerSplit
 constexpr int kPage = 16;
 
-int prefill_bq_host(int group) { return group >= 8 ? 16 : (group == 1 ? 64 : 32); }
+int prefill_bq_host(int group) { return 128 / group; }  // must match the prefill kernel
 }  // namespace
 
 int32_t decode_splits(int32_t c) {

@@ -16,20 +16,21 @@ namespace eb {
 constexpr float kNegInf = -__builtin_inff();
 
 // ===========================================================================
-// Decode: one work item = (decode request, split of 32 pages, kv head), 4
-// wavefronts.  Wave w streams pages w, w+4, ... of the split.  Lane layout
+// Decode: one work item = (decode request, split of 32 pages, kv head), NW
+// wavefronts (4 alone, 8 inside the mixed launch).  Wave w streams pages w,
+// w+NW, ... of the split.  Lane layout
 // over a 16 x HD page block: each 16-byte load instruction covers 1 KiB, lane
 // l holding 8 dims of one token; LPT = HD/8 lanes share a token.  Scores are
 // reduced over those lanes with DPP; each lane keeps its own running
 // (max, sum, output) over the tokens it sees, and the partial states are
 // merged at the end (shuffles within the wave, LDS across waves).
 // ===========================================================================
-template <int HD, int G>
+template <int HD, int G, int NW>
 struct DecodeTraits {
   static constexpr int LPT = HD / 8;   // lanes per token
   static constexpr int TG = 64 / LPT;  // tokens per load instruction
   static constexpr int NLD = HD / 32;  // load instructions per page block = tokens per lane per page
-  static constexpr int LDS_BYTES = 4 * G * (HD + 2) * 4;
+  static constexpr int LDS_BYTES = NW * G * (HD + 2) * 4;
 };
 
 // Merge running softmax state (m, l, o) with another one.
@@ -109,11 +110,11 @@ __device__ __forceinline__ void decode_page_update(const u32x4_t (&k)[HD / 32], 
   }
 }
 
-template <int HD, int G>
+template <int HD, int G, int NW>
 __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
                                             const DevMeta md, int item, int kh, uint16_t *__restrict__ out,
                                             float *__restrict__ part_o, float *__restrict__ part_ml, float *lds) {
-  using Tr = DecodeTraits<HD, G>;
+  using Tr = DecodeTraits<HD, G, NW>;
   constexpr int LPT = Tr::LPT, NLD = Tr::NLD;
   constexpr int SPLIT = kDecodePagesPerSplit * kPageSize;
   const int lane = threadIdx.x & 63;
@@ -155,7 +156,7 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
     for (int i = 0; i < 8; ++i) o[h][i] = 0.f;
   }
 
-  // Wave w streams pages w, w+4, ... through a ring of page buffers (three
+  // Wave w streams pages w, w+NW, ... through a ring of page buffers (three
   // for G <= 2, two for larger groups, whose accumulators need the
   // registers), rotated in straight-line code; pages past the split's end
   // load as zeros without memory traffic and are masked out.
@@ -170,25 +171,25 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
   decode_page_update<HD, G>(K_, V_, qw, mrun, lrun, o, P_, k1, lane, qscale); \
   __builtin_amdgcn_sched_barrier(0);
   EB_LOAD(ka, va, pfirst)
-  EB_LOAD(kb, vb, pfirst + 4)
+  EB_LOAD(kb, vb, pfirst + NW)
   if constexpr (G <= 2) {
-    EB_LOAD(kc, vc, pfirst + 8)
-    for (int p = pfirst; p < pg1; p += 12) {
+    EB_LOAD(kc, vc, pfirst + 2 * NW)
+    for (int p = pfirst; p < pg1; p += 3 * NW) {
       EB_UPDATE(ka, va, p)
-      EB_LOAD(ka, va, p + 12)
-      EB_UPDATE(kb, vb, p + 4)
-      EB_LOAD(kb, vb, p + 16)
-      EB_UPDATE(kc, vc, p + 8)
-      EB_LOAD(kc, vc, p + 20)
+      EB_LOAD(ka, va, p + 3 * NW)
+      EB_UPDATE(kb, vb, p + NW)
+      EB_LOAD(kb, vb, p + 4 * NW)
+      EB_UPDATE(kc, vc, p + 2 * NW)
+      EB_LOAD(kc, vc, p + 5 * NW)
     }
   } else {
     (void)kc;
     (void)vc;
-    for (int p = pfirst; p < pg1; p += 8) {
+    for (int p = pfirst; p < pg1; p += 2 * NW) {
       EB_UPDATE(ka, va, p)
-      EB_LOAD(ka, va, p + 8)
-      EB_UPDATE(kb, vb, p + 4)
-      EB_LOAD(kb, vb, p + 12)
+      EB_LOAD(ka, va, p + 2 * NW)
+      EB_UPDATE(kb, vb, p + NW)
+      EB_LOAD(kb, vb, p + 3 * NW)
     }
   }
 #undef EB_LOAD
@@ -207,9 +208,9 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
       lse_merge<8>(mrun[h], lrun[h], o[h], m2, l2, o2);
     }
   }
-  // across the 4 waves through LDS: [wave][h][HD] outputs, then [wave][h][2]
+  // across the NW waves through LDS: [wave][h][HD] outputs, then [wave][h][2]
   float *lo_ = lds;
-  float *lml = lds + 4 * G * HD;
+  float *lml = lds + NW * G * HD;
   if (lane < LPT) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
@@ -226,10 +227,10 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
     const int h = e / HD, dim = e - h * HD;
     float mx = kNegInf;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) mx = fmaxf(mx, lml[(w * G + h) * 2]);
+    for (int w = 0; w < NW; ++w) mx = fmaxf(mx, lml[(w * G + h) * 2]);
     float L = 0.f, O = 0.f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < NW; ++w) {
       const float mw = lml[(w * G + h) * 2];
       const float a = (mw == kNegInf) ? 0.f : fast_exp2(mw - mx);
       L += a * lml[(w * G + h) * 2 + 1];
@@ -286,23 +287,27 @@ __global__ __launch_bounds__(64) void k_decode_combine(DevMeta md, const float *
 
 // ===========================================================================
 // Prefill: one work item = (request, block of BQ query positions, kv head):
-// G heads x BQ positions = 16-row blocks shared out over 4 wavefronts.  Keys
-// and values stream through LDS in tiles of 64 positions gathered from 4
-// pages.  Scores are formed transposed, S^T = K Q^T, with the 16x16x32 bf16
-// MFMA, so a lane holds one query column and the row max needs only two
-// cross-lane steps; P^T stays in registers as the B operand of O^T = V^T P^T
-// (keys permuted consistently on both operands), with V^T staged in LDS.
+// G heads x BQ positions = 128 query rows, one 16-row block per wavefront
+// (8 wavefronts).  Keys and values stream through LDS in tiles of 64
+// positions gathered from 4 pages; the next tile's global loads are issued
+// before the current tile is consumed.  Scores are formed transposed,
+// S^T = K Q^T, with the 16x16x32 bf16 MFMA, so a lane holds one query column
+// and the row max needs only two cross-lane steps; P^T stays in registers as
+// the B operand of O^T = V^T P^T (keys permuted consistently on both
+// operands), with V^T staged in LDS.
 // ===========================================================================
 template <int HD, int G>
 struct PrefillTraits {
-  static constexpr int BQ = (G >= 8) ? 16 : ((G == 1) ? 64 : 32);
-  static constexpr int RB_TOTAL = G * BQ / 16;  // 16-row blocks per item
-  static constexpr int RB = RB_TOTAL / 4;       // per wavefront
+  static constexpr int NW = 8;                  // wavefronts per item
+  static constexpr int BQ = 128 / G;            // query positions per item
   static constexpr int KT = 64;                 // keys per tile
   static constexpr int KS_STRIDE = HD + 8;      // bf16 elements per K row in LDS
   static constexpr int VT_STRIDE = KT + 4;      // bf16 elements per V^T row in LDS
   static constexpr int LDS_BYTES = (KT * KS_STRIDE + HD * VT_STRIDE) * 2;
-  static_assert(RB_TOTAL % 4 == 0 && RB >= 1, "row blocks");
+  static constexpr int KCH = KT * (HD / 8);     // 16-byte K chunks per tile
+  static constexpr int VCH = (KT / 2) * (HD / 8);  // (key pair, 8 dims) V units per tile
+  static constexpr int KPT = (KCH + NW * 64 - 1) / (NW * 64);  // per thread
+  static constexpr int VPT = (VCH + NW * 64 - 1) / (NW * 64);
 };
 
 template <int HD, int G>
@@ -310,11 +315,14 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
                                              const DevMeta md, int tile, int kh, uint16_t *__restrict__ out,
                                              uint16_t *lds) {
   using Tr = PrefillTraits<HD, G>;
-  constexpr int BQ = Tr::BQ, RB = Tr::RB, KT = Tr::KT, KSS = Tr::KS_STRIDE, VTS = Tr::VT_STRIDE;
+  constexpr int NW = Tr::NW, BQ = Tr::BQ, KT = Tr::KT, KSS = Tr::KS_STRIDE, VTS = Tr::VT_STRIDE;
+  constexpr int KCH = Tr::KCH, VCH = Tr::VCH, KPT = Tr::KPT, VPT = Tr::VPT;
   constexpr int NKS = HD / 32;  // k-steps of the QK^T product
   constexpr int NOB = HD / 16;  // 16-dim output blocks
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  constexpr int NT = NW * 64;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int cols = (nq + 2 * nkv) * HD;
   const int seq = md.tile_seq[tile];
   const int qb = md.tile_qb[tile];
@@ -324,159 +332,162 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
   const int q_lo = qb * BQ;                 // first query (chunk-relative)
   const int q_hi = min(n, q_lo + BQ);       // one past the last
   const int kend = c + q_hi;                // keys needed: 0 .. kend-1
+  const int klen = c + n;                   // keys that exist
   const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
-  const int npages = (c + n + kPageSize - 1) / kPageSize;
+  const int npages = (klen + kPageSize - 1) / kPageSize;
   uint16_t *Ks = lds;
   uint16_t *Vt = lds + KT * KSS;
   const float qscale = kLog2e / sqrtf((float)HD);
-  const int lq = lane & 15;   // query column of this lane inside a 16-row block
+  const int lq = lane & 15;   // query column of this lane inside the 16-row block
   const int lg = lane >> 4;   // lane group 0..3
 
-  // row blocks of this wave: rb = wave + 4 i -> (head, 16-query sub-block)
-  u32x4_t qreg[RB][NKS];
-  int qpos[RB];
-  bool qok[RB];
-#pragma unroll
-  for (int i = 0; i < RB; ++i) {
-    const int rb = wave + 4 * i;
-    const int h = rb % G, sub = rb / G;
-    const int qrel = q_lo + sub * 16 + lq;
-    qok[i] = qrel < q_hi;
-    qpos[i] = c + qrel;
+  // this wave's row block: head h, 16 query positions sub*16 ..
+  const int h = wave % G, sub = wave / G;
+  const int qrel = q_lo + sub * 16 + lq;
+  const bool qok = qrel < q_hi;
+  const int qpos = c + qrel;
+  u32x4_t qreg[NKS];
+  {
     const uint16_t *src = qkv + (size_t)(row0 + qrel) * cols + (kh * G + h) * HD + lg * 8;
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) qreg[i][ks] = qok[i] ? ld_u32x4(src + ks * 32) : u32x4_t{0, 0, 0, 0};
+    for (int ks = 0; ks < NKS; ++ks) qreg[ks] = qok ? ld_u32x4(src + ks * 32) : u32x4_t{0, 0, 0, 0};
   }
-  f32x4_t oacc[RB][NOB];
-  float mrun[RB], lrun[RB];
+  f32x4_t oacc[NOB];
 #pragma unroll
-  for (int i = 0; i < RB; ++i) {
-    mrun[i] = kNegInf;
-    lrun[i] = 0.f;
-#pragma unroll
-    for (int ob = 0; ob < NOB; ++ob) oacc[i][ob] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  }
-  const int min_qpos = c + q_lo;
-  const int ntiles = (kend + KT - 1) / KT;
-  for (int t = 0; t < ntiles; ++t) {
+  for (int ob = 0; ob < NOB; ++ob) oacc[ob] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float mrun = kNegInf, lrun = 0.f;
+
+  // global -> register staging of one K/V tile (keys past c + n read as 0)
+  u32x4_t kreg[KPT], vreg[VPT][2];
+  auto cache_addr = [&](int kp) -> long {
+    if (kp >= klen) return -1;
+    const int pg = kp / kPageSize;
+    const int phys = pg < npages ? bt[pg] : -1;
+    if (phys < 0 || phys >= kv.num_pages) return -1;
+    return (((long)phys * nkv + kh) * kPageSize + kp % kPageSize) * HD;
+  };
+  auto fetch = [&](int t) {
     const int k0 = t * KT;
-    // ---- stage K (row-major) and V^T into LDS; keys >= c + n are zero ----
-    for (int u = threadIdx.x; u < KT * (HD / 8); u += 256) {
-      const int key = u / (HD / 8), dc = u - key * (HD / 8);
-      const int kp = k0 + key;
-      u32x4_t w = {0, 0, 0, 0};
-      if (kp < c + n) {
-        const int pg = kp / kPageSize;
-        const int phys = pg < npages ? bt[pg] : -1;
-        if (phys >= 0 && phys < kv.num_pages)
-          w = ld_u32x4(kv.k + (((size_t)phys * nkv + kh) * kPageSize + kp % kPageSize) * HD + dc * 8);
-      }
-      st_u32x4(Ks + key * KSS + dc * 8, w);
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int u = tid + i * NT;
+      const int key = u / (HD / 8), dc = u % (HD / 8);
+      const long a = u < KCH ? cache_addr(k0 + key) : -1;
+      kreg[i] = a >= 0 ? ld_u32x4(kv.k + a + dc * 8) : u32x4_t{0, 0, 0, 0};
     }
-    for (int u = threadIdx.x; u < (KT / 2) * (HD / 8); u += 256) {
-      const int kpair = u / (HD / 8), dc = u - kpair * (HD / 8);
-      u32x4_t w[2];
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int u = tid + i * NT;
+      const int kpair = u / (HD / 8), dc = u % (HD / 8);
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const int kp = k0 + 2 * kpair + e;
-        w[e] = u32x4_t{0, 0, 0, 0};
-        if (kp < c + n) {
-          const int pg = kp / kPageSize;
-          const int phys = pg < npages ? bt[pg] : -1;
-          if (phys >= 0 && phys < kv.num_pages)
-            w[e] = ld_u32x4(kv.v + (((size_t)phys * nkv + kh) * kPageSize + kp % kPageSize) * HD + dc * 8);
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint32_t lo0 = w[0][i] & 0xFFFFu, hi0 = w[0][i] >> 16;
-        const uint32_t lo1 = w[1][i] & 0xFFFFu, hi1 = w[1][i] >> 16;
-        *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * i) * VTS + 2 * kpair) = lo0 | (lo1 << 16);
-        *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * i + 1) * VTS + 2 * kpair) = hi0 | (hi1 << 16);
+        const long a = u < VCH ? cache_addr(k0 + 2 * kpair + e) : -1;
+        vreg[i][e] = a >= 0 ? ld_u32x4(kv.v + a + dc * 8) : u32x4_t{0, 0, 0, 0};
       }
     }
+  };
+  auto stage = [&]() {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int u = tid + i * NT;
+      if (u < KCH) st_u32x4(Ks + (u / (HD / 8)) * KSS + (u % (HD / 8)) * 8, kreg[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int u = tid + i * NT;
+      if (u < VCH) {
+        const int kpair = u / (HD / 8), dc = u % (HD / 8);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t a0 = vreg[i][0][j], a1 = vreg[i][1][j];
+          *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j) * VTS + 2 * kpair) = (a0 & 0xFFFFu) | (a1 << 16);
+          *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j + 1) * VTS + 2 * kpair) = (a0 >> 16) | (a1 & 0xFFFF0000u);
+        }
+      }
+    }
+  };
+
+  const int min_qpos = c + q_lo;
+  const int ntiles = (kend + KT - 1) / KT;
+  fetch(0);
+  for (int t = 0; t < ntiles; ++t) {
+    const int k0 = t * KT;
+    stage();
     __syncthreads();
-    const bool need_mask = (k0 + KT - 1) > min_qpos;
+    if (t + 1 < ntiles) fetch(t + 1);   // in flight while this tile is consumed
+    const bool need_mask = (k0 + KT - 1) > min_qpos || !qok;
+    // S^T block kb: keys k0 + 16 kb + 4 lg + j, query column lq
+    f32x4_t sc[4];
 #pragma unroll
-    for (int i = 0; i < RB; ++i) {
-      // S^T block kb: keys k0 + 16 kb + 4 lg + j, query column lq
-      f32x4_t s[4];
+    for (int kb = 0; kb < 4; ++kb) {
+      sc[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        s[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-          const u32x4_t a = ld_u32x4(Ks + (kb * 16 + lq) * KSS + ks * 32 + lg * 8);
-          s[kb] = mfma16x16x32(a, qreg[i][ks], s[kb]);
-        }
+      for (int ks = 0; ks < NKS; ++ks) {
+        const u32x4_t a = ld_u32x4(Ks + (kb * 16 + lq) * KSS + ks * 32 + lg * 8);
+        sc[kb] = mfma16x16x32(a, qreg[ks], sc[kb]);
       }
-      float mx = mrun[i];
+    }
+    float mx = mrun;
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+    for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          float v = s[kb][j] * qscale;
-          if (need_mask || !qok[i]) {
-            const int kp = k0 + kb * 16 + lg * 4 + j;
-            if (kp > qpos[i] || !qok[i]) v = kNegInf;
-          }
-          s[kb][j] = v;
-          mx = fmaxf(mx, v);
+      for (int j = 0; j < 4; ++j) {
+        float v = sc[kb][j] * qscale;
+        if (need_mask) {
+          const int kp = k0 + kb * 16 + lg * 4 + j;
+          if (kp > qpos || !qok) v = kNegInf;
         }
-      mx = fmaxf(mx, shfl_xor_f32(mx, 16));
-      mx = fmaxf(mx, shfl_xor_f32(mx, 32));
-      const float alpha = (mrun[i] == kNegInf) ? 0.f : fast_exp2(mrun[i] - mx);
-      const bool live = mx != kNegInf;
-      float l = lrun[i] * alpha;
-      uint32_t pk[4][2];
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        float p4[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          p4[j] = (live && s[kb][j] != kNegInf) ? fast_exp2(s[kb][j] - mx) : 0.f;
-          l += p4[j];
-        }
-        pk[kb][0] = pack_bf16x2(p4[0], p4[1]);
-        pk[kb][1] = pack_bf16x2(p4[2], p4[3]);
+        sc[kb][j] = v;
+        mx = fmaxf(mx, v);
       }
-      lrun[i] = l;
-      mrun[i] = mx;
+    mx = fmaxf(mx, shfl_xor_f32(mx, 16));
+    mx = fmaxf(mx, shfl_xor_f32(mx, 32));
+    const float alpha = (mrun == kNegInf) ? 0.f : fast_exp2(mrun - mx);
+    const bool live = mx != kNegInf;
+    float l = lrun * alpha;
+    uint32_t pk[4][2];
 #pragma unroll
-      for (int ob = 0; ob < NOB; ++ob) {
-        f32x4_t acc = oacc[i][ob] * alpha;
+    for (int kb = 0; kb < 4; ++kb) {
+      float p4[4];
 #pragma unroll
-        for (int ks2 = 0; ks2 < 2; ++ks2) {
-          // B (P^T): keys {4 lg .. +3} of block 2 ks2, then of block 2 ks2 + 1
-          const u32x4_t b = {pk[2 * ks2][0], pk[2 * ks2][1], pk[2 * ks2 + 1][0], pk[2 * ks2 + 1][1]};
-          // A (V^T): dim ob*16 + lq, the same keys
-          const uint16_t *vrow = Vt + (ob * 16 + lq) * VTS + ks2 * 32 + lg * 4;
-          const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vrow);
-          const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vrow + 16);
-          const u32x4_t a = {a0[0], a0[1], a1[0], a1[1]};
-          acc = mfma16x16x32(a, b, acc);
-        }
-        oacc[i][ob] = acc;
+      for (int j = 0; j < 4; ++j) {
+        p4[j] = (live && sc[kb][j] != kNegInf) ? fast_exp2(sc[kb][j] - mx) : 0.f;
+        l += p4[j];
       }
+      pk[kb][0] = pack_bf16x2(p4[0], p4[1]);
+      pk[kb][1] = pack_bf16x2(p4[2], p4[3]);
+    }
+    lrun = l;
+    mrun = mx;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) {
+      f32x4_t acc = oacc[ob] * alpha;
+#pragma unroll
+      for (int ks2 = 0; ks2 < 2; ++ks2) {
+        // B (P^T): keys {4 lg .. +3} of block 2 ks2, then of block 2 ks2 + 1
+        const u32x4_t b = {pk[2 * ks2][0], pk[2 * ks2][1], pk[2 * ks2 + 1][0], pk[2 * ks2 + 1][1]};
+        // A (V^T): dim ob*16 + lq, the same keys
+        const uint16_t *vrow = Vt + (ob * 16 + lq) * VTS + ks2 * 32 + lg * 4;
+        const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vrow);
+        const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vrow + 16);
+        const u32x4_t a = {a0[0], a0[1], a1[0], a1[1]};
+        acc = mfma16x16x32(a, b, acc);
+      }
+      oacc[ob] = acc;
     }
     __syncthreads();
   }
   // normalise and store: lane holds dims ob*16 + 4 lg + j of query lq
-#pragma unroll
-  for (int i = 0; i < RB; ++i) {
-    float l = lrun[i];
-    l += shfl_xor_f32(l, 16);
-    l += shfl_xor_f32(l, 32);
-    if (!qok[i]) continue;
-    const int rb = wave + 4 * i;
-    const int h = rb % G, sub = rb / G;
-    const int qrel = q_lo + sub * 16 + lq;
+  float l = lrun;
+  l += shfl_xor_f32(l, 16);
+  l += shfl_xor_f32(l, 32);
+  if (qok) {
     const float inv = 1.0f / l;
     uint16_t *dst = out + (size_t)(row0 + qrel) * nq * HD + (kh * G + h) * HD + lg * 4;
 #pragma unroll
     for (int ob = 0; ob < NOB; ++ob) {
-      u32x2_t w = {pack_bf16x2(oacc[i][ob][0] * inv, oacc[i][ob][1] * inv),
-                   pack_bf16x2(oacc[i][ob][2] * inv, oacc[i][ob][3] * inv)};
+      u32x2_t w = {pack_bf16x2(oacc[ob][0] * inv, oacc[ob][1] * inv),
+                   pack_bf16x2(oacc[ob][2] * inv, oacc[ob][3] * inv)};
       *reinterpret_cast<u32x2_t *>(dst + ob * 16) = w;
     }
   }
@@ -488,30 +499,31 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
 template <int HD, int G>
 __global__ __launch_bounds__(256) void k_decode(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
                                                 float *part_o, float *part_ml) {
-  __shared__ float lds[DecodeTraits<HD, G>::LDS_BYTES / 4];
-  decode_item<HD, G>(qkv, nq, nkv, kv, md, blockIdx.x, blockIdx.y, out, part_o, part_ml, lds);
+  __shared__ float lds[DecodeTraits<HD, G, 4>::LDS_BYTES / 4];
+  decode_item<HD, G, 4>(qkv, nq, nkv, kv, md, blockIdx.x, blockIdx.y, out, part_o, part_ml, lds);
 }
 
 template <int HD, int G>
-__global__ __launch_bounds__(256) void k_prefill(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
+__global__ __launch_bounds__(512) void k_prefill(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
                                                  uint16_t *out) {
   __shared__ __attribute__((aligned(16))) uint16_t lds[PrefillTraits<HD, G>::LDS_BYTES / 2];
   prefill_item<HD, G>(qkv, nq, nkv, kv, md, blockIdx.x, blockIdx.y, out, lds);
 }
 
 // One grid for a mixed step: items [0, n_tiles) are prefill tiles (longest
-// first), the rest decode splits; every block branches uniformly on its kind.
+// first), the rest decode splits; every block branches uniformly on its kind
+// (8 wavefronts for both kinds).
 template <int HD, int G>
-__global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
+__global__ __launch_bounds__(512) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
                                                float *part_o, float *part_ml) {
-  constexpr int PB = PrefillTraits<HD, G>::LDS_BYTES, DB = DecodeTraits<HD, G>::LDS_BYTES;
+  constexpr int PB = PrefillTraits<HD, G>::LDS_BYTES, DB = DecodeTraits<HD, G, 8>::LDS_BYTES;
   __shared__ __attribute__((aligned(16))) uint16_t lds[(PB > DB ? PB : DB) / 2];
   const int b = blockIdx.x;
   if (b < md.n_tiles)
     prefill_item<HD, G>(qkv, nq, nkv, kv, md, b, blockIdx.y, out, lds);
   else
-    decode_item<HD, G>(qkv, nq, nkv, kv, md, b - md.n_tiles, blockIdx.y, out, part_o, part_ml,
-                       reinterpret_cast<float *>(lds));
+    decode_item<HD, G, 8>(qkv, nq, nkv, kv, md, b - md.n_tiles, blockIdx.y, out, part_o, part_ml,
+                          reinterpret_cast<float *>(lds));
 }
 
 template <int HD, int G>
@@ -523,10 +535,10 @@ static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const 
   if (!(parts & 1)) {
     // combine only
   } else if (kind == 2 && has_dec && has_pf) {
-    hipLaunchKernelGGL((k_mixed<HD, G>), dim3(m.n_tiles + m.total_splits, nkv), dim3(256), 0, st, qkv, nq, nkv, kv, m,
+    hipLaunchKernelGGL((k_mixed<HD, G>), dim3(m.n_tiles + m.total_splits, nkv), dim3(512), 0, st, qkv, nq, nkv, kv, m,
                        out, part_o, part_ml);
   } else {
-    if (has_pf) hipLaunchKernelGGL((k_prefill<HD, G>), dim3(m.n_tiles, nkv), dim3(256), 0, st, qkv, nq, nkv, kv, m, out);
+    if (has_pf) hipLaunchKernelGGL((k_prefill<HD, G>), dim3(m.n_tiles, nkv), dim3(512), 0, st, qkv, nq, nkv, kv, m, out);
     if (has_dec)
       hipLaunchKernelGGL((k_decode<HD, G>), dim3(m.total_splits, nkv), dim3(256), 0, st, qkv, nq, nkv, kv, m, out,
                          part_o, part_ml);
