@@ -10,8 +10,10 @@ with every input resident in HBM before the timed region.
 
 Prints one JSON line.  Other workloads: --workload prefill8b (8 prompts,
 lengths 256..2048 capped at 8192 tokens), mixed8b --r R (2048-token step at
-decode share R), copy (a plain device copy of known size, used to calibrate
-the HBM byte counters).
+decode share R), sweep8b (the mixed step at decode shares 0, 0.1, ..., 1 and
+several token budgets, with the exclusive endpoints, K(r), kappa, the
+per-share linear fits and the crossover share), copy (a plain device copy of
+known size, used to calibrate the HBM byte counters).
 """
 from __future__ import annotations
 
@@ -42,7 +44,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="decode8b", choices=["decode8b", "prefill8b", "mixed8b", "copy"])
+    ap.add_argument("--workload", default="decode8b", choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "copy"])
+    ap.add_argument("--budgets", default="1024,2048", help="token budgets of the sweep (for alpha/beta fits)")
+    ap.add_argument("--ctx16", action="store_true", help="sweep with every decode context = 16 instead")
     ap.add_argument("--r", type=float, default=0.5, help="decode share for mixed8b")
     ap.add_argument("--budget", type=int, default=2048, help="token budget for mixed8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -138,6 +142,107 @@ def cpu_baseline(shape, batch, w, pool, x, mode, target_s):
 
 
 # ----------------------------------------------------------------------------
+# timing
+# ----------------------------------------------------------------------------
+
+def measure(B, h, step_fn, w, pool, batch, x, y, ws, steps, warmup, profile_steps=None):
+    """(ms per step over ``steps`` back-to-back steps, mean per-stage ms over a
+    second pass with the library's stage events)."""
+    import torch
+    call = lambda: step_fn(h, w, pool.k_cache, pool.v_cache, pool.block_tables, batch.context_lens,  # noqa: E731
+                           batch.chunk_lens, x, y=y, ws=ws)
+    for _ in range(warmup):
+        call()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        call()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / steps * 1e3
+    ps = steps if profile_steps is None else profile_steps
+    B.eb_profile(h, True)
+    acc = {}
+    for _ in range(ps):
+        call()
+        for k, v in B.eb_profile_read(h).items():
+            acc[k] = acc.get(k, 0.0) + v
+    B.eb_profile(h, False)
+    torch.cuda.synchronize()
+    return ms, {k: v / ps for k, v in acc.items()}
+
+
+def sweep(args, dev):
+    """Mixed 8B step over decode shares 0, 0.1, .., 1 at several budgets."""
+    import numpy as np
+    import torch
+
+    from paper_2606_00516_amd import analysis as AN
+    from paper_2606_00516_amd import binding as B
+    from paper_2606_00516_amd import inputs as gen
+    shape = gen.L8B
+    w = gen.make_weights(shape, device=dev)
+    budgets = [int(b) for b in args.budgets.split(",")]
+    rs = [round(0.1 * i, 1) for i in range(11)]
+    dec_ctx = (16, 16) if args.ctx16 else (1024, 8192)
+    pts = []
+
+    def run(batch, mode):
+        pool = gen.make_kv_pool(shape, batch, device=dev, poison=False)
+        x = gen.make_x(shape, batch.num_tokens, device=dev)
+        y = torch.empty_like(x)
+        h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
+        ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
+        fn = {"decode": B.eb_layer_step_decode, "prefill": B.eb_layer_step_prefill,
+              "mixed": B.eb_layer_step_mixed}[mode]
+        ms, st = measure(B, h, fn, w, pool, batch, x, y, ws, args.steps, args.warmup, max(3, args.steps // 2))
+        del pool, x, y, ws, h
+        torch.cuda.empty_cache()
+        gemm = sum(v for k, v in st.items() if k.endswith("gemm"))
+        attn = st.get("attention", 0.0) + st.get("attention_combine", 0.0)
+        wk = step_work(shape, batch)
+        return {"ms": ms, "gemm_ms": gemm, "attention_ms": attn, "other_ms": sum(st.values()) - gemm - attn,
+                "kv_bytes_decode": wk["kv_bytes_decode"], "n_tok": wk["T"], "n_decode": batch.num_decode}
+
+    for bud in budgets:
+        for r in rs:
+            s0 = gen.seeds()["batch"]
+            rng = np.random.default_rng([s0, int(round(r * 1000)), bud])
+            batch = gen.batch_mixed_budget(r, bud, rng, dec_ctx=dec_ctx)
+            p = run(batch, "mixed")
+            p.update(r=r, budget=bud, mode="mixed")
+            pts.append(p)
+            print(f"# B={bud} r={r:.1f} ms={p['ms']:.4f} attn={p['attention_ms']:.4f} gemm={p['gemm_ms']:.4f}",
+                  file=sys.stderr, flush=True)
+            if r in (0.0, 1.0):
+                q = run(batch, "prefill" if r == 0.0 else "decode")
+                q.update(r=r, budget=bud, mode="prefill" if r == 0.0 else "decode")
+                pts.append(q)
+    # analysis at the largest budget: K(r), EB line, kappa
+    big = max(budgets)
+    mb = sorted([p for p in pts if p["budget"] == big and p["mode"] == "mixed"], key=lambda p: p["r"])
+    r_arr = [p["r"] for p in mb]
+    K = [p["ms"] for p in mb]
+    Ka = [p["attention_ms"] for p in mb]
+    rep = AN.sweep_report(r_arr, K)
+    rep_attn = AN.sweep_report(r_arr, Ka)
+    out = {"budget": big, "r": r_arr, "K_ms": K, "attention_ms": Ka, "gemm_ms": [p["gemm_ms"] for p in mb],
+           "other_ms": [p["other_ms"] for p in mb], "K_bar_ms": list(AN.eb_line(r_arr, K[0], K[-1])),
+           "fit": rep, "attention_fit": rep_attn,
+           "eb_endpoints_ms": {p["mode"]: p["ms"] for p in pts if p["budget"] == big and p["mode"] != "mixed"},
+           "eb_favoured_r": AN.eb_favoured(r_arr, K, 0.02 * max(K))}
+    # per-share linear fits over budgets and the crossover share
+    if len(budgets) >= 2:
+        betas, alphas, r2s = [], [], []
+        for r in rs:
+            ps = [p for p in pts if p["r"] == r and p["mode"] == "mixed"]
+            a, b_, r2 = AN.linear_fit([p["n_tok"] for p in ps], [p["ms"] for p in ps])
+            alphas.append(a)
+            betas.append(b_)
+            r2s.append(r2)
+        out.update(alpha_ms=alphas, beta_ms_per_token=betas, r2=r2s,
+                   crossover_r=AN.crossover_primary(rs, betas))
+    return out, pts
+
 
 def main():
     args = parse()
@@ -170,6 +275,26 @@ def main():
                           "GBps": 2 * n / dt / 1e9}))
         return
 
+    if args.workload == "sweep8b":
+        t0 = time.perf_counter()
+        out, pts = sweep(args, dev)
+        wall = time.perf_counter() - t0
+        big = out["budget"]
+        line = {"metric": METRIC, "value": round(out["fit"]["kappa"], 4), "unit": "kappa (dimensionless)",
+                "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+                "ms_per_step": round(out["K_ms"][-1], 5), "higher_is_better": False, "scaling": "weak",
+                "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+                "config": {"workload": f"llama3-8b-layer MB sweep, budgets {args.budgets}, decode ctx "
+                                       f"{'16' if args.ctx16 else 'U[1024,8192]'}, r = 0..1 step 0.1",
+                           "parallelism": "single-gpu"},
+                "sweep": out, "points": pts, "wall_s": round(wall, 1)}
+        js = json.dumps(line)
+        print(js)
+        if args.json_out:
+            with open(args.json_out, "w") as f:
+                f.write(js + "\n")
+        return
+
     label, shape, batch, mode = workload(args)
     step_fn = {"decode": B.eb_layer_step_decode, "prefill": B.eb_layer_step_prefill,
                "mixed": B.eb_layer_step_mixed}[mode]
@@ -180,28 +305,7 @@ def main():
     y = torch.empty_like(x)
     h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
     ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
-    call = lambda: step_fn(h, w, pool.k_cache, pool.v_cache, pool.block_tables, batch.context_lens,  # noqa: E731
-                           batch.chunk_lens, x, y=y, ws=ws)
-    for _ in range(args.warmup):
-        call()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        call()
-    torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) / args.steps * 1e3
-
-    # per-stage durations: HIP events the library records around each stage on
-    # the stream it launches on, over a second pass of the same steps
-    B.eb_profile(h, True)
-    acc = {}
-    for _ in range(args.steps):
-        call()
-        for k, v in B.eb_profile_read(h).items():
-            acc[k] = acc.get(k, 0.0) + v
-    B.eb_profile(h, False)
-    stages = {k: v / args.steps for k, v in acc.items()}
-    torch.cuda.synchronize()
+    ms, stages = measure(B, h, step_fn, w, pool, batch, x, y, ws, args.steps, args.warmup)
 
     wk = step_work(shape, batch)
     step_bytes = wk["kv_bytes_decode"] + wk["kv_bytes_prefill"] + wk["weight_bytes"] + wk["act_bytes"]

@@ -78,6 +78,7 @@ DevMeta meta_at(const HostPlan &p, const int32_t *dev) {
   m.row_pos = dev + p.o_row_pos;
   m.dec_seq = dev + p.o_dec_seq;
   m.dec_split_off = dev + p.o_dec_off;
+  m.dec_unit_off = dev + p.o_unit_off;
   m.comb_list = dev + p.o_comb;
   m.tile_seq = dev + p.o_tseq;
   m.tile_qb = dev + p.o_tqb;
@@ -86,6 +87,7 @@ DevMeta meta_at(const HostPlan &p, const int32_t *dev) {
   m.T = p.T;
   m.n_dec = p.n_dec;
   m.total_splits = p.total_splits;
+  m.total_units = p.total_units;
   m.n_comb = p.n_comb;
   m.n_tiles = p.n_tiles;
   return m;
@@ -181,7 +183,7 @@ eb_status run_step(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *k
   if (!x || !y) return fail(EB_ERR_NULL, "x or y is NULL");
   if (x == y) return fail(EB_ERR_BATCH, "y must not alias x");
   HostPlan p;
-  build_plan(h->cfg, *b, p);
+  build_plan(h->cfg, *b, mode, p);
   const Shape &sh = h->shape;
   const WsLayout L = layout_for(sh, p, true);
   s = check_ws(ws, ws_bytes, L.total);
@@ -321,7 +323,7 @@ size_t eb_workspace_bytes(const eb_handle *h, const eb_batch *batch, eb_mode mod
   std::string err;
   if (check_batch(h->cfg, batch, -1, mode, err) != EB_OK) return 0;
   HostPlan p;
-  build_plan(h->cfg, *batch, p);
+  build_plan(h->cfg, *batch, mode, p);
   return layout_for(h->shape, p, true).total;
 }
 
@@ -433,7 +435,7 @@ eb_status eb_op_rope_kv_append(eb_handle *h, void *qkv, const eb_kv_cache *kv, c
   if (batch->num_tokens == 0) return EB_OK;
   if (!qkv) return fail(EB_ERR_NULL, "qkv is NULL");
   HostPlan p;
-  build_plan(h->cfg, *batch, p);
+  build_plan(h->cfg, *batch, EB_MODE_MIXED, p);
   const WsLayout L = layout_for(h->shape, p, false);
   s = check_ws(ws, ws_bytes, L.total);
   if (s != EB_OK) return s;
@@ -454,7 +456,7 @@ eb_status eb_op_attention(eb_handle *h, const void *qkv, const eb_kv_cache *kv, 
   if (batch->num_tokens == 0) return EB_OK;
   if (!qkv || !out) return fail(EB_ERR_NULL, "qkv or out is NULL");
   HostPlan p;
-  build_plan(h->cfg, *batch, p);
+  build_plan(h->cfg, *batch, mode, p);
   const WsLayout L = layout_for(h->shape, p, false);
   s = check_ws(ws, ws_bytes, L.total);
   if (s != EB_OK) return s;
@@ -479,7 +481,7 @@ eb_status eb_op_gather_kv(eb_handle *h, const eb_kv_cache *kv, const eb_batch *b
   if (batch->num_seqs == 0) return EB_OK;
   if (!out_k || !out_v) return fail(EB_ERR_NULL, "out_k or out_v is NULL");
   HostPlan p;
-  build_plan(h->cfg, *batch, p);
+  build_plan(h->cfg, *batch, EB_MODE_MIXED, p);
   const WsLayout L = layout_for(h->shape, p, false);
   s = check_ws(ws, ws_bytes, L.total);
   if (s != EB_OK) return s;

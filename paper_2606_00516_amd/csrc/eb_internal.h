@@ -11,10 +11,17 @@ namespace eb {
 // length, so its result is the same in any batch.
 constexpr int kDecodePagesPerSplit = 32;
 constexpr int kPageSize = 16;
+// A decode request with at most this many keys (context + 1) runs as units
+// of kShortDecodeHeads kv heads, one wavefront each, instead of page splits.
+constexpr int kShortDecodeKeys = 64;
+constexpr int kShortDecodeHeads = 4;
 
-// Prefill attention tiles: query positions per tile for a GQA group size
-// (must agree with PrefillTraits in the attention kernels).
-inline int prefill_bq(int group) { return 128 / group; }
+// Prefill attention items: query positions per item for a GQA group size,
+// in the prefill-only launch and inside the mixed launch (must agree with
+// PrefillTraits in the attention kernels).
+inline int prefill_bq(int group, bool mixed_launch) {
+  return mixed_launch ? (group >= 4 ? 16 : 64 / group) : 128 / group;
+}
 
 // Per-step metadata in device memory (all int32), produced by the planner.
 struct DevMeta {
@@ -25,11 +32,12 @@ struct DevMeta {
   const int32_t *row_pos;       // [T] absolute position of each row
   const int32_t *dec_seq;       // [D] request index of each decode request
   const int32_t *dec_split_off; // [D+1] prefix sum of split counts
+  const int32_t *dec_unit_off;  // [D+1] prefix sum of work units (blocks)
   const int32_t *comb_list;     // [C] decode indices with >= 2 splits
   const int32_t *tile_seq;      // [NT] prefill tiles, longest first
   const int32_t *tile_qb;       // [NT] query block of each tile
   const int32_t *gather_off;    // [S+1] prefix sum of (c + n)
-  int32_t S, T, n_dec, total_splits, n_comb, n_tiles;
+  int32_t S, T, n_dec, total_splits, total_units, n_comb, n_tiles;
 };
 
 struct KV {

@@ -8,8 +8,13 @@ namespace eb {
 namespace {
 constexpr int kPagesPerSplit = 32;  // must match kDecodePagesPerSplit
 constexpr int kPage = 16;
+constexpr int kShortKeys = 64;      // must match kShortDecodeKeys
+constexpr int kShortHeads = 4;      // must match kShortDecodeHeads
 
-int prefill_bq_host(int group) { return 128 / group; }  // must match the prefill kernel
+// query positions per prefill item (must match the attention kernels)
+int prefill_bq_host(int group, bool mixed_launch) {
+  return mixed_launch ? (group >= 4 ? 16 : 64 / group) : 128 / group;
+}
 }  // namespace
 
 int32_t decode_splits(int32_t c) {
@@ -146,13 +151,16 @@ eb_status check_tables(const eb_layer_config &cfg, const eb_batch &b, const int3
 
 size_t plan_capacity(int32_t max_seqs, int32_t max_tokens, int32_t group) {
   const size_t S = (size_t)max_seqs, T = (size_t)max_tokens;
-  const size_t tiles = T / (size_t)prefill_bq_host(group) + S + 1;
-  return 8 * S + 2 * T + 2 * tiles + 64;  // + per-array alignment padding
+  const size_t tiles = T / (size_t)std::min(prefill_bq_host(group, true), prefill_bq_host(group, false)) + S + 1;
+  return 9 * S + 2 * T + 2 * tiles + 64;  // + per-array alignment padding
 }
 
-void build_plan(const eb_layer_config &cfg, const eb_batch &b, HostPlan &p) {
+void build_plan(const eb_layer_config &cfg, const eb_batch &b, eb_mode mode, HostPlan &p) {
   const int S = b.num_seqs, T = b.num_tokens;
-  const int bq = prefill_bq_host(cfg.n_q_heads / cfg.n_kv_heads);
+  bool any_dec = false, any_pf = false;
+  for (int i = 0; i < S; ++i) (b.chunk_lens_host[i] == 1 ? any_dec : any_pf) = true;
+  const bool mixed_launch = mode == EB_MODE_MIXED && any_dec && any_pf;
+  const int bq = prefill_bq_host(cfg.n_q_heads / cfg.n_kv_heads, mixed_launch);
   p = HostPlan();
   p.S = S;
   p.T = T;
@@ -162,7 +170,8 @@ void build_plan(const eb_layer_config &cfg, const eb_batch &b, HostPlan &p) {
     goff[i + 1] = goff[i] + b.context_lens_host[i] + b.chunk_lens_host[i];
   }
   p.gather_total = goff[S];
-  std::vector<int32_t> row_seq(T), row_pos(T), dec_seq, dec_off(1, 0), comb;
+  std::vector<int32_t> row_seq(T), row_pos(T), dec_seq, dec_off(1, 0), unit_off(1, 0), comb;
+  const int nkv = cfg.n_kv_heads;
   struct Tile {
     int32_t seq, qb, cost;
   };
@@ -178,6 +187,8 @@ void build_plan(const eb_layer_config &cfg, const eb_batch &b, HostPlan &p) {
       if (ns >= 2) comb.push_back((int32_t)dec_seq.size());
       dec_seq.push_back(i);
       dec_off.push_back(dec_off.back() + ns);
+      const int units = (c + 1 <= kShortKeys) ? (nkv + kShortHeads - 1) / kShortHeads : ns * nkv;
+      unit_off.push_back(unit_off.back() + units);
     } else {
       const int nqb = (n + bq - 1) / bq;
       for (int qb = 0; qb < nqb; ++qb) tiles.push_back({i, qb, c + std::min(n, (qb + 1) * bq)});
@@ -186,6 +197,7 @@ void build_plan(const eb_layer_config &cfg, const eb_batch &b, HostPlan &p) {
   std::stable_sort(tiles.begin(), tiles.end(), [](const Tile &a, const Tile &b) { return a.cost > b.cost; });
   p.n_dec = (int32_t)dec_seq.size();
   p.total_splits = dec_off.back();
+  p.total_units = unit_off.back();
   p.n_comb = (int32_t)comb.size();
   p.n_tiles = (int32_t)tiles.size();
 
@@ -204,6 +216,7 @@ void build_plan(const eb_layer_config &cfg, const eb_batch &b, HostPlan &p) {
   p.o_row_pos = put(row_pos.data(), row_pos.size());
   p.o_dec_seq = put(dec_seq.data(), dec_seq.size());
   p.o_dec_off = put(dec_off.data(), dec_off.size());
+  p.o_unit_off = put(unit_off.data(), unit_off.size());
   p.o_comb = put(comb.data(), comb.size());
   std::vector<int32_t> tseq(tiles.size()), tqb(tiles.size());
   for (size_t t = 0; t < tiles.size(); ++t) {

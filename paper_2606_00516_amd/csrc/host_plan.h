@@ -12,12 +12,12 @@ namespace eb {
 
 struct HostPlan {
   int32_t S = 0, T = 0;
-  int32_t n_dec = 0, total_splits = 0, n_comb = 0, n_tiles = 0;
+  int32_t n_dec = 0, total_splits = 0, total_units = 0, n_comb = 0, n_tiles = 0;
   int64_t gather_total = 0;
   std::vector<int32_t> blob;  // every metadata array, concatenated
   // offsets (in int32 elements) of each array inside blob
-  size_t o_ctx = 0, o_len = 0, o_row = 0, o_row_seq = 0, o_row_pos = 0, o_dec_seq = 0, o_dec_off = 0, o_comb = 0,
-         o_tseq = 0, o_tqb = 0, o_goff = 0;
+  size_t o_ctx = 0, o_len = 0, o_row = 0, o_row_seq = 0, o_row_pos = 0, o_dec_seq = 0, o_dec_off = 0, o_unit_off = 0,
+         o_comb = 0, o_tseq = 0, o_tqb = 0, o_goff = 0;
 };
 
 // Shape support: head_dim in {64, 128}; G = n_q / n_kv in {1, 2, 4, 8};
@@ -37,7 +37,9 @@ eb_status check_tables(const eb_layer_config &cfg, const eb_batch &b, const int3
 // Build the metadata of a step: row offsets, per-row request and position,
 // the decode split list, the prefill tile list (longest first) and gather
 // offsets.  The batch must have passed check_batch.
-void build_plan(const eb_layer_config &cfg, const eb_batch &b, HostPlan &p);
+// The prefill item size depends on the launch: `mode` says which launch the
+// step makes (a mixed batch in EB_MODE_MIXED uses the single mixed grid).
+void build_plan(const eb_layer_config &cfg, const eb_batch &b, eb_mode mode, HostPlan &p);
 
 // Upper bound of blob size (int32 elements) for a handle's limits.
 size_t plan_capacity(int32_t max_seqs, int32_t max_tokens, int32_t group);

@@ -16,9 +16,10 @@ namespace eb {
 constexpr float kNegInf = -__builtin_inff();
 
 // ===========================================================================
-// Decode: one work item = (decode request, split of 32 pages, kv head), NW
-// wavefronts (4 alone, 8 inside the mixed launch).  Wave w streams pages w,
-// w+NW, ... of the split.  Lane layout
+// Decode: one work unit = (decode request, split of 32 pages, kv head) with
+// NW wavefronts streaming pages w, w+NW, .. of the split, or, for a request
+// with at most 64 keys, (decode request, 4 kv heads) with one wavefront per
+// kv head.  Lane layout
 // over a 16 x HD page block: each 16-byte load instruction covers 1 KiB, lane
 // l holding 8 dims of one token; LPT = HD/8 lanes share a token.  Scores are
 // reduced over those lanes with DPP; each lane keeps its own running
@@ -110,92 +111,55 @@ __device__ __forceinline__ void decode_page_update(const u32x4_t (&k)[HD / 32], 
   }
 }
 
-template <int HD, int G, int NW>
-__device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
-                                            const DevMeta md, int item, int kh, uint16_t *__restrict__ out,
-                                            float *__restrict__ part_o, float *__restrict__ part_ml, float *lds) {
-  using Tr = DecodeTraits<HD, G, NW>;
-  constexpr int LPT = Tr::LPT, NLD = Tr::NLD;
-  constexpr int SPLIT = kDecodePagesPerSplit * kPageSize;
-  const int lane = threadIdx.x & 63;
-  // wave index made visibly uniform, so page addressing stays scalar
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int cols = (nq + 2 * nkv) * HD;
-
-  // locate the decode request owning this split
-  int lo = 0, hi = md.n_dec - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (md.dec_split_off[mid] <= item) lo = mid; else hi = mid - 1;
-  }
-  const int d = lo;
-  const int s0 = md.dec_split_off[d];
-  const int split = item - s0;
-  const int nsplit = md.dec_split_off[d + 1] - s0;
-  const int seq = md.dec_seq[d];
-  const int nkeys = md.seq_ctx[seq] + 1;
-  const int row = md.seq_row[seq];
-  const int k0 = split * SPLIT;
-  const int k1 = min(nkeys, k0 + SPLIT);
-  const int pg0 = k0 / kPageSize, pg1 = (k1 + kPageSize - 1) / kPageSize;
-  const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
-
-  // queries of the G heads, this lane's 8 dims, as bf16 pairs (loaded
-  // first: the page loads issued after them then stay in flight)
-  const int dq = (lane % LPT) * 8;
-  const float qscale = kLog2e / sqrtf((float)HD);
-  u32x4_t qw[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) qw[h] = ld_u32x4(qkv + (size_t)row * cols + (kh * G + h) * HD + dq);
-  float mrun[G], lrun[G], o[G][8];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    mrun[h] = kNegInf;
-    lrun[h] = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) o[h][i] = 0.f;
-  }
-
-  // Wave w streams pages w, w+NW, ... through a ring of page buffers (three
-  // for G <= 2, two for larger groups, whose accumulators need the
-  // registers), rotated in straight-line code; pages past the split's end
-  // load as zeros without memory traffic and are masked out.
-  const int pfirst = pg0 + wave;
+// Stream pages p_first, p_first + stride, .. (< pg1) of one (request, kv
+// head) through a ring of page buffers (three for G <= 2, two for larger
+// groups, whose accumulators need the registers), rotated in straight-line
+// code; pages past the end load as zeros without memory traffic and are
+// masked out.  Scheduling barriers keep page loads and page updates in
+// program order, so the wait before an update covers only that page.
+template <int HD, int G>
+__device__ __forceinline__ void decode_stream(const KV kv, const int32_t *bt, int p_first, int stride, int pg1, int k1,
+                                              int nkv, int kh, int lane, float qscale, const u32x4_t (&qw)[G],
+                                              float (&mrun)[G], float (&lrun)[G], float (&o)[G][8]) {
+  constexpr int NLD = HD / 32;
   u32x4_t ka[NLD], va[NLD], kb[NLD], vb[NLD], kc[NLD], vc[NLD];
-  // scheduling barriers keep page loads and page updates in program order,
-  // so the wait before an update covers only that page's loads
 #define EB_LOAD(K_, V_, P_)                                                  \
   decode_load_page<HD, NLD>(K_, V_, kv, bt, P_, pg1, nkv, kh, lane);         \
   __builtin_amdgcn_sched_barrier(0);
 #define EB_UPDATE(K_, V_, P_)                                                \
   decode_page_update<HD, G>(K_, V_, qw, mrun, lrun, o, P_, k1, lane, qscale); \
   __builtin_amdgcn_sched_barrier(0);
-  EB_LOAD(ka, va, pfirst)
-  EB_LOAD(kb, vb, pfirst + NW)
+  EB_LOAD(ka, va, p_first)
+  EB_LOAD(kb, vb, p_first + stride)
   if constexpr (G <= 2) {
-    EB_LOAD(kc, vc, pfirst + 2 * NW)
-    for (int p = pfirst; p < pg1; p += 3 * NW) {
+    EB_LOAD(kc, vc, p_first + 2 * stride)
+    for (int p = p_first; p < pg1; p += 3 * stride) {
       EB_UPDATE(ka, va, p)
-      EB_LOAD(ka, va, p + 3 * NW)
-      EB_UPDATE(kb, vb, p + NW)
-      EB_LOAD(kb, vb, p + 4 * NW)
-      EB_UPDATE(kc, vc, p + 2 * NW)
-      EB_LOAD(kc, vc, p + 5 * NW)
+      EB_LOAD(ka, va, p + 3 * stride)
+      EB_UPDATE(kb, vb, p + stride)
+      EB_LOAD(kb, vb, p + 4 * stride)
+      EB_UPDATE(kc, vc, p + 2 * stride)
+      EB_LOAD(kc, vc, p + 5 * stride)
     }
   } else {
     (void)kc;
     (void)vc;
-    for (int p = pfirst; p < pg1; p += 2 * NW) {
+    for (int p = p_first; p < pg1; p += 2 * stride) {
       EB_UPDATE(ka, va, p)
-      EB_LOAD(ka, va, p + 2 * NW)
-      EB_UPDATE(kb, vb, p + NW)
-      EB_LOAD(kb, vb, p + 3 * NW)
+      EB_LOAD(ka, va, p + 2 * stride)
+      EB_UPDATE(kb, vb, p + stride)
+      EB_LOAD(kb, vb, p + 3 * stride)
     }
   }
 #undef EB_LOAD
 #undef EB_UPDATE
+}
 
-  // merge the token groups of this wave (lanes with equal lane % LPT)
+// Merge the token groups of a wave (lanes with equal lane % LPT): afterwards
+// every lane holds the wave's state for its 8 dims.
+template <int HD, int G>
+__device__ __forceinline__ void decode_merge_lanes(float (&mrun)[G], float (&lrun)[G], float (&o)[G][8]) {
+  constexpr int LPT = HD / 8;
 #pragma unroll
   for (int mask = LPT; mask < 64; mask <<= 1) {
 #pragma unroll
@@ -208,6 +172,89 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
       lse_merge<8>(mrun[h], lrun[h], o[h], m2, l2, o2);
     }
   }
+}
+
+template <int HD, int G>
+__device__ __forceinline__ void decode_load_q(const uint16_t *__restrict__ qkv, int cols, int row, int kh, int lane,
+                                              u32x4_t (&qw)[G], float (&mrun)[G], float (&lrun)[G],
+                                              float (&o)[G][8]) {
+  const int dq = (lane % (HD / 8)) * 8;
+#pragma unroll
+  for (int h = 0; h < G; ++h) qw[h] = ld_u32x4(qkv + (size_t)row * cols + (kh * G + h) * HD + dq);
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    mrun[h] = kNegInf;
+    lrun[h] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[h][i] = 0.f;
+  }
+}
+
+// One decode work unit.  Unit u of decode request d (binary search over the
+// unit prefix sums): a request with at most kShortDecodeKeys keys has one
+// unit per 4 kv heads, each wavefront taking one kv head and all its pages
+// and writing its output directly; a longer request has one unit per
+// (split of 32 pages, kv head), its NW wavefronts streaming pages w, w+NW, ..
+// and merging through LDS, with the result written directly (one split) or
+// as a partial for the combine.  Which kind a request gets depends only on
+// its own length.
+template <int HD, int G, int NW>
+__device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
+                                            const DevMeta md, int unit, uint16_t *__restrict__ out,
+                                            float *__restrict__ part_o, float *__restrict__ part_ml, float *lds) {
+  using Tr = DecodeTraits<HD, G, NW>;
+  constexpr int LPT = Tr::LPT;
+  constexpr int SPLIT = kDecodePagesPerSplit * kPageSize;
+  const int lane = threadIdx.x & 63;
+  // wave index made visibly uniform, so page addressing stays scalar
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int cols = (nq + 2 * nkv) * HD;
+  const float qscale = kLog2e / sqrtf((float)HD);
+
+  int lo = 0, hi = md.n_dec - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (md.dec_unit_off[mid] <= unit) lo = mid; else hi = mid - 1;
+  }
+  const int d = lo;
+  const int local = unit - md.dec_unit_off[d];
+  const int seq = md.dec_seq[d];
+  const int nkeys = md.seq_ctx[seq] + 1;
+  const int row = md.seq_row[seq];
+  const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
+  const int dq = (lane % LPT) * 8;
+  u32x4_t qw[G];
+  float mrun[G], lrun[G], o[G][8];
+
+  if (nkeys <= kShortDecodeKeys) {
+    const int kh = local * kShortDecodeHeads + wave;
+    if (wave >= kShortDecodeHeads || kh >= nkv) return;
+    decode_load_q<HD, G>(qkv, cols, row, kh, lane, qw, mrun, lrun, o);
+    decode_stream<HD, G>(kv, bt, 0, 1, (nkeys + kPageSize - 1) / kPageSize, nkeys, nkv, kh, lane, qscale, qw, mrun,
+                         lrun, o);
+    decode_merge_lanes<HD, G>(mrun, lrun, o);
+    if (lane < LPT) {
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float inv = 1.0f / lrun[h];
+        const u32x4_t w = {pack_bf16x2(o[h][0] * inv, o[h][1] * inv), pack_bf16x2(o[h][2] * inv, o[h][3] * inv),
+                           pack_bf16x2(o[h][4] * inv, o[h][5] * inv), pack_bf16x2(o[h][6] * inv, o[h][7] * inv)};
+        st_u32x4(out + (size_t)row * nq * HD + (kh * G + h) * HD + dq, w);
+      }
+    }
+    return;
+  }
+
+  const int split = local / nkv, kh = local - split * nkv;
+  const int item = md.dec_split_off[d] + split;   // global split index (partials)
+  const int nsplit = md.dec_split_off[d + 1] - md.dec_split_off[d];
+  const int k0 = split * SPLIT;
+  const int k1 = min(nkeys, k0 + SPLIT);
+  const int pg0 = k0 / kPageSize, pg1 = (k1 + kPageSize - 1) / kPageSize;
+  decode_load_q<HD, G>(qkv, cols, row, kh, lane, qw, mrun, lrun, o);
+  decode_stream<HD, G>(kv, bt, pg0 + wave, NW, pg1, k1, nkv, kh, lane, qscale, qw, mrun, lrun, o);
+  decode_merge_lanes<HD, G>(mrun, lrun, o);
+
   // across the NW waves through LDS: [wave][h][HD] outputs, then [wave][h][2]
   float *lo_ = lds;
   float *lml = lds + NW * G * HD;
@@ -287,35 +334,38 @@ __global__ __launch_bounds__(64) void k_decode_combine(DevMeta md, const float *
 
 // ===========================================================================
 // Prefill: one work item = (request, block of BQ query positions, kv head):
-// G heads x BQ positions = 128 query rows, one 16-row block per wavefront
-// (8 wavefronts).  Keys and values stream through LDS in tiles of 64
+// G heads x BQ positions, cut into 16-row blocks (one head, 16 positions)
+// shared out over NW wavefronts (8 in the prefill-only launch, 4 inside the
+// mixed launch).  Keys and values stream through LDS in tiles of 64
 // positions gathered from 4 pages; the next tile's global loads are issued
 // before the current tile is consumed.  Scores are formed transposed,
 // S^T = K Q^T, with the 16x16x32 bf16 MFMA, so a lane holds one query column
 // and the row max needs only two cross-lane steps; P^T stays in registers as
 // the B operand of O^T = V^T P^T (keys permuted consistently on both
-// operands), with V^T staged in LDS.
+// operands), with V^T staged in LDS.  A row's arithmetic does not depend on
+// which item it sits in, so both launches give the same bits.
 // ===========================================================================
-template <int HD, int G>
+template <int HD, int G, int NW>
 struct PrefillTraits {
-  static constexpr int NW = 8;                  // wavefronts per item
-  static constexpr int BQ = 128 / G;            // query positions per item
-  static constexpr int KT = 64;                 // keys per tile
-  static constexpr int KS_STRIDE = HD + 8;      // bf16 elements per K row in LDS
-  static constexpr int VT_STRIDE = KT + 4;      // bf16 elements per V^T row in LDS
+  static constexpr int BQ = NW == 8 ? 128 / G : (G >= 4 ? 16 : 64 / G);  // query positions per item
+  static constexpr int RB = (G * BQ / 16) / NW;  // 16-row blocks per wavefront
+  static constexpr int KT = 64;                  // keys per tile
+  static constexpr int KS_STRIDE = HD + 8;       // bf16 elements per K row in LDS
+  static constexpr int VT_STRIDE = KT + 4;       // bf16 elements per V^T row in LDS
   static constexpr int LDS_BYTES = (KT * KS_STRIDE + HD * VT_STRIDE) * 2;
-  static constexpr int KCH = KT * (HD / 8);     // 16-byte K chunks per tile
+  static constexpr int KCH = KT * (HD / 8);      // 16-byte K chunks per tile
   static constexpr int VCH = (KT / 2) * (HD / 8);  // (key pair, 8 dims) V units per tile
   static constexpr int KPT = (KCH + NW * 64 - 1) / (NW * 64);  // per thread
   static constexpr int VPT = (VCH + NW * 64 - 1) / (NW * 64);
+  static_assert(RB >= 1 && RB * NW * 16 == G * BQ, "row blocks");
 };
 
-template <int HD, int G>
+template <int HD, int G, int NW>
 __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
                                              const DevMeta md, int tile, int kh, uint16_t *__restrict__ out,
                                              uint16_t *lds) {
-  using Tr = PrefillTraits<HD, G>;
-  constexpr int NW = Tr::NW, BQ = Tr::BQ, KT = Tr::KT, KSS = Tr::KS_STRIDE, VTS = Tr::VT_STRIDE;
+  using Tr = PrefillTraits<HD, G, NW>;
+  constexpr int BQ = Tr::BQ, RB = Tr::RB, KT = Tr::KT, KSS = Tr::KS_STRIDE, VTS = Tr::VT_STRIDE;
   constexpr int KCH = Tr::KCH, VCH = Tr::VCH, KPT = Tr::KPT, VPT = Tr::VPT;
   constexpr int NKS = HD / 32;  // k-steps of the QK^T product
   constexpr int NOB = HD / 16;  // 16-dim output blocks
@@ -338,24 +388,33 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
   uint16_t *Ks = lds;
   uint16_t *Vt = lds + KT * KSS;
   const float qscale = kLog2e / sqrtf((float)HD);
-  const int lq = lane & 15;   // query column of this lane inside the 16-row block
+  const int lq = lane & 15;   // query column of this lane inside a 16-row block
   const int lg = lane >> 4;   // lane group 0..3
 
-  // this wave's row block: head h, 16 query positions sub*16 ..
-  const int h = wave % G, sub = wave / G;
-  const int qrel = q_lo + sub * 16 + lq;
-  const bool qok = qrel < q_hi;
-  const int qpos = c + qrel;
-  u32x4_t qreg[NKS];
-  {
-    const uint16_t *src = qkv + (size_t)(row0 + qrel) * cols + (kh * G + h) * HD + lg * 8;
+  // row blocks of this wave: rb = wave + NW i -> head rb % G, positions
+  // (rb / G) * 16 ..
+  u32x4_t qreg[RB][NKS];
+  int qrel[RB];
+  bool qok[RB];
 #pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) qreg[ks] = qok ? ld_u32x4(src + ks * 32) : u32x4_t{0, 0, 0, 0};
+  for (int i = 0; i < RB; ++i) {
+    const int rb = wave + NW * i;
+    const int h = rb % G, sub = rb / G;
+    qrel[i] = q_lo + sub * 16 + lq;
+    qok[i] = qrel[i] < q_hi;
+    const uint16_t *src = qkv + (size_t)(row0 + qrel[i]) * cols + (kh * G + h) * HD + lg * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qreg[i][ks] = qok[i] ? ld_u32x4(src + ks * 32) : u32x4_t{0, 0, 0, 0};
   }
-  f32x4_t oacc[NOB];
+  f32x4_t oacc[RB][NOB];
+  float mrun[RB], lrun[RB];
 #pragma unroll
-  for (int ob = 0; ob < NOB; ++ob) oacc[ob] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float mrun = kNegInf, lrun = 0.f;
+  for (int i = 0; i < RB; ++i) {
+    mrun[i] = kNegInf;
+    lrun[i] = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) oacc[i][ob] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
 
   // global -> register staging of one K/V tile (keys past c + n read as 0)
   u32x4_t kreg[KPT], vreg[VPT][2];
@@ -415,80 +474,88 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
     stage();
     __syncthreads();
     if (t + 1 < ntiles) fetch(t + 1);   // in flight while this tile is consumed
-    const bool need_mask = (k0 + KT - 1) > min_qpos || !qok;
-    // S^T block kb: keys k0 + 16 kb + 4 lg + j, query column lq
-    f32x4_t sc[4];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      sc[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < RB; ++i) {
+      const bool need_mask = (k0 + KT - 1) > min_qpos || !qok[i];
+      const int qpos = c + qrel[i];
+      // S^T block kb: keys k0 + 16 kb + 4 lg + j, query column lq
+      f32x4_t sc[4];
 #pragma unroll
-      for (int ks = 0; ks < NKS; ++ks) {
-        const u32x4_t a = ld_u32x4(Ks + (kb * 16 + lq) * KSS + ks * 32 + lg * 8);
-        sc[kb] = mfma16x16x32(a, qreg[ks], sc[kb]);
-      }
-    }
-    float mx = mrun;
+      for (int kb = 0; kb < 4; ++kb) {
+        sc[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float v = sc[kb][j] * qscale;
-        if (need_mask) {
-          const int kp = k0 + kb * 16 + lg * 4 + j;
-          if (kp > qpos || !qok) v = kNegInf;
+        for (int ks = 0; ks < NKS; ++ks) {
+          const u32x4_t a = ld_u32x4(Ks + (kb * 16 + lq) * KSS + ks * 32 + lg * 8);
+          sc[kb] = mfma16x16x32(a, qreg[i][ks], sc[kb]);
         }
-        sc[kb][j] = v;
-        mx = fmaxf(mx, v);
       }
-    mx = fmaxf(mx, shfl_xor_f32(mx, 16));
-    mx = fmaxf(mx, shfl_xor_f32(mx, 32));
-    const float alpha = (mrun == kNegInf) ? 0.f : fast_exp2(mrun - mx);
-    const bool live = mx != kNegInf;
-    float l = lrun * alpha;
-    uint32_t pk[4][2];
+      float mx = mrun[i];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      float p4[4];
+      for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        p4[j] = (live && sc[kb][j] != kNegInf) ? fast_exp2(sc[kb][j] - mx) : 0.f;
-        l += p4[j];
+        for (int j = 0; j < 4; ++j) {
+          float v = sc[kb][j] * qscale;
+          if (need_mask) {
+            const int kp = k0 + kb * 16 + lg * 4 + j;
+            if (kp > qpos || !qok[i]) v = kNegInf;
+          }
+          sc[kb][j] = v;
+          mx = fmaxf(mx, v);
+        }
+      mx = fmaxf(mx, shfl_xor_f32(mx, 16));
+      mx = fmaxf(mx, shfl_xor_f32(mx, 32));
+      const float alpha = (mrun[i] == kNegInf) ? 0.f : fast_exp2(mrun[i] - mx);
+      const bool live = mx != kNegInf;
+      float l = lrun[i] * alpha;
+      uint32_t pk[4][2];
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) {
+        float p4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          p4[j] = (live && sc[kb][j] != kNegInf) ? fast_exp2(sc[kb][j] - mx) : 0.f;
+          l += p4[j];
+        }
+        pk[kb][0] = pack_bf16x2(p4[0], p4[1]);
+        pk[kb][1] = pack_bf16x2(p4[2], p4[3]);
       }
-      pk[kb][0] = pack_bf16x2(p4[0], p4[1]);
-      pk[kb][1] = pack_bf16x2(p4[2], p4[3]);
-    }
-    lrun = l;
-    mrun = mx;
+      lrun[i] = l;
+      mrun[i] = mx;
 #pragma unroll
-    for (int ob = 0; ob < NOB; ++ob) {
-      f32x4_t acc = oacc[ob] * alpha;
+      for (int ob = 0; ob < NOB; ++ob) {
+        f32x4_t acc = oacc[i][ob] * alpha;
 #pragma unroll
-      for (int ks2 = 0; ks2 < 2; ++ks2) {
-        // B (P^T): keys {4 lg .. +3} of block 2 ks2, then of block 2 ks2 + 1
-        const u32x4_t b = {pk[2 * ks2][0], pk[2 * ks2][1], pk[2 * ks2 + 1][0], pk[2 * ks2 + 1][1]};
-        // A (V^T): dim ob*16 + lq, the same keys
-        const uint16_t *vrow = Vt + (ob * 16 + lq) * VTS + ks2 * 32 + lg * 4;
-        const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vrow);
-        const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vrow + 16);
-        const u32x4_t a = {a0[0], a0[1], a1[0], a1[1]};
-        acc = mfma16x16x32(a, b, acc);
+        for (int ks2 = 0; ks2 < 2; ++ks2) {
+          // B (P^T): keys {4 lg .. +3} of block 2 ks2, then of block 2 ks2 + 1
+          const u32x4_t b = {pk[2 * ks2][0], pk[2 * ks2][1], pk[2 * ks2 + 1][0], pk[2 * ks2 + 1][1]};
+          // A (V^T): dim ob*16 + lq, the same keys
+          const uint16_t *vrow = Vt + (ob * 16 + lq) * VTS + ks2 * 32 + lg * 4;
+          const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vrow);
+          const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vrow + 16);
+          const u32x4_t a = {a0[0], a0[1], a1[0], a1[1]};
+          acc = mfma16x16x32(a, b, acc);
+        }
+        oacc[i][ob] = acc;
       }
-      oacc[ob] = acc;
     }
     __syncthreads();
   }
   // normalise and store: lane holds dims ob*16 + 4 lg + j of query lq
-  float l = lrun;
-  l += shfl_xor_f32(l, 16);
-  l += shfl_xor_f32(l, 32);
-  if (qok) {
-    const float inv = 1.0f / l;
-    uint16_t *dst = out + (size_t)(row0 + qrel) * nq * HD + (kh * G + h) * HD + lg * 4;
 #pragma unroll
-    for (int ob = 0; ob < NOB; ++ob) {
-      u32x2_t w = {pack_bf16x2(oacc[ob][0] * inv, oacc[ob][1] * inv),
-                   pack_bf16x2(oacc[ob][2] * inv, oacc[ob][3] * inv)};
-      *reinterpret_cast<u32x2_t *>(dst + ob * 16) = w;
+  for (int i = 0; i < RB; ++i) {
+    float l = lrun[i];
+    l += shfl_xor_f32(l, 16);
+    l += shfl_xor_f32(l, 32);
+    if (qok[i]) {
+      const int h = (wave + NW * i) % G;
+      const float inv = 1.0f / l;
+      uint16_t *dst = out + (size_t)(row0 + qrel[i]) * nq * HD + (kh * G + h) * HD + lg * 4;
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) {
+        u32x2_t w = {pack_bf16x2(oacc[i][ob][0] * inv, oacc[i][ob][1] * inv),
+                     pack_bf16x2(oacc[i][ob][2] * inv, oacc[i][ob][3] * inv)};
+        *reinterpret_cast<u32x2_t *>(dst + ob * 16) = w;
+      }
     }
   }
 }
@@ -500,29 +567,29 @@ template <int HD, int G>
 __global__ __launch_bounds__(256) void k_decode(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
                                                 float *part_o, float *part_ml) {
   __shared__ float lds[DecodeTraits<HD, G, 4>::LDS_BYTES / 4];
-  decode_item<HD, G, 4>(qkv, nq, nkv, kv, md, blockIdx.x, blockIdx.y, out, part_o, part_ml, lds);
+  decode_item<HD, G, 4>(qkv, nq, nkv, kv, md, blockIdx.x, out, part_o, part_ml, lds);
 }
 
 template <int HD, int G>
 __global__ __launch_bounds__(512) void k_prefill(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
                                                  uint16_t *out) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[PrefillTraits<HD, G>::LDS_BYTES / 2];
-  prefill_item<HD, G>(qkv, nq, nkv, kv, md, blockIdx.x, blockIdx.y, out, lds);
+  __shared__ __attribute__((aligned(16))) uint16_t lds[PrefillTraits<HD, G, 8>::LDS_BYTES / 2];
+  prefill_item<HD, G, 8>(qkv, nq, nkv, kv, md, blockIdx.x / nkv, blockIdx.x % nkv, out, lds);
 }
 
 // One grid for a mixed step: items [0, n_tiles) are prefill tiles (longest
-// first), the rest decode splits; every block branches uniformly on its kind
-// (8 wavefronts for both kinds).
+// first), the rest decode splits; every block (4 wavefronts) branches
+// uniformly on its kind.  Decode items run exactly the decode-only code.
 template <int HD, int G>
-__global__ __launch_bounds__(512) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
+__global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
                                                float *part_o, float *part_ml) {
-  constexpr int PB = PrefillTraits<HD, G>::LDS_BYTES, DB = DecodeTraits<HD, G, 8>::LDS_BYTES;
+  constexpr int PB = PrefillTraits<HD, G, 4>::LDS_BYTES, DB = DecodeTraits<HD, G, 4>::LDS_BYTES;
   __shared__ __attribute__((aligned(16))) uint16_t lds[(PB > DB ? PB : DB) / 2];
   const int b = blockIdx.x;
-  if (b < md.n_tiles)
-    prefill_item<HD, G>(qkv, nq, nkv, kv, md, b, blockIdx.y, out, lds);
+  if (b < md.n_tiles * nkv)
+    prefill_item<HD, G, 4>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, lds);
   else
-    decode_item<HD, G, 8>(qkv, nq, nkv, kv, md, b - md.n_tiles, blockIdx.y, out, part_o, part_ml,
+    decode_item<HD, G, 4>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml,
                           reinterpret_cast<float *>(lds));
 }
 
@@ -535,12 +602,13 @@ static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const 
   if (!(parts & 1)) {
     // combine only
   } else if (kind == 2 && has_dec && has_pf) {
-    hipLaunchKernelGGL((k_mixed<HD, G>), dim3(m.n_tiles + m.total_splits, nkv), dim3(512), 0, st, qkv, nq, nkv, kv, m,
-                       out, part_o, part_ml);
+    hipLaunchKernelGGL((k_mixed<HD, G>), dim3(m.n_tiles * nkv + m.total_units), dim3(256), 0, st, qkv, nq, nkv, kv,
+                       m, out, part_o, part_ml);
   } else {
-    if (has_pf) hipLaunchKernelGGL((k_prefill<HD, G>), dim3(m.n_tiles, nkv), dim3(512), 0, st, qkv, nq, nkv, kv, m, out);
+    if (has_pf)
+      hipLaunchKernelGGL((k_prefill<HD, G>), dim3(m.n_tiles * nkv), dim3(512), 0, st, qkv, nq, nkv, kv, m, out);
     if (has_dec)
-      hipLaunchKernelGGL((k_decode<HD, G>), dim3(m.total_splits, nkv), dim3(256), 0, st, qkv, nq, nkv, kv, m, out,
+      hipLaunchKernelGGL((k_decode<HD, G>), dim3(m.total_units), dim3(256), 0, st, qkv, nq, nkv, kv, m, out,
                          part_o, part_ml);
   }
   hipError_t e = hipGetLastError();

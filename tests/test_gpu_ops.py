@@ -235,7 +235,9 @@ def test_one_hot_attention_bit_exact(shape, target):
     # q = e0 * 100 for every head, key `target` = e0 * 100, all other keys
     # = -e0 * 100: the score gap is far past fp32 exp underflow, so every row
     # that can see the target returns exactly that key's value vector.
-    batch = gen.Batch(np.array([720, 0, 690], np.int32), np.array([1, 64, 30], np.int32))
+    # long decode (2 splits), prefill from 0, prefill with a prefix, and a
+    # short decode request (at most 64 keys: one wavefront per kv head)
+    batch = gen.Batch(np.array([720, 0, 690, 40], np.int32), np.array([1, 64, 30, 1], np.int32))
     case = _filled_case(shape, batch)
     nq, nkv, hd = shape.n_q_heads, shape.n_kv_heads, shape.head_dim
     kb = gen.bits(case.pool.k_cache).copy()
