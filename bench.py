@@ -117,28 +117,38 @@ def cpu_baseline(shape, batch, w, pool, x, mode, target_s):
     off = batch.row_offsets
     xb = gen.bits(x)
     done, spent, rows, kv_bytes = [], 0.0, 0, 0
-    order = np.argsort(batch.chunk_lens, kind="stable")     # cheapest requests first
-    for i in order:
-        ids = torch.as_tensor(bt_host[i, :need[i]].astype(np.int64), device=pool.k_cache.device)
-        kb = gen.bits(pool.k_cache.index_select(0, ids)).copy()
-        vb = gen.bits(pool.v_cache.index_select(0, ids)).copy()
-        bt = np.arange(need[i], dtype=np.int32)[None]
-        xs = xb[off[i]:off[i + 1]]
-        t0 = time.perf_counter()
-        oracle.layer_step(cfg, W, kb, vb, bt, batch.context_lens[i:i + 1], batch.chunk_lens[i:i + 1], xs)
-        spent += time.perf_counter() - t0
-        done.append(int(i))
-        rows += int(batch.chunk_lens[i])
-        c, n = int(batch.context_lens[i]), int(batch.chunk_lens[i])
-        kv_bytes += (c + n) * shape.n_kv_heads * shape.head_dim * 4
-        if spent >= target_s:
-            break
-    # one oracle call per request re-reads the weights each time; count them once
-    gbps = (kv_bytes + shape.weight_bytes()) / spent / 1e9
+    # cheapest requests first; passes over the whole workload repeat until
+    # about target_s seconds of oracle time have been spent (at most 8 passes)
+    order = list(np.argsort(batch.chunk_lens, kind="stable"))
+    staged = {}
+    passes = 0
+    while spent < target_s and passes < 8:
+        for i in order:
+            if i not in staged:
+                ids = torch.as_tensor(bt_host[i, :need[i]].astype(np.int64), device=pool.k_cache.device)
+                staged[i] = (gen.bits(pool.k_cache.index_select(0, ids)).copy(),
+                             gen.bits(pool.v_cache.index_select(0, ids)).copy())
+            kb0, vb0 = staged[i]
+            kb, vb = kb0.copy(), vb0.copy()
+            bt = np.arange(need[i], dtype=np.int32)[None]
+            xs = xb[off[i]:off[i + 1]]
+            t0 = time.perf_counter()
+            oracle.layer_step(cfg, W, kb, vb, bt, batch.context_lens[i:i + 1], batch.chunk_lens[i:i + 1], xs)
+            spent += time.perf_counter() - t0
+            done.append(int(i))
+            rows += int(batch.chunk_lens[i])
+            c, n = int(batch.context_lens[i]), int(batch.chunk_lens[i])
+            kv_bytes += (c + n) * shape.n_kv_heads * shape.head_dim * 4
+            if spent >= target_s:
+                break
+        passes += 1
+    # algorithmic bytes of the step-equivalents done: the weights once per
+    # whole-workload step (rows / T of them) plus each request's K/V
+    gbps = (kv_bytes + shape.weight_bytes() * rows / batch.num_tokens) / spent / 1e9
     return {"value": round(gbps, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
             "tokens_per_s": round(rows / spent, 3), "seconds": round(spent, 2),
-            "sample": f"{len(done)} of {batch.num_seqs} requests ({rows} rows) of the same workload, fp32 numpy "
-                      f"oracle in batched mode, one request per call"}
+            "sample": f"{len(done)} request-steps ({rows} rows; {passes} pass(es) over the {batch.num_seqs} requests "
+                      f"of the same workload), fp32 numpy oracle in batched mode, one request per call"}
 
 
 # ----------------------------------------------------------------------------
