@@ -170,6 +170,7 @@ eb_status eb_op_rmsnorm(const eb_handle *h, const void *x, const void *gamma, vo
 
 /* out = epilogue(A W^T): A bf16 [M, K], W bf16 [N, K], out bf16 [M, N] (or
  * [M, N/2] for EB_EPI_SILU_MUL), residual bf16 [M, N] (EB_EPI_RESIDUAL only).
+ * N and K must be multiples of 8 (EB_ERR_CONFIG otherwise).
  * ws: device scratch of at least eb_op_gemm_workspace_bytes(M, N, K). */
 size_t eb_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
 eb_status eb_op_gemm(const void *A, const void *W, void *out, const void *residual, int32_t M, int32_t N,

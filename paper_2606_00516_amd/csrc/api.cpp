@@ -410,7 +410,7 @@ size_t eb_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
 eb_status eb_op_gemm(const void *A, const void *W, void *out, const void *residual, int32_t M, int32_t N, int32_t K,
                      eb_epilogue epi, void *ws, size_t ws_bytes, void *stream) {
   if (M < 0 || N <= 0 || K <= 0) return fail(EB_ERR_CONFIG, "M must be >= 0, N and K > 0");
-  if (K % 8) return fail(EB_ERR_CONFIG, "K must be a multiple of 8");
+  if (K % 8 || N % 8) return fail(EB_ERR_CONFIG, "N and K must be multiples of 8");
   if (epi != EB_EPI_STORE && epi != EB_EPI_RESIDUAL && epi != EB_EPI_SILU_MUL)
     return fail(EB_ERR_CONFIG, "unknown epilogue");
   if (epi == EB_EPI_SILU_MUL && N % 2) return fail(EB_ERR_CONFIG, "SiLU epilogue needs an even N");

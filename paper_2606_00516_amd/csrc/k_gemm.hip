@@ -41,153 +41,151 @@ __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)
 // ===========================================================================
 // skinny
 // ===========================================================================
-constexpr int SK_BN = 64;     // logical columns per block
-constexpr int SK_BM = 64;     // rows per block
+constexpr int SK_BN = 64;                // logical columns per block
+constexpr int SK_BM = 64;                // rows per block
+constexpr int SK_KC = 128;               // K per stage
+constexpr int SK_ROWB = SK_KC * 2 + 16;  // LDS bytes per tile row (padded)
+constexpr int SK_LDS = 2 * (SK_BN + SK_BM) * SK_ROWB;
 
-// One k-step (32 deep) of operand fragments for a 64 x 64 block: 4 row
-// blocks of A, 4 column blocks of W (16 x 32 each, 16 bytes per lane).
-struct SkinnyFrags {
-  u32x4_t a[4], b[4];
-};
-
-// Offsets are byte offsets into A / W; a fragment outside the matrix (row
-// past the end, k past K, k-step past the split) gets an offset past the
-// descriptor's range and loads as zero without memory traffic.
-__device__ __forceinline__ void skinny_load(SkinnyFrags &f, buf_rsrc_t ra, buf_rsrc_t rw, const uint32_t (&aoff)[4],
-                                            const uint32_t (&woff)[4], int ks, int ks_end, int lk, int K) {
-  const int k = ks * 32 + lk;
-  const bool kin = ks < ks_end && k < K;
-  const uint32_t kb = (uint32_t)k * 2u;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    f.a[i] = buf_ld_u32x4<0>(ra, (int)(kin ? aoff[i] + kb : 0xFFFFFFF0u));
-    f.b[i] = buf_ld_u32x4<kAuxNT>(rw, (int)(kin ? woff[i] + kb : 0xFFFFFFF0u));
-  }
-}
-
-__device__ __forceinline__ void skinny_mma(f32x4_t (&acc)[4][4], const SkinnyFrags &f) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(f.a[i], f.b[j], acc[i][j]);
-}
+// Logical column (0..63 in the block) of row j (0..15) of wave w's slice:
+// columns 8w..8w+7 and 32+8w..32+8w+7, so that a SiLU group's gate column
+// and its up partner (32 apart) land in the same wave.
+__device__ __forceinline__ int sk_col(int w, int j) { return j < 8 ? 8 * w + j : 32 + 8 * w + (j - 8); }
 
 __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict__ A, const uint16_t *__restrict__ W,
                                                      uint16_t *__restrict__ out, const uint16_t *__restrict__ res,
                                                      float *__restrict__ part, int M, int N, int K, int epi,
                                                      int ksteps_per_split) {
-  __shared__ float red[SK_BM][SK_BN + 4];
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  extern __shared__ __attribute__((aligned(16))) uint8_t sk_lds[];  // [2][64 W rows + 64 A rows][SK_ROWB]
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n0 = blockIdx.x * SK_BN;
   const int split = blockIdx.y;
   const int m0 = blockIdx.z * SK_BM;
-  const int nsteps = K / 32 + ((K & 31) ? 1 : 0);
-  const int ks_begin = split * ksteps_per_split;
-  const int ks_end = min(nsteps, ks_begin + ksteps_per_split);
-  const int lr = lane & 15, lk = (lane >> 4) * 8;
-  const int wrows = epi == EPI_SILU_MUL ? N : N;  // rows of W
-
-  // byte offsets of this lane's operand rows (0xFFFFFFF0 = none)
-  uint32_t aoff[4], woff[4];
-#pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    const int m = m0 + b * 16 + lr;
-    aoff[b] = m < M ? (uint32_t)m * (uint32_t)K * 2u : 0xFFFFFFF0u;
-    const int wr = w_row_of(n0 + b * 16 + lr, N, epi);
-    woff[b] = wr >= 0 ? (uint32_t)wr * (uint32_t)K * 2u : 0xFFFFFFF0u;
-  }
+  const int kbeg = split * ksteps_per_split * 32;
+  const int kend = min(K, kbeg + ksteps_per_split * 32);
+  const int nst = (kend - kbeg + SK_KC - 1) / SK_KC;
   const buf_rsrc_t ra = make_rsrc(A, (int)min((size_t)M * K * 2, (size_t)0x7FFFFFFF));
-  const buf_rsrc_t rw = make_rsrc(W, (int)min((size_t)wrows * K * 2, (size_t)0x7FFFFFFF));
-  f32x4_t acc[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const buf_rsrc_t rw = make_rsrc(W, (int)min((size_t)N * K * 2, (size_t)0x7FFFFFFF));
 
-  // wave w takes k-steps ks_begin + w, + 4, ...; four k-steps of fragments
-  // in flight, rotated in straight-line code (scheduling barriers keep each
-  // load group and each MFMA group in program order, so the wait before an
-  // MFMA group covers only its own fragments)
-  SkinnyFrags f0, f1, f2, f3;
-  const int ks0 = ks_begin + wave;
-  skinny_load(f0, ra, rw, aoff, woff, ks0, ks_end, lk, K);
-  __builtin_amdgcn_sched_barrier(0);
-  skinny_load(f1, ra, rw, aoff, woff, ks0 + 4, ks_end, lk, K);
-  __builtin_amdgcn_sched_barrier(0);
-  skinny_load(f2, ra, rw, aoff, woff, ks0 + 8, ks_end, lk, K);
-  __builtin_amdgcn_sched_barrier(0);
-  skinny_load(f3, ra, rw, aoff, woff, ks0 + 12, ks_end, lk, K);
-  __builtin_amdgcn_sched_barrier(0);
-  for (int ks = ks0; ks < ks_end; ks += 16) {
-    skinny_mma(acc, f0);
-    __builtin_amdgcn_sched_barrier(0);
-    skinny_load(f0, ra, rw, aoff, woff, ks + 16, ks_end, lk, K);
-    __builtin_amdgcn_sched_barrier(0);
-    skinny_mma(acc, f1);
-    __builtin_amdgcn_sched_barrier(0);
-    skinny_load(f1, ra, rw, aoff, woff, ks + 20, ks_end, lk, K);
-    __builtin_amdgcn_sched_barrier(0);
-    skinny_mma(acc, f2);
-    __builtin_amdgcn_sched_barrier(0);
-    skinny_load(f2, ra, rw, aoff, woff, ks + 24, ks_end, lk, K);
-    __builtin_amdgcn_sched_barrier(0);
-    skinny_mma(acc, f3);
-    __builtin_amdgcn_sched_barrier(0);
-    skinny_load(f3, ra, rw, aoff, woff, ks + 28, ks_end, lk, K);
-    __builtin_amdgcn_sched_barrier(0);
+  // Staging: thread t moves 16-byte chunk t % 16 of tile rows t / 16 + 16 j
+  // (each wave instruction reads 4 rows x 256 contiguous bytes); rows outside
+  // the operands, k past the block's range: offsets past the descriptor's
+  // range, loaded as zero without memory traffic.
+  const int ch = tid & 15, r0 = tid >> 4;
+  uint32_t woff[4], aoff[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int wr = w_row_of(n0 + r0 + 16 * j, N, epi);
+    woff[j] = wr >= 0 ? ((uint32_t)wr * (uint32_t)K + (uint32_t)(ch * 8)) * 2u : 0x80000000u;
+    const int m = m0 + r0 + 16 * j;
+    aoff[j] = m < M ? ((uint32_t)m * (uint32_t)K + (uint32_t)(ch * 8)) * 2u : 0x80000000u;
   }
-  // reduce the 4 waves' accumulators in LDS, in wave order (deterministic)
-  for (int w = 0; w < 4; ++w) {
-    if (wave == w) {
+  u32x4_t wa[4], aa[4], wb[4], ab[4];
+  auto gload = [&](int s, u32x4_t (&wr)[4], u32x4_t (&ar)[4]) {
+    const int k = kbeg + s * SK_KC + ch * 8;
+    const bool ok = s < nst && k < kend;
+    const uint32_t kb = (uint32_t)(kbeg + s * SK_KC) * 2u;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            float &dst = red[i * 16 + (lane >> 4) * 4 + e][j * 16 + lr];
-            dst = (w == 0) ? acc[i][j][e] : dst + acc[i][j][e];
-          }
+    for (int j = 0; j < 4; ++j) {
+      wr[j] = buf_ld_u32x4<kAuxNT>(rw, (int)(ok ? woff[j] + kb : 0x80000000u));
+      ar[j] = buf_ld_u32x4<0>(ra, (int)(ok ? aoff[j] + kb : 0x80000000u));
     }
+  };
+  auto swrite = [&](int buf, const u32x4_t (&wr)[4], const u32x4_t (&ar)[4]) {
+    uint8_t *b = sk_lds + buf * (SK_BN + SK_BM) * SK_ROWB;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      *reinterpret_cast<u32x4_t *>(b + (r0 + 16 * j) * SK_ROWB + ch * 16) = wr[j];
+      *reinterpret_cast<u32x4_t *>(b + (SK_BN + r0 + 16 * j) * SK_ROWB + ch * 16) = ar[j];
+    }
+  };
+  // Waves split the block's columns (16 each, see sk_col) and run the whole
+  // K range: the product is formed transposed, D[n][m] = W A^T, so a lane
+  // ends with 4 consecutive columns of one row.
+  f32x4_t acc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int lr = lane & 15, lg = lane >> 4;
+  const int my_wrow = sk_col(wave, lr);
+  auto compute = [&](int buf) {
+    const uint8_t *b = sk_lds + buf * (SK_BN + SK_BM) * SK_ROWB;
+#pragma unroll
+    for (int ks = 0; ks < SK_KC / 32; ++ks) {
+      const u32x4_t wf = *reinterpret_cast<const u32x4_t *>(b + my_wrow * SK_ROWB + (ks * 4 + lg) * 16);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const u32x4_t af = *reinterpret_cast<const u32x4_t *>(b + (SK_BN + i * 16 + lr) * SK_ROWB + (ks * 4 + lg) * 16);
+        acc[i] = mfma16x16x32(wf, af, acc[i]);
+      }
+    }
+  };
+  // Two stages in flight in registers, one in LDS: write stage s + 1 while
+  // stage s is consumed, one barrier per stage.
+  gload(0, wa, aa);
+  swrite(0, wa, aa);
+  gload(1, wa, aa);
+  gload(2, wb, ab);
+  __syncthreads();
+  for (int st = 0; st < nst; st += 2) {
+    compute(0);
+    swrite(1, wa, aa);
+    gload(st + 3, wa, aa);
+    __syncthreads();
+    if (st + 1 >= nst) break;
+    compute(1);
+    swrite(0, wb, ab);
+    gload(st + 4, wb, ab);
     __syncthreads();
   }
-  // 256 threads x 16 columns: row t/4, columns (t%4)*16 .. +16
-  const int r = threadIdx.x >> 2, cq = (threadIdx.x & 3) * 16;
-  const int m = m0 + r;
-  if (m >= M) return;
-  float v[16];
-#pragma unroll
-  for (int c = 0; c < 16; ++c) v[c] = red[r][cq + c];
+
+  // lane: rows m = m0 + 16 i + lr, logical columns c .. c+3 of the block,
+  // c = sk_col(wave, 4 lg)
+  const int c = sk_col(wave, 4 * lg);
   const int ncols = logical_cols(N, epi);
   if (part) {  // split-K partial, logical column space
-    float *dst = part + ((size_t)split * M + m) * ncols + n0 + cq;
 #pragma unroll
-    for (int c = 0; c < 16; ++c)
-      if (n0 + cq + c < ncols) dst[c] = v[c];
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + i * 16 + lr;
+      if (m < M && n0 + c < ncols)
+        *reinterpret_cast<f32x4_t *>(part + ((size_t)split * M + m) * ncols + n0 + c) = acc[i];
+    }
     return;
   }
   if (epi == EPI_SILU_MUL) {
-    // columns cq..cq+15 of the 64-group: gate if cq < 32, the matching up
-    // values sit in columns cq+32..; threads with cq < 32 finish the group
-    if (cq >= 32) return;
+    // up partners sit 2 lane groups away (xor 32); lanes with lg < 2 finish
     const int F = N >> 1;
-    const int f0 = (n0 >> 1) + cq;
+    const int f = (n0 >> 1) + 8 * wave + 4 * lg;
 #pragma unroll
-    for (int c = 0; c < 16; ++c) {
-      const float g = v[c];
-      const float u = red[r][cq + 32 + c];
-      if (f0 + c < F) out[(size_t)m * F + f0 + c] = (uint16_t)f32_to_bf16_bits(silu_f(g) * u);
+    for (int i = 0; i < 4; ++i) {
+      f32x4_t u;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) u[e] = shfl_xor_f32(acc[i][e], 32);
+      const int m = m0 + i * 16 + lr;
+      if (lg < 2 && m < M && f < F) {
+        u32x2_t w = {pack_bf16x2(silu_f(acc[i][0]) * u[0], silu_f(acc[i][1]) * u[1]),
+                     pack_bf16x2(silu_f(acc[i][2]) * u[2], silu_f(acc[i][3]) * u[3])};
+        *reinterpret_cast<u32x2_t *>(out + (size_t)m * F + f) = w;
+      }
     }
     return;
   }
+  const int n = n0 + c;
 #pragma unroll
-  for (int c = 0; c < 16; ++c) {
-    const int n = n0 + cq + c;
-    if (n < N) {
-      float x = v[c];
-      if (epi == EPI_RESIDUAL) x += bf16_to_f32(res[(size_t)m * N + n]);
-      out[(size_t)m * N + n] = (uint16_t)f32_to_bf16_bits(x);
+  for (int i = 0; i < 4; ++i) {
+    const int m = m0 + i * 16 + lr;
+    if (m < M && n < N) {
+      f32x4_t v = acc[i];
+      if (epi == EPI_RESIDUAL) {
+        const u32x2_t r = *reinterpret_cast<const u32x2_t *>(res + (size_t)m * N + n);
+        v[0] += bf16_lo(r[0]);
+        v[1] += bf16_hi(r[0]);
+        v[2] += bf16_lo(r[1]);
+        v[3] += bf16_hi(r[1]);
+      }
+      u32x2_t w = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+      *reinterpret_cast<u32x2_t *>(out + (size_t)m * N + n) = w;
     }
   }
 }
@@ -496,9 +494,9 @@ static int skinny_splits(int M, int N, int K) {
   const int mt = (M + SK_BM - 1) / SK_BM;
   const int nsteps = (K + 31) / 32;
   int splits = 1;
-  // aim for about 2 blocks per CU (512) without going below 16 k-steps per
-  // wave (the 4-deep operand ring needs a few trips to pay off)
-  while (ncol_tiles * mt * splits * 2 <= 512 && nsteps / (splits * 2) >= 4 * 16) splits *= 2;
+  // at least 384 blocks (the staging ring holds ~2 per CU) while each split
+  // keeps 4 or more stages of 128 in K
+  while (ncol_tiles * mt * splits < 384 && nsteps / (splits * 2) >= 16) splits *= 2;
   return splits;
 }
 
@@ -531,7 +529,7 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, 
     const int per = (nsteps + splits - 1) / splits;
     float *part = splits > 1 ? reinterpret_cast<float *>(ws) : nullptr;
     dim3 grid((ncols + SK_BN - 1) / SK_BN, splits, (M + SK_BM - 1) / SK_BM);
-    hipLaunchKernelGGL(k_gemm_skinny, grid, dim3(256), 0, st, A, W, out, res, part, M, N, K, epi, per);
+    hipLaunchKernelGGL(k_gemm_skinny, grid, dim3(256), SK_LDS, st, A, W, out, res, part, M, N, K, epi, per);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
     const int outc = epi == EPI_SILU_MUL ? N / 2 : N;
