@@ -44,7 +44,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="decode8b", choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "copy"])
+    ap.add_argument("--workload", default="decode8b", choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "decode70b", "copy"])
     ap.add_argument("--budgets", default="1024,2048", help="token budgets of the sweep (for alpha/beta fits)")
     ap.add_argument("--ctx16", action="store_true", help="sweep with every decode context = 16 instead")
     ap.add_argument("--r", type=float, default=0.5, help="decode share for mixed8b")
@@ -87,6 +87,9 @@ def workload(args):
     if args.workload == "prefill8b":
         return "llama3-8b-layer prefill EB: 8 prompts U[256,2048] capped at 8192 tokens", gen.L8B, \
             gen.batch_8b_prefill(), "prefill"
+    if args.workload == "decode70b":
+        return "llama3-70b-layer decode EB (one layer): 256 requests, ctx U[2048,16384], page 16", gen.L70B, \
+            gen.batch_70b_decode(), "decode"
     b = gen.batch_8b_mixed(args.r, args.budget)
     return (f"llama3-8b-layer MB: {args.budget}-token step, decode share {args.r:.2f}, decode ctx U[1024,8192], "
             f"chunks U[256,1024] with prefix U[0,2048]"), gen.L8B, b, "mixed"
@@ -345,7 +348,7 @@ def main():
     # HBM traffic from committed counter runs, only if the kernel is unchanged
     try:
         cnt = json.load(open(COUNTERS))
-        key = "decode_attention_8b" if mode == "decode" else None
+        key = {"decode8b": "decode_attention_8b"}.get(args.workload)
         ent = cnt.get(key) if key else None
         if ent and ent.get("source_sha") == sha_of(ATTN_SRC):
             roof["traffic"] = ent["bytes_per_dispatch"]

@@ -91,6 +91,15 @@ EB_DEV f32x4_t mfma16x16x32(u32x4_t a, u32x4_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
 }
 
+// D = A B + C on one 16x16x16 bf16 tile.  Operand layout (lane l):
+//   A: row l % 16, k = 4 (l / 16) .. + 3      B: col l % 16, same k
+//   C/D: as for the 16x16x32 tile
+EB_DEV f32x4_t mfma16x16x16(u32x2_t a, u32x2_t b, f32x4_t c) {
+  typedef short i16x4_t __attribute__((ext_vector_type(4)));
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, a), __builtin_bit_cast(i16x4_t, b), c,
+                                                    0, 0, 0);
+}
+
 // c + a.lo * b.lo + a.hi * b.hi on bf16 pairs packed in 32-bit words.  (The
 // words arrive as plain values: bit-casting a vector element in place has
 // been seen to read element 0 instead.)

@@ -174,6 +174,44 @@ __device__ __forceinline__ void decode_merge_lanes(float (&mrun)[G], float (&lru
   }
 }
 
+// Merge the per-wave softmax states a work unit left in LDS ([wave][h][HD]
+// outputs, then [wave][h][2] max and sum) and write the unit's result: the
+// final row (one split) or a partial for the combine.
+template <int HD, int G, int NW>
+__device__ __forceinline__ void decode_merge_waves(const float *lds, int row, int kh, int nq, int nkv, int item,
+                                                   int nsplit, uint16_t *__restrict__ out, float *__restrict__ part_o,
+                                                   float *__restrict__ part_ml) {
+  const float *lo_ = lds;
+  const float *lml = lds + NW * G * HD;
+  __syncthreads();
+  for (int e = threadIdx.x; e < G * HD; e += blockDim.x) {
+    const int h = e / HD, dim = e - h * HD;
+    float mx = kNegInf;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) mx = fmaxf(mx, lml[(w * G + h) * 2]);
+    float L = 0.f, O = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float mw = lml[(w * G + h) * 2];
+      const float a = (mw == kNegInf) ? 0.f : fast_exp2(mw - mx);
+      L += a * lml[(w * G + h) * 2 + 1];
+      O += a * lo_[(w * G + h) * HD + dim];
+    }
+    const int qh = kh * G + h;
+    if (nsplit == 1) {
+      out[(size_t)row * nq * HD + qh * HD + dim] = (uint16_t)f32_to_bf16_bits(O / L);
+    } else {
+      const size_t slot = ((size_t)item * nkv + kh) * G + h;
+      part_o[slot * HD + dim] = O;
+      if (dim == 0) {
+        part_ml[slot * 2] = mx;
+        part_ml[slot * 2 + 1] = L;
+      }
+    }
+  }
+  __syncthreads();
+}
+
 template <int HD, int G>
 __device__ __forceinline__ void decode_load_q(const uint16_t *__restrict__ qkv, int cols, int row, int kh, int lane,
                                               u32x4_t (&qw)[G], float (&mrun)[G], float (&lrun)[G],
@@ -188,6 +226,323 @@ __device__ __forceinline__ void decode_load_q(const uint16_t *__restrict__ qkv, 
 #pragma unroll
     for (int i = 0; i < 8; ++i) o[h][i] = 0.f;
   }
+}
+
+// ---------------------------------------------------------------------------
+// Decode on the matrix cores, used for the larger query groups (G >= 4),
+// where the per-lane form above spends most of its issue slots on redundant
+// score reductions and exponentials.  Per wavefront and pair of pages (A, B)
+// of one kv head:
+//   S^T[token][head] = K Q^T     A = K in its cache layout (lane l: token
+//                                l % 16, dims 8 (l / 16) + 32 ks ..), B = Q^T
+//   V pieces         = V Sel_h   Sel_h is the 0/1 matrix that keeps dims
+//                                16 h .. 16 h + 15 of a 32-dim chunk, so the
+//                                product is exact and leaves lane l with 4
+//                                consecutive tokens of one dim
+//   O^T[dim][head]  += V^T P^T   keys ordered (A tokens 4 (l/16) .. + 3, B
+//                                tokens 4 (l/16) .. + 3) in both operands
+// The 16 MFMA columns are query heads (G of them used): lane l serves head
+// l % 16 and holds 4 tokens of each page's scores, so only the running max
+// crosses lanes (two steps).  P enters the product rounded to bf16; the sum
+// l is kept in fp32.
+// ---------------------------------------------------------------------------
+template <int G>
+constexpr bool kDecodeMfma = G >= 4;
+
+// Page blocks reach LDS by direct loads (no registers): each 16-byte chunk
+// of a block goes to a position swizzled by its token, so that every load
+// instruction still covers whole 256-byte token rows of HBM and the MFMA
+// operand reads (16 tokens x one chunk per quarter-wave) hit 16 different
+// bank groups.  A wavefront owns four page slots (K block then V block)
+// and keeps three pages in flight while it works on the fourth.
+template <int HD>
+struct MdecTraits {
+  static constexpr int BLK = kPageSize * HD * 2;  // bytes of one (page, kv head) block
+  static constexpr int SLOT = 2 * BLK;            // K block, then V block
+  static constexpr int NDMA = BLK / 1024;         // 1 KiB load instructions per block
+  static constexpr int ROW = HD * 2;              // bytes per token row
+};
+
+template <int HD>
+EB_DEV int mdec_swz(int t) {
+  return HD == 128 ? (t & 15) : ((t >> 1) & 7);
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// Start the loads of page p's K and V blocks into a slot; slots at or past
+// k1 (and pages past the end or with a bad table entry) land as zeros
+// without memory traffic, so cache poison never reaches the products.
+template <int HD>
+__device__ __forceinline__ void mdec_dma_page(uint8_t *slot, const uint32_t *goff, const KV kv,
+                                              const int32_t *bt, int p, int pg1, int k1, int nkv, int kh) {
+  using Tr = MdecTraits<HD>;
+  const int phys = p < pg1 ? bt[p] : -1;
+  const int nvalid = min(max(k1 - p * kPageSize, 0), kPageSize);
+  const bool ok = phys >= 0 && phys < kv.num_pages;
+  const size_t off = ok ? ((size_t)phys * nkv + kh) * kPageSize * HD : 0;
+  // wave-uniform by construction; said so, so the descriptor stays scalar
+  const int bytes = __builtin_amdgcn_readfirstlane(ok ? nvalid * Tr::ROW : 0);
+  const buf_rsrc_t rk = make_rsrc(kv.k + off, bytes);
+  const buf_rsrc_t rv = make_rsrc(kv.v + off, bytes);
+#pragma unroll
+  for (int i = 0; i < Tr::NDMA; ++i) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void_t *)(slot + i * 1024), 16, goff[i], 0, 0, kAuxNT);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void_t *)(slot + Tr::BLK + i * 1024), 16, goff[i], 0, 0,
+                                             kAuxNT);
+  }
+}
+
+// Upper halves of two fp32 values that hold bf16 numbers exactly, packed.
+EB_DEV uint32_t bf16_pair_exact(float lo, float hi) {
+  return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
+}
+
+// Round two fp32 values to bf16 (nearest even) and pack them.
+EB_DEV uint32_t bf16_pair_rne(float lo, float hi) {
+  typedef float f32x2_v __attribute__((ext_vector_type(2)));
+  const f32x2_v f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
+}
+
+// Online-softmax update with the page in a slot; the page holds at least one
+// key below k1, so the new running max is finite.
+template <int HD>
+__device__ __forceinline__ void mdec_page_update(const uint8_t *slot, const u32x4_t (&qb)[HD / 32],
+                                                 const u32x4_t (&sel)[2], float &mrun, float &lsum,
+                                                 f32x4_t (&oacc)[HD / 16], int p, int k1, int lane, float qscale) {
+  using Tr = MdecTraits<HD>;
+  constexpr int NKS = HD / 32;
+  const int r = lane & 15, g = lane >> 4;
+  const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
+  const uint8_t *rowp = slot + r * Tr::ROW;
+  const int sw = mdec_swz<HD>(r);
+  f32x4_t sa = zero;
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    const u32x4_t a = *reinterpret_cast<const u32x4_t *>(rowp + (((g + 4 * ks) ^ sw) << 4));
+    sa = mfma16x16x32(a, qb[ks], sa);
+  }
+  float s[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) s[j] = sa[j] * qscale;
+  if (p * kPageSize + kPageSize > k1) {  // wave-uniform: the page reaches past the last key
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (p * kPageSize + 4 * g + j >= k1) s[j] = kNegInf;
+  }
+  float mx = fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3]));
+  mx = fmaxf(mx, shfl_xor_f32(mx, 16));
+  mx = fmaxf(mx, shfl_xor_f32(mx, 32));
+  const float mnew = fmaxf(mrun, mx);
+  const float alpha = (mrun == kNegInf) ? 0.f : fast_exp2(mrun - mnew);
+  float pr[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) pr[j] = fast_exp2(s[j] - mnew);
+  lsum = lsum * alpha + ((pr[0] + pr[1]) + (pr[2] + pr[3]));
+  mrun = mnew;
+  // P^T (keys 4 g .. 4 g + 3 of this lane's head) as the B operand of the
+  // 16x16x16 product
+  const u32x2_t pt = {bf16_pair_rne(pr[0], pr[1]), bf16_pair_rne(pr[2], pr[3])};
+#pragma unroll
+  for (int ks = 0; ks < NKS; ++ks) {
+    const u32x4_t vv = *reinterpret_cast<const u32x4_t *>(rowp + Tr::BLK + (((g + 4 * ks) ^ sw) << 4));
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const f32x4_t t = mfma16x16x32(vv, sel[h], zero);  // V[4 g + j][32 ks + 16 h + r]
+      const u32x2_t a = {bf16_pair_exact(t[0], t[1]), bf16_pair_exact(t[2], t[3])};
+      oacc[2 * ks + h] = mfma16x16x16(a, pt, oacc[2 * ks + h] * alpha);
+    }
+  }
+}
+
+// Stream pages p_first, p_first + stride, .. (< pg1) through the wave's
+// NSLOT slots (NSLOT - 1 pages in flight while one is consumed).  Loads of
+// pages past the end cost no memory traffic; every load has landed when
+// this returns.
+template <int HD, int NSLOT>
+__device__ __forceinline__ void mdec_stream(uint8_t *s0, uint8_t *s1, uint8_t *s2, uint8_t *s3, const KV kv,
+                                            const int32_t *bt, int p_first, int stride, int pg1, int k1, int nkv,
+                                            int kh, int lane, float qscale, const u32x4_t (&qb)[HD / 32],
+                                            const u32x4_t (&sel)[2], float &mrun, float &lsum,
+                                            f32x4_t (&oacc)[HD / 16]) {
+  using Tr = MdecTraits<HD>;
+  static_assert(NSLOT >= 2 && NSLOT <= 4, "ring depth");
+  uint32_t goff[Tr::NDMA];
+#pragma unroll
+  for (int i = 0; i < Tr::NDMA; ++i) {
+    const int e = i * 1024 + lane * 16;  // byte of the slot block this lane fills
+    const int t = e / Tr::ROW, u = (e % Tr::ROW) >> 4;
+    goff[i] = (uint32_t)(t * Tr::ROW + ((u ^ mdec_swz<HD>(t)) << 4));
+  }
+#define EB_DMA(S_, P_)                                                  \
+  mdec_dma_page<HD>(S_, goff, kv, bt, P_, pg1, k1, nkv, kh);            \
+  __builtin_amdgcn_sched_barrier(0);
+#define EB_UPD(S_, P_)                                                                  \
+  if ((P_) < pg1) mdec_page_update<HD>(S_, qb, sel, mrun, lsum, oacc, P_, k1, lane, qscale); \
+  __builtin_amdgcn_sched_barrier(0);
+  if constexpr (NSLOT == 2) {
+    (void)s2;
+    (void)s3;
+    EB_DMA(s0, p_first)
+    for (int p = p_first; p < pg1; p += 2 * stride) {
+      EB_DMA(s1, p + stride)
+      EB_UPD(s0, p)
+      EB_DMA(s0, p + 2 * stride)
+      EB_UPD(s1, p + stride)
+    }
+  } else if constexpr (NSLOT == 3) {
+    (void)s3;
+    EB_DMA(s0, p_first)
+    EB_DMA(s1, p_first + stride)
+    for (int p = p_first; p < pg1; p += 3 * stride) {
+      EB_DMA(s2, p + 2 * stride)
+      EB_UPD(s0, p)
+      EB_DMA(s0, p + 3 * stride)
+      EB_UPD(s1, p + stride)
+      EB_DMA(s1, p + 4 * stride)
+      EB_UPD(s2, p + 2 * stride)
+    }
+  } else {
+    EB_DMA(s0, p_first)
+    EB_DMA(s1, p_first + stride)
+    EB_DMA(s2, p_first + 2 * stride)
+    for (int p = p_first; p < pg1; p += 4 * stride) {
+      EB_DMA(s3, p + 3 * stride)
+      EB_UPD(s0, p)
+      EB_DMA(s0, p + 4 * stride)
+      EB_UPD(s1, p + stride)
+      EB_DMA(s1, p + 5 * stride)
+      EB_UPD(s2, p + 2 * stride)
+      EB_DMA(s2, p + 6 * stride)
+      EB_UPD(s3, p + 3 * stride)
+    }
+  }
+#undef EB_DMA
+#undef EB_UPD
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// q of the G heads of kv head kh as the B operand (columns >= G zero), the
+// two selection matrices, and the empty softmax state.
+template <int HD, int G>
+__device__ __forceinline__ void mdec_init(const uint16_t *__restrict__ qkv, int cols, int row, int kh, int lane,
+                                          u32x4_t (&qb)[HD / 32], u32x4_t (&sel)[2], float &mrun, float &lsum,
+                                          f32x4_t (&oacc)[HD / 16]) {
+  const int c = lane & 15, g = lane >> 4;
+  const bool live = c < G;
+  const uint16_t *src = qkv + (size_t)row * cols + (kh * G + (live ? c : 0)) * HD + g * 8;
+#pragma unroll
+  for (int ks = 0; ks < HD / 32; ++ks) {
+    const u32x4_t v = ld_u32x4(src + ks * 32);
+    qb[ks] = live ? v : u32x4_t{0u, 0u, 0u, 0u};
+  }
+  // Sel_h[k][c] = 1 where k = c + 16 h: lane (c, g) holds k = 8 g .. 8 g + 7
+  const uint32_t one = (c & 1) ? 0x3F800000u : 0x3F80u;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const bool hit = g == 2 * h + (c >> 3);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sel[h][e] = (hit && e == ((c & 7) >> 1)) ? one : 0u;
+  }
+  mrun = kNegInf;
+  lsum = 0.f;
+#pragma unroll
+  for (int ob = 0; ob < HD / 16; ++ob) oacc[ob] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+}
+
+// One decode work unit on the matrix cores (same units as decode_item),
+// run by NW wavefronts with NSLOT-deep page rings.  l0..l3: the block's
+// slot arrays (NW slots each; the first NSLOT are used); the cross-wave
+// merge reuses l0 once every wave has finished streaming.
+template <int HD, int NW, int NSLOT>
+struct MdecBlock {
+  static constexpr int SLOT_ARRAY = NW * MdecTraits<HD>::SLOT;  // bytes per slot array
+};
+
+template <int HD, int G, int NW, int NSLOT>
+__device__ __forceinline__ void decode_item_mfma(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
+                                                 const DevMeta md, int unit, uint16_t *__restrict__ out,
+                                                 float *__restrict__ part_o, float *__restrict__ part_ml, uint8_t *l0,
+                                                 uint8_t *l1, uint8_t *l2, uint8_t *l3) {
+  constexpr int SLOT = MdecTraits<HD>::SLOT;
+  constexpr int SPLIT = kDecodePagesPerSplit * kPageSize;
+  constexpr int NOB = HD / 16;
+  static_assert(DecodeTraits<HD, G, NW>::LDS_BYTES <= MdecBlock<HD, NW, NSLOT>::SLOT_ARRAY, "merge area");
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int cols = (nq + 2 * nkv) * HD;
+  const float qscale = kLog2e / sqrtf((float)HD);
+  const int c = lane & 15, g = lane >> 4;
+  uint8_t *w0 = l0 + wave * SLOT, *w1 = l1 + wave * SLOT, *w2 = l2 + wave * SLOT, *w3 = l3 + wave * SLOT;
+
+  int lo = 0, hi = md.n_dec - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (md.dec_unit_off[mid] <= unit) lo = mid; else hi = mid - 1;
+  }
+  const int d = lo;
+  const int local = unit - md.dec_unit_off[d];
+  const int seq = md.dec_seq[d];
+  const int nkeys = md.seq_ctx[seq] + 1;
+  const int row = md.seq_row[seq];
+  const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
+  u32x4_t qb[HD / 32], sel[2];
+  float mrun, lsum;
+  f32x4_t oacc[NOB];
+
+  if (nkeys <= kShortDecodeKeys) {
+    // one wavefront per kv head, all its pages, output written directly
+    for (int hw = wave; hw < kShortDecodeHeads; hw += NW) {
+      const int kh = local * kShortDecodeHeads + hw;
+      if (kh >= nkv) break;
+      mdec_init<HD, G>(qkv, cols, row, kh, lane, qb, sel, mrun, lsum, oacc);
+      mdec_stream<HD, NSLOT>(w0, w1, w2, w3, kv, bt, 0, 1, (nkeys + kPageSize - 1) / kPageSize, nkeys, nkv, kh, lane,
+                             qscale, qb, sel, mrun, lsum, oacc);
+      lsum += shfl_xor_f32(lsum, 16);
+      lsum += shfl_xor_f32(lsum, 32);
+      if (c < G) {
+        const float inv = 1.0f / lsum;
+        uint16_t *dst = out + (size_t)row * nq * HD + (kh * G + c) * HD + g * 4;
+#pragma unroll
+        for (int ob = 0; ob < NOB; ++ob) {
+          const u32x2_t w = {pack_bf16x2(oacc[ob][0] * inv, oacc[ob][1] * inv),
+                             pack_bf16x2(oacc[ob][2] * inv, oacc[ob][3] * inv)};
+          *reinterpret_cast<u32x2_t *>(dst + ob * 16) = w;
+        }
+      }
+    }
+    return;
+  }
+
+  const int split = local / nkv, kh = local - split * nkv;
+  const int item = md.dec_split_off[d] + split;
+  const int nsplit = md.dec_split_off[d + 1] - md.dec_split_off[d];
+  const int k0 = split * SPLIT;
+  const int k1 = min(nkeys, k0 + SPLIT);
+  const int pg0 = k0 / kPageSize, pg1 = (k1 + kPageSize - 1) / kPageSize;
+  mdec_init<HD, G>(qkv, cols, row, kh, lane, qb, sel, mrun, lsum, oacc);
+  mdec_stream<HD, NSLOT>(w0, w1, w2, w3, kv, bt, pg0 + wave, NW, pg1, k1, nkv, kh, lane, qscale, qb, sel, mrun, lsum,
+                         oacc);
+  lsum += shfl_xor_f32(lsum, 16);
+  lsum += shfl_xor_f32(lsum, 32);
+  // across the NW waves through LDS (reusing l0 once every wave is done with
+  // its slots): [wave][h][HD] outputs, then [wave][h][2]
+  float *merge = reinterpret_cast<float *>(l0);
+  __syncthreads();
+  if (c < G) {
+    float *o_ = merge + (wave * G + c) * HD + g * 4;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o_[ob * 16 + j] = oacc[ob][j];
+    if (g == 0) {
+      float *ml = merge + NW * G * HD + (wave * G + c) * 2;
+      ml[0] = mrun;
+      ml[1] = lsum;
+    }
+  }
+  decode_merge_waves<HD, G, NW>(merge, row, kh, nq, nkv, item, nsplit, out, part_o, part_ml);
 }
 
 // One decode work unit.  Unit u of decode request d (binary search over the
@@ -269,33 +624,7 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
       }
     }
   }
-  __syncthreads();
-  for (int e = threadIdx.x; e < G * HD; e += blockDim.x) {
-    const int h = e / HD, dim = e - h * HD;
-    float mx = kNegInf;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) mx = fmaxf(mx, lml[(w * G + h) * 2]);
-    float L = 0.f, O = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const float mw = lml[(w * G + h) * 2];
-      const float a = (mw == kNegInf) ? 0.f : fast_exp2(mw - mx);
-      L += a * lml[(w * G + h) * 2 + 1];
-      O += a * lo_[(w * G + h) * HD + dim];
-    }
-    const int qh = kh * G + h;
-    if (nsplit == 1) {
-      out[(size_t)row * nq * HD + qh * HD + dim] = (uint16_t)f32_to_bf16_bits(O / L);
-    } else {
-      const size_t slot = ((size_t)item * nkv + kh) * G + h;
-      part_o[slot * HD + dim] = O;
-      if (dim == 0) {
-        part_ml[slot * 2] = mx;
-        part_ml[slot * 2 + 1] = L;
-      }
-    }
-  }
-  __syncthreads();
+  decode_merge_waves<HD, G, NW>(lds, row, kh, nq, nkv, item, nsplit, out, part_o, part_ml);
 }
 
 // Combine the splits of one decode request for one query head:
@@ -352,7 +681,9 @@ struct PrefillTraits {
   static constexpr int KT = 64;                  // keys per tile
   static constexpr int KS_STRIDE = HD + 8;       // bf16 elements per K row in LDS
   static constexpr int VT_STRIDE = KT + 4;       // bf16 elements per V^T row in LDS
-  static constexpr int LDS_BYTES = (KT * KS_STRIDE + HD * VT_STRIDE) * 2;
+  static constexpr int KS_BYTES = KT * KS_STRIDE * 2;  // K tile
+  static constexpr int VT_BYTES = HD * VT_STRIDE * 2;  // V^T tile
+  static constexpr int LDS_BYTES = KS_BYTES + VT_BYTES;
   static constexpr int KCH = KT * (HD / 8);      // 16-byte K chunks per tile
   static constexpr int VCH = (KT / 2) * (HD / 8);  // (key pair, 8 dims) V units per tile
   static constexpr int KPT = (KCH + NW * 64 - 1) / (NW * 64);  // per thread
@@ -363,7 +694,7 @@ struct PrefillTraits {
 template <int HD, int G, int NW>
 __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
                                              const DevMeta md, int tile, int kh, uint16_t *__restrict__ out,
-                                             uint16_t *lds) {
+                                             uint16_t *Ks, uint16_t *Vt) {
   using Tr = PrefillTraits<HD, G, NW>;
   constexpr int BQ = Tr::BQ, RB = Tr::RB, KT = Tr::KT, KSS = Tr::KS_STRIDE, VTS = Tr::VT_STRIDE;
   constexpr int KCH = Tr::KCH, VCH = Tr::VCH, KPT = Tr::KPT, VPT = Tr::VPT;
@@ -385,8 +716,6 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
   const int klen = c + n;                   // keys that exist
   const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
   const int npages = (klen + kPageSize - 1) / kPageSize;
-  uint16_t *Ks = lds;
-  uint16_t *Vt = lds + KT * KSS;
   const float qscale = kLog2e / sqrtf((float)HD);
   const int lq = lane & 15;   // query column of this lane inside a 16-row block
   const int lg = lane >> 4;   // lane group 0..3
@@ -564,17 +893,38 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
 // kernels
 // ---------------------------------------------------------------------------
 template <int HD, int G>
-__global__ __launch_bounds__(256) void k_decode(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
-                                                float *part_o, float *part_ml) {
+__global__ __launch_bounds__(256, 2) void k_decode(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
+                                                   uint16_t *out, float *part_o, float *part_ml) {
   __shared__ float lds[DecodeTraits<HD, G, 4>::LDS_BYTES / 4];
   decode_item<HD, G, 4>(qkv, nq, nkv, kv, md, blockIdx.x, out, part_o, part_ml, lds);
+}
+
+// The matrix-core decode keeps its page slots in separate LDS arrays, so the
+// compiler's wait before reading one slot covers only that slot's loads.
+// Decode-only launch: kDecWaves wavefronts per block, kDecSlots-deep rings.
+constexpr int kDecWaves = 4, kDecSlots = 2;
+#define EB_MDEC_LDS(HD_, NW_, NSLOT_)                                                                 \
+  __shared__ __attribute__((aligned(16))) uint8_t l0[MdecBlock<HD_, NW_, NSLOT_>::SLOT_ARRAY];          \
+  __shared__ __attribute__((aligned(16))) uint8_t l1[MdecBlock<HD_, NW_, NSLOT_>::SLOT_ARRAY];          \
+  __shared__ __attribute__((aligned(16))) uint8_t l2[NSLOT_ > 2 ? MdecBlock<HD_, NW_, NSLOT_>::SLOT_ARRAY : 16]; \
+  __shared__ __attribute__((aligned(16))) uint8_t l3[NSLOT_ > 3 ? MdecBlock<HD_, NW_, NSLOT_>::SLOT_ARRAY : 16];
+
+template <int HD, int G>
+__global__ __launch_bounds__(64 * kDecWaves) void k_decode_mfma(const uint16_t *qkv, int nq, int nkv, KV kv,
+                                                                DevMeta md, uint16_t *out, float *part_o,
+                                                                float *part_ml) {
+  EB_MDEC_LDS(HD, kDecWaves, kDecSlots)
+  decode_item_mfma<HD, G, kDecWaves, kDecSlots>(qkv, nq, nkv, kv, md, blockIdx.x, out, part_o, part_ml, l0, l1, l2,
+                                                l3);
 }
 
 template <int HD, int G>
 __global__ __launch_bounds__(512) void k_prefill(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
                                                  uint16_t *out) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[PrefillTraits<HD, G, 8>::LDS_BYTES / 2];
-  prefill_item<HD, G, 8>(qkv, nq, nkv, kv, md, blockIdx.x / nkv, blockIdx.x % nkv, out, lds);
+  using Tr = PrefillTraits<HD, G, 8>;
+  __shared__ __attribute__((aligned(16))) uint16_t lds[Tr::LDS_BYTES / 2];
+  prefill_item<HD, G, 8>(qkv, nq, nkv, kv, md, blockIdx.x / nkv, blockIdx.x % nkv, out, lds,
+                         lds + Tr::KS_BYTES / 2);
 }
 
 // One grid for a mixed step: items [0, n_tiles) are prefill tiles (longest
@@ -583,15 +933,36 @@ __global__ __launch_bounds__(512) void k_prefill(const uint16_t *qkv, int nq, in
 template <int HD, int G>
 __global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
                                                float *part_o, float *part_ml) {
-  constexpr int PB = PrefillTraits<HD, G, 4>::LDS_BYTES, DB = DecodeTraits<HD, G, 4>::LDS_BYTES;
+  using Tr = PrefillTraits<HD, G, 4>;
+  constexpr int PB = Tr::LDS_BYTES, DB = DecodeTraits<HD, G, 4>::LDS_BYTES;
   __shared__ __attribute__((aligned(16))) uint16_t lds[(PB > DB ? PB : DB) / 2];
   const int b = blockIdx.x;
   if (b < md.n_tiles * nkv)
-    prefill_item<HD, G, 4>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, lds);
+    prefill_item<HD, G, 4>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, lds, lds + Tr::KS_BYTES / 2);
   else
     decode_item<HD, G, 4>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml,
                           reinterpret_cast<float *>(lds));
 }
+
+// The same with matrix-core decode items; prefill tiles borrow two of the
+// page-slot arrays.
+template <int HD, int G>
+__global__ __launch_bounds__(256) void k_mixed_mfma(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
+                                                    uint16_t *out, float *part_o, float *part_ml) {
+  using Tr = PrefillTraits<HD, G, 4>;
+  constexpr int MS = 2;  // ring depth of decode items in the mixed launch
+  static_assert(Tr::KS_BYTES <= MdecBlock<HD, 4, MS>::SLOT_ARRAY && Tr::VT_BYTES <= MdecBlock<HD, 4, MS>::SLOT_ARRAY,
+                "LDS");
+  EB_MDEC_LDS(HD, 4, MS)
+  const int b = blockIdx.x;
+  if (b < md.n_tiles * nkv)
+    prefill_item<HD, G, 4>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, reinterpret_cast<uint16_t *>(l0),
+                           reinterpret_cast<uint16_t *>(l1));
+  else
+    decode_item_mfma<HD, G, 4, MS>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml, l0, l1, l2,
+                                   l3);
+}
+#undef EB_MDEC_LDS
 
 template <int HD, int G>
 static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const KV &kv, const DevMeta &m,
@@ -602,14 +973,23 @@ static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const 
   if (!(parts & 1)) {
     // combine only
   } else if (kind == 2 && has_dec && has_pf) {
-    hipLaunchKernelGGL((k_mixed<HD, G>), dim3(m.n_tiles * nkv + m.total_units), dim3(256), 0, st, qkv, nq, nkv, kv,
-                       m, out, part_o, part_ml);
+    if constexpr (kDecodeMfma<G>)
+      hipLaunchKernelGGL((k_mixed_mfma<HD, G>), dim3(m.n_tiles * nkv + m.total_units), dim3(256), 0, st, qkv, nq,
+                         nkv, kv, m, out, part_o, part_ml);
+    else
+      hipLaunchKernelGGL((k_mixed<HD, G>), dim3(m.n_tiles * nkv + m.total_units), dim3(256), 0, st, qkv, nq, nkv,
+                         kv, m, out, part_o, part_ml);
   } else {
     if (has_pf)
       hipLaunchKernelGGL((k_prefill<HD, G>), dim3(m.n_tiles * nkv), dim3(512), 0, st, qkv, nq, nkv, kv, m, out);
-    if (has_dec)
-      hipLaunchKernelGGL((k_decode<HD, G>), dim3(m.total_units), dim3(256), 0, st, qkv, nq, nkv, kv, m, out,
-                         part_o, part_ml);
+    if (has_dec) {
+      if constexpr (kDecodeMfma<G>)
+        hipLaunchKernelGGL((k_decode_mfma<HD, G>), dim3(m.total_units), dim3(64 * kDecWaves), 0, st, qkv, nq, nkv,
+                           kv, m, out, part_o, part_ml);
+      else
+        hipLaunchKernelGGL((k_decode<HD, G>), dim3(m.total_units), dim3(256), 0, st, qkv, nq, nkv, kv, m, out,
+                           part_o, part_ml);
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -2,11 +2,13 @@
 // W [N, K] weights, both K-contiguous bf16, fp32 accumulation on the
 // 16x16x32 bf16 MFMA.
 //
-//  * skinny: M <= 64 rows per tile (decode-sized batches).  The product is
-//    bound by streaming W from HBM once, so each wavefront loads MFMA operand
-//    fragments straight from global memory (no LDS staging); the 4 waves of a
-//    block split K and reduce through LDS; blocks may further split K, with a
-//    small reduction kernel applying the epilogue.
+//  * skinny: decode-sized batches (up to 256 rows, 64-row x 64-column
+//    tiles).  The product is bound by streaming W from HBM once: tiles stage
+//    W and A through LDS in 128-wide K slices read as whole 256-byte rows,
+//    the 4 waves of a block split the tile's columns, the row blocks of a
+//    column tile run side by side on one XCD so W comes from HBM once, and
+//    blocks may further split K, with a small reduction kernel applying the
+//    epilogue.
 //  * tiled: larger M.  128x128 output tiles, K tiles of 64 double-buffered in
 //    LDS, 4 waves each owning a 64x64 sub-tile.
 //
@@ -55,14 +57,19 @@ __device__ __forceinline__ int sk_col(int w, int j) { return j < 8 ? 8 * w + j :
 __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict__ A, const uint16_t *__restrict__ W,
                                                      uint16_t *__restrict__ out, const uint16_t *__restrict__ res,
                                                      float *__restrict__ part, int M, int N, int K, int epi,
-                                                     int ksteps_per_split) {
+                                                     int ksteps_per_split, int tiles, int mt, int per_xcd) {
   extern __shared__ __attribute__((aligned(16))) uint8_t sk_lds[];  // [2][64 W rows + 64 A rows][SK_ROWB]
+  // block b takes tile (b % 8) * per_xcd + b / 8, so each XCD walks its own
+  // contiguous tile range; the mt row blocks of one column tile are
+  // neighbours there and share the W tile through that XCD's L2
+  const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (t >= tiles) return;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n0 = blockIdx.x * SK_BN;
+  const int n0 = (t / mt) * SK_BN;
   const int split = blockIdx.y;
-  const int m0 = blockIdx.z * SK_BM;
+  const int m0 = (t % mt) * SK_BM;
   const int kbeg = split * ksteps_per_split * 32;
   const int kend = min(K, kbeg + ksteps_per_split * 32);
   const int nst = (kend - kbeg + SK_KC - 1) / SK_KC;
@@ -489,6 +496,10 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
 // ===========================================================================
 // planning and launch
 // ===========================================================================
+// Row counts up to this use the skinny kernel (weight streaming: the row
+// blocks of a column tile run side by side and read W once from HBM).
+constexpr int kSkinnyMaxRows = 256;
+
 static int skinny_splits(int M, int N, int K) {
   const int ncol_tiles = (N + SK_BN - 1) / SK_BN;
   const int mt = (M + SK_BM - 1) / SK_BM;
@@ -502,20 +513,22 @@ static int skinny_splits(int M, int N, int K) {
 
 GemmPlan plan_gemm(int M, int N, int K, int epi) {
   GemmPlan p{};
-  if (M <= 64) {
+  const int ncols = logical_cols(N, epi);
+  const bool fits = (size_t)M * K * 2 < ((size_t)1 << 31) && (size_t)N * K * 2 < ((size_t)1 << 31);
+  // 256 x 256 tiles once the grid covers at least half the CUs
+  const long big_tiles = (long)((M + BG_BM - 1) / BG_BM) * ((ncols + BG_BN - 1) / BG_BN);
+  if (K % BG_BK == 0 && N % 8 == 0 && fits && M >= 256 && big_tiles >= 128) {
+    p.kind = 2;
+  } else if (M <= kSkinnyMaxRows) {
     p.kind = 0;
-    const int ncols = logical_cols(N, epi);
     p.splits = skinny_splits(M, ncols, K);
     p.ws_bytes = p.splits > 1 ? (size_t)p.splits * M * ncols * sizeof(float) : 0;
+    return p;
   } else {
-    const int ncols = logical_cols(N, epi);
-    const bool fits = (size_t)M * K * 2 < ((size_t)1 << 31) && (size_t)N * K * 2 < ((size_t)1 << 31);
-    // 256 x 256 tiles once the grid covers at least half the CUs
-    const long big_tiles = (long)((M + BG_BM - 1) / BG_BM) * ((ncols + BG_BN - 1) / BG_BN);
-    p.kind = (K % BG_BK == 0 && N % 8 == 0 && fits && M >= 256 && big_tiles >= 128) ? 2 : 1;
-    p.splits = 1;
-    p.ws_bytes = 0;
+    p.kind = 1;
   }
+  p.splits = 1;
+  p.ws_bytes = 0;
   return p;
 }
 
@@ -528,8 +541,12 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, 
     const int splits = p.splits;
     const int per = (nsteps + splits - 1) / splits;
     float *part = splits > 1 ? reinterpret_cast<float *>(ws) : nullptr;
-    dim3 grid((ncols + SK_BN - 1) / SK_BN, splits, (M + SK_BM - 1) / SK_BM);
-    hipLaunchKernelGGL(k_gemm_skinny, grid, dim3(256), SK_LDS, st, A, W, out, res, part, M, N, K, epi, per);
+    const int mt = (M + SK_BM - 1) / SK_BM;
+    const int tiles = ((ncols + SK_BN - 1) / SK_BN) * mt;
+    const int per_xcd = (tiles + 7) / 8;
+    dim3 grid(8 * per_xcd, splits);
+    hipLaunchKernelGGL(k_gemm_skinny, grid, dim3(256), SK_LDS, st, A, W, out, res, part, M, N, K, epi, per, tiles, mt,
+                       per_xcd);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
     const int outc = epi == EPI_SILU_MUL ? N / 2 : N;

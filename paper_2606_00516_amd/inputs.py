@@ -240,6 +240,20 @@ def batch_8b_mixed(r: float, budget: int = 2048, seed: Optional[int] = None, **k
     return batch_mixed_budget(r, budget, rng, **kw)
 
 
+def batch_70b_decode(seed: Optional[int] = None) -> Batch:
+    """256 decode requests, contexts U{2048..16384} (the 70B-shaped step)."""
+    rng = np.random.default_rng([seeds()["batch"] if seed is None else seed, 70])
+    return batch_decode(256, 2048, 16384, rng)
+
+
+def batch_70b_mixed(r: float, budget: int = 4096, seed: Optional[int] = None) -> Batch:
+    """The 70B-shaped mixed step at decode share r: decode contexts
+    U{2048..16384}; prefill chunks and prefixes as in the 8B sweep."""
+    s = seeds()["batch"] if seed is None else seed
+    rng = np.random.default_rng([s, 70, int(round(r * 1000)), budget])
+    return batch_mixed_budget(r, budget, rng, dec_ctx=(2048, 16384))
+
+
 # ----------------------------------------------------------------------------
 # paged KV pool
 # ----------------------------------------------------------------------------

@@ -26,6 +26,8 @@ def _bf(shape, seed, scale=1.0):
 
 @pytest.mark.parametrize("M,N,K", [(1, 256, 256), (4, 512, 256), (64, 1376, 256), (37, 256, 688), (64, 6144, 4096),
                                    (130, 512, 256), (256, 688, 264), (512, 1024, 512), (300, 1376, 256),
+                                   # 256-row weight streaming (70B-shaped decode batch), ragged rows
+                                   (256, 10240, 8192), (200, 4104, 1024),
                                    # 256 x 256 LDS-streamed tiles: aligned, and ragged in M, N and F
                                    (1024, 8192, 1024), (1000, 8200, 512), (2048, 6144, 4096)])
 @pytest.mark.parametrize("epi", ["store", "residual", "silu_mul"])
@@ -229,7 +231,7 @@ def test_mixed_launch_equals_separate_launches():
     assert torch.equal(a, b)
 
 
-@pytest.mark.parametrize("shape", [gen.TINY, gen.L8B])
+@pytest.mark.parametrize("shape", [gen.TINY, gen.L8B, gen.L70B], ids=lambda s: s.name)
 @pytest.mark.parametrize("target", [0, 15, 16, 17, 511, 512, 513, 700])
 def test_one_hot_attention_bit_exact(shape, target):
     # q = e0 * 100 for every head, key `target` = e0 * 100, all other keys
