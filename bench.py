@@ -12,8 +12,11 @@ Prints one JSON line.  Other workloads: --workload prefill8b (8 prompts,
 lengths 256..2048 capped at 8192 tokens), mixed8b --r R (2048-token step at
 decode share R), sweep8b (the mixed step at decode shares 0, 0.1, ..., 1 and
 several token budgets, with the exclusive endpoints, K(r), kappa, the
-per-share linear fits and the crossover share), copy (a plain device copy of
-known size, used to calibrate the HBM byte counters).
+per-share linear fits and the crossover share), decode70b (one
+Llama-3-70B-shaped layer, 256 decode requests with contexts 2048..16384),
+stack70b (the 70B-shaped model step: --layers decoder layers, 80 by default,
+as an exclusive decode step and as 4096-token mixed steps), copy (a plain
+device copy of known size, used to calibrate the HBM byte counters).
 """
 from __future__ import annotations
 
@@ -44,7 +47,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="decode8b", choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "decode70b", "copy"])
+    ap.add_argument("--workload", default="decode8b",
+                    choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "decode70b", "stack70b", "copy"])
+    ap.add_argument("--layers", type=int, default=80, help="decoder layers of the stack70b model step")
+    ap.add_argument("--stack-r", default="0.2,0.5,0.8", help="decode shares of the stack70b mixed steps")
     ap.add_argument("--budgets", default="1024,2048", help="token budgets of the sweep (for alpha/beta fits)")
     ap.add_argument("--ctx16", action="store_true", help="sweep with every decode context = 16 instead")
     ap.add_argument("--r", type=float, default=0.5, help="decode share for mixed8b")
@@ -257,6 +263,86 @@ def sweep(args, dev):
     return out, pts
 
 
+def stack70b(args, dev):
+    """The 70B-shaped model step: ``args.layers`` decoder layers with their own
+    random-init bf16 weights, as an exclusive decode step (256 requests,
+    contexts U[2048,16384]) and as 4096-token mixed steps at the given decode
+    shares.  The KV pool of one layer is as large as the batch needs; as many
+    distinct pools as fit in the HBM left after the weights are allocated and
+    layer l reads pool l mod n_pools (every pool is far larger than the
+    caches, so each layer streams its context from HBM either way)."""
+    import numpy as np
+    import torch
+
+    from paper_2606_00516_amd import binding as B
+    from paper_2606_00516_amd import inputs as gen
+    shape = gen.L70B
+    L = args.layers
+    s0 = gen.seeds()
+    t0 = time.perf_counter()
+    weights = [gen.make_weights(shape, seed=s0["weights"] + l, device=dev) for l in range(L)]
+    torch.cuda.synchronize()
+    print(f"# {L} layers of weights generated in {time.perf_counter() - t0:.1f} s "
+          f"({L * shape.weight_bytes() / 1e9:.1f} GB)", file=sys.stderr, flush=True)
+    points = [("decode", gen.batch_70b_decode(), "decode")]
+    for r in [float(v) for v in args.stack_r.split(",") if v]:
+        points.append((f"mixed r={r:.1f}", gen.batch_70b_mixed(r), "mixed"))
+    out = []
+    for name, batch, mode in points:
+        h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
+        nbytes = B.eb_stack_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode)
+        ws = B.alloc_workspace(nbytes, dev)
+        pool_bytes = int(gen.pages_needed(batch).sum()) * shape.n_kv_heads * shape.page_size * shape.head_dim * 4
+        free = torch.cuda.mem_get_info()[0]
+        n_pools = max(1, min(L, int((free - (4 << 30)) // max(pool_bytes, 1))))
+        t1 = time.perf_counter()
+        pools = [gen.make_kv_pool(shape, batch, seed=s0["kv"] + i, device=dev, poison=False) for i in range(n_pools)]
+        x = gen.make_x(shape, batch.num_tokens, device=dev)
+        y = torch.empty_like(x)
+        caches = [(pools[l % n_pools].k_cache, pools[l % n_pools].v_cache, pools[l % n_pools].block_tables)
+                  for l in range(L)]
+        torch.cuda.synchronize()
+        print(f"# {name}: {batch.num_seqs} requests, {batch.num_tokens} rows, {n_pools} pool(s) of "
+              f"{pool_bytes / 1e9:.1f} GB in {time.perf_counter() - t1:.1f} s", file=sys.stderr, flush=True)
+        call = lambda: B.eb_stack_step(h, mode, weights, caches, batch.context_lens, batch.chunk_lens, x,  # noqa
+                                       y=y, ws=ws)
+        for _ in range(args.warmup):
+            call()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(args.steps):
+            call()
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t1) / args.steps * 1e3
+        B.eb_profile(h, True)
+        call()
+        st = B.eb_profile_read(h)
+        B.eb_profile(h, False)
+        torch.cuda.synchronize()
+        wk = step_work(shape, batch)
+        kv = wk["kv_bytes_decode"] + wk["kv_bytes_prefill"]
+        gemm_ms = sum(v for k, v in st.items() if k.endswith("gemm"))
+        attn_ms = st.get("attention", 0.0)
+        pt = {"point": name, "mode": mode, "n_tok": wk["T"], "n_decode": batch.num_decode,
+              "decode_share": round(batch.num_decode / wk["T"], 4), "ms_per_step": round(ms, 3),
+              "tokens_per_s": round(wk["T"] / (ms / 1e3), 1),
+              "step_bytes": L * (kv + wk["weight_bytes"] + wk["act_bytes"]),
+              "step_flops": L * (wk["gemm_flops"] + wk["attn_flops_decode"] + wk["attn_flops_prefill"]),
+              "kv_bytes_per_layer": kv, "kv_pools": n_pools,
+              "stage_ms_sum_over_layers": {k: round(v, 3) for k, v in st.items()},
+              "gemm_ms": round(gemm_ms, 3), "attention_ms": round(attn_ms, 3),
+              "gemm_tflops": round(L * wk["gemm_flops"] / (gemm_ms / 1e3) / 1e12, 1) if gemm_ms else None}
+        if mode == "decode":
+            pt["attention_hbm_gbps"] = round(L * wk["kv_bytes_decode"] / (attn_ms / 1e3) / 1e9, 1)
+        pt["whole_step_gbps"] = round(pt["step_bytes"] / (ms / 1e3) / 1e9, 1)
+        print(f"# {name}: {ms:.2f} ms/step, attention {attn_ms:.1f} ms, GEMMs {gemm_ms:.1f} ms", file=sys.stderr,
+              flush=True)
+        out.append(pt)
+        del pools, caches, x, y, ws, h, call
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -308,6 +394,27 @@ def main():
                 f.write(js + "\n")
         return
 
+    if args.workload == "stack70b":
+        t0 = time.perf_counter()
+        pts = stack70b(args, dev)
+        dec = pts[0]
+        line = {"metric": METRIC, "value": dec["whole_step_gbps"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+                "warmup": args.warmup, "ms_per_step": dec["ms_per_step"], "higher_is_better": True,
+                "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+                "config": {"workload": f"llama3-70b-shaped model step, {args.layers} layers: decode EB 256 requests "
+                                       f"ctx U[2048,16384]; MB 4096-token steps at r = {args.stack_r}",
+                           "parallelism": "single-gpu"},
+                "roofline": {"kernel": "k_decode_mfma (decode attention, summed over layers)", "bound": "hbm",
+                             "achieved": dec["attention_hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                             "frac": round(dec["attention_hbm_gbps"] / HBM_PEAK_GBPS, 4), "traffic": None},
+                "points": pts, "wall_s": round(time.perf_counter() - t0, 1)}
+        js = json.dumps(line)
+        print(js)
+        if args.json_out:
+            with open(args.json_out, "w") as f:
+                f.write(js + "\n")
+        return
+
     label, shape, batch, mode = workload(args)
     step_fn = {"decode": B.eb_layer_step_decode, "prefill": B.eb_layer_step_prefill,
                "mixed": B.eb_layer_step_mixed}[mode]
@@ -331,7 +438,7 @@ def main():
         value = step_bytes / (ms / 1e3) / 1e9
         a_ms = stages["attention"]
         achieved = wk["kv_bytes_decode"] / (a_ms / 1e3) / 1e9
-        roof = {"kernel": "k_decode (split-K paged decode attention)", "bound": "hbm",
+        roof = {"kernel": "k_decode_mfma (split-K paged decode attention on MFMA, LDS page ring)", "bound": "hbm",
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "avg_launch_ms": round(a_ms, 5),
                 "bytes_per_launch": wk["kv_bytes_decode"], "traffic": None}

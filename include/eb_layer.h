@@ -141,6 +141,27 @@ eb_status eb_layer_step_mixed(eb_handle *h, const eb_layer_weights *w, const eb_
                               const eb_batch *batch, const void *x, void *y, void *ws, size_t ws_bytes,
                               void *stream);
 
+/* A model step: n_layers decoder layers over one batch.  The paper's
+ * iteration time is that of the whole model over the batch (Sec. 1,
+ * Sec. 3.1 "Timing Model"); every layer sees the same requests and rows.
+ * Layer l maps its input (x for l = 0, layer l - 1's output otherwise) to
+ * its output with weights[l] and kv[l]; layer n_layers - 1 writes y (which
+ * must not alias x).  weights and kv are HOST arrays of n_layers structs;
+ * kv entries may name the same cache arrays, in which case each layer
+ * writes the new positions' slots in turn and attends over its own values
+ * (it appends before it attends).  The batch is planned and its metadata
+ * staged once for all layers.  mode is one of the three step modes, with the
+ * same batch constraints as the layer entry points.  ws must hold
+ * eb_stack_workspace_bytes() bytes (one layer's workspace plus one
+ * activation buffer that alternates with y).  With profiling on,
+ * eb_profile_read() returns each stage's time summed over the layers.
+ * Errors as for the layer steps, plus EB_ERR_CONFIG for n_layers < 1 and
+ * EB_ERR_MODE for an unknown mode; a failing layer is named in the message. */
+size_t eb_stack_workspace_bytes(const eb_handle *h, const eb_batch *batch, eb_mode mode);
+eb_status eb_stack_step(eb_handle *h, eb_mode mode, int32_t n_layers, const eb_layer_weights *weights,
+                        const eb_kv_cache *kv, const eb_batch *batch, const void *x, void *y, void *ws,
+                        size_t ws_bytes, void *stream);
+
 /* Host-only check of a step's inputs (no GPU needed): shape support, lengths,
  * mode constraints, and block-table contents (ids in [0, num_pages) for every
  * needed logical page, no physical page used twice).  block_tables_host is

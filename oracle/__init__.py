@@ -15,6 +15,7 @@ from .layer import (  # noqa: F401
     attend_one,
     paged_attention_row,
     layer_step,
+    stack_step,
     prepare_weights,
     LayerCfg,
 )

@@ -274,3 +274,26 @@ def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
         else:
             raise ValueError(mode)
     return (y, inter) if intermediates else y
+
+
+def stack_step(cfg: LayerCfg, Ws: Sequence[dict], k_caches: Sequence[np.ndarray], v_caches: Sequence[np.ndarray],
+               block_tables: Sequence[np.ndarray], context_lens: Sequence[int], chunk_lens: Sequence[int],
+               x_bits: np.ndarray, mode: str = "batched", seqs: Optional[Sequence[int]] = None) -> np.ndarray:
+    """A model step: the layers one after another over the same batch.
+
+    The paper's iteration is a pass of the whole model over the batch
+    (Sec. 1; Sec. 3.1 "Timing Model"); every layer sees the same requests at
+    the same positions.  Layer l takes the previous layer's output as bf16
+    (the layer interface carries bf16 activations), appends into its own
+    cache (k_caches[l], v_caches[l], mutated in place; entries may be the
+    same arrays, in which case each layer overwrites the new slots in turn)
+    and the last layer's output is returned in working precision.
+    """
+    xb = x_bits
+    y = None
+    for l, W in enumerate(Ws):
+        y = layer_step(cfg, W, k_caches[l], v_caches[l], block_tables[l], context_lens, chunk_lens, xb,
+                       mode=mode, seqs=seqs)
+        if l + 1 < len(Ws):
+            xb = f32_to_bf16_bits(y.astype(np.float32))
+    return y

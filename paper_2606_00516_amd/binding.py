@@ -28,7 +28,8 @@ EPILOGUES = {"store": 0, "residual": 1, "silu_mul": 2}
 SYMBOLS = ("eb_create", "eb_destroy", "eb_workspace_bytes", "eb_layer_step_decode", "eb_layer_step_prefill",
            "eb_layer_step_mixed", "eb_validate", "eb_status_str", "eb_last_error", "eb_op_rmsnorm",
            "eb_op_gemm_workspace_bytes", "eb_op_gemm", "eb_op_rope_kv_append", "eb_op_attention",
-           "eb_op_gather_kv", "eb_profile", "eb_profile_read", "eb_profile_stage_name")
+           "eb_op_gather_kv", "eb_profile", "eb_profile_read", "eb_profile_stage_name", "eb_stack_workspace_bytes",
+           "eb_stack_step")
 
 
 class EbError(RuntimeError):
@@ -85,6 +86,8 @@ def lib() -> ctypes.CDLL:
         "eb_profile": (I32, [VP, I32]),
         "eb_profile_read": (I32, [VP, P(ctypes.c_float), I32]),
         "eb_profile_stage_name": (ctypes.c_char_p, [I32]),
+        "eb_stack_workspace_bytes": (SZ, [VP, P(Batch), I32]),
+        "eb_stack_step": (I32, [VP, I32, I32, P(LayerWeights), P(KvCache), P(Batch), VP, VP, VP, SZ, VP]),
     }
     for name in ("eb_layer_step_decode", "eb_layer_step_prefill", "eb_layer_step_mixed"):
         sig[name] = (I32, [VP, P(LayerWeights), P(KvCache), P(Batch), VP, VP, VP, SZ, VP])
@@ -206,6 +209,30 @@ def eb_layer_step_mixed(h, weights, k_cache, v_cache, block_tables, context_lens
                         stream=None):
     return _step("eb_layer_step_mixed", h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x,
                  y, ws, stream)
+
+
+def eb_stack_workspace_bytes(h: Handle, context_lens, chunk_lens, mode: str) -> int:
+    hb = HostBatch(context_lens, chunk_lens)
+    return int(lib().eb_stack_workspace_bytes(h.h, ctypes.byref(hb.c), MODES[mode]))
+
+
+def eb_stack_step(h: Handle, mode: str, weights: list, caches: list, context_lens, chunk_lens, x: torch.Tensor,
+                  y: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, stream=None):
+    """n = len(weights) layers; caches[l] = (k_cache, v_cache, block_tables)
+    of layer l (entries may repeat the same tensors)."""
+    n = len(weights)
+    if len(caches) != n:
+        raise ValueError("one cache entry per layer")
+    hb = HostBatch(context_lens, chunk_lens)
+    if y is None:
+        y = torch.empty_like(x)
+    if ws is None:
+        ws = alloc_workspace(lib().eb_stack_workspace_bytes(h.h, ctypes.byref(hb.c), MODES[mode]), x.device)
+    ws_arr = (LayerWeights * n)(*[weights_struct(w) for w in weights])
+    kv_arr = (KvCache * n)(*[kv_struct(*c) for c in caches])
+    _check(lib().eb_stack_step(h.h, MODES[mode], n, ws_arr, kv_arr, ctypes.byref(hb.c), _ptr(x), _ptr(y), _ptr(ws),
+                               ws.numel(), _stream(stream)))
+    return y
 
 
 def eb_validate(shape, context_lens, chunk_lens, block_tables_host: np.ndarray, num_pages: int, mode: str) -> int:

@@ -3,7 +3,10 @@
 #include <hip/hip_runtime.h>
 #include <string.h>
 
+#include <algorithm>
+
 #include <string>
+#include <vector>
 
 #include "../../include/eb_layer.h"
 #include "eb_internal.h"
@@ -35,10 +38,13 @@ Shape shape_of(const eb_layer_config &c) {
 
 // Byte offsets of everything a step keeps in the caller's workspace.
 struct WsLayout {
-  size_t meta = 0, act = 0, qkv = 0, attn = 0, h1 = 0, mlp = 0, part_o = 0, part_ml = 0, gemm = 0, total = 0;
+  size_t meta = 0, act = 0, qkv = 0, attn = 0, h1 = 0, mlp = 0, part_o = 0, part_ml = 0, gemm = 0, alt = 0,
+         total = 0;
 };
 
-WsLayout layout_for(const Shape &s, const HostPlan &p, bool full_step) {
+// full_step: buffers of a whole layer; stack: plus the second activation
+// buffer that consecutive layers of a stack alternate with y.
+WsLayout layout_for(const Shape &s, const HostPlan &p, bool full_step, bool stack = false) {
   WsLayout L;
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -64,6 +70,7 @@ WsLayout layout_for(const Shape &s, const HostPlan &p, bool full_step) {
                                plan_gemm(M, s.hidden, s.ffn, EPI_RESIDUAL)};
     for (const auto &gp : plans) g = gp.ws_bytes > g ? gp.ws_bytes : g;
     L.gemm = take(g);
+    if (stack) L.alt = take(T * s.hidden * 2);
   }
   L.total = off;
   return L;
@@ -109,10 +116,12 @@ struct eb_handle {
   hipEvent_t ev[kRing];
   bool used[kRing];
   int next;
-  // per-stage timing of the last step (eb_profile)
+  // per-stage timing of the last step (eb_profile): events bracket stage s
+  // of layer l at pev[2 (l kStages + s)] and the next one
   bool prof;
   bool prof_valid;
-  hipEvent_t pev[2 * kStages];
+  int prof_layers;
+  std::vector<hipEvent_t> pev;
 };
 
 namespace {
@@ -170,76 +179,131 @@ KV kv_of(const eb_kv_cache *kv) {
             kv->num_pages, kv->max_pages_per_seq};
 }
 
-eb_status run_step(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv, const eb_batch *b, const void *x,
-                   void *y, void *ws, size_t ws_bytes, void *stream, eb_mode mode) {
-  if (!h) return fail(EB_ERR_NULL, "handle is NULL");
+eb_status check_weights(const eb_layer_weights *w) {
   if (!w || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm || !w->w_gate_up || !w->w_down)
     return fail(EB_ERR_NULL, "a weight pointer is NULL");
-  eb_status s = check_kv(kv);
+  return EB_OK;
+}
+
+// Workspace buffers of one layer body.
+struct StepBufs {
+  uint16_t *act, *qkv, *attn, *h1, *mlp, *alt;
+  float *part_o, *part_ml;
+  void *gws;
+};
+
+StepBufs bufs_at(char *base, const WsLayout &L) {
+  return StepBufs{reinterpret_cast<uint16_t *>(base + L.act),  reinterpret_cast<uint16_t *>(base + L.qkv),
+                  reinterpret_cast<uint16_t *>(base + L.attn), reinterpret_cast<uint16_t *>(base + L.h1),
+                  reinterpret_cast<uint16_t *>(base + L.mlp),  L.alt ? reinterpret_cast<uint16_t *>(base + L.alt)
+                                                                      : nullptr,
+                  reinterpret_cast<float *>(base + L.part_o), reinterpret_cast<float *>(base + L.part_ml),
+                  base + L.gemm};
+}
+
+// Make sure the profiling event pool covers n layers.
+eb_status grow_events(eb_handle *h, int layers) {
+  const size_t need = (size_t)2 * kStages * layers;
+  while (h->pev.size() < need) {
+    hipEvent_t e = nullptr;
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) return hip_fail(r, "hipEventCreate");
+    h->pev.push_back(e);
+  }
+  return EB_OK;
+}
+
+// The nine stages of one layer on the stream: x -> y with weights w and
+// cache kvd; the batch metadata m is already in the workspace.
+eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, const DevMeta &m, const StepBufs &B,
+                     const uint16_t *xin, uint16_t *yout, int T, eb_mode mode, int layer, hipStream_t st) {
+  const Shape &sh = h->shape;
+  hipError_t e;
+  auto mark = [&](int i) -> hipError_t {
+    return h->prof ? hipEventRecord(h->pev[(size_t)2 * kStages * layer + i], st) : hipSuccess;
+  };
+#define EB_STAGE(idx, call, what)                                       \
+  if ((e = mark(2 * (idx))) != hipSuccess) return hip_fail(e, "hipEventRecord"); \
+  if ((e = (call)) != hipSuccess) return hip_fail(e, what);              \
+  if ((e = mark(2 * (idx) + 1)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+  EB_STAGE(0, launch_rmsnorm(xin, static_cast<const uint16_t *>(w->attn_norm), B.act, T, sh.hidden, sh.eps, st),
+           "rmsnorm1");
+  EB_STAGE(1,
+           launch_gemm(plan_gemm(T, sh.qkv_cols(), sh.hidden, EPI_STORE), B.act,
+                       static_cast<const uint16_t *>(w->w_qkv), B.qkv, nullptr, T, sh.qkv_cols(), sh.hidden,
+                       EPI_STORE, B.gws, st),
+           "qkv gemm");
+  EB_STAGE(2, launch_rope_append(sh, B.qkv, kvd, m, st), "rope/kv append");
+  const int kind = mode == EB_MODE_DECODE ? 0 : (mode == EB_MODE_PREFILL ? 1 : 2);
+  EB_STAGE(3, launch_attention(sh, B.qkv, kvd, m, B.attn, B.part_o, B.part_ml, kind, st, 1), "attention");
+  EB_STAGE(4, launch_attention(sh, B.qkv, kvd, m, B.attn, B.part_o, B.part_ml, kind, st, 2), "attention combine");
+  EB_STAGE(5,
+           launch_gemm(plan_gemm(T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL), B.attn,
+                       static_cast<const uint16_t *>(w->w_o), B.h1, xin, T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL,
+                       B.gws, st),
+           "o gemm");
+  EB_STAGE(6, launch_rmsnorm(B.h1, static_cast<const uint16_t *>(w->mlp_norm), B.act, T, sh.hidden, sh.eps, st),
+           "rmsnorm2");
+  EB_STAGE(7,
+           launch_gemm(plan_gemm(T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL), B.act,
+                       static_cast<const uint16_t *>(w->w_gate_up), B.mlp, nullptr, T, 2 * sh.ffn, sh.hidden,
+                       EPI_SILU_MUL, B.gws, st),
+           "gate/up gemm");
+  EB_STAGE(8,
+           launch_gemm(plan_gemm(T, sh.hidden, sh.ffn, EPI_RESIDUAL), B.mlp,
+                       static_cast<const uint16_t *>(w->w_down), yout, B.h1, T, sh.hidden, sh.ffn, EPI_RESIDUAL,
+                       B.gws, st),
+           "down gemm");
+#undef EB_STAGE
+  return EB_OK;
+}
+
+// n_layers layer bodies over one planned batch: layer l reads x (l = 0) or
+// the previous layer's output and writes y or the alternate buffer, so that
+// the last layer writes y.  Every check runs before anything is enqueued.
+eb_status run_layers(eb_handle *h, int32_t n_layers, const eb_layer_weights *w, const eb_kv_cache *kv,
+                     const eb_batch *b, const void *x, void *y, void *ws, size_t ws_bytes, void *stream,
+                     eb_mode mode) {
+  if (!h) return fail(EB_ERR_NULL, "handle is NULL");
+  if (n_layers < 1) return fail(EB_ERR_CONFIG, "n_layers must be >= 1");
+  if (!w || !kv) return fail(EB_ERR_NULL, "weights or kv is NULL");
+  int32_t min_pages = 0;
+  for (int l = 0; l < n_layers; ++l) {
+    eb_status s = check_weights(&w[l]);
+    if (s == EB_OK) s = check_kv(&kv[l]);
+    if (s != EB_OK) return n_layers > 1 ? fail(s, "layer " + std::to_string(l) + ": " + g_err) : s;
+    min_pages = l == 0 ? kv[l].max_pages_per_seq : std::min(min_pages, kv[l].max_pages_per_seq);
+  }
+  eb_status s = check_common(h, b, mode, min_pages);
   if (s != EB_OK) return s;
-  s = check_common(h, b, mode, kv->max_pages_per_seq);
-  if (s != EB_OK) return s;
+  h->prof_valid = false;
   if (b->num_tokens == 0) return EB_OK;
   if (!x || !y) return fail(EB_ERR_NULL, "x or y is NULL");
   if (x == y) return fail(EB_ERR_BATCH, "y must not alias x");
   HostPlan p;
   build_plan(h->cfg, *b, mode, p);
-  const Shape &sh = h->shape;
-  const WsLayout L = layout_for(sh, p, true);
+  const bool stack = n_layers > 1;
+  const WsLayout L = layout_for(h->shape, p, true, stack);
   s = check_ws(ws, ws_bytes, L.total);
   if (s != EB_OK) return s;
+  if (h->prof) {
+    s = grow_events(h, n_layers);
+    if (s != EB_OK) return s;
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   char *base = static_cast<char *>(ws);
   s = stage_meta(h, p, ws, L, st);
   if (s != EB_OK) return s;
   const DevMeta m = meta_at(p, reinterpret_cast<const int32_t *>(base + L.meta));
-  const KV kvd = kv_of(kv);
-  uint16_t *act = reinterpret_cast<uint16_t *>(base + L.act);
-  uint16_t *qkv = reinterpret_cast<uint16_t *>(base + L.qkv);
-  uint16_t *attn = reinterpret_cast<uint16_t *>(base + L.attn);
-  uint16_t *h1 = reinterpret_cast<uint16_t *>(base + L.h1);
-  uint16_t *mlp = reinterpret_cast<uint16_t *>(base + L.mlp);
-  float *part_o = reinterpret_cast<float *>(base + L.part_o);
-  float *part_ml = reinterpret_cast<float *>(base + L.part_ml);
-  void *gws = base + L.gemm;
-  const uint16_t *xin = static_cast<const uint16_t *>(x);
-  uint16_t *yout = static_cast<uint16_t *>(y);
-  const int T = p.T;
-  hipError_t e;
-  h->prof_valid = false;
-  auto mark = [&](int i) -> hipError_t { return h->prof ? hipEventRecord(h->pev[i], st) : hipSuccess; };
-#define EB_STAGE(idx, call, what)                                       \
-  if ((e = mark(2 * (idx))) != hipSuccess) return hip_fail(e, "hipEventRecord"); \
-  if ((e = (call)) != hipSuccess) return hip_fail(e, what);              \
-  if ((e = mark(2 * (idx) + 1)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  EB_STAGE(0, launch_rmsnorm(xin, static_cast<const uint16_t *>(w->attn_norm), act, T, sh.hidden, sh.eps, st),
-           "rmsnorm1");
-  EB_STAGE(1,
-           launch_gemm(plan_gemm(T, sh.qkv_cols(), sh.hidden, EPI_STORE), act,
-                       static_cast<const uint16_t *>(w->w_qkv), qkv, nullptr, T, sh.qkv_cols(), sh.hidden, EPI_STORE,
-                       gws, st),
-           "qkv gemm");
-  EB_STAGE(2, launch_rope_append(sh, qkv, kvd, m, st), "rope/kv append");
-  const int kind = mode == EB_MODE_DECODE ? 0 : (mode == EB_MODE_PREFILL ? 1 : 2);
-  EB_STAGE(3, launch_attention(sh, qkv, kvd, m, attn, part_o, part_ml, kind, st, 1), "attention");
-  EB_STAGE(4, launch_attention(sh, qkv, kvd, m, attn, part_o, part_ml, kind, st, 2), "attention combine");
-  EB_STAGE(5,
-           launch_gemm(plan_gemm(T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL), attn,
-                       static_cast<const uint16_t *>(w->w_o), h1, xin, T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, gws,
-                       st),
-           "o gemm");
-  EB_STAGE(6, launch_rmsnorm(h1, static_cast<const uint16_t *>(w->mlp_norm), act, T, sh.hidden, sh.eps, st),
-           "rmsnorm2");
-  EB_STAGE(7,
-           launch_gemm(plan_gemm(T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL), act,
-                       static_cast<const uint16_t *>(w->w_gate_up), mlp, nullptr, T, 2 * sh.ffn, sh.hidden,
-                       EPI_SILU_MUL, gws, st),
-           "gate/up gemm");
-  EB_STAGE(8,
-           launch_gemm(plan_gemm(T, sh.hidden, sh.ffn, EPI_RESIDUAL), mlp, static_cast<const uint16_t *>(w->w_down),
-                       yout, h1, T, sh.hidden, sh.ffn, EPI_RESIDUAL, gws, st),
-           "down gemm");
-#undef EB_STAGE
+  const StepBufs B = bufs_at(base, L);
+  const uint16_t *in = static_cast<const uint16_t *>(x);
+  for (int l = 0; l < n_layers; ++l) {
+    uint16_t *out = ((n_layers - 1 - l) % 2 == 0) ? static_cast<uint16_t *>(y) : B.alt;
+    s = layer_body(h, &w[l], kv_of(&kv[l]), m, B, in, out, p.T, mode, l, st);
+    if (s != EB_OK) return s;
+    in = out;
+  }
+  h->prof_layers = n_layers;
   h->prof_valid = h->prof;
   return EB_OK;
 }
@@ -286,7 +350,7 @@ eb_status eb_create(const eb_layer_config *cfg, int32_t max_seqs, int32_t max_to
   h->slot_cap = plan_capacity(max_seqs, max_tokens, cfg->n_q_heads / cfg->n_kv_heads);
   h->prof = false;
   h->prof_valid = false;
-  for (int i = 0; i < 2 * kStages; ++i) h->pev[i] = nullptr;
+  h->prof_layers = 0;
   for (int k = 0; k < kRing; ++k) {
     h->pinned[k] = nullptr;
     h->ev[k] = nullptr;
@@ -313,8 +377,7 @@ void eb_destroy(eb_handle *h) {
     }
     if (h->pinned[k]) (void)hipHostFree(h->pinned[k]);
   }
-  for (int i = 0; i < 2 * kStages; ++i)
-    if (h->pev[i]) (void)hipEventDestroy(h->pev[i]);
+  for (hipEvent_t e : h->pev) (void)hipEventDestroy(e);
   delete h;
 }
 
@@ -329,17 +392,34 @@ size_t eb_workspace_bytes(const eb_handle *h, const eb_batch *batch, eb_mode mod
 
 eb_status eb_layer_step_decode(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv, const eb_batch *batch,
                                const void *x, void *y, void *ws, size_t ws_bytes, void *stream) {
-  return run_step(h, w, kv, batch, x, y, ws, ws_bytes, stream, EB_MODE_DECODE);
+  return run_layers(h, 1, w, kv, batch, x, y, ws, ws_bytes, stream, EB_MODE_DECODE);
 }
 
 eb_status eb_layer_step_prefill(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv, const eb_batch *batch,
                                 const void *x, void *y, void *ws, size_t ws_bytes, void *stream) {
-  return run_step(h, w, kv, batch, x, y, ws, ws_bytes, stream, EB_MODE_PREFILL);
+  return run_layers(h, 1, w, kv, batch, x, y, ws, ws_bytes, stream, EB_MODE_PREFILL);
 }
 
 eb_status eb_layer_step_mixed(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv, const eb_batch *batch,
                               const void *x, void *y, void *ws, size_t ws_bytes, void *stream) {
-  return run_step(h, w, kv, batch, x, y, ws, ws_bytes, stream, EB_MODE_MIXED);
+  return run_layers(h, 1, w, kv, batch, x, y, ws, ws_bytes, stream, EB_MODE_MIXED);
+}
+
+size_t eb_stack_workspace_bytes(const eb_handle *h, const eb_batch *batch, eb_mode mode) {
+  if (!h) return 0;
+  std::string err;
+  if (check_batch(h->cfg, batch, -1, mode, err) != EB_OK) return 0;
+  HostPlan p;
+  build_plan(h->cfg, *batch, mode, p);
+  return layout_for(h->shape, p, true, true).total;
+}
+
+eb_status eb_stack_step(eb_handle *h, eb_mode mode, int32_t n_layers, const eb_layer_weights *weights,
+                        const eb_kv_cache *kv, const eb_batch *batch, const void *x, void *y, void *ws,
+                        size_t ws_bytes, void *stream) {
+  if (mode != EB_MODE_DECODE && mode != EB_MODE_PREFILL && mode != EB_MODE_MIXED)
+    return fail(EB_ERR_MODE, "unknown mode");
+  return run_layers(h, n_layers, weights, kv, batch, x, y, ws, ws_bytes, stream, mode);
 }
 
 eb_status eb_validate(const eb_layer_config *cfg, const eb_batch *batch, const int32_t *block_tables_host,
@@ -358,11 +438,9 @@ eb_status eb_validate(const eb_layer_config *cfg, const eb_batch *batch, const i
 
 eb_status eb_profile(eb_handle *h, int32_t enable) {
   if (!h) return fail(EB_ERR_NULL, "handle is NULL");
-  if (enable && !h->pev[0]) {
-    for (int i = 0; i < 2 * kStages; ++i) {
-      hipError_t e = hipEventCreate(&h->pev[i]);
-      if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
-    }
+  if (enable) {
+    eb_status s = grow_events(h, 1);
+    if (s != EB_OK) return s;
   }
   h->prof = enable != 0;
   h->prof_valid = false;
@@ -371,12 +449,18 @@ eb_status eb_profile(eb_handle *h, int32_t enable) {
 
 int32_t eb_profile_read(eb_handle *h, float *ms, int32_t cap) {
   if (!h || !h->prof_valid) return 0;
-  if (hipEventSynchronize(h->pev[2 * kStages - 1]) != hipSuccess) return -1;
+  const size_t last = (size_t)2 * kStages * h->prof_layers - 1;
+  if (hipEventSynchronize(h->pev[last]) != hipSuccess) return -1;
   const int n = cap < kStages ? cap : kStages;
   for (int i = 0; i < n; ++i) {
-    float t = 0.f;
-    if (hipEventElapsedTime(&t, h->pev[2 * i], h->pev[2 * i + 1]) != hipSuccess) return -1;
-    ms[i] = t;
+    float sum = 0.f;
+    for (int l = 0; l < h->prof_layers; ++l) {
+      const size_t b = (size_t)2 * (l * kStages + i);
+      float t = 0.f;
+      if (hipEventElapsedTime(&t, h->pev[b], h->pev[b + 1]) != hipSuccess) return -1;
+      sum += t;
+    }
+    ms[i] = sum;
   }
   return n;
 }

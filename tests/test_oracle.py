@@ -431,3 +431,70 @@ def test_subset_equals_full_batch():
     for i in (1, 4):
         assert np.array_equal(y_sub[off[i]:off[i + 1]], y_all[off[i]:off[i + 1]])
     assert np.isnan(y_sub[off[0]:off[1]]).all()
+
+
+# ---------------------------------------------------------------- stacked layers
+
+def _layer_inputs(shape, batch, w_seed, kv_seed, x_seed=None, proj_std=0.2):
+    case = make_case(shape, batch, weights=gen.make_weights(shape, seed=w_seed, proj_std=proj_std),
+                     kv_seed=kv_seed, x_seed=x_seed)
+    return case.oracle_inputs()
+
+
+def test_stack_two_layers_vs_hf():
+    # Two different layers, each with its own paged cache and block tables.
+    # Layer 0 is the fp64 library layer on x; its output, rounded to bf16,
+    # feeds layer 1 (the layer interface is bf16).  The oracle's bf16 hand-off
+    # must agree with the rounded library output (up to a last-bit flip where
+    # the fp64 values straddle a rounding boundary), and its final rows must
+    # be the library layer 1 on that hand-off.
+    shape = gen.TINY
+    o0 = _layer_inputs(shape, _HF_BATCH, 101, 201)
+    o1 = _layer_inputs(shape, _HF_BATCH, 102, 202)
+    assert not np.array_equal(o0["block_tables"], o1["block_tables"])
+    cfg = o0["cfg"]
+    W0 = L.prepare_weights(o0["w_bits"], cfg, np.float64)
+    W1 = L.prepare_weights(o1["w_bits"], cfg, np.float64)
+    k0, v0, k1, v1 = (o0["k_cache"].copy(), o0["v_cache"].copy(), o1["k_cache"].copy(), o1["v_cache"].copy())
+    y = L.stack_step(cfg, [W0, W1], [k0, k1], [v0, v1], [o0["block_tables"], o1["block_tables"]],
+                     o0["context_lens"], o0["chunk_lens"], o0["x_bits"])
+    x1 = L.f32_to_bf16_bits(L.layer_step(cfg, W0, o0["k_cache"].copy(), o0["v_cache"].copy(), o0["block_tables"],
+                                         o0["context_lens"], o0["chunk_lens"], o0["x_bits"]).astype(np.float32))
+    off = _HF_BATCH.row_offsets
+    hand = np.concatenate([_hf_reference(shape, o0, i)[2] for i in range(_HF_BATCH.num_seqs)])
+    hf_bits = L.f32_to_bf16_bits(hand.astype(np.float32))
+    same = np.mean(hf_bits == x1)
+    assert same > 0.999, same
+    assert maxrel(L.bf16_bits_to_f32(hf_bits), L.bf16_bits_to_f32(x1)) < 2 ** -7
+    o1h = dict(o1, x_bits=x1, context_lens=o0["context_lens"], chunk_lens=o0["chunk_lens"])
+    for i in range(_HF_BATCH.num_seqs):
+        rows = slice(off[i], off[i + 1])
+        assert maxrel(y[rows], _hf_reference(shape, o1h, i)[2]) < 1e-9
+    # each layer appended into its own cache only
+    for kc, o in ((k0, o0), (k1, o1)):
+        assert not np.array_equal(kc, o["k_cache"])
+
+
+def test_stack_of_identity_layers_returns_x():
+    # with the output projection and the down projection zero, every layer
+    # is the identity on x (h1 = x, y = h1), whatever the attention and MLP
+    # compute, so a stack of them returns x exactly and still fills each
+    # layer's cache
+    shape = gen.TINY
+    batch = gen.batch_tiny(mode="mixed")
+    Ws, ks, vs, bts = [], [], [], []
+    x_bits = None
+    for l in range(3):
+        o = _layer_inputs(shape, batch, 300 + l, 400 + l, proj_std=0.02)
+        o["w_bits"]["w_o"][:] = 0
+        o["w_bits"]["w_down"][:] = 0
+        Ws.append(L.prepare_weights(o["w_bits"], o["cfg"]))
+        ks.append(o["k_cache"])
+        vs.append(o["v_cache"])
+        bts.append(o["block_tables"])
+        x_bits = o["x_bits"] if x_bits is None else x_bits
+    before = [k.copy() for k in ks]
+    y = L.stack_step(o["cfg"], Ws, ks, vs, bts, batch.context_lens, batch.chunk_lens, x_bits)
+    assert np.array_equal(L.f32_to_bf16_bits(y.astype(np.float32)), x_bits)
+    for k, kb in zip(ks, before):
+        assert not np.array_equal(k, kb)
