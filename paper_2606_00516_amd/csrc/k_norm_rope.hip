@@ -6,8 +6,12 @@ namespace eb {
 
 // ---------------------------------------------------------------------------
 // RMSNorm: out = bf16(x / sqrt(mean(x^2) + eps) * gamma).  One wavefront per
-// row, 16-byte accesses; the second pass re-reads the row from cache.
+// row, 16-byte accesses.  Rows of up to 64 * 8 * MAXC elements stay in
+// registers: every load of the row is issued before the first use, so the
+// kernel waits for memory once; longer rows take a second pass.
 // ---------------------------------------------------------------------------
+constexpr int kNormMaxChunks = 16;  // 16-byte chunks per lane held in registers (rows up to 8192)
+
 __global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t *__restrict__ x, const uint16_t *__restrict__ g,
                                                  uint16_t *__restrict__ out, int rows, int d, float eps) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -16,6 +20,37 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t *__restrict__ x,
   const uint16_t *xr = x + (size_t)row * d;
   uint16_t *orow = out + (size_t)row * d;
   const int nch = d >> 3;
+  if (nch <= 64 * kNormMaxChunks) {
+    u32x4_t v[kNormMaxChunks];
+#pragma unroll
+    for (int j = 0; j < kNormMaxChunks; ++j) {
+      const int c = lane + 64 * j;
+      v[j] = c < nch ? ld_u32x4(xr + c * 8) : u32x4_t{0u, 0u, 0u, 0u};
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < kNormMaxChunks; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float a = bf16_lo(v[j][i]), b = bf16_hi(v[j][i]);
+        ss += a * a + b * b;
+      }
+    ss = wave_sum(ss);
+    const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+    for (int j = 0; j < kNormMaxChunks; ++j) {
+      const int c = lane + 64 * j;
+      if (c < nch) {
+        const u32x4_t gv = ld_u32x4(g + c * 8);  // gamma: shared by all rows, an L2 hit
+        u32x4_t o;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          o[i] = pack_bf16x2(bf16_lo(v[j][i]) * inv * bf16_lo(gv[i]), bf16_hi(v[j][i]) * inv * bf16_hi(gv[i]));
+        st_u32x4(orow + c * 8, o);
+      }
+    }
+    return;
+  }
   float ss = 0.f;
   for (int c = lane; c < nch; c += 64) {
     u32x4_t v = ld_u32x4(xr + c * 8);
@@ -49,7 +84,10 @@ hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gamma, uint16_t *ou
 // RoPE (rotate-half pairs (t, t + hd/2), frequency theta^(-2t/hd), angle
 // formed in fp64) on the q and k heads of one QKV row, q rotated in place,
 // rotated k and v stored at the row's slot of its request's paged cache.
-// One block per row.
+// One block per row; a thread moves 8 consecutive dims of one half of a
+// head and their 8 partners in 16-byte accesses.  The angle pos * freq is
+// formed and reduced to [-pi, pi] in fp64; its sine and cosine are then
+// taken in fp32 (the reduced angle is small, so fp32 is accurate to an ulp).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv, uint16_t *__restrict__ kc,
                                                      uint16_t *__restrict__ vc, const int32_t *__restrict__ bt,
@@ -62,10 +100,13 @@ __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv,
   const int half = hd >> 1;
   for (int t = threadIdx.x; t < half; t += blockDim.x) {
     const double inv_freq = exp2(-(2.0 * t / hd) * log2_theta);
-    double s, c;
-    sincos((double)pos * inv_freq, &s, &c);
-    cs[t] = (float)c;
-    sn[t] = (float)s;
+    const double ang = (double)pos * inv_freq;
+    const double two_pi = 6.283185307179586476925286766559;
+    const double red = fma(-rint(ang / two_pi), two_pi, ang);
+    float s, c;
+    sincosf((float)red, &s, &c);
+    cs[t] = c;
+    sn[t] = s;
   }
   __syncthreads();
   const int cols = (nq + 2 * nkv) * hd;
@@ -73,31 +114,37 @@ __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv,
   const int page = bt[(size_t)seq * max_pages + pos / kPageSize];
   const bool page_ok = page >= 0 && page < num_pages;
   const int slot = pos % kPageSize;
-  // q and k: one thread per rotation pair
-  const int pairs = (nq + nkv) * half;
-  for (int i = threadIdx.x; i < pairs; i += blockDim.x) {
-    const int h = i / half, t = i - h * half;
-    const float a = bf16_to_f32(row[h * hd + t]);
-    const float b = bf16_to_f32(row[h * hd + t + half]);
-    const float c = cs[t], s = sn[t];
-    const uint16_t ra = (uint16_t)f32_to_bf16_bits(a * c - b * s);
-    const uint16_t rb = (uint16_t)f32_to_bf16_bits(a * s + b * c);
+  const int hch = half / 8;  // 8-dim chunks per half head
+  // q and k heads: (head, chunk of the first half) per thread
+  const int items = (nq + nkv) * hch;
+  for (int i = threadIdx.x; i < items; i += blockDim.x) {
+    const int h = i / hch, t0 = (i - h * hch) * 8;
+    const u32x4_t a = ld_u32x4(row + h * hd + t0);
+    const u32x4_t b = ld_u32x4(row + h * hd + t0 + half);
+    u32x4_t ra, rb;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float c0 = cs[t0 + 2 * e], s0 = sn[t0 + 2 * e], c1 = cs[t0 + 2 * e + 1], s1 = sn[t0 + 2 * e + 1];
+      const float a0 = bf16_lo(a[e]), a1 = bf16_hi(a[e]), b0 = bf16_lo(b[e]), b1 = bf16_hi(b[e]);
+      ra[e] = pack_bf16x2(a0 * c0 - b0 * s0, a1 * c1 - b1 * s1);
+      rb[e] = pack_bf16x2(a0 * s0 + b0 * c0, a1 * s1 + b1 * c1);
+    }
     if (h < nq) {
-      row[h * hd + t] = ra;
-      row[h * hd + t + half] = rb;
+      st_u32x4(row + h * hd + t0, ra);
+      st_u32x4(row + h * hd + t0 + half, rb);
     } else if (page_ok) {
-      const int kh = h - nq;
-      uint16_t *dst = kc + (((size_t)page * nkv + kh) * kPageSize + slot) * hd;
-      dst[t] = ra;
-      dst[t + half] = rb;
+      uint16_t *dst = kc + (((size_t)page * nkv + (h - nq)) * kPageSize + slot) * hd;
+      st_u32x4(dst + t0, ra);
+      st_u32x4(dst + t0 + half, rb);
     }
   }
-  // v: plain copy
+  // v: plain copy, 16 bytes per thread
   if (page_ok) {
     const uint16_t *vsrc = row + (nq + nkv) * hd;
-    for (int i = threadIdx.x; i < nkv * hd; i += blockDim.x) {
-      const int kh = i / hd, dd = i - kh * hd;
-      vc[(((size_t)page * nkv + kh) * kPageSize + slot) * hd + dd] = vsrc[i];
+    const int vch = nkv * hd / 8;
+    for (int i = threadIdx.x; i < vch; i += blockDim.x) {
+      const int kh = (i * 8) / hd, dd = i * 8 - kh * hd;
+      st_u32x4(vc + (((size_t)page * nkv + kh) * kPageSize + slot) * hd + dd, ld_u32x4(vsrc + i * 8));
     }
   }
 }
