@@ -442,6 +442,18 @@ def main():
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBPS, 4), "avg_launch_ms": round(a_ms, 5),
                 "bytes_per_launch": wk["kv_bytes_decode"], "traffic": None}
+    elif mode == "mixed":
+        # the step is dominated by the single mixed attention launch, whose
+        # decode items stream the requests' K/V from HBM
+        unit = "TFLOP/s"
+        value = step_flops / (ms / 1e3) / 1e12
+        a_ms = stages["attention"]
+        kv_b = wk["kv_bytes_decode"] + wk["kv_bytes_prefill"]
+        achieved = kv_b / (a_ms / 1e3) / 1e9
+        roof = {"kernel": "k_mixed_mfma (prefill tiles + decode splits in one launch)", "bound": "hbm",
+                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "avg_launch_ms": round(a_ms, 5),
+                "bytes_per_launch": kv_b, "prefill_attention_flops": wk["attn_flops_prefill"], "traffic": None}
     else:
         unit = "TFLOP/s"
         value = step_flops / (ms / 1e3) / 1e12
@@ -455,7 +467,7 @@ def main():
     # HBM traffic from committed counter runs, only if the kernel is unchanged
     try:
         cnt = json.load(open(COUNTERS))
-        key = {"decode8b": "decode_attention_8b"}.get(args.workload)
+        key = {"decode8b": "decode_attention_8b", "decode70b": "decode_attention_70b"}.get(args.workload)
         ent = cnt.get(key) if key else None
         if ent and ent.get("source_sha") == sha_of(ATTN_SRC):
             roof["traffic"] = ent["bytes_per_dispatch"]
