@@ -48,11 +48,14 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="decode8b",
-                    choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "decode70b", "stack70b", "copy"])
+                    choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "decode70b", "stack70b", "policy8b",
+                             "copy"])
+    ap.add_argument("--calib-out", default=None, help="policy8b: write the calibrated step-cost profile here")
     ap.add_argument("--layers", type=int, default=80, help="decoder layers of the stack70b model step")
     ap.add_argument("--stack-r", default="0.2,0.5,0.8", help="decode shares of the stack70b mixed steps")
     ap.add_argument("--budgets", default="1024,2048", help="token budgets of the sweep (for alpha/beta fits)")
     ap.add_argument("--ctx16", action="store_true", help="sweep with every decode context = 16 instead")
+    ap.add_argument("--dec-ctx", default=None, help="decode context range lo,hi of the sweep (default 1024,8192)")
     ap.add_argument("--r", type=float, default=0.5, help="decode share for mixed8b")
     ap.add_argument("--budget", type=int, default=2048, help="token budget for mixed8b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -203,6 +206,9 @@ def sweep(args, dev):
     budgets = [int(b) for b in args.budgets.split(",")]
     rs = [round(0.1 * i, 1) for i in range(11)]
     dec_ctx = (16, 16) if args.ctx16 else (1024, 8192)
+    if args.dec_ctx:
+        lo, hi = (int(v) for v in args.dec_ctx.split(","))
+        dec_ctx = (lo, hi)
     pts = []
 
     def run(batch, mode):
@@ -343,6 +349,46 @@ def stack70b(args, dev):
     return out
 
 
+def policy8b(args, dev):
+    """The batching decision on this GPU: calibrate the linear step-cost model
+    from an 8B-layer MB sweep whose decode contexts (512..1024) match the
+    paper's synthetic mixes, evaluate the crossover condition and theta_0 for
+    those mixes, and run the serving-loop simulator (EB(k0*), MB, EB+) priced
+    by the measured coefficients."""
+    from paper_2606_00516_amd import cost_model as CM
+    from paper_2606_00516_amd import scheduler_sim as SIM
+    args.dec_ctx = args.dec_ctx or "512,1024"
+    args.budgets = args.budgets if args.budgets != "1024,2048" else "512,1024,2048,4096"
+    sw, pts = sweep(args, dev)
+    c = CM.calibrate(pts, label=f"MI355X llama3-8b layer, decode ctx U[{args.dec_ctx}]")
+    prof = {"hardware": "MI355X", "shape": "llama3-8b layer", "decode_ctx": args.dec_ctx,
+            "budgets": args.budgets, "costs": c.to_dict()}
+    if args.calib_out:
+        with open(args.calib_out, "w") as f:
+            json.dump(prof, f, indent=1)
+    table = CM.evaluate(c, Ns=(64, 256, 1024, 4096))
+    sims = []
+    for mu_L, mu_O in CM.PAPER_MIXES:
+        wl = SIM.Workload(SIM.fixed_inputs(mu_L), SIM.geometric_outputs(mu_O), f"{mu_L}/{mu_O}")
+        for N in (256, 1024):
+            th0 = CM.solve_theta0(c.alpha_p / (c.alpha_d * mu_O))
+            k0 = max(1, int(th0 * N))
+            row = {"mix": f"{mu_L}/{mu_O}", "N": N, "theta0": th0, "k0": k0}
+            for pol in ("eb", "mb", "ebplus"):
+                r = SIM.Simulator(c, wl, SIM.SimCfg(N=N, k=k0, B=8192, policy=pol, max_completions=3000,
+                                                    warmup=300), seed=0).run()
+                row[pol] = {"requests_per_s_per_layer": round(r.throughput, 3),
+                            "eb_iteration_share": round(r.eb_iterations / max(1, r.iterations), 3)}
+            d = CM.compare(c, mu_L, mu_O, N)
+            row["condition_favours"] = "MB" if d.mb_favoured else "EB"
+            sims.append(row)
+            print(f"# mix {mu_L}/{mu_O} N={N}: theta0={th0:.3f} EB {row['eb']['requests_per_s_per_layer']} "
+                  f"MB {row['mb']['requests_per_s_per_layer']} EB+ {row['ebplus']['requests_per_s_per_layer']} "
+                  f"(condition: {row['condition_favours']})", file=sys.stderr, flush=True)
+    return {"calibration": prof, "sweep": {k: sw[k] for k in ("budget", "r", "K_ms", "fit", "crossover_r")
+                                           if k in sw}, "decisions": table, "simulated": sims}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -384,9 +430,27 @@ def main():
                 "ms_per_step": round(out["K_ms"][-1], 5), "higher_is_better": False, "scaling": "weak",
                 "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
                 "config": {"workload": f"llama3-8b-layer MB sweep, budgets {args.budgets}, decode ctx "
-                                       f"{'16' if args.ctx16 else 'U[1024,8192]'}, r = 0..1 step 0.1",
+                                       f"{args.dec_ctx or ('16' if args.ctx16 else '1024,8192')}, r = 0..1 step 0.1",
                            "parallelism": "single-gpu"},
                 "sweep": out, "points": pts, "wall_s": round(wall, 1)}
+        js = json.dumps(line)
+        print(js)
+        if args.json_out:
+            with open(args.json_out, "w") as f:
+                f.write(js + "\n")
+        return
+
+    if args.workload == "policy8b":
+        t0 = time.perf_counter()
+        out = policy8b(args, dev)
+        line = {"metric": METRIC, "value": out["sweep"].get("crossover_r"), "unit": "crossover decode share",
+                "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": None,
+                "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+                "data": "synthetic",
+                "config": {"workload": f"llama3-8b-layer cost model: MB sweep budgets {args.budgets}, decode ctx "
+                                       f"{args.dec_ctx}; decisions and simulated EB / MB / EB+ for the paper's "
+                                       f"mixes", "parallelism": "single-gpu"},
+                **out, "wall_s": round(time.perf_counter() - t0, 1)}
         js = json.dumps(line)
         print(js)
         if args.json_out:
