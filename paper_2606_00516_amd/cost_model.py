@@ -35,7 +35,9 @@ layer count.
 from __future__ import annotations
 
 import dataclasses
+import json
 import math
+import os
 from typing import Dict, Iterable, List, Optional, Sequence, Tuple
 
 import numpy as np
@@ -115,14 +117,12 @@ def calibrate(points: Sequence[dict], label: str = "") -> StepCosts:
     return StepCosts(ap, bp, ad, bd, float(np.mean(inner)), c, label, r2)
 
 
-PROFILE_DIR = __import__("os").path.join(__import__("os").path.dirname(__file__), "calibration")
+PROFILE_DIR = os.path.join(os.path.dirname(os.path.abspath(__file__)), "calibration")
 
 
 def load_profile(path: Optional[str] = None) -> StepCosts:
     """Step costs from a calibration profile written by the benchmark's
     policy workload (default: the MI355X profile of the 8B-shaped layer)."""
-    import json
-    import os
     path = path or os.path.join(PROFILE_DIR, "mi355x_llama3_8b_layer.json")
     with open(path) as f:
         prof = json.load(f)
