@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="decode8b",
                     choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "decode70b", "stack70b", "policy8b",
-                             "copy"])
+                             "long8b", "copy"])
     ap.add_argument("--calib-out", default=None, help="policy8b: write the calibrated step-cost profile here")
     ap.add_argument("--layers", type=int, default=80, help="decoder layers of the stack70b model step")
     ap.add_argument("--stack-r", default="0.2,0.5,0.8", help="decode shares of the stack70b mixed steps")
@@ -389,6 +389,72 @@ def policy8b(args, dev):
                                            if k in sw}, "decisions": table, "simulated": sims}
 
 
+def long8b(args, dev):
+    """Long contexts on the 8B-shaped layer, after the paper's 128K-input /
+    64-output runs (App. A.1): (a) decode steps of 4 requests at contexts
+    near 128K; (b) the 16 chunked-prefill steps of one 128K prompt under an
+    8192-token budget, each chunk attending over the chunks before it;
+    (c) single-iteration prefill of one prompt of 1K..128K tokens (the
+    paper's stress test beyond the budget) with the R^2 of the linear model
+    over the practical range (<= 8K) and over the whole range."""
+    import numpy as np
+    import torch
+
+    from paper_2606_00516_amd import analysis as AN
+    from paper_2606_00516_amd import binding as B
+    from paper_2606_00516_amd import inputs as gen
+    shape = gen.L8B
+    w = gen.make_weights(shape, device=dev)
+    steps = max(2, args.steps // 5)
+
+    def run(batch, mode):
+        pool = gen.make_kv_pool(shape, batch, device=dev, poison=False)
+        x = gen.make_x(shape, batch.num_tokens, device=dev)
+        y = torch.empty_like(x)
+        h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
+        ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
+        fn = {"decode": B.eb_layer_step_decode, "prefill": B.eb_layer_step_prefill}[mode]
+        ms, st = measure(B, h, fn, w, pool, batch, x, y, ws, steps, 1, 1)
+        del pool, x, y, ws, h
+        torch.cuda.empty_cache()
+        wk = step_work(shape, batch)
+        return ms, st, wk
+
+    out = {}
+    c = np.array([131072 - 64 + 16 * j for j in range(4)], np.int32)
+    ms, st, wk = run(gen.Batch(c, np.ones(4, np.int32), "decode128k"), "decode")
+    out["decode_128k"] = {"ms": round(ms, 4), "attention_ms": round(st["attention"], 4),
+                          "attention_hbm_gbps": round(wk["kv_bytes_decode"] / (st["attention"] / 1e3) / 1e9, 1),
+                          "kv_bytes": wk["kv_bytes_decode"]}
+    print(f"# decode at 128K: {ms:.3f} ms/step, attention {st['attention']:.3f} ms "
+          f"({out['decode_128k']['attention_hbm_gbps']} GB/s)", file=sys.stderr, flush=True)
+    chunks = []
+    for i in (0, 4, 8, 12, 15):
+        ms, st, wk = run(gen.Batch(np.array([8192 * i], np.int32), np.array([8192], np.int32), f"chunk{i}"), "prefill")
+        fl = wk["attn_flops_prefill"]
+        chunks.append({"chunk": i, "prefix": 8192 * i, "ms": round(ms, 4), "attention_ms": round(st["attention"], 4),
+                       "attention_tflops": round(fl / (st["attention"] / 1e3) / 1e12, 1),
+                       "gemm_ms": round(sum(v for k, v in st.items() if k.endswith("gemm")), 4)})
+        print(f"# chunk {i} (prefix {8192 * i}): {ms:.3f} ms, attention {st['attention']:.3f} ms "
+              f"({chunks[-1]['attention_tflops']} TFLOP/s)", file=sys.stderr, flush=True)
+    out["chunked_prefill_128k"] = chunks
+    single = []
+    for n in (1024, 2048, 4096, 8192, 16384, 32768, 65536, 131072):
+        ms, st, wk = run(gen.Batch(np.zeros(1, np.int32), np.array([n], np.int32), f"prompt{n}"), "prefill")
+        single.append({"n_tok": n, "ms": round(ms, 4), "attention_ms": round(st["attention"], 4),
+                       "gemm_ms": round(sum(v for k, v in st.items() if k.endswith("gemm")), 4)})
+        print(f"# single prompt {n}: {ms:.3f} ms (attention {st['attention']:.3f})", file=sys.stderr, flush=True)
+    xs = [p["n_tok"] for p in single]
+    ys = [p["ms"] for p in single]
+    small = [i for i, v in enumerate(xs) if v <= 8192]
+    a8, b8, r2_8 = AN.linear_fit([xs[i] for i in small], [ys[i] for i in small])
+    aa, ba, r2_all = AN.linear_fit(xs, ys)
+    out["single_prompt"] = single
+    out["linear_fit"] = {"r2_le_8k": r2_8, "r2_all": r2_all, "beta_ms_per_token_le_8k": b8,
+                         "beta_ms_per_token_all": ba}
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -433,6 +499,24 @@ def main():
                                        f"{args.dec_ctx or ('16' if args.ctx16 else '1024,8192')}, r = 0..1 step 0.1",
                            "parallelism": "single-gpu"},
                 "sweep": out, "points": pts, "wall_s": round(wall, 1)}
+        js = json.dumps(line)
+        print(js)
+        if args.json_out:
+            with open(args.json_out, "w") as f:
+                f.write(js + "\n")
+        return
+
+    if args.workload == "long8b":
+        t0 = time.perf_counter()
+        out = long8b(args, dev)
+        d = out["decode_128k"]
+        line = {"metric": METRIC, "value": d["attention_hbm_gbps"], "unit": "GB/s", "n_gpus": 1,
+                "steps": args.steps, "warmup": 1, "ms_per_step": d["ms"], "higher_is_better": True,
+                "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+                "config": {"workload": "llama3-8b layer, 128K contexts: decode of 4 requests, chunked prefill of a "
+                                       "128K prompt (8192-token chunks), single-iteration prompts 1K..128K",
+                           "parallelism": "single-gpu"},
+                **out, "wall_s": round(time.perf_counter() - t0, 1)}
         js = json.dumps(line)
         print(js)
         if args.json_out:

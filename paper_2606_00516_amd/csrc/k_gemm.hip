@@ -514,7 +514,9 @@ static int skinny_splits(int M, int N, int K) {
 GemmPlan plan_gemm(int M, int N, int K, int epi) {
   GemmPlan p{};
   const int ncols = logical_cols(N, epi);
-  const bool fits = (size_t)M * K * 2 < ((size_t)1 << 31) && (size_t)N * K * 2 < ((size_t)1 << 31);
+  // the big kernel addresses W through a 32-bit buffer range; A is cut into
+  // row chunks that each fit one (launch_gemm)
+  const bool fits = (size_t)N * K * 2 < ((size_t)1 << 31) && (size_t)BG_BM * K * 2 < ((size_t)1 << 31);
   // 256 x 256 tiles once the grid covers at least half the CUs
   const long big_tiles = (long)((M + BG_BM - 1) / BG_BM) * ((ncols + BG_BN - 1) / BG_BN);
   if (K % BG_BK == 0 && N % 8 == 0 && fits && M >= 256 && big_tiles >= 128) {
@@ -556,11 +558,21 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, 
     return hipGetLastError();
   }
   if (p.kind == 2) {
-    const int tm = (M + BG_BM - 1) / BG_BM, tn = (ncols + BG_BN - 1) / BG_BN;
-    const int per_xcd = (tm * tn + 7) / 8;
-    hipLaunchKernelGGL(k_gemm_big, dim3(8 * per_xcd), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A, W, out, res, M, N, K, epi,
-                       tm, tn, per_xcd);
-    return hipGetLastError();
+    // rows per launch: A's slice must stay inside a 32-bit buffer range
+    const size_t rows_fit = ((((size_t)1 << 31) - 1) / ((size_t)K * 2)) / BG_BM * BG_BM;
+    const int chunk = (int)(rows_fit < (size_t)M ? rows_fit : (size_t)M);
+    const size_t out_cols = epi == EPI_SILU_MUL ? (size_t)N / 2 : (size_t)N;
+    for (int m0 = 0; m0 < M; m0 += chunk) {
+      const int mc = M - m0 < chunk ? M - m0 : chunk;
+      const int tm = (mc + BG_BM - 1) / BG_BM, tn = (ncols + BG_BN - 1) / BG_BN;
+      const int per_xcd = (tm * tn + 7) / 8;
+      hipLaunchKernelGGL(k_gemm_big, dim3(8 * per_xcd), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A + (size_t)m0 * K, W,
+                         out + (size_t)m0 * out_cols, res ? res + (size_t)m0 * N : nullptr, mc, N, K, epi, tm, tn,
+                         per_xcd);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
   }
   const int tiles_m = (M + TL_BM - 1) / TL_BM, tiles_n = (ncols + TL_BN - 1) / TL_BN;
   hipLaunchKernelGGL(k_gemm_tiled, dim3(tiles_m * tiles_n), dim3(256), 0, st, A, W, out, res, M, N, K, epi, tiles_m,
