@@ -667,16 +667,26 @@ __global__ __launch_bounds__(64) void k_decode_combine(DevMeta md, const float *
 // shared out over NW wavefronts (8 in the prefill-only launch, 4 inside the
 // mixed launch).  Keys and values stream through LDS in tiles of 64
 // positions gathered from 4 pages; the next tile's global loads are issued
-// before the current tile is consumed.  Scores are formed transposed,
+// before the current tile is consumed, and a wave holding several row blocks
+// reads each K and V^T fragment once for all of them.  Scores are formed
+// transposed,
 // S^T = K Q^T, with the 16x16x32 bf16 MFMA, so a lane holds one query column
 // and the row max needs only two cross-lane steps; P^T stays in registers as
 // the B operand of O^T = V^T P^T (keys permuted consistently on both
 // operands), with V^T staged in LDS.  A row's arithmetic does not depend on
 // which item it sits in, so both launches give the same bits.
 // ===========================================================================
-template <int HD, int G, int NW>
+// Query positions per prefill item: 128 rows (G heads x 128/G positions) in
+// the prefill-only launch, 64 rows (at most 16 positions) inside the mixed
+// launch; the planner's prefill_bq() gives the same numbers.
+template <int G, bool MIXED>
+constexpr int prefill_item_positions() {
+  return MIXED ? (G >= 4 ? 16 : 64 / G) : 128 / G;
+}
+
+template <int HD, int G, int NW, int BQ_>
 struct PrefillTraits {
-  static constexpr int BQ = NW == 8 ? 128 / G : (G >= 4 ? 16 : 64 / G);  // query positions per item
+  static constexpr int BQ = BQ_;                 // query positions per item
   static constexpr int RB = (G * BQ / 16) / NW;  // 16-row blocks per wavefront
   static constexpr int KT = 64;                  // keys per tile
   static constexpr int KS_STRIDE = HD + 8;       // bf16 elements per K row in LDS
@@ -691,11 +701,11 @@ struct PrefillTraits {
   static_assert(RB >= 1 && RB * NW * 16 == G * BQ, "row blocks");
 };
 
-template <int HD, int G, int NW>
+template <int HD, int G, int NW, int BQ_>
 __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
                                              const DevMeta md, int tile, int kh, uint16_t *__restrict__ out,
                                              uint16_t *Ks, uint16_t *Vt) {
-  using Tr = PrefillTraits<HD, G, NW>;
+  using Tr = PrefillTraits<HD, G, NW, BQ_>;
   constexpr int BQ = Tr::BQ, RB = Tr::RB, KT = Tr::KT, KSS = Tr::KS_STRIDE, VTS = Tr::VT_STRIDE;
   constexpr int KCH = Tr::KCH, VCH = Tr::VCH, KPT = Tr::KPT, VPT = Tr::VPT;
   constexpr int NKS = HD / 32;  // k-steps of the QK^T product
@@ -803,69 +813,87 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
     stage();
     __syncthreads();
     if (t + 1 < ntiles) fetch(t + 1);   // in flight while this tile is consumed
+    // S^T blocks of every row block (keys k0 + 16 kb + 4 lg + j, query
+    // column lq): a K fragment is read from LDS once for all RB blocks
+    f32x4_t sc[RB][4];
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb) sc[i][kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        const u32x4_t a = ld_u32x4(Ks + (kb * 16 + lq) * KSS + ks * 32 + lg * 8);
+#pragma unroll
+        for (int i = 0; i < RB; ++i) sc[i][kb] = mfma16x16x32(a, qreg[i][ks], sc[i][kb]);
+      }
+    uint32_t pk[RB][4][2];
+    float alpha[RB];
+    bool rescale[RB];
 #pragma unroll
     for (int i = 0; i < RB; ++i) {
       const bool need_mask = (k0 + KT - 1) > min_qpos || !qok[i];
       const int qpos = c + qrel[i];
-      // S^T block kb: keys k0 + 16 kb + 4 lg + j, query column lq
-      f32x4_t sc[4];
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        sc[kb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-          const u32x4_t a = ld_u32x4(Ks + (kb * 16 + lq) * KSS + ks * 32 + lg * 8);
-          sc[kb] = mfma16x16x32(a, qreg[i][ks], sc[kb]);
-        }
-      }
-      float mx = mrun[i];
+      // the max is taken on the raw scores (qscale > 0 keeps the order and
+      // the rounding), the scale enters the exponent through one fma
+      float mraw = kNegInf;
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          float v = sc[kb][j] * qscale;
           if (need_mask) {
             const int kp = k0 + kb * 16 + lg * 4 + j;
-            if (kp > qpos || !qok[i]) v = kNegInf;
+            if (kp > qpos || !qok[i]) sc[i][kb][j] = kNegInf;
           }
-          sc[kb][j] = v;
-          mx = fmaxf(mx, v);
+          mraw = fmaxf(mraw, sc[i][kb][j]);
         }
-      mx = fmaxf(mx, shfl_xor_f32(mx, 16));
-      mx = fmaxf(mx, shfl_xor_f32(mx, 32));
-      const float alpha = (mrun[i] == kNegInf) ? 0.f : fast_exp2(mrun[i] - mx);
-      const bool live = mx != kNegInf;
-      float l = lrun[i] * alpha;
-      uint32_t pk[4][2];
+      mraw = fmaxf(mraw, shfl_xor_f32(mraw, 16));
+      mraw = fmaxf(mraw, shfl_xor_f32(mraw, 32));
+      const float mx = fmaxf(mrun[i], mraw * qscale);
+      alpha[i] = (mrun[i] == kNegInf) ? 0.f : fast_exp2(mrun[i] - mx);
+      // masked scores are -inf, so exp2 gives 0 without a select; a row with
+      // nothing visible yet keeps an offset of 0
+      const float neg = mx != kNegInf ? -mx : 0.f;
+      float l = lrun[i] * alpha[i];
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) {
         float p4[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          p4[j] = (live && sc[kb][j] != kNegInf) ? fast_exp2(sc[kb][j] - mx) : 0.f;
+          p4[j] = fast_exp2(fmaf(sc[i][kb][j], qscale, neg));
           l += p4[j];
         }
-        pk[kb][0] = pack_bf16x2(p4[0], p4[1]);
-        pk[kb][1] = pack_bf16x2(p4[2], p4[3]);
+        pk[i][kb][0] = bf16_pair_rne(p4[0], p4[1]);
+        pk[i][kb][1] = bf16_pair_rne(p4[2], p4[3]);
       }
       lrun[i] = l;
       mrun[i] = mx;
+      // scaling by exactly 1 changes nothing: skip it while no lane's max moved
+      rescale[i] = __builtin_amdgcn_ballot_w64(alpha[i] != 1.0f) != 0;
+    }
+    // O^T += V^T P^T: a V^T fragment is read once for all RB blocks
 #pragma unroll
-      for (int ob = 0; ob < NOB; ++ob) {
-        f32x4_t acc = oacc[i][ob] * alpha;
+    for (int ob = 0; ob < NOB; ++ob) {
+      f32x4_t acc[RB];
 #pragma unroll
-        for (int ks2 = 0; ks2 < 2; ++ks2) {
-          // B (P^T): keys {4 lg .. +3} of block 2 ks2, then of block 2 ks2 + 1
-          const u32x4_t b = {pk[2 * ks2][0], pk[2 * ks2][1], pk[2 * ks2 + 1][0], pk[2 * ks2 + 1][1]};
-          // A (V^T): dim ob*16 + lq, the same keys
-          const uint16_t *vrow = Vt + (ob * 16 + lq) * VTS + ks2 * 32 + lg * 4;
-          const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vrow);
-          const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vrow + 16);
-          const u32x4_t a = {a0[0], a0[1], a1[0], a1[1]};
-          acc = mfma16x16x32(a, b, acc);
+      for (int i = 0; i < RB; ++i) acc[i] = rescale[i] ? oacc[i][ob] * alpha[i] : oacc[i][ob];
+#pragma unroll
+      for (int ks2 = 0; ks2 < 2; ++ks2) {
+        // A (V^T): dim ob*16 + lq, keys {4 lg .. +3} of block 2 ks2, then of
+        // block 2 ks2 + 1; B (P^T): the same keys
+        const uint16_t *vrow = Vt + (ob * 16 + lq) * VTS + ks2 * 32 + lg * 4;
+        const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vrow);
+        const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vrow + 16);
+        const u32x4_t a = {a0[0], a0[1], a1[0], a1[1]};
+#pragma unroll
+        for (int i = 0; i < RB; ++i) {
+          const u32x4_t b = {pk[i][2 * ks2][0], pk[i][2 * ks2][1], pk[i][2 * ks2 + 1][0], pk[i][2 * ks2 + 1][1]};
+          acc[i] = mfma16x16x32(a, b, acc[i]);
         }
-        oacc[i][ob] = acc;
       }
+#pragma unroll
+      for (int i = 0; i < RB; ++i) oacc[i][ob] = acc[i];
     }
     __syncthreads();
   }
@@ -918,13 +946,20 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode_mfma(const uint16_t *
                                                 l3);
 }
 
+// Prefill-only launch: 8 wavefronts per 128-row item, one 16-row block per
+// wave.  (Two blocks per wave in 4-wave items halve the LDS reads per MFMA
+// but measure slower: a wave's serial softmax -> product chain, not LDS
+// bandwidth, bounds the tile loop.)
+constexpr int kPrefillWaves = 8;
+
 template <int HD, int G>
-__global__ __launch_bounds__(512) void k_prefill(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
-                                                 uint16_t *out) {
-  using Tr = PrefillTraits<HD, G, 8>;
+__global__ __launch_bounds__(64 * kPrefillWaves) void k_prefill(const uint16_t *qkv, int nq, int nkv, KV kv,
+                                                                   DevMeta md, uint16_t *out) {
+  constexpr int BQ = prefill_item_positions<G, false>();
+  using Tr = PrefillTraits<HD, G, kPrefillWaves, BQ>;
   __shared__ __attribute__((aligned(16))) uint16_t lds[Tr::LDS_BYTES / 2];
-  prefill_item<HD, G, 8>(qkv, nq, nkv, kv, md, blockIdx.x / nkv, blockIdx.x % nkv, out, lds,
-                         lds + Tr::KS_BYTES / 2);
+  prefill_item<HD, G, kPrefillWaves, BQ>(qkv, nq, nkv, kv, md, blockIdx.x / nkv, blockIdx.x % nkv, out, lds,
+                                         lds + Tr::KS_BYTES / 2);
 }
 
 // One grid for a mixed step: items [0, n_tiles) are prefill tiles (longest
@@ -933,12 +968,13 @@ __global__ __launch_bounds__(512) void k_prefill(const uint16_t *qkv, int nq, in
 template <int HD, int G>
 __global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
                                                float *part_o, float *part_ml) {
-  using Tr = PrefillTraits<HD, G, 4>;
+  constexpr int BQ = prefill_item_positions<G, true>();
+  using Tr = PrefillTraits<HD, G, 4, BQ>;
   constexpr int PB = Tr::LDS_BYTES, DB = DecodeTraits<HD, G, 4>::LDS_BYTES;
   __shared__ __attribute__((aligned(16))) uint16_t lds[(PB > DB ? PB : DB) / 2];
   const int b = blockIdx.x;
   if (b < md.n_tiles * nkv)
-    prefill_item<HD, G, 4>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, lds, lds + Tr::KS_BYTES / 2);
+    prefill_item<HD, G, 4, BQ>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, lds, lds + Tr::KS_BYTES / 2);
   else
     decode_item<HD, G, 4>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml,
                           reinterpret_cast<float *>(lds));
@@ -949,14 +985,15 @@ __global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int 
 template <int HD, int G>
 __global__ __launch_bounds__(256) void k_mixed_mfma(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
                                                     uint16_t *out, float *part_o, float *part_ml) {
-  using Tr = PrefillTraits<HD, G, 4>;
+  constexpr int BQ = prefill_item_positions<G, true>();
+  using Tr = PrefillTraits<HD, G, 4, BQ>;
   constexpr int MS = 2;  // ring depth of decode items in the mixed launch
   static_assert(Tr::KS_BYTES <= MdecBlock<HD, 4, MS>::SLOT_ARRAY && Tr::VT_BYTES <= MdecBlock<HD, 4, MS>::SLOT_ARRAY,
                 "LDS");
   EB_MDEC_LDS(HD, 4, MS)
   const int b = blockIdx.x;
   if (b < md.n_tiles * nkv)
-    prefill_item<HD, G, 4>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, reinterpret_cast<uint16_t *>(l0),
+    prefill_item<HD, G, 4, BQ>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, reinterpret_cast<uint16_t *>(l0),
                            reinterpret_cast<uint16_t *>(l1));
   else
     decode_item_mfma<HD, G, 4, MS>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml, l0, l1, l2,
@@ -981,7 +1018,8 @@ static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const 
                          kv, m, out, part_o, part_ml);
   } else {
     if (has_pf)
-      hipLaunchKernelGGL((k_prefill<HD, G>), dim3(m.n_tiles * nkv), dim3(512), 0, st, qkv, nq, nkv, kv, m, out);
+      hipLaunchKernelGGL((k_prefill<HD, G>), dim3(m.n_tiles * nkv), dim3(64 * kPrefillWaves), 0, st, qkv, nq, nkv,
+                         kv, m, out);
     if (has_dec) {
       if constexpr (kDecodeMfma<G>)
         hipLaunchKernelGGL((k_decode_mfma<HD, G>), dim3(m.total_units), dim3(64 * kDecWaves), 0, st, qkv, nq, nkv,
