@@ -684,6 +684,17 @@ constexpr int prefill_item_positions() {
   return MIXED ? (G >= 4 ? 16 : 64 / G) : 128 / G;
 }
 
+// V^T in LDS: row = head dimension, 68 bf16 per row; the 8-byte group of
+// keys 4 g .. 4 g + 3 of row r sits at group g ^ ((r >> 4) & 7).  LDS
+// serves 128 bytes per pass over 32 banks: without the exchange the
+// transposing 4-byte stores (16 row groups x 2 key pairs per pass) hit 4
+// banks 8 times each; with it they spread over all 32, while the 8-byte
+// operand reads (16 rows per pass, 68-wide rows put consecutive rows 8
+// bytes apart modulo 128) stay conflict free.  Within the operand loop the
+// exchange depends only on the 16-row block, so each read keeps a constant
+// offset from one of four per-lane bases.
+__device__ __forceinline__ int vt_col(int r, int key) { return 4 * ((key >> 2) ^ ((r >> 4) & 7)) + (key & 3); }
+
 template <int HD, int G, int NW, int BQ_>
 struct PrefillTraits {
   static constexpr int BQ = BQ_;                 // query positions per item
@@ -795,11 +806,13 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
       const int u = tid + i * NT;
       if (u < VCH) {
         const int kpair = u / (HD / 8), dc = u % (HD / 8);
+        // rows dc * 8 .. + 7 share one group exchange (see vt_col)
+        const int col = vt_col(dc * 8, 2 * kpair);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const uint32_t a0 = vreg[i][0][j], a1 = vreg[i][1][j];
-          *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j) * VTS + 2 * kpair) = (a0 & 0xFFFFu) | (a1 << 16);
-          *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j + 1) * VTS + 2 * kpair) = (a0 >> 16) | (a1 & 0xFFFF0000u);
+          *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j) * VTS + col) = (a0 & 0xFFFFu) | (a1 << 16);
+          *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j + 1) * VTS + col) = (a0 >> 16) | (a1 & 0xFFFF0000u);
         }
       }
     }
@@ -882,9 +895,10 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
       for (int ks2 = 0; ks2 < 2; ++ks2) {
         // A (V^T): dim ob*16 + lq, keys {4 lg .. +3} of block 2 ks2, then of
         // block 2 ks2 + 1; B (P^T): the same keys
-        const uint16_t *vrow = Vt + (ob * 16 + lq) * VTS + ks2 * 32 + lg * 4;
-        const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vrow);
-        const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vrow + 16);
+        const int vr = ob * 16 + lq;
+        const uint16_t *vrow = Vt + vr * VTS;
+        const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vrow + vt_col(vr, ks2 * 32 + lg * 4));
+        const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vrow + vt_col(vr, ks2 * 32 + lg * 4 + 16));
         const u32x4_t a = {a0[0], a0[1], a1[0], a1[1]};
 #pragma unroll
         for (int i = 0; i < RB; ++i) {
