@@ -766,32 +766,67 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
     for (int ob = 0; ob < NOB; ++ob) oacc[i][ob] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  // global -> register staging of one K/V tile (keys past c + n read as 0)
-  u32x4_t kreg[KPT], vreg[VPT][2];
-  auto cache_addr = [&](int kp) -> long {
-    if (kp >= klen) return -1;
-    const int pg = kp / kPageSize;
-    const int phys = pg < npages ? bt[pg] : -1;
-    if (phys < 0 || phys >= kv.num_pages) return -1;
-    return (((long)phys * nkv + kh) * kPageSize + kp % kPageSize) * HD;
+  // global -> register staging of one K/V tile (keys past c + n read as 0).
+  // A tile's 64 keys sit in 4 pages; their block-table entries are loaded
+  // together one tile ahead of the data loads that use them, so a tile's
+  // gather costs one memory round trip, overlapped with the previous tile's
+  // products.  Every load reads a valid address (position 0 of the cache for
+  // an absent key) and the result is zeroed afterwards: no divergent branch.
+  typedef int i32x4_t __attribute__((ext_vector_type(4)));
+  constexpr int PPT = KT / kPageSize;  // pages per tile
+  static_assert(PPT == 4, "tile = 4 pages");
+  // the block table is read-only here: through the constant address space
+  // the entries (uniform per tile) come by scalar loads into scalar
+  // registers, counted apart from the vector loads of K and V
+  typedef const __attribute__((address_space(4))) int32_t *bt_ptr_t;
+  const bt_ptr_t btc = (bt_ptr_t)bt;
+  auto bt_tile = [&](int t) -> i32x4_t {
+    const int p0 = t * PPT;
+    i32x4_t r = {-1, -1, -1, -1};
+#pragma unroll
+    for (int j = 0; j < PPT; ++j)
+      if (p0 + j < npages) r[j] = btc[p0 + j];
+    return r;
   };
-  auto fetch = [&](int t) {
+  u32x4_t kreg[KPT], vreg[VPT][2];
+  uint32_t present = 0;  // bit i: K load i, bit KPT + 2 i + e: V load (i, e)
+  // The lanes of one load instruction cover 64 / (HD / 8) consecutive keys
+  // of K (or twice that of V), all in one page: the page, its validity and
+  // its base address are wave-uniform (scalar registers); a lane adds only
+  // its row and chunk.  An absent page reads page block 0 and is zeroed.
+  static_assert(HD == 64 || HD == 128, "keys of one load within one page");
+  auto page_base = [&](const uint16_t *arr, const i32x4_t &btv, int j, bool &ok) -> const uint16_t * {
+    const int phys = j == 0 ? btv[0] : j == 1 ? btv[1] : j == 2 ? btv[2] : btv[3];
+    ok = phys >= 0 && phys < kv.num_pages;
+    return arr + (ok ? ((size_t)phys * nkv + kh) * (kPageSize * HD) : 0);
+  };
+  // the data of absent keys is zeroed when staged (zeroing right after the
+  // load would wait for it)
+  auto fetch = [&](int t, const i32x4_t &btv) {
     const int k0 = t * KT;
+    present = 0;
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int u = tid + i * NT;
       const int key = u / (HD / 8), dc = u % (HD / 8);
-      const long a = u < KCH ? cache_addr(k0 + key) : -1;
-      kreg[i] = a >= 0 ? ld_u32x4(kv.k + a + dc * 8) : u32x4_t{0, 0, 0, 0};
+      const int j = __builtin_amdgcn_readfirstlane(key / kPageSize);
+      bool pok;
+      const uint16_t *pb = page_base(kv.k, btv, j, pok);
+      kreg[i] = ld_u32x4(pb + (key % kPageSize) * HD + dc * 8);
+      present |= (u < KCH && pok && k0 + key < klen ? 1u : 0u) << i;
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int u = tid + i * NT;
       const int kpair = u / (HD / 8), dc = u % (HD / 8);
+      const int j = __builtin_amdgcn_readfirstlane((2 * kpair) / kPageSize);
+      bool pok;
+      const uint16_t *pb = page_base(kv.v, btv, j, pok);
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const long a = u < VCH ? cache_addr(k0 + 2 * kpair + e) : -1;
-        vreg[i][e] = a >= 0 ? ld_u32x4(kv.v + a + dc * 8) : u32x4_t{0, 0, 0, 0};
+        const int key = 2 * kpair + e;
+        vreg[i][e] = ld_u32x4(pb + (key % kPageSize) * HD + dc * 8);
+        present |= (u < VCH && pok && k0 + key < klen ? 1u : 0u) << (KPT + 2 * i + e);
       }
     }
   };
@@ -799,7 +834,9 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int u = tid + i * NT;
-      if (u < KCH) st_u32x4(Ks + (u / (HD / 8)) * KSS + (u % (HD / 8)) * 8, kreg[i]);
+      if (u < KCH)
+        st_u32x4(Ks + (u / (HD / 8)) * KSS + (u % (HD / 8)) * 8,
+                 (present >> i) & 1u ? kreg[i] : u32x4_t{0, 0, 0, 0});
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
@@ -808,9 +845,10 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
         const int kpair = u / (HD / 8), dc = u % (HD / 8);
         // rows dc * 8 .. + 7 share one group exchange (see vt_col)
         const int col = vt_col(dc * 8, 2 * kpair);
+        const bool p0 = (present >> (KPT + 2 * i)) & 1u, p1 = (present >> (KPT + 2 * i + 1)) & 1u;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const uint32_t a0 = vreg[i][0][j], a1 = vreg[i][1][j];
+          const uint32_t a0 = p0 ? vreg[i][0][j] : 0u, a1 = p1 ? vreg[i][1][j] : 0u;
           *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j) * VTS + col) = (a0 & 0xFFFFu) | (a1 << 16);
           *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j + 1) * VTS + col) = (a0 >> 16) | (a1 & 0xFFFF0000u);
         }
@@ -820,12 +858,17 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
 
   const int min_qpos = c + q_lo;
   const int ntiles = (kend + KT - 1) / KT;
-  fetch(0);
+  i32x4_t bt_next = bt_tile(1);
+  fetch(0, bt_tile(0));
   for (int t = 0; t < ntiles; ++t) {
     const int k0 = t * KT;
     stage();
     __syncthreads();
-    if (t + 1 < ntiles) fetch(t + 1);   // in flight while this tile is consumed
+    if (t + 1 < ntiles) {  // in flight while this tile is consumed
+      const i32x4_t bt_cur = bt_next;
+      bt_next = bt_tile(t + 2);
+      fetch(t + 1, bt_cur);
+    }
     // S^T blocks of every row block (keys k0 + 16 kb + 4 lg + j, query
     // column lq): a K fragment is read from LDS once for all RB blocks
     f32x4_t sc[RB][4];
