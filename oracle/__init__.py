@@ -19,3 +19,4 @@ from .layer import (  # noqa: F401
     prepare_weights,
     LayerCfg,
 )
+from . import fp8  # noqa: F401,E402  (E4M3 cache codes)
