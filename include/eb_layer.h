@@ -86,16 +86,32 @@ typedef struct eb_layer_weights {
   const void *attn_norm, *w_qkv, *w_o, *mlp_norm, *w_gate_up, *w_down;
 } eb_layer_weights;
 
-/* Paged KV cache (device).  k_cache, v_cache: bf16 [num_pages, n_kv_heads,
- * page_size, head_dim].  block_tables: int32 [num_seqs, max_pages_per_seq];
- * logical page j of request i is physical page block_tables[i][j].  Entries
- * past a request's last needed page are never read.  The library never
- * allocates or frees pages. */
+/* Element type of the KV cache. */
+typedef enum {
+  EB_KV_BF16 = 0,     /* bf16 values */
+  EB_KV_FP8_E4M3 = 1  /* 8-bit codes, OCP E4M3 (bias 7, no infinity, 0x7F/0xFF NaN, largest finite 448) */
+} eb_kv_dtype;
+
+/* Paged KV cache (device).  k_cache, v_cache: [num_pages, n_kv_heads,
+ * page_size, head_dim] elements of kv_dtype.  block_tables: int32
+ * [num_seqs, max_pages_per_seq]; logical page j of request i is physical
+ * page block_tables[i][j].  Entries past a request's last needed page are
+ * never read.  The library never allocates or frees pages.
+ *
+ * An 8-bit cache halves the bytes a decode step streams (decode attention
+ * reads every cached position of every decode request: Sec. 1, App. A.2).
+ * A cached code stands for decode(code) * scale (k_scale for keys, v_scale
+ * for values); the step stores e4m3(bf16(x) / scale), the division rounded in
+ * fp32, nearest-even, saturated to +-448 (NaN keeps its sign: 0x7F / 0xFF).
+ * Scales must be finite and positive for EB_KV_FP8_E4M3 and are ignored for
+ * bf16; a zero-initialised struct is a bf16 cache. */
 typedef struct eb_kv_cache {
   void *k_cache, *v_cache;
   int32_t num_pages;
   const int32_t *block_tables;
   int32_t max_pages_per_seq;
+  int32_t kv_dtype; /* eb_kv_dtype */
+  float k_scale, v_scale;
 } eb_kv_cache;
 
 /* One step's requests.  context_lens_host[i] = c_i, tokens already cached
@@ -211,8 +227,9 @@ eb_status eb_op_attention(eb_handle *h, const void *qkv, const eb_kv_cache *kv, 
                           void *out, void *ws, size_t ws_bytes, eb_mode mode, void *stream);
 
 /* Dense copy of every request's cached positions 0 .. c_i + n_i - 1 through
- * its block table: out_k, out_v bf16 [sum_i (c_i + n_i), n_kv_heads,
- * head_dim], requests in order.  Pure paging: bit-exact. */
+ * its block table: out_k, out_v [sum_i (c_i + n_i), n_kv_heads, head_dim]
+ * elements of the cache's type (bf16, or the raw 8-bit codes), requests in
+ * order.  Pure paging: bit-exact. */
 eb_status eb_op_gather_kv(eb_handle *h, const eb_kv_cache *kv, const eb_batch *batch, void *out_k,
                           void *out_v, void *ws, size_t ws_bytes, void *stream);
 

@@ -34,9 +34,11 @@ invariances.
 from __future__ import annotations
 
 import dataclasses
-from typing import Dict, Optional, Sequence
+from typing import Dict, Optional, Sequence, Tuple
 
 import numpy as np
+
+from . import fp8
 
 
 @dataclasses.dataclass(frozen=True)
@@ -114,25 +116,34 @@ def silu(z: np.ndarray) -> np.ndarray:
 # ----------------------------------------------------------------------------
 
 def gather_positions(cache_bits: np.ndarray, bt_row: np.ndarray, npos: int, page: int,
-                     dtype=np.float32) -> np.ndarray:
+                     dtype=np.float32, scale: Optional[float] = None) -> np.ndarray:
     """Positions 0..npos-1 of one request from the paged cache.
 
-    cache_bits: [num_pages, n_kv, page, hd] bf16 bits.  Logical position p of
-    the request lives in physical page bt_row[p // page], slot p % page.
+    cache_bits: [num_pages, n_kv, page, hd] bf16 bits, or 8-bit E4M3 codes
+    when ``scale`` is given (values decode(code) * scale).  Logical position
+    p of the request lives in physical page bt_row[p // page], slot p % page.
     Returns [npos, n_kv, hd].
     """
     p = np.arange(npos)
     phys = np.asarray(bt_row)[p // page]
     slot = p % page
+    if scale is not None:
+        return fp8.dequantize(cache_bits[phys, :, slot, :], scale).astype(dtype)
     return bf16_bits_to_f32(cache_bits[phys, :, slot, :]).astype(dtype)
 
 
 def append_kv(cache_bits: np.ndarray, bt_row: np.ndarray, positions: np.ndarray, vals: np.ndarray,
-              page: int) -> None:
-    """Write vals [rows, n_kv, hd] (rounded to bf16) at the given positions."""
+              page: int, scale: Optional[float] = None) -> None:
+    """Write vals [rows, n_kv, hd] (rounded to bf16) at the given positions;
+    with ``scale``, the cache holds 8-bit codes of the bf16 values divided by
+    the scale."""
     positions = np.asarray(positions)
     phys = np.asarray(bt_row)[positions // page]
-    cache_bits[phys, :, positions % page, :] = f32_to_bf16_bits(vals.astype(np.float32))
+    b = f32_to_bf16_bits(vals.astype(np.float32))
+    if scale is not None:
+        cache_bits[phys, :, positions % page, :] = fp8.quantize_cache_value(bf16_bits_to_f32(b), scale)
+    else:
+        cache_bits[phys, :, positions % page, :] = b
 
 
 def attend_one(q: np.ndarray, keys: np.ndarray, vals: np.ndarray) -> np.ndarray:
@@ -146,13 +157,14 @@ def attend_one(q: np.ndarray, keys: np.ndarray, vals: np.ndarray) -> np.ndarray:
 
 
 def paged_attention_row(q: np.ndarray, k_cache: np.ndarray, v_cache: np.ndarray, bt_row: np.ndarray,
-                        pos: int, page: int, group: int) -> np.ndarray:
+                        pos: int, page: int, group: int, kv_scales=None) -> np.ndarray:
     """Attention of one query row at position pos over keys 0..pos.
 
     q: [n_q, hd].  Query head h reads kv head h // group.  Returns [n_q, hd].
     """
-    K = gather_positions(k_cache, bt_row, pos + 1, page, q.dtype)
-    V = gather_positions(v_cache, bt_row, pos + 1, page, q.dtype)
+    ks, vs = kv_scales if kv_scales is not None else (None, None)
+    K = gather_positions(k_cache, bt_row, pos + 1, page, q.dtype, ks)
+    V = gather_positions(v_cache, bt_row, pos + 1, page, q.dtype, vs)
     out = np.empty_like(q)
     for h in range(q.shape[0]):
         g = h // group
@@ -206,8 +218,9 @@ def prepare_weights(w_bits: Dict[str, np.ndarray], cfg: LayerCfg, dtype=np.float
 def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
                block_tables: np.ndarray, context_lens: Sequence[int], chunk_lens: Sequence[int],
                x_bits: np.ndarray, mode: str = "batched", seqs: Optional[Sequence[int]] = None,
-               intermediates: bool = False):
-    """One decoder-layer step.  Mutates k_cache / v_cache (bf16 bits) in place.
+               intermediates: bool = False, kv_scales: Optional[Tuple[float, float]] = None):
+    """One decoder-layer step.  Mutates k_cache / v_cache (bf16 bits, or
+    8-bit E4M3 codes when kv_scales = (k_scale, v_scale) is given) in place.
 
     Rows of request i are x rows off_i .. off_i + n_i - 1 (off = exclusive
     prefix sum of chunk_lens) at positions c_i .. c_i + n_i - 1.  ``seqs``
@@ -220,6 +233,7 @@ def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
     causal mask.  Returns y [T, hidden] and, if asked, a dict of the
     intermediates q, k, v (after RoPE), attn, h1, m.
     """
+    ks, vs = kv_scales if kv_scales is not None else (None, None)
     dtype = W["wq"].dtype
     nq, nkv, hd, G, P = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.group, cfg.page_size
     ctx = np.asarray(context_lens, np.int64)
@@ -242,9 +256,9 @@ def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
                 q = rope((W["wq"] @ a).reshape(nq, hd), pos, cfg.rope_theta)
                 k = rope((W["wk"] @ a).reshape(nkv, hd), pos, cfg.rope_theta)
                 v = (W["wv"] @ a).reshape(nkv, hd)
-                append_kv(k_cache, bt, np.array([pos]), k[None], P)
-                append_kv(v_cache, bt, np.array([pos]), v[None], P)
-                o = paged_attention_row(q, k_cache, v_cache, bt, pos, P, G).reshape(-1)
+                append_kv(k_cache, bt, np.array([pos]), k[None], P, ks)
+                append_kv(v_cache, bt, np.array([pos]), v[None], P, vs)
+                o = paged_attention_row(q, k_cache, v_cache, bt, pos, P, G, kv_scales).reshape(-1)
                 h1 = x[r] + W["wo"] @ o
                 b = rmsnorm(h1, W["g2"], cfg.rms_eps)
                 m = silu(W["wg"] @ b) * (W["wu"] @ b)
@@ -259,10 +273,10 @@ def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
             q = rope((a @ W["wq"].T).reshape(n, nq, hd), pos, cfg.rope_theta)
             k = rope((a @ W["wk"].T).reshape(n, nkv, hd), pos, cfg.rope_theta)
             v = (a @ W["wv"].T).reshape(n, nkv, hd)
-            append_kv(k_cache, bt, pos, k, P)
-            append_kv(v_cache, bt, pos, v, P)
-            K = gather_positions(k_cache, bt, c + n, P, dtype)
-            V = gather_positions(v_cache, bt, c + n, P, dtype)
+            append_kv(k_cache, bt, pos, k, P, ks)
+            append_kv(v_cache, bt, pos, v, P, vs)
+            K = gather_positions(k_cache, bt, c + n, P, dtype, ks)
+            V = gather_positions(v_cache, bt, c + n, P, dtype, vs)
             o = causal_attention_seq(q, K, V, pos, G).reshape(n, nq * hd)
             h1 = x[rows] + o @ W["wo"].T
             b = rmsnorm(h1, W["g2"], cfg.rms_eps)
@@ -278,7 +292,8 @@ def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
 
 def stack_step(cfg: LayerCfg, Ws: Sequence[dict], k_caches: Sequence[np.ndarray], v_caches: Sequence[np.ndarray],
                block_tables: Sequence[np.ndarray], context_lens: Sequence[int], chunk_lens: Sequence[int],
-               x_bits: np.ndarray, mode: str = "batched", seqs: Optional[Sequence[int]] = None) -> np.ndarray:
+               x_bits: np.ndarray, mode: str = "batched", seqs: Optional[Sequence[int]] = None,
+               kv_scales: Optional[Sequence[Tuple[float, float]]] = None) -> np.ndarray:
     """A model step: the layers one after another over the same batch.
 
     The paper's iteration is a pass of the whole model over the batch
@@ -287,13 +302,14 @@ def stack_step(cfg: LayerCfg, Ws: Sequence[dict], k_caches: Sequence[np.ndarray]
     (the layer interface carries bf16 activations), appends into its own
     cache (k_caches[l], v_caches[l], mutated in place; entries may be the
     same arrays, in which case each layer overwrites the new slots in turn)
-    and the last layer's output is returned in working precision.
+    and the last layer's output is returned in working precision.  With
+    kv_scales[l] the caches of layer l hold 8-bit codes.
     """
     xb = x_bits
     y = None
     for l, W in enumerate(Ws):
         y = layer_step(cfg, W, k_caches[l], v_caches[l], block_tables[l], context_lens, chunk_lens, xb,
-                       mode=mode, seqs=seqs)
+                       mode=mode, seqs=seqs, kv_scales=None if kv_scales is None else kv_scales[l])
         if l + 1 < len(Ws):
             xb = f32_to_bf16_bits(y.astype(np.float32))
     return y

@@ -50,7 +50,12 @@ class LayerWeights(ctypes.Structure):
 
 class KvCache(ctypes.Structure):
     _fields_ = [("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p), ("num_pages", ctypes.c_int32),
-                ("block_tables", ctypes.c_void_p), ("max_pages_per_seq", ctypes.c_int32)]
+                ("block_tables", ctypes.c_void_p), ("max_pages_per_seq", ctypes.c_int32),
+                ("kv_dtype", ctypes.c_int32), ("k_scale", ctypes.c_float), ("v_scale", ctypes.c_float)]
+
+
+KV_BF16, KV_FP8_E4M3 = 0, 1
+_CODE_DTYPES = (torch.uint8,) + ((torch.float8_e4m3fn,) if hasattr(torch, "float8_e4m3fn") else ())
 
 
 class Batch(ctypes.Structure):
@@ -134,11 +139,20 @@ class HostBatch:
         self.c = Batch(len(self.ctx), int(self.chk.sum()), self.ctx.ctypes.data, self.chk.ctypes.data)
 
 
-def kv_struct(k_cache: torch.Tensor, v_cache: torch.Tensor, block_tables: torch.Tensor) -> KvCache:
-    assert k_cache.dtype == torch.bfloat16 and v_cache.dtype == torch.bfloat16
+def kv_struct(k_cache: torch.Tensor, v_cache: torch.Tensor, block_tables: torch.Tensor,
+              kv_scales=None) -> KvCache:
+    """bf16 caches, or 8-bit E4M3 code caches (uint8 / float8_e4m3fn) with
+    kv_scales = (k_scale, v_scale)."""
     assert block_tables.dtype == torch.int32 and block_tables.dim() == 2
+    assert k_cache.dtype == v_cache.dtype
+    if k_cache.dtype in _CODE_DTYPES:
+        if kv_scales is None:
+            raise ValueError("an 8-bit cache needs kv_scales = (k_scale, v_scale)")
+        return KvCache(_ptr(k_cache), _ptr(v_cache), int(k_cache.shape[0]), _ptr(block_tables),
+                       int(block_tables.shape[1]), KV_FP8_E4M3, float(kv_scales[0]), float(kv_scales[1]))
+    assert k_cache.dtype == torch.bfloat16
     return KvCache(_ptr(k_cache), _ptr(v_cache), int(k_cache.shape[0]), _ptr(block_tables),
-                   int(block_tables.shape[1]))
+                   int(block_tables.shape[1]), KV_BF16, 1.0, 1.0)
 
 
 def weights_struct(w: dict) -> LayerWeights:
@@ -178,7 +192,8 @@ def alloc_workspace(nbytes: int, device="cuda") -> torch.Tensor:
 
 
 def _step(name, h: Handle, weights: dict, k_cache, v_cache, block_tables, context_lens, chunk_lens,
-          x: torch.Tensor, y: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, stream=None):
+          x: torch.Tensor, y: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, stream=None,
+          kv_scales=None):
     hb = HostBatch(context_lens, chunk_lens)
     mode = {"eb_layer_step_decode": "decode", "eb_layer_step_prefill": "prefill",
             "eb_layer_step_mixed": "mixed"}[name]
@@ -186,7 +201,7 @@ def _step(name, h: Handle, weights: dict, k_cache, v_cache, block_tables, contex
         y = torch.empty_like(x)
     if ws is None:
         ws = alloc_workspace(lib().eb_workspace_bytes(h.h, ctypes.byref(hb.c), MODES[mode]), x.device)
-    kv = kv_struct(k_cache, v_cache, block_tables)
+    kv = kv_struct(k_cache, v_cache, block_tables, kv_scales)
     w = weights_struct(weights)
     _check(getattr(lib(), name)(h.h, ctypes.byref(w), ctypes.byref(kv), ctypes.byref(hb.c), _ptr(x), _ptr(y),
                                 _ptr(ws), ws.numel(), _stream(stream)))
@@ -194,21 +209,21 @@ def _step(name, h: Handle, weights: dict, k_cache, v_cache, block_tables, contex
 
 
 def eb_layer_step_decode(h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x, y=None, ws=None,
-                         stream=None):
+                         stream=None, kv_scales=None):
     return _step("eb_layer_step_decode", h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x,
-                 y, ws, stream)
+                 y, ws, stream, kv_scales)
 
 
 def eb_layer_step_prefill(h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x, y=None, ws=None,
-                          stream=None):
+                          stream=None, kv_scales=None):
     return _step("eb_layer_step_prefill", h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x,
-                 y, ws, stream)
+                 y, ws, stream, kv_scales)
 
 
 def eb_layer_step_mixed(h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x, y=None, ws=None,
-                        stream=None):
+                        stream=None, kv_scales=None):
     return _step("eb_layer_step_mixed", h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x,
-                 y, ws, stream)
+                 y, ws, stream, kv_scales)
 
 
 def eb_stack_workspace_bytes(h: Handle, context_lens, chunk_lens, mode: str) -> int:
@@ -219,7 +234,8 @@ def eb_stack_workspace_bytes(h: Handle, context_lens, chunk_lens, mode: str) -> 
 def eb_stack_step(h: Handle, mode: str, weights: list, caches: list, context_lens, chunk_lens, x: torch.Tensor,
                   y: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None, stream=None):
     """n = len(weights) layers; caches[l] = (k_cache, v_cache, block_tables)
-    of layer l (entries may repeat the same tensors)."""
+    of layer l, plus (k_scale, v_scale) for an 8-bit cache (entries may
+    repeat the same tensors)."""
     n = len(weights)
     if len(caches) != n:
         raise ValueError("one cache entry per layer")
@@ -277,36 +293,39 @@ def _op_ws(h, hb, mode="mixed", device="cuda"):
 
 
 def eb_op_rope_kv_append(h: Handle, qkv: torch.Tensor, k_cache, v_cache, block_tables, context_lens, chunk_lens,
-                         stream=None):
+                         stream=None, kv_scales=None):
     hb = HostBatch(context_lens, chunk_lens)
     ws = _op_ws(h, hb, device=qkv.device)
-    kv = kv_struct(k_cache, v_cache, block_tables)
+    kv = kv_struct(k_cache, v_cache, block_tables, kv_scales)
     _check(lib().eb_op_rope_kv_append(h.h, _ptr(qkv), ctypes.byref(kv), ctypes.byref(hb.c), _ptr(ws), ws.numel(),
                                       _stream(stream)))
     return qkv
 
 
 def eb_op_attention(h: Handle, qkv: torch.Tensor, k_cache, v_cache, block_tables, context_lens, chunk_lens,
-                    mode: str = "mixed", out: Optional[torch.Tensor] = None, stream=None):
+                    mode: str = "mixed", out: Optional[torch.Tensor] = None, stream=None, kv_scales=None):
     hb = HostBatch(context_lens, chunk_lens)
     s = h.shape
     T = int(hb.chk.sum())
     out = torch.empty(T, s.n_q_heads * s.head_dim, dtype=torch.bfloat16, device=qkv.device) if out is None else out
     ws = _op_ws(h, hb, mode if mode in MODES else "mixed", qkv.device)
-    kv = kv_struct(k_cache, v_cache, block_tables)
+    kv = kv_struct(k_cache, v_cache, block_tables, kv_scales)
     _check(lib().eb_op_attention(h.h, _ptr(qkv), ctypes.byref(kv), ctypes.byref(hb.c), _ptr(out), _ptr(ws),
                                  ws.numel(), MODES[mode], _stream(stream)))
     return out
 
 
-def eb_op_gather_kv(h: Handle, k_cache, v_cache, block_tables, context_lens, chunk_lens, stream=None):
+def eb_op_gather_kv(h: Handle, k_cache, v_cache, block_tables, context_lens, chunk_lens, stream=None,
+                    kv_scales=None):
+    """Dense copies of every cached position (raw elements: bf16, or the
+    8-bit codes of an 8-bit cache)."""
     hb = HostBatch(context_lens, chunk_lens)
     s = h.shape
     total = int((hb.ctx.astype(np.int64) + hb.chk).sum())
-    ok = torch.empty(total, s.n_kv_heads, s.head_dim, dtype=torch.bfloat16, device=k_cache.device)
+    ok = torch.empty(total, s.n_kv_heads, s.head_dim, dtype=k_cache.dtype, device=k_cache.device)
     ov = torch.empty_like(ok)
     ws = _op_ws(h, hb, device=k_cache.device)
-    kv = kv_struct(k_cache, v_cache, block_tables)
+    kv = kv_struct(k_cache, v_cache, block_tables, kv_scales if kv_scales is not None else (1.0, 1.0))
     _check(lib().eb_op_gather_kv(h.h, ctypes.byref(kv), ctypes.byref(hb.c), _ptr(ok), _ptr(ov), _ptr(ws), ws.numel(),
                                  _stream(stream)))
     return ok, ov

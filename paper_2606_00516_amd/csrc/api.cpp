@@ -1,5 +1,6 @@
 // C ABI of libeb.so: handle, workspace carve-up, validation and the launch
 // sequence of one decoder-layer step on the caller's stream.
+#include <cmath>
 #include <hip/hip_runtime.h>
 #include <string.h>
 
@@ -151,6 +152,10 @@ eb_status check_kv(const eb_kv_cache *kv) {
   if (!kv->k_cache || !kv->v_cache || !kv->block_tables) return fail(EB_ERR_NULL, "kv cache or block table is NULL");
   if (kv->num_pages <= 0 || kv->max_pages_per_seq <= 0)
     return fail(EB_ERR_PAGES, "num_pages and max_pages_per_seq must be positive");
+  if (kv->kv_dtype != EB_KV_BF16 && kv->kv_dtype != EB_KV_FP8_E4M3) return fail(EB_ERR_CONFIG, "unknown kv_dtype");
+  if (kv->kv_dtype == EB_KV_FP8_E4M3 &&
+      !(std::isfinite(kv->k_scale) && kv->k_scale > 0.f && std::isfinite(kv->v_scale) && kv->v_scale > 0.f))
+    return fail(EB_ERR_CONFIG, "an 8-bit cache needs finite positive k_scale and v_scale");
   return EB_OK;
 }
 
@@ -175,8 +180,9 @@ eb_status check_ws(void *ws, size_t ws_bytes, size_t need) {
 }
 
 KV kv_of(const eb_kv_cache *kv) {
+  const bool f8 = kv->kv_dtype == EB_KV_FP8_E4M3;
   return KV{static_cast<uint16_t *>(kv->k_cache), static_cast<uint16_t *>(kv->v_cache), kv->block_tables,
-            kv->num_pages, kv->max_pages_per_seq};
+            kv->num_pages, kv->max_pages_per_seq, f8 ? 1 : 0, f8 ? kv->k_scale : 1.f, f8 ? kv->v_scale : 1.f};
 }
 
 eb_status check_weights(const eb_layer_weights *w) {

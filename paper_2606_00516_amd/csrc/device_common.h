@@ -82,7 +82,40 @@ EB_DEV u32x4_t buf_ld_u32x4(buf_rsrc_t r, int off) {
   return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, AUX));
 }
 
+// 8-byte load at byte offset `off` (same conventions).
+template <int AUX = 0>
+EB_DEV u32x2_t buf_ld_u32x2(buf_rsrc_t r, int off) {
+  return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, AUX));
+}
+
 EB_DEV bf16x8_t as_bf16x8(u32x4_t v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+// 8-bit E4M3 cache codes (OCP: bias 7, no infinity, 0x7F / 0xFF NaN,
+// largest finite 448).  Eight codes (element i in byte i of the two words) as
+// eight bf16 values: every code's value is exact in bf16.
+template <bool HI>
+EB_DEV uint32_t e4m3x2_to_bf16x2(uint32_t w) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, HI));
+}
+EB_DEV u32x4_t e4m3x8_to_bf16x8(u32x2_t w) {
+  return u32x4_t{e4m3x2_to_bf16x2<false>(w[0]), e4m3x2_to_bf16x2<true>(w[0]), e4m3x2_to_bf16x2<false>(w[1]),
+                 e4m3x2_to_bf16x2<true>(w[1])};
+}
+// Nearest codes (ties to even) of four fp32 values, byte i for value i,
+// saturated to +-448 (the conversion itself does not saturate); a NaN keeps
+// its sign with the all-ones exponent and mantissa.
+EB_DEV uint32_t e4m3x4_from_f32(float a, float b, float c, float d) {
+  const float x[4] = {a, b, c, d};
+  float y[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) y[i] = __builtin_amdgcn_fmed3f(x[i], -448.0f, 448.0f);
+  uint32_t w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[0], y[1], 0, false);
+  w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(y[2], y[3], (int)w, true);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (x[i] != x[i]) w = (w & ~(0xFFu << (8 * i))) | ((0x7Fu | ((__float_as_uint(x[i]) >> 24) & 0x80u)) << (8 * i));
+  return w;
+}
 
 // D = A B + C on one 16x16x32 bf16 tile.  Operand layout (lane l):
 //   A: row l % 16, k = 8 (l / 16) .. + 7      B: col l % 16, same k

@@ -41,9 +41,13 @@ struct DevMeta {
 };
 
 struct KV {
-  uint16_t *k, *v;
+  uint16_t *k, *v;      // element type per f8: bf16, or 8-bit E4M3 codes (read through k8 / v8)
   const int32_t *bt;
   int32_t num_pages, max_pages;
+  int32_t f8;           // 1: 8-bit codes
+  float ks, vs;         // value of a code = decode(code) * scale (8-bit caches)
+  __host__ __device__ uint8_t *k8() const { return reinterpret_cast<uint8_t *>(k); }
+  __host__ __device__ uint8_t *v8() const { return reinterpret_cast<uint8_t *>(v); }
 };
 
 struct Shape {

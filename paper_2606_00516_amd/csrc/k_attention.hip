@@ -8,12 +8,28 @@
 // heads, so each cached byte is read once per item.
 #include <math.h>
 
+#include <type_traits>
+
 #include "device_common.h"
 #include "eb_internal.h"
 
 namespace eb {
 
 constexpr float kNegInf = -__builtin_inff();
+
+// Cache words a lane holds for 8 consecutive dims of one token: 16 bytes of
+// bf16, or 8 bytes of 8-bit codes (F8), turned into bf16 words when used
+// (the codes' values are exact in bf16; the scales enter the score scale and
+// the output normalisation).
+template <bool F8>
+using RawT = typename std::conditional<F8, u32x2_t, u32x4_t>::type;
+template <bool F8>
+EB_DEV u32x4_t raw_bf16(const RawT<F8> &w) {
+  if constexpr (F8)
+    return e4m3x8_to_bf16x8(w);
+  else
+    return w;
+}
 
 // ===========================================================================
 // Decode: one work unit = (decode request, split of 32 pages, kv head) with
@@ -48,31 +64,50 @@ __device__ __forceinline__ void lse_merge(float &m, float &l, float *o, float m2
 
 // Page buffers a wavefront keeps in flight while it works on another page
 // (three named register sets, rotated by hand so they stay in registers).
-template <int HD, int NLD>
-__device__ __forceinline__ void decode_load_page(u32x4_t (&k)[NLD], u32x4_t (&v)[NLD], const KV kv,
+template <int HD, int NLD, bool F8>
+__device__ __forceinline__ void decode_load_page(RawT<F8> (&k)[NLD], RawT<F8> (&v)[NLD], const KV kv,
                                                  const int32_t *bt, int p, int pg1, int nkv, int kh, int lane) {
   // page p of the split is wave-uniform; past the end (or a bad table
   // entry) the descriptors cover zero bytes and the loads return zero
   const int phys = p < pg1 ? bt[p] : -1;
   const bool ok = phys >= 0 && phys < kv.num_pages;
   const size_t off = ok ? ((size_t)phys * nkv + kh) * kPageSize * HD : 0;
-  const int bytes = ok ? kPageSize * HD * 2 : 0;
-  const buf_rsrc_t rk = make_rsrc(kv.k + off, bytes);
-  const buf_rsrc_t rv = make_rsrc(kv.v + off, bytes);
+  if constexpr (F8) {
+    // a lane's 8 codes sit at byte 8 lane + 512 j of the block (same tokens
+    // and dims as the 16 bf16 bytes below)
+    const int bytes8 = __builtin_amdgcn_readfirstlane(ok ? kPageSize * HD : 0);
+    const buf_rsrc_t rk = make_rsrc(kv.k8() + off, bytes8);
+    const buf_rsrc_t rv = make_rsrc(kv.v8() + off, bytes8);
 #pragma unroll
-  for (int j = 0; j < NLD; ++j) {
-    k[j] = buf_ld_u32x4<kAuxNT>(rk, lane * 16 + j * 1024);
-    v[j] = buf_ld_u32x4<kAuxNT>(rv, lane * 16 + j * 1024);
+    for (int j = 0; j < NLD; ++j) {
+      k[j] = buf_ld_u32x2<kAuxNT>(rk, lane * 8 + j * 512);
+      v[j] = buf_ld_u32x2<kAuxNT>(rv, lane * 8 + j * 512);
+    }
+  } else {
+    const int bytes = ok ? kPageSize * HD * 2 : 0;
+    const buf_rsrc_t rk = make_rsrc(kv.k + off, bytes);
+    const buf_rsrc_t rv = make_rsrc(kv.v + off, bytes);
+#pragma unroll
+    for (int j = 0; j < NLD; ++j) {
+      k[j] = buf_ld_u32x4<kAuxNT>(rk, lane * 16 + j * 1024);
+      v[j] = buf_ld_u32x4<kAuxNT>(rv, lane * 16 + j * 1024);
+    }
   }
 }
 
 // Online-softmax update of one lane's (max, sum, output) state with the
 // tokens of one page it holds.
-template <int HD, int G>
-__device__ __forceinline__ void decode_page_update(const u32x4_t (&k)[HD / 32], const u32x4_t (&v)[HD / 32],
+template <int HD, int G, bool F8>
+__device__ __forceinline__ void decode_page_update(const RawT<F8> (&kr)[HD / 32], const RawT<F8> (&vr)[HD / 32],
                                                    const u32x4_t (&qw)[G], float (&mrun)[G], float (&lrun)[G],
                                                    float (&o)[G][8], int p, int k1, int lane, float qscale) {
   constexpr int LPT = HD / 8, TG = 64 / LPT, NLD = HD / 32;
+  u32x4_t k[NLD], v[NLD];
+#pragma unroll
+  for (int j = 0; j < NLD; ++j) {
+    k[j] = raw_bf16<F8>(kr[j]);
+    v[j] = raw_bf16<F8>(vr[j]);
+  }
   bool valid[NLD];
 #pragma unroll
   for (int j = 0; j < NLD; ++j) valid[j] = p * kPageSize + j * TG + lane / LPT < k1;
@@ -117,17 +152,17 @@ __device__ __forceinline__ void decode_page_update(const u32x4_t (&k)[HD / 32], 
 // code; pages past the end load as zeros without memory traffic and are
 // masked out.  Scheduling barriers keep page loads and page updates in
 // program order, so the wait before an update covers only that page.
-template <int HD, int G>
+template <int HD, int G, bool F8>
 __device__ __forceinline__ void decode_stream(const KV kv, const int32_t *bt, int p_first, int stride, int pg1, int k1,
                                               int nkv, int kh, int lane, float qscale, const u32x4_t (&qw)[G],
                                               float (&mrun)[G], float (&lrun)[G], float (&o)[G][8]) {
   constexpr int NLD = HD / 32;
-  u32x4_t ka[NLD], va[NLD], kb[NLD], vb[NLD], kc[NLD], vc[NLD];
+  RawT<F8> ka[NLD], va[NLD], kb[NLD], vb[NLD], kc[NLD], vc[NLD];
 #define EB_LOAD(K_, V_, P_)                                                  \
-  decode_load_page<HD, NLD>(K_, V_, kv, bt, P_, pg1, nkv, kh, lane);         \
+  decode_load_page<HD, NLD, F8>(K_, V_, kv, bt, P_, pg1, nkv, kh, lane);     \
   __builtin_amdgcn_sched_barrier(0);
-#define EB_UPDATE(K_, V_, P_)                                                \
-  decode_page_update<HD, G>(K_, V_, qw, mrun, lrun, o, P_, k1, lane, qscale); \
+#define EB_UPDATE(K_, V_, P_)                                                    \
+  decode_page_update<HD, G, F8>(K_, V_, qw, mrun, lrun, o, P_, k1, lane, qscale); \
   __builtin_amdgcn_sched_barrier(0);
   EB_LOAD(ka, va, p_first)
   EB_LOAD(kb, vb, p_first + stride)
@@ -177,10 +212,11 @@ __device__ __forceinline__ void decode_merge_lanes(float (&mrun)[G], float (&lru
 // Merge the per-wave softmax states a work unit left in LDS ([wave][h][HD]
 // outputs, then [wave][h][2] max and sum) and write the unit's result: the
 // final row (one split) or a partial for the combine.
+// vscale: the value scale of an 8-bit cache (1 for bf16: exact).
 template <int HD, int G, int NW>
 __device__ __forceinline__ void decode_merge_waves(const float *lds, int row, int kh, int nq, int nkv, int item,
                                                    int nsplit, uint16_t *__restrict__ out, float *__restrict__ part_o,
-                                                   float *__restrict__ part_ml) {
+                                                   float *__restrict__ part_ml, float vscale) {
   const float *lo_ = lds;
   const float *lml = lds + NW * G * HD;
   __syncthreads();
@@ -197,6 +233,7 @@ __device__ __forceinline__ void decode_merge_waves(const float *lds, int row, in
       L += a * lml[(w * G + h) * 2 + 1];
       O += a * lo_[(w * G + h) * HD + dim];
     }
+    O *= vscale;
     const int qh = kh * G + h;
     if (nsplit == 1) {
       out[(size_t)row * nq * HD + qh * HD + dim] = (uint16_t)f32_to_bf16_bits(O / L);
@@ -255,17 +292,22 @@ constexpr bool kDecodeMfma = G >= 4;
 // operand reads (16 tokens x one chunk per quarter-wave) hit 16 different
 // bank groups.  A wavefront owns four page slots (K block then V block)
 // and keeps three pages in flight while it works on the fourth.
-template <int HD>
+template <int HD, bool F8 = false>
 struct MdecTraits {
-  static constexpr int BLK = kPageSize * HD * 2;  // bytes of one (page, kv head) block
-  static constexpr int SLOT = 2 * BLK;            // K block, then V block
-  static constexpr int NDMA = BLK / 1024;         // 1 KiB load instructions per block
-  static constexpr int ROW = HD * 2;              // bytes per token row
+  static constexpr int ES = F8 ? 1 : 2;            // bytes per cached element
+  static constexpr int BLK = kPageSize * HD * ES;  // bytes of one (page, kv head) block
+  static constexpr int SLOT = 2 * BLK;             // K block, then V block
+  static constexpr int NDMA = BLK / 1024;          // 1 KiB load instructions per block
+  static constexpr int ROW = HD * ES;              // bytes per token row
+  static_assert(NDMA >= 1, "block of at least 1 KiB");
 };
 
-template <int HD>
+// 16-byte chunk position exchange of token row t: rows of 256 bytes (bf16,
+// HD 128) take t & 15, 128-byte rows t & 7, 64-byte rows (t >> 1) & 3 ...
+template <int HD, bool F8 = false>
 EB_DEV int mdec_swz(int t) {
-  return HD == 128 ? (t & 15) : ((t >> 1) & 7);
+  constexpr int ROW = MdecTraits<HD, F8>::ROW;
+  return ROW == 256 ? (t & 15) : ROW == 128 ? ((F8 ? t : (t >> 1)) & 7) : ((t >> 1) & 3);
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -273,18 +315,18 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // Start the loads of page p's K and V blocks into a slot; slots at or past
 // k1 (and pages past the end or with a bad table entry) land as zeros
 // without memory traffic, so cache poison never reaches the products.
-template <int HD>
+template <int HD, bool F8>
 __device__ __forceinline__ void mdec_dma_page(uint8_t *slot, const uint32_t *goff, const KV kv,
                                               const int32_t *bt, int p, int pg1, int k1, int nkv, int kh) {
-  using Tr = MdecTraits<HD>;
+  using Tr = MdecTraits<HD, F8>;
   const int phys = p < pg1 ? bt[p] : -1;
   const int nvalid = min(max(k1 - p * kPageSize, 0), kPageSize);
   const bool ok = phys >= 0 && phys < kv.num_pages;
   const size_t off = ok ? ((size_t)phys * nkv + kh) * kPageSize * HD : 0;
   // wave-uniform by construction; said so, so the descriptor stays scalar
   const int bytes = __builtin_amdgcn_readfirstlane(ok ? nvalid * Tr::ROW : 0);
-  const buf_rsrc_t rk = make_rsrc(kv.k + off, bytes);
-  const buf_rsrc_t rv = make_rsrc(kv.v + off, bytes);
+  const buf_rsrc_t rk = F8 ? make_rsrc(kv.k8() + off, bytes) : make_rsrc(kv.k + off, bytes);
+  const buf_rsrc_t rv = F8 ? make_rsrc(kv.v8() + off, bytes) : make_rsrc(kv.v + off, bytes);
 #pragma unroll
   for (int i = 0; i < Tr::NDMA; ++i) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void_t *)(slot + i * 1024), 16, goff[i], 0, 0, kAuxNT);
@@ -307,22 +349,28 @@ EB_DEV uint32_t bf16_pair_rne(float lo, float hi) {
 
 // Online-softmax update with the page in a slot; the page holds at least one
 // key below k1, so the new running max is finite.
-template <int HD>
+template <int HD, bool F8>
 __device__ __forceinline__ void mdec_page_update(const uint8_t *slot, const u32x4_t (&qb)[HD / 32],
                                                  const u32x4_t (&sel)[2], float &mrun, float &lsum,
                                                  f32x4_t (&oacc)[HD / 16], int p, int k1, int lane, float qscale) {
-  using Tr = MdecTraits<HD>;
+  using Tr = MdecTraits<HD, F8>;
   constexpr int NKS = HD / 32;
   const int r = lane & 15, g = lane >> 4;
   const f32x4_t zero = {0.f, 0.f, 0.f, 0.f};
   const uint8_t *rowp = slot + r * Tr::ROW;
-  const int sw = mdec_swz<HD>(r);
+  const int sw = mdec_swz<HD, F8>(r);
+  // dims 8 g + 32 ks .. + 7 of token r: a 16-byte chunk of bf16, or half of
+  // one of 8-bit codes
+  auto dims8 = [&](const uint8_t *base, int ks) -> u32x4_t {
+    if constexpr (F8)
+      return e4m3x8_to_bf16x8(
+          *reinterpret_cast<const u32x2_t *>(base + ((((g >> 1) + 2 * ks) ^ sw) << 4) + ((g & 1) << 3)));
+    else
+      return *reinterpret_cast<const u32x4_t *>(base + (((g + 4 * ks) ^ sw) << 4));
+  };
   f32x4_t sa = zero;
 #pragma unroll
-  for (int ks = 0; ks < NKS; ++ks) {
-    const u32x4_t a = *reinterpret_cast<const u32x4_t *>(rowp + (((g + 4 * ks) ^ sw) << 4));
-    sa = mfma16x16x32(a, qb[ks], sa);
-  }
+  for (int ks = 0; ks < NKS; ++ks) sa = mfma16x16x32(dims8(rowp, ks), qb[ks], sa);
   float s[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) s[j] = sa[j] * qscale;
@@ -346,7 +394,7 @@ __device__ __forceinline__ void mdec_page_update(const uint8_t *slot, const u32x
   const u32x2_t pt = {bf16_pair_rne(pr[0], pr[1]), bf16_pair_rne(pr[2], pr[3])};
 #pragma unroll
   for (int ks = 0; ks < NKS; ++ks) {
-    const u32x4_t vv = *reinterpret_cast<const u32x4_t *>(rowp + Tr::BLK + (((g + 4 * ks) ^ sw) << 4));
+    const u32x4_t vv = dims8(rowp + Tr::BLK, ks);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const f32x4_t t = mfma16x16x32(vv, sel[h], zero);  // V[4 g + j][32 ks + 16 h + r]
@@ -360,26 +408,26 @@ __device__ __forceinline__ void mdec_page_update(const uint8_t *slot, const u32x
 // NSLOT slots (NSLOT - 1 pages in flight while one is consumed).  Loads of
 // pages past the end cost no memory traffic; every load has landed when
 // this returns.
-template <int HD, int NSLOT>
+template <int HD, int NSLOT, bool F8>
 __device__ __forceinline__ void mdec_stream(uint8_t *s0, uint8_t *s1, uint8_t *s2, uint8_t *s3, const KV kv,
                                             const int32_t *bt, int p_first, int stride, int pg1, int k1, int nkv,
                                             int kh, int lane, float qscale, const u32x4_t (&qb)[HD / 32],
                                             const u32x4_t (&sel)[2], float &mrun, float &lsum,
                                             f32x4_t (&oacc)[HD / 16]) {
-  using Tr = MdecTraits<HD>;
+  using Tr = MdecTraits<HD, F8>;
   static_assert(NSLOT >= 2 && NSLOT <= 4, "ring depth");
   uint32_t goff[Tr::NDMA];
 #pragma unroll
   for (int i = 0; i < Tr::NDMA; ++i) {
     const int e = i * 1024 + lane * 16;  // byte of the slot block this lane fills
     const int t = e / Tr::ROW, u = (e % Tr::ROW) >> 4;
-    goff[i] = (uint32_t)(t * Tr::ROW + ((u ^ mdec_swz<HD>(t)) << 4));
+    goff[i] = (uint32_t)(t * Tr::ROW + ((u ^ mdec_swz<HD, F8>(t)) << 4));
   }
 #define EB_DMA(S_, P_)                                                  \
-  mdec_dma_page<HD>(S_, goff, kv, bt, P_, pg1, k1, nkv, kh);            \
+  mdec_dma_page<HD, F8>(S_, goff, kv, bt, P_, pg1, k1, nkv, kh);        \
   __builtin_amdgcn_sched_barrier(0);
 #define EB_UPD(S_, P_)                                                                  \
-  if ((P_) < pg1) mdec_page_update<HD>(S_, qb, sel, mrun, lsum, oacc, P_, k1, lane, qscale); \
+  if ((P_) < pg1) mdec_page_update<HD, F8>(S_, qb, sel, mrun, lsum, oacc, P_, k1, lane, qscale); \
   __builtin_amdgcn_sched_barrier(0);
   if constexpr (NSLOT == 2) {
     (void)s2;
@@ -460,19 +508,20 @@ struct MdecBlock {
   static constexpr int SLOT_ARRAY = NW * MdecTraits<HD>::SLOT;  // bytes per slot array
 };
 
-template <int HD, int G, int NW, int NSLOT>
+template <int HD, int G, int NW, int NSLOT, bool F8>
 __device__ __forceinline__ void decode_item_mfma(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
                                                  const DevMeta md, int unit, uint16_t *__restrict__ out,
                                                  float *__restrict__ part_o, float *__restrict__ part_ml, uint8_t *l0,
                                                  uint8_t *l1, uint8_t *l2, uint8_t *l3) {
-  constexpr int SLOT = MdecTraits<HD>::SLOT;
+  constexpr int SLOT = MdecTraits<HD>::SLOT;  // the bf16 slot size (an 8-bit page uses its first half)
   constexpr int SPLIT = kDecodePagesPerSplit * kPageSize;
   constexpr int NOB = HD / 16;
   static_assert(DecodeTraits<HD, G, NW>::LDS_BYTES <= MdecBlock<HD, NW, NSLOT>::SLOT_ARRAY, "merge area");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int cols = (nq + 2 * nkv) * HD;
-  const float qscale = kLog2e / sqrtf((float)HD);
+  const float qscale = F8 ? kLog2e / sqrtf((float)HD) * kv.ks : kLog2e / sqrtf((float)HD);
+  const float vscale = F8 ? kv.vs : 1.f;
   const int c = lane & 15, g = lane >> 4;
   uint8_t *w0 = l0 + wave * SLOT, *w1 = l1 + wave * SLOT, *w2 = l2 + wave * SLOT, *w3 = l3 + wave * SLOT;
 
@@ -497,12 +546,12 @@ __device__ __forceinline__ void decode_item_mfma(const uint16_t *__restrict__ qk
       const int kh = local * kShortDecodeHeads + hw;
       if (kh >= nkv) break;
       mdec_init<HD, G>(qkv, cols, row, kh, lane, qb, sel, mrun, lsum, oacc);
-      mdec_stream<HD, NSLOT>(w0, w1, w2, w3, kv, bt, 0, 1, (nkeys + kPageSize - 1) / kPageSize, nkeys, nkv, kh, lane,
-                             qscale, qb, sel, mrun, lsum, oacc);
+      mdec_stream<HD, NSLOT, F8>(w0, w1, w2, w3, kv, bt, 0, 1, (nkeys + kPageSize - 1) / kPageSize, nkeys, nkv, kh,
+                                 lane, qscale, qb, sel, mrun, lsum, oacc);
       lsum += shfl_xor_f32(lsum, 16);
       lsum += shfl_xor_f32(lsum, 32);
       if (c < G) {
-        const float inv = 1.0f / lsum;
+        const float inv = F8 ? vscale / lsum : 1.0f / lsum;
         uint16_t *dst = out + (size_t)row * nq * HD + (kh * G + c) * HD + g * 4;
 #pragma unroll
         for (int ob = 0; ob < NOB; ++ob) {
@@ -522,8 +571,8 @@ __device__ __forceinline__ void decode_item_mfma(const uint16_t *__restrict__ qk
   const int k1 = min(nkeys, k0 + SPLIT);
   const int pg0 = k0 / kPageSize, pg1 = (k1 + kPageSize - 1) / kPageSize;
   mdec_init<HD, G>(qkv, cols, row, kh, lane, qb, sel, mrun, lsum, oacc);
-  mdec_stream<HD, NSLOT>(w0, w1, w2, w3, kv, bt, pg0 + wave, NW, pg1, k1, nkv, kh, lane, qscale, qb, sel, mrun, lsum,
-                         oacc);
+  mdec_stream<HD, NSLOT, F8>(w0, w1, w2, w3, kv, bt, pg0 + wave, NW, pg1, k1, nkv, kh, lane, qscale, qb, sel, mrun,
+                             lsum, oacc);
   lsum += shfl_xor_f32(lsum, 16);
   lsum += shfl_xor_f32(lsum, 32);
   // across the NW waves through LDS (reusing l0 once every wave is done with
@@ -542,7 +591,7 @@ __device__ __forceinline__ void decode_item_mfma(const uint16_t *__restrict__ qk
       ml[1] = lsum;
     }
   }
-  decode_merge_waves<HD, G, NW>(merge, row, kh, nq, nkv, item, nsplit, out, part_o, part_ml);
+  decode_merge_waves<HD, G, NW>(merge, row, kh, nq, nkv, item, nsplit, out, part_o, part_ml, vscale);
 }
 
 // One decode work unit.  Unit u of decode request d (binary search over the
@@ -553,7 +602,7 @@ __device__ __forceinline__ void decode_item_mfma(const uint16_t *__restrict__ qk
 // and merging through LDS, with the result written directly (one split) or
 // as a partial for the combine.  Which kind a request gets depends only on
 // its own length.
-template <int HD, int G, int NW>
+template <int HD, int G, int NW, bool F8>
 __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
                                             const DevMeta md, int unit, uint16_t *__restrict__ out,
                                             float *__restrict__ part_o, float *__restrict__ part_ml, float *lds) {
@@ -564,7 +613,8 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
   // wave index made visibly uniform, so page addressing stays scalar
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int cols = (nq + 2 * nkv) * HD;
-  const float qscale = kLog2e / sqrtf((float)HD);
+  const float qscale = F8 ? kLog2e / sqrtf((float)HD) * kv.ks : kLog2e / sqrtf((float)HD);
+  const float vscale = F8 ? kv.vs : 1.f;
 
   int lo = 0, hi = md.n_dec - 1;
   while (lo < hi) {
@@ -585,13 +635,13 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
     const int kh = local * kShortDecodeHeads + wave;
     if (wave >= kShortDecodeHeads || kh >= nkv) return;
     decode_load_q<HD, G>(qkv, cols, row, kh, lane, qw, mrun, lrun, o);
-    decode_stream<HD, G>(kv, bt, 0, 1, (nkeys + kPageSize - 1) / kPageSize, nkeys, nkv, kh, lane, qscale, qw, mrun,
-                         lrun, o);
+    decode_stream<HD, G, F8>(kv, bt, 0, 1, (nkeys + kPageSize - 1) / kPageSize, nkeys, nkv, kh, lane, qscale, qw,
+                             mrun, lrun, o);
     decode_merge_lanes<HD, G>(mrun, lrun, o);
     if (lane < LPT) {
 #pragma unroll
       for (int h = 0; h < G; ++h) {
-        const float inv = 1.0f / lrun[h];
+        const float inv = F8 ? vscale / lrun[h] : 1.0f / lrun[h];
         const u32x4_t w = {pack_bf16x2(o[h][0] * inv, o[h][1] * inv), pack_bf16x2(o[h][2] * inv, o[h][3] * inv),
                            pack_bf16x2(o[h][4] * inv, o[h][5] * inv), pack_bf16x2(o[h][6] * inv, o[h][7] * inv)};
         st_u32x4(out + (size_t)row * nq * HD + (kh * G + h) * HD + dq, w);
@@ -607,7 +657,7 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
   const int k1 = min(nkeys, k0 + SPLIT);
   const int pg0 = k0 / kPageSize, pg1 = (k1 + kPageSize - 1) / kPageSize;
   decode_load_q<HD, G>(qkv, cols, row, kh, lane, qw, mrun, lrun, o);
-  decode_stream<HD, G>(kv, bt, pg0 + wave, NW, pg1, k1, nkv, kh, lane, qscale, qw, mrun, lrun, o);
+  decode_stream<HD, G, F8>(kv, bt, pg0 + wave, NW, pg1, k1, nkv, kh, lane, qscale, qw, mrun, lrun, o);
   decode_merge_lanes<HD, G>(mrun, lrun, o);
 
   // across the NW waves through LDS: [wave][h][HD] outputs, then [wave][h][2]
@@ -624,7 +674,7 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
       }
     }
   }
-  decode_merge_waves<HD, G, NW>(lds, row, kh, nq, nkv, item, nsplit, out, part_o, part_ml);
+  decode_merge_waves<HD, G, NW>(lds, row, kh, nq, nkv, item, nsplit, out, part_o, part_ml, vscale);
 }
 
 // Combine the splits of one decode request for one query head:
@@ -712,7 +762,7 @@ struct PrefillTraits {
   static_assert(RB >= 1 && RB * NW * 16 == G * BQ, "row blocks");
 };
 
-template <int HD, int G, int NW, int BQ_>
+template <int HD, int G, int NW, int BQ_, bool F8>
 __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
                                              const DevMeta md, int tile, int kh, uint16_t *__restrict__ out,
                                              uint16_t *Ks, uint16_t *Vt) {
@@ -737,7 +787,7 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
   const int klen = c + n;                   // keys that exist
   const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
   const int npages = (klen + kPageSize - 1) / kPageSize;
-  const float qscale = kLog2e / sqrtf((float)HD);
+  const float qscale = F8 ? kLog2e / sqrtf((float)HD) * kv.ks : kLog2e / sqrtf((float)HD);
   const int lq = lane & 15;   // query column of this lane inside a 16-row block
   const int lg = lane >> 4;   // lane group 0..3
 
@@ -788,18 +838,27 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
       if (p0 + j < npages) r[j] = btc[p0 + j];
     return r;
   };
-  u32x4_t kreg[KPT], vreg[VPT][2];
+  RawT<F8> kreg[KPT], vreg[VPT][2];
   uint32_t present = 0;  // bit i: K load i, bit KPT + 2 i + e: V load (i, e)
   // The lanes of one load instruction cover 64 / (HD / 8) consecutive keys
   // of K (or twice that of V), all in one page: the page, its validity and
   // its base address are wave-uniform (scalar registers); a lane adds only
   // its row and chunk.  An absent page reads page block 0 and is zeroed.
   static_assert(HD == 64 || HD == 128, "keys of one load within one page");
-  auto page_base = [&](const uint16_t *arr, const i32x4_t &btv, int j, bool &ok) -> const uint16_t * {
+  typedef typename std::conditional<F8, const uint8_t, const uint16_t>::type elem_t;
+  auto page_base = [&](elem_t *arr, const i32x4_t &btv, int j, bool &ok) -> elem_t * {
     const int phys = j == 0 ? btv[0] : j == 1 ? btv[1] : j == 2 ? btv[2] : btv[3];
     ok = phys >= 0 && phys < kv.num_pages;
     return arr + (ok ? ((size_t)phys * nkv + kh) * (kPageSize * HD) : 0);
   };
+  // 8 dims of one token: 16 bytes of bf16 or 8 bytes of codes
+  auto ld8 = [&](elem_t *p) -> RawT<F8> {
+    if constexpr (F8)
+      return *reinterpret_cast<const u32x2_t *>(p);
+    else
+      return ld_u32x4(p);
+  };
+  elem_t *const kbase = reinterpret_cast<elem_t *>(kv.k), *const vbase = reinterpret_cast<elem_t *>(kv.v);
   // the data of absent keys is zeroed when staged (zeroing right after the
   // load would wait for it)
   auto fetch = [&](int t, const i32x4_t &btv) {
@@ -811,8 +870,8 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
       const int key = u / (HD / 8), dc = u % (HD / 8);
       const int j = __builtin_amdgcn_readfirstlane(key / kPageSize);
       bool pok;
-      const uint16_t *pb = page_base(kv.k, btv, j, pok);
-      kreg[i] = ld_u32x4(pb + (key % kPageSize) * HD + dc * 8);
+      elem_t *pb = page_base(kbase, btv, j, pok);
+      kreg[i] = ld8(pb + (key % kPageSize) * HD + dc * 8);
       present |= (u < KCH && pok && k0 + key < klen ? 1u : 0u) << i;
     }
 #pragma unroll
@@ -821,11 +880,11 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
       const int kpair = u / (HD / 8), dc = u % (HD / 8);
       const int j = __builtin_amdgcn_readfirstlane((2 * kpair) / kPageSize);
       bool pok;
-      const uint16_t *pb = page_base(kv.v, btv, j, pok);
+      elem_t *pb = page_base(vbase, btv, j, pok);
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         const int key = 2 * kpair + e;
-        vreg[i][e] = ld_u32x4(pb + (key % kPageSize) * HD + dc * 8);
+        vreg[i][e] = ld8(pb + (key % kPageSize) * HD + dc * 8);
         present |= (u < VCH && pok && k0 + key < klen ? 1u : 0u) << (KPT + 2 * i + e);
       }
     }
@@ -836,7 +895,7 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
       const int u = tid + i * NT;
       if (u < KCH)
         st_u32x4(Ks + (u / (HD / 8)) * KSS + (u % (HD / 8)) * 8,
-                 (present >> i) & 1u ? kreg[i] : u32x4_t{0, 0, 0, 0});
+                 (present >> i) & 1u ? raw_bf16<F8>(kreg[i]) : u32x4_t{0, 0, 0, 0});
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
@@ -846,9 +905,10 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
         // rows dc * 8 .. + 7 share one group exchange (see vt_col)
         const int col = vt_col(dc * 8, 2 * kpair);
         const bool p0 = (present >> (KPT + 2 * i)) & 1u, p1 = (present >> (KPT + 2 * i + 1)) & 1u;
+        const u32x4_t v0 = raw_bf16<F8>(vreg[i][0]), v1 = raw_bf16<F8>(vreg[i][1]);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const uint32_t a0 = p0 ? vreg[i][0][j] : 0u, a1 = p1 ? vreg[i][1][j] : 0u;
+          const uint32_t a0 = p0 ? v0[j] : 0u, a1 = p1 ? v1[j] : 0u;
           *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j) * VTS + col) = (a0 & 0xFFFFu) | (a1 << 16);
           *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j + 1) * VTS + col) = (a0 >> 16) | (a1 & 0xFFFF0000u);
         }
@@ -962,7 +1022,7 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
     l += shfl_xor_f32(l, 32);
     if (qok[i]) {
       const int h = (wave + NW * i) % G;
-      const float inv = 1.0f / l;
+      const float inv = F8 ? kv.vs / l : 1.0f / l;
       uint16_t *dst = out + (size_t)(row0 + qrel[i]) * nq * HD + (kh * G + h) * HD + lg * 4;
 #pragma unroll
       for (int ob = 0; ob < NOB; ++ob) {
@@ -977,11 +1037,11 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
 // ---------------------------------------------------------------------------
 // kernels
 // ---------------------------------------------------------------------------
-template <int HD, int G>
+template <int HD, int G, bool F8>
 __global__ __launch_bounds__(256, 2) void k_decode(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
                                                    uint16_t *out, float *part_o, float *part_ml) {
   __shared__ float lds[DecodeTraits<HD, G, 4>::LDS_BYTES / 4];
-  decode_item<HD, G, 4>(qkv, nq, nkv, kv, md, blockIdx.x, out, part_o, part_ml, lds);
+  decode_item<HD, G, 4, F8>(qkv, nq, nkv, kv, md, blockIdx.x, out, part_o, part_ml, lds);
 }
 
 // The matrix-core decode keeps its page slots in separate LDS arrays, so the
@@ -994,13 +1054,13 @@ constexpr int kDecWaves = 4, kDecSlots = 2;
   __shared__ __attribute__((aligned(16))) uint8_t l2[NSLOT_ > 2 ? MdecBlock<HD_, NW_, NSLOT_>::SLOT_ARRAY : 16]; \
   __shared__ __attribute__((aligned(16))) uint8_t l3[NSLOT_ > 3 ? MdecBlock<HD_, NW_, NSLOT_>::SLOT_ARRAY : 16];
 
-template <int HD, int G>
+template <int HD, int G, bool F8>
 __global__ __launch_bounds__(64 * kDecWaves) void k_decode_mfma(const uint16_t *qkv, int nq, int nkv, KV kv,
                                                                 DevMeta md, uint16_t *out, float *part_o,
                                                                 float *part_ml) {
   EB_MDEC_LDS(HD, kDecWaves, kDecSlots)
-  decode_item_mfma<HD, G, kDecWaves, kDecSlots>(qkv, nq, nkv, kv, md, blockIdx.x, out, part_o, part_ml, l0, l1, l2,
-                                                l3);
+  decode_item_mfma<HD, G, kDecWaves, kDecSlots, F8>(qkv, nq, nkv, kv, md, blockIdx.x, out, part_o, part_ml, l0, l1,
+                                                    l2, l3);
 }
 
 // Prefill-only launch: 8 wavefronts per 128-row item, one 16-row block per
@@ -1009,20 +1069,20 @@ __global__ __launch_bounds__(64 * kDecWaves) void k_decode_mfma(const uint16_t *
 // bandwidth, bounds the tile loop.)
 constexpr int kPrefillWaves = 8;
 
-template <int HD, int G>
+template <int HD, int G, bool F8>
 __global__ __launch_bounds__(64 * kPrefillWaves) void k_prefill(const uint16_t *qkv, int nq, int nkv, KV kv,
                                                                    DevMeta md, uint16_t *out) {
   constexpr int BQ = prefill_item_positions<G, false>();
   using Tr = PrefillTraits<HD, G, kPrefillWaves, BQ>;
   __shared__ __attribute__((aligned(16))) uint16_t lds[Tr::LDS_BYTES / 2];
-  prefill_item<HD, G, kPrefillWaves, BQ>(qkv, nq, nkv, kv, md, blockIdx.x / nkv, blockIdx.x % nkv, out, lds,
-                                         lds + Tr::KS_BYTES / 2);
+  prefill_item<HD, G, kPrefillWaves, BQ, F8>(qkv, nq, nkv, kv, md, blockIdx.x / nkv, blockIdx.x % nkv, out, lds,
+                                             lds + Tr::KS_BYTES / 2);
 }
 
 // One grid for a mixed step: items [0, n_tiles) are prefill tiles (longest
 // first), the rest decode splits; every block (4 wavefronts) branches
 // uniformly on its kind.  Decode items run exactly the decode-only code.
-template <int HD, int G>
+template <int HD, int G, bool F8>
 __global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
                                                float *part_o, float *part_ml) {
   constexpr int BQ = prefill_item_positions<G, true>();
@@ -1031,15 +1091,15 @@ __global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int 
   __shared__ __attribute__((aligned(16))) uint16_t lds[(PB > DB ? PB : DB) / 2];
   const int b = blockIdx.x;
   if (b < md.n_tiles * nkv)
-    prefill_item<HD, G, 4, BQ>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, lds, lds + Tr::KS_BYTES / 2);
+    prefill_item<HD, G, 4, BQ, F8>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, lds, lds + Tr::KS_BYTES / 2);
   else
-    decode_item<HD, G, 4>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml,
-                          reinterpret_cast<float *>(lds));
+    decode_item<HD, G, 4, F8>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml,
+                              reinterpret_cast<float *>(lds));
 }
 
 // The same with matrix-core decode items; prefill tiles borrow two of the
 // page-slot arrays.
-template <int HD, int G>
+template <int HD, int G, bool F8>
 __global__ __launch_bounds__(256) void k_mixed_mfma(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
                                                     uint16_t *out, float *part_o, float *part_ml) {
   constexpr int BQ = prefill_item_positions<G, true>();
@@ -1050,15 +1110,15 @@ __global__ __launch_bounds__(256) void k_mixed_mfma(const uint16_t *qkv, int nq,
   EB_MDEC_LDS(HD, 4, MS)
   const int b = blockIdx.x;
   if (b < md.n_tiles * nkv)
-    prefill_item<HD, G, 4, BQ>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, reinterpret_cast<uint16_t *>(l0),
-                           reinterpret_cast<uint16_t *>(l1));
+    prefill_item<HD, G, 4, BQ, F8>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, reinterpret_cast<uint16_t *>(l0),
+                                   reinterpret_cast<uint16_t *>(l1));
   else
-    decode_item_mfma<HD, G, 4, MS>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml, l0, l1, l2,
-                                   l3);
+    decode_item_mfma<HD, G, 4, MS, F8>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml, l0, l1, l2,
+                                       l3);
 }
 #undef EB_MDEC_LDS
 
-template <int HD, int G>
+template <int HD, int G, bool F8>
 static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const KV &kv, const DevMeta &m,
                                      uint16_t *out, float *part_o, float *part_ml, int kind, int parts,
                                      hipStream_t st) {
@@ -1068,21 +1128,21 @@ static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const 
     // combine only
   } else if (kind == 2 && has_dec && has_pf) {
     if constexpr (kDecodeMfma<G>)
-      hipLaunchKernelGGL((k_mixed_mfma<HD, G>), dim3(m.n_tiles * nkv + m.total_units), dim3(256), 0, st, qkv, nq,
+      hipLaunchKernelGGL((k_mixed_mfma<HD, G, F8>), dim3(m.n_tiles * nkv + m.total_units), dim3(256), 0, st, qkv, nq,
                          nkv, kv, m, out, part_o, part_ml);
     else
-      hipLaunchKernelGGL((k_mixed<HD, G>), dim3(m.n_tiles * nkv + m.total_units), dim3(256), 0, st, qkv, nq, nkv,
+      hipLaunchKernelGGL((k_mixed<HD, G, F8>), dim3(m.n_tiles * nkv + m.total_units), dim3(256), 0, st, qkv, nq, nkv,
                          kv, m, out, part_o, part_ml);
   } else {
     if (has_pf)
-      hipLaunchKernelGGL((k_prefill<HD, G>), dim3(m.n_tiles * nkv), dim3(64 * kPrefillWaves), 0, st, qkv, nq, nkv,
+      hipLaunchKernelGGL((k_prefill<HD, G, F8>), dim3(m.n_tiles * nkv), dim3(64 * kPrefillWaves), 0, st, qkv, nq, nkv,
                          kv, m, out);
     if (has_dec) {
       if constexpr (kDecodeMfma<G>)
-        hipLaunchKernelGGL((k_decode_mfma<HD, G>), dim3(m.total_units), dim3(64 * kDecWaves), 0, st, qkv, nq, nkv,
+        hipLaunchKernelGGL((k_decode_mfma<HD, G, F8>), dim3(m.total_units), dim3(64 * kDecWaves), 0, st, qkv, nq, nkv,
                            kv, m, out, part_o, part_ml);
       else
-        hipLaunchKernelGGL((k_decode<HD, G>), dim3(m.total_units), dim3(256), 0, st, qkv, nq, nkv, kv, m, out,
+        hipLaunchKernelGGL((k_decode<HD, G, F8>), dim3(m.total_units), dim3(256), 0, st, qkv, nq, nkv, kv, m, out,
                            part_o, part_ml);
     }
   }
@@ -1096,8 +1156,10 @@ static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const 
 hipError_t launch_attention(const Shape &s, const uint16_t *qkv, const KV &kv, const DevMeta &m, uint16_t *out,
                             float *part_o, float *part_ml, int kind, hipStream_t st, int parts) {
   const int G = s.group();
-#define EB_ATT_CASE(HD_, G_) \
-  if (s.hd == HD_ && G == G_) return launch_attention_t<HD_, G_>(s, qkv, kv, m, out, part_o, part_ml, kind, parts, st);
+#define EB_ATT_CASE(HD_, G_)                                                                                 \
+  if (s.hd == HD_ && G == G_)                                                                                \
+    return kv.f8 ? launch_attention_t<HD_, G_, true>(s, qkv, kv, m, out, part_o, part_ml, kind, parts, st)   \
+                 : launch_attention_t<HD_, G_, false>(s, qkv, kv, m, out, part_o, part_ml, kind, parts, st);
   EB_ATT_CASE(128, 1) EB_ATT_CASE(128, 2) EB_ATT_CASE(128, 4) EB_ATT_CASE(128, 8)
   EB_ATT_CASE(64, 1) EB_ATT_CASE(64, 2) EB_ATT_CASE(64, 4) EB_ATT_CASE(64, 8)
 #undef EB_ATT_CASE

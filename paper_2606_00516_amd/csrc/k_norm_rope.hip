@@ -84,15 +84,28 @@ hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gamma, uint16_t *ou
 // RoPE (rotate-half pairs (t, t + hd/2), frequency theta^(-2t/hd), angle
 // formed in fp64) on the q and k heads of one QKV row, q rotated in place,
 // rotated k and v stored at the row's slot of its request's paged cache.
+// Codes of eight bf16 values (packed pairs) divided by scale.
+__device__ __forceinline__ u32x2_t e4m3x8_of_bf16x8(u32x4_t w, float scale) {
+  u32x2_t r;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+    r[i] = e4m3x4_from_f32(bf16_lo(w[2 * i]) / scale, bf16_hi(w[2 * i]) / scale, bf16_lo(w[2 * i + 1]) / scale,
+                           bf16_hi(w[2 * i + 1]) / scale);
+  return r;
+}
+
 // One block per row; a thread moves 8 consecutive dims of one half of a
 // head and their 8 partners in 16-byte accesses.  The angle pos * freq is
 // formed and reduced to [-pi, pi] in fp64; its sine and cosine are then
 // taken in fp32 (the reduced angle is small, so fp32 is accurate to an ulp).
 // ---------------------------------------------------------------------------
+// With an 8-bit cache (F8) the new K and V enter as codes of their bf16
+// values divided by the scale (the division rounded in fp32).
+template <bool F8>
 __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv, uint16_t *__restrict__ kc,
                                                      uint16_t *__restrict__ vc, const int32_t *__restrict__ bt,
                                                      int num_pages, int max_pages, DevMeta m, int nq, int nkv,
-                                                     int hd, double log2_theta) {
+                                                     int hd, double log2_theta, float ks, float vs) {
   __shared__ float cs[64], sn[64];
   const int r = blockIdx.x;
   const int seq = m.row_seq[r];
@@ -133,9 +146,15 @@ __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv,
       st_u32x4(row + h * hd + t0, ra);
       st_u32x4(row + h * hd + t0 + half, rb);
     } else if (page_ok) {
-      uint16_t *dst = kc + (((size_t)page * nkv + (h - nq)) * kPageSize + slot) * hd;
-      st_u32x4(dst + t0, ra);
-      st_u32x4(dst + t0 + half, rb);
+      const size_t e0 = (((size_t)page * nkv + (h - nq)) * kPageSize + slot) * hd;
+      if constexpr (F8) {
+        uint8_t *dst = reinterpret_cast<uint8_t *>(kc) + e0;
+        *reinterpret_cast<u32x2_t *>(dst + t0) = e4m3x8_of_bf16x8(ra, ks);
+        *reinterpret_cast<u32x2_t *>(dst + t0 + half) = e4m3x8_of_bf16x8(rb, ks);
+      } else {
+        st_u32x4(kc + e0 + t0, ra);
+        st_u32x4(kc + e0 + t0 + half, rb);
+      }
     }
   }
   // v: plain copy, 16 bytes per thread
@@ -144,27 +163,37 @@ __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv,
     const int vch = nkv * hd / 8;
     for (int i = threadIdx.x; i < vch; i += blockDim.x) {
       const int kh = (i * 8) / hd, dd = i * 8 - kh * hd;
-      st_u32x4(vc + (((size_t)page * nkv + kh) * kPageSize + slot) * hd + dd, ld_u32x4(vsrc + i * 8));
+      const size_t e0 = (((size_t)page * nkv + kh) * kPageSize + slot) * hd + dd;
+      if constexpr (F8)
+        *reinterpret_cast<u32x2_t *>(reinterpret_cast<uint8_t *>(vc) + e0) = e4m3x8_of_bf16x8(ld_u32x4(vsrc + i * 8), vs);
+      else
+        st_u32x4(vc + e0, ld_u32x4(vsrc + i * 8));
     }
   }
 }
 
 hipError_t launch_rope_append(const Shape &s, uint16_t *qkv, const KV &kv, const DevMeta &m, hipStream_t st) {
   if (m.T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_rope_append, dim3(m.T), dim3(256), 0, st, qkv, kv.k, kv.v, kv.bt, kv.num_pages, kv.max_pages,
-                     m, s.nq, s.nkv, s.hd, log2((double)s.theta));
+  if (kv.f8)
+    hipLaunchKernelGGL(k_rope_append<true>, dim3(m.T), dim3(256), 0, st, qkv, kv.k, kv.v, kv.bt, kv.num_pages,
+                       kv.max_pages, m, s.nq, s.nkv, s.hd, log2((double)s.theta), kv.ks, kv.vs);
+  else
+    hipLaunchKernelGGL(k_rope_append<false>, dim3(m.T), dim3(256), 0, st, qkv, kv.k, kv.v, kv.bt, kv.num_pages,
+                       kv.max_pages, m, s.nq, s.nkv, s.hd, log2((double)s.theta), 1.f, 1.f);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
 // Dense gather of cached positions through the block tables (bit-exact
-// paging probe).  One thread per (position, kv head, 16-byte chunk).
+// paging probe).  One thread per (position, kv head, 16-byte chunk); ES
+// bytes per element (2: bf16, 1: 8-bit codes, copied as they are).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_gather_kv(const uint16_t *__restrict__ kc, const uint16_t *__restrict__ vc,
+template <int ES>
+__global__ __launch_bounds__(256) void k_gather_kv(const uint8_t *__restrict__ kc, const uint8_t *__restrict__ vc,
                                                    const int32_t *__restrict__ bt, int num_pages, int max_pages,
-                                                   DevMeta m, int nkv, int hd, uint16_t *__restrict__ ok,
-                                                   uint16_t *__restrict__ ov) {
-  const int chunks = hd / 8;
+                                                   DevMeta m, int nkv, int hd, uint8_t *__restrict__ ok,
+                                                   uint8_t *__restrict__ ov) {
+  const int chunks = hd * ES / 16;
   const long total = (long)m.gather_off[m.S] * nkv * chunks;
   for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total; idx += (long)gridDim.x * blockDim.x) {
     const int c = (int)(idx % chunks);
@@ -181,11 +210,11 @@ __global__ __launch_bounds__(256) void k_gather_kv(const uint16_t *__restrict__ 
     const int page = bt[(size_t)seq * max_pages + p / kPageSize];
     u32x4_t kv4 = {0, 0, 0, 0}, vv4 = {0, 0, 0, 0};
     if (page >= 0 && page < num_pages) {
-      const size_t src = (((size_t)page * nkv + kh) * kPageSize + p % kPageSize) * hd + c * 8;
+      const size_t src = ((((size_t)page * nkv + kh) * kPageSize + p % kPageSize) * hd) * ES + c * 16;
       kv4 = ld_u32x4(kc + src);
       vv4 = ld_u32x4(vc + src);
     }
-    const size_t dst = ((size_t)gp * nkv + kh) * hd + c * 8;
+    const size_t dst = (((size_t)gp * nkv + kh) * hd) * ES + c * 16;
     st_u32x4(ok + dst, kv4);
     st_u32x4(ov + dst, vv4);
   }
@@ -194,8 +223,14 @@ __global__ __launch_bounds__(256) void k_gather_kv(const uint16_t *__restrict__ 
 hipError_t launch_gather_kv(const Shape &s, const KV &kv, const DevMeta &m, uint16_t *out_k, uint16_t *out_v,
                             hipStream_t st) {
   if (m.S <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_gather_kv, dim3(1024), dim3(256), 0, st, kv.k, kv.v, kv.bt, kv.num_pages, kv.max_pages, m,
-                     s.nkv, s.hd, out_k, out_v);
+  uint8_t *ok = reinterpret_cast<uint8_t *>(out_k), *ov = reinterpret_cast<uint8_t *>(out_v);
+  if (kv.f8)
+    hipLaunchKernelGGL(k_gather_kv<1>, dim3(1024), dim3(256), 0, st, kv.k8(), kv.v8(), kv.bt, kv.num_pages,
+                       kv.max_pages, m, s.nkv, s.hd, ok, ov);
+  else
+    hipLaunchKernelGGL(k_gather_kv<2>, dim3(1024), dim3(256), 0, st, reinterpret_cast<const uint8_t *>(kv.k),
+                       reinterpret_cast<const uint8_t *>(kv.v), kv.bt, kv.num_pages, kv.max_pages, m, s.nkv, s.hd,
+                       ok, ov);
   return hipGetLastError();
 }
 

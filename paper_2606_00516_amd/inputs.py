@@ -334,6 +334,44 @@ def make_kv_pool(shape: LayerShape, batch: Batch, seed: Optional[int] = None, de
     return KVPool(kc, vc, bt_t, pool, bt.shape[1])
 
 
+def make_kv_pool_codes(shape: LayerShape, batch: Batch, seed: Optional[int] = None, device="cpu",
+                       spare_pages: int = 0, poison: bool = True,
+                       max_pages_per_seq: Optional[int] = None) -> KVPool:
+    """Paged 8-bit K/V pool (uint8 E4M3 codes) holding each request's prior
+    context: random bytes with a random sign bit, an exponent field in 4..9
+    and a random 3-bit mantissa (code values 1/8 .. 3.75 in magnitude).  With
+    ``poison`` every other slot holds the NaN code 0x7F."""
+    if seed is None:
+        seed = seeds()["kv"]
+    bt, pool = make_block_tables(batch, spare_pages, seed, shape.page_size, max_pages_per_seq)
+    nkv, P, hd = shape.n_kv_heads, shape.page_size, shape.head_dim
+    g = _gen(device, seed)
+    fill = 0x7F if poison else 0
+    kc = torch.full((pool, nkv, P, hd), fill, dtype=torch.uint8, device=device)
+    vc = torch.full((pool, nkv, P, hd), fill, dtype=torch.uint8, device=device)
+    bt_t = torch.from_numpy(bt).to(device)
+
+    def codes(n):
+        sign = torch.randint(0, 2, (n, nkv, hd), generator=g, device=device) << 7
+        ex = torch.randint(4, 10, (n, nkv, hd), generator=g, device=device) << 3
+        man = torch.randint(0, 8, (n, nkv, hd), generator=g, device=device)
+        return (sign | ex | man).to(torch.uint8)
+
+    for i in range(batch.num_seqs):
+        c = int(batch.context_lens[i])
+        if c == 0:
+            continue
+        npg = (c + P - 1) // P
+        pages = bt_t[i, :npg].long()
+        kvals, vvals = codes(npg * P), codes(npg * P)
+        if poison and c % P:
+            kvals[c:] = 0x7F
+            vvals[c:] = 0x7F
+        kc[pages] = kvals.view(npg, P, nkv, hd).permute(0, 2, 1, 3)
+        vc[pages] = vvals.view(npg, P, nkv, hd).permute(0, 2, 1, 3)
+    return KVPool(kc, vc, bt_t, pool, bt.shape[1])
+
+
 def make_x(shape: LayerShape, num_tokens: int, seed: Optional[int] = None, device="cpu") -> torch.Tensor:
     """Activations entering the layer: bf16 N(0, 1), [num_tokens, hidden]."""
     if seed is None:
