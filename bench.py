@@ -58,6 +58,8 @@ def parse():
     ap.add_argument("--dec-ctx", default=None, help="decode context range lo,hi of the sweep (default 1024,8192)")
     ap.add_argument("--r", type=float, default=0.5, help="decode share for mixed8b")
     ap.add_argument("--budget", type=int, default=2048, help="token budget for mixed8b")
+    ap.add_argument("--kv", default="bf16", choices=["bf16", "fp8"],
+                    help="KV cache element: bf16, or 8-bit E4M3 codes with per-tensor k/v scales")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
     ap.add_argument("--json-out", default=None)
@@ -68,15 +70,16 @@ def parse():
 # algorithmic work of a step (each byte / flop counted once)
 # ----------------------------------------------------------------------------
 
-def step_work(shape, batch):
-    """Bytes and FLOPs a step must move / compute at minimum."""
+def step_work(shape, batch, kv_elem=2):
+    """Bytes and FLOPs a step must move / compute at minimum (``kv_elem``:
+    bytes per cached K or V element, 2 for bf16, 1 for 8-bit codes)."""
     import numpy as np
     nkv, hd, nq, d = shape.n_kv_heads, shape.head_dim, shape.n_q_heads, shape.hidden
     c = batch.context_lens.astype(np.int64)
     n = batch.chunk_lens.astype(np.int64)
     dec = n == 1
-    kv_bytes_dec = int(((c[dec] + 1) * nkv * hd * 4).sum())
-    kv_bytes_pf = int(((c[~dec] + n[~dec]) * nkv * hd * 4).sum())
+    kv_bytes_dec = int(((c[dec] + 1) * nkv * hd * 2 * kv_elem).sum())
+    kv_bytes_pf = int(((c[~dec] + n[~dec]) * nkv * hd * 2 * kv_elem).sum())
     T = int(n.sum())
     w_bytes = shape.weight_bytes()
     act_bytes = T * d * 2 * 2
@@ -108,7 +111,20 @@ def workload(args):
 # CPU oracle baseline
 # ----------------------------------------------------------------------------
 
-def cpu_baseline(shape, batch, w, pool, x, mode, target_s):
+# per-tensor scales of the 8-bit cache: the synthetic codes span 1/8 .. 7.5 in
+# magnitude, so cached values span about 0.06 .. 3.75 like the bf16 N(0, 1) pool
+FP8_SCALES = (0.5, 0.5)
+KV_LABEL = {"bf16": "bf16", "fp8": "fp8-e4m3 codes, per-tensor k/v scales"}
+
+
+def make_pool(gen, shape, batch, kv, **kw):
+    """(paged K/V pool, kv_scales or None) for cache element ``kv``."""
+    if kv == "fp8":
+        return gen.make_kv_pool_codes(shape, batch, **kw), FP8_SCALES
+    return gen.make_kv_pool(shape, batch, **kw), None
+
+
+def cpu_baseline(shape, batch, w, pool, x, mode, target_s, kv_scales=None):
     """The oracle as it is, on the host's cores, over as many requests of the
     same workload as fit in about ``target_s`` seconds."""
     import numpy as np
@@ -138,19 +154,21 @@ def cpu_baseline(shape, batch, w, pool, x, mode, target_s):
         for i in order:
             if i not in staged:
                 ids = torch.as_tensor(bt_host[i, :need[i]].astype(np.int64), device=pool.k_cache.device)
-                staged[i] = (gen.bits(pool.k_cache.index_select(0, ids)).copy(),
-                             gen.bits(pool.v_cache.index_select(0, ids)).copy())
+                host = (lambda t: t.cpu().numpy().copy()) if kv_scales is not None else \
+                    (lambda t: gen.bits(t).copy())
+                staged[i] = (host(pool.k_cache.index_select(0, ids)), host(pool.v_cache.index_select(0, ids)))
             kb0, vb0 = staged[i]
             kb, vb = kb0.copy(), vb0.copy()
             bt = np.arange(need[i], dtype=np.int32)[None]
             xs = xb[off[i]:off[i + 1]]
             t0 = time.perf_counter()
-            oracle.layer_step(cfg, W, kb, vb, bt, batch.context_lens[i:i + 1], batch.chunk_lens[i:i + 1], xs)
+            oracle.layer_step(cfg, W, kb, vb, bt, batch.context_lens[i:i + 1], batch.chunk_lens[i:i + 1], xs,
+                              kv_scales=kv_scales)
             spent += time.perf_counter() - t0
             done.append(int(i))
             rows += int(batch.chunk_lens[i])
             c, n = int(batch.context_lens[i]), int(batch.chunk_lens[i])
-            kv_bytes += (c + n) * shape.n_kv_heads * shape.head_dim * 4
+            kv_bytes += (c + n) * shape.n_kv_heads * shape.head_dim * (2 if kv_scales is not None else 4)
             if spent >= target_s:
                 break
         passes += 1
@@ -167,12 +185,12 @@ def cpu_baseline(shape, batch, w, pool, x, mode, target_s):
 # timing
 # ----------------------------------------------------------------------------
 
-def measure(B, h, step_fn, w, pool, batch, x, y, ws, steps, warmup, profile_steps=None):
+def measure(B, h, step_fn, w, pool, batch, x, y, ws, steps, warmup, profile_steps=None, kv_scales=None):
     """(ms per step over ``steps`` back-to-back steps, mean per-stage ms over a
     second pass with the library's stage events)."""
     import torch
     call = lambda: step_fn(h, w, pool.k_cache, pool.v_cache, pool.block_tables, batch.context_lens,  # noqa: E731
-                           batch.chunk_lens, x, y=y, ws=ws)
+                           batch.chunk_lens, x, y=y, ws=ws, kv_scales=kv_scales)
     for _ in range(warmup):
         call()
     torch.cuda.synchronize()
@@ -212,19 +230,20 @@ def sweep(args, dev):
     pts = []
 
     def run(batch, mode):
-        pool = gen.make_kv_pool(shape, batch, device=dev, poison=False)
+        pool, kvs = make_pool(gen, shape, batch, args.kv, device=dev, poison=False)
         x = gen.make_x(shape, batch.num_tokens, device=dev)
         y = torch.empty_like(x)
         h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
         ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
         fn = {"decode": B.eb_layer_step_decode, "prefill": B.eb_layer_step_prefill,
               "mixed": B.eb_layer_step_mixed}[mode]
-        ms, st = measure(B, h, fn, w, pool, batch, x, y, ws, args.steps, args.warmup, max(3, args.steps // 2))
+        ms, st = measure(B, h, fn, w, pool, batch, x, y, ws, args.steps, args.warmup, max(3, args.steps // 2),
+                         kv_scales=kvs)
         del pool, x, y, ws, h
         torch.cuda.empty_cache()
         gemm = sum(v for k, v in st.items() if k.endswith("gemm"))
         attn = st.get("attention", 0.0) + st.get("attention_combine", 0.0)
-        wk = step_work(shape, batch)
+        wk = step_work(shape, batch, 1 if args.kv == "fp8" else 2)
         return {"ms": ms, "gemm_ms": gemm, "attention_ms": attn, "other_ms": sum(st.values()) - gemm - attn,
                 "kv_bytes_decode": wk["kv_bytes_decode"], "n_tok": wk["T"], "n_decode": batch.num_decode}
 
@@ -298,15 +317,19 @@ def stack70b(args, dev):
         h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
         nbytes = B.eb_stack_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode)
         ws = B.alloc_workspace(nbytes, dev)
-        pool_bytes = int(gen.pages_needed(batch).sum()) * shape.n_kv_heads * shape.page_size * shape.head_dim * 4
+        kv_elem = 1 if args.kv == "fp8" else 2
+        pool_bytes = int(gen.pages_needed(batch).sum()) * shape.n_kv_heads * shape.page_size * shape.head_dim * \
+            2 * kv_elem
         free = torch.cuda.mem_get_info()[0]
         n_pools = max(1, min(L, int((free - (4 << 30)) // max(pool_bytes, 1))))
         t1 = time.perf_counter()
-        pools = [gen.make_kv_pool(shape, batch, seed=s0["kv"] + i, device=dev, poison=False) for i in range(n_pools)]
+        made = [make_pool(gen, shape, batch, args.kv, seed=s0["kv"] + i, device=dev, poison=False)
+                for i in range(n_pools)]
+        pools = [m[0] for m in made]
         x = gen.make_x(shape, batch.num_tokens, device=dev)
         y = torch.empty_like(x)
-        caches = [(pools[l % n_pools].k_cache, pools[l % n_pools].v_cache, pools[l % n_pools].block_tables)
-                  for l in range(L)]
+        caches = [(pools[l % n_pools].k_cache, pools[l % n_pools].v_cache, pools[l % n_pools].block_tables) +
+                  ((made[0][1],) if made[0][1] is not None else ()) for l in range(L)]
         torch.cuda.synchronize()
         print(f"# {name}: {batch.num_seqs} requests, {batch.num_tokens} rows, {n_pools} pool(s) of "
               f"{pool_bytes / 1e9:.1f} GB in {time.perf_counter() - t1:.1f} s", file=sys.stderr, flush=True)
@@ -325,7 +348,7 @@ def stack70b(args, dev):
         st = B.eb_profile_read(h)
         B.eb_profile(h, False)
         torch.cuda.synchronize()
-        wk = step_work(shape, batch)
+        wk = step_work(shape, batch, kv_elem)
         kv = wk["kv_bytes_decode"] + wk["kv_bytes_prefill"]
         gemm_ms = sum(v for k, v in st.items() if k.endswith("gemm"))
         attn_ms = st.get("attention", 0.0)
@@ -344,7 +367,7 @@ def stack70b(args, dev):
         print(f"# {name}: {ms:.2f} ms/step, attention {attn_ms:.1f} ms, GEMMs {gemm_ms:.1f} ms", file=sys.stderr,
               flush=True)
         out.append(pt)
-        del pools, caches, x, y, ws, h, call
+        del made, pools, caches, x, y, ws, h, call
         torch.cuda.empty_cache()
     return out
 
@@ -408,16 +431,16 @@ def long8b(args, dev):
     steps = max(2, args.steps // 5)
 
     def run(batch, mode):
-        pool = gen.make_kv_pool(shape, batch, device=dev, poison=False)
+        pool, kvs = make_pool(gen, shape, batch, args.kv, device=dev, poison=False)
         x = gen.make_x(shape, batch.num_tokens, device=dev)
         y = torch.empty_like(x)
         h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
         ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
         fn = {"decode": B.eb_layer_step_decode, "prefill": B.eb_layer_step_prefill}[mode]
-        ms, st = measure(B, h, fn, w, pool, batch, x, y, ws, steps, 1, 1)
+        ms, st = measure(B, h, fn, w, pool, batch, x, y, ws, steps, 1, 1, kv_scales=kvs)
         del pool, x, y, ws, h
         torch.cuda.empty_cache()
-        wk = step_work(shape, batch)
+        wk = step_work(shape, batch, 1 if args.kv == "fp8" else 2)
         return ms, st, wk
 
     out = {}
@@ -497,7 +520,7 @@ def main():
                 "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
                 "config": {"workload": f"llama3-8b-layer MB sweep, budgets {args.budgets}, decode ctx "
                                        f"{args.dec_ctx or ('16' if args.ctx16 else '1024,8192')}, r = 0..1 step 0.1",
-                           "parallelism": "single-gpu"},
+                           "kv_cache": KV_LABEL[args.kv], "parallelism": "single-gpu"},
                 "sweep": out, "points": pts, "wall_s": round(wall, 1)}
         js = json.dumps(line)
         print(js)
@@ -515,7 +538,7 @@ def main():
                 "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
                 "config": {"workload": "llama3-8b layer, 128K contexts: decode of 4 requests, chunked prefill of a "
                                        "128K prompt (8192-token chunks), single-iteration prompts 1K..128K",
-                           "parallelism": "single-gpu"},
+                           "kv_cache": KV_LABEL[args.kv], "parallelism": "single-gpu"},
                 **out, "wall_s": round(time.perf_counter() - t0, 1)}
         js = json.dumps(line)
         print(js)
@@ -533,7 +556,7 @@ def main():
                 "data": "synthetic",
                 "config": {"workload": f"llama3-8b-layer cost model: MB sweep budgets {args.budgets}, decode ctx "
                                        f"{args.dec_ctx}; decisions and simulated EB / MB / EB+ for the paper's "
-                                       f"mixes", "parallelism": "single-gpu"},
+                                       f"mixes", "kv_cache": KV_LABEL[args.kv], "parallelism": "single-gpu"},
                 **out, "wall_s": round(time.perf_counter() - t0, 1)}
         js = json.dumps(line)
         print(js)
@@ -551,7 +574,7 @@ def main():
                 "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
                 "config": {"workload": f"llama3-70b-shaped model step, {args.layers} layers: decode EB 256 requests "
                                        f"ctx U[2048,16384]; MB 4096-token steps at r = {args.stack_r}",
-                           "parallelism": "single-gpu"},
+                           "kv_cache": KV_LABEL[args.kv], "parallelism": "single-gpu"},
                 "roofline": {"kernel": "k_decode_mfma (decode attention, summed over layers)", "bound": "hbm",
                              "achieved": dec["attention_hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                              "frac": round(dec["attention_hbm_gbps"] / HBM_PEAK_GBPS, 4), "traffic": None},
@@ -568,14 +591,14 @@ def main():
                "mixed": B.eb_layer_step_mixed}[mode]
     # inputs generated on the GPU and left resident in HBM
     w = gen.make_weights(shape, device=dev)
-    pool = gen.make_kv_pool(shape, batch, device=dev)
+    pool, kvs = make_pool(gen, shape, batch, args.kv, device=dev)
     x = gen.make_x(shape, batch.num_tokens, device=dev)
     y = torch.empty_like(x)
     h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
     ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
-    ms, stages = measure(B, h, step_fn, w, pool, batch, x, y, ws, args.steps, args.warmup)
+    ms, stages = measure(B, h, step_fn, w, pool, batch, x, y, ws, args.steps, args.warmup, kv_scales=kvs)
 
-    wk = step_work(shape, batch)
+    wk = step_work(shape, batch, 1 if args.kv == "fp8" else 2)
     step_bytes = wk["kv_bytes_decode"] + wk["kv_bytes_prefill"] + wk["weight_bytes"] + wk["act_bytes"]
     step_flops = wk["gemm_flops"] + wk["attn_flops_decode"] + wk["attn_flops_prefill"]
     gemm_ms = sum(v for k, v in stages.items() if k.endswith("gemm"))
@@ -616,6 +639,7 @@ def main():
     try:
         cnt = json.load(open(COUNTERS))
         key = {"decode8b": "decode_attention_8b", "decode70b": "decode_attention_70b"}.get(args.workload)
+        key = key + "_fp8" if key and args.kv == "fp8" else key
         ent = cnt.get(key) if key else None
         if ent and ent.get("source_sha") == sha_of(ATTN_SRC):
             roof["traffic"] = ent["bytes_per_dispatch"]
@@ -626,8 +650,10 @@ def main():
         "metric": METRIC, "value": round(value, 3), "unit": unit, "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": label, "num_tokens": wk["T"], "num_requests": batch.num_seqs,
-                   "decode_share": round(batch.num_decode / max(wk["T"], 1), 4), "parallelism": "single-gpu"},
+        "config": {"workload": label, "kv_cache": KV_LABEL[args.kv], "num_tokens": wk["T"],
+                   "num_requests": batch.num_seqs,
+                   "decode_share": round(batch.num_decode / max(wk["T"], 1), 4), "kv_cache": KV_LABEL[args.kv],
+                   "parallelism": "single-gpu"},
         "tokens_per_s": round(wk["T"] / (ms / 1e3), 1),
         "step_bytes": step_bytes, "step_flops": step_flops,
         "stage_ms": {k: round(v, 5) for k, v in stages.items()},
@@ -635,7 +661,7 @@ def main():
         "roofline": roof,
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(shape, batch, w, pool, x, mode, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(shape, batch, w, pool, x, mode, args.cpu_seconds, kvs)
     out = json.dumps(line)
     print(out)
     if args.json_out:

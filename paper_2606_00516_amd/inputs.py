@@ -339,7 +339,7 @@ def make_kv_pool_codes(shape: LayerShape, batch: Batch, seed: Optional[int] = No
                        max_pages_per_seq: Optional[int] = None) -> KVPool:
     """Paged 8-bit K/V pool (uint8 E4M3 codes) holding each request's prior
     context: random bytes with a random sign bit, an exponent field in 4..9
-    and a random 3-bit mantissa (code values 1/8 .. 3.75 in magnitude).  With
+    and a random 3-bit mantissa (code values 1/8 .. 7.5 in magnitude).  With
     ``poison`` every other slot holds the NaN code 0x7F."""
     if seed is None:
         seed = seeds()["kv"]

@@ -1,6 +1,9 @@
 """Pins of the oracle's E4M3 cache codes (oracle/fp8.py): torch's own
 float8_e4m3fn conversions (a library routine) for every code and for values in
-range, closed forms for the saturating and non-finite cases and the ties."""
+range, closed forms for the saturating and non-finite cases and the ties; and
+of the layer step on an 8-bit cache: the transformers Llama layer in fp64 whose
+cache reads and writes through torch's conversions, with planted mistakes in
+the oracle's code handling that must fail it."""
 import numpy as np
 import pytest
 import torch
@@ -57,3 +60,87 @@ def test_cache_value_round_trip_error():
     back = F.dequantize(F.quantize_cache_value(v, 0.125), 0.125)
     big = np.abs(v) > 0.125 * 2 ** -6
     assert np.all(np.abs(back[big] - v[big]) <= np.abs(v[big]) / 16 + 1e-12)
+
+
+# ------------------------------------------------- the layer step on codes
+
+from oracle import layer as L  # noqa: E402
+import oracle  # noqa: E402
+from paper_2606_00516_amd import inputs as gen  # noqa: E402
+from tests._cases import oracle_cfg  # noqa: E402
+from tests._hf import hf_reference  # noqa: E402
+
+KS, VS = 0.37, 0.61
+# a prompt chunk over a paged prefix, a prompt with no prefix and a decode row
+_BATCH = gen.Batch(np.array([40, 0, 77], np.int32), np.array([56, 33, 1], np.int32))
+
+
+def _code_inputs():
+    shape = gen.TINY
+    w = gen.make_weights(shape, proj_std=0.2)
+    pool = gen.make_kv_pool_codes(shape, _BATCH, spare_pages=3, poison=True)
+    return shape, dict(cfg=oracle_cfg(shape), w_bits={k: gen.bits(v) for k, v in w.items()},
+                       k_cache=pool.k_cache.numpy().copy(), v_cache=pool.v_cache.numpy().copy(),
+                       block_tables=pool.block_tables.numpy(), context_lens=_BATCH.context_lens,
+                       chunk_lens=_BATCH.chunk_lens, x_bits=gen.bits(gen.make_x(shape, _BATCH.num_tokens)))
+
+
+def _oracle_on_codes(o, mode="batched"):
+    W = oracle.prepare_weights(o["w_bits"], o["cfg"], np.float64)
+    kc, vc = o["k_cache"].copy(), o["v_cache"].copy()
+    y, inter = oracle.layer_step(o["cfg"], W, kc, vc, o["block_tables"], o["context_lens"], o["chunk_lens"],
+                                 o["x_bits"], mode=mode, intermediates=True, kv_scales=(KS, VS))
+    return y, inter, kc, vc
+
+
+def _maxrel(a, b):
+    return float(np.max(np.abs(np.asarray(a) - b)) / max(np.max(np.abs(b)), 1e-30))
+
+
+@pytest.mark.parametrize("mode", ["batched", "exact"])
+def test_layer_on_codes_matches_transformers(mode):
+    # the transformers Llama layer in fp64 whose cache reads and writes codes
+    # through torch's float8_e4m3fn: the same layer on an 8-bit cache
+    shape, o = _code_inputs()
+    y, inter, kc, vc = _oracle_on_codes(o, mode)
+    x = L.bf16_bits_to_f32(o["x_bits"]).astype(np.float64)
+    off = _BATCH.row_offsets
+    for i in range(_BATCH.num_seqs):
+        rows = slice(off[i], off[i + 1])
+        attn_b, mlp_b, y_ref = hf_reference(shape, o, i, (KS, VS))
+        assert _maxrel(inter["h1"][rows] - x[rows], attn_b) < 1e-9
+        assert _maxrel(y[rows], y_ref) < 1e-9
+    # the codes written are the new positions' only; everything else unchanged
+    changed = np.any(kc != o["k_cache"], axis=(1, 3)) | np.any(vc != o["v_cache"], axis=(1, 3))
+    bt = o["block_tables"]
+    want = np.zeros_like(changed)
+    for i in range(_BATCH.num_seqs):
+        p = int(_BATCH.context_lens[i]) + np.arange(int(_BATCH.chunk_lens[i]))
+        want[bt[i][p // 16], p % 16] = True
+    assert np.array_equal(changed & ~want, np.zeros_like(changed))
+
+
+def test_planted_code_mistakes_are_caught(monkeypatch):
+    # each mistake planted in the oracle's code handling moves the attention
+    # branch far outside the 1e-9 bound of the transformers pin
+    shape, o = _code_inputs()
+    x = L.bf16_bits_to_f32(o["x_bits"]).astype(np.float64)
+    refs = [hf_reference(shape, o, i, (KS, VS))[0] for i in range(_BATCH.num_seqs)]
+    good_q, good_d = F.quantize_cache_value, F.dequantize
+
+    def truncate(v, s):  # round toward zero instead of to nearest
+        q = good_q(v, s)
+        over = np.abs(good_d(q, s)) > np.abs(np.asarray(v, np.float64))
+        return np.where(over & ((q & 0x7F) > 0), q - 1, q).astype(np.uint8)
+
+    plants = {"no scale on read": ("dequantize", lambda c, s: good_d(c, 1.0)),
+              "no division on write": ("quantize_cache_value", lambda v, s: good_q(v, 1.0)),
+              "truncating encoder": ("quantize_cache_value", truncate)}
+    for name, (fn, bad) in plants.items():
+        with monkeypatch.context() as m:
+            m.setattr(F, fn, bad)
+            _, inter, _, _ = _oracle_on_codes(o)
+        off = _BATCH.row_offsets
+        worst = max(_maxrel(inter["h1"][off[i]:off[i + 1]] - x[off[i]:off[i + 1]], refs[i])
+                    for i in range(_BATCH.num_seqs))
+        assert worst > 1e-3, (name, worst)

@@ -9,6 +9,7 @@ import oracle
 from oracle import layer as L
 from paper_2606_00516_amd import inputs as gen
 from tests._cases import make_case, oracle_cfg, tiny_case
+from tests._hf import hf_reference as _hf_reference
 
 RNG = np.random.default_rng(1234)
 
@@ -169,82 +170,6 @@ def test_paged_gather_identity_and_relabelling():
 
 
 # ---------------------------------------------------------------- whole layer
-
-def _hf_layer(shape, w_bits):
-    from transformers import LlamaConfig
-    from transformers.models.llama.modeling_llama import LlamaDecoderLayer, LlamaRotaryEmbedding
-    cfg = LlamaConfig(hidden_size=shape.hidden, intermediate_size=shape.ffn,
-                      num_attention_heads=shape.n_q_heads, num_key_value_heads=shape.n_kv_heads,
-                      head_dim=shape.head_dim, rms_norm_eps=shape.rms_eps, rope_theta=shape.rope_theta,
-                      attention_bias=False, mlp_bias=False)
-    cfg._attn_implementation = "sdpa"  # the eager path takes its softmax in fp32
-    layer = LlamaDecoderLayer(cfg, layer_idx=0).double()
-    rot = LlamaRotaryEmbedding(cfg).double()
-    # the library forms its frequencies in fp32; recompute them in fp64
-    hd = shape.head_dim
-    rot.inv_freq = shape.rope_theta ** (-torch.arange(0, hd, 2, dtype=torch.float64) / hd)
-    f = lambda k: torch.from_numpy(L.bf16_bits_to_f32(w_bits[k]).astype(np.float64))  # noqa: E731
-    nq, nkv, hd, ff = shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn
-    qkv, gu = f("w_qkv"), f("w_gate_up")
-    # the library's RMSNorm module computes in fp32; use torch's in fp64
-    layer.input_layernorm = torch.nn.RMSNorm(shape.hidden, eps=shape.rms_eps, dtype=torch.float64)
-    layer.post_attention_layernorm = torch.nn.RMSNorm(shape.hidden, eps=shape.rms_eps, dtype=torch.float64)
-    with torch.no_grad():
-        layer.self_attn.q_proj.weight.copy_(qkv[: nq * hd])
-        layer.self_attn.k_proj.weight.copy_(qkv[nq * hd:(nq + nkv) * hd])
-        layer.self_attn.v_proj.weight.copy_(qkv[(nq + nkv) * hd:])
-        layer.self_attn.o_proj.weight.copy_(f("w_o"))
-        layer.mlp.gate_proj.weight.copy_(gu[:ff])
-        layer.mlp.up_proj.weight.copy_(gu[ff:])
-        layer.mlp.down_proj.weight.copy_(f("w_down"))
-        layer.input_layernorm.weight.copy_(f("attn_norm"))
-        layer.post_attention_layernorm.weight.copy_(f("mlp_norm"))
-    return layer, rot
-
-
-class _Bf16Cache:
-    """Minimal KV cache for the library layer: holds a request's prior K/V and
-    stores each appended K/V rounded to bf16 (through fp32), as a bf16 paged
-    cache does; returns everything stored so far."""
-
-    def __init__(self, k_prior, v_prior):
-        self.k, self.v = k_prior, v_prior            # [1, n_kv, c, hd] fp64
-
-    def update(self, k, v, layer_idx, cache_kwargs=None):
-        rnd = lambda t: t.float().to(torch.bfloat16).double()  # noqa: E731
-        self.k = torch.cat([self.k, rnd(k)], dim=2)
-        self.v = torch.cat([self.v, rnd(v)], dim=2)
-        return self.k, self.v
-
-
-def _hf_reference(shape, o, seq):
-    """The library decoder layer in fp64 on request ``seq`` of an oracle input
-    set: returns (h1 - x, y - h1, y) for that request's rows."""
-    layer, rot = _hf_layer(shape, o["w_bits"])
-    c, n = int(o["context_lens"][seq]), int(o["chunk_lens"][seq])
-    r0 = int(np.sum(o["chunk_lens"][:seq]))
-    bt = o["block_tables"][seq]
-    pos = np.arange(c)
-    kp = L.bf16_bits_to_f32(o["k_cache"][bt[pos // 16], :, pos % 16, :]).astype(np.float64)
-    vp = L.bf16_bits_to_f32(o["v_cache"][bt[pos // 16], :, pos % 16, :]).astype(np.float64)
-    cache = _Bf16Cache(torch.from_numpy(kp).permute(1, 0, 2)[None], torch.from_numpy(vp).permute(1, 0, 2)[None])
-    x = torch.from_numpy(L.bf16_bits_to_f32(o["x_bits"][r0:r0 + n]).astype(np.float64))[None]
-    p = torch.arange(c, c + n)[None]
-    mask = torch.zeros(n, c + n, dtype=torch.float64)
-    mask[torch.arange(c + n)[None, :] > (c + torch.arange(n))[:, None]] = float("-inf")
-    # the library's rotary module forms angles in fp32; give the layer fp64
-    # cos/sin in its own (duplicated-halves) format instead
-    ang = p[0].double()[:, None] * rot.inv_freq[None, :]
-    emb = torch.cat([ang, ang], dim=-1)[None]
-    pe = (emb.cos(), emb.sin())
-    with torch.no_grad():
-        a = layer.input_layernorm(x)
-        attn_branch = layer.self_attn(a, attention_mask=mask[None, None], position_ids=p,
-                                      position_embeddings=pe, past_key_values=cache)[0]
-        h1 = x + attn_branch
-        mlp_branch = layer.mlp(layer.post_attention_layernorm(h1))
-    return attn_branch[0].numpy(), mlp_branch[0].numpy(), (h1 + mlp_branch)[0].numpy()
-
 
 # A prompt chunk with a paged prior prefix, and decode rows, against the
 # library decoder layer in fp64.  Projections N(0, 0.2) make the softmax
