@@ -13,6 +13,8 @@
 #include "eb_internal.h"
 #include "host_plan.h"
 
+static_assert(eb::kDecInfo == eb::kDecInfoInts, "decode record layout");
+
 using namespace eb;
 
 namespace {
@@ -87,6 +89,7 @@ DevMeta meta_at(const HostPlan &p, const int32_t *dev) {
   m.dec_seq = dev + p.o_dec_seq;
   m.dec_split_off = dev + p.o_dec_off;
   m.dec_unit_off = dev + p.o_unit_off;
+  m.dec_info = dev + p.o_dec_info;
   m.comb_list = dev + p.o_comb;
   m.tile_seq = dev + p.o_tseq;
   m.tile_qb = dev + p.o_tqb;

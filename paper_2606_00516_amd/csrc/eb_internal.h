@@ -15,6 +15,8 @@ constexpr int kPageSize = 16;
 // of kShortDecodeHeads kv heads, one wavefront each, instead of page splits.
 constexpr int kShortDecodeKeys = 64;
 constexpr int kShortDecodeHeads = 4;
+// int32 fields per decode-request record in DevMeta::dec_info
+constexpr int kDecInfoInts = 8;
 
 // Prefill attention items: query positions per item for a GQA group size,
 // in the prefill-only launch and inside the mixed launch (must agree with
@@ -33,6 +35,8 @@ struct DevMeta {
   const int32_t *dec_seq;       // [D] request index of each decode request
   const int32_t *dec_split_off; // [D+1] prefix sum of split counts
   const int32_t *dec_unit_off;  // [D+1] prefix sum of work units (blocks)
+  const int32_t *dec_info;      // [D+1][8] {first unit, first split, request, row, keys, 0, 0, 0}; the
+                                // closing record holds the unit and split totals
   const int32_t *comb_list;     // [C] decode indices with >= 2 splits
   const int32_t *tile_seq;      // [NT] prefill tiles, longest first
   const int32_t *tile_qb;       // [NT] query block of each tile

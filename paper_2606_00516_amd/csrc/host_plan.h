@@ -10,6 +10,10 @@
 
 namespace eb {
 
+// int32 fields of a decode request's record: first work unit, first split,
+// request, first row, keys (c + 1), padding to 32 bytes
+constexpr int kDecInfo = 8;
+
 struct HostPlan {
   int32_t S = 0, T = 0;
   int32_t n_dec = 0, total_splits = 0, total_units = 0, n_comb = 0, n_tiles = 0;
@@ -17,7 +21,7 @@ struct HostPlan {
   std::vector<int32_t> blob;  // every metadata array, concatenated
   // offsets (in int32 elements) of each array inside blob
   size_t o_ctx = 0, o_len = 0, o_row = 0, o_row_seq = 0, o_row_pos = 0, o_dec_seq = 0, o_dec_off = 0, o_unit_off = 0,
-         o_comb = 0, o_tseq = 0, o_tqb = 0, o_goff = 0;
+         o_dec_info = 0, o_comb = 0, o_tseq = 0, o_tqb = 0, o_goff = 0;
 };
 
 // Shape support: head_dim in {64, 128}; G = n_q / n_kv in {1, 2, 4, 8};

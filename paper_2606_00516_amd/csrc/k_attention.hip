@@ -213,12 +213,51 @@ __device__ __forceinline__ void decode_merge_lanes(float (&mrun)[G], float (&lru
 // outputs, then [wave][h][2] max and sum) and write the unit's result: the
 // final row (one split) or a partial for the combine.
 // vscale: the value scale of an 8-bit cache (1 for bf16: exact).
+// The decode request a work unit belongs to.  The whole block looks it up at
+// once: thread t tests requests t, t + blockDim.x, .. against the unit
+// ranges of their records, so the lookup costs one round of independent
+// loads instead of a chain of dependent ones; the match goes through LDS.
+struct DecUnit {
+  int local;      // unit index within the request
+  int split_off;  // first global split index of the request
+  int nsplit;     // splits of the request
+  int seq, row, nkeys;
+};
+
+__device__ __forceinline__ DecUnit find_decode_unit(const DevMeta &md, int unit) {
+  __shared__ int32_t cell[8];
+  for (int t = threadIdx.x; t < md.n_dec; t += blockDim.x) {
+    const int32_t *r = md.dec_info + (size_t)t * kDecInfoInts;
+    u32x4_t a = ld_u32x4(r);                                                   // unit, split, seq, row
+    u32x4_t b = ld_u32x4(r + 4);                                               // keys, ..
+    u32x4_t n = ld_u32x4(r + kDecInfoInts);                                    // the next record
+    // all three loads issued before the test (not only by the matching thread)
+    asm volatile("" : "+v"(a), "+v"(b), "+v"(n));
+    if ((int)a[0] <= unit && unit < (int)n[0]) {
+      cell[0] = unit - (int)a[0];
+      cell[1] = (int)a[1];
+      cell[2] = (int)(n[1] - a[1]);
+      cell[3] = (int)a[2];
+      cell[4] = (int)a[3];
+      cell[5] = (int)b[0];
+    }
+  }
+  __syncthreads();
+  DecUnit u;
+  u.local = __builtin_amdgcn_readfirstlane(cell[0]);
+  u.split_off = __builtin_amdgcn_readfirstlane(cell[1]);
+  u.nsplit = __builtin_amdgcn_readfirstlane(cell[2]);
+  u.seq = __builtin_amdgcn_readfirstlane(cell[3]);
+  u.row = __builtin_amdgcn_readfirstlane(cell[4]);
+  u.nkeys = __builtin_amdgcn_readfirstlane(cell[5]);
+  return u;
+}
+
 template <int HD, int G, int NW>
-__device__ __forceinline__ void decode_merge_waves(const float *lds, int row, int kh, int nq, int nkv, int item,
-                                                   int nsplit, uint16_t *__restrict__ out, float *__restrict__ part_o,
-                                                   float *__restrict__ part_ml, float vscale) {
-  const float *lo_ = lds;
-  const float *lml = lds + NW * G * HD;
+__device__ __forceinline__ void decode_merge_waves(const float *lo_, const float *lml, int row, int kh, int nq,
+                                                   int nkv, int item, int nsplit, uint16_t *__restrict__ out,
+                                                   float *__restrict__ part_o, float *__restrict__ part_ml,
+                                                   float vscale) {
   __syncthreads();
   for (int e = threadIdx.x; e < G * HD; e += blockDim.x) {
     const int h = e / HD, dim = e - h * HD;
@@ -312,14 +351,14 @@ EB_DEV int mdec_swz(int t) {
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// Start the loads of page p's K and V blocks into a slot; slots at or past
-// k1 (and pages past the end or with a bad table entry) land as zeros
-// without memory traffic, so cache poison never reaches the products.
+// Start the loads of page p (physical page phys, -1 past the end) K and V
+// blocks into a slot; slots at or past k1 (and pages past the end or with a
+// bad table entry) land as zeros without memory traffic, so cache poison
+// never reaches the products.
 template <int HD, bool F8>
-__device__ __forceinline__ void mdec_dma_page(uint8_t *slot, const uint32_t *goff, const KV kv,
-                                              const int32_t *bt, int p, int pg1, int k1, int nkv, int kh) {
+__device__ __forceinline__ void mdec_dma_page(uint8_t *slot, const uint32_t *goff, const KV kv, int phys, int p,
+                                              int k1, int nkv, int kh) {
   using Tr = MdecTraits<HD, F8>;
-  const int phys = p < pg1 ? bt[p] : -1;
   const int nvalid = min(max(k1 - p * kPageSize, 0), kPageSize);
   const bool ok = phys >= 0 && phys < kv.num_pages;
   const size_t off = ok ? ((size_t)phys * nkv + kh) * kPageSize * HD : 0;
@@ -405,17 +444,21 @@ __device__ __forceinline__ void mdec_page_update(const uint8_t *slot, const u32x
 }
 
 // Stream pages p_first, p_first + stride, .. (< pg1) through the wave's
-// NSLOT slots (NSLOT - 1 pages in flight while one is consumed).  Loads of
-// pages past the end cost no memory traffic; every load has landed when
-// this returns.
+// NSLOT slots (NSLOT - 1 pages in flight while one is consumed).  Lane l of
+// vbt holds the physical page of page pbase + l (all pages streamed lie in
+// pbase .. pbase + 63), so no page waits for a table load.  Loads of pages
+// past the end cost no memory traffic; every load has landed when this
+// returns.
 template <int HD, int NSLOT, bool F8>
 __device__ __forceinline__ void mdec_stream(uint8_t *s0, uint8_t *s1, uint8_t *s2, uint8_t *s3, const KV kv,
-                                            const int32_t *bt, int p_first, int stride, int pg1, int k1, int nkv,
+                                            int vbt, int pbase, int p_first, int stride, int pg1, int k1, int nkv,
                                             int kh, int lane, float qscale, const u32x4_t (&qb)[HD / 32],
                                             const u32x4_t (&sel)[2], float &mrun, float &lsum,
                                             f32x4_t (&oacc)[HD / 16]) {
   using Tr = MdecTraits<HD, F8>;
   static_assert(NSLOT >= 2 && NSLOT <= 4, "ring depth");
+  static_assert(kDecodePagesPerSplit <= 64 && (kShortDecodeKeys + kPageSize - 1) / kPageSize <= 64,
+                "a wave's pages fit one table entry per lane");
   uint32_t goff[Tr::NDMA];
 #pragma unroll
   for (int i = 0; i < Tr::NDMA; ++i) {
@@ -423,8 +466,9 @@ __device__ __forceinline__ void mdec_stream(uint8_t *s0, uint8_t *s1, uint8_t *s
     const int t = e / Tr::ROW, u = (e % Tr::ROW) >> 4;
     goff[i] = (uint32_t)(t * Tr::ROW + ((u ^ mdec_swz<HD, F8>(t)) << 4));
   }
-#define EB_DMA(S_, P_)                                                  \
-  mdec_dma_page<HD, F8>(S_, goff, kv, bt, P_, pg1, k1, nkv, kh);        \
+#define EB_DMA(S_, P_)                                                                             \
+  mdec_dma_page<HD, F8>(S_, goff, kv, (P_) < pg1 ? __builtin_amdgcn_readlane(vbt, (P_) - pbase) : -1, P_, k1, \
+                        nkv, kh);                                                                    \
   __builtin_amdgcn_sched_barrier(0);
 #define EB_UPD(S_, P_)                                                                  \
   if ((P_) < pg1) mdec_page_update<HD, F8>(S_, qb, sel, mrun, lsum, oacc, P_, k1, lane, qscale); \
@@ -501,22 +545,18 @@ __device__ __forceinline__ void mdec_init(const uint16_t *__restrict__ qkv, int 
 
 // One decode work unit on the matrix cores (same units as decode_item),
 // run by NW wavefronts with NSLOT-deep page rings.  l0..l3: the block's
-// slot arrays (NW slots each; the first NSLOT are used); the cross-wave
-// merge reuses l0 once every wave has finished streaming.
-template <int HD, int NW, int NSLOT>
-struct MdecBlock {
-  static constexpr int SLOT_ARRAY = NW * MdecTraits<HD>::SLOT;  // bytes per slot array
-};
-
-template <int HD, int G, int NW, int NSLOT, bool F8>
+// slot arrays (NW slots of SLOT bytes each; the first NSLOT arrays are
+// used); once every wave has finished streaming, the cross-wave merge puts
+// the outputs in l0 and the (max, sum) pairs in l1.
+template <int HD, int G, int NW, int NSLOT, bool F8, int SLOT>
 __device__ __forceinline__ void decode_item_mfma(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
                                                  const DevMeta md, int unit, uint16_t *__restrict__ out,
                                                  float *__restrict__ part_o, float *__restrict__ part_ml, uint8_t *l0,
                                                  uint8_t *l1, uint8_t *l2, uint8_t *l3) {
-  constexpr int SLOT = MdecTraits<HD>::SLOT;  // the bf16 slot size (an 8-bit page uses its first half)
   constexpr int SPLIT = kDecodePagesPerSplit * kPageSize;
   constexpr int NOB = HD / 16;
-  static_assert(DecodeTraits<HD, G, NW>::LDS_BYTES <= MdecBlock<HD, NW, NSLOT>::SLOT_ARRAY, "merge area");
+  static_assert(SLOT >= MdecTraits<HD, F8>::SLOT, "slot holds a page's K and V blocks");
+  static_assert(NW * G * HD * 4 <= NW * SLOT && NW * G * 2 * 4 <= NW * SLOT, "merge area");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int cols = (nq + 2 * nkv) * HD;
@@ -525,17 +565,9 @@ __device__ __forceinline__ void decode_item_mfma(const uint16_t *__restrict__ qk
   const int c = lane & 15, g = lane >> 4;
   uint8_t *w0 = l0 + wave * SLOT, *w1 = l1 + wave * SLOT, *w2 = l2 + wave * SLOT, *w3 = l3 + wave * SLOT;
 
-  int lo = 0, hi = md.n_dec - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (md.dec_unit_off[mid] <= unit) lo = mid; else hi = mid - 1;
-  }
-  const int d = lo;
-  const int local = unit - md.dec_unit_off[d];
-  const int seq = md.dec_seq[d];
-  const int nkeys = md.seq_ctx[seq] + 1;
-  const int row = md.seq_row[seq];
-  const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
+  const DecUnit du = find_decode_unit(md, unit);
+  const int local = du.local, nkeys = du.nkeys, row = du.row;
+  const int32_t *bt = kv.bt + (size_t)du.seq * kv.max_pages;
   u32x4_t qb[HD / 32], sel[2];
   float mrun, lsum;
   f32x4_t oacc[NOB];
@@ -545,9 +577,11 @@ __device__ __forceinline__ void decode_item_mfma(const uint16_t *__restrict__ qk
     for (int hw = wave; hw < kShortDecodeHeads; hw += NW) {
       const int kh = local * kShortDecodeHeads + hw;
       if (kh >= nkv) break;
+      const int npg = (nkeys + kPageSize - 1) / kPageSize;
+      const int vbt = lane < npg ? bt[lane] : -1;
       mdec_init<HD, G>(qkv, cols, row, kh, lane, qb, sel, mrun, lsum, oacc);
-      mdec_stream<HD, NSLOT, F8>(w0, w1, w2, w3, kv, bt, 0, 1, (nkeys + kPageSize - 1) / kPageSize, nkeys, nkv, kh,
-                                 lane, qscale, qb, sel, mrun, lsum, oacc);
+      mdec_stream<HD, NSLOT, F8>(w0, w1, w2, w3, kv, vbt, 0, 0, 1, npg, nkeys, nkv, kh, lane, qscale, qb, sel, mrun,
+                                 lsum, oacc);
       lsum += shfl_xor_f32(lsum, 16);
       lsum += shfl_xor_f32(lsum, 32);
       if (c < G) {
@@ -565,33 +599,35 @@ __device__ __forceinline__ void decode_item_mfma(const uint16_t *__restrict__ qk
   }
 
   const int split = local / nkv, kh = local - split * nkv;
-  const int item = md.dec_split_off[d] + split;
-  const int nsplit = md.dec_split_off[d + 1] - md.dec_split_off[d];
+  const int item = du.split_off + split;
+  const int nsplit = du.nsplit;
   const int k0 = split * SPLIT;
   const int k1 = min(nkeys, k0 + SPLIT);
   const int pg0 = k0 / kPageSize, pg1 = (k1 + kPageSize - 1) / kPageSize;
+  // the split's block-table entries, one per lane, fetched once
+  const int vbt = pg0 + lane < pg1 ? bt[pg0 + lane] : -1;
   mdec_init<HD, G>(qkv, cols, row, kh, lane, qb, sel, mrun, lsum, oacc);
-  mdec_stream<HD, NSLOT, F8>(w0, w1, w2, w3, kv, bt, pg0 + wave, NW, pg1, k1, nkv, kh, lane, qscale, qb, sel, mrun,
-                             lsum, oacc);
+  mdec_stream<HD, NSLOT, F8>(w0, w1, w2, w3, kv, vbt, pg0, pg0 + wave, NW, pg1, k1, nkv, kh, lane, qscale, qb, sel,
+                             mrun, lsum, oacc);
   lsum += shfl_xor_f32(lsum, 16);
   lsum += shfl_xor_f32(lsum, 32);
-  // across the NW waves through LDS (reusing l0 once every wave is done with
-  // its slots): [wave][h][HD] outputs, then [wave][h][2]
-  float *merge = reinterpret_cast<float *>(l0);
+  // across the NW waves through LDS (reusing the slots once every wave is
+  // done with them): [wave][h][HD] outputs in l0, [wave][h][2] in l1
+  float *merge_o = reinterpret_cast<float *>(l0), *merge_ml = reinterpret_cast<float *>(l1);
   __syncthreads();
   if (c < G) {
-    float *o_ = merge + (wave * G + c) * HD + g * 4;
+    float *o_ = merge_o + (wave * G + c) * HD + g * 4;
 #pragma unroll
     for (int ob = 0; ob < NOB; ++ob)
 #pragma unroll
       for (int j = 0; j < 4; ++j) o_[ob * 16 + j] = oacc[ob][j];
     if (g == 0) {
-      float *ml = merge + NW * G * HD + (wave * G + c) * 2;
+      float *ml = merge_ml + (wave * G + c) * 2;
       ml[0] = mrun;
       ml[1] = lsum;
     }
   }
-  decode_merge_waves<HD, G, NW>(merge, row, kh, nq, nkv, item, nsplit, out, part_o, part_ml, vscale);
+  decode_merge_waves<HD, G, NW>(merge_o, merge_ml, row, kh, nq, nkv, item, nsplit, out, part_o, part_ml, vscale);
 }
 
 // One decode work unit.  Unit u of decode request d (binary search over the
@@ -616,17 +652,9 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
   const float qscale = F8 ? kLog2e / sqrtf((float)HD) * kv.ks : kLog2e / sqrtf((float)HD);
   const float vscale = F8 ? kv.vs : 1.f;
 
-  int lo = 0, hi = md.n_dec - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (md.dec_unit_off[mid] <= unit) lo = mid; else hi = mid - 1;
-  }
-  const int d = lo;
-  const int local = unit - md.dec_unit_off[d];
-  const int seq = md.dec_seq[d];
-  const int nkeys = md.seq_ctx[seq] + 1;
-  const int row = md.seq_row[seq];
-  const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
+  const DecUnit du = find_decode_unit(md, unit);
+  const int local = du.local, nkeys = du.nkeys, row = du.row;
+  const int32_t *bt = kv.bt + (size_t)du.seq * kv.max_pages;
   const int dq = (lane % LPT) * 8;
   u32x4_t qw[G];
   float mrun[G], lrun[G], o[G][8];
@@ -651,8 +679,8 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
   }
 
   const int split = local / nkv, kh = local - split * nkv;
-  const int item = md.dec_split_off[d] + split;   // global split index (partials)
-  const int nsplit = md.dec_split_off[d + 1] - md.dec_split_off[d];
+  const int item = du.split_off + split;   // global split index (partials)
+  const int nsplit = du.nsplit;
   const int k0 = split * SPLIT;
   const int k1 = min(nkeys, k0 + SPLIT);
   const int pg0 = k0 / kPageSize, pg1 = (k1 + kPageSize - 1) / kPageSize;
@@ -674,7 +702,8 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
       }
     }
   }
-  decode_merge_waves<HD, G, NW>(lds, row, kh, nq, nkv, item, nsplit, out, part_o, part_ml, vscale);
+  decode_merge_waves<HD, G, NW>(lds, lds + NW * G * HD, row, kh, nq, nkv, item, nsplit, out, part_o, part_ml,
+                                vscale);
 }
 
 // Combine the splits of one decode request for one query head:
@@ -1046,21 +1075,26 @@ __global__ __launch_bounds__(256, 2) void k_decode(const uint16_t *qkv, int nq, 
 
 // The matrix-core decode keeps its page slots in separate LDS arrays, so the
 // compiler's wait before reading one slot covers only that slot's loads.
-// Decode-only launch: kDecWaves wavefronts per block, kDecSlots-deep rings.
-constexpr int kDecWaves = 4, kDecSlots = 2;
-#define EB_MDEC_LDS(HD_, NW_, NSLOT_)                                                                 \
-  __shared__ __attribute__((aligned(16))) uint8_t l0[MdecBlock<HD_, NW_, NSLOT_>::SLOT_ARRAY];          \
-  __shared__ __attribute__((aligned(16))) uint8_t l1[MdecBlock<HD_, NW_, NSLOT_>::SLOT_ARRAY];          \
-  __shared__ __attribute__((aligned(16))) uint8_t l2[NSLOT_ > 2 ? MdecBlock<HD_, NW_, NSLOT_>::SLOT_ARRAY : 16]; \
-  __shared__ __attribute__((aligned(16))) uint8_t l3[NSLOT_ > 3 ? MdecBlock<HD_, NW_, NSLOT_>::SLOT_ARRAY : 16];
+// Decode-only launch: kDecWaves wavefronts per block, rings kDecSlots deep
+// for bf16 pages and kDecSlotsF8 deep for 8-bit ones (a slot sized to the
+// page, half the bf16 one).
+constexpr int kDecWaves = 4, kDecSlots = 2, kDecSlotsF8 = 2;
+#define EB_MDEC_LDS(ARRAY_, NSLOT_)                                                  \
+  __shared__ __attribute__((aligned(16))) uint8_t l0[ARRAY_];                        \
+  __shared__ __attribute__((aligned(16))) uint8_t l1[ARRAY_];                        \
+  __shared__ __attribute__((aligned(16))) uint8_t l2[NSLOT_ > 2 ? (ARRAY_) : 16];    \
+  __shared__ __attribute__((aligned(16))) uint8_t l3[NSLOT_ > 3 ? (ARRAY_) : 16];
 
+// 8-bit pages: four blocks per CU (LDS 4 x 32 KiB), so at most 128 registers
 template <int HD, int G, bool F8>
-__global__ __launch_bounds__(64 * kDecWaves) void k_decode_mfma(const uint16_t *qkv, int nq, int nkv, KV kv,
+__global__ __launch_bounds__(64 * kDecWaves, F8 ? 4 : 1) void k_decode_mfma(const uint16_t *qkv, int nq, int nkv, KV kv,
                                                                 DevMeta md, uint16_t *out, float *part_o,
                                                                 float *part_ml) {
-  EB_MDEC_LDS(HD, kDecWaves, kDecSlots)
-  decode_item_mfma<HD, G, kDecWaves, kDecSlots, F8>(qkv, nq, nkv, kv, md, blockIdx.x, out, part_o, part_ml, l0, l1,
-                                                    l2, l3);
+  constexpr int NS = F8 ? kDecSlotsF8 : kDecSlots;
+  constexpr int SLOT = MdecTraits<HD, F8>::SLOT;
+  EB_MDEC_LDS(kDecWaves * SLOT, NS)
+  decode_item_mfma<HD, G, kDecWaves, NS, F8, SLOT>(qkv, nq, nkv, kv, md, blockIdx.x, out, part_o, part_ml, l0, l1,
+                                                   l2, l3);
 }
 
 // Prefill-only launch: 8 wavefronts per 128-row item, one 16-row block per
@@ -1104,17 +1138,17 @@ __global__ __launch_bounds__(256) void k_mixed_mfma(const uint16_t *qkv, int nq,
                                                     uint16_t *out, float *part_o, float *part_ml) {
   constexpr int BQ = prefill_item_positions<G, true>();
   using Tr = PrefillTraits<HD, G, 4, BQ>;
-  constexpr int MS = 2;  // ring depth of decode items in the mixed launch
-  static_assert(Tr::KS_BYTES <= MdecBlock<HD, 4, MS>::SLOT_ARRAY && Tr::VT_BYTES <= MdecBlock<HD, 4, MS>::SLOT_ARRAY,
-                "LDS");
-  EB_MDEC_LDS(HD, 4, MS)
+  constexpr int MS = 2;                           // ring depth of decode items in the mixed launch
+  constexpr int SLOT = MdecTraits<HD>::SLOT;      // bf16-sized slots: prefill tiles stage bf16
+  static_assert(Tr::KS_BYTES <= 4 * SLOT && Tr::VT_BYTES <= 4 * SLOT, "LDS");
+  EB_MDEC_LDS(4 * SLOT, MS)
   const int b = blockIdx.x;
   if (b < md.n_tiles * nkv)
     prefill_item<HD, G, 4, BQ, F8>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, reinterpret_cast<uint16_t *>(l0),
                                    reinterpret_cast<uint16_t *>(l1));
   else
-    decode_item_mfma<HD, G, 4, MS, F8>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml, l0, l1, l2,
-                                       l3);
+    decode_item_mfma<HD, G, 4, MS, F8, SLOT>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml, l0, l1,
+                                             l2, l3);
 }
 #undef EB_MDEC_LDS
 
