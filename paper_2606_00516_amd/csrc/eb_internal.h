@@ -76,8 +76,9 @@ hipError_t launch_attention(const Shape &s, const uint16_t *qkv, const KV &kv, c
 // GEMM planning shared by the op entry and the step.
 enum GemmEpi { EPI_STORE = 0, EPI_RESIDUAL = 1, EPI_SILU_MUL = 2 };
 struct GemmPlan {
-  int kind;      // 0 = skinny weight-streaming, 1 = LDS-tiled
-  int splits;    // split-K factor (skinny only)
+  int kind;      // 0 = skinny weight-streaming, 1 = LDS-tiled, 2 = 256 x 256 tiles
+  int splits;    // split-K factor (skinny, and big with few tiles)
+  int kt_per;    // big: 64-wide K tiles per split
   size_t ws_bytes;
 };
 GemmPlan plan_gemm(int M, int N, int K, int epi);

@@ -213,10 +213,11 @@ __device__ __forceinline__ void decode_merge_lanes(float (&mrun)[G], float (&lru
 // outputs, then [wave][h][2] max and sum) and write the unit's result: the
 // final row (one split) or a partial for the combine.
 // vscale: the value scale of an 8-bit cache (1 for bf16: exact).
-// The decode request a work unit belongs to.  The whole block looks it up at
-// once: thread t tests requests t, t + blockDim.x, .. against the unit
-// ranges of their records, so the lookup costs one round of independent
-// loads instead of a chain of dependent ones; the match goes through LDS.
+// The decode request a work unit belongs to, found by each wavefront on its
+// own: a 64-way search over the requests' first units (lane i probes the
+// i-th of 64 evenly spaced records, the ballot keeps the last one at or
+// below the unit), so 64 requests take one round of loads and 4096 two,
+// then one read of the request's record.
 struct DecUnit {
   int local;      // unit index within the request
   int split_off;  // first global split index of the request
@@ -225,31 +226,28 @@ struct DecUnit {
 };
 
 __device__ __forceinline__ DecUnit find_decode_unit(const DevMeta &md, int unit) {
-  __shared__ int32_t cell[8];
-  for (int t = threadIdx.x; t < md.n_dec; t += blockDim.x) {
-    const int32_t *r = md.dec_info + (size_t)t * kDecInfoInts;
-    u32x4_t a = ld_u32x4(r);                                                   // unit, split, seq, row
-    u32x4_t b = ld_u32x4(r + 4);                                               // keys, ..
-    u32x4_t n = ld_u32x4(r + kDecInfoInts);                                    // the next record
-    // all three loads issued before the test (not only by the matching thread)
-    asm volatile("" : "+v"(a), "+v"(b), "+v"(n));
-    if ((int)a[0] <= unit && unit < (int)n[0]) {
-      cell[0] = unit - (int)a[0];
-      cell[1] = (int)a[1];
-      cell[2] = (int)(n[1] - a[1]);
-      cell[3] = (int)a[2];
-      cell[4] = (int)a[3];
-      cell[5] = (int)b[0];
-    }
+  const int lane = threadIdx.x & 63;
+  int lo = 0, n = md.n_dec;  // the request lies in [lo, lo + n)
+  while (n > 1) {
+    const int step = (n + 63) >> 6;
+    const int idx = lo + lane * step;
+    const bool ok = idx < lo + n && md.dec_info[(size_t)idx * kDecInfoInts] <= unit;
+    // records are in unit order, so the probes at or below the unit are a
+    // prefix of the lanes (lane 0's always is)
+    const int last = __builtin_popcountll(__builtin_amdgcn_ballot_w64(ok)) - 1;
+    const int nlo = lo + last * step;
+    n = min(step, lo + n - nlo);
+    lo = nlo;
   }
-  __syncthreads();
+  lo = __builtin_amdgcn_readfirstlane(lo);
+  const int32_t *r = md.dec_info + (size_t)lo * kDecInfoInts;
   DecUnit u;
-  u.local = __builtin_amdgcn_readfirstlane(cell[0]);
-  u.split_off = __builtin_amdgcn_readfirstlane(cell[1]);
-  u.nsplit = __builtin_amdgcn_readfirstlane(cell[2]);
-  u.seq = __builtin_amdgcn_readfirstlane(cell[3]);
-  u.row = __builtin_amdgcn_readfirstlane(cell[4]);
-  u.nkeys = __builtin_amdgcn_readfirstlane(cell[5]);
+  u.local = unit - r[0];
+  u.split_off = r[1];
+  u.nsplit = r[kDecInfoInts + 1] - r[1];
+  u.seq = r[2];
+  u.row = r[3];
+  u.nkeys = r[4];
   return u;
 }
 

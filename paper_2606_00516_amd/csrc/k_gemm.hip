@@ -351,6 +351,9 @@ __global__ __launch_bounds__(256) void k_gemm_tiled(const uint16_t *__restrict__
 // epilogue stores 8 bytes at a time.  LDS rows are 128 bytes (64 bf16 of
 // K); the 16-byte chunk c of row r sits at chunk c ^ ((r >> 1) & 7), which
 // makes the MFMA operand reads of 16 consecutive rows conflict free.
+// With fewer tiles than CUs (decode-sized M of 256 against a few thousand
+// columns) blocks split K (gridDim.y splits of kt_per K tiles) and write
+// fp32 partials in logical column space for the split-K epilogue kernel.
 // Requires K % 64 == 0, N % 8 == 0 and both operands under 2 GiB (32-bit
 // offsets).
 // ===========================================================================
@@ -362,8 +365,9 @@ __device__ __forceinline__ int bg_swz(int row, int chunk) { return chunk ^ ((row
 
 __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restrict__ A,
                                                          const uint16_t *__restrict__ W, uint16_t *__restrict__ out,
-                                                         const uint16_t *__restrict__ res, int M, int N, int K,
-                                                         int epi, int tiles_m, int tiles_n, int per_xcd) {
+                                                         const uint16_t *__restrict__ res, float *__restrict__ part,
+                                                         int M, int N, int K, int epi, int tiles_m, int tiles_n,
+                                                         int per_xcd, int kt_per) {
   extern __shared__ __attribute__((aligned(16))) uint8_t bg_lds[];  // [2][A tile | W tile]
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -383,7 +387,8 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
   const int tn = first_n + inb % gsz;
   const int tm = inb / gsz;
   const int m0 = tm * BG_BM, n0 = tn * BG_BN;
-  const int nk = K / BG_BK;
+  const int split = blockIdx.y;
+  const int kt0 = split * kt_per, kt1 = min(K / BG_BK, kt0 + kt_per);
 
   const buf_rsrc_t ra = make_rsrc(A, (int)min((size_t)M * K * 2, (size_t)0x7FFFFFFF));
   const buf_rsrc_t rw = make_rsrc(W, (int)min((size_t)N * K * 2, (size_t)0x7FFFFFFF));
@@ -420,11 +425,11 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
     for (int j = 0; j < 8; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int lr = lane & 15, lg = lane >> 4;
-  dma(0, 0);
+  dma(kt0, 0);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) dma(kt + 1, buf ^ 1);
+  for (int kt = kt0; kt < kt1; ++kt) {
+    const int buf = (kt - kt0) & 1;
+    if (kt + 1 < kt1) dma(kt + 1, buf ^ 1);
     const uint8_t *sa = bg_lds + buf * 2 * BG_TILE_BYTES;
     const uint8_t *sw = sa + BG_TILE_BYTES;
 #pragma unroll
@@ -451,6 +456,19 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
   // epilogue: lane holds out[m][n .. n+3] with m = m0 + wm*128 + 16 im + lr,
   // n = n0 + wn*64 + 16 jn + 4 lg (N and F are multiples of 4, so a group of
   // 4 columns is either wholly inside or wholly outside)
+  if (part) {  // split-K partial, logical column space
+    const int ncols = logical_cols(N, epi);
+#pragma unroll
+    for (int jn = 0; jn < 4; ++jn) {
+      const int n = n0 + wn * 64 + jn * 16 + lg * 4;
+#pragma unroll
+      for (int im = 0; im < 8; ++im) {
+        const int m = m0 + wm * 128 + im * 16 + lr;
+        if (m < M && n < ncols) *reinterpret_cast<f32x4_t *>(part + ((size_t)split * M + m) * ncols + n) = acc[jn][im];
+      }
+    }
+    return;
+  }
   if (epi == EPI_SILU_MUL) {
     // the wave's 64 columns are one [32 gate | 32 up] group: blocks jn and
     // jn + 2 pair up
@@ -500,6 +518,15 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
 // blocks of a column tile run side by side and read W once from HBM).
 constexpr int kSkinnyMaxRows = 256;
 
+static hipError_t launch_splitk_epilogue(const float *part, int splits, uint16_t *out, const uint16_t *res, int M,
+                                         int N, int epi, hipStream_t st) {
+  const int outc = epi == EPI_SILU_MUL ? N / 2 : N;
+  const long total = (long)M * outc;
+  const int blocks = (int)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
+  hipLaunchKernelGGL(k_gemm_splitk_epilogue, dim3(blocks), dim3(256), 0, st, part, splits, out, res, M, N, epi);
+  return hipGetLastError();
+}
+
 static int skinny_splits(int M, int N, int K) {
   const int ncol_tiles = (N + SK_BN - 1) / SK_BN;
   const int mt = (M + SK_BM - 1) / SK_BM;
@@ -519,8 +546,21 @@ GemmPlan plan_gemm(int M, int N, int K, int epi) {
   const bool fits = (size_t)N * K * 2 < ((size_t)1 << 31) && (size_t)BG_BM * K * 2 < ((size_t)1 << 31);
   // 256 x 256 tiles once the grid covers at least half the CUs
   const long big_tiles = (long)((M + BG_BM - 1) / BG_BM) * ((ncols + BG_BN - 1) / BG_BN);
-  if (K % BG_BK == 0 && N % 8 == 0 && fits && M >= 256 && big_tiles >= 128) {
+  if (K % BG_BK == 0 && N % 8 == 0 && fits && M >= 256) {
+    // one block per CU: split K while the tiles cover under half the CUs,
+    // keeping at least 8 K tiles per split
     p.kind = 2;
+    const int nk = K / BG_BK;
+    int splits = 1;
+    if (big_tiles < 128 && (size_t)M * K * 2 < ((size_t)1 << 31)) {
+      const long by_cus = 256 / big_tiles, by_k = nk / 8;
+      splits = (int)(by_cus < by_k ? by_cus : by_k);
+    }
+    if (splits < 1) splits = 1;
+    p.kt_per = (nk + splits - 1) / splits;
+    p.splits = (nk + p.kt_per - 1) / p.kt_per;
+    p.ws_bytes = p.splits > 1 ? (size_t)p.splits * M * ncols * sizeof(float) : 0;
+    return p;
   } else if (M <= kSkinnyMaxRows) {
     p.kind = 0;
     p.splits = skinny_splits(M, ncols, K);
@@ -551,13 +591,19 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, 
                        per_xcd);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
-    const int outc = epi == EPI_SILU_MUL ? N / 2 : N;
-    const long total = (long)M * outc;
-    const int blocks = (int)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
-    hipLaunchKernelGGL(k_gemm_splitk_epilogue, dim3(blocks), dim3(256), 0, st, part, splits, out, res, M, N, epi);
-    return hipGetLastError();
+    return launch_splitk_epilogue(part, splits, out, res, M, N, epi, st);
   }
   if (p.kind == 2) {
+    if (p.splits > 1) {  // one launch (the plan only splits a few tiles), then the partial sums
+      const int tm = (M + BG_BM - 1) / BG_BM, tn = (ncols + BG_BN - 1) / BG_BN;
+      const int per_xcd = (tm * tn + 7) / 8;
+      float *part = reinterpret_cast<float *>(ws);
+      hipLaunchKernelGGL(k_gemm_big, dim3(8 * per_xcd, p.splits), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A, W, out,
+                         res, part, M, N, K, epi, tm, tn, per_xcd, p.kt_per);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      return launch_splitk_epilogue(part, p.splits, out, res, M, N, epi, st);
+    }
     // rows per launch: A's slice must stay inside a 32-bit buffer range
     const size_t rows_fit = ((((size_t)1 << 31) - 1) / ((size_t)K * 2)) / BG_BM * BG_BM;
     const int chunk = (int)(rows_fit < (size_t)M ? rows_fit : (size_t)M);
@@ -567,8 +613,8 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, 
       const int tm = (mc + BG_BM - 1) / BG_BM, tn = (ncols + BG_BN - 1) / BG_BN;
       const int per_xcd = (tm * tn + 7) / 8;
       hipLaunchKernelGGL(k_gemm_big, dim3(8 * per_xcd), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A + (size_t)m0 * K, W,
-                         out + (size_t)m0 * out_cols, res ? res + (size_t)m0 * N : nullptr, mc, N, K, epi, tm, tn,
-                         per_xcd);
+                         out + (size_t)m0 * out_cols, res ? res + (size_t)m0 * N : nullptr, nullptr, mc, N, K, epi,
+                         tm, tn, per_xcd, K / BG_BK);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
     }

@@ -29,7 +29,10 @@ def _bf(shape, seed, scale=1.0):
                                    # 256-row weight streaming (70B-shaped decode batch), ragged rows
                                    (256, 10240, 8192), (200, 4104, 1024),
                                    # 256 x 256 LDS-streamed tiles: aligned, and ragged in M, N and F
-                                   (1024, 8192, 1024), (1000, 8200, 512), (2048, 6144, 4096)])
+                                   (1024, 8192, 1024), (1000, 8200, 512), (2048, 6144, 4096),
+                                   # 256 x 256 tiles splitting K (few tiles): uneven splits, ragged M, N and F,
+                                   # the 70B-shaped down projection
+                                   (300, 1032, 2048), (256, 8192, 28672)])
 @pytest.mark.parametrize("epi", ["store", "residual", "silu_mul"])
 def test_gemm(M, N, K, epi):
     A = _bf((M, K), 1)
