@@ -14,6 +14,7 @@
 #include "host_plan.h"
 
 static_assert(eb::kDecInfo == eb::kDecInfoInts, "decode record layout");
+static_assert(eb::kCombInfo == eb::kCombInfoInts, "combine record layout");
 
 using namespace eb;
 
@@ -86,9 +87,6 @@ DevMeta meta_at(const HostPlan &p, const int32_t *dev) {
   m.seq_row = dev + p.o_row;
   m.row_seq = dev + p.o_row_seq;
   m.row_pos = dev + p.o_row_pos;
-  m.dec_seq = dev + p.o_dec_seq;
-  m.dec_split_off = dev + p.o_dec_off;
-  m.dec_unit_off = dev + p.o_unit_off;
   m.dec_info = dev + p.o_dec_info;
   m.comb_list = dev + p.o_comb;
   m.tile_seq = dev + p.o_tseq;

@@ -17,6 +17,8 @@ constexpr int kShortDecodeKeys = 64;
 constexpr int kShortDecodeHeads = 4;
 // int32 fields per decode-request record in DevMeta::dec_info
 constexpr int kDecInfoInts = 8;
+// int32 fields per record in DevMeta::comb_list
+constexpr int kCombInfoInts = 4;
 
 // Prefill attention items: query positions per item for a GQA group size,
 // in the prefill-only launch and inside the mixed launch (must agree with
@@ -32,12 +34,9 @@ struct DevMeta {
   const int32_t *seq_row;       // [S+1] first row of each request
   const int32_t *row_seq;       // [T] request of each row
   const int32_t *row_pos;       // [T] absolute position of each row
-  const int32_t *dec_seq;       // [D] request index of each decode request
-  const int32_t *dec_split_off; // [D+1] prefix sum of split counts
-  const int32_t *dec_unit_off;  // [D+1] prefix sum of work units (blocks)
   const int32_t *dec_info;      // [D+1][8] {first unit, first split, request, row, keys, 0, 0, 0}; the
                                 // closing record holds the unit and split totals
-  const int32_t *comb_list;     // [C] decode indices with >= 2 splits
+  const int32_t *comb_list;     // [C][4] decode requests with >= 2 splits: {first split, splits, row, 0}
   const int32_t *tile_seq;      // [NT] prefill tiles, longest first
   const int32_t *tile_qb;       // [NT] query block of each tile
   const int32_t *gather_off;    // [S+1] prefix sum of (c + n)

@@ -152,7 +152,7 @@ eb_status check_tables(const eb_layer_config &cfg, const eb_batch &b, const int3
 size_t plan_capacity(int32_t max_seqs, int32_t max_tokens, int32_t group) {
   const size_t S = (size_t)max_seqs, T = (size_t)max_tokens;
   const size_t tiles = T / (size_t)std::min(prefill_bq_host(group, true), prefill_bq_host(group, false)) + S + 1;
-  return 9 * S + kDecInfo * (S + 1) + 2 * T + 2 * tiles + 64;  // + per-array alignment padding
+  return 4 * S + kDecInfo * (S + 1) + kCombInfo * S + 2 * T + 2 * tiles + 64;  // + per-array alignment padding
 }
 
 void build_plan(const eb_layer_config &cfg, const eb_batch &b, eb_mode mode, HostPlan &p) {
@@ -214,9 +214,6 @@ void build_plan(const eb_layer_config &cfg, const eb_batch &b, eb_mode mode, Hos
   p.o_row = put(row.data(), row.size());
   p.o_row_seq = put(row_seq.data(), row_seq.size());
   p.o_row_pos = put(row_pos.data(), row_pos.size());
-  p.o_dec_seq = put(dec_seq.data(), dec_seq.size());
-  p.o_dec_off = put(dec_off.data(), dec_off.size());
-  p.o_unit_off = put(unit_off.data(), unit_off.size());
   // one record per decode request and a closing one (totals)
   std::vector<int32_t> info((size_t)kDecInfo * (dec_seq.size() + 1), 0);
   for (size_t d = 0; d <= dec_seq.size(); ++d) {
@@ -231,7 +228,14 @@ void build_plan(const eb_layer_config &cfg, const eb_batch &b, eb_mode mode, Hos
     }
   }
   p.o_dec_info = put(info.data(), info.size());
-  p.o_comb = put(comb.data(), comb.size());
+  std::vector<int32_t> comb_rec((size_t)kCombInfo * comb.size(), 0);
+  for (size_t j = 0; j < comb.size(); ++j) {
+    const int d = comb[j];
+    comb_rec[j * kCombInfo + 0] = dec_off[d];
+    comb_rec[j * kCombInfo + 1] = dec_off[d + 1] - dec_off[d];
+    comb_rec[j * kCombInfo + 2] = row[dec_seq[d]];
+  }
+  p.o_comb = put(comb_rec.data(), comb_rec.size());
   std::vector<int32_t> tseq(tiles.size()), tqb(tiles.size());
   for (size_t t = 0; t < tiles.size(); ++t) {
     tseq[t] = tiles[t].seq;

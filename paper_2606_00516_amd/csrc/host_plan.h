@@ -13,6 +13,9 @@ namespace eb {
 // int32 fields of a decode request's record: first work unit, first split,
 // request, first row, keys (c + 1), padding to 32 bytes
 constexpr int kDecInfo = 8;
+// int32 fields of a combine record (decode request with >= 2 splits): first
+// split, splits, row, padding
+constexpr int kCombInfo = 4;
 
 struct HostPlan {
   int32_t S = 0, T = 0;
@@ -20,8 +23,8 @@ struct HostPlan {
   int64_t gather_total = 0;
   std::vector<int32_t> blob;  // every metadata array, concatenated
   // offsets (in int32 elements) of each array inside blob
-  size_t o_ctx = 0, o_len = 0, o_row = 0, o_row_seq = 0, o_row_pos = 0, o_dec_seq = 0, o_dec_off = 0, o_unit_off = 0,
-         o_dec_info = 0, o_comb = 0, o_tseq = 0, o_tqb = 0, o_goff = 0;
+  size_t o_ctx = 0, o_len = 0, o_row = 0, o_row_seq = 0, o_row_pos = 0, o_dec_info = 0, o_comb = 0, o_tseq = 0,
+         o_tqb = 0, o_goff = 0;
 };
 
 // Shape support: head_dim in {64, 128}; G = n_q / n_kv in {1, 2, 4, 8};

@@ -705,37 +705,56 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
 }
 
 // Combine the splits of one decode request for one query head:
-// o = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s with M = max_s m_s, the
-// max and both sums reduced across the wavefront.
+// o = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s with M = max_s m_s.  Lane
+// s % 64 holds split s's weight; the output dims (HD / 64 per lane) sum the
+// partials eight splits at a time, their loads issued together.
 template <int HD, int G>
 __global__ __launch_bounds__(64) void k_decode_combine(DevMeta md, const float *__restrict__ part_o,
                                                        const float *__restrict__ part_ml, uint16_t *__restrict__ out,
                                                        int nq, int nkv) {
-  const int d = md.comb_list[blockIdx.x];
+  constexpr int DPL = HD / 64;  // dims per lane
+  const int32_t *rec = md.comb_list + (size_t)blockIdx.x * kCombInfoInts;
+  const int s0 = rec[0], ns = rec[1], row = rec[2];
   const int qh = blockIdx.y;
   const int kh = qh / G, h = qh - kh * G;
   const int lane = threadIdx.x;
-  const int s0 = md.dec_split_off[d], ns = md.dec_split_off[d + 1] - s0;
-  const int row = md.seq_row[md.dec_seq[d]];
-  auto slot = [&](int s) { return ((size_t)(s0 + s) * nkv + kh) * G + h; };
+  const size_t stride = (size_t)nkv * G;  // slots between consecutive splits
+  const size_t base = ((size_t)s0 * nkv + kh) * G + h;
   float mx = kNegInf;
-  for (int s = lane; s < ns; s += 64) mx = fmaxf(mx, part_ml[slot(s) * 2]);
+  for (int s = lane; s < ns; s += 64) mx = fmaxf(mx, part_ml[(base + s * stride) * 2]);
   mx = wave_max(mx);
   float den = 0.f;
-  for (int s = lane; s < ns; s += 64) {
-    const float ms = part_ml[slot(s) * 2];
-    den += (ms == kNegInf) ? 0.f : fast_exp2(ms - mx) * part_ml[slot(s) * 2 + 1];
+  float acc[DPL];
+#pragma unroll
+  for (int i = 0; i < DPL; ++i) acc[i] = 0.f;
+  for (int c = 0; c < ns; c += 64) {
+    const int s = c + lane;
+    float wgt = 0.f;
+    if (s < ns) {
+      const float ms = part_ml[(base + s * stride) * 2];
+      wgt = (ms == kNegInf) ? 0.f : fast_exp2(ms - mx);
+      den += wgt * part_ml[(base + s * stride) * 2 + 1];
+    }
+    const int n = min(64, ns - c);
+    for (int j = 0; j < n; j += 8) {
+      float o[8][DPL];
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int i = 0; i < DPL; ++i)
+          o[u][i] = j + u < n ? part_o[(base + (size_t)(c + j + u) * stride) * HD + lane * DPL + i] : 0.f;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wgt), j + u));
+#pragma unroll
+        for (int i = 0; i < DPL; ++i) acc[i] += a * o[u][i];
+      }
+    }
   }
   den = wave_sum(den);
-  for (int dim = lane; dim < HD; dim += 64) {
-    float acc = 0.f;
-    for (int s = 0; s < ns; ++s) {
-      const float ms = part_ml[slot(s) * 2];
-      const float a = (ms == kNegInf) ? 0.f : fast_exp2(ms - mx);
-      acc += a * part_o[slot(s) * HD + dim];
-    }
-    out[(size_t)row * nq * HD + qh * HD + dim] = (uint16_t)f32_to_bf16_bits(acc / den);
-  }
+#pragma unroll
+  for (int i = 0; i < DPL; ++i)
+    out[(size_t)row * nq * HD + qh * HD + lane * DPL + i] = (uint16_t)f32_to_bf16_bits(acc[i] / den);
 }
 
 // ===========================================================================

@@ -7,8 +7,8 @@ namespace eb {
 // ---------------------------------------------------------------------------
 // RMSNorm: out = bf16(x / sqrt(mean(x^2) + eps) * gamma).  One wavefront per
 // row, 16-byte accesses.  Rows of up to 64 * 8 * MAXC elements stay in
-// registers: every load of the row is issued before the first use, so the
-// kernel waits for memory once; longer rows take a second pass.
+// registers: every load of the row and of gamma is issued before the first
+// use, so the kernel waits for memory once; longer rows take a second pass.
 // ---------------------------------------------------------------------------
 constexpr int kNormMaxChunks = 16;  // 16-byte chunks per lane held in registers (rows up to 8192)
 
@@ -21,11 +21,16 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t *__restrict__ x,
   uint16_t *orow = out + (size_t)row * d;
   const int nch = d >> 3;
   if (nch <= 64 * kNormMaxChunks) {
-    u32x4_t v[kNormMaxChunks];
+    u32x4_t v[kNormMaxChunks], gv[kNormMaxChunks];
 #pragma unroll
     for (int j = 0; j < kNormMaxChunks; ++j) {
       const int c = lane + 64 * j;
       v[j] = c < nch ? ld_u32x4(xr + c * 8) : u32x4_t{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int j = 0; j < kNormMaxChunks; ++j) {
+      const int c = lane + 64 * j;
+      gv[j] = c < nch ? ld_u32x4(g + c * 8) : u32x4_t{0u, 0u, 0u, 0u};  // shared by all rows: an L2 hit
     }
     float ss = 0.f;
 #pragma unroll
@@ -41,11 +46,10 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t *__restrict__ x,
     for (int j = 0; j < kNormMaxChunks; ++j) {
       const int c = lane + 64 * j;
       if (c < nch) {
-        const u32x4_t gv = ld_u32x4(g + c * 8);  // gamma: shared by all rows, an L2 hit
         u32x4_t o;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          o[i] = pack_bf16x2(bf16_lo(v[j][i]) * inv * bf16_lo(gv[i]), bf16_hi(v[j][i]) * inv * bf16_hi(gv[i]));
+          o[i] = pack_bf16x2(bf16_lo(v[j][i]) * inv * bf16_lo(gv[j][i]), bf16_hi(v[j][i]) * inv * bf16_hi(gv[j][i]));
         st_u32x4(orow + c * 8, o);
       }
     }
