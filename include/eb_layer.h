@@ -185,14 +185,19 @@ eb_status eb_stack_step(eb_handle *h, eb_mode mode, int32_t n_layers, const eb_l
 eb_status eb_validate(const eb_layer_config *cfg, const eb_batch *batch, const int32_t *block_tables_host,
                       int32_t num_pages, int32_t max_pages_per_seq, eb_mode mode);
 
-/* Per-stage timing.  With eb_profile(h, 1) every step records HIP events
- * around each stage on its stream (a few microseconds of overhead per
- * stage); eb_profile_read() waits for the last step recorded on h and
- * writes the duration in ms of up to `cap` stages into ms[] (host), in
- * launch order, returning how many it wrote (0 if no profiled step has run,
- * -1 on a HIP error).  Stage names: eb_profile_stage_name(i) (NULL past the
- * last).  Stages a step does not need read 0. */
-eb_status eb_profile(eb_handle *h, int32_t enable);
+/* Per-stage timing.  eb_profile(h, n, mask) with n >= 1 makes every
+ * following step on h record HIP events around the stages whose bit is set
+ * in mask (bit i: stage i; 0: every stage) on its stream (a marker per stage
+ * boundary, a few microseconds of host time each, no synchronisation), into
+ * a ring of n step slots created by this call; n = 0 switches it off.
+ * eb_profile_read() waits for the recorded steps and writes into ms[] (host)
+ * the duration in ms of up to `cap` stages, in launch order, averaged over
+ * the recorded steps (the last n of them), each a sum over the step's layers
+ * (stages outside the mask read 0); it returns how many it wrote (0 if no
+ * profiled step has run since eb_profile, -1 on a HIP error).  Stage names:
+ * eb_profile_stage_name(i) (NULL past the last).  Stages a step does not need
+ * read 0.  EB_ERR_CONFIG for n < 0 or a mask bit past the last stage. */
+eb_status eb_profile(eb_handle *h, int32_t steps, uint32_t stage_mask);
 int32_t eb_profile_read(eb_handle *h, float *ms, int32_t cap);
 const char *eb_profile_stage_name(int32_t i);
 

@@ -88,7 +88,7 @@ def lib() -> ctypes.CDLL:
         "eb_op_rope_kv_append": (I32, [VP, VP, P(KvCache), P(Batch), VP, SZ, VP]),
         "eb_op_attention": (I32, [VP, VP, P(KvCache), P(Batch), VP, VP, SZ, I32, VP]),
         "eb_op_gather_kv": (I32, [VP, P(KvCache), P(Batch), VP, VP, VP, SZ, VP]),
-        "eb_profile": (I32, [VP, I32]),
+        "eb_profile": (I32, [VP, I32, ctypes.c_uint32]),
         "eb_profile_read": (I32, [VP, P(ctypes.c_float), I32]),
         "eb_profile_stage_name": (ctypes.c_char_p, [I32]),
         "eb_stack_workspace_bytes": (SZ, [VP, P(Batch), I32]),
@@ -331,12 +331,20 @@ def eb_op_gather_kv(h: Handle, k_cache, v_cache, block_tables, context_lens, chu
     return ok, ov
 
 
-def eb_profile(h: Handle, enable: bool = True):
-    _check(lib().eb_profile(h.h, 1 if enable else 0))
+def eb_profile(h: Handle, enable: bool = True, steps: int = 1, stages=None):
+    """Record the stage events of the following steps (a ring of `steps`
+    slots; `stages`: names of the stages to bracket, all if None), or stop
+    recording."""
+    mask = 0
+    if stages is not None:
+        names = [lib().eb_profile_stage_name(i).decode() for i in range(32) if lib().eb_profile_stage_name(i)]
+        for n in stages:
+            mask |= 1 << names.index(n)
+    _check(lib().eb_profile(h.h, int(steps) if enable else 0, mask))
 
 
 def eb_profile_read(h: Handle) -> dict:
-    """Stage name -> ms of the last profiled step on this handle."""
+    """Stage name -> ms, averaged over the recorded steps on this handle."""
     buf = (ctypes.c_float * 32)()
     n = lib().eb_profile_read(h.h, buf, 32)
     if n < 0:

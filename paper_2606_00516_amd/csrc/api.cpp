@@ -118,12 +118,16 @@ struct eb_handle {
   hipEvent_t ev[kRing];
   bool used[kRing];
   int next;
-  // per-stage timing of the last step (eb_profile): events bracket stage s
-  // of layer l at pev[2 (l kStages + s)] and the next one
+  // per-stage timing (eb_profile): step j of a profiled run records into
+  // slot j % prof_slots, where events [2 (l kStages + s)] and the next one
+  // bracket stage s of layer l
   bool prof;
-  bool prof_valid;
-  int prof_layers;
-  std::vector<hipEvent_t> pev;
+  uint32_t prof_mask;  // stages recorded (bit s: stage s)
+  int prof_slots;
+  long prof_count;  // steps recorded since profiling was switched on
+  std::vector<std::vector<hipEvent_t>> pslot;
+  std::vector<int> slot_layers;
+  int max_layers;  // most layers a step on this handle has run
 };
 
 namespace {
@@ -208,14 +212,14 @@ StepBufs bufs_at(char *base, const WsLayout &L) {
                   base + L.gemm};
 }
 
-// Make sure the profiling event pool covers n layers.
-eb_status grow_events(eb_handle *h, int layers) {
+// Make sure a profiling slot's events cover n layers.
+eb_status grow_events(std::vector<hipEvent_t> &pev, int layers) {
   const size_t need = (size_t)2 * kStages * layers;
-  while (h->pev.size() < need) {
+  while (pev.size() < need) {
     hipEvent_t e = nullptr;
     hipError_t r = hipEventCreate(&e);
     if (r != hipSuccess) return hip_fail(r, "hipEventCreate");
-    h->pev.push_back(e);
+    pev.push_back(e);
   }
   return EB_OK;
 }
@@ -223,11 +227,13 @@ eb_status grow_events(eb_handle *h, int layers) {
 // The nine stages of one layer on the stream: x -> y with weights w and
 // cache kvd; the batch metadata m is already in the workspace.
 eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, const DevMeta &m, const StepBufs &B,
-                     const uint16_t *xin, uint16_t *yout, int T, eb_mode mode, int layer, hipStream_t st) {
+                     const uint16_t *xin, uint16_t *yout, int T, eb_mode mode, int layer, hipEvent_t *pev,
+                     hipStream_t st) {
   const Shape &sh = h->shape;
   hipError_t e;
   auto mark = [&](int i) -> hipError_t {
-    return h->prof ? hipEventRecord(h->pev[(size_t)2 * kStages * layer + i], st) : hipSuccess;
+    return pev && ((h->prof_mask >> (i / 2)) & 1u) ? hipEventRecord(pev[(size_t)2 * kStages * layer + i], st)
+                                                   : hipSuccess;
   };
 #define EB_STAGE(idx, call, what)                                       \
   if ((e = mark(2 * (idx))) != hipSuccess) return hip_fail(e, "hipEventRecord"); \
@@ -283,8 +289,8 @@ eb_status run_layers(eb_handle *h, int32_t n_layers, const eb_layer_weights *w, 
   }
   eb_status s = check_common(h, b, mode, min_pages);
   if (s != EB_OK) return s;
-  h->prof_valid = false;
   if (b->num_tokens == 0) return EB_OK;
+  if (n_layers > h->max_layers) h->max_layers = n_layers;
   if (!x || !y) return fail(EB_ERR_NULL, "x or y is NULL");
   if (x == y) return fail(EB_ERR_BATCH, "y must not alias x");
   HostPlan p;
@@ -293,8 +299,9 @@ eb_status run_layers(eb_handle *h, int32_t n_layers, const eb_layer_weights *w, 
   const WsLayout L = layout_for(h->shape, p, true, stack);
   s = check_ws(ws, ws_bytes, L.total);
   if (s != EB_OK) return s;
-  if (h->prof) {
-    s = grow_events(h, n_layers);
+  const int slot = h->prof ? (int)(h->prof_count % h->prof_slots) : -1;
+  if (slot >= 0) {
+    s = grow_events(h->pslot[slot], n_layers);
     if (s != EB_OK) return s;
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -306,12 +313,15 @@ eb_status run_layers(eb_handle *h, int32_t n_layers, const eb_layer_weights *w, 
   const uint16_t *in = static_cast<const uint16_t *>(x);
   for (int l = 0; l < n_layers; ++l) {
     uint16_t *out = ((n_layers - 1 - l) % 2 == 0) ? static_cast<uint16_t *>(y) : B.alt;
-    s = layer_body(h, &w[l], kv_of(&kv[l]), m, B, in, out, p.T, mode, l, st);
+    s = layer_body(h, &w[l], kv_of(&kv[l]), m, B, in, out, p.T, mode, l,
+                   slot >= 0 ? h->pslot[slot].data() : nullptr, st);
     if (s != EB_OK) return s;
     in = out;
   }
-  h->prof_layers = n_layers;
-  h->prof_valid = h->prof;
+  if (slot >= 0) {
+    h->slot_layers[slot] = n_layers;
+    ++h->prof_count;
+  }
   return EB_OK;
 }
 
@@ -356,8 +366,10 @@ eb_status eb_create(const eb_layer_config *cfg, int32_t max_seqs, int32_t max_to
   }
   h->slot_cap = plan_capacity(max_seqs, max_tokens, cfg->n_q_heads / cfg->n_kv_heads);
   h->prof = false;
-  h->prof_valid = false;
-  h->prof_layers = 0;
+  h->prof_slots = 0;
+  h->prof_mask = 0;
+  h->prof_count = 0;
+  h->max_layers = 1;
   for (int k = 0; k < kRing; ++k) {
     h->pinned[k] = nullptr;
     h->ev[k] = nullptr;
@@ -384,7 +396,8 @@ void eb_destroy(eb_handle *h) {
     }
     if (h->pinned[k]) (void)hipHostFree(h->pinned[k]);
   }
-  for (hipEvent_t e : h->pev) (void)hipEventDestroy(e);
+  for (auto &pev : h->pslot)
+    for (hipEvent_t e : pev) (void)hipEventDestroy(e);
   delete h;
 }
 
@@ -443,31 +456,52 @@ eb_status eb_validate(const eb_layer_config *cfg, const eb_batch *batch, const i
   return EB_OK;
 }
 
-eb_status eb_profile(eb_handle *h, int32_t enable) {
+eb_status eb_profile(eb_handle *h, int32_t steps, uint32_t stage_mask) {
   if (!h) return fail(EB_ERR_NULL, "handle is NULL");
-  if (enable) {
-    eb_status s = grow_events(h, 1);
-    if (s != EB_OK) return s;
+  if (steps < 0) return fail(EB_ERR_CONFIG, "steps must be >= 0");
+  const uint32_t all = (1u << kStages) - 1u;
+  if (stage_mask & ~all) return fail(EB_ERR_CONFIG, "stage_mask names an unknown stage");
+  if (steps > 0) {
+    // every slot's events exist before the first profiled step, for as many
+    // layers as the handle's largest step so far (a larger step adds its own)
+    if ((int)h->pslot.size() < steps) h->pslot.resize(steps);
+    for (int k = 0; k < steps; ++k) {
+      eb_status s = grow_events(h->pslot[k], h->max_layers);
+      if (s != EB_OK) return s;
+    }
+    h->slot_layers.assign(steps, 0);
   }
-  h->prof = enable != 0;
-  h->prof_valid = false;
+  h->prof = steps > 0;
+  h->prof_mask = stage_mask ? stage_mask : all;
+  h->prof_slots = steps;
+  h->prof_count = 0;
   return EB_OK;
 }
 
 int32_t eb_profile_read(eb_handle *h, float *ms, int32_t cap) {
-  if (!h || !h->prof_valid) return 0;
-  const size_t last = (size_t)2 * kStages * h->prof_layers - 1;
-  if (hipEventSynchronize(h->pev[last]) != hipSuccess) return -1;
+  if (!h || !h->prof || h->prof_count == 0) return 0;
+  const int nrec = h->prof_count < h->prof_slots ? (int)h->prof_count : h->prof_slots;
+  int last_stage = kStages - 1;
+  while (!((h->prof_mask >> last_stage) & 1u)) --last_stage;
+  for (int k = 0; k < nrec; ++k) {
+    const size_t last = (size_t)2 * (kStages * (h->slot_layers[k] - 1) + last_stage) + 1;
+    if (hipEventSynchronize(h->pslot[k][last]) != hipSuccess) return -1;
+  }
   const int n = cap < kStages ? cap : kStages;
   for (int i = 0; i < n; ++i) {
-    float sum = 0.f;
-    for (int l = 0; l < h->prof_layers; ++l) {
-      const size_t b = (size_t)2 * (l * kStages + i);
-      float t = 0.f;
-      if (hipEventElapsedTime(&t, h->pev[b], h->pev[b + 1]) != hipSuccess) return -1;
-      sum += t;
+    double sum = 0.0;
+    if (!((h->prof_mask >> i) & 1u)) {
+      ms[i] = 0.f;
+      continue;
     }
-    ms[i] = sum;
+    for (int k = 0; k < nrec; ++k)
+      for (int l = 0; l < h->slot_layers[k]; ++l) {
+        const size_t b = (size_t)2 * (l * kStages + i);
+        float t = 0.f;
+        if (hipEventElapsedTime(&t, h->pslot[k][b], h->pslot[k][b + 1]) != hipSuccess) return -1;
+        sum += t;
+      }
+    ms[i] = (float)(sum / nrec);
   }
   return n;
 }

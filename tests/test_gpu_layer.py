@@ -105,6 +105,33 @@ def test_empty_batch_is_a_noop():
         assert y.shape == (0, shape.hidden)
 
 
+def test_profile_ring_over_steps():
+    # stage events of several steps in a ring of slots: a read averages the
+    # recorded steps (here after the ring wrapped), off means nothing to read
+    case = tiny_case("mixed")
+    d = DevCase(case)
+    b = case.batch
+    h = B.Handle(case.shape, b.num_seqs, b.num_tokens)
+    assert B.eb_profile_read(h) == {}
+    B.eb_profile(h, True, steps=3)
+    assert B.eb_profile_read(h) == {}
+    for _ in range(5):
+        STEP["mixed"](h, d.w, d.k, d.v, d.bt, b.context_lens, b.chunk_lens, d.x)
+    st = B.eb_profile_read(h)
+    assert len(st) == 9 and st["attention"] > 0 and st["qkv_gemm"] > 0, st
+    assert all(v >= 0 for v in st.values()), st
+    # one stage only: the others read 0
+    B.eb_profile(h, True, steps=2, stages=["attention"])
+    for _ in range(2):
+        STEP["mixed"](h, d.w, d.k, d.v, d.bt, b.context_lens, b.chunk_lens, d.x)
+    one = B.eb_profile_read(h)
+    assert one["attention"] > 0 and all(v == 0 for k, v in one.items() if k != "attention"), one
+    B.eb_profile(h, False)
+    assert B.eb_profile_read(h) == {}
+    assert B.lib().eb_profile(h.h, -1, 0) == -2  # EB_ERR_CONFIG
+    assert B.lib().eb_profile(h.h, 1, 1 << 9) == -2
+
+
 def test_step_errors_enqueue_nothing():
     shape = gen.TINY
     case = tiny_case("mixed")
