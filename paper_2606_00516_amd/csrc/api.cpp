@@ -88,6 +88,8 @@ DevMeta meta_at(const HostPlan &p, const int32_t *dev) {
   m.row_seq = dev + p.o_row_seq;
   m.row_pos = dev + p.o_row_pos;
   m.dec_info = dev + p.o_dec_info;
+  m.dec_part = dev + p.o_part;
+  m.dec_short = dev + p.o_short;
   m.comb_list = dev + p.o_comb;
   m.tile_seq = dev + p.o_tseq;
   m.tile_qb = dev + p.o_tqb;
@@ -99,6 +101,9 @@ DevMeta meta_at(const HostPlan &p, const int32_t *dev) {
   m.total_units = p.total_units;
   m.n_comb = p.n_comb;
   m.n_tiles = p.n_tiles;
+  m.n_full_units = p.n_full_units;
+  m.n_part = p.n_part;
+  m.n_short = p.n_short;
   return m;
 }
 

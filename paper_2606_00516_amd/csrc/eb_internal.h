@@ -34,13 +34,16 @@ struct DevMeta {
   const int32_t *seq_row;       // [S+1] first row of each request
   const int32_t *row_seq;       // [T] request of each row
   const int32_t *row_pos;       // [T] absolute position of each row
-  const int32_t *dec_info;      // [D+1][8] {first unit, first split, request, row, keys, 0, 0, 0}; the
-                                // closing record holds the unit and split totals
+  const int32_t *dec_info;      // [D+1][8] {first full-split unit, first split, request, row, keys, splits,
+                                // 0, 0}; the closing record holds the full-split unit count
+  const int32_t *dec_part;      // [n_part] requests whose last split is shorter, longest first
+  const int32_t *dec_short;     // [n_short] requests of at most kShortDecodeKeys keys
   const int32_t *comb_list;     // [C][4] decode requests with >= 2 splits: {first split, splits, row, 0}
   const int32_t *tile_seq;      // [NT] prefill tiles, longest first
   const int32_t *tile_qb;       // [NT] query block of each tile
   const int32_t *gather_off;    // [S+1] prefix sum of (c + n)
   int32_t S, T, n_dec, total_splits, total_units, n_comb, n_tiles;
+  int32_t n_full_units, n_part, n_short;  // decode units: full splits, then shorter last splits, then short requests
 };
 
 struct KV {

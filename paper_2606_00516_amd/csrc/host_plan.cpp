@@ -152,7 +152,7 @@ eb_status check_tables(const eb_layer_config &cfg, const eb_batch &b, const int3
 size_t plan_capacity(int32_t max_seqs, int32_t max_tokens, int32_t group) {
   const size_t S = (size_t)max_seqs, T = (size_t)max_tokens;
   const size_t tiles = T / (size_t)std::min(prefill_bq_host(group, true), prefill_bq_host(group, false)) + S + 1;
-  return 4 * S + kDecInfo * (S + 1) + kCombInfo * S + 2 * T + 2 * tiles + 64;  // + per-array alignment padding
+  return 6 * S + kDecInfo * (S + 1) + kCombInfo * S + 2 * T + 2 * tiles + 64;  // + per-array alignment padding
 }
 
 void build_plan(const eb_layer_config &cfg, const eb_batch &b, eb_mode mode, HostPlan &p) {
@@ -170,7 +170,11 @@ void build_plan(const eb_layer_config &cfg, const eb_batch &b, eb_mode mode, Hos
     goff[i + 1] = goff[i] + b.context_lens_host[i] + b.chunk_lens_host[i];
   }
   p.gather_total = goff[S];
-  std::vector<int32_t> row_seq(T), row_pos(T), dec_seq, dec_off(1, 0), unit_off(1, 0), comb;
+  std::vector<int32_t> row_seq(T), row_pos(T), dec_seq, dec_off(1, 0), full_off(1, 0), comb, shorts;
+  struct Part {
+    int32_t d, pages;
+  };
+  std::vector<Part> parts;
   const int nkv = cfg.n_kv_heads;
   struct Tile {
     int32_t seq, qb, cost;
@@ -184,20 +188,34 @@ void build_plan(const eb_layer_config &cfg, const eb_batch &b, eb_mode mode, Hos
     }
     if (n == 1) {
       const int32_t ns = decode_splits(c);
-      if (ns >= 2) comb.push_back((int32_t)dec_seq.size());
+      const int32_t d = (int32_t)dec_seq.size();
+      if (ns >= 2) comb.push_back(d);
       dec_seq.push_back(i);
       dec_off.push_back(dec_off.back() + ns);
-      const int units = (c + 1 <= kShortKeys) ? (nkv + kShortHeads - 1) / kShortHeads : ns * nkv;
-      unit_off.push_back(unit_off.back() + units);
+      const int32_t keys = c + 1, per = kPagesPerSplit * kPage;
+      int32_t nfull = 0;
+      if (keys <= kShortKeys) {
+        shorts.push_back(d);
+      } else {
+        nfull = keys / per;  // splits of exactly 32 pages
+        if (keys % per) parts.push_back({d, (keys % per + kPage - 1) / kPage});
+      }
+      full_off.push_back(full_off.back() + nfull * nkv);
     } else {
       const int nqb = (n + bq - 1) / bq;
       for (int qb = 0; qb < nqb; ++qb) tiles.push_back({i, qb, c + std::min(n, (qb + 1) * bq)});
     }
   }
   std::stable_sort(tiles.begin(), tiles.end(), [](const Tile &a, const Tile &b) { return a.cost > b.cost; });
+  // longest last splits first (ties in request order): the launch ends on
+  // the shortest units, which keeps its tail short
+  std::stable_sort(parts.begin(), parts.end(), [](const Part &a, const Part &b) { return a.pages > b.pages; });
   p.n_dec = (int32_t)dec_seq.size();
   p.total_splits = dec_off.back();
-  p.total_units = unit_off.back();
+  p.n_full_units = full_off.back();
+  p.n_part = (int32_t)parts.size();
+  p.n_short = (int32_t)shorts.size();
+  p.total_units = p.n_full_units + p.n_part * nkv + p.n_short * ((nkv + kShortHeads - 1) / kShortHeads);
   p.n_comb = (int32_t)comb.size();
   p.n_tiles = (int32_t)tiles.size();
 
@@ -218,16 +236,21 @@ void build_plan(const eb_layer_config &cfg, const eb_batch &b, eb_mode mode, Hos
   std::vector<int32_t> info((size_t)kDecInfo * (dec_seq.size() + 1), 0);
   for (size_t d = 0; d <= dec_seq.size(); ++d) {
     int32_t *r = &info[d * kDecInfo];
-    r[0] = unit_off[d];
+    r[0] = full_off[d];
     r[1] = dec_off[d];
     if (d < dec_seq.size()) {
       const int i = dec_seq[d];
       r[2] = i;
       r[3] = row[i];
       r[4] = b.context_lens_host[i] + 1;
+      r[5] = dec_off[d + 1] - dec_off[d];
     }
   }
   p.o_dec_info = put(info.data(), info.size());
+  std::vector<int32_t> part_d(parts.size());
+  for (size_t j = 0; j < parts.size(); ++j) part_d[j] = parts[j].d;
+  p.o_part = put(part_d.data(), part_d.size());
+  p.o_short = put(shorts.data(), shorts.size());
   std::vector<int32_t> comb_rec((size_t)kCombInfo * comb.size(), 0);
   for (size_t j = 0; j < comb.size(); ++j) {
     const int d = comb[j];

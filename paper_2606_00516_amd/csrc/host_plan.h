@@ -10,8 +10,9 @@
 
 namespace eb {
 
-// int32 fields of a decode request's record: first work unit, first split,
-// request, first row, keys (c + 1), padding to 32 bytes
+// int32 fields of a decode request's record: first work unit among the
+// full splits, first split, request, first row, keys (c + 1), splits,
+// padding to 32 bytes
 constexpr int kDecInfo = 8;
 // int32 fields of a combine record (decode request with >= 2 splits): first
 // split, splits, row, padding
@@ -20,11 +21,16 @@ constexpr int kCombInfo = 4;
 struct HostPlan {
   int32_t S = 0, T = 0;
   int32_t n_dec = 0, total_splits = 0, total_units = 0, n_comb = 0, n_tiles = 0;
+  // decode work units in launch order: the full 32-page splits (request by
+  // request, n_full_units of them), then the requests' shorter last splits,
+  // longest first (n_part requests x n_kv units), then the requests of at
+  // most kShortKeys keys (n_short of them)
+  int32_t n_full_units = 0, n_part = 0, n_short = 0;
   int64_t gather_total = 0;
   std::vector<int32_t> blob;  // every metadata array, concatenated
   // offsets (in int32 elements) of each array inside blob
   size_t o_ctx = 0, o_len = 0, o_row = 0, o_row_seq = 0, o_row_pos = 0, o_dec_info = 0, o_comb = 0, o_tseq = 0,
-         o_tqb = 0, o_goff = 0;
+         o_tqb = 0, o_goff = 0, o_part = 0, o_short = 0;
 };
 
 // Shape support: head_dim in {64, 128}; G = n_q / n_kv in {1, 2, 4, 8};

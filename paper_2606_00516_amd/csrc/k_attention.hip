@@ -213,42 +213,61 @@ __device__ __forceinline__ void decode_merge_lanes(float (&mrun)[G], float (&lru
 // outputs, then [wave][h][2] max and sum) and write the unit's result: the
 // final row (one split) or a partial for the combine.
 // vscale: the value scale of an 8-bit cache (1 for bf16: exact).
-// The decode request a work unit belongs to, found by each wavefront on its
-// own: a 64-way search over the requests' first units (lane i probes the
-// i-th of 64 evenly spaced records, the ballot keeps the last one at or
-// below the unit), so 64 requests take one round of loads and 4096 two,
-// then one read of the request's record.
+// The decode request and work of a unit.  Units come in three runs (the
+// plan's launch order): the full 32-page splits, request by request (each
+// wavefront finds the request by a 64-way search over the records' first
+// full-split units: lane i probes the i-th of 64 evenly spaced records, the
+// ballot keeps the last one at or below the unit; one round of loads for 64
+// requests, two for 4096); then the shorter last splits of the requests
+// listed longest first, n_kv units each; then the requests of at most
+// kShortDecodeKeys keys.  Every unit computes the same result wherever it
+// sits in the order.
 struct DecUnit {
-  int local;      // unit index within the request
+  int local;      // split * n_kv + kv head, or the head group of a short request
   int split_off;  // first global split index of the request
   int nsplit;     // splits of the request
   int seq, row, nkeys;
 };
 
-__device__ __forceinline__ DecUnit find_decode_unit(const DevMeta &md, int unit) {
-  const int lane = threadIdx.x & 63;
-  int lo = 0, n = md.n_dec;  // the request lies in [lo, lo + n)
-  while (n > 1) {
-    const int step = (n + 63) >> 6;
-    const int idx = lo + lane * step;
-    const bool ok = idx < lo + n && md.dec_info[(size_t)idx * kDecInfoInts] <= unit;
-    // records are in unit order, so the probes at or below the unit are a
-    // prefix of the lanes (lane 0's always is)
-    const int last = __builtin_popcountll(__builtin_amdgcn_ballot_w64(ok)) - 1;
-    const int nlo = lo + last * step;
-    n = min(step, lo + n - nlo);
-    lo = nlo;
+__device__ __forceinline__ DecUnit find_decode_unit(const DevMeta &md, int unit, int nkv) {
+  int d, local;
+  if (unit < md.n_full_units) {
+    const int lane = threadIdx.x & 63;
+    int lo = 0, n = md.n_dec;  // the request lies in [lo, lo + n)
+    while (n > 1) {
+      const int step = (n + 63) >> 6;
+      const int idx = lo + lane * step;
+      // first full-split units do not decrease with the request index, so
+      // the probes at or below the unit are a prefix of the lanes
+      const bool ok = idx < lo + n && md.dec_info[(size_t)idx * kDecInfoInts] <= unit;
+      const int last = __builtin_popcountll(__builtin_amdgcn_ballot_w64(ok)) - 1;
+      const int nlo = lo + last * step;
+      n = min(step, lo + n - nlo);
+      lo = nlo;
+    }
+    d = __builtin_amdgcn_readfirstlane(lo);
+    local = unit - md.dec_info[(size_t)d * kDecInfoInts];
+  } else if (unit < md.n_full_units + md.n_part * nkv) {
+    const int u = unit - md.n_full_units;
+    const int i = u / nkv;
+    d = md.dec_part[i];
+    local = (md.dec_info[(size_t)d * kDecInfoInts + 5] - 1) * nkv + (u - i * nkv);  // the last split
+  } else {
+    const int nsu = (nkv + kShortDecodeHeads - 1) / kShortDecodeHeads;
+    const int u = unit - md.n_full_units - md.n_part * nkv;
+    const int i = u / nsu;
+    d = md.dec_short[i];
+    local = u - i * nsu;
   }
-  lo = __builtin_amdgcn_readfirstlane(lo);
-  const int32_t *r = md.dec_info + (size_t)lo * kDecInfoInts;
-  DecUnit u;
-  u.local = unit - r[0];
-  u.split_off = r[1];
-  u.nsplit = r[kDecInfoInts + 1] - r[1];
-  u.seq = r[2];
-  u.row = r[3];
-  u.nkeys = r[4];
-  return u;
+  const int32_t *r = md.dec_info + (size_t)d * kDecInfoInts;
+  DecUnit du;
+  du.local = local;
+  du.split_off = r[1];
+  du.seq = r[2];
+  du.row = r[3];
+  du.nkeys = r[4];
+  du.nsplit = r[5];
+  return du;
 }
 
 template <int HD, int G, int NW>
@@ -563,7 +582,7 @@ __device__ __forceinline__ void decode_item_mfma(const uint16_t *__restrict__ qk
   const int c = lane & 15, g = lane >> 4;
   uint8_t *w0 = l0 + wave * SLOT, *w1 = l1 + wave * SLOT, *w2 = l2 + wave * SLOT, *w3 = l3 + wave * SLOT;
 
-  const DecUnit du = find_decode_unit(md, unit);
+  const DecUnit du = find_decode_unit(md, unit, nkv);
   const int local = du.local, nkeys = du.nkeys, row = du.row;
   const int32_t *bt = kv.bt + (size_t)du.seq * kv.max_pages;
   u32x4_t qb[HD / 32], sel[2];
@@ -650,7 +669,7 @@ __device__ __forceinline__ void decode_item(const uint16_t *__restrict__ qkv, in
   const float qscale = F8 ? kLog2e / sqrtf((float)HD) * kv.ks : kLog2e / sqrtf((float)HD);
   const float vscale = F8 ? kv.vs : 1.f;
 
-  const DecUnit du = find_decode_unit(md, unit);
+  const DecUnit du = find_decode_unit(md, unit, nkv);
   const int local = du.local, nkeys = du.nkeys, row = du.row;
   const int32_t *bt = kv.bt + (size_t)du.seq * kv.max_pages;
   const int dq = (lane % LPT) * 8;
