@@ -825,6 +825,7 @@ struct PrefillTraits {
   static constexpr int KPT = (KCH + NW * 64 - 1) / (NW * 64);  // per thread
   static constexpr int VPT = (VCH + NW * 64 - 1) / (NW * 64);
   static_assert(RB >= 1 && RB * NW * 16 == G * BQ, "row blocks");
+  static_assert(BQ % 16 == 0, "a 16-row block holds 16 positions of one head");
 };
 
 template <int HD, int G, int NW, int BQ_, bool F8>
