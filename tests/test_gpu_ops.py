@@ -181,6 +181,11 @@ ATT_BATCHES = {
                                                    np.array([1, 77, 1, 130, 1], np.int32))),
     "70b-shape-small": (gen.L70B, lambda: gen.Batch(np.array([600, 12, 1030], np.int32),
                                                      np.array([1, 40, 1], np.int32))),
+    # decode work-order edges: last splits exactly full (512 and 1024 keys),
+    # the short / split boundary (64 and 65 keys), last splits of 1 and 31
+    # pages, and requests listed out of size order
+    "8b-decode-edges": (gen.L8B, lambda: gen.Batch(np.array([511, 63, 64, 1023, 512, 1007, 3, 2000], np.int32),
+                                                    np.ones(8, np.int32))),
 }
 
 
@@ -204,7 +209,7 @@ def test_attention_vs_oracle(name, mode):
     assert max(errs) < TOL, errs
 
 
-@pytest.mark.parametrize("name", ["tiny-decode", "8b-mixed-small"])
+@pytest.mark.parametrize("name", ["tiny-decode", "8b-mixed-small", "8b-decode-edges"])
 def test_attention_decode_plan(name):
     shape, mk = ATT_BATCHES[name]
     batch = mk()
