@@ -24,7 +24,7 @@ constexpr int kCombInfoInts = 4;
 // in the prefill-only launch and inside the mixed launch (must agree with
 // PrefillTraits in the attention kernels).
 inline int prefill_bq(int group, bool mixed_launch) {
-  return mixed_launch ? (group >= 4 ? 16 : 64 / group) : 128 / group;
+  return mixed_launch ? 64 / group : 128 / group;
 }
 
 // Per-step metadata in device memory (all int32), produced by the planner.

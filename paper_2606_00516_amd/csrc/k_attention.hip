@@ -792,11 +792,13 @@ __global__ __launch_bounds__(64) void k_decode_combine(DevMeta md, const float *
 // which item it sits in, so both launches give the same bits.
 // ===========================================================================
 // Query positions per prefill item: 128 rows (G heads x 128/G positions) in
-// the prefill-only launch, 64 rows (at most 16 positions) inside the mixed
-// launch; the planner's prefill_bq() gives the same numbers.
+// the prefill-only launch, 64 rows (one 16-row block per wave of the 4-wave
+// block: 8 positions of two heads per block for G = 8) inside the mixed
+// launch, which keeps the mixed kernel to two blocks per CU; the planner's
+// prefill_bq() gives the same numbers.
 template <int G, bool MIXED>
 constexpr int prefill_item_positions() {
-  return MIXED ? (G >= 4 ? 16 : 64 / G) : 128 / G;
+  return MIXED ? 64 / G : 128 / G;
 }
 
 // V^T in LDS: row = head dimension, 68 bf16 per row; the 8-byte group of
@@ -825,7 +827,9 @@ struct PrefillTraits {
   static constexpr int KPT = (KCH + NW * 64 - 1) / (NW * 64);  // per thread
   static constexpr int VPT = (VCH + NW * 64 - 1) / (NW * 64);
   static_assert(RB >= 1 && RB * NW * 16 == G * BQ, "row blocks");
-  static_assert(BQ % 16 == 0, "a 16-row block holds 16 positions of one head");
+  // a 16-row block holds 16 positions of one head, or 16 / BQ heads of BQ
+  // positions each
+  static_assert(BQ % 16 == 0 || (16 % BQ == 0 && G % (16 / BQ) == 0), "row block shape");
 };
 
 template <int HD, int G, int NW, int BQ_, bool F8>
@@ -857,18 +861,24 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
   const int lq = lane & 15;   // query column of this lane inside a 16-row block
   const int lg = lane >> 4;   // lane group 0..3
 
-  // row blocks of this wave: rb = wave + NW i -> head rb % G, positions
-  // (rb / G) * 16 ..
+  // row blocks of this wave: rb = wave + NW i, each HPB heads x RPH
+  // positions (RPH = min(16, BQ)); lane lq serves head hb HPB + lq / RPH at
+  // position q_lo + sub RPH + lq % RPH, where hb = rb % (G / HPB), sub = rb /
+  // (G / HPB).  A row's arithmetic does not depend on the block shape: the
+  // products and reductions are per query column.
+  constexpr int RPH = BQ < 16 ? BQ : 16, HPB = 16 / RPH, HG = G / HPB;
+  int hrow[RB];
   u32x4_t qreg[RB][NKS];
   int qrel[RB];
   bool qok[RB];
 #pragma unroll
   for (int i = 0; i < RB; ++i) {
     const int rb = wave + NW * i;
-    const int h = rb % G, sub = rb / G;
-    qrel[i] = q_lo + sub * 16 + lq;
+    const int hb = rb % HG, sub = rb / HG;
+    hrow[i] = hb * HPB + lq / RPH;
+    qrel[i] = q_lo + sub * RPH + lq % RPH;
     qok[i] = qrel[i] < q_hi;
-    const uint16_t *src = qkv + (size_t)(row0 + qrel[i]) * cols + (kh * G + h) * HD + lg * 8;
+    const uint16_t *src = qkv + (size_t)(row0 + qrel[i]) * cols + (kh * G + hrow[i]) * HD + lg * 8;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks) qreg[i][ks] = qok[i] ? ld_u32x4(src + ks * 32) : u32x4_t{0, 0, 0, 0};
   }
@@ -1087,7 +1097,7 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
     l += shfl_xor_f32(l, 16);
     l += shfl_xor_f32(l, 32);
     if (qok[i]) {
-      const int h = (wave + NW * i) % G;
+      const int h = hrow[i];
       const float inv = F8 ? kv.vs / l : 1.0f / l;
       uint16_t *dst = out + (size_t)(row0 + qrel[i]) * nq * HD + (kh * G + h) * HD + lg * 4;
 #pragma unroll

@@ -225,9 +225,11 @@ def test_attention_decode_plan(name):
     assert max(errs) < TOL, errs
 
 
-def test_mixed_launch_equals_separate_launches():
-    # the single mixed grid runs the same device code per item: bitwise equal
-    shape, mk = ATT_BATCHES["tiny-ragged"]
+@pytest.mark.parametrize("name", ["tiny-ragged", "8b-mixed-small", "70b-shape-small"])
+def test_mixed_launch_equals_separate_launches(name):
+    # the single mixed grid runs the same device code per item (its prefill
+    # items hold 64 rows, the prefill-only launch's 128): bitwise equal
+    shape, mk = ATT_BATCHES[name]
     batch = mk()
     case = _filled_case(shape, batch)
     d = DevCase(case)
