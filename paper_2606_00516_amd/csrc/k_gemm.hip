@@ -547,12 +547,12 @@ GemmPlan plan_gemm(int M, int N, int K, int epi) {
   // 256 x 256 tiles once the grid covers at least half the CUs
   const long big_tiles = (long)((M + BG_BM - 1) / BG_BM) * ((ncols + BG_BN - 1) / BG_BN);
   if (K % BG_BK == 0 && N % 8 == 0 && fits && M >= 256) {
-    // one block per CU: split K while the tiles cover under half the CUs,
+    // one block per CU: split K while the tiles cover at most half the CUs,
     // keeping at least 8 K tiles per split
     p.kind = 2;
     const int nk = K / BG_BK;
     int splits = 1;
-    if (big_tiles < 128 && (size_t)M * K * 2 < ((size_t)1 << 31)) {
+    if (big_tiles <= 128 && (size_t)M * K * 2 < ((size_t)1 << 31)) {
       const long by_cus = 256 / big_tiles, by_k = nk / 8;
       splits = (int)(by_cus < by_k ? by_cus : by_k);
     }
