@@ -217,12 +217,14 @@ StepBufs bufs_at(char *base, const WsLayout &L) {
                   base + L.gemm};
 }
 
-// Make sure a profiling slot's events cover n layers.
+// Make sure a profiling slot's events cover n layers.  They only time the
+// stages: recording them skips the system-scope fence (an L2 write-back and
+// invalidation that would perturb the very work being timed).
 eb_status grow_events(std::vector<hipEvent_t> &pev, int layers) {
   const size_t need = (size_t)2 * kStages * layers;
   while (pev.size() < need) {
     hipEvent_t e = nullptr;
-    hipError_t r = hipEventCreate(&e);
+    hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
     if (r != hipSuccess) return hip_fail(r, "hipEventCreate");
     pev.push_back(e);
   }
