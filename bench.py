@@ -146,11 +146,11 @@ def cpu_baseline(shape, batch, w, pool, x, mode, target_s, kv_scales=None):
     xb = gen.bits(x)
     done, spent, rows, kv_bytes = [], 0.0, 0, 0
     # cheapest requests first; passes over the whole workload repeat until
-    # about target_s seconds of oracle time have been spent (at most 8 passes)
+    # about target_s seconds of oracle time have been spent (at most 64 passes)
     order = list(np.argsort(batch.chunk_lens, kind="stable"))
     staged = {}
     passes = 0
-    while spent < target_s and passes < 8:
+    while spent < target_s and passes < 64:
         for i in order:
             if i not in staged:
                 ids = torch.as_tensor(bt_host[i, :need[i]].astype(np.int64), device=pool.k_cache.device)
