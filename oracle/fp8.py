@@ -19,6 +19,9 @@ e4m3(bf16(value) / scale) with the division in float32, rounded to nearest
 (ties to even) and saturated to +-448 beyond the largest finite value (also
 for +-inf); NaN encodes as 0x7F with the input's sign.  A cached code reads
 back as decode(code) * scale.
+
+8-bit weights: a projection W [out, in] is held as codes with one scale per
+output row; the weight it stands for is decode(code[n][k]) * scale[n].
 """
 from __future__ import annotations
 
@@ -68,3 +71,9 @@ def quantize_cache_value(bf16_value_f32, scale: float) -> np.ndarray:
 def dequantize(codes, scale: float) -> np.ndarray:
     """Values a cached code stands for: decode(code) * scale (float64)."""
     return e4m3_decode(codes) * float(scale)
+
+
+def dequantize_rows(codes, scales) -> np.ndarray:
+    """Weights 8-bit codes [out, in] with one scale per output row stand for:
+    decode(code[n][k]) * scales[n] (float64)."""
+    return e4m3_decode(codes) * np.asarray(scales, np.float64)[:, None]

@@ -203,9 +203,18 @@ def prepare_weights(w_bits: Dict[str, np.ndarray], cfg: LayerCfg, dtype=np.float
     """bf16 weight bits -> working-precision arrays, split into named parts.
 
     w_qkv rows: q heads, k heads, v heads; w_gate_up rows: gate then up.
+    A projection given as 8-bit E4M3 codes (uint8) comes with its per-row
+    scales under "s_" + the name without "w_" (s_qkv, s_o, s_gate_up,
+    s_down): its weights are decode(code) * scale of the row, formed in
+    float64.  The norm gains are always bf16.
     """
     nq, nkv, hd, f = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.ffn
-    cv = lambda k: bf16_bits_to_f32(w_bits[k]).astype(dtype)  # noqa: E731
+
+    def cv(k):
+        w = w_bits[k]
+        if w.dtype == np.uint8:
+            return fp8.dequantize_rows(w, w_bits["s_" + k[2:]]).astype(dtype)
+        return bf16_bits_to_f32(w).astype(dtype)
     qkv = cv("w_qkv")
     gu = cv("w_gate_up")
     return {

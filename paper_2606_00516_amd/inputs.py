@@ -298,6 +298,63 @@ def make_block_tables(batch: Batch, spare_pages: int, seed: int, page: int = PAG
     return bt, pool
 
 
+def make_weights_fp8(shape: LayerShape, seed: Optional[int] = None, device="cpu",
+                     proj_std: float = 0.02) -> dict:
+    """Layer weights with the four projections as 8-bit E4M3 codes (uint8,
+    [out, in]) and one float32 scale per output row (keys s_qkv, s_o,
+    s_gate_up, s_down); norm gains bf16 as in make_weights.
+
+    Codes are random bytes with a random sign bit, an exponent field in 4..9
+    and a random 3-bit mantissa (values 1/8 .. 7.5 in magnitude, RMS about
+    2.3); row scales are proj_std / 2.3 times U[0.5, 1.5], so the weights
+    they stand for have about proj_std spread and every row a scale of its own.
+    """
+    if seed is None:
+        seed = seeds()["weights"]
+    g = _gen(device, seed)
+    d, hd = shape.hidden, shape.head_dim
+    f = shape.ffn
+
+    def codes(rows, cols):
+        w = torch.empty(rows, cols, dtype=torch.uint8, device=device)
+        step = max(1, (1 << 26) // cols)
+        for r0 in range(0, rows, step):
+            r1 = min(rows, r0 + step)
+            n = (r1 - r0, cols)
+            sign = torch.randint(0, 2, n, generator=g, device=device) << 7
+            ex = torch.randint(4, 10, n, generator=g, device=device) << 3
+            man = torch.randint(0, 8, n, generator=g, device=device)
+            w[r0:r1] = (sign | ex | man).to(torch.uint8)
+        return w
+
+    def scales(rows):
+        return (proj_std / 2.3) * (0.5 + torch.rand(rows, generator=g, device=device))
+
+    def gain():
+        return (1.0 + 0.1 * torch.randn(d, generator=g, device=device)).to(torch.bfloat16)
+
+    return {
+        "attn_norm": gain(),
+        "w_qkv": codes(shape.qkv_rows, d), "s_qkv": scales(shape.qkv_rows),
+        "w_o": codes(d, shape.n_q_heads * hd), "s_o": scales(d),
+        "mlp_norm": gain(),
+        "w_gate_up": codes(2 * f, d), "s_gate_up": scales(2 * f),
+        "w_down": codes(d, f), "s_down": scales(d),
+    }
+
+
+def weight_arrays(w: dict) -> dict:
+    """Host numpy form of a weight dict: bf16 bit patterns, 8-bit codes and
+    float32 row scales as they are."""
+    out = {}
+    for k, v in w.items():
+        if v.dtype == torch.bfloat16:
+            out[k] = bits(v)
+        else:
+            out[k] = v.detach().contiguous().cpu().numpy()
+    return out
+
+
 def make_kv_pool(shape: LayerShape, batch: Batch, seed: Optional[int] = None, device="cpu",
                  spare_pages: int = 0, poison: bool = True,
                  max_pages_per_seq: Optional[int] = None) -> KVPool:

@@ -19,7 +19,13 @@ def hf_layer(shape, w_bits):
     # the library forms its frequencies in fp32; recompute them in fp64
     hd = shape.head_dim
     rot.inv_freq = shape.rope_theta ** (-torch.arange(0, hd, 2, dtype=torch.float64) / hd)
-    f = lambda k: torch.from_numpy(L.bf16_bits_to_f32(w_bits[k]).astype(np.float64))  # noqa: E731
+    def f(k):
+        # bf16 bits, or 8-bit codes with row scales decoded by torch's float8_e4m3fn
+        w = w_bits[k]
+        if w.dtype == np.uint8:
+            s = torch.from_numpy(np.asarray(w_bits["s_" + k[2:]], np.float64))
+            return torch.from_numpy(np.ascontiguousarray(w)).view(torch.float8_e4m3fn).double() * s[:, None]
+        return torch.from_numpy(L.bf16_bits_to_f32(w).astype(np.float64))
     nq, nkv, hd, ff = shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn
     qkv, gu = f("w_qkv"), f("w_gate_up")
     # the library's RMSNorm module computes in fp32; use torch's in fp64

@@ -144,3 +144,59 @@ def test_planted_code_mistakes_are_caught(monkeypatch):
         worst = max(_maxrel(inter["h1"][off[i]:off[i + 1]] - x[off[i]:off[i + 1]], refs[i])
                     for i in range(_BATCH.num_seqs))
         assert worst > 1e-3, (name, worst)
+
+
+# ------------------------------------------------- 8-bit weights
+
+def test_weight_rows_match_torch():
+    rng = np.random.default_rng(5)
+    codes = rng.integers(0, 256, (37, 50)).astype(np.uint8)
+    codes[(codes & 0x7F) == 0x7F] = 0x3A  # no NaN codes in weights
+    scales = rng.uniform(0.001, 0.01, 37).astype(np.float32)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).double() * torch.from_numpy(scales).double()[:, None]
+    assert np.array_equal(F.dequantize_rows(codes, scales), ref.numpy())
+
+
+def _w8_inputs():
+    shape = gen.TINY
+    w = gen.make_weights_fp8(shape, proj_std=0.2)
+    pool = gen.make_kv_pool(shape, _BATCH, spare_pages=3, poison=True)
+    return shape, dict(cfg=oracle_cfg(shape), w_bits=gen.weight_arrays(w),
+                       k_cache=gen.bits(pool.k_cache).copy(), v_cache=gen.bits(pool.v_cache).copy(),
+                       block_tables=pool.block_tables.numpy(), context_lens=_BATCH.context_lens,
+                       chunk_lens=_BATCH.chunk_lens, x_bits=gen.bits(gen.make_x(shape, _BATCH.num_tokens)))
+
+
+@pytest.mark.parametrize("mode", ["batched", "exact"])
+def test_layer_with_8bit_weights_matches_transformers(mode):
+    # the transformers Llama layer in fp64 with the weights torch decodes from
+    # the codes and row scales: the same layer as the oracle's on 8-bit weights
+    shape, o = _w8_inputs()
+    W = oracle.prepare_weights(o["w_bits"], o["cfg"], np.float64)
+    y, inter = oracle.layer_step(o["cfg"], W, o["k_cache"].copy(), o["v_cache"].copy(), o["block_tables"],
+                                 o["context_lens"], o["chunk_lens"], o["x_bits"], mode=mode, intermediates=True)
+    x = L.bf16_bits_to_f32(o["x_bits"]).astype(np.float64)
+    off = _BATCH.row_offsets
+    for i in range(_BATCH.num_seqs):
+        rows = slice(off[i], off[i + 1])
+        attn_b, mlp_b, y_ref = hf_reference(shape, o, i)
+        assert _maxrel(inter["h1"][rows] - x[rows], attn_b) < 1e-9
+        assert _maxrel(y[rows], y_ref) < 1e-9
+
+
+def test_planted_weight_scale_mistakes_are_caught(monkeypatch):
+    # row scales ignored, or taken per column: the pin above must fail
+    shape, o = _w8_inputs()
+    refs = [hf_reference(shape, o, i)[2] for i in range(_BATCH.num_seqs)]
+    good = F.dequantize_rows
+    plants = {"no row scale": lambda c, s: F.e4m3_decode(c) * float(np.mean(s)),
+              "scale per column": lambda c, s: F.e4m3_decode(c) * np.resize(np.asarray(s, np.float64), c.shape[1])[None, :]}
+    for name, bad in plants.items():
+        with monkeypatch.context() as m:
+            m.setattr(F, "dequantize_rows", bad)
+            W = oracle.prepare_weights(o["w_bits"], o["cfg"], np.float64)
+        y = oracle.layer_step(o["cfg"], W, o["k_cache"].copy(), o["v_cache"].copy(), o["block_tables"],
+                              o["context_lens"], o["chunk_lens"], o["x_bits"])
+        off = _BATCH.row_offsets
+        worst = max(_maxrel(y[off[i]:off[i + 1]], refs[i]) for i in range(_BATCH.num_seqs))
+        assert worst > 1e-3, (name, worst)
