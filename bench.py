@@ -60,6 +60,8 @@ def parse():
     ap.add_argument("--budget", type=int, default=2048, help="token budget for mixed8b")
     ap.add_argument("--kv", default="bf16", choices=["bf16", "fp8"],
                     help="KV cache element: bf16, or 8-bit E4M3 codes with per-tensor k/v scales")
+    ap.add_argument("--weights", default="bf16", choices=["bf16", "fp8"],
+                    help="projection weights: bf16, or 8-bit E4M3 codes with one fp32 scale per output row")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
     ap.add_argument("--json-out", default=None)
@@ -70,9 +72,21 @@ def parse():
 # algorithmic work of a step (each byte / flop counted once)
 # ----------------------------------------------------------------------------
 
-def step_work(shape, batch, kv_elem=2):
+def weight_bytes(shape, kind="bf16"):
+    """Bytes of one layer's weights: bf16, or 8-bit projection codes plus one
+    fp32 scale per projection row (norm gains bf16 either way)."""
+    if kind == "bf16":
+        return shape.weight_bytes()
+    d, f = shape.hidden, shape.ffn
+    codes = shape.qkv_rows * d + d * shape.n_q_heads * shape.head_dim + 2 * f * d + d * f
+    rows = shape.qkv_rows + d + 2 * f + d
+    return codes + 4 * rows + 2 * 2 * d
+
+
+def step_work(shape, batch, kv_elem=2, w_kind="bf16"):
     """Bytes and FLOPs a step must move / compute at minimum (``kv_elem``:
-    bytes per cached K or V element, 2 for bf16, 1 for 8-bit codes)."""
+    bytes per cached K or V element, 2 for bf16, 1 for 8-bit codes;
+    ``w_kind``: the projection weights' type)."""
     import numpy as np
     nkv, hd, nq, d = shape.n_kv_heads, shape.head_dim, shape.n_q_heads, shape.hidden
     c = batch.context_lens.astype(np.int64)
@@ -81,7 +95,7 @@ def step_work(shape, batch, kv_elem=2):
     kv_bytes_dec = int(((c[dec] + 1) * nkv * hd * 2 * kv_elem).sum())
     kv_bytes_pf = int(((c[~dec] + n[~dec]) * nkv * hd * 2 * kv_elem).sum())
     T = int(n.sum())
-    w_bytes = shape.weight_bytes()
+    w_bytes = weight_bytes(shape, w_kind)
     act_bytes = T * d * 2 * 2
     gemm_flops = 2 * T * (shape.qkv_rows * d + d * nq * hd + 2 * shape.ffn * d + d * shape.ffn)
     attn_flops_dec = int((4 * nq * hd * (c[dec] + 1)).sum())
@@ -115,6 +129,12 @@ def workload(args):
 # magnitude, so cached values span about 0.06 .. 3.75 like the bf16 N(0, 1) pool
 FP8_SCALES = (0.5, 0.5)
 KV_LABEL = {"bf16": "bf16", "fp8": "fp8-e4m3 codes, per-tensor k/v scales"}
+W_LABEL = {"bf16": "bf16", "fp8": "fp8-e4m3 codes, one fp32 scale per output row"}
+
+
+def make_w(gen, shape, kind, **kw):
+    """One layer's random-init weights of type ``kind``."""
+    return gen.make_weights_fp8(shape, **kw) if kind == "fp8" else gen.make_weights(shape, **kw)
 
 
 def make_pool(gen, shape, batch, kv, **kw):
@@ -139,7 +159,8 @@ def cpu_baseline(shape, batch, w, pool, x, mode, target_s, kv_scales=None):
         threads = 1
     cfg = oracle.LayerCfg(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn,
                           shape.page_size, shape.rms_eps, shape.rope_theta)
-    W = oracle.prepare_weights({k: gen.bits(v) for k, v in w.items()}, cfg)
+    W = oracle.prepare_weights(gen.weight_arrays(w), cfg)
+    w_kind = "fp8" if w["w_qkv"].dtype == torch.uint8 else "bf16"
     need = gen.pages_needed(batch)
     bt_host = pool.block_tables.cpu().numpy()
     off = batch.row_offsets
@@ -174,7 +195,7 @@ def cpu_baseline(shape, batch, w, pool, x, mode, target_s, kv_scales=None):
         passes += 1
     # algorithmic bytes of the step-equivalents done: the weights once per
     # whole-workload step (rows / T of them) plus each request's K/V
-    gbps = (kv_bytes + shape.weight_bytes() * rows / batch.num_tokens) / spent / 1e9
+    gbps = (kv_bytes + weight_bytes(shape, w_kind) * rows / batch.num_tokens) / spent / 1e9
     return {"value": round(gbps, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
             "tokens_per_s": round(rows / spent, 3), "seconds": round(spent, 2),
             "sample": f"{len(done)} request-steps ({rows} rows; {passes} pass(es) over the {batch.num_seqs} requests "
@@ -308,10 +329,10 @@ def stack70b(args, dev):
     L = args.layers
     s0 = gen.seeds()
     t0 = time.perf_counter()
-    weights = [gen.make_weights(shape, seed=s0["weights"] + l, device=dev) for l in range(L)]
+    weights = [make_w(gen, shape, args.weights, seed=s0["weights"] + l, device=dev) for l in range(L)]
     torch.cuda.synchronize()
     print(f"# {L} layers of weights generated in {time.perf_counter() - t0:.1f} s "
-          f"({L * shape.weight_bytes() / 1e9:.1f} GB)", file=sys.stderr, flush=True)
+          f"({L * weight_bytes(shape, args.weights) / 1e9:.1f} GB)", file=sys.stderr, flush=True)
     points = [("decode", gen.batch_70b_decode(), "decode")]
     for r in [float(v) for v in args.stack_r.split(",") if v]:
         points.append((f"mixed r={r:.1f}", gen.batch_70b_mixed(r), "mixed"))
@@ -355,7 +376,7 @@ def stack70b(args, dev):
         call()
         st = B.eb_profile_read(h)
         B.eb_profile(h, False)
-        wk = step_work(shape, batch, kv_elem)
+        wk = step_work(shape, batch, kv_elem, args.weights)
         kv = wk["kv_bytes_decode"] + wk["kv_bytes_prefill"]
         gemm_ms = sum(v for k, v in st.items() if k.endswith("gemm"))
         attn_ms = attn_timed
@@ -581,7 +602,8 @@ def main():
                 "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
                 "config": {"workload": f"llama3-70b-shaped model step, {args.layers} layers: decode EB 256 requests "
                                        f"ctx U[2048,16384]; MB 4096-token steps at r = {args.stack_r}",
-                           "kv_cache": KV_LABEL[args.kv], "parallelism": "single-gpu"},
+                           "kv_cache": KV_LABEL[args.kv], "weights": W_LABEL[args.weights],
+                           "parallelism": "single-gpu"},
                 "roofline": {"kernel": "k_decode_mfma (decode attention, summed over layers)", "bound": "hbm",
                              "achieved": dec["attention_hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                              "frac": round(dec["attention_hbm_gbps"] / HBM_PEAK_GBPS, 4), "traffic": None},
@@ -597,7 +619,7 @@ def main():
     step_fn = {"decode": B.eb_layer_step_decode, "prefill": B.eb_layer_step_prefill,
                "mixed": B.eb_layer_step_mixed}[mode]
     # inputs generated on the GPU and left resident in HBM
-    w = gen.make_weights(shape, device=dev)
+    w = make_w(gen, shape, args.weights, device=dev)
     pool, kvs = make_pool(gen, shape, batch, args.kv, device=dev)
     x = gen.make_x(shape, batch.num_tokens, device=dev)
     y = torch.empty_like(x)
@@ -607,7 +629,7 @@ def main():
     ms, stages, t_ms = measure(B, h, step_fn, w, pool, batch, x, y, ws, args.steps, args.warmup, kv_scales=kvs,
                                timed_stage=timed_stage)
 
-    wk = step_work(shape, batch, 1 if args.kv == "fp8" else 2)
+    wk = step_work(shape, batch, 1 if args.kv == "fp8" else 2, args.weights)
     step_bytes = wk["kv_bytes_decode"] + wk["kv_bytes_prefill"] + wk["weight_bytes"] + wk["act_bytes"]
     step_flops = wk["gemm_flops"] + wk["attn_flops_decode"] + wk["attn_flops_prefill"]
     gemm_ms = sum(v for k, v in stages.items() if k.endswith("gemm"))
@@ -640,7 +662,9 @@ def main():
         g_ms = t_ms
         fl = 2 * wk["T"] * 2 * shape.ffn * shape.hidden
         achieved = fl / (g_ms / 1e3) / 1e12
-        roof = {"kernel": "k_gemm_big (gate/up projection + SiLU*mul, 256x256 tiles)", "bound": "mfma",
+        roof = {"kernel": "k_gemm_big (gate/up projection + SiLU*mul, 256x256 tiles" +
+                          (", 8-bit weights converted to bf16 in LDS)" if args.weights == "fp8" else ")"),
+                "bound": "mfma",
                 "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / BF16_PEAK_TFLOPS, 4), "avg_launch_ms": round(g_ms, 5),
                 "flops_per_launch": fl, "traffic": None}
@@ -659,7 +683,8 @@ def main():
         "metric": METRIC, "value": round(value, 3), "unit": unit, "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": label, "kv_cache": KV_LABEL[args.kv], "num_tokens": wk["T"],
+        "config": {"workload": label, "kv_cache": KV_LABEL[args.kv], "weights": W_LABEL[args.weights],
+                   "num_tokens": wk["T"],
                    "num_requests": batch.num_seqs,
                    "decode_share": round(batch.num_decode / max(wk["T"], 1), 4), "kv_cache": KV_LABEL[args.kv],
                    "parallelism": "single-gpu"},

@@ -76,14 +76,29 @@ typedef struct eb_layer_config {
   float rms_eps, rope_theta;
 } eb_layer_config;
 
-/* Device pointers to bf16 weights in the [out, in] layout:
- *   attn_norm, mlp_norm  [hidden]
+/* Element type of the four projection matrices. */
+typedef enum {
+  EB_W_BF16 = 0,     /* bf16 values */
+  EB_W_FP8_E4M3 = 1  /* 8-bit OCP E4M3 codes with one fp32 scale per output row */
+} eb_weight_dtype;
+
+/* Device pointers to the weights in the [out, in] layout:
+ *   attn_norm, mlp_norm  [hidden] (bf16 always)
  *   w_qkv     [(n_q + 2 n_kv) head_dim, hidden], rows q heads, k heads, v heads
  *   w_o       [hidden, n_q head_dim]
  *   w_gate_up [2 ffn, hidden], rows gate then up
- *   w_down    [hidden, ffn] */
+ *   w_down    [hidden, ffn]
+ * w_dtype EB_W_BF16 (a zero-initialised struct): the projections hold bf16.
+ * EB_W_FP8_E4M3: they hold E4M3 codes (one byte each, same layout) and
+ * s_qkv, s_o, s_gate_up, s_down point to fp32 scales, one per row of the
+ * matching matrix; the weight a code stands for is decode(code) * scale of
+ * its row (the E4M3 values convert exactly to bf16 for the products, the
+ * scale multiplies the fp32 sum).  A NaN code (0x7F, 0xFF) is the caller's
+ * to avoid.  The scale pointers are ignored for bf16 weights. */
 typedef struct eb_layer_weights {
   const void *attn_norm, *w_qkv, *w_o, *mlp_norm, *w_gate_up, *w_down;
+  int32_t w_dtype;
+  const float *s_qkv, *s_o, *s_gate_up, *s_down;
 } eb_layer_weights;
 
 /* Element type of the KV cache. */
@@ -217,6 +232,17 @@ eb_status eb_op_rmsnorm(const eb_handle *h, const void *x, const void *gamma, vo
 size_t eb_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K);
 eb_status eb_op_gemm(const void *A, const void *W, void *out, const void *residual, int32_t M, int32_t N,
                      int32_t K, eb_epilogue epi, void *ws, size_t ws_bytes, void *stream);
+
+/* eb_op_gemm with 8-bit weights: W holds E4M3 codes [N, K] (one byte each)
+ * and w_scale (device, fp32 [N], 16-byte aligned) one scale per row; the
+ * product is out = epilogue(A (decode(W) * w_scale)^T), the scale applied to
+ * each column's fp32 sum.  ws: at least eb_op_gemm_workspace_bytes(M, N, K),
+ * which covers both weight types.  EB_ERR_LIMITS when no kernel reaches the
+ * operands through its 32-bit buffer ranges: W of 2^31 bytes or more, or A
+ * of 2^31 bytes or more unless K is a multiple of 64, M >= 256 and W is
+ * under 2^30 bytes.  A NaN code (0x7F, 0xFF) is the caller's to avoid. */
+eb_status eb_op_gemm_w8(const void *A, const void *W, const float *w_scale, void *out, const void *residual,
+                        int32_t M, int32_t N, int32_t K, eb_epilogue epi, void *ws, size_t ws_bytes, void *stream);
 
 /* RoPE on the q and k heads of qkv (bf16 [num_tokens, (n_q + 2 n_kv) head_dim],
  * the QKV projection output) at pos = c_i + j; q is rotated in place, the

@@ -27,7 +27,7 @@ EPILOGUES = {"store": 0, "residual": 1, "silu_mul": 2}
 # every symbol include/eb_layer.h declares
 SYMBOLS = ("eb_create", "eb_destroy", "eb_workspace_bytes", "eb_layer_step_decode", "eb_layer_step_prefill",
            "eb_layer_step_mixed", "eb_validate", "eb_status_str", "eb_last_error", "eb_op_rmsnorm",
-           "eb_op_gemm_workspace_bytes", "eb_op_gemm", "eb_op_rope_kv_append", "eb_op_attention",
+           "eb_op_gemm_workspace_bytes", "eb_op_gemm", "eb_op_gemm_w8", "eb_op_rope_kv_append", "eb_op_attention",
            "eb_op_gather_kv", "eb_profile", "eb_profile_read", "eb_profile_stage_name", "eb_stack_workspace_bytes",
            "eb_stack_step")
 
@@ -45,7 +45,11 @@ class LayerConfig(ctypes.Structure):
 
 
 class LayerWeights(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_void_p) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")]
+    _fields_ = [(n, ctypes.c_void_p) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")] + \
+        [("w_dtype", ctypes.c_int32)] + [(n, ctypes.c_void_p) for n in ("s_qkv", "s_o", "s_gate_up", "s_down")]
+
+
+W_BF16, W_FP8_E4M3 = 0, 1
 
 
 class KvCache(ctypes.Structure):
@@ -85,6 +89,7 @@ def lib() -> ctypes.CDLL:
         "eb_op_rmsnorm": (I32, [VP, VP, VP, VP, I32, VP]),
         "eb_op_gemm_workspace_bytes": (SZ, [I32, I32, I32]),
         "eb_op_gemm": (I32, [VP, VP, VP, VP, I32, I32, I32, I32, VP, SZ, VP]),
+        "eb_op_gemm_w8": (I32, [VP, VP, VP, VP, VP, I32, I32, I32, I32, VP, SZ, VP]),
         "eb_op_rope_kv_append": (I32, [VP, VP, P(KvCache), P(Batch), VP, SZ, VP]),
         "eb_op_attention": (I32, [VP, VP, P(KvCache), P(Batch), VP, VP, SZ, I32, VP]),
         "eb_op_gather_kv": (I32, [VP, P(KvCache), P(Batch), VP, VP, VP, SZ, VP]),
@@ -156,7 +161,16 @@ def kv_struct(k_cache: torch.Tensor, v_cache: torch.Tensor, block_tables: torch.
 
 
 def weights_struct(w: dict) -> LayerWeights:
-    return LayerWeights(*[_ptr(w[k]) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")])
+    """Weights dict -> struct: bf16 projections, or uint8 / float8_e4m3fn
+    codes with float32 row scales under s_qkv, s_o, s_gate_up, s_down."""
+    lw = LayerWeights(*[_ptr(w[k]) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")])
+    if w["w_qkv"].dtype in _CODE_DTYPES:
+        lw.w_dtype = W_FP8_E4M3
+        for k in ("s_qkv", "s_o", "s_gate_up", "s_down"):
+            if w[k].dtype != torch.float32 or not w[k].is_contiguous():
+                raise ValueError(f"{k} must be contiguous float32")
+            setattr(lw, k, _ptr(w[k]))
+    return lw
 
 
 class Handle:
@@ -285,6 +299,24 @@ def eb_op_gemm(A: torch.Tensor, W: torch.Tensor, epilogue: str = "store", residu
     ws = alloc_workspace(nb, A.device)
     _check(lib().eb_op_gemm(_ptr(A), _ptr(W), _ptr(out), _ptr(residual), M, N, K, EPILOGUES[epilogue], _ptr(ws),
                             ws.numel(), _stream(stream)))
+    return out
+
+
+def eb_op_gemm_w8(A: torch.Tensor, W: torch.Tensor, w_scale: torch.Tensor, epilogue: str = "store",
+                  residual: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None, stream=None):
+    """W: uint8 E4M3 codes [N, K]; w_scale: float32 [N], one scale per row."""
+    if W.dtype not in _CODE_DTYPES or w_scale.dtype != torch.float32 or not w_scale.is_contiguous():
+        raise TypeError("W must hold uint8 codes and w_scale contiguous float32 row scales")
+    M, K = A.shape
+    N = W.shape[0]
+    if w_scale.numel() != N:
+        raise ValueError("w_scale needs one scale per row of W")
+    ncol = N // 2 if epilogue == "silu_mul" else N
+    out = torch.empty(M, ncol, dtype=torch.bfloat16, device=A.device) if out is None else out
+    nb = int(lib().eb_op_gemm_workspace_bytes(M, N, K))
+    ws = alloc_workspace(nb, A.device)
+    _check(lib().eb_op_gemm_w8(_ptr(A), _ptr(W), _ptr(w_scale), _ptr(out), _ptr(residual), M, N, K,
+                               EPILOGUES[epilogue], _ptr(ws), ws.numel(), _stream(stream)))
     return out
 
 

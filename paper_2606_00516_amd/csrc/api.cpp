@@ -68,11 +68,14 @@ WsLayout layout_for(const Shape &s, const HostPlan &p, bool full_step, bool stac
     L.mlp = take(T * s.ffn * 2);
     size_t g = 0;
     const int M = p.T;
-    const GemmPlan plans[4] = {plan_gemm(M, s.qkv_cols(), s.hidden, EPI_STORE),
-                               plan_gemm(M, s.hidden, s.nq * s.hd, EPI_RESIDUAL),
-                               plan_gemm(M, 2 * s.ffn, s.hidden, EPI_SILU_MUL),
-                               plan_gemm(M, s.hidden, s.ffn, EPI_RESIDUAL)};
-    for (const auto &gp : plans) g = gp.ws_bytes > g ? gp.ws_bytes : g;
+    // room for the plans of either weight type
+    for (int w8 = 0; w8 < 2; ++w8) {
+      const GemmPlan plans[4] = {plan_gemm(M, s.qkv_cols(), s.hidden, EPI_STORE, w8),
+                                 plan_gemm(M, s.hidden, s.nq * s.hd, EPI_RESIDUAL, w8),
+                                 plan_gemm(M, 2 * s.ffn, s.hidden, EPI_SILU_MUL, w8),
+                                 plan_gemm(M, s.hidden, s.ffn, EPI_RESIDUAL, w8)};
+      for (const auto &gp : plans) g = gp.ws_bytes > g ? gp.ws_bytes : g;
+    }
     L.gemm = take(g);
     if (stack) L.alt = take(T * s.hidden * 2);
   }
@@ -195,9 +198,25 @@ KV kv_of(const eb_kv_cache *kv) {
             kv->num_pages, kv->max_pages_per_seq, f8 ? 1 : 0, f8 ? kv->k_scale : 1.f, f8 ? kv->v_scale : 1.f};
 }
 
-eb_status check_weights(const eb_layer_weights *w) {
+// The weights of one layer for a batch of T tokens: pointers, the weight
+// type, and (8-bit weights) scales and that a kernel takes every projection.
+eb_status check_weights(const eb_layer_weights *w, const Shape &sh, int T) {
   if (!w || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm || !w->w_gate_up || !w->w_down)
     return fail(EB_ERR_NULL, "a weight pointer is NULL");
+  if (w->w_dtype == EB_W_BF16) return EB_OK;
+  if (w->w_dtype != EB_W_FP8_E4M3) return fail(EB_ERR_CONFIG, "unknown w_dtype");
+  const float *sc[4] = {w->s_qkv, w->s_o, w->s_gate_up, w->s_down};
+  for (const float *p : sc) {
+    if (!p) return fail(EB_ERR_NULL, "8-bit weights need the four row-scale pointers");
+    if (reinterpret_cast<uintptr_t>(p) % 16) return fail(EB_ERR_CONFIG, "row scales must be 16-byte aligned");
+  }
+  const int shp[4][3] = {{sh.qkv_cols(), sh.hidden, EPI_STORE},
+                         {sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL},
+                         {2 * sh.ffn, sh.hidden, EPI_SILU_MUL},
+                         {sh.hidden, sh.ffn, EPI_RESIDUAL}};
+  for (const auto &g : shp)
+    if (plan_gemm(T, g[0], g[1], g[2], true).kind < 0)
+      return fail(EB_ERR_LIMITS, "8-bit projection too large for the GEMM kernels");
   return EB_OK;
 }
 
@@ -237,6 +256,7 @@ eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, con
                      const uint16_t *xin, uint16_t *yout, int T, eb_mode mode, int layer, hipEvent_t *pev,
                      hipStream_t st) {
   const Shape &sh = h->shape;
+  const bool w8 = w->w_dtype == EB_W_FP8_E4M3;
   hipError_t e;
   auto mark = [&](int i) -> hipError_t {
     return pev && ((h->prof_mask >> (i / 2)) & 1u) ? hipEventRecord(pev[(size_t)2 * kStages * layer + i], st)
@@ -249,30 +269,27 @@ eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, con
   EB_STAGE(0, launch_rmsnorm(xin, static_cast<const uint16_t *>(w->attn_norm), B.act, T, sh.hidden, sh.eps, st),
            "rmsnorm1");
   EB_STAGE(1,
-           launch_gemm(plan_gemm(T, sh.qkv_cols(), sh.hidden, EPI_STORE), B.act,
-                       static_cast<const uint16_t *>(w->w_qkv), B.qkv, nullptr, T, sh.qkv_cols(), sh.hidden,
-                       EPI_STORE, B.gws, st),
+           launch_gemm(plan_gemm(T, sh.qkv_cols(), sh.hidden, EPI_STORE, w8), B.act, w->w_qkv,
+                       w8 ? w->s_qkv : nullptr, B.qkv, nullptr, T, sh.qkv_cols(), sh.hidden, EPI_STORE, B.gws, st),
            "qkv gemm");
   EB_STAGE(2, launch_rope_append(sh, B.qkv, kvd, m, st), "rope/kv append");
   const int kind = mode == EB_MODE_DECODE ? 0 : (mode == EB_MODE_PREFILL ? 1 : 2);
   EB_STAGE(3, launch_attention(sh, B.qkv, kvd, m, B.attn, B.part_o, B.part_ml, kind, st, 1), "attention");
   EB_STAGE(4, launch_attention(sh, B.qkv, kvd, m, B.attn, B.part_o, B.part_ml, kind, st, 2), "attention combine");
   EB_STAGE(5,
-           launch_gemm(plan_gemm(T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL), B.attn,
-                       static_cast<const uint16_t *>(w->w_o), B.h1, xin, T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL,
-                       B.gws, st),
+           launch_gemm(plan_gemm(T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, w8), B.attn, w->w_o,
+                       w8 ? w->s_o : nullptr, B.h1, xin, T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, B.gws, st),
            "o gemm");
   EB_STAGE(6, launch_rmsnorm(B.h1, static_cast<const uint16_t *>(w->mlp_norm), B.act, T, sh.hidden, sh.eps, st),
            "rmsnorm2");
   EB_STAGE(7,
-           launch_gemm(plan_gemm(T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL), B.act,
-                       static_cast<const uint16_t *>(w->w_gate_up), B.mlp, nullptr, T, 2 * sh.ffn, sh.hidden,
-                       EPI_SILU_MUL, B.gws, st),
+           launch_gemm(plan_gemm(T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL, w8), B.act, w->w_gate_up,
+                       w8 ? w->s_gate_up : nullptr, B.mlp, nullptr, T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL, B.gws,
+                       st),
            "gate/up gemm");
   EB_STAGE(8,
-           launch_gemm(plan_gemm(T, sh.hidden, sh.ffn, EPI_RESIDUAL), B.mlp,
-                       static_cast<const uint16_t *>(w->w_down), yout, B.h1, T, sh.hidden, sh.ffn, EPI_RESIDUAL,
-                       B.gws, st),
+           launch_gemm(plan_gemm(T, sh.hidden, sh.ffn, EPI_RESIDUAL, w8), B.mlp, w->w_down,
+                       w8 ? w->s_down : nullptr, yout, B.h1, T, sh.hidden, sh.ffn, EPI_RESIDUAL, B.gws, st),
            "down gemm");
 #undef EB_STAGE
   return EB_OK;
@@ -288,8 +305,9 @@ eb_status run_layers(eb_handle *h, int32_t n_layers, const eb_layer_weights *w, 
   if (n_layers < 1) return fail(EB_ERR_CONFIG, "n_layers must be >= 1");
   if (!w || !kv) return fail(EB_ERR_NULL, "weights or kv is NULL");
   int32_t min_pages = 0;
+  const int T = b && b->num_tokens > 0 ? b->num_tokens : 1;  // (b itself is checked below)
   for (int l = 0; l < n_layers; ++l) {
-    eb_status s = check_weights(&w[l]);
+    eb_status s = check_weights(&w[l], h->shape, T);
     if (s == EB_OK) s = check_kv(&kv[l]);
     if (s != EB_OK) return n_layers > 1 ? fail(s, "layer " + std::to_string(l) + ": " + g_err) : s;
     min_pages = l == 0 ? kv[l].max_pages_per_seq : std::min(min_pages, kv[l].max_pages_per_seq);
@@ -532,15 +550,17 @@ eb_status eb_op_rmsnorm(const eb_handle *h, const void *x, const void *gamma, vo
 size_t eb_op_gemm_workspace_bytes(int32_t M, int32_t N, int32_t K) {
   if (M <= 0 || N <= 0 || K <= 0) return 0;
   size_t g = 0;
-  for (int epi = 0; epi < 3; ++epi) {
-    const size_t b = plan_gemm(M, N, K, epi).ws_bytes;
-    g = b > g ? b : g;
-  }
+  for (int w8 = 0; w8 < 2; ++w8)
+    for (int epi = 0; epi < 3; ++epi) {
+      const size_t b = plan_gemm(M, N, K, epi, w8).ws_bytes;
+      g = b > g ? b : g;
+    }
   return g;
 }
 
-eb_status eb_op_gemm(const void *A, const void *W, void *out, const void *residual, int32_t M, int32_t N, int32_t K,
-                     eb_epilogue epi, void *ws, size_t ws_bytes, void *stream) {
+namespace {
+eb_status op_gemm(const void *A, const void *W, const float *wscale, void *out, const void *residual, int32_t M,
+                  int32_t N, int32_t K, eb_epilogue epi, void *ws, size_t ws_bytes, void *stream) {
   if (M < 0 || N <= 0 || K <= 0) return fail(EB_ERR_CONFIG, "M must be >= 0, N and K > 0");
   if (K % 8 || N % 8) return fail(EB_ERR_CONFIG, "N and K must be multiples of 8");
   if (epi != EB_EPI_STORE && epi != EB_EPI_RESIDUAL && epi != EB_EPI_SILU_MUL)
@@ -549,13 +569,28 @@ eb_status eb_op_gemm(const void *A, const void *W, void *out, const void *residu
   if (M == 0) return EB_OK;
   if (!A || !W || !out) return fail(EB_ERR_NULL, "A, W or out is NULL");
   if (epi == EB_EPI_RESIDUAL && !residual) return fail(EB_ERR_NULL, "residual is NULL");
-  const GemmPlan p = plan_gemm(M, N, K, (int)epi);
+  const bool w8 = wscale != nullptr;
+  if (w8 && reinterpret_cast<uintptr_t>(wscale) % 16) return fail(EB_ERR_CONFIG, "row scales must be 16-byte aligned");
+  const GemmPlan p = plan_gemm(M, N, K, (int)epi, w8);
+  if (p.kind < 0) return fail(EB_ERR_LIMITS, "operands too large for the 8-bit GEMM kernels");
   eb_status s = check_ws(ws, ws_bytes, p.ws_bytes);
   if (s != EB_OK) return s;
-  hipError_t e = launch_gemm(p, static_cast<const uint16_t *>(A), static_cast<const uint16_t *>(W),
-                             static_cast<uint16_t *>(out), static_cast<const uint16_t *>(residual), M, N, K, (int)epi,
-                             ws, static_cast<hipStream_t>(stream));
+  hipError_t e = launch_gemm(p, static_cast<const uint16_t *>(A), W, wscale, static_cast<uint16_t *>(out),
+                             static_cast<const uint16_t *>(residual), M, N, K, (int)epi, ws,
+                             static_cast<hipStream_t>(stream));
   return e == hipSuccess ? EB_OK : hip_fail(e, "gemm");
+}
+}  // namespace
+
+eb_status eb_op_gemm(const void *A, const void *W, void *out, const void *residual, int32_t M, int32_t N, int32_t K,
+                     eb_epilogue epi, void *ws, size_t ws_bytes, void *stream) {
+  return op_gemm(A, W, nullptr, out, residual, M, N, K, epi, ws, ws_bytes, stream);
+}
+
+eb_status eb_op_gemm_w8(const void *A, const void *W, const float *w_scale, void *out, const void *residual,
+                        int32_t M, int32_t N, int32_t K, eb_epilogue epi, void *ws, size_t ws_bytes, void *stream) {
+  if (!w_scale && M > 0) return fail(EB_ERR_NULL, "w_scale is NULL");
+  return op_gemm(A, W, w_scale, out, residual, M, N, K, epi, ws, ws_bytes, stream);
 }
 
 eb_status eb_op_rope_kv_append(eb_handle *h, void *qkv, const eb_kv_cache *kv, const eb_batch *batch, void *ws,

@@ -78,13 +78,15 @@ hipError_t launch_attention(const Shape &s, const uint16_t *qkv, const KV &kv, c
 // GEMM planning shared by the op entry and the step.
 enum GemmEpi { EPI_STORE = 0, EPI_RESIDUAL = 1, EPI_SILU_MUL = 2 };
 struct GemmPlan {
-  int kind;      // 0 = skinny weight-streaming, 1 = LDS-tiled, 2 = 256 x 256 tiles
+  int kind;      // 0 = skinny weight-streaming, 1 = LDS-tiled, 2 = 256 x 256 tiles, -1 = none fits
   int splits;    // split-K factor (skinny, and big with few tiles)
   int kt_per;    // big: 64-wide K tiles per split
   size_t ws_bytes;
 };
-GemmPlan plan_gemm(int M, int N, int K, int epi);
-hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, uint16_t *out,
+// w8: W holds 8-bit E4M3 codes with one fp32 scale per row (launch_gemm's
+// wscale, null for bf16 weights); such plans never take the tiled kernel.
+GemmPlan plan_gemm(int M, int N, int K, int epi, bool w8 = false);
+hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, const float *wscale, uint16_t *out,
                        const uint16_t *residual, int M, int N, int K, int epi, void *ws, hipStream_t st);
 
 }  // namespace eb

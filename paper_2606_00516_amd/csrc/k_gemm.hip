@@ -40,6 +40,15 @@ __host__ __device__ static inline int logical_cols(int N, int epi) {
 
 __device__ __forceinline__ float silu_f(float g) { return g / (1.0f + __expf(-g)); }
 
+// 8-bit weights: the fp32 sums of logical columns c .. c + 3 (one W row
+// each, consecutive within a column group) times their rows' scales.
+__device__ __forceinline__ f32x4_t row_scaled(f32x4_t v, const float *__restrict__ wscale, int c, int N, int epi) {
+  const int wr = w_row_of(c, N, epi);
+  if (wr < 0) return v;
+  const f32x4_t s = *reinterpret_cast<const f32x4_t *>(wscale + wr);
+  return v * s;
+}
+
 // ===========================================================================
 // skinny
 // ===========================================================================
@@ -54,10 +63,12 @@ constexpr int SK_LDS = 2 * (SK_BN + SK_BM) * SK_ROWB;
 // and its up partner (32 apart) land in the same wave.
 __device__ __forceinline__ int sk_col(int w, int j) { return j < 8 ? 8 * w + j : 32 + 8 * w + (j - 8); }
 
-__global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict__ A, const uint16_t *__restrict__ W,
-                                                     uint16_t *__restrict__ out, const uint16_t *__restrict__ res,
-                                                     float *__restrict__ part, int M, int N, int K, int epi,
-                                                     int ksteps_per_split, int tiles, int mt, int per_xcd) {
+template <bool W8>
+__global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict__ A, const void *__restrict__ W,
+                                                     const float *__restrict__ wscale, uint16_t *__restrict__ out,
+                                                     const uint16_t *__restrict__ res, float *__restrict__ part, int M,
+                                                     int N, int K, int epi, int ksteps_per_split, int tiles, int mt,
+                                                     int per_xcd) {
   extern __shared__ __attribute__((aligned(16))) uint8_t sk_lds[];  // [2][64 W rows + 64 A rows][SK_ROWB]
   // block b takes tile (b % 8) * per_xcd + b / 8, so each XCD walks its own
   // contiguous tile range; the mt row blocks of one column tile are
@@ -73,8 +84,9 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
   const int kbeg = split * ksteps_per_split * 32;
   const int kend = min(K, kbeg + ksteps_per_split * 32);
   const int nst = (kend - kbeg + SK_KC - 1) / SK_KC;
+  constexpr uint32_t WES = W8 ? 1u : 2u;  // bytes per W element
   const buf_rsrc_t ra = make_rsrc(A, (int)min((size_t)M * K * 2, (size_t)0x7FFFFFFF));
-  const buf_rsrc_t rw = make_rsrc(W, (int)min((size_t)N * K * 2, (size_t)0x7FFFFFFF));
+  const buf_rsrc_t rw = make_rsrc(W, (int)min((size_t)N * K * WES, (size_t)0x7FFFFFFF));
 
   // Staging: thread t moves 16-byte chunk t % 16 of tile rows t / 16 + 16 j
   // (each wave instruction reads 4 rows x 256 contiguous bytes); rows outside
@@ -85,7 +97,7 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int wr = w_row_of(n0 + r0 + 16 * j, N, epi);
-    woff[j] = wr >= 0 ? ((uint32_t)wr * (uint32_t)K + (uint32_t)(ch * 8)) * 2u : 0x80000000u;
+    woff[j] = wr >= 0 ? ((uint32_t)wr * (uint32_t)K + (uint32_t)(ch * 8)) * WES : 0x80000000u;
     const int m = m0 + r0 + 16 * j;
     aoff[j] = m < M ? ((uint32_t)m * (uint32_t)K + (uint32_t)(ch * 8)) * 2u : 0x80000000u;
   }
@@ -96,7 +108,12 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
     const uint32_t kb = (uint32_t)(kbeg + s * SK_KC) * 2u;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      wr[j] = buf_ld_u32x4<kAuxNT>(rw, (int)(ok ? woff[j] + kb : 0x80000000u));
+      if constexpr (W8) {  // 8 codes in the low half; exact bf16 images when staged
+        const u32x2_t c = buf_ld_u32x2<kAuxNT>(rw, (int)(ok ? woff[j] + kb / 2u : 0x80000000u));
+        wr[j] = u32x4_t{c[0], c[1], 0u, 0u};
+      } else {
+        wr[j] = buf_ld_u32x4<kAuxNT>(rw, (int)(ok ? woff[j] + kb : 0x80000000u));
+      }
       ar[j] = buf_ld_u32x4<0>(ra, (int)(ok ? aoff[j] + kb : 0x80000000u));
     }
   };
@@ -104,7 +121,9 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
     uint8_t *b = sk_lds + buf * (SK_BN + SK_BM) * SK_ROWB;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      *reinterpret_cast<u32x4_t *>(b + (r0 + 16 * j) * SK_ROWB + ch * 16) = wr[j];
+      u32x4_t wv = wr[j];
+      if constexpr (W8) wv = e4m3x8_to_bf16x8(u32x2_t{wr[j][0], wr[j][1]});
+      *reinterpret_cast<u32x4_t *>(b + (r0 + 16 * j) * SK_ROWB + ch * 16) = wv;
       *reinterpret_cast<u32x4_t *>(b + (SK_BN + r0 + 16 * j) * SK_ROWB + ch * 16) = ar[j];
     }
   };
@@ -151,6 +170,12 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
   // c = sk_col(wave, 4 lg)
   const int c = sk_col(wave, 4 * lg);
   const int ncols = logical_cols(N, epi);
+  if constexpr (W8) {
+    if (n0 + c < ncols) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[i] = row_scaled(acc[i], wscale, n0 + c, N, epi);
+    }
+  }
   if (part) {  // split-K partial, logical column space
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -363,8 +388,9 @@ constexpr int BG_TILE_BYTES = 256 * BG_BK * 2;  // one operand tile: 32 KiB
 
 __device__ __forceinline__ int bg_swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
-__global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restrict__ A,
-                                                         const uint16_t *__restrict__ W, uint16_t *__restrict__ out,
+template <bool W8>
+__global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restrict__ A, const void *__restrict__ W,
+                                                         const float *__restrict__ wscale, uint16_t *__restrict__ out,
                                                          const uint16_t *__restrict__ res, float *__restrict__ part,
                                                          int M, int N, int K, int epi, int tiles_m, int tiles_n,
                                                          int per_xcd, int kt_per) {
@@ -390,8 +416,9 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
   const int split = blockIdx.y;
   const int kt0 = split * kt_per, kt1 = min(K / BG_BK, kt0 + kt_per);
 
+  constexpr uint32_t WES = W8 ? 1u : 2u;  // bytes per W element
   const buf_rsrc_t ra = make_rsrc(A, (int)min((size_t)M * K * 2, (size_t)0x7FFFFFFF));
-  const buf_rsrc_t rw = make_rsrc(W, (int)min((size_t)N * K * 2, (size_t)0x7FFFFFFF));
+  const buf_rsrc_t rw = make_rsrc(W, (int)min((size_t)N * K * WES, (size_t)0x7FFFFFFF));
   // DMA: wave w moves LDS rows [32 w, 32 w + 32) of both tiles, 8 rows
   // (1 KiB) per instruction; lane l fills row 8 i + l / 8, physical chunk
   // l % 8 with logical chunk bg_swz(row, l % 8).  Rows outside the operands
@@ -404,18 +431,31 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
     const int m = m0 + row;
     aoff[i] = m < M ? ((uint32_t)m * (uint32_t)K + (uint32_t)(c * 8)) * 2u : 0x80000000u;
     const int wr = w_row_of(n0 + row, N, epi);
-    woff[i] = wr >= 0 ? ((uint32_t)wr * (uint32_t)K + (uint32_t)(c * 8)) * 2u : 0x80000000u;
+    woff[i] = wr >= 0 ? ((uint32_t)wr * (uint32_t)K + (uint32_t)(c * 8)) * WES : 0x80000000u;
   }
   typedef __attribute__((address_space(3))) void lds_void;
+  // 8-bit weights come through registers: lane l of wave w holds the 8
+  // codes of row 32 w + 8 i + l / 8, logical chunk bg_swz(row, l % 8) (the
+  // same positions the DMA fills), converted to bf16 when written to LDS
+  u32x2_t wcodes[4];
   auto dma = [&](int kt, int buf) {
     uint8_t *base = bg_lds + buf * 2 * BG_TILE_BYTES + wave * 32 * 128;
     const uint32_t kb = (uint32_t)kt * BG_BK * 2u;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void *)(base + i * 1024), 16, aoff[i] + kb, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void *)(base + BG_TILE_BYTES + i * 1024), 16, woff[i] + kb,
-                                               0, 0, 0);
+      if constexpr (W8)
+        wcodes[i] = buf_ld_u32x2<0>(rw, (int)(woff[i] == 0x80000000u ? woff[i] : woff[i] + kb / 2u));
+      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_void *)(base + BG_TILE_BYTES + i * 1024), 16, woff[i] + kb,
+                                                 0, 0, 0);
     }
+  };
+  auto wstore = [&](int buf) {  // 8-bit weights: the converted W tile of the last dma into LDS
+    uint8_t *base = bg_lds + buf * 2 * BG_TILE_BYTES + BG_TILE_BYTES + wave * 32 * 128;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<u32x4_t *>(base + i * 1024 + lane * 16) = e4m3x8_to_bf16x8(wcodes[i]);
   };
 
   f32x4_t acc[4][8];  // [W block jn][A block im]: rows n, cols m
@@ -426,6 +466,7 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
 
   const int lr = lane & 15, lg = lane >> 4;
   dma(kt0, 0);
+  if constexpr (W8) wstore(0);
   __syncthreads();
   for (int kt = kt0; kt < kt1; ++kt) {
     const int buf = (kt - kt0) & 1;
@@ -450,7 +491,20 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
 #pragma unroll
         for (int im = 0; im < 8; ++im) acc[jn][im] = mfma16x16x32(wf[jn], af[im], acc[jn][im]);
     }
+    // the other buffer was last read in the previous step, before its barrier
+    if constexpr (W8)
+      if (kt + 1 < kt1) wstore(buf ^ 1);
     __syncthreads();
+  }
+  if constexpr (W8) {  // the rows' scales, before any epilogue or partial
+#pragma unroll
+    for (int jn = 0; jn < 4; ++jn) {
+      const int n = n0 + wn * 64 + jn * 16 + lg * 4;
+      if (n < logical_cols(N, epi)) {
+#pragma unroll
+        for (int im = 0; im < 8; ++im) acc[jn][im] = row_scaled(acc[jn][im], wscale, n, N, epi);
+      }
+    }
   }
 
   // epilogue: lane holds out[m][n .. n+3] with m = m0 + wm*128 + 16 im + lr,
@@ -538,7 +592,7 @@ static int skinny_splits(int M, int N, int K) {
   return splits;
 }
 
-GemmPlan plan_gemm(int M, int N, int K, int epi) {
+GemmPlan plan_gemm(int M, int N, int K, int epi, bool w8) {
   GemmPlan p{};
   const int ncols = logical_cols(N, epi);
   // the big kernel addresses W through a 32-bit buffer range; A is cut into
@@ -561,22 +615,26 @@ GemmPlan plan_gemm(int M, int N, int K, int epi) {
     p.splits = (nk + p.kt_per - 1) / p.kt_per;
     p.ws_bytes = p.splits > 1 ? (size_t)p.splits * M * ncols * sizeof(float) : 0;
     return p;
-  } else if (M <= kSkinnyMaxRows) {
+  }
+  // the skinny kernel addresses both operands through 32-bit buffer ranges
+  const bool sk_fits = (size_t)N * K * (w8 ? 1 : 2) < ((size_t)1 << 31) && (size_t)M * K * 2 < ((size_t)1 << 31);
+  if ((M <= kSkinnyMaxRows || w8) && sk_fits) {  // (the tiled kernel reads bf16 weights only)
     p.kind = 0;
     p.splits = skinny_splits(M, ncols, K);
     p.ws_bytes = p.splits > 1 ? (size_t)p.splits * M * ncols * sizeof(float) : 0;
     return p;
-  } else {
-    p.kind = 1;
   }
+  p.kind = w8 ? -1 : 1;  // -1: no kernel here addresses 8-bit operands this large
   p.splits = 1;
   p.ws_bytes = 0;
   return p;
 }
 
-hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, uint16_t *out, const uint16_t *res,
-                       int M, int N, int K, int epi, void *ws, hipStream_t st) {
+hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, const float *wscale, uint16_t *out,
+                       const uint16_t *res, int M, int N, int K, int epi, void *ws, hipStream_t st) {
   if (M <= 0) return hipSuccess;
+  const bool w8 = wscale != nullptr;
+  if (p.kind < 0 || (w8 && p.kind == 1)) return hipErrorInvalidValue;
   const int ncols = logical_cols(N, epi);
   if (p.kind == 0) {
     const int nsteps = (K + 31) / 32;
@@ -587,8 +645,12 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, 
     const int tiles = ((ncols + SK_BN - 1) / SK_BN) * mt;
     const int per_xcd = (tiles + 7) / 8;
     dim3 grid(8 * per_xcd, splits);
-    hipLaunchKernelGGL(k_gemm_skinny, grid, dim3(256), SK_LDS, st, A, W, out, res, part, M, N, K, epi, per, tiles, mt,
-                       per_xcd);
+    if (w8)
+      hipLaunchKernelGGL(k_gemm_skinny<true>, grid, dim3(256), SK_LDS, st, A, W, wscale, out, res, part, M, N, K, epi,
+                         per, tiles, mt, per_xcd);
+    else
+      hipLaunchKernelGGL(k_gemm_skinny<false>, grid, dim3(256), SK_LDS, st, A, W, wscale, out, res, part, M, N, K,
+                         epi, per, tiles, mt, per_xcd);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
     return launch_splitk_epilogue(part, splits, out, res, M, N, epi, st);
@@ -598,8 +660,12 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, 
       const int tm = (M + BG_BM - 1) / BG_BM, tn = (ncols + BG_BN - 1) / BG_BN;
       const int per_xcd = (tm * tn + 7) / 8;
       float *part = reinterpret_cast<float *>(ws);
-      hipLaunchKernelGGL(k_gemm_big, dim3(8 * per_xcd, p.splits), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A, W, out,
-                         res, part, M, N, K, epi, tm, tn, per_xcd, p.kt_per);
+      if (w8)
+        hipLaunchKernelGGL(k_gemm_big<true>, dim3(8 * per_xcd, p.splits), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A,
+                           W, wscale, out, res, part, M, N, K, epi, tm, tn, per_xcd, p.kt_per);
+      else
+        hipLaunchKernelGGL(k_gemm_big<false>, dim3(8 * per_xcd, p.splits), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A,
+                           W, wscale, out, res, part, M, N, K, epi, tm, tn, per_xcd, p.kt_per);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       return launch_splitk_epilogue(part, p.splits, out, res, M, N, epi, st);
@@ -612,16 +678,22 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const uint16_t *W, 
       const int mc = M - m0 < chunk ? M - m0 : chunk;
       const int tm = (mc + BG_BM - 1) / BG_BM, tn = (ncols + BG_BN - 1) / BG_BN;
       const int per_xcd = (tm * tn + 7) / 8;
-      hipLaunchKernelGGL(k_gemm_big, dim3(8 * per_xcd), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A + (size_t)m0 * K, W,
-                         out + (size_t)m0 * out_cols, res ? res + (size_t)m0 * N : nullptr, nullptr, mc, N, K, epi,
-                         tm, tn, per_xcd, K / BG_BK);
+      if (w8)
+        hipLaunchKernelGGL(k_gemm_big<true>, dim3(8 * per_xcd), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st,
+                           A + (size_t)m0 * K, W, wscale, out + (size_t)m0 * out_cols,
+                           res ? res + (size_t)m0 * N : nullptr, nullptr, mc, N, K, epi, tm, tn, per_xcd, K / BG_BK);
+      else
+        hipLaunchKernelGGL(k_gemm_big<false>, dim3(8 * per_xcd), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st,
+                           A + (size_t)m0 * K, W, wscale, out + (size_t)m0 * out_cols,
+                           res ? res + (size_t)m0 * N : nullptr, nullptr, mc, N, K, epi, tm, tn, per_xcd, K / BG_BK);
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
     }
     return hipSuccess;
   }
   const int tiles_m = (M + TL_BM - 1) / TL_BM, tiles_n = (ncols + TL_BN - 1) / TL_BN;
-  hipLaunchKernelGGL(k_gemm_tiled, dim3(tiles_m * tiles_n), dim3(256), 0, st, A, W, out, res, M, N, K, epi, tiles_m,
+  hipLaunchKernelGGL(k_gemm_tiled, dim3(tiles_m * tiles_n), dim3(256), 0, st, A,
+                     static_cast<const uint16_t *>(W), out, res, M, N, K, epi, tiles_m,
                      tiles_n);
   return hipGetLastError();
 }

@@ -298,6 +298,24 @@ def make_block_tables(batch: Batch, spare_pages: int, seed: int, page: int = PAG
     return bt, pool
 
 
+def _fp8_codes(g, rows: int, cols: int, device) -> torch.Tensor:
+    """Random E4M3 codes: random sign, exponent field 4..9, random mantissa."""
+    w = torch.empty(rows, cols, dtype=torch.uint8, device=device)
+    step = max(1, (1 << 26) // cols)
+    for r0 in range(0, rows, step):
+        r1 = min(rows, r0 + step)
+        n = (r1 - r0, cols)
+        sign = torch.randint(0, 2, n, generator=g, device=device) << 7
+        ex = torch.randint(4, 10, n, generator=g, device=device) << 3
+        man = torch.randint(0, 8, n, generator=g, device=device)
+        w[r0:r1] = (sign | ex | man).to(torch.uint8)
+    return w
+
+
+def _row_scales(g, rows: int, proj_std: float, device) -> torch.Tensor:
+    return (proj_std / 2.3) * (0.5 + torch.rand(rows, generator=g, device=device))
+
+
 def make_weights_fp8(shape: LayerShape, seed: Optional[int] = None, device="cpu",
                      proj_std: float = 0.02) -> dict:
     """Layer weights with the four projections as 8-bit E4M3 codes (uint8,
@@ -316,19 +334,10 @@ def make_weights_fp8(shape: LayerShape, seed: Optional[int] = None, device="cpu"
     f = shape.ffn
 
     def codes(rows, cols):
-        w = torch.empty(rows, cols, dtype=torch.uint8, device=device)
-        step = max(1, (1 << 26) // cols)
-        for r0 in range(0, rows, step):
-            r1 = min(rows, r0 + step)
-            n = (r1 - r0, cols)
-            sign = torch.randint(0, 2, n, generator=g, device=device) << 7
-            ex = torch.randint(4, 10, n, generator=g, device=device) << 3
-            man = torch.randint(0, 8, n, generator=g, device=device)
-            w[r0:r1] = (sign | ex | man).to(torch.uint8)
-        return w
+        return _fp8_codes(g, rows, cols, device)
 
     def scales(rows):
-        return (proj_std / 2.3) * (0.5 + torch.rand(rows, generator=g, device=device))
+        return _row_scales(g, rows, proj_std, device)
 
     def gain():
         return (1.0 + 0.1 * torch.randn(d, generator=g, device=device)).to(torch.bfloat16)
@@ -341,6 +350,13 @@ def make_weights_fp8(shape: LayerShape, seed: Optional[int] = None, device="cpu"
         "w_gate_up": codes(2 * f, d), "s_gate_up": scales(2 * f),
         "w_down": codes(d, f), "s_down": scales(d),
     }
+
+
+def make_fp8_matrix(rows: int, cols: int, seed: int, device="cpu", proj_std: float = 0.02):
+    """One [rows, cols] weight matrix as (uint8 E4M3 codes, float32 row
+    scales), drawn as the projections of make_weights_fp8 are."""
+    g = _gen(device, seed)
+    return _fp8_codes(g, rows, cols, device), _row_scales(g, rows, proj_std, device)
 
 
 def weight_arrays(w: dict) -> dict:
