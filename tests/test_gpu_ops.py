@@ -32,7 +32,10 @@ def _bf(shape, seed, scale=1.0):
                                    (1024, 8192, 1024), (1000, 8200, 512), (2048, 6144, 4096),
                                    # 256 x 256 tiles splitting K (few tiles): uneven splits, ragged M, N and F,
                                    # the 70B-shaped down projection
-                                   (300, 1032, 2048), (256, 8192, 28672)])
+                                   (300, 1032, 2048), (256, 8192, 28672),
+                                   # decode-sized row counts: one K stage, ragged N and F, split K, the
+                                   # 8B-shaped down projection
+                                   (63, 4104, 128), (17, 1032, 384), (1, 8200, 1152), (64, 4096, 14336)])
 @pytest.mark.parametrize("epi", ["store", "residual", "silu_mul"])
 def test_gemm(M, N, K, epi):
     A = _bf((M, K), 1)

@@ -59,7 +59,9 @@ def _reference_product(M, N, K):
     # 256 x 256 tiles: aligned, ragged in M, N and F
     (1024, 8192, 1024), (1000, 8200, 512), (2048, 6144, 4096),
     # 256 x 256 tiles splitting K: uneven splits and ragged shapes, the 70B-shaped down projection
-    (300, 1032, 2048), (256, 8192, 28672)])
+    (300, 1032, 2048), (256, 8192, 28672),
+    # decode-sized row counts: one K stage, ragged N and F, split K, the 8B-shaped down projection
+    (63, 4104, 256), (17, 1032, 768), (5, 520, 512), (64, 4096, 14336)])
 @pytest.mark.parametrize("epi", ["store", "residual", "silu_mul"])
 def test_gemm_w8(M, N, K, epi):
     A, codes, scales, prod = _reference_product(M, N, K)
