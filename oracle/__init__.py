@@ -20,3 +20,4 @@ from .layer import (  # noqa: F401
     LayerCfg,
 )
 from . import fp8  # noqa: F401,E402  (E4M3 cache codes)
+from . import moe  # noqa: F401,E402  (mixture-of-experts block)
