@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="decode8b",
                     choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "decode70b", "stack70b", "policy8b",
-                             "long8b", "copy"])
+                             "long8b", "moe30b", "copy"])
     ap.add_argument("--calib-out", default=None, help="policy8b: write the calibrated step-cost profile here")
     ap.add_argument("--layers", type=int, default=80, help="decoder layers of the stack70b model step")
     ap.add_argument("--stack-r", default="0.2,0.5,0.8", help="decode shares of the stack70b mixed steps")
@@ -506,6 +506,57 @@ def long8b(args, dev):
     return out
 
 
+def moe30b(args, dev):
+    """The Qwen3-30B-A3B mixture-of-experts feed-forward block (128 experts,
+    8 per token, expert width 768, hidden 2048) on a 64-token decode batch
+    (weight streaming: most experts are hit, each read once) and an
+    8192-token prefill batch (about 512 rows per expert, MFMA work)."""
+    import torch
+
+    from paper_2606_00516_amd import binding as B
+    from paper_2606_00516_amd import inputs as gen
+    shape = gen.MOE30B
+    E, d, k, F = shape.n_experts, shape.hidden, shape.top_k, shape.expert_ffn
+    w = gen.make_moe_weights(shape, device=dev)
+    pts = []
+    for name, T in (("decode", 64), ("prefill", 8192)):
+        g = torch.Generator(device=dev).manual_seed(11 + T)
+        b = torch.randn(T, d, generator=g, device=dev).to(torch.bfloat16)
+        res = torch.randn(T, d, generator=g, device=dev).to(torch.bfloat16)
+        y = torch.empty_like(b)
+        ws = B.alloc_workspace(int(B.lib().eb_op_moe_ffn_workspace_bytes(T, d, E, k, F)), dev)
+        _, ids, _ = B.eb_op_moe_ffn(b, w["w_router"], w["w_gate_up"], w["w_down"], k, residual=res, out=y, ws=ws,
+                                    return_routing=True)
+        torch.cuda.synchronize()
+        hit = int(torch.unique(ids).numel())
+        call = lambda: B.eb_op_moe_ffn(b, w["w_router"], w["w_gate_up"], w["w_down"], k, residual=res,  # noqa
+                                       out=y, ws=ws)
+        for _ in range(args.warmup):
+            call()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(args.steps):
+            call()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        # algorithmic work: the router and every expert hit read once, the
+        # activations in and out; products over the T k assignments
+        wbytes = E * d * 2 + hit * shape.expert_bytes()
+        act = 3 * T * d * 2
+        flops = 2 * T * E * d + 2 * T * k * 3 * F * d
+        pt = {"point": name, "tokens": T, "experts_hit": hit, "ms": round(ms, 5),
+              "tokens_per_s": round(T / (ms / 1e3), 1), "weight_bytes": wbytes,
+              "hbm_gbps": round((wbytes + act) / (ms / 1e3) / 1e9, 1),
+              "tflops": round(flops / (ms / 1e3) / 1e12, 1)}
+        pts.append(pt)
+        print(f"# moe {name}: {ms:.3f} ms, {hit} experts hit, {pt['hbm_gbps']} GB/s, {pt['tflops']} TFLOP/s",
+              file=sys.stderr, flush=True)
+        del b, res, y, ws
+    return pts
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -586,6 +637,29 @@ def main():
                                        f"{args.dec_ctx}; decisions and simulated EB / MB / EB+ for the paper's "
                                        f"mixes", "kv_cache": KV_LABEL[args.kv], "parallelism": "single-gpu"},
                 **out, "wall_s": round(time.perf_counter() - t0, 1)}
+        js = json.dumps(line)
+        print(js)
+        if args.json_out:
+            with open(args.json_out, "w") as f:
+                f.write(js + "\n")
+        return
+
+    if args.workload == "moe30b":
+        t0 = time.perf_counter()
+        pts = moe30b(args, dev)
+        dec, pre = pts
+        line = {"metric": METRIC, "value": dec["hbm_gbps"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+                "warmup": args.warmup, "ms_per_step": dec["ms"], "higher_is_better": True, "scaling": "weak",
+                "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+                "config": {"workload": "qwen3-30b-a3b MoE feed-forward block (E=128, k=8, F=768, d=2048): decode "
+                                       "64 tokens, prefill 8192 tokens", "parallelism": "single-gpu"},
+                "roofline": {"kernel": "eb_op_moe_ffn (router, plan, grouped gate/up and down GEMMs, combine) on "
+                                       "the decode batch", "bound": "hbm", "achieved": dec["hbm_gbps"],
+                             "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                             "frac": round(dec["hbm_gbps"] / HBM_PEAK_GBPS, 4), "traffic": None},
+                "prefill_roofline": {"bound": "mfma", "achieved": pre["tflops"], "peak": BF16_PEAK_TFLOPS,
+                                     "unit": "TFLOP/s", "frac": round(pre["tflops"] / BF16_PEAK_TFLOPS, 4)},
+                "points": pts, "wall_s": round(time.perf_counter() - t0, 1)}
         js = json.dumps(line)
         print(js)
         if args.json_out:

@@ -244,6 +244,30 @@ eb_status eb_op_gemm(const void *A, const void *W, void *out, const void *residu
 eb_status eb_op_gemm_w8(const void *A, const void *W, const float *w_scale, void *out, const void *residual,
                         int32_t M, int32_t N, int32_t K, eb_epilogue epi, void *ws, size_t ws_bytes, void *stream);
 
+/* Mixture-of-experts feed-forward block (the paper's MoE model, Qwen3-30B-A3B,
+ * Sec. 4.1 "Models"; its routing and expert work dominate that model's step,
+ * App. A.2 "Kernel breakdown"), in place of the dense SwiGLU:
+ *   logits[t] = b[t] W_r^T, fp32 sums of the bf16 products, kept in fp32
+ *   S(t)      = the top_k largest logits of token t (equal logits: lower expert)
+ *   w[t, e]   = exp(logits[t, e] - max_t) / (sum of the same over S(t) when
+ *               renormalize, over all E experts otherwise), e in S(t)
+ *   m         = SiLU(b[t] Wg_e^T) * (b[t] Wu_e^T), rounded to bf16
+ *   out[t]    = bf16(residual[t] + sum_{e in S(t)} w[t, e] * (m Wd_e^T))
+ * b bf16 [T, d] (the block's normalised input), residual bf16 [T, d] or NULL,
+ * w_router bf16 [E, d], w_gate_up bf16 [E, 2F, d] (per expert: F gate rows,
+ * then F up rows), w_down bf16 [E, d, F], out bf16 [T, d]; all device memory,
+ * caller-owned.  ids_out (int32 [T, top_k]) and weights_out (fp32 [T, top_k]),
+ * when not NULL, receive each token's experts (largest logit first) and
+ * weights.  Requires d % 32 == 0, F % 8 == 0, E % 16 == 0 and E <= 256,
+ * 1 <= top_k <= min(E, 64) (EB_ERR_CONFIG); operands within the kernels'
+ * 32-bit ranges (EB_ERR_LIMITS).  NaN inputs are the caller's to avoid.
+ * ws: device scratch of at least eb_op_moe_ffn_workspace_bytes(...). */
+size_t eb_op_moe_ffn_workspace_bytes(int32_t T, int32_t d, int32_t E, int32_t top_k, int32_t F);
+eb_status eb_op_moe_ffn(const void *b, const void *residual, const void *w_router, const void *w_gate_up,
+                        const void *w_down, int32_t T, int32_t d, int32_t E, int32_t top_k, int32_t F,
+                        int32_t renormalize, void *out, int32_t *ids_out, float *weights_out, void *ws,
+                        size_t ws_bytes, void *stream);
+
 /* RoPE on the q and k heads of qkv (bf16 [num_tokens, (n_q + 2 n_kv) head_dim],
  * the QKV projection output) at pos = c_i + j; q is rotated in place, the
  * rotated k and the v heads are written to the cache. */

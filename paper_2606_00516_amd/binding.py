@@ -27,7 +27,7 @@ EPILOGUES = {"store": 0, "residual": 1, "silu_mul": 2}
 # every symbol include/eb_layer.h declares
 SYMBOLS = ("eb_create", "eb_destroy", "eb_workspace_bytes", "eb_layer_step_decode", "eb_layer_step_prefill",
            "eb_layer_step_mixed", "eb_validate", "eb_status_str", "eb_last_error", "eb_op_rmsnorm",
-           "eb_op_gemm_workspace_bytes", "eb_op_gemm", "eb_op_gemm_w8", "eb_op_rope_kv_append", "eb_op_attention",
+           "eb_op_gemm_workspace_bytes", "eb_op_gemm", "eb_op_gemm_w8", "eb_op_moe_ffn_workspace_bytes", "eb_op_moe_ffn", "eb_op_rope_kv_append", "eb_op_attention",
            "eb_op_gather_kv", "eb_profile", "eb_profile_read", "eb_profile_stage_name", "eb_stack_workspace_bytes",
            "eb_stack_step")
 
@@ -90,6 +90,8 @@ def lib() -> ctypes.CDLL:
         "eb_op_gemm_workspace_bytes": (SZ, [I32, I32, I32]),
         "eb_op_gemm": (I32, [VP, VP, VP, VP, I32, I32, I32, I32, VP, SZ, VP]),
         "eb_op_gemm_w8": (I32, [VP, VP, VP, VP, VP, I32, I32, I32, I32, VP, SZ, VP]),
+        "eb_op_moe_ffn_workspace_bytes": (SZ, [I32, I32, I32, I32, I32]),
+        "eb_op_moe_ffn": (I32, [VP, VP, VP, VP, VP, I32, I32, I32, I32, I32, I32, VP, VP, VP, VP, SZ, VP]),
         "eb_op_rope_kv_append": (I32, [VP, VP, P(KvCache), P(Batch), VP, SZ, VP]),
         "eb_op_attention": (I32, [VP, VP, P(KvCache), P(Batch), VP, VP, SZ, I32, VP]),
         "eb_op_gather_kv": (I32, [VP, P(KvCache), P(Batch), VP, VP, VP, SZ, VP]),
@@ -318,6 +320,32 @@ def eb_op_gemm_w8(A: torch.Tensor, W: torch.Tensor, w_scale: torch.Tensor, epilo
     _check(lib().eb_op_gemm_w8(_ptr(A), _ptr(W), _ptr(w_scale), _ptr(out), _ptr(residual), M, N, K,
                                EPILOGUES[epilogue], _ptr(ws), ws.numel(), _stream(stream)))
     return out
+
+
+def eb_op_moe_ffn(b: torch.Tensor, w_router: torch.Tensor, w_gate_up: torch.Tensor, w_down: torch.Tensor,
+                  top_k: int, residual: Optional[torch.Tensor] = None, renormalize: bool = True,
+                  out: Optional[torch.Tensor] = None, return_routing: bool = False,
+                  ws: Optional[torch.Tensor] = None, stream=None):
+    """MoE feed-forward block: b [T, d], w_router [E, d], w_gate_up [E, 2F, d],
+    w_down [E, d, F], all bf16; returns out [T, d] (and the int32 expert ids
+    and fp32 weights [T, top_k] with ``return_routing``)."""
+    for t in (b, w_router, w_gate_up, w_down) + ((residual,) if residual is not None else ()):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous():
+            raise TypeError("MoE operands must be contiguous bf16")
+    T, d = b.shape
+    E = w_router.shape[0]
+    F = w_gate_up.shape[1] // 2
+    if w_router.shape != (E, d) or w_gate_up.shape != (E, 2 * F, d) or w_down.shape != (E, d, F):
+        raise ValueError("MoE weight shapes do not match")
+    out = torch.empty(T, d, dtype=torch.bfloat16, device=b.device) if out is None else out
+    ids = torch.empty(T, top_k, dtype=torch.int32, device=b.device) if return_routing else None
+    wts = torch.empty(T, top_k, dtype=torch.float32, device=b.device) if return_routing else None
+    if ws is None:
+        ws = alloc_workspace(int(lib().eb_op_moe_ffn_workspace_bytes(T, d, E, top_k, F)), b.device)
+    _check(lib().eb_op_moe_ffn(_ptr(b), _ptr(residual), _ptr(w_router), _ptr(w_gate_up), _ptr(w_down), T, d, E,
+                               int(top_k), F, 1 if renormalize else 0, _ptr(out), _ptr(ids), _ptr(wts), _ptr(ws),
+                               ws.numel(), _stream(stream)))
+    return (out, ids, wts) if return_routing else out
 
 
 def _op_ws(h, hb, mode="mixed", device="cuda"):

@@ -593,6 +593,96 @@ eb_status eb_op_gemm_w8(const void *A, const void *W, const float *w_scale, void
   return op_gemm(A, W, w_scale, out, residual, M, N, K, epi, ws, ws_bytes, stream);
 }
 
+namespace {
+// Workspace of the MoE block: routing, the sorted order and tiles, the
+// experts' SwiGLU outputs (bf16) and down products (fp32), 256-byte aligned.
+struct MoeLayout {
+  size_t logits, ids, wts, offsets, sorted_tok, pos_of, tiles, n_tiles, m, y, total;
+  int max_tiles;
+};
+MoeLayout moe_layout(int T, int d, int E, int k, int F) {
+  MoeLayout L{};
+  const size_t P = (size_t)T * k;
+  L.max_tiles = (int)((P + 63) / 64) + E;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.logits = take((size_t)T * E * 4);
+  L.ids = take(P * 4);
+  L.wts = take(P * 4);
+  L.offsets = take((size_t)(E + 1) * 4);
+  L.sorted_tok = take(P * 4);
+  L.pos_of = take(P * 4);
+  L.tiles = take((size_t)3 * L.max_tiles * 4);
+  L.n_tiles = take(4);
+  L.m = take(P * F * 2);
+  L.y = take(P * d * 4);
+  L.total = off;
+  return L;
+}
+eb_status check_moe(int T, int d, int E, int k, int F) {
+  if (T < 0 || d <= 0 || E <= 0 || k <= 0 || F <= 0) return fail(EB_ERR_CONFIG, "MoE sizes must be positive");
+  if (d % 32) return fail(EB_ERR_CONFIG, "MoE hidden size must be a multiple of 32");
+  if (F % 8) return fail(EB_ERR_CONFIG, "MoE expert width must be a multiple of 8");
+  if (E % 16 || E > 256) return fail(EB_ERR_CONFIG, "MoE expert count must be a multiple of 16, at most 256");
+  if (k > E || k > 64) return fail(EB_ERR_CONFIG, "MoE top_k must be at most the expert count and 64");
+  const size_t P = (size_t)T * k;
+  if ((size_t)T * d * 2 >= ((size_t)1 << 31) || P * F * 2 >= ((size_t)1 << 31) ||
+      (size_t)2 * F * d * 2 >= ((size_t)1 << 31) || P >= ((size_t)1 << 30))
+    return fail(EB_ERR_LIMITS, "MoE operands exceed the kernels' 32-bit ranges");
+  return EB_OK;
+}
+}  // namespace
+
+size_t eb_op_moe_ffn_workspace_bytes(int32_t T, int32_t d, int32_t E, int32_t top_k, int32_t F) {
+  if (T <= 0 || d <= 0 || E <= 0 || top_k <= 0 || F <= 0) return 0;
+  return moe_layout(T, d, E, top_k, F).total;
+}
+
+eb_status eb_op_moe_ffn(const void *b, const void *residual, const void *w_router, const void *w_gate_up,
+                        const void *w_down, int32_t T, int32_t d, int32_t E, int32_t top_k, int32_t F,
+                        int32_t renormalize, void *out, int32_t *ids_out, float *weights_out, void *ws,
+                        size_t ws_bytes, void *stream) {
+  eb_status s = check_moe(T, d, E, top_k, F);
+  if (s != EB_OK) return s;
+  if (T == 0) return EB_OK;
+  if (!b || !w_router || !w_gate_up || !w_down || !out) return fail(EB_ERR_NULL, "an input or out is NULL");
+  const MoeLayout L = moe_layout(T, d, E, top_k, F);
+  s = check_ws(ws, ws_bytes, L.total);
+  if (s != EB_OK) return s;
+  char *base = static_cast<char *>(ws);
+  float *logits = reinterpret_cast<float *>(base + L.logits);
+  int32_t *ids = reinterpret_cast<int32_t *>(base + L.ids);
+  float *wts = reinterpret_cast<float *>(base + L.wts);
+  int32_t *offsets = reinterpret_cast<int32_t *>(base + L.offsets);
+  int32_t *sorted_tok = reinterpret_cast<int32_t *>(base + L.sorted_tok);
+  int32_t *pos_of = reinterpret_cast<int32_t *>(base + L.pos_of);
+  int32_t *tiles = reinterpret_cast<int32_t *>(base + L.tiles);
+  int32_t *n_tiles = reinterpret_cast<int32_t *>(base + L.n_tiles);
+  uint16_t *m = reinterpret_cast<uint16_t *>(base + L.m);
+  float *y = reinterpret_cast<float *>(base + L.y);
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const int P = T * top_k;
+  hipError_t e = launch_moe_route(static_cast<const uint16_t *>(b), static_cast<const uint16_t *>(w_router), T, d, E,
+                                  top_k, renormalize ? 1 : 0, logits, ids, wts, st);
+  if (e == hipSuccess) e = launch_moe_plan(ids, P, E, top_k, L.max_tiles, offsets, sorted_tok, pos_of, tiles, n_tiles, st);
+  if (e == hipSuccess)
+    e = launch_gemm_grouped(static_cast<const uint16_t *>(b), T, sorted_tok, static_cast<const uint16_t *>(w_gate_up),
+                            m, false, tiles, n_tiles, L.max_tiles, 2 * F, d, EPI_SILU_MUL, st);
+  if (e == hipSuccess)
+    e = launch_gemm_grouped(m, P, nullptr, static_cast<const uint16_t *>(w_down), y, true, tiles, n_tiles,
+                            L.max_tiles, d, F, EPI_STORE, st);
+  if (e == hipSuccess)
+    e = launch_moe_combine(y, pos_of, wts, static_cast<const uint16_t *>(residual), static_cast<uint16_t *>(out), T, d,
+                           top_k, st);
+  if (e == hipSuccess && ids_out) e = hipMemcpyAsync(ids_out, ids, (size_t)P * 4, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess && weights_out) e = hipMemcpyAsync(weights_out, wts, (size_t)P * 4, hipMemcpyDeviceToDevice, st);
+  return e == hipSuccess ? EB_OK : hip_fail(e, "moe ffn");
+}
+
 eb_status eb_op_rope_kv_append(eb_handle *h, void *qkv, const eb_kv_cache *kv, const eb_batch *batch, void *ws,
                                size_t ws_bytes, void *stream) {
   eb_status s = check_kv(kv);

@@ -89,4 +89,19 @@ GemmPlan plan_gemm(int M, int N, int K, int epi, bool w8 = false);
 hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, const float *wscale, uint16_t *out,
                        const uint16_t *residual, int M, int N, int K, int epi, void *ws, hipStream_t st);
 
+// Mixture-of-experts block.  The grouped GEMM multiplies row tiles of
+// expert-sorted rows (tables [3][max_tiles]: expert, first sorted row, rows;
+// *n_tiles of them in use) by their expert's W ([E][N][K] bf16), gathering A
+// rows through a_rows (null: the sorted row itself); SiLU epilogue to bf16
+// [rows, N / 2], or store to fp32 [rows, N] when f32_out.
+hipError_t launch_gemm_grouped(const uint16_t *A, int a_nrows, const int32_t *a_rows, const uint16_t *W, void *out,
+                               bool f32_out, const int32_t *tiles, const int32_t *n_tiles, int max_tiles, int N, int K,
+                               int epi, hipStream_t st);
+hipError_t launch_moe_route(const uint16_t *b, const uint16_t *wr, int T, int d, int E, int k, int renormalize,
+                            float *logits, int32_t *ids, float *wts, hipStream_t st);
+hipError_t launch_moe_plan(const int32_t *ids, int P, int E, int k, int max_tiles, int32_t *offsets,
+                           int32_t *sorted_tok, int32_t *pos_of, int32_t *tiles, int32_t *n_tiles, hipStream_t st);
+hipError_t launch_moe_combine(const float *y, const int32_t *pos_of, const float *wts, const uint16_t *res,
+                              uint16_t *out, int T, int d, int k, hipStream_t st);
+
 }  // namespace eb

@@ -566,6 +566,139 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
 }
 
 // ===========================================================================
+// grouped: the experts of a mixture-of-experts block
+// ===========================================================================
+// Rows are sorted by expert; a row tile is up to 64 consecutive sorted rows of
+// one expert (tile tables: expert, first sorted row, rows).  Block b takes row
+// tile b / col_tiles and column tile b % col_tiles of that expert's W, so the
+// column tiles of one row tile run side by side and share its A rows, and
+// the row tiles of one expert follow each other and share its W tiles in L2.
+// The main loop is the weight-streaming kernel's: W and A staged through LDS
+// in 128-wide K slices, the 4 waves split the tile's columns (transposed
+// product).  A rows are gathered through a_rows (null: the sorted row
+// itself).  SiLU: bf16 [rows, N / 2]; store: fp32 [rows, N].
+template <bool F32OUT>
+__global__ __launch_bounds__(256) void k_gemm_grouped(const uint16_t *__restrict__ A, int a_nrows,
+                                                      const int32_t *__restrict__ a_rows,
+                                                      const uint16_t *__restrict__ W, void *__restrict__ out,
+                                                      const int32_t *__restrict__ tiles,
+                                                      const int32_t *__restrict__ n_tiles, int max_tiles, int N,
+                                                      int K, int epi, int col_tiles) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t gg_lds[];  // [2][64 W rows + 64 A rows][SK_ROWB]
+  const int rt = blockIdx.x / col_tiles, ct = blockIdx.x % col_tiles;
+  if (rt >= __builtin_amdgcn_readfirstlane(*n_tiles)) return;
+  const int e = __builtin_amdgcn_readfirstlane(tiles[rt]);
+  const int row0 = __builtin_amdgcn_readfirstlane(tiles[max_tiles + rt]);
+  const int rows = __builtin_amdgcn_readfirstlane(tiles[2 * max_tiles + rt]);
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n0 = ct * SK_BN;
+  const int nst = (K + SK_KC - 1) / SK_KC;
+  const uint16_t *We = W + (size_t)e * N * K;
+  const buf_rsrc_t ra = make_rsrc(A, (int)min((size_t)a_nrows * K * 2, (size_t)0x7FFFFFFF));
+  const buf_rsrc_t rw = make_rsrc(We, (int)min((size_t)N * K * 2, (size_t)0x7FFFFFFF));
+
+  // staging as in the weight-streaming kernel: thread t moves 16-byte chunk
+  // t % 16 of tile rows t / 16 + 16 j; rows outside the tile or the operands
+  // and k past K load zeros without memory traffic
+  const int ch = tid & 15, r0 = tid >> 4;
+  uint32_t woff[4], aoff[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int wr = w_row_of(n0 + r0 + 16 * j, N, epi);
+    woff[j] = wr >= 0 ? ((uint32_t)wr * (uint32_t)K + (uint32_t)(ch * 8)) * 2u : 0x80000000u;
+    const int r = r0 + 16 * j;
+    const int ar = r < rows ? (a_rows ? a_rows[row0 + r] : row0 + r) : -1;
+    aoff[j] = ar >= 0 && ar < a_nrows ? ((uint32_t)ar * (uint32_t)K + (uint32_t)(ch * 8)) * 2u : 0x80000000u;
+  }
+  u32x4_t wa[4], aa[4], wb[4], ab[4];
+  auto gload = [&](int s, u32x4_t (&wr)[4], u32x4_t (&ar)[4]) {
+    const int k = s * SK_KC + ch * 8;
+    const bool ok = s < nst && k < K;
+    const uint32_t kb = (uint32_t)(s * SK_KC) * 2u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      wr[j] = buf_ld_u32x4<kAuxNT>(rw, (int)(ok ? woff[j] + kb : 0x80000000u));
+      ar[j] = buf_ld_u32x4<0>(ra, (int)(ok ? aoff[j] + kb : 0x80000000u));
+    }
+  };
+  auto swrite = [&](int buf, const u32x4_t (&wr)[4], const u32x4_t (&ar)[4]) {
+    uint8_t *b = gg_lds + buf * (SK_BN + SK_BM) * SK_ROWB;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      *reinterpret_cast<u32x4_t *>(b + (r0 + 16 * j) * SK_ROWB + ch * 16) = wr[j];
+      *reinterpret_cast<u32x4_t *>(b + (SK_BN + r0 + 16 * j) * SK_ROWB + ch * 16) = ar[j];
+    }
+  };
+  f32x4_t acc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int lr = lane & 15, lg = lane >> 4;
+  const int my_wrow = sk_col(wave, lr);
+  auto compute = [&](int buf) {
+    const uint8_t *b = gg_lds + buf * (SK_BN + SK_BM) * SK_ROWB;
+#pragma unroll
+    for (int ks = 0; ks < SK_KC / 32; ++ks) {
+      const u32x4_t wf = *reinterpret_cast<const u32x4_t *>(b + my_wrow * SK_ROWB + (ks * 4 + lg) * 16);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const u32x4_t af = *reinterpret_cast<const u32x4_t *>(b + (SK_BN + i * 16 + lr) * SK_ROWB + (ks * 4 + lg) * 16);
+        acc[i] = mfma16x16x32(wf, af, acc[i]);
+      }
+    }
+  };
+  gload(0, wa, aa);
+  swrite(0, wa, aa);
+  gload(1, wa, aa);
+  gload(2, wb, ab);
+  __syncthreads();
+  for (int st = 0; st < nst; st += 2) {
+    compute(0);
+    swrite(1, wa, aa);
+    gload(st + 3, wa, aa);
+    __syncthreads();
+    if (st + 1 >= nst) break;
+    compute(1);
+    swrite(0, wb, ab);
+    gload(st + 4, wb, ab);
+    __syncthreads();
+  }
+
+  // lane: tile rows 16 i + lr, logical columns c .. c + 3, c = sk_col(wave, 4 lg)
+  const int c = sk_col(wave, 4 * lg);
+  if (epi == EPI_SILU_MUL) {
+    const int F = N >> 1;
+    const int f = (n0 >> 1) + 8 * wave + 4 * lg;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f32x4_t u;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) u[q] = shfl_xor_f32(acc[i][q], 32);
+      const int m = i * 16 + lr;
+      if (!F32OUT && lg < 2 && m < rows && f < F) {
+        const u32x2_t w = {pack_bf16x2(silu_f(acc[i][0]) * u[0], silu_f(acc[i][1]) * u[1]),
+                           pack_bf16x2(silu_f(acc[i][2]) * u[2], silu_f(acc[i][3]) * u[3])};
+        *reinterpret_cast<u32x2_t *>(static_cast<uint16_t *>(out) + (size_t)(row0 + m) * F + f) = w;
+      }
+    }
+    return;
+  }
+  const int n = n0 + c;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int m = i * 16 + lr;
+    if (m < rows && n < N) {
+      if constexpr (F32OUT)
+        *reinterpret_cast<f32x4_t *>(static_cast<float *>(out) + (size_t)(row0 + m) * N + n) = acc[i];
+      else
+        *reinterpret_cast<u32x2_t *>(static_cast<uint16_t *>(out) + (size_t)(row0 + m) * N + n) =
+            u32x2_t{pack_bf16x2(acc[i][0], acc[i][1]), pack_bf16x2(acc[i][2], acc[i][3])};
+    }
+  }
+}
+
+// ===========================================================================
 // planning and launch
 // ===========================================================================
 // Row counts up to this use the skinny kernel (weight streaming: the row
@@ -695,6 +828,21 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, cons
   hipLaunchKernelGGL(k_gemm_tiled, dim3(tiles_m * tiles_n), dim3(256), 0, st, A,
                      static_cast<const uint16_t *>(W), out, res, M, N, K, epi, tiles_m,
                      tiles_n);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_grouped(const uint16_t *A, int a_nrows, const int32_t *a_rows, const uint16_t *W, void *out,
+                               bool f32_out, const int32_t *tiles, const int32_t *n_tiles, int max_tiles, int N, int K,
+                               int epi, hipStream_t st) {
+  if (max_tiles <= 0) return hipSuccess;
+  const int col_tiles = (logical_cols(N, epi) + SK_BN - 1) / SK_BN;
+  const dim3 grid((unsigned)max_tiles * (unsigned)col_tiles);
+  if (f32_out)
+    hipLaunchKernelGGL(k_gemm_grouped<true>, grid, dim3(256), SK_LDS, st, A, a_nrows, a_rows, W, out, tiles, n_tiles,
+                       max_tiles, N, K, epi, col_tiles);
+  else
+    hipLaunchKernelGGL(k_gemm_grouped<false>, grid, dim3(256), SK_LDS, st, A, a_nrows, a_rows, W, out, tiles,
+                       n_tiles, max_tiles, N, K, epi, col_tiles);
   return hipGetLastError();
 }
 

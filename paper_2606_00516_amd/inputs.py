@@ -359,6 +359,43 @@ def make_fp8_matrix(rows: int, cols: int, seed: int, device="cpu", proj_std: flo
     return _fp8_codes(g, rows, cols, device), _row_scales(g, rows, proj_std, device)
 
 
+@dataclasses.dataclass(frozen=True)
+class MoeShape:
+    name: str
+    hidden: int
+    n_experts: int
+    top_k: int
+    expert_ffn: int
+
+    def expert_bytes(self) -> int:
+        """bf16 bytes of one expert's gate/up and down projections."""
+        return 2 * (2 * self.expert_ffn * self.hidden + self.hidden * self.expert_ffn)
+
+
+# Qwen3-30B-A3B's MoE feed-forward block: hidden 2048, 128 experts, 8 per
+# token, expert SwiGLU width 768, renormalised top-k weights.
+MOE30B = MoeShape("qwen3-30b-a3b-moe", 2048, 128, 8, 768)
+MOE_TINY = MoeShape("moe-tiny", 256, 16, 4, 128)
+
+
+def make_moe_weights(shape: MoeShape, seed: Optional[int] = None, device="cpu", proj_std: float = 0.02) -> dict:
+    """bf16 MoE block weights: router [E, d] ~ N(0, 1 / d) (logits of
+    N(0, 1) inputs spread about 1), gate/up [E, 2F, d] (per expert F gate
+    rows, then F up rows) and down [E, d, F] ~ N(0, proj_std)."""
+    if seed is None:
+        seed = seeds()["weights"] + 7
+    g = _gen(device, seed)
+    E, d, F = shape.n_experts, shape.hidden, shape.expert_ffn
+
+    def draw(*sz, std):
+        w = torch.empty(*sz, dtype=torch.bfloat16, device=device)
+        for e in range(sz[0]):   # one expert at a time keeps the fp32 temporary small
+            w[e] = (torch.randn(*sz[1:], generator=g, device=device) * std).to(torch.bfloat16)
+        return w
+    return {"w_router": (torch.randn(E, d, generator=g, device=device) / d ** 0.5).to(torch.bfloat16),
+            "w_gate_up": draw(E, 2 * F, d, std=proj_std), "w_down": draw(E, d, F, std=proj_std)}
+
+
 def weight_arrays(w: dict) -> dict:
     """Host numpy form of a weight dict: bf16 bit patterns, 8-bit codes and
     float32 row scales as they are."""
