@@ -666,15 +666,21 @@ eb_status eb_op_moe_ffn(const void *b, const void *residual, const void *w_route
   float *y = reinterpret_cast<float *>(base + L.y);
   const hipStream_t st = static_cast<hipStream_t>(stream);
   const int P = T * top_k;
+  // experts with a few rows each (decode batches) stream their weights in
+  // 64-row tiles; with 128 or more rows per expert on average the 256 x 256
+  // kernel takes tiles of up to 256 rows
+  const bool big = (long)P >= 128L * E && d % 64 == 0 && F % 64 == 0;
+  auto grouped = big ? launch_gemm_grouped_big : launch_gemm_grouped;
   hipError_t e = launch_moe_route(static_cast<const uint16_t *>(b), static_cast<const uint16_t *>(w_router), T, d, E,
                                   top_k, renormalize ? 1 : 0, logits, ids, wts, st);
-  if (e == hipSuccess) e = launch_moe_plan(ids, P, E, top_k, L.max_tiles, offsets, sorted_tok, pos_of, tiles, n_tiles, st);
   if (e == hipSuccess)
-    e = launch_gemm_grouped(static_cast<const uint16_t *>(b), T, sorted_tok, static_cast<const uint16_t *>(w_gate_up),
-                            m, false, tiles, n_tiles, L.max_tiles, 2 * F, d, EPI_SILU_MUL, st);
+    e = launch_moe_plan(ids, P, E, top_k, big ? 256 : 64, L.max_tiles, offsets, sorted_tok, pos_of, tiles, n_tiles, st);
   if (e == hipSuccess)
-    e = launch_gemm_grouped(m, P, nullptr, static_cast<const uint16_t *>(w_down), y, true, tiles, n_tiles,
-                            L.max_tiles, d, F, EPI_STORE, st);
+    e = grouped(static_cast<const uint16_t *>(b), T, sorted_tok, static_cast<const uint16_t *>(w_gate_up), m, false,
+                tiles, n_tiles, L.max_tiles, 2 * F, d, EPI_SILU_MUL, st);
+  if (e == hipSuccess)
+    e = grouped(m, P, nullptr, static_cast<const uint16_t *>(w_down), y, true, tiles, n_tiles, L.max_tiles, d, F,
+                EPI_STORE, st);
   if (e == hipSuccess)
     e = launch_moe_combine(y, pos_of, wts, static_cast<const uint16_t *>(residual), static_cast<uint16_t *>(out), T, d,
                            top_k, st);

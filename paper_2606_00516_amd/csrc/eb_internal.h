@@ -97,9 +97,13 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, cons
 hipError_t launch_gemm_grouped(const uint16_t *A, int a_nrows, const int32_t *a_rows, const uint16_t *W, void *out,
                                bool f32_out, const int32_t *tiles, const int32_t *n_tiles, int max_tiles, int N, int K,
                                int epi, hipStream_t st);
+// The same on the 256 x 256 kernel: tiles of up to 256 rows, K a multiple of 64.
+hipError_t launch_gemm_grouped_big(const uint16_t *A, int a_nrows, const int32_t *a_rows, const uint16_t *W,
+                                   void *out, bool f32_out, const int32_t *tiles, const int32_t *n_tiles, int max_tiles,
+                                   int N, int K, int epi, hipStream_t st);
 hipError_t launch_moe_route(const uint16_t *b, const uint16_t *wr, int T, int d, int E, int k, int renormalize,
                             float *logits, int32_t *ids, float *wts, hipStream_t st);
-hipError_t launch_moe_plan(const int32_t *ids, int P, int E, int k, int max_tiles, int32_t *offsets,
+hipError_t launch_moe_plan(const int32_t *ids, int P, int E, int k, int tile_rows, int max_tiles, int32_t *offsets,
                            int32_t *sorted_tok, int32_t *pos_of, int32_t *tiles, int32_t *n_tiles, hipStream_t st);
 hipError_t launch_moe_combine(const float *y, const int32_t *pos_of, const float *wts, const uint16_t *res,
                               uint16_t *out, int T, int d, int k, hipStream_t st);

@@ -388,12 +388,22 @@ constexpr int BG_TILE_BYTES = 256 * BG_BK * 2;  // one operand tile: 32 KiB
 
 __device__ __forceinline__ int bg_swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
 
-template <bool W8>
+// Grouped use (the experts of a mixture-of-experts block): a tile is up to
+// 256 expert-sorted rows of one expert (tables [3][max_tiles]: expert, first
+// sorted row, rows); block b takes tile b / tiles_n and column tile
+// b % tiles_n of that expert's W ([E][N][K]); A rows are gathered through
+// a_rows (null: the sorted row itself); the store epilogue may write fp32.
+struct GroupedArgs {
+  const int32_t *a_rows, *tiles, *n_tiles;
+  int max_tiles, a_nrows, f32_out;
+};
+
+template <bool W8, bool GROUPED>
 __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restrict__ A, const void *__restrict__ W,
                                                          const float *__restrict__ wscale, uint16_t *__restrict__ out,
                                                          const uint16_t *__restrict__ res, float *__restrict__ part,
                                                          int M, int N, int K, int epi, int tiles_m, int tiles_n,
-                                                         int per_xcd, int kt_per) {
+                                                         int per_xcd, int kt_per, GroupedArgs ga) {
   extern __shared__ __attribute__((aligned(16))) uint8_t bg_lds[];  // [2][A tile | W tile]
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -402,23 +412,38 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
   // block b works on tile (b % 8) * per_xcd + b / 8: each XCD walks its own
   // contiguous run of the (grouped) tile order and its L2 keeps the shared
   // A and W panels.
-  const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (t >= tiles_m * tiles_n) return;
-  const int group = 8;
-  const int per_group = group * tiles_m;
-  const int gidx = t / per_group;
-  const int first_n = gidx * group;
-  const int gsz = min(group, tiles_n - first_n);
-  const int inb = t - gidx * per_group;
-  const int tn = first_n + inb % gsz;
-  const int tm = inb / gsz;
-  const int m0 = tm * BG_BM, n0 = tn * BG_BN;
+  int m0, n0, mlim;  // first row, first logical column, rows of the tile in use
+  const void *Wt = W;
+  if constexpr (GROUPED) {
+    const int rt = blockIdx.x / tiles_n;
+    if (rt >= __builtin_amdgcn_readfirstlane(*ga.n_tiles)) return;
+    const int e = __builtin_amdgcn_readfirstlane(ga.tiles[rt]);
+    m0 = __builtin_amdgcn_readfirstlane(ga.tiles[ga.max_tiles + rt]);
+    mlim = __builtin_amdgcn_readfirstlane(ga.tiles[2 * ga.max_tiles + rt]);
+    n0 = (blockIdx.x % tiles_n) * BG_BN;
+    Wt = static_cast<const uint16_t *>(W) + (size_t)e * N * K;
+  } else {
+    const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (t >= tiles_m * tiles_n) return;
+    const int group = 8;
+    const int per_group = group * tiles_m;
+    const int gidx = t / per_group;
+    const int first_n = gidx * group;
+    const int gsz = min(group, tiles_n - first_n);
+    const int inb = t - gidx * per_group;
+    const int tn = first_n + inb % gsz;
+    const int tm = inb / gsz;
+    m0 = tm * BG_BM;
+    n0 = tn * BG_BN;
+    mlim = M - m0;
+  }
   const int split = blockIdx.y;
   const int kt0 = split * kt_per, kt1 = min(K / BG_BK, kt0 + kt_per);
 
   constexpr uint32_t WES = W8 ? 1u : 2u;  // bytes per W element
-  const buf_rsrc_t ra = make_rsrc(A, (int)min((size_t)M * K * 2, (size_t)0x7FFFFFFF));
-  const buf_rsrc_t rw = make_rsrc(W, (int)min((size_t)N * K * WES, (size_t)0x7FFFFFFF));
+  const int a_nrows = GROUPED ? ga.a_nrows : M;
+  const buf_rsrc_t ra = make_rsrc(A, (int)min((size_t)a_nrows * K * 2, (size_t)0x7FFFFFFF));
+  const buf_rsrc_t rw = make_rsrc(Wt, (int)min((size_t)N * K * WES, (size_t)0x7FFFFFFF));
   // DMA: wave w moves LDS rows [32 w, 32 w + 32) of both tiles, 8 rows
   // (1 KiB) per instruction; lane l fills row 8 i + l / 8, physical chunk
   // l % 8 with logical chunk bg_swz(row, l % 8).  Rows outside the operands
@@ -428,8 +453,10 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
   for (int i = 0; i < 4; ++i) {
     const int row = wave * 32 + i * 8 + (lane >> 3);
     const int c = bg_swz(row, lane & 7);
-    const int m = m0 + row;
-    aoff[i] = m < M ? ((uint32_t)m * (uint32_t)K + (uint32_t)(c * 8)) * 2u : 0x80000000u;
+    int ar = row < mlim ? m0 + row : -1;
+    if constexpr (GROUPED)
+      if (ar >= 0 && ga.a_rows) ar = ga.a_rows[ar];
+    aoff[i] = ar >= 0 && ar < a_nrows ? ((uint32_t)ar * (uint32_t)K + (uint32_t)(c * 8)) * 2u : 0x80000000u;
     const int wr = w_row_of(n0 + row, N, epi);
     woff[i] = wr >= 0 ? ((uint32_t)wr * (uint32_t)K + (uint32_t)(c * 8)) * WES : 0x80000000u;
   }
@@ -518,7 +545,7 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
 #pragma unroll
       for (int im = 0; im < 8; ++im) {
         const int m = m0 + wm * 128 + im * 16 + lr;
-        if (m < M && n < ncols) *reinterpret_cast<f32x4_t *>(part + ((size_t)split * M + m) * ncols + n) = acc[jn][im];
+        if (m - m0 < mlim && n < ncols) *reinterpret_cast<f32x4_t *>(part + ((size_t)split * M + m) * ncols + n) = acc[jn][im];
       }
     }
     return;
@@ -533,7 +560,7 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
 #pragma unroll
       for (int im = 0; im < 8; ++im) {
         const int m = m0 + wm * 128 + im * 16 + lr;
-        if (m < M && f < F) {
+        if (m - m0 < mlim && f < F) {
           const f32x4_t gv = acc[jj][im], uv = acc[jj + 2][im];
           u32x2_t w = {pack_bf16x2(silu_f(gv[0]) * uv[0], silu_f(gv[1]) * uv[1]),
                        pack_bf16x2(silu_f(gv[2]) * uv[2], silu_f(gv[3]) * uv[3])};
@@ -549,8 +576,14 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
 #pragma unroll
     for (int im = 0; im < 8; ++im) {
       const int m = m0 + wm * 128 + im * 16 + lr;
-      if (m < M && n < N) {
+      if (m - m0 < mlim && n < N) {
         f32x4_t v = acc[jn][im];
+        if constexpr (GROUPED) {
+          if (ga.f32_out) {
+            *reinterpret_cast<f32x4_t *>(reinterpret_cast<float *>(out) + (size_t)m * N + n) = v;
+            continue;
+          }
+        }
         if (epi == EPI_RESIDUAL) {
           const u32x2_t r = *reinterpret_cast<const u32x2_t *>(res + (size_t)m * N + n);
           v[0] += bf16_lo(r[0]);
@@ -794,11 +827,11 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, cons
       const int per_xcd = (tm * tn + 7) / 8;
       float *part = reinterpret_cast<float *>(ws);
       if (w8)
-        hipLaunchKernelGGL(k_gemm_big<true>, dim3(8 * per_xcd, p.splits), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A,
-                           W, wscale, out, res, part, M, N, K, epi, tm, tn, per_xcd, p.kt_per);
+        hipLaunchKernelGGL((k_gemm_big<true, false>), dim3(8 * per_xcd, p.splits), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A,
+                           W, wscale, out, res, part, M, N, K, epi, tm, tn, per_xcd, p.kt_per, GroupedArgs{});
       else
-        hipLaunchKernelGGL(k_gemm_big<false>, dim3(8 * per_xcd, p.splits), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A,
-                           W, wscale, out, res, part, M, N, K, epi, tm, tn, per_xcd, p.kt_per);
+        hipLaunchKernelGGL((k_gemm_big<false, false>), dim3(8 * per_xcd, p.splits), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st, A,
+                           W, wscale, out, res, part, M, N, K, epi, tm, tn, per_xcd, p.kt_per, GroupedArgs{});
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
       return launch_splitk_epilogue(part, p.splits, out, res, M, N, epi, st);
@@ -812,13 +845,15 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, cons
       const int tm = (mc + BG_BM - 1) / BG_BM, tn = (ncols + BG_BN - 1) / BG_BN;
       const int per_xcd = (tm * tn + 7) / 8;
       if (w8)
-        hipLaunchKernelGGL(k_gemm_big<true>, dim3(8 * per_xcd), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st,
+        hipLaunchKernelGGL((k_gemm_big<true, false>), dim3(8 * per_xcd), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st,
                            A + (size_t)m0 * K, W, wscale, out + (size_t)m0 * out_cols,
-                           res ? res + (size_t)m0 * N : nullptr, nullptr, mc, N, K, epi, tm, tn, per_xcd, K / BG_BK);
+                           res ? res + (size_t)m0 * N : nullptr, nullptr, mc, N, K, epi, tm, tn, per_xcd, K / BG_BK,
+                           GroupedArgs{});
       else
-        hipLaunchKernelGGL(k_gemm_big<false>, dim3(8 * per_xcd), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st,
+        hipLaunchKernelGGL((k_gemm_big<false, false>), dim3(8 * per_xcd), dim3(BG_THREADS), 4 * BG_TILE_BYTES, st,
                            A + (size_t)m0 * K, W, wscale, out + (size_t)m0 * out_cols,
-                           res ? res + (size_t)m0 * N : nullptr, nullptr, mc, N, K, epi, tm, tn, per_xcd, K / BG_BK);
+                           res ? res + (size_t)m0 * N : nullptr, nullptr, mc, N, K, epi, tm, tn, per_xcd, K / BG_BK,
+                           GroupedArgs{});
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
     }
@@ -828,6 +863,19 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, cons
   hipLaunchKernelGGL(k_gemm_tiled, dim3(tiles_m * tiles_n), dim3(256), 0, st, A,
                      static_cast<const uint16_t *>(W), out, res, M, N, K, epi, tiles_m,
                      tiles_n);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_grouped_big(const uint16_t *A, int a_nrows, const int32_t *a_rows, const uint16_t *W,
+                                   void *out, bool f32_out, const int32_t *tiles, const int32_t *n_tiles, int max_tiles,
+                                   int N, int K, int epi, hipStream_t st) {
+  if (max_tiles <= 0) return hipSuccess;
+  if (K % BG_BK) return hipErrorInvalidValue;
+  const int tiles_n = (logical_cols(N, epi) + BG_BN - 1) / BG_BN;
+  const GroupedArgs ga{a_rows, tiles, n_tiles, max_tiles, a_nrows, f32_out ? 1 : 0};
+  hipLaunchKernelGGL((k_gemm_big<false, true>), dim3((unsigned)max_tiles * (unsigned)tiles_n), dim3(BG_THREADS),
+                     4 * BG_TILE_BYTES, st, A, W, nullptr, static_cast<uint16_t *>(out), nullptr, nullptr, 0, N, K,
+                     epi, 0, tiles_n, 0, K / BG_BK, ga);
   return hipGetLastError();
 }
 

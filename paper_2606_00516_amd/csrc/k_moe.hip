@@ -107,12 +107,13 @@ __global__ __launch_bounds__(256) void k_moe_topk(const float *__restrict__ logi
 }
 
 // One block: expert counts, their offsets in the sorted order, the row
-// tiles (up to 64 rows of one expert) and each assignment's sorted position.
+// tiles (up to tile_rows rows of one expert) and each assignment's sorted
+// position.
 // Positions within an expert follow the order of the block's atomics; every
 // later step is independent of that order (rows are independent in the
 // products and the combine reads the slots in token order).
 __global__ __launch_bounds__(1024) void k_moe_plan(const int32_t *__restrict__ ids, int P, int E, int k,
-                                                   int max_tiles, int32_t *__restrict__ offsets,
+                                                   int tile_rows, int max_tiles, int32_t *__restrict__ offsets,
                                                    int32_t *__restrict__ sorted_tok, int32_t *__restrict__ pos_of,
                                                    int32_t *__restrict__ tiles, int32_t *__restrict__ n_tiles) {
   __shared__ int cnt[256], cur[256], toff[257];
@@ -131,7 +132,7 @@ __global__ __launch_bounds__(1024) void k_moe_plan(const int32_t *__restrict__ i
       cur[e] = o;
       toff[e] = to;
       o += cnt[e];
-      to += (cnt[e] + 63) / 64;
+      to += (cnt[e] + tile_rows - 1) / tile_rows;
     }
     offsets[E] = o;
     toff[E] = to;
@@ -140,10 +141,10 @@ __global__ __launch_bounds__(1024) void k_moe_plan(const int32_t *__restrict__ i
   __syncthreads();
   for (int e = tid; e < E; e += blockDim.x) {
     const int n = cnt[e], base = cur[e];
-    for (int j = 0, r = toff[e]; j < n && r < max_tiles; j += 64, ++r) {
+    for (int j = 0, r = toff[e]; j < n && r < max_tiles; j += tile_rows, ++r) {
       tiles[r] = e;
       tiles[max_tiles + r] = base + j;
-      tiles[2 * max_tiles + r] = min(64, n - j);
+      tiles[2 * max_tiles + r] = min(tile_rows, n - j);
     }
   }
   __syncthreads();
@@ -190,10 +191,10 @@ hipError_t launch_moe_route(const uint16_t *b, const uint16_t *wr, int T, int d,
   return hipGetLastError();
 }
 
-hipError_t launch_moe_plan(const int32_t *ids, int P, int E, int k, int max_tiles, int32_t *offsets,
+hipError_t launch_moe_plan(const int32_t *ids, int P, int E, int k, int tile_rows, int max_tiles, int32_t *offsets,
                            int32_t *sorted_tok, int32_t *pos_of, int32_t *tiles, int32_t *n_tiles, hipStream_t st) {
-  hipLaunchKernelGGL(k_moe_plan, dim3(1), dim3(1024), 0, st, ids, P, E, k, max_tiles, offsets, sorted_tok, pos_of,
-                     tiles, n_tiles);
+  hipLaunchKernelGGL(k_moe_plan, dim3(1), dim3(1024), 0, st, ids, P, E, k, tile_rows, max_tiles, offsets, sorted_tok,
+                     pos_of, tiles, n_tiles);
   return hipGetLastError();
 }
 

@@ -7,7 +7,8 @@ the fp32 summation error), the ids are distinct and in logit order, and the
 weights equal the oracle's weights for that choice.  The block's output is
 then compared element by element with the oracle evaluated under the same
 choice.  Cases: ragged token counts (one token, fewer tokens than a tile,
-several tiles per expert), the Qwen3-30B-A3B shape at a decode batch, routing
+several tiles per expert, enough rows per expert for the 256 x 256 kernel),
+the Qwen3-30B-A3B shape at a decode and a prefill batch, routing
 that sends every token to the same experts (empty experts, one expert with
 many row tiles), plain softmax weights, and argument errors."""
 import ctypes
@@ -70,7 +71,9 @@ def _check(shape, w, b, res, renormalize=True, min_same=0.9):
     return ids, err
 
 
-@pytest.mark.parametrize("T", [1, 7, 100, 333])
+@pytest.mark.parametrize("T", [1, 7, 100, 333,
+                               # 128 or more rows per expert: the 256 x 256 kernel on tiles of up to 256 rows
+                               600, 1500])
 def test_moe_small_vs_oracle(T):
     w, b, res = _case(gen.MOE_TINY, T)
     _check(gen.MOE_TINY, w, b, res)
@@ -88,12 +91,19 @@ def test_moe_30b_shape_decode_batch():
     assert len(np.unique(ids)) > 100
 
 
-def test_moe_every_token_to_the_same_experts():
+def test_moe_30b_shape_prefill_batch():
+    # 2048 tokens, 128 rows per expert on average: the 256 x 256 kernel
+    w, b, res = _case(gen.MOE30B, 2048, seed=9)
+    _check(gen.MOE30B, w, b, res)
+
+
+@pytest.mark.parametrize("T", [300, 600])
+def test_moe_every_token_to_the_same_experts(T):
     # a constant input feature and a router that scores experts 0..k-1 far
-    # above the rest on it: one expert receives all 300 tokens (five row
-    # tiles), twelve receive none
+    # above the rest on it: each of them receives every token (300: five
+    # 64-row tiles; 600: three tiles of up to 256 rows), twelve receive none
     shape = gen.MOE_TINY
-    w, b, res = _case(shape, 300, seed=7)
+    w, b, res = _case(shape, T, seed=7)
     b[:, 0] = 8.0
     wr = (w["w_router"].float() * 1e-3)
     wr[:, 0] = -4.0
