@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="decode8b",
                     choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "decode70b", "stack70b", "policy8b",
-                             "long8b", "moe30b", "copy"])
+                             "long8b", "moe30b", "q30b", "copy"])
     ap.add_argument("--calib-out", default=None, help="policy8b: write the calibrated step-cost profile here")
     ap.add_argument("--layers", type=int, default=80, help="decoder layers of the stack70b model step")
     ap.add_argument("--stack-r", default="0.2,0.5,0.8", help="decode shares of the stack70b mixed steps")
@@ -557,6 +557,42 @@ def moe30b(args, dev):
     return pts
 
 
+def q30b(args, dev):
+    """The Qwen3-30B-A3B-shaped layer (attention of 32 q / 4 kv heads, the
+    mixture-of-experts feed-forward) on the 8B-style batches: 64 decode
+    requests, 8 prompts of prefill, and a 2048-token mixed step at r = 0.5."""
+    import torch
+
+    from paper_2606_00516_amd import binding as B
+    from paper_2606_00516_amd import inputs as gen
+    shape = gen.Q30B
+    w = gen.make_weights(shape, device=dev)
+    pts = []
+    for name, batch, mode in (("decode", gen.batch_8b_decode(), "decode"),
+                              ("prefill", gen.batch_8b_prefill(), "prefill"),
+                              ("mixed r=0.5", gen.batch_8b_mixed(0.5), "mixed")):
+        step_fn = {"decode": B.eb_layer_step_decode, "prefill": B.eb_layer_step_prefill,
+                   "mixed": B.eb_layer_step_mixed}[mode]
+        pool, _ = make_pool(gen, shape, batch, "bf16", device=dev, poison=False)
+        x = gen.make_x(shape, batch.num_tokens, device=dev)
+        y = torch.empty_like(x)
+        h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
+        ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
+        ms, stages, t_att = measure(B, h, step_fn, w, pool, batch, x, y, ws, args.steps, args.warmup,
+                                    timed_stage="attention")
+        wk = step_work(shape, batch)
+        pt = {"point": name, "mode": mode, "tokens": wk["T"], "ms_per_step": round(ms, 5),
+              "tokens_per_s": round(wk["T"] / (ms / 1e3), 1), "attention_ms": round(t_att, 5),
+              "stage_ms": {k: round(v, 5) for k, v in stages.items()}}
+        if mode == "decode":
+            pt["attention_hbm_gbps"] = round(wk["kv_bytes_decode"] / (t_att / 1e3) / 1e9, 1)
+        pts.append(pt)
+        print(f"# q30b {name}: {ms:.3f} ms/step, attention {t_att:.3f} ms", file=sys.stderr, flush=True)
+        del pool, x, y, ws, h
+        torch.cuda.empty_cache()
+    return pts
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -659,6 +695,28 @@ def main():
                              "frac": round(dec["hbm_gbps"] / HBM_PEAK_GBPS, 4), "traffic": None},
                 "prefill_roofline": {"bound": "mfma", "achieved": pre["tflops"], "peak": BF16_PEAK_TFLOPS,
                                      "unit": "TFLOP/s", "frac": round(pre["tflops"] / BF16_PEAK_TFLOPS, 4)},
+                "points": pts, "wall_s": round(time.perf_counter() - t0, 1)}
+        js = json.dumps(line)
+        print(js)
+        if args.json_out:
+            with open(args.json_out, "w") as f:
+                f.write(js + "\n")
+        return
+
+    if args.workload == "q30b":
+        t0 = time.perf_counter()
+        pts = q30b(args, dev)
+        dec = pts[0]
+        line = {"metric": METRIC, "value": dec["attention_hbm_gbps"], "unit": "GB/s", "n_gpus": 1,
+                "steps": args.steps, "warmup": args.warmup, "ms_per_step": dec["ms_per_step"],
+                "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+                "data": "synthetic",
+                "config": {"workload": "qwen3-30b-a3b-shaped layer (attention + MoE feed-forward): decode EB 64 "
+                                       "requests ctx U[512,4096]; prefill EB 8 prompts; MB 2048 tokens at r = 0.5",
+                           "parallelism": "single-gpu"},
+                "roofline": {"kernel": "k_decode_mfma (decode attention, G = 8)", "bound": "hbm",
+                             "achieved": dec["attention_hbm_gbps"], "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                             "frac": round(dec["attention_hbm_gbps"] / HBM_PEAK_GBPS, 4), "traffic": None},
                 "points": pts, "wall_s": round(time.perf_counter() - t0, 1)}
         js = json.dumps(line)
         print(js)

@@ -70,10 +70,16 @@ typedef enum eb_epilogue {
   EB_EPI_SILU_MUL = 2  /* W holds [gate; up] (2F rows): out[:, f] = bf16(SiLU(g_f) * u_f), F = N / 2 */
 } eb_epilogue;
 
-/* Layer shape.  rms_eps: RMSNorm epsilon; rope_theta: RoPE base. */
+/* Layer shape.  rms_eps: RMSNorm epsilon; rope_theta: RoPE base.
+ * n_experts > 0 makes the feed-forward part the mixture-of-experts block of
+ * eb_op_moe_ffn (top_k experts per token, expert SwiGLU width expert_ffn,
+ * renormalised weights unless moe_renormalize is 0; ffn is then unused and
+ * may be 0); n_experts = 0 (a zero-initialised tail) is the dense SwiGLU of
+ * width ffn. */
 typedef struct eb_layer_config {
   int32_t hidden, n_q_heads, n_kv_heads, head_dim, ffn, page_size;
   float rms_eps, rope_theta;
+  int32_t n_experts, top_k, expert_ffn, moe_renormalize;
 } eb_layer_config;
 
 /* Element type of the four projection matrices. */
@@ -99,6 +105,11 @@ typedef struct eb_layer_weights {
   const void *attn_norm, *w_qkv, *w_o, *mlp_norm, *w_gate_up, *w_down;
   int32_t w_dtype;
   const float *s_qkv, *s_o, *s_gate_up, *s_down;
+  /* mixture-of-experts layers (n_experts > 0; bf16 weights only, w_gate_up
+   * and w_down unused): router [E, hidden], experts' gate/up
+   * [E, 2 expert_ffn, hidden] (per expert gate rows, then up rows) and down
+   * [E, hidden, expert_ffn] */
+  const void *w_router, *w_experts_gate_up, *w_experts_down;
 } eb_layer_weights;
 
 /* Element type of the KV cache. */

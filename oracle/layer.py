@@ -51,6 +51,10 @@ class LayerCfg:
     page_size: int = 16
     rms_eps: float = 1e-5
     rope_theta: float = 1e4
+    n_experts: int = 0          # > 0: mixture-of-experts feed-forward (oracle/moe.py)
+    top_k: int = 0
+    expert_ffn: int = 0
+    moe_renormalize: bool = True
 
     @property
     def group(self) -> int:
@@ -216,12 +220,30 @@ def prepare_weights(w_bits: Dict[str, np.ndarray], cfg: LayerCfg, dtype=np.float
             return fp8.dequantize_rows(w, w_bits["s_" + k[2:]]).astype(dtype)
         return bf16_bits_to_f32(w).astype(dtype)
     qkv = cv("w_qkv")
+    W = {"g1": cv("attn_norm"), "g2": cv("mlp_norm"),
+         "wq": qkv[: nq * hd], "wk": qkv[nq * hd: (nq + nkv) * hd], "wv": qkv[(nq + nkv) * hd:], "wo": cv("w_o")}
+    if cfg.n_experts:
+        # the MoE block works from the bf16 weights themselves
+        W["moe"] = (w_bits["w_router"], w_bits["w_experts_gate_up"], w_bits["w_experts_down"])
+        return W
     gu = cv("w_gate_up")
-    return {
-        "g1": cv("attn_norm"), "g2": cv("mlp_norm"),
-        "wq": qkv[: nq * hd], "wk": qkv[nq * hd: (nq + nkv) * hd], "wv": qkv[(nq + nkv) * hd:],
-        "wo": cv("w_o"), "wg": gu[:f], "wu": gu[f:], "wd": cv("w_down"),
-    }
+    W.update({"wg": gu[:f], "wu": gu[f:], "wd": cv("w_down")})
+    return W
+
+
+def feed_forward(cfg: LayerCfg, W: dict, h1: np.ndarray):
+    """(y, m): y = h1 + FFN(RMSNorm(h1) * g2) for rows h1 [n, d] (or one row
+    [d]).  Dense: m = SiLU(b Wg^T) * (b Wu^T), y = h1 + m Wd^T.  Mixture of
+    experts: the block of oracle/moe.py on b rounded to bf16 (the input the
+    layer hands the block), m = None."""
+    b = rmsnorm(h1, W["g2"], cfg.rms_eps)
+    if cfg.n_experts:
+        from . import moe
+        rows = np.atleast_2d(b)
+        y = moe.moe_ffn(f32_to_bf16_bits(rows.astype(np.float32)), *W["moe"], cfg.top_k, cfg.moe_renormalize)
+        return h1 + y.reshape(h1.shape).astype(h1.dtype), None
+    m = silu(b @ W["wg"].T) * (b @ W["wu"].T)
+    return h1 + m @ W["wd"].T, m
 
 
 def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
@@ -269,12 +291,11 @@ def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
                 append_kv(v_cache, bt, np.array([pos]), v[None], P, vs)
                 o = paged_attention_row(q, k_cache, v_cache, bt, pos, P, G, kv_scales).reshape(-1)
                 h1 = x[r] + W["wo"] @ o
-                b = rmsnorm(h1, W["g2"], cfg.rms_eps)
-                m = silu(W["wg"] @ b) * (W["wu"] @ b)
-                y[r] = h1 + W["wd"] @ m
+                y[r], m = feed_forward(cfg, W, h1)
                 if inter is not None:
                     for key, val in (("q", q), ("k", k), ("v", v), ("attn", o), ("h1", h1), ("m", m)):
-                        inter[key][r] = val
+                        if val is not None:
+                            inter[key][r] = val
         elif mode == "batched":
             rows = slice(r0, r0 + n)
             pos = c + np.arange(n)
@@ -288,12 +309,11 @@ def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
             V = gather_positions(v_cache, bt, c + n, P, dtype, vs)
             o = causal_attention_seq(q, K, V, pos, G).reshape(n, nq * hd)
             h1 = x[rows] + o @ W["wo"].T
-            b = rmsnorm(h1, W["g2"], cfg.rms_eps)
-            m = silu(b @ W["wg"].T) * (b @ W["wu"].T)
-            y[rows] = h1 + m @ W["wd"].T
+            y[rows], m = feed_forward(cfg, W, h1)
             if inter is not None:
                 for key, val in (("q", q), ("k", k), ("v", v), ("attn", o), ("h1", h1), ("m", m)):
-                    inter[key][rows] = val
+                    if val is not None:
+                        inter[key][rows] = val
         else:
             raise ValueError(mode)
     return (y, inter) if intermediates else y

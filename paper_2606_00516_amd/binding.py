@@ -41,12 +41,15 @@ class EbError(RuntimeError):
 class LayerConfig(ctypes.Structure):
     _fields_ = [("hidden", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32), ("page_size", ctypes.c_int32),
-                ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float)]
+                ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float),
+                ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32), ("expert_ffn", ctypes.c_int32),
+                ("moe_renormalize", ctypes.c_int32)]
 
 
 class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")] + \
-        [("w_dtype", ctypes.c_int32)] + [(n, ctypes.c_void_p) for n in ("s_qkv", "s_o", "s_gate_up", "s_down")]
+        [("w_dtype", ctypes.c_int32)] + [(n, ctypes.c_void_p) for n in ("s_qkv", "s_o", "s_gate_up", "s_down")] + \
+        [(n, ctypes.c_void_p) for n in ("w_router", "w_experts_gate_up", "w_experts_down")]
 
 
 W_BF16, W_FP8_E4M3 = 0, 1
@@ -134,7 +137,9 @@ def _stream(stream=None):
 def config_of(shape) -> LayerConfig:
     """LayerConfig from any object with the layer-shape attributes."""
     return LayerConfig(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn,
-                       getattr(shape, "page_size", 16), float(shape.rms_eps), float(shape.rope_theta))
+                       getattr(shape, "page_size", 16), float(shape.rms_eps), float(shape.rope_theta),
+                       getattr(shape, "n_experts", 0), getattr(shape, "top_k", 0), getattr(shape, "expert_ffn", 0),
+                       1 if getattr(shape, "moe_renormalize", True) else 0)
 
 
 class HostBatch:
@@ -164,8 +169,13 @@ def kv_struct(k_cache: torch.Tensor, v_cache: torch.Tensor, block_tables: torch.
 
 def weights_struct(w: dict) -> LayerWeights:
     """Weights dict -> struct: bf16 projections, or uint8 / float8_e4m3fn
-    codes with float32 row scales under s_qkv, s_o, s_gate_up, s_down."""
-    lw = LayerWeights(*[_ptr(w[k]) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")])
+    codes with float32 row scales under s_qkv, s_o, s_gate_up, s_down;
+    a mixture-of-experts layer brings w_router, w_experts_gate_up and
+    w_experts_down instead of w_gate_up and w_down."""
+    lw = LayerWeights(*[_ptr(w.get(k)) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")])
+    for k in ("w_router", "w_experts_gate_up", "w_experts_down"):
+        if k in w:
+            setattr(lw, k, _ptr(w[k]))
     if w["w_qkv"].dtype in _CODE_DTYPES:
         lw.w_dtype = W_FP8_E4M3
         for k in ("s_qkv", "s_o", "s_gate_up", "s_down"):

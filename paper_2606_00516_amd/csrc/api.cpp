@@ -37,13 +37,125 @@ const char *const kStageNames[kStages] = {"rmsnorm_1", "qkv_gemm", "rope_kv_appe
 size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
 
 Shape shape_of(const eb_layer_config &c) {
-  return Shape{c.hidden, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn, c.rms_eps, c.rope_theta};
+  Shape s{c.hidden, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn, c.rms_eps, c.rope_theta};
+  if (c.n_experts > 0) {
+    s.ne = c.n_experts;
+    s.topk = c.top_k;
+    s.effn = c.expert_ffn;
+    s.renorm = c.moe_renormalize ? 1 : 0;
+  }
+  return s;
 }
+
+namespace {
+// Workspace of the MoE block: routing, the sorted order and tiles, the
+// experts' SwiGLU outputs (bf16) and down products (fp32), 256-byte aligned.
+struct MoeLayout {
+  size_t logits, ids, wts, offsets, sorted_tok, pos_of, tiles, n_tiles, m, y, total;
+  int max_tiles;
+};
+MoeLayout moe_layout(int T, int d, int E, int k, int F) {
+  MoeLayout L{};
+  const size_t P = (size_t)T * k;
+  L.max_tiles = (int)((P + 63) / 64) + E;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.logits = take((size_t)T * E * 4);
+  L.ids = take(P * 4);
+  L.wts = take(P * 4);
+  L.offsets = take((size_t)(E + 1) * 4);
+  L.sorted_tok = take(P * 4);
+  L.pos_of = take(P * 4);
+  L.tiles = take((size_t)3 * L.max_tiles * 4);
+  L.n_tiles = take(4);
+  L.m = take(P * F * 2);
+  L.y = take(P * d * 4);
+  L.total = off;
+  return L;
+}
+eb_status moe_limits(int T, int d, int E, int k, int F) {
+  const size_t P = (size_t)T * k;
+  (void)E;
+  if ((size_t)T * d * 2 >= ((size_t)1 << 31) || P * F * 2 >= ((size_t)1 << 31) ||
+      (size_t)2 * F * d * 2 >= ((size_t)1 << 31) || P >= ((size_t)1 << 30))
+    return fail(EB_ERR_LIMITS, "MoE operands exceed the kernels' 32-bit ranges");
+  return EB_OK;
+}
+eb_status check_moe(int T, int d, int E, int k, int F) {
+  if (T < 0 || d <= 0 || E <= 0 || k <= 0 || F <= 0) return fail(EB_ERR_CONFIG, "MoE sizes must be positive");
+  if (d % 32) return fail(EB_ERR_CONFIG, "MoE hidden size must be a multiple of 32");
+  if (F % 8) return fail(EB_ERR_CONFIG, "MoE expert width must be a multiple of 8");
+  if (E % 16 || E > 256) return fail(EB_ERR_CONFIG, "MoE expert count must be a multiple of 16, at most 256");
+  if (k > E || k > 64) return fail(EB_ERR_CONFIG, "MoE top_k must be at most the expert count and 64");
+  return moe_limits(T, d, E, k, F);
+}
+
+// The block on the stream: routing, the sorted order and the gate/up
+// products (first), then the down products and the weighted combine with
+// the residual (second); b is the block's input, out its output.
+struct MoeArgs {
+  const uint16_t *b, *res, *w_router, *w_gate_up, *w_down;
+  uint16_t *out;
+  int T, d, E, k, F, renorm;
+  char *ws;
+};
+struct MoeBufs {
+  float *logits, *wts, *y;
+  int32_t *ids, *offsets, *sorted_tok, *pos_of, *tiles, *n_tiles;
+  uint16_t *m;
+  int max_tiles;
+  bool big;
+};
+MoeBufs moe_bufs(const MoeArgs &a) {
+  const MoeLayout L = moe_layout(a.T, a.d, a.E, a.k, a.F);
+  MoeBufs B;
+  B.logits = reinterpret_cast<float *>(a.ws + L.logits);
+  B.ids = reinterpret_cast<int32_t *>(a.ws + L.ids);
+  B.wts = reinterpret_cast<float *>(a.ws + L.wts);
+  B.offsets = reinterpret_cast<int32_t *>(a.ws + L.offsets);
+  B.sorted_tok = reinterpret_cast<int32_t *>(a.ws + L.sorted_tok);
+  B.pos_of = reinterpret_cast<int32_t *>(a.ws + L.pos_of);
+  B.tiles = reinterpret_cast<int32_t *>(a.ws + L.tiles);
+  B.n_tiles = reinterpret_cast<int32_t *>(a.ws + L.n_tiles);
+  B.m = reinterpret_cast<uint16_t *>(a.ws + L.m);
+  B.y = reinterpret_cast<float *>(a.ws + L.y);
+  B.max_tiles = L.max_tiles;
+  // experts with a few rows each (decode batches) stream their weights in
+  // 64-row tiles; with 128 or more rows per expert on average the 256 x 256
+  // kernel takes tiles of up to 256 rows
+  B.big = (long)a.T * a.k >= 128L * a.E && a.d % 64 == 0 && a.F % 64 == 0;
+  return B;
+}
+hipError_t moe_first(const MoeArgs &a, hipStream_t st) {
+  const MoeBufs B = moe_bufs(a);
+  auto grouped = B.big ? launch_gemm_grouped_big : launch_gemm_grouped;
+  hipError_t e = launch_moe_route(a.b, a.w_router, a.T, a.d, a.E, a.k, a.renorm, B.logits, B.ids, B.wts, st);
+  if (e == hipSuccess)
+    e = launch_moe_plan(B.ids, a.T * a.k, a.E, a.k, B.big ? 256 : 64, B.max_tiles, B.offsets, B.sorted_tok, B.pos_of,
+                        B.tiles, B.n_tiles, st);
+  if (e == hipSuccess)
+    e = grouped(a.b, a.T, B.sorted_tok, a.w_gate_up, B.m, false, B.tiles, B.n_tiles, B.max_tiles, 2 * a.F, a.d,
+                EPI_SILU_MUL, st);
+  return e;
+}
+hipError_t moe_second(const MoeArgs &a, hipStream_t st) {
+  const MoeBufs B = moe_bufs(a);
+  auto grouped = B.big ? launch_gemm_grouped_big : launch_gemm_grouped;
+  hipError_t e = grouped(B.m, a.T * a.k, nullptr, a.w_down, B.y, true, B.tiles, B.n_tiles, B.max_tiles, a.d, a.F,
+                         EPI_STORE, st);
+  if (e == hipSuccess) e = launch_moe_combine(B.y, B.pos_of, B.wts, a.res, a.out, a.T, a.d, a.k, st);
+  return e;
+}
+}  // namespace
 
 // Byte offsets of everything a step keeps in the caller's workspace.
 struct WsLayout {
   size_t meta = 0, act = 0, qkv = 0, attn = 0, h1 = 0, mlp = 0, part_o = 0, part_ml = 0, gemm = 0, alt = 0,
-         total = 0;
+         moe = 0, total = 0;
 };
 
 // full_step: buffers of a whole layer; stack: plus the second activation
@@ -65,17 +177,21 @@ WsLayout layout_for(const Shape &s, const HostPlan &p, bool full_step, bool stac
     L.qkv = take(T * s.qkv_cols() * 2);
     L.attn = take(T * s.nq * s.hd * 2);
     L.h1 = take(T * s.hidden * 2);
-    L.mlp = take(T * s.ffn * 2);
+    if (!s.moe()) L.mlp = take(T * s.ffn * 2);
     size_t g = 0;
     const int M = p.T;
-    // room for the plans of either weight type
+    // room for the plans of either weight type (the feed-forward ones when dense)
     for (int w8 = 0; w8 < 2; ++w8) {
-      const GemmPlan plans[4] = {plan_gemm(M, s.qkv_cols(), s.hidden, EPI_STORE, w8),
-                                 plan_gemm(M, s.hidden, s.nq * s.hd, EPI_RESIDUAL, w8),
-                                 plan_gemm(M, 2 * s.ffn, s.hidden, EPI_SILU_MUL, w8),
-                                 plan_gemm(M, s.hidden, s.ffn, EPI_RESIDUAL, w8)};
-      for (const auto &gp : plans) g = gp.ws_bytes > g ? gp.ws_bytes : g;
+      const int nplans = s.moe() ? 2 : 4;  // (an MoE layer has no dense feed-forward GEMMs)
+      for (int i = 0; i < nplans; ++i) {
+        const GemmPlan gp = i == 0   ? plan_gemm(M, s.qkv_cols(), s.hidden, EPI_STORE, w8)
+                            : i == 1 ? plan_gemm(M, s.hidden, s.nq * s.hd, EPI_RESIDUAL, w8)
+                            : i == 2 ? plan_gemm(M, 2 * s.ffn, s.hidden, EPI_SILU_MUL, w8)
+                                     : plan_gemm(M, s.hidden, s.ffn, EPI_RESIDUAL, w8);
+        g = gp.ws_bytes > g ? gp.ws_bytes : g;
+      }
     }
+    if (s.moe()) L.moe = take(moe_layout(p.T, s.hidden, s.ne, s.topk, s.effn).total);
     L.gemm = take(g);
     if (stack) L.alt = take(T * s.hidden * 2);
   }
@@ -201,8 +317,16 @@ KV kv_of(const eb_kv_cache *kv) {
 // The weights of one layer for a batch of T tokens: pointers, the weight
 // type, and (8-bit weights) scales and that a kernel takes every projection.
 eb_status check_weights(const eb_layer_weights *w, const Shape &sh, int T) {
-  if (!w || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm || !w->w_gate_up || !w->w_down)
+  if (!w || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm)
     return fail(EB_ERR_NULL, "a weight pointer is NULL");
+  if (sh.moe()) {
+    if (!w->w_router || !w->w_experts_gate_up || !w->w_experts_down)
+      return fail(EB_ERR_NULL, "a mixture-of-experts weight pointer is NULL");
+    if (w->w_dtype != EB_W_BF16) return fail(EB_ERR_CONFIG, "mixture-of-experts layers take bf16 weights");
+    if (moe_limits(T, sh.hidden, sh.ne, sh.topk, sh.effn) != EB_OK) return EB_ERR_LIMITS;
+    return EB_OK;
+  }
+  if (!w->w_gate_up || !w->w_down) return fail(EB_ERR_NULL, "a weight pointer is NULL");
   if (w->w_dtype == EB_W_BF16) return EB_OK;
   if (w->w_dtype != EB_W_FP8_E4M3) return fail(EB_ERR_CONFIG, "unknown w_dtype");
   const float *sc[4] = {w->s_qkv, w->s_o, w->s_gate_up, w->s_down};
@@ -225,6 +349,7 @@ struct StepBufs {
   uint16_t *act, *qkv, *attn, *h1, *mlp, *alt;
   float *part_o, *part_ml;
   void *gws;
+  char *moe;
 };
 
 StepBufs bufs_at(char *base, const WsLayout &L) {
@@ -233,7 +358,7 @@ StepBufs bufs_at(char *base, const WsLayout &L) {
                   reinterpret_cast<uint16_t *>(base + L.mlp),  L.alt ? reinterpret_cast<uint16_t *>(base + L.alt)
                                                                       : nullptr,
                   reinterpret_cast<float *>(base + L.part_o), reinterpret_cast<float *>(base + L.part_ml),
-                  base + L.gemm};
+                  base + L.gemm, base + L.moe};
 }
 
 // Make sure a profiling slot's events cover n layers.  They only time the
@@ -282,6 +407,17 @@ eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, con
            "o gemm");
   EB_STAGE(6, launch_rmsnorm(B.h1, static_cast<const uint16_t *>(w->mlp_norm), B.act, T, sh.hidden, sh.eps, st),
            "rmsnorm2");
+  if (sh.moe()) {
+    // the mixture-of-experts block: stage 7 routes and runs the gate/up
+    // products, stage 8 the down products and the combine with h1
+    const MoeArgs ma{B.act, B.h1, static_cast<const uint16_t *>(w->w_router),
+                     static_cast<const uint16_t *>(w->w_experts_gate_up),
+                     static_cast<const uint16_t *>(w->w_experts_down), yout, T, sh.hidden, sh.ne, sh.topk, sh.effn,
+                     sh.renorm, B.moe};
+    EB_STAGE(7, moe_first(ma, st), "moe routing and gate/up");
+    EB_STAGE(8, moe_second(ma, st), "moe down and combine");
+    return EB_OK;
+  }
   EB_STAGE(7,
            launch_gemm(plan_gemm(T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL, w8), B.act, w->w_gate_up,
                        w8 ? w->s_gate_up : nullptr, B.mlp, nullptr, T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL, B.gws,
@@ -593,49 +729,6 @@ eb_status eb_op_gemm_w8(const void *A, const void *W, const float *w_scale, void
   return op_gemm(A, W, w_scale, out, residual, M, N, K, epi, ws, ws_bytes, stream);
 }
 
-namespace {
-// Workspace of the MoE block: routing, the sorted order and tiles, the
-// experts' SwiGLU outputs (bf16) and down products (fp32), 256-byte aligned.
-struct MoeLayout {
-  size_t logits, ids, wts, offsets, sorted_tok, pos_of, tiles, n_tiles, m, y, total;
-  int max_tiles;
-};
-MoeLayout moe_layout(int T, int d, int E, int k, int F) {
-  MoeLayout L{};
-  const size_t P = (size_t)T * k;
-  L.max_tiles = (int)((P + 63) / 64) + E;
-  size_t off = 0;
-  auto take = [&](size_t bytes) {
-    const size_t o = off;
-    off = align_up(off + bytes);
-    return o;
-  };
-  L.logits = take((size_t)T * E * 4);
-  L.ids = take(P * 4);
-  L.wts = take(P * 4);
-  L.offsets = take((size_t)(E + 1) * 4);
-  L.sorted_tok = take(P * 4);
-  L.pos_of = take(P * 4);
-  L.tiles = take((size_t)3 * L.max_tiles * 4);
-  L.n_tiles = take(4);
-  L.m = take(P * F * 2);
-  L.y = take(P * d * 4);
-  L.total = off;
-  return L;
-}
-eb_status check_moe(int T, int d, int E, int k, int F) {
-  if (T < 0 || d <= 0 || E <= 0 || k <= 0 || F <= 0) return fail(EB_ERR_CONFIG, "MoE sizes must be positive");
-  if (d % 32) return fail(EB_ERR_CONFIG, "MoE hidden size must be a multiple of 32");
-  if (F % 8) return fail(EB_ERR_CONFIG, "MoE expert width must be a multiple of 8");
-  if (E % 16 || E > 256) return fail(EB_ERR_CONFIG, "MoE expert count must be a multiple of 16, at most 256");
-  if (k > E || k > 64) return fail(EB_ERR_CONFIG, "MoE top_k must be at most the expert count and 64");
-  const size_t P = (size_t)T * k;
-  if ((size_t)T * d * 2 >= ((size_t)1 << 31) || P * F * 2 >= ((size_t)1 << 31) ||
-      (size_t)2 * F * d * 2 >= ((size_t)1 << 31) || P >= ((size_t)1 << 30))
-    return fail(EB_ERR_LIMITS, "MoE operands exceed the kernels' 32-bit ranges");
-  return EB_OK;
-}
-}  // namespace
 
 size_t eb_op_moe_ffn_workspace_bytes(int32_t T, int32_t d, int32_t E, int32_t top_k, int32_t F) {
   if (T <= 0 || d <= 0 || E <= 0 || top_k <= 0 || F <= 0) return 0;
@@ -650,42 +743,19 @@ eb_status eb_op_moe_ffn(const void *b, const void *residual, const void *w_route
   if (s != EB_OK) return s;
   if (T == 0) return EB_OK;
   if (!b || !w_router || !w_gate_up || !w_down || !out) return fail(EB_ERR_NULL, "an input or out is NULL");
-  const MoeLayout L = moe_layout(T, d, E, top_k, F);
-  s = check_ws(ws, ws_bytes, L.total);
+  s = check_ws(ws, ws_bytes, moe_layout(T, d, E, top_k, F).total);
   if (s != EB_OK) return s;
-  char *base = static_cast<char *>(ws);
-  float *logits = reinterpret_cast<float *>(base + L.logits);
-  int32_t *ids = reinterpret_cast<int32_t *>(base + L.ids);
-  float *wts = reinterpret_cast<float *>(base + L.wts);
-  int32_t *offsets = reinterpret_cast<int32_t *>(base + L.offsets);
-  int32_t *sorted_tok = reinterpret_cast<int32_t *>(base + L.sorted_tok);
-  int32_t *pos_of = reinterpret_cast<int32_t *>(base + L.pos_of);
-  int32_t *tiles = reinterpret_cast<int32_t *>(base + L.tiles);
-  int32_t *n_tiles = reinterpret_cast<int32_t *>(base + L.n_tiles);
-  uint16_t *m = reinterpret_cast<uint16_t *>(base + L.m);
-  float *y = reinterpret_cast<float *>(base + L.y);
+  const MoeArgs ma{static_cast<const uint16_t *>(b), static_cast<const uint16_t *>(residual),
+                   static_cast<const uint16_t *>(w_router), static_cast<const uint16_t *>(w_gate_up),
+                   static_cast<const uint16_t *>(w_down), static_cast<uint16_t *>(out), T, d, E, top_k, F,
+                   renormalize ? 1 : 0, static_cast<char *>(ws)};
   const hipStream_t st = static_cast<hipStream_t>(stream);
-  const int P = T * top_k;
-  // experts with a few rows each (decode batches) stream their weights in
-  // 64-row tiles; with 128 or more rows per expert on average the 256 x 256
-  // kernel takes tiles of up to 256 rows
-  const bool big = (long)P >= 128L * E && d % 64 == 0 && F % 64 == 0;
-  auto grouped = big ? launch_gemm_grouped_big : launch_gemm_grouped;
-  hipError_t e = launch_moe_route(static_cast<const uint16_t *>(b), static_cast<const uint16_t *>(w_router), T, d, E,
-                                  top_k, renormalize ? 1 : 0, logits, ids, wts, st);
-  if (e == hipSuccess)
-    e = launch_moe_plan(ids, P, E, top_k, big ? 256 : 64, L.max_tiles, offsets, sorted_tok, pos_of, tiles, n_tiles, st);
-  if (e == hipSuccess)
-    e = grouped(static_cast<const uint16_t *>(b), T, sorted_tok, static_cast<const uint16_t *>(w_gate_up), m, false,
-                tiles, n_tiles, L.max_tiles, 2 * F, d, EPI_SILU_MUL, st);
-  if (e == hipSuccess)
-    e = grouped(m, P, nullptr, static_cast<const uint16_t *>(w_down), y, true, tiles, n_tiles, L.max_tiles, d, F,
-                EPI_STORE, st);
-  if (e == hipSuccess)
-    e = launch_moe_combine(y, pos_of, wts, static_cast<const uint16_t *>(residual), static_cast<uint16_t *>(out), T, d,
-                           top_k, st);
-  if (e == hipSuccess && ids_out) e = hipMemcpyAsync(ids_out, ids, (size_t)P * 4, hipMemcpyDeviceToDevice, st);
-  if (e == hipSuccess && weights_out) e = hipMemcpyAsync(weights_out, wts, (size_t)P * 4, hipMemcpyDeviceToDevice, st);
+  const MoeBufs B = moe_bufs(ma);
+  const size_t P = (size_t)T * top_k;
+  hipError_t e = moe_first(ma, st);
+  if (e == hipSuccess) e = moe_second(ma, st);
+  if (e == hipSuccess && ids_out) e = hipMemcpyAsync(ids_out, B.ids, P * 4, hipMemcpyDeviceToDevice, st);
+  if (e == hipSuccess && weights_out) e = hipMemcpyAsync(weights_out, B.wts, P * 4, hipMemcpyDeviceToDevice, st);
   return e == hipSuccess ? EB_OK : hip_fail(e, "moe ffn");
 }
 

@@ -59,6 +59,8 @@ struct KV {
 struct Shape {
   int32_t hidden, nq, nkv, hd, ffn;
   float eps, theta;
+  int32_t ne = 0, topk = 0, effn = 0, renorm = 1;  // mixture-of-experts feed-forward when ne > 0
+  bool moe() const { return ne > 0; }
   int32_t qkv_cols() const { return (nq + 2 * nkv) * hd; }
   int32_t group() const { return nq / nkv; }
 };

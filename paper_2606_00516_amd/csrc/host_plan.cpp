@@ -29,7 +29,8 @@ eb_status check_config(const eb_layer_config *cfg, std::string &err) {
     return EB_ERR_NULL;
   }
   const eb_layer_config &c = *cfg;
-  if (c.hidden <= 0 || c.n_q_heads <= 0 || c.n_kv_heads <= 0 || c.head_dim <= 0 || c.ffn <= 0) {
+  if (c.hidden <= 0 || c.n_q_heads <= 0 || c.n_kv_heads <= 0 || c.head_dim <= 0 || c.ffn < 0 ||
+      (c.ffn == 0 && c.n_experts <= 0)) {
     err = "layer sizes must be positive";
     return EB_ERR_CONFIG;
   }
@@ -53,6 +54,18 @@ eb_status check_config(const eb_layer_config *cfg, std::string &err) {
   if (c.hidden % 8 || c.ffn % 8) {
     err = "hidden and ffn must be multiples of 8";
     return EB_ERR_CONFIG;
+  }
+  if (c.n_experts < 0) {
+    err = "n_experts must be >= 0";
+    return EB_ERR_CONFIG;
+  }
+  if (c.n_experts > 0) {
+    if (c.n_experts % 16 || c.n_experts > 256 || c.top_k < 1 || c.top_k > c.n_experts || c.top_k > 64 ||
+        c.expert_ffn <= 0 || c.expert_ffn % 8 || c.hidden % 32) {
+      err = "mixture-of-experts layer: n_experts a multiple of 16 up to 256, 1 <= top_k <= min(n_experts, 64), "
+            "expert_ffn a positive multiple of 8, hidden a multiple of 32";
+      return EB_ERR_CONFIG;
+    }
   }
   if (!(c.rms_eps > 0.f) || !(c.rope_theta > 0.f)) {
     err = "rms_eps and rope_theta must be positive";

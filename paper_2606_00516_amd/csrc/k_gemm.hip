@@ -760,6 +760,8 @@ static int skinny_splits(int M, int N, int K) {
 
 GemmPlan plan_gemm(int M, int N, int K, int epi, bool w8) {
   GemmPlan p{};
+  p.splits = 1;
+  if (M <= 0 || N <= 0 || K <= 0) return p;  // nothing to plan (kind 0, no workspace)
   const int ncols = logical_cols(N, epi);
   // the big kernel addresses W through a 32-bit buffer range; A is cut into
   // row chunks that each fit one (launch_gemm)

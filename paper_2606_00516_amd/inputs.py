@@ -38,6 +38,10 @@ class LayerShape:
     rope_theta: float
     rms_eps: float = 1e-5
     page_size: int = PAGE_SIZE
+    # mixture-of-experts feed-forward when n_experts > 0 (ffn then unused)
+    n_experts: int = 0
+    top_k: int = 0
+    expert_ffn: int = 0
 
     @property
     def group(self) -> int:
@@ -49,6 +53,10 @@ class LayerShape:
 
     def weight_bytes(self) -> int:
         d, f = self.hidden, self.ffn
+        if self.n_experts:
+            n = self.qkv_rows * d + d * self.n_q_heads * self.head_dim + 2 * d + self.n_experts * d + \
+                self.n_experts * 3 * self.expert_ffn * d
+            return 2 * n
         n = self.qkv_rows * d + d * self.n_q_heads * self.head_dim + 2 * f * d + d * f + 2 * d
         return 2 * n
 
@@ -60,8 +68,14 @@ TINY = LayerShape("tiny", 256, 4, 2, 64, 688, 1e4)
 L8B = LayerShape("llama3-8b", 4096, 32, 8, 128, 14336, 5e5)
 # Llama-3-70B-shaped layer, same theta reading.
 L70B = LayerShape("llama3-70b", 8192, 64, 8, 128, 28672, 5e5)
+# Mixture-of-experts layers: attention as in the dense layers (no q/k norms),
+# the feed-forward replaced by the MoE block.  Qwen3-30B-A3B shapes: hidden
+# 2048, 32 q / 4 kv heads of 128, 128 experts, 8 per token, width 768, RoPE
+# theta 1e6; and a tiny one for the parity tests.
+Q30B = LayerShape("qwen3-30b-a3b", 2048, 32, 4, 128, 0, 1e6, n_experts=128, top_k=8, expert_ffn=768)
+TINY_MOE = LayerShape("tiny-moe", 256, 4, 2, 64, 0, 1e4, n_experts=16, top_k=4, expert_ffn=128)
 
-SHAPES = {s.name: s for s in (TINY, L8B, L70B)}
+SHAPES = {s.name: s for s in (TINY, L8B, L70B, Q30B, TINY_MOE)}
 
 
 def seeds(base: int = BASE_SEED) -> dict:
@@ -116,6 +130,14 @@ def make_weights(shape: LayerShape, seed: Optional[int] = None, device="cpu",
     def gain():
         return (1.0 + 0.1 * torch.randn(d, generator=g, device=device)).to(torch.bfloat16)
 
+    if shape.n_experts:  # attention as above, a mixture-of-experts feed-forward
+        w = {"attn_norm": gain(), "w_qkv": proj(shape.qkv_rows, d), "w_o": proj(d, shape.n_q_heads * hd),
+             "mlp_norm": gain()}
+        moe = make_moe_weights(MoeShape(shape.name, d, shape.n_experts, shape.top_k, shape.expert_ffn),
+                               seed=seed + 1, device=device, proj_std=proj_std)
+        w.update({"w_router": moe["w_router"], "w_experts_gate_up": moe["w_gate_up"],
+                  "w_experts_down": moe["w_down"]})
+        return w
     return {
         "attn_norm": gain(),
         "w_qkv": proj(shape.qkv_rows, d),

@@ -138,3 +138,50 @@ def test_planted_mistakes_fail_the_transformers_pin(monkeypatch):
     swapped = np.concatenate([o["wgu"][:, F:], o["wgu"][:, :F]], axis=1)
     y = MO.moe_ffn(o["b"], o["wr"], swapped, o["wd"], 4, True)
     assert np.max(np.abs(y - y_hf)) > tol
+
+
+# ---------------------------------------------------------------- MoE layer
+
+def _moe_layer_case(identical=False):
+    from paper_2606_00516_amd import inputs as gen
+    from tests._cases import make_case, oracle_cfg
+    shape = gen.TINY_MOE
+    case = make_case(shape, gen.batch_tiny(mode="mixed"), spare_pages=2)
+    if identical:
+        # every expert the same SwiGLU: the renormalised weights sum to one,
+        # so the block is that SwiGLU whatever the routing
+        for k in ("w_experts_gate_up", "w_experts_down"):
+            case.weights[k] = case.weights[k][:1].repeat(shape.n_experts, 1, 1)
+    return shape, case, oracle_cfg(shape)
+
+
+def test_moe_layer_with_identical_experts_is_the_dense_layer():
+    import dataclasses
+    shape, case, cfg = _moe_layer_case(identical=True)
+    y_moe, _ = case.run_oracle(dtype=np.float64)
+    dense_cfg = dataclasses.replace(cfg, ffn=shape.expert_ffn, n_experts=0, top_k=0, expert_ffn=0)
+    o = case.oracle_inputs()
+    wb = dict(o["w_bits"])
+    wb["w_gate_up"] = wb.pop("w_experts_gate_up")[0]
+    wb["w_down"] = wb.pop("w_experts_down")[0]
+    W = oracle_prepare(wb, dense_cfg)
+    y_dense = OL.layer_step(dense_cfg, W, o["k_cache"], o["v_cache"], o["block_tables"], o["context_lens"],
+                            o["chunk_lens"], o["x_bits"])
+    # the MoE block sees its input rounded to bf16, the dense feed-forward
+    # does not: the two agree to that rounding
+    assert np.max(np.abs(y_moe - y_dense)) <= 1e-2 * np.max(np.abs(y_dense))
+    assert np.max(np.abs(y_moe - y_dense)) > 0
+
+
+def test_moe_layer_is_attention_then_the_pinned_block():
+    shape, case, cfg = _moe_layer_case()
+    (y, inter), o = case.run_oracle(dtype=np.float64, intermediates=True)
+    W = oracle_prepare(o["w_bits"], cfg, np.float64)
+    b = OL.rmsnorm(inter["h1"], W["g2"], cfg.rms_eps)
+    blk = MO.moe_ffn(OL.f32_to_bf16_bits(b.astype(np.float32)), o["w_bits"]["w_router"],
+                     o["w_bits"]["w_experts_gate_up"], o["w_bits"]["w_experts_down"], shape.top_k)
+    assert np.max(np.abs(y - (inter["h1"] + blk))) <= 1e-12 * np.max(np.abs(y))
+
+
+def oracle_prepare(w_bits, cfg, dtype=np.float64):
+    return OL.prepare_weights(w_bits, cfg, dtype)
