@@ -51,6 +51,9 @@ def parse():
                     choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "decode70b", "stack70b", "policy8b",
                              "long8b", "moe30b", "q30b", "copy"])
     ap.add_argument("--calib-out", default=None, help="policy8b: write the calibrated step-cost profile here")
+    ap.add_argument("--shape", default="l8b", choices=["l8b", "q30b"],
+                    help="layer of the sweep8b / policy8b workloads: the llama3-8b layer, or the "
+                         "qwen3-30b-a3b-shaped mixture-of-experts layer")
     ap.add_argument("--layers", type=int, default=80, help="decoder layers of the stack70b model step")
     ap.add_argument("--stack-r", default="0.2,0.5,0.8", help="decode shares of the stack70b mixed steps")
     ap.add_argument("--budgets", default="1024,2048", help="token budgets of the sweep (for alpha/beta fits)")
@@ -237,14 +240,15 @@ def measure(B, h, step_fn, w, pool, batch, x, y, ws, steps, warmup, kv_scales=No
 
 
 def sweep(args, dev):
-    """Mixed 8B step over decode shares 0, 0.1, .., 1 at several budgets."""
+    """Mixed step of the chosen layer (the 8B one by default) over decode
+    shares 0, 0.1, .., 1 at several budgets."""
     import numpy as np
     import torch
 
     from paper_2606_00516_amd import analysis as AN
     from paper_2606_00516_amd import binding as B
     from paper_2606_00516_amd import inputs as gen
-    shape = gen.L8B
+    shape = gen.Q30B if args.shape == "q30b" else gen.L8B
     w = gen.make_weights(shape, device=dev)
     budgets = [int(b) for b in args.budgets.split(",")]
     rs = [round(0.1 * i, 1) for i in range(11)]
@@ -411,8 +415,9 @@ def policy8b(args, dev):
     args.dec_ctx = args.dec_ctx or "512,1024"
     args.budgets = args.budgets if args.budgets != "1024,2048" else "512,1024,2048,4096"
     sw, pts = sweep(args, dev)
-    c = CM.calibrate(pts, label=f"MI355X llama3-8b layer, decode ctx U[{args.dec_ctx}]")
-    prof = {"hardware": "MI355X", "shape": "llama3-8b layer", "decode_ctx": args.dec_ctx,
+    layer = "qwen3-30b-a3b-shaped MoE layer" if args.shape == "q30b" else "llama3-8b layer"
+    c = CM.calibrate(pts, label=f"MI355X {layer}, decode ctx U[{args.dec_ctx}]")
+    prof = {"hardware": "MI355X", "shape": layer, "decode_ctx": args.dec_ctx,
             "budgets": args.budgets, "costs": c.to_dict()}
     if args.calib_out:
         with open(args.calib_out, "w") as f:
@@ -669,7 +674,7 @@ def main():
                 "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": None,
                 "higher_is_better": False, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
                 "data": "synthetic",
-                "config": {"workload": f"llama3-8b-layer cost model: MB sweep budgets {args.budgets}, decode ctx "
+                "config": {"workload": f"{'qwen3-30b-a3b-shaped MoE' if args.shape == 'q30b' else 'llama3-8b'}-layer cost model: MB sweep budgets {args.budgets}, decode ctx "
                                        f"{args.dec_ctx}; decisions and simulated EB / MB / EB+ for the paper's "
                                        f"mixes", "kv_cache": KV_LABEL[args.kv], "parallelism": "single-gpu"},
                 **out, "wall_s": round(time.perf_counter() - t0, 1)}
