@@ -401,11 +401,16 @@ eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, con
   const int kind = mode == EB_MODE_DECODE ? 0 : (mode == EB_MODE_PREFILL ? 1 : 2);
   EB_STAGE(3, launch_attention(sh, B.qkv, kvd, m, B.attn, B.part_o, B.part_ml, kind, st, 1), "attention");
   EB_STAGE(4, launch_attention(sh, B.qkv, kvd, m, B.attn, B.part_o, B.part_ml, kind, st, 2), "attention combine");
+  // when the O projection splits K (decode-sized batches) its split-K sum
+  // also writes RMSNorm(h1) * g2, and stage 6 has nothing left to do
+  NormFuse nf{static_cast<const uint16_t *>(w->mlp_norm), B.act, sh.eps, false};
   EB_STAGE(5,
            launch_gemm(plan_gemm(T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, w8), B.attn, w->w_o,
-                       w8 ? w->s_o : nullptr, B.h1, xin, T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, B.gws, st),
+                       w8 ? w->s_o : nullptr, B.h1, xin, T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, B.gws, st, &nf),
            "o gemm");
-  EB_STAGE(6, launch_rmsnorm(B.h1, static_cast<const uint16_t *>(w->mlp_norm), B.act, T, sh.hidden, sh.eps, st),
+  EB_STAGE(6,
+           nf.done ? hipSuccess
+                   : launch_rmsnorm(B.h1, static_cast<const uint16_t *>(w->mlp_norm), B.act, T, sh.hidden, sh.eps, st),
            "rmsnorm2");
   if (sh.moe()) {
     // the mixture-of-experts block: stage 7 routes and runs the gate/up

@@ -88,8 +88,18 @@ struct GemmPlan {
 // w8: W holds 8-bit E4M3 codes with one fp32 scale per row (launch_gemm's
 // wscale, null for bf16 weights); such plans never take the tiled kernel.
 GemmPlan plan_gemm(int M, int N, int K, int epi, bool w8 = false);
+// With nf, a residual GEMM whose plan splits K also writes the RMSNorm of
+// its result rows (gamma, out, eps) from the split-K sum and sets nf->done;
+// otherwise nf->done stays false and the caller runs the norm itself.
+struct NormFuse {
+  const uint16_t *gamma;
+  uint16_t *out;
+  float eps;
+  bool done;
+};
 hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, const float *wscale, uint16_t *out,
-                       const uint16_t *residual, int M, int N, int K, int epi, void *ws, hipStream_t st);
+                       const uint16_t *residual, int M, int N, int K, int epi, void *ws, hipStream_t st,
+                       NormFuse *nf = nullptr);
 
 // Mixture-of-experts block.  The grouped GEMM multiplies row tiles of
 // expert-sorted rows (tables [3][max_tiles]: expert, first sorted row, rows;

@@ -738,6 +738,91 @@ __global__ __launch_bounds__(256) void k_gemm_grouped(const uint16_t *__restrict
 // blocks of a column tile run side by side and read W once from HBM).
 constexpr int kSkinnyMaxRows = 256;
 
+// The split-K sum of a residual GEMM and the RMSNorm of its rows in one
+// pass: h = bf16(sum_s part[s] + res) is stored (the splits summed in order,
+// as the split-K epilogue does), then out = bf16(h * inv * g) with inv from
+// the rounded h.  One block per row: thread t takes the 8-column chunks
+// t, t + 256, .. (rows up to 256 * 4 chunks wide), issues the loads of eight
+// splits before adding them, and the sum of squares is reduced across the
+// block.
+constexpr int kFuseMaxChunks = 4;
+__global__ __launch_bounds__(256) void k_splitk_residual_rmsnorm(const float *__restrict__ part, int splits,
+                                                                 const uint16_t *__restrict__ res,
+                                                                 uint16_t *__restrict__ h,
+                                                                 const uint16_t *__restrict__ g,
+                                                                 uint16_t *__restrict__ out, int M, int N,
+                                                                 float eps) {
+  __shared__ float red[4];
+  const int row = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int nch = N >> 3;
+  u32x4_t v[kFuseMaxChunks];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < kFuseMaxChunks; ++j) {
+    const int c = tid + 256 * j;
+    v[j] = u32x4_t{0u, 0u, 0u, 0u};
+    if (c < nch) {
+      f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+      const float *pp = part + (size_t)row * N + c * 8;
+      const size_t stride = (size_t)M * N;
+      for (int s0i = 0; s0i < splits; s0i += 8) {
+        f32x4_t a[8], b[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const bool ok = s0i + q < splits;
+          a[q] = ok ? *reinterpret_cast<const f32x4_t *>(pp + (s0i + q) * stride) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+          b[q] = ok ? *reinterpret_cast<const f32x4_t *>(pp + (s0i + q) * stride + 4) : f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          s0 += a[q];
+          s1 += b[q];
+        }
+      }
+      const u32x4_t r = ld_u32x4(res + (size_t)row * N + c * 8);
+      s0[0] += bf16_lo(r[0]);
+      s0[1] += bf16_hi(r[0]);
+      s0[2] += bf16_lo(r[1]);
+      s0[3] += bf16_hi(r[1]);
+      s1[0] += bf16_lo(r[2]);
+      s1[1] += bf16_hi(r[2]);
+      s1[2] += bf16_lo(r[3]);
+      s1[3] += bf16_hi(r[3]);
+      v[j] = u32x4_t{pack_bf16x2(s0[0], s0[1]), pack_bf16x2(s0[2], s0[3]), pack_bf16x2(s1[0], s1[1]),
+                     pack_bf16x2(s1[2], s1[3])};
+      st_u32x4(h + (size_t)row * N + c * 8, v[j]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float x = bf16_lo(v[j][i]), y = bf16_hi(v[j][i]);
+        ss += x * x + y * y;
+      }
+    }
+  }
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
+  const float inv = 1.0f / sqrtf(tot / (float)N + eps);
+#pragma unroll
+  for (int j = 0; j < kFuseMaxChunks; ++j) {
+    const int c = tid + 256 * j;
+    if (c < nch) {
+      const u32x4_t gv = ld_u32x4(g + c * 8);
+      u32x4_t o;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        o[i] = pack_bf16x2(bf16_lo(v[j][i]) * inv * bf16_lo(gv[i]), bf16_hi(v[j][i]) * inv * bf16_hi(gv[i]));
+      st_u32x4(out + (size_t)row * N + c * 8, o);
+    }
+  }
+}
+
+// The split-K sum and epilogue, or with nf (residual epilogue, rows fit) the
+// sum fused with the RMSNorm of the result rows (nf->done set).
+static hipError_t finish_splitk(const float *part, int splits, uint16_t *out, const uint16_t *res, int M, int N,
+                                int epi, NormFuse *nf, hipStream_t st);
+
 static hipError_t launch_splitk_epilogue(const float *part, int splits, uint16_t *out, const uint16_t *res, int M,
                                          int N, int epi, hipStream_t st) {
   const int outc = epi == EPI_SILU_MUL ? N / 2 : N;
@@ -745,6 +830,17 @@ static hipError_t launch_splitk_epilogue(const float *part, int splits, uint16_t
   const int blocks = (int)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
   hipLaunchKernelGGL(k_gemm_splitk_epilogue, dim3(blocks), dim3(256), 0, st, part, splits, out, res, M, N, epi);
   return hipGetLastError();
+}
+
+static hipError_t finish_splitk(const float *part, int splits, uint16_t *out, const uint16_t *res, int M, int N,
+                                int epi, NormFuse *nf, hipStream_t st) {
+  if (nf && nf->gamma && epi == EPI_RESIDUAL && N % 8 == 0 && N / 8 <= 256 * kFuseMaxChunks) {
+    hipLaunchKernelGGL(k_splitk_residual_rmsnorm, dim3(M), dim3(256), 0, st, part, splits, res, out, nf->gamma,
+                       nf->out, M, N, nf->eps);
+    nf->done = true;
+    return hipGetLastError();
+  }
+  return launch_splitk_epilogue(part, splits, out, res, M, N, epi, st);
 }
 
 static int skinny_splits(int M, int N, int K) {
@@ -799,7 +895,8 @@ GemmPlan plan_gemm(int M, int N, int K, int epi, bool w8) {
 }
 
 hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, const float *wscale, uint16_t *out,
-                       const uint16_t *res, int M, int N, int K, int epi, void *ws, hipStream_t st) {
+                       const uint16_t *res, int M, int N, int K, int epi, void *ws, hipStream_t st, NormFuse *nf) {
+  if (nf) nf->done = false;
   if (M <= 0) return hipSuccess;
   const bool w8 = wscale != nullptr;
   if (p.kind < 0 || (w8 && p.kind == 1)) return hipErrorInvalidValue;
@@ -821,7 +918,7 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, cons
                          epi, per, tiles, mt, per_xcd);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
-    return launch_splitk_epilogue(part, splits, out, res, M, N, epi, st);
+    return finish_splitk(part, splits, out, res, M, N, epi, nf, st);
   }
   if (p.kind == 2) {
     if (p.splits > 1) {  // one launch (the plan only splits a few tiles), then the partial sums
@@ -836,7 +933,7 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, cons
                            W, wscale, out, res, part, M, N, K, epi, tm, tn, per_xcd, p.kt_per, GroupedArgs{});
       hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
-      return launch_splitk_epilogue(part, p.splits, out, res, M, N, epi, st);
+      return finish_splitk(part, p.splits, out, res, M, N, epi, nf, st);
     }
     // rows per launch: A's slice must stay inside a 32-bit buffer range
     const size_t rows_fit = ((((size_t)1 << 31) - 1) / ((size_t)K * 2)) / BG_BM * BG_BM;
