@@ -65,6 +65,23 @@ def test_validate_rejects_unsupported_shapes(field, value):
     assert B.eb_last_error()
 
 
+def test_validate_moe_layers():
+    # the mixture-of-experts layer shapes validate; each rule of the MoE
+    # config fails with EB_ERR_CONFIG (n_experts a multiple of 16 up to 256,
+    # 1 <= top_k <= min(n_experts, 64), expert_ffn a positive multiple of 8,
+    # hidden a multiple of 32; the dense ffn may then be 0, not otherwise)
+    import dataclasses
+    b, bt, pool = _ok_case()
+    assert B.eb_validate(gen.TINY_MOE, b.context_lens, b.chunk_lens, bt, pool, "mixed") == 0
+    assert B.eb_validate(gen.Q30B, b.context_lens, b.chunk_lens, bt, pool, "mixed") == 0
+    for field, value in (("n_experts", 20), ("n_experts", 272), ("top_k", 0), ("top_k", 17), ("expert_ffn", 100),
+                         ("expert_ffn", 0), ("hidden", 264)):
+        shape = dataclasses.replace(gen.TINY_MOE, **{field: value})
+        assert B.eb_validate(shape, b.context_lens, b.chunk_lens, bt, pool, "mixed") == -2, (field, value)
+    assert B.eb_validate(dataclasses.replace(gen.TINY, ffn=0), b.context_lens, b.chunk_lens, bt, pool,
+                         "mixed") == -2
+
+
 def test_validate_batch_errors():
     b, bt, pool = _ok_case()
     ctx, chk = b.context_lens.copy(), b.chunk_lens.copy()
