@@ -809,6 +809,8 @@ def main():
     try:
         cnt = json.load(open(COUNTERS))
         key = {"decode8b": "decode_attention_8b", "decode70b": "decode_attention_70b"}.get(args.workload)
+        if args.workload == "mixed8b" and args.r == 0.5 and args.budget == 2048:
+            key = "mixed_attention_8b"  # (counters taken at the default share and budget only)
         key = key + "_fp8" if key and args.kv == "fp8" else key
         ent = cnt.get(key) if key else None
         if ent and ent.get("source_sha") == sha_of(ATTN_SRC):
