@@ -55,6 +55,7 @@ class LayerCfg:
     top_k: int = 0
     expert_ffn: int = 0
     moe_renormalize: bool = True
+    qk_norm: bool = False       # RMSNorm of every q and k head (gains q_norm, k_norm) before RoPE
 
     @property
     def group(self) -> int:
@@ -210,7 +211,8 @@ def prepare_weights(w_bits: Dict[str, np.ndarray], cfg: LayerCfg, dtype=np.float
     A projection given as 8-bit E4M3 codes (uint8) comes with its per-row
     scales under "s_" + the name without "w_" (s_qkv, s_o, s_gate_up,
     s_down): its weights are decode(code) * scale of the row, formed in
-    float64.  The norm gains are always bf16.
+    float64.  The norm gains are always bf16 (q_norm, k_norm [head_dim]
+    when cfg.qk_norm).
     """
     nq, nkv, hd, f = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.ffn
 
@@ -222,6 +224,8 @@ def prepare_weights(w_bits: Dict[str, np.ndarray], cfg: LayerCfg, dtype=np.float
     qkv = cv("w_qkv")
     W = {"g1": cv("attn_norm"), "g2": cv("mlp_norm"),
          "wq": qkv[: nq * hd], "wk": qkv[nq * hd: (nq + nkv) * hd], "wv": qkv[(nq + nkv) * hd:], "wo": cv("w_o")}
+    if cfg.qk_norm:
+        W["gq"], W["gk"] = cv("q_norm"), cv("k_norm")
     if cfg.n_experts:
         # the MoE block works from the bf16 weights themselves
         W["moe"] = (w_bits["w_router"], w_bits["w_experts_gate_up"], w_bits["w_experts_down"])
@@ -261,7 +265,9 @@ def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
     mode 'exact': one row at a time with matrix-vector products, rows of a
     request in order (append the row's K/V, then attend).  mode 'batched': the
     same definition with one matrix product per request and an explicit
-    causal mask.  Returns y [T, hidden] and, if asked, a dict of the
+    causal mask.  With cfg.qk_norm every q and k head is RMS-normalised
+    over its head_dim values and scaled by its gain before RoPE (the Qwen3
+    attention block).  Returns y [T, hidden] and, if asked, a dict of the
     intermediates q, k, v (after RoPE), attn, h1, m.
     """
     ks, vs = kv_scales if kv_scales is not None else (None, None)
@@ -277,6 +283,9 @@ def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
              (("q", (nq, hd)), ("k", (nkv, hd)), ("v", (nkv, hd)), ("attn", (nq * hd,)),
               ("h1", (cfg.hidden,)), ("m", (cfg.ffn,)))} if intermediates else None
     todo = range(len(ctx)) if seqs is None else seqs
+
+    def head_norm(u, gain):
+        return rmsnorm(u, W[gain], cfg.rms_eps) if cfg.qk_norm else u
     for i in todo:
         r0, n, c = int(off[i]), int(chk[i]), int(ctx[i])
         bt = block_tables[i]
@@ -284,8 +293,8 @@ def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
             for j in range(n):
                 r, pos = r0 + j, c + j
                 a = rmsnorm(x[r], W["g1"], cfg.rms_eps)
-                q = rope((W["wq"] @ a).reshape(nq, hd), pos, cfg.rope_theta)
-                k = rope((W["wk"] @ a).reshape(nkv, hd), pos, cfg.rope_theta)
+                q = rope(head_norm((W["wq"] @ a).reshape(nq, hd), "gq"), pos, cfg.rope_theta)
+                k = rope(head_norm((W["wk"] @ a).reshape(nkv, hd), "gk"), pos, cfg.rope_theta)
                 v = (W["wv"] @ a).reshape(nkv, hd)
                 append_kv(k_cache, bt, np.array([pos]), k[None], P, ks)
                 append_kv(v_cache, bt, np.array([pos]), v[None], P, vs)
@@ -300,8 +309,8 @@ def layer_step(cfg: LayerCfg, W: dict, k_cache: np.ndarray, v_cache: np.ndarray,
             rows = slice(r0, r0 + n)
             pos = c + np.arange(n)
             a = rmsnorm(x[rows], W["g1"], cfg.rms_eps)
-            q = rope((a @ W["wq"].T).reshape(n, nq, hd), pos, cfg.rope_theta)
-            k = rope((a @ W["wk"].T).reshape(n, nkv, hd), pos, cfg.rope_theta)
+            q = rope(head_norm((a @ W["wq"].T).reshape(n, nq, hd), "gq"), pos, cfg.rope_theta)
+            k = rope(head_norm((a @ W["wk"].T).reshape(n, nkv, hd), "gk"), pos, cfg.rope_theta)
             v = (a @ W["wv"].T).reshape(n, nkv, hd)
             append_kv(k_cache, bt, pos, k, P, ks)
             append_kv(v_cache, bt, pos, v, P, vs)

@@ -42,6 +42,8 @@ class LayerShape:
     n_experts: int = 0
     top_k: int = 0
     expert_ffn: int = 0
+    # per-head RMSNorm of q and k before RoPE (Qwen3), gains [head_dim] each
+    qk_norm: bool = False
 
     @property
     def group(self) -> int:
@@ -56,7 +58,7 @@ class LayerShape:
         if self.n_experts:
             n = self.qkv_rows * d + d * self.n_q_heads * self.head_dim + 2 * d + self.n_experts * d + \
                 self.n_experts * 3 * self.expert_ffn * d
-            return 2 * n
+            return 2 * n + (4 * self.head_dim if self.qk_norm else 0)
         n = self.qkv_rows * d + d * self.n_q_heads * self.head_dim + 2 * f * d + d * f + 2 * d
         return 2 * n
 
@@ -72,8 +74,11 @@ L70B = LayerShape("llama3-70b", 8192, 64, 8, 128, 28672, 5e5)
 # the feed-forward replaced by the MoE block.  Qwen3-30B-A3B shapes: hidden
 # 2048, 32 q / 4 kv heads of 128, 128 experts, 8 per token, width 768, RoPE
 # theta 1e6; and a tiny one for the parity tests.
-Q30B = LayerShape("qwen3-30b-a3b", 2048, 32, 4, 128, 0, 1e6, n_experts=128, top_k=8, expert_ffn=768)
-TINY_MOE = LayerShape("tiny-moe", 256, 4, 2, 64, 0, 1e4, n_experts=16, top_k=4, expert_ffn=128)
+Q30B = LayerShape("qwen3-30b-a3b", 2048, 32, 4, 128, 0, 1e6, n_experts=128, top_k=8, expert_ffn=768,
+                   qk_norm=True)
+TINY_MOE = LayerShape("tiny-moe", 256, 4, 2, 64, 0, 1e4, n_experts=16, top_k=4, expert_ffn=128, qk_norm=True)
+# the dense tiny layer with the Qwen3 q/k norms
+TINY_QKN = LayerShape("tiny-qk-norm", 256, 4, 2, 64, 688, 1e4, qk_norm=True)
 
 SHAPES = {s.name: s for s in (TINY, L8B, L70B, Q30B, TINY_MOE)}
 
@@ -127,8 +132,13 @@ def make_weights(shape: LayerShape, seed: Optional[int] = None, device="cpu",
             w[r0:r1] = (torch.randn(r1 - r0, cols, generator=g, device=device) * proj_std).to(torch.bfloat16)
         return w
 
-    def gain():
-        return (1.0 + 0.1 * torch.randn(d, generator=g, device=device)).to(torch.bfloat16)
+    def gain(n=d):
+        return (1.0 + 0.1 * torch.randn(n, generator=g, device=device)).to(torch.bfloat16)
+
+    def with_qk_norm(w):
+        if shape.qk_norm:
+            w.update({"q_norm": gain(hd), "k_norm": gain(hd)})
+        return w
 
     if shape.n_experts:  # attention as above, a mixture-of-experts feed-forward
         w = {"attn_norm": gain(), "w_qkv": proj(shape.qkv_rows, d), "w_o": proj(d, shape.n_q_heads * hd),
@@ -137,15 +147,15 @@ def make_weights(shape: LayerShape, seed: Optional[int] = None, device="cpu",
                                seed=seed + 1, device=device, proj_std=proj_std)
         w.update({"w_router": moe["w_router"], "w_experts_gate_up": moe["w_gate_up"],
                   "w_experts_down": moe["w_down"]})
-        return w
-    return {
+        return with_qk_norm(w)
+    return with_qk_norm({
         "attn_norm": gain(),
         "w_qkv": proj(shape.qkv_rows, d),
         "w_o": proj(d, shape.n_q_heads * hd),
         "mlp_norm": gain(),
         "w_gate_up": proj(2 * f, d),
         "w_down": proj(d, f),
-    }
+    })
 
 
 # ----------------------------------------------------------------------------

@@ -14,7 +14,7 @@ import oracle
 def oracle_cfg(shape: gen.LayerShape) -> oracle.LayerCfg:
     return oracle.LayerCfg(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn,
                            shape.page_size, shape.rms_eps, shape.rope_theta, shape.n_experts, shape.top_k,
-                           shape.expert_ffn)
+                           shape.expert_ffn, qk_norm=shape.qk_norm)
 
 
 @dataclasses.dataclass

@@ -7,15 +7,22 @@ from oracle import layer as L
 
 
 def hf_layer(shape, w_bits):
-    from transformers import LlamaConfig
-    from transformers.models.llama.modeling_llama import LlamaDecoderLayer, LlamaRotaryEmbedding
-    cfg = LlamaConfig(hidden_size=shape.hidden, intermediate_size=shape.ffn,
+    """The Llama decoder layer, or for a shape with q/k norms the Qwen3 one."""
+    if shape.qk_norm:
+        from transformers import Qwen3Config as Config
+        from transformers.models.qwen3.modeling_qwen3 import Qwen3DecoderLayer as Layer
+        from transformers.models.qwen3.modeling_qwen3 import Qwen3RotaryEmbedding as Rotary
+    else:
+        from transformers import LlamaConfig as Config
+        from transformers.models.llama.modeling_llama import LlamaDecoderLayer as Layer
+        from transformers.models.llama.modeling_llama import LlamaRotaryEmbedding as Rotary
+    cfg = Config(hidden_size=shape.hidden, intermediate_size=shape.ffn,
                       num_attention_heads=shape.n_q_heads, num_key_value_heads=shape.n_kv_heads,
                       head_dim=shape.head_dim, rms_norm_eps=shape.rms_eps, rope_theta=shape.rope_theta,
                       attention_bias=False, mlp_bias=False)
     cfg._attn_implementation = "sdpa"  # the eager path takes its softmax in fp32
-    layer = LlamaDecoderLayer(cfg, layer_idx=0).double()
-    rot = LlamaRotaryEmbedding(cfg).double()
+    layer = Layer(cfg, layer_idx=0).double()
+    rot = Rotary(cfg).double()
     # the library forms its frequencies in fp32; recompute them in fp64
     hd = shape.head_dim
     rot.inv_freq = shape.rope_theta ** (-torch.arange(0, hd, 2, dtype=torch.float64) / hd)
@@ -31,6 +38,9 @@ def hf_layer(shape, w_bits):
     # the library's RMSNorm module computes in fp32; use torch's in fp64
     layer.input_layernorm = torch.nn.RMSNorm(shape.hidden, eps=shape.rms_eps, dtype=torch.float64)
     layer.post_attention_layernorm = torch.nn.RMSNorm(shape.hidden, eps=shape.rms_eps, dtype=torch.float64)
+    if shape.qk_norm:
+        layer.self_attn.q_norm = torch.nn.RMSNorm(shape.head_dim, eps=shape.rms_eps, dtype=torch.float64)
+        layer.self_attn.k_norm = torch.nn.RMSNorm(shape.head_dim, eps=shape.rms_eps, dtype=torch.float64)
     with torch.no_grad():
         layer.self_attn.q_proj.weight.copy_(qkv[: nq * hd])
         layer.self_attn.k_proj.weight.copy_(qkv[nq * hd:(nq + nkv) * hd])
@@ -41,6 +51,9 @@ def hf_layer(shape, w_bits):
         layer.mlp.down_proj.weight.copy_(f("w_down"))
         layer.input_layernorm.weight.copy_(f("attn_norm"))
         layer.post_attention_layernorm.weight.copy_(f("mlp_norm"))
+        if shape.qk_norm:
+            layer.self_attn.q_norm.weight.copy_(f("q_norm"))
+            layer.self_attn.k_norm.weight.copy_(f("k_norm"))
     return layer, rot
 
 

@@ -423,3 +423,53 @@ def test_stack_of_identity_layers_returns_x():
     assert np.array_equal(L.f32_to_bf16_bits(y.astype(np.float32)), x_bits)
     for k, kb in zip(ks, before):
         assert not np.array_equal(k, kb)
+
+
+@pytest.mark.parametrize("mode", ["batched", "exact"])
+def test_layer_with_qk_norm_matches_transformers_qwen3_layer(mode):
+    # the Qwen3 attention block: RMSNorm of every q and k head before RoPE
+    shape = gen.TINY_QKN
+    case = make_case(shape, _HF_BATCH, weights=gen.make_weights(shape, proj_std=0.2))
+    (y, inter), o = case.run_oracle(mode=mode, dtype=np.float64, intermediates=True)
+    o0 = case.oracle_inputs()
+    x = L.bf16_bits_to_f32(o0["x_bits"]).astype(np.float64)
+    off = _HF_BATCH.row_offsets
+    for i in range(_HF_BATCH.num_seqs):
+        rows = slice(off[i], off[i + 1])
+        attn_b, _, y_ref = _hf_reference(shape, o0, i)
+        assert maxrel(inter["h1"][rows] - x[rows], attn_b) < 1e-9
+        assert maxrel(y[rows], y_ref) < 1e-9
+
+
+def test_qk_norm_planted_mistakes_are_caught(monkeypatch):
+    # the norms left out, taken over all of a row's q (or k) heads at once,
+    # or the two gains swapped: each moves the attention branch far outside
+    # the 1e-9 bound above
+    import dataclasses
+    shape = gen.TINY_QKN
+    case = make_case(shape, _HF_BATCH, weights=gen.make_weights(shape, proj_std=0.2))
+    o0 = case.oracle_inputs()
+    x = L.bf16_bits_to_f32(o0["x_bits"]).astype(np.float64)
+    off = _HF_BATCH.row_offsets
+    refs = [_hf_reference(shape, o0, i)[0] for i in range(_HF_BATCH.num_seqs)]
+    good = L.rmsnorm
+
+    def whole_row(u, gamma, eps):
+        if gamma.shape[0] != u.shape[-1]:
+            return good(u, gamma, eps)
+        flat = u.reshape(u.shape[:-2] + (-1,))
+        return good(flat, np.tile(gamma, u.shape[-2]), eps).reshape(u.shape)
+
+    def run(cfg, w_bits):
+        W = oracle.prepare_weights(w_bits, cfg, np.float64)
+        _, inter = oracle.layer_step(cfg, W, o0["k_cache"].copy(), o0["v_cache"].copy(), o0["block_tables"],
+                                     o0["context_lens"], o0["chunk_lens"], o0["x_bits"], intermediates=True)
+        return max(maxrel(inter["h1"][off[i]:off[i + 1]] - x[off[i]:off[i + 1]], refs[i])
+                   for i in range(_HF_BATCH.num_seqs))
+    assert run(o0["cfg"], o0["w_bits"]) < 1e-9
+    assert run(dataclasses.replace(o0["cfg"], qk_norm=False), o0["w_bits"]) > 1e-3, "no norms"
+    swapped = dict(o0["w_bits"], q_norm=o0["w_bits"]["k_norm"], k_norm=o0["w_bits"]["q_norm"])
+    assert run(o0["cfg"], swapped) > 1e-3, "gains swapped"
+    with monkeypatch.context() as mp:
+        mp.setattr(L, "rmsnorm", whole_row)
+        assert run(o0["cfg"], o0["w_bits"]) > 1e-3, "norm over the whole row"
