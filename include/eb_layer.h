@@ -75,11 +75,15 @@ typedef enum eb_epilogue {
  * eb_op_moe_ffn (top_k experts per token, expert SwiGLU width expert_ffn,
  * renormalised weights unless moe_renormalize is 0; ffn is then unused and
  * may be 0); n_experts = 0 (a zero-initialised tail) is the dense SwiGLU of
- * width ffn. */
+ * width ffn.  qk_norm != 0 (the Qwen3 attention block): every q and k head of
+ * the QKV projection is RMS-normalised over its head_dim values (epsilon
+ * rms_eps, fp32) and multiplied by the gain q_norm or k_norm before RoPE;
+ * 0 (a zero-initialised tail): no such norm. */
 typedef struct eb_layer_config {
   int32_t hidden, n_q_heads, n_kv_heads, head_dim, ffn, page_size;
   float rms_eps, rope_theta;
   int32_t n_experts, top_k, expert_ffn, moe_renormalize;
+  int32_t qk_norm;
 } eb_layer_config;
 
 /* Element type of the four projection matrices. */
@@ -110,6 +114,9 @@ typedef struct eb_layer_weights {
    * [E, 2 expert_ffn, hidden] (per expert gate rows, then up rows) and down
    * [E, hidden, expert_ffn] */
   const void *w_router, *w_experts_gate_up, *w_experts_down;
+  /* per-head q and k norm gains, bf16 [head_dim] each (qk_norm layers;
+   * unused otherwise) */
+  const void *q_norm, *k_norm;
 } eb_layer_weights;
 
 /* Element type of the KV cache. */
@@ -281,7 +288,9 @@ eb_status eb_op_moe_ffn(const void *b, const void *residual, const void *w_route
 
 /* RoPE on the q and k heads of qkv (bf16 [num_tokens, (n_q + 2 n_kv) head_dim],
  * the QKV projection output) at pos = c_i + j; q is rotated in place, the
- * rotated k and the v heads are written to the cache. */
+ * rotated k and the v heads are written to the cache.  A handle whose config
+ * has qk_norm set gets EB_ERR_CONFIG: this entry has no norm gains (the layer
+ * step entry points apply the norms). */
 eb_status eb_op_rope_kv_append(eb_handle *h, void *qkv, const eb_kv_cache *kv, const eb_batch *batch,
                                void *ws, size_t ws_bytes, void *stream);
 

@@ -43,13 +43,13 @@ class LayerConfig(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32), ("page_size", ctypes.c_int32),
                 ("rms_eps", ctypes.c_float), ("rope_theta", ctypes.c_float),
                 ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32), ("expert_ffn", ctypes.c_int32),
-                ("moe_renormalize", ctypes.c_int32)]
+                ("moe_renormalize", ctypes.c_int32), ("qk_norm", ctypes.c_int32)]
 
 
 class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")] + \
         [("w_dtype", ctypes.c_int32)] + [(n, ctypes.c_void_p) for n in ("s_qkv", "s_o", "s_gate_up", "s_down")] + \
-        [(n, ctypes.c_void_p) for n in ("w_router", "w_experts_gate_up", "w_experts_down")]
+        [(n, ctypes.c_void_p) for n in ("w_router", "w_experts_gate_up", "w_experts_down", "q_norm", "k_norm")]
 
 
 W_BF16, W_FP8_E4M3 = 0, 1
@@ -139,7 +139,7 @@ def config_of(shape) -> LayerConfig:
     return LayerConfig(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.ffn,
                        getattr(shape, "page_size", 16), float(shape.rms_eps), float(shape.rope_theta),
                        getattr(shape, "n_experts", 0), getattr(shape, "top_k", 0), getattr(shape, "expert_ffn", 0),
-                       1 if getattr(shape, "moe_renormalize", True) else 0)
+                       1 if getattr(shape, "moe_renormalize", True) else 0, 1 if getattr(shape, "qk_norm", False) else 0)
 
 
 class HostBatch:
@@ -171,9 +171,10 @@ def weights_struct(w: dict) -> LayerWeights:
     """Weights dict -> struct: bf16 projections, or uint8 / float8_e4m3fn
     codes with float32 row scales under s_qkv, s_o, s_gate_up, s_down;
     a mixture-of-experts layer brings w_router, w_experts_gate_up and
-    w_experts_down instead of w_gate_up and w_down."""
+    w_experts_down instead of w_gate_up and w_down; a layer with q/k norms
+    brings their gains under q_norm and k_norm."""
     lw = LayerWeights(*[_ptr(w.get(k)) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")])
-    for k in ("w_router", "w_experts_gate_up", "w_experts_down"):
+    for k in ("w_router", "w_experts_gate_up", "w_experts_down", "q_norm", "k_norm"):
         if k in w:
             setattr(lw, k, _ptr(w[k]))
     if w["w_qkv"].dtype in _CODE_DTYPES:

@@ -44,6 +44,7 @@ Shape shape_of(const eb_layer_config &c) {
     s.effn = c.expert_ffn;
     s.renorm = c.moe_renormalize ? 1 : 0;
   }
+  s.qkn = c.qk_norm ? 1 : 0;
   return s;
 }
 
@@ -319,6 +320,7 @@ KV kv_of(const eb_kv_cache *kv) {
 eb_status check_weights(const eb_layer_weights *w, const Shape &sh, int T) {
   if (!w || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm)
     return fail(EB_ERR_NULL, "a weight pointer is NULL");
+  if (sh.qkn && (!w->q_norm || !w->k_norm)) return fail(EB_ERR_NULL, "q_norm or k_norm is NULL");
   if (sh.moe()) {
     if (!w->w_router || !w->w_experts_gate_up || !w->w_experts_down)
       return fail(EB_ERR_NULL, "a mixture-of-experts weight pointer is NULL");
@@ -397,7 +399,10 @@ eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, con
            launch_gemm(plan_gemm(T, sh.qkv_cols(), sh.hidden, EPI_STORE, w8), B.act, w->w_qkv,
                        w8 ? w->s_qkv : nullptr, B.qkv, nullptr, T, sh.qkv_cols(), sh.hidden, EPI_STORE, B.gws, st),
            "qkv gemm");
-  EB_STAGE(2, launch_rope_append(sh, B.qkv, kvd, m, st), "rope/kv append");
+  EB_STAGE(2,
+           launch_rope_append(sh, B.qkv, kvd, m, st, static_cast<const uint16_t *>(w->q_norm),
+                              static_cast<const uint16_t *>(w->k_norm)),
+           "rope/kv append");
   const int kind = mode == EB_MODE_DECODE ? 0 : (mode == EB_MODE_PREFILL ? 1 : 2);
   EB_STAGE(3, launch_attention(sh, B.qkv, kvd, m, B.attn, B.part_o, B.part_ml, kind, st, 1), "attention");
   EB_STAGE(4, launch_attention(sh, B.qkv, kvd, m, B.attn, B.part_o, B.part_ml, kind, st, 2), "attention combine");
@@ -772,6 +777,7 @@ eb_status eb_op_rope_kv_append(eb_handle *h, void *qkv, const eb_kv_cache *kv, c
   if (s != EB_OK) return s;
   if (batch->num_tokens == 0) return EB_OK;
   if (!qkv) return fail(EB_ERR_NULL, "qkv is NULL");
+  if (h->shape.qkn) return fail(EB_ERR_CONFIG, "qk_norm layers: the norm gains come with the layer step entry points");
   HostPlan p;
   build_plan(h->cfg, *batch, EB_MODE_MIXED, p);
   const WsLayout L = layout_for(h->shape, p, false);

@@ -60,6 +60,7 @@ struct Shape {
   int32_t hidden, nq, nkv, hd, ffn;
   float eps, theta;
   int32_t ne = 0, topk = 0, effn = 0, renorm = 1;  // mixture-of-experts feed-forward when ne > 0
+  int32_t qkn = 0;                                  // per-head q/k RMSNorm before RoPE
   bool moe() const { return ne > 0; }
   int32_t qkv_cols() const { return (nq + 2 * nkv) * hd; }
   int32_t group() const { return nq / nkv; }
@@ -68,7 +69,9 @@ struct Shape {
 // ---- launchers (each returns the launch error) ----
 hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gamma, uint16_t *out, int rows, int d, float eps,
                           hipStream_t st);
-hipError_t launch_rope_append(const Shape &s, uint16_t *qkv, const KV &kv, const DevMeta &m, hipStream_t st);
+// gq, gk: the per-head norm gains, required when s.qkn
+hipError_t launch_rope_append(const Shape &s, uint16_t *qkv, const KV &kv, const DevMeta &m, hipStream_t st,
+                              const uint16_t *gq = nullptr, const uint16_t *gk = nullptr);
 hipError_t launch_gather_kv(const Shape &s, const KV &kv, const DevMeta &m, uint16_t *out_k, uint16_t *out_v,
                             hipStream_t st);
 

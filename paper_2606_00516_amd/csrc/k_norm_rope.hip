@@ -104,12 +104,16 @@ __device__ __forceinline__ u32x2_t e4m3x8_of_bf16x8(u32x4_t w, float scale) {
 // taken in fp32 (the reduced angle is small, so fp32 is accurate to an ulp).
 // ---------------------------------------------------------------------------
 // With an 8-bit cache (F8) the new K and V enter as codes of their bf16
-// values divided by the scale (the division rounded in fp32).
-template <bool F8>
+// values divided by the scale (the division rounded in fp32).  With QKN each
+// q and k head is first RMS-normalised over its hd values and scaled by its
+// gain (gq for q heads, gk for k heads), in fp32, before the rotation.
+template <bool F8, bool QKN>
 __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv, uint16_t *__restrict__ kc,
                                                      uint16_t *__restrict__ vc, const int32_t *__restrict__ bt,
                                                      int num_pages, int max_pages, DevMeta m, int nq, int nkv,
-                                                     int hd, double log2_theta, float ks, float vs) {
+                                                     int hd, double log2_theta, float ks, float vs,
+                                                     const uint16_t *__restrict__ gq,
+                                                     const uint16_t *__restrict__ gk, float eps) {
   __shared__ float cs[64], sn[64];
   const int r = blockIdx.x;
   const int seq = m.row_seq[r];
@@ -138,11 +142,38 @@ __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv,
     const int h = i / hch, t0 = (i - h * hch) * 8;
     const u32x4_t a = ld_u32x4(row + h * hd + t0);
     const u32x4_t b = ld_u32x4(row + h * hd + t0 + half);
+    float fa[8], fb[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      fa[2 * e] = bf16_lo(a[e]);
+      fa[2 * e + 1] = bf16_hi(a[e]);
+      fb[2 * e] = bf16_lo(b[e]);
+      fb[2 * e + 1] = bf16_hi(b[e]);
+    }
+    if constexpr (QKN) {
+      // the hch threads of one head are adjacent lanes of one wavefront (hch
+      // divides 64 and the thread count, items is a multiple of hch), all
+      // active together: the head's sum of squares in log2(hch) exchanges
+      float ss = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ss += fa[e] * fa[e] + fb[e] * fb[e];
+      for (int o = 1; o < hch; o <<= 1) ss += __shfl_xor(ss, o, 64);
+      const float rs = 1.f / sqrtf(ss / (float)hd + eps);
+      const uint16_t *gain = h < nq ? gq : gk;
+      const u32x4_t ga = ld_u32x4(gain + t0), gb = ld_u32x4(gain + t0 + half);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        fa[2 * e] = fa[2 * e] * rs * bf16_lo(ga[e]);
+        fa[2 * e + 1] = fa[2 * e + 1] * rs * bf16_hi(ga[e]);
+        fb[2 * e] = fb[2 * e] * rs * bf16_lo(gb[e]);
+        fb[2 * e + 1] = fb[2 * e + 1] * rs * bf16_hi(gb[e]);
+      }
+    }
     u32x4_t ra, rb;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const float c0 = cs[t0 + 2 * e], s0 = sn[t0 + 2 * e], c1 = cs[t0 + 2 * e + 1], s1 = sn[t0 + 2 * e + 1];
-      const float a0 = bf16_lo(a[e]), a1 = bf16_hi(a[e]), b0 = bf16_lo(b[e]), b1 = bf16_hi(b[e]);
+      const float a0 = fa[2 * e], a1 = fa[2 * e + 1], b0 = fb[2 * e], b1 = fb[2 * e + 1];
       ra[e] = pack_bf16x2(a0 * c0 - b0 * s0, a1 * c1 - b1 * s1);
       rb[e] = pack_bf16x2(a0 * s0 + b0 * c0, a1 * s1 + b1 * c1);
     }
@@ -176,14 +207,25 @@ __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv,
   }
 }
 
-hipError_t launch_rope_append(const Shape &s, uint16_t *qkv, const KV &kv, const DevMeta &m, hipStream_t st) {
+hipError_t launch_rope_append(const Shape &s, uint16_t *qkv, const KV &kv, const DevMeta &m, hipStream_t st,
+                              const uint16_t *gq, const uint16_t *gk) {
   if (m.T <= 0) return hipSuccess;
-  if (kv.f8)
-    hipLaunchKernelGGL(k_rope_append<true>, dim3(m.T), dim3(256), 0, st, qkv, kv.k, kv.v, kv.bt, kv.num_pages,
-                       kv.max_pages, m, s.nq, s.nkv, s.hd, log2((double)s.theta), kv.ks, kv.vs);
-  else
-    hipLaunchKernelGGL(k_rope_append<false>, dim3(m.T), dim3(256), 0, st, qkv, kv.k, kv.v, kv.bt, kv.num_pages,
-                       kv.max_pages, m, s.nq, s.nkv, s.hd, log2((double)s.theta), 1.f, 1.f);
+  if (s.qkn && (!gq || !gk)) return hipErrorInvalidValue;
+#define EB_ROPE_APPEND(F8_, QKN_)                                                                                   \
+  hipLaunchKernelGGL((k_rope_append<F8_, QKN_>), dim3(m.T), dim3(256), 0, st, qkv, kv.k, kv.v, kv.bt, kv.num_pages, \
+                     kv.max_pages, m, s.nq, s.nkv, s.hd, log2((double)s.theta), kv.ks, kv.vs, gq, gk, s.eps)
+  if (kv.f8) {
+    if (s.qkn)
+      EB_ROPE_APPEND(true, true);
+    else
+      EB_ROPE_APPEND(true, false);
+  } else {
+    if (s.qkn)
+      EB_ROPE_APPEND(false, true);
+    else
+      EB_ROPE_APPEND(false, false);
+  }
+#undef EB_ROPE_APPEND
   return hipGetLastError();
 }
 
