@@ -66,6 +66,8 @@ def parse():
     ap.add_argument("--weights", default="bf16", choices=["bf16", "fp8"],
                     help="projection weights: bf16, or 8-bit E4M3 codes with one fp32 scale per output row")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="decode8b: skip the prefill step and the MB sweep that the default line carries")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
     ap.add_argument("--json-out", default=None)
     return ap.parse_args()
@@ -199,7 +201,7 @@ def cpu_baseline(shape, batch, w, pool, x, mode, target_s, kv_scales=None):
     # algorithmic bytes of the step-equivalents done: the weights once per
     # whole-workload step (rows / T of them) plus each request's K/V
     gbps = (kv_bytes + weight_bytes(shape, w_kind) * rows / batch.num_tokens) / spent / 1e9
-    return {"value": round(gbps, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+    return {"value": round(gbps, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle", **host_facts(),
             "tokens_per_s": round(rows / spent, 3), "seconds": round(spent, 2),
             "sample": f"{len(done)} request-steps ({rows} rows; {passes} pass(es) over the {batch.num_seqs} requests "
                       f"of the same workload), fp32 numpy oracle in batched mode, one request per call"}
@@ -209,39 +211,74 @@ def cpu_baseline(shape, batch, w, pool, x, mode, target_s, kv_scales=None):
 # timing
 # ----------------------------------------------------------------------------
 
+FLUSH_BYTES = 512 << 20
+_FLUSH = {}
+
+
+def flush_caches(device):
+    """Write a 512 MiB scratch buffer: more than the 256 MB Infinity Cache and
+    the L2s together, so the next step finds none of its operands cached."""
+    import torch
+    buf = _FLUSH.get(str(device))
+    if buf is None:
+        buf = _FLUSH[str(device)] = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=device)
+    buf.zero_()
+
+
+def stats_of(times_ms):
+    import numpy as np
+    t = np.asarray(times_ms, np.float64)
+    return {"mean_ms": round(float(t.mean()), 5), "median_ms": round(float(np.median(t)), 5),
+            "p10_ms": round(float(np.percentile(t, 10)), 5), "p90_ms": round(float(np.percentile(t, 90)), 5),
+            "n": int(t.size)}
+
+
 def measure(B, h, step_fn, w, pool, batch, x, y, ws, steps, warmup, kv_scales=None, timed_stage=None):
-    """(ms per step over ``steps`` back-to-back steps, per-stage ms, ms of
-    ``timed_stage``).  In the timed region the library brackets only
-    ``timed_stage`` with HIP events on the step's stream (two markers per step,
-    in a ring of ``steps`` slots created before the region), so its mean
-    comes from the timed steps themselves without making them host bound; the
-    full per-stage breakdown (a marker at every stage boundary) comes from a
-    second pass of as many steps."""
+    """(mean ms per step, per-stage ms, ms of ``timed_stage``, timing stats).
+
+    Every timed step is preceded by a 512 MiB cache flush outside its own
+    pair of HIP events (recorded on the step's stream), so each step starts
+    cold and the flush is not timed; the stats give the mean, median, p10
+    and p90 of the per-step times and the wall time per step of the whole
+    bracketed region (flushes included).  In the timed steps the library
+    also brackets ``timed_stage`` with HIP events of its own (two markers
+    per step, in a ring of ``steps`` slots created before the region), so its
+    mean comes from the timed steps themselves; the full per-stage breakdown
+    (a marker at every stage boundary) comes from a second pass of as many
+    steps, flushed the same way."""
     import torch
     call = lambda: step_fn(h, w, pool.k_cache, pool.v_cache, pool.block_tables, batch.context_lens,  # noqa: E731
                            batch.chunk_lens, x, y=y, ws=ws, kv_scales=kv_scales)
     for _ in range(warmup):
+        flush_caches(x.device)
         call()
     if timed_stage:
         B.eb_profile(h, True, steps=steps, stages=[timed_stage])
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(steps):
+    for a, b in evs:
+        flush_caches(x.device)
+        a.record()
         call()
+        b.record()
     torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) / steps * 1e3
+    wall_ms = (time.perf_counter() - t0) / steps * 1e3
+    st = stats_of([a.elapsed_time(b) for a, b in evs])
+    st["wall_ms_per_step_incl_flush"] = round(wall_ms, 5)
     timed = B.eb_profile_read(h)[timed_stage] if timed_stage else None
     B.eb_profile(h, True, steps=steps)
     for _ in range(steps):
+        flush_caches(x.device)
         call()
     stages = B.eb_profile_read(h)
     B.eb_profile(h, False)
-    return ms, stages, timed
+    return st["mean_ms"], stages, timed, st
 
 
-def sweep(args, dev):
+def sweep(args, dev, budgets=None, w=None):
     """Mixed step of the chosen layer (the 8B one by default) over decode
-    shares 0, 0.1, .., 1 at several budgets."""
+    shares 0, 0.1, .., 1 at several budgets (``budgets``, else --budgets)."""
     import numpy as np
     import torch
 
@@ -249,8 +286,10 @@ def sweep(args, dev):
     from paper_2606_00516_amd import binding as B
     from paper_2606_00516_amd import inputs as gen
     shape = gen.Q30B if args.shape == "q30b" else gen.L8B
-    w = gen.make_weights(shape, device=dev)
-    budgets = [int(b) for b in args.budgets.split(",")]
+    if w is None:
+        w = gen.make_weights(shape, device=dev)
+    if budgets is None:
+        budgets = [int(b) for b in args.budgets.split(",")]
     rs = [round(0.1 * i, 1) for i in range(11)]
     dec_ctx = (16, 16) if args.ctx16 else (1024, 8192)
     if args.dec_ctx:
@@ -266,14 +305,20 @@ def sweep(args, dev):
         ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
         fn = {"decode": B.eb_layer_step_decode, "prefill": B.eb_layer_step_prefill,
               "mixed": B.eb_layer_step_mixed}[mode]
-        ms, st, _ = measure(B, h, fn, w, pool, batch, x, y, ws, args.steps, args.warmup, kv_scales=kvs)
+        ms, st, _, tst = measure(B, h, fn, w, pool, batch, x, y, ws, args.steps, args.warmup, kv_scales=kvs)
         del pool, x, y, ws, h
         torch.cuda.empty_cache()
         gemm = sum(v for k, v in st.items() if k.endswith("gemm"))
         attn = st.get("attention", 0.0) + st.get("attention_combine", 0.0)
         wk = step_work(shape, batch, 1 if args.kv == "fp8" else 2)
-        return {"ms": ms, "gemm_ms": gemm, "attention_ms": attn, "other_ms": sum(st.values()) - gemm - attn,
-                "kv_bytes_decode": wk["kv_bytes_decode"], "n_tok": wk["T"], "n_decode": batch.num_decode}
+        kv_b = wk["kv_bytes_decode"] + wk["kv_bytes_prefill"]
+        a_ms = st.get("attention", 0.0)
+        return {"ms": ms, "median_ms": tst["median_ms"], "p10_ms": tst["p10_ms"], "p90_ms": tst["p90_ms"],
+                "gemm_ms": gemm, "attention_ms": attn, "other_ms": sum(st.values()) - gemm - attn,
+                "kv_bytes_decode": wk["kv_bytes_decode"], "kv_bytes": kv_b,
+                "attention_kernel_hbm_frac": round(kv_b / (a_ms / 1e3) / 1e9 / HBM_PEAK_GBPS, 4) if a_ms else None,
+                "gemm_tflops": round(wk["gemm_flops"] / (gemm / 1e3) / 1e12, 1) if gemm else None,
+                "n_tok": wk["T"], "n_decode": batch.num_decode}
 
     for bud in budgets:
         for r in rs:
@@ -470,7 +515,7 @@ def long8b(args, dev):
         h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
         ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
         fn = {"decode": B.eb_layer_step_decode, "prefill": B.eb_layer_step_prefill}[mode]
-        ms, st, _ = measure(B, h, fn, w, pool, batch, x, y, ws, steps, 1, kv_scales=kvs)
+        ms, st, _, _ = measure(B, h, fn, w, pool, batch, x, y, ws, steps, 1, kv_scales=kvs)
         del pool, x, y, ws, h
         torch.cuda.empty_cache()
         wk = step_work(shape, batch, 1 if args.kv == "fp8" else 2)
@@ -583,7 +628,7 @@ def q30b(args, dev):
         y = torch.empty_like(x)
         h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
         ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
-        ms, stages, t_att = measure(B, h, step_fn, w, pool, batch, x, y, ws, args.steps, args.warmup,
+        ms, stages, t_att, _ = measure(B, h, step_fn, w, pool, batch, x, y, ws, args.steps, args.warmup,
                                     timed_stage="attention")
         wk = step_work(shape, batch)
         pt = {"point": name, "mode": mode, "tokens": wk["T"], "ms_per_step": round(ms, 5),
@@ -596,6 +641,129 @@ def q30b(args, dev):
         del pool, x, y, ws, h
         torch.cuda.empty_cache()
     return pts
+
+
+def prefill_part(args, dev, w):
+    """The exclusive-prefill step of the 8B layer (8 prompts U[256,2048]
+    capped at 8192 tokens): step TFLOP/s, the gate/up GEMM and the prefill
+    attention kernel against the bf16 MFMA peak."""
+    import torch
+
+    from paper_2606_00516_amd import binding as B
+    from paper_2606_00516_amd import inputs as gen
+    shape, batch = gen.L8B, gen.batch_8b_prefill()
+    pool, kvs = make_pool(gen, shape, batch, "bf16", device=dev)
+    x = gen.make_x(shape, batch.num_tokens, device=dev)
+    y = torch.empty_like(x)
+    h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
+    ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, "prefill"), dev)
+    ms, st, g_ms, tst = measure(B, h, B.eb_layer_step_prefill, w, pool, batch, x, y, ws, args.steps, args.warmup,
+                                timed_stage="gate_up_gemm")
+    del pool, x, y, ws, h
+    torch.cuda.empty_cache()
+    wk = step_work(shape, batch)
+    flops = wk["gemm_flops"] + wk["attn_flops_prefill"]
+    gemm_ms = sum(v for k, v in st.items() if k.endswith("gemm"))
+    fl_gu = 2 * wk["T"] * 2 * shape.ffn * shape.hidden
+    a_ms = st["attention"]
+    return {"workload": "llama3-8b-layer prefill EB: 8 prompts U[256,2048] capped at 8192 tokens, "
+                        f"lengths {batch.chunk_lens.tolist()}",
+            "ms_per_step": ms, **{k: v for k, v in tst.items() if k != "mean_ms"},
+            "step_tflops": round(flops / (ms / 1e3) / 1e12, 1),
+            "step_frac_of_mfma_peak": round(flops / (ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+            "gemm_ms": round(gemm_ms, 5), "gemm_tflops": round(wk["gemm_flops"] / (gemm_ms / 1e3) / 1e12, 1),
+            "gemm_frac": round(wk["gemm_flops"] / (gemm_ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+            "stage_ms": {k: round(v, 5) for k, v in st.items()},
+            "roofline": {"kernel": "k_gemm_big (gate/up projection + SiLU*mul, 256x256 tiles)", "bound": "mfma",
+                         "achieved": round(fl_gu / (g_ms / 1e3) / 1e12, 1), "peak": BF16_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(fl_gu / (g_ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                         "avg_launch_ms": round(g_ms, 5), "flops_per_launch": fl_gu},
+            "attention_roofline": {"kernel": "k_prefill (causal prefill attention, MFMA)", "bound": "mfma",
+                                   "achieved": round(wk["attn_flops_prefill"] / (a_ms / 1e3) / 1e12, 1),
+                                   "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                   "frac": round(wk["attn_flops_prefill"] / (a_ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS,
+                                                 4),
+                                   "avg_launch_ms": round(a_ms, 5), "flops_per_launch": wk["attn_flops_prefill"]}}
+
+
+def sweep_part(args, dev, w, repeats=3):
+    """The 8B MB sweep at the 2048-token budget (decode ctx U[1024,8192],
+    r = 0, 0.1, .., 1) ``repeats`` times, for K(r) and the spread of kappa,
+    and once at budgets 512, 1024 and 4096 for the per-share linear fits
+    T = alpha + beta n_tok and the crossover share."""
+    import copy
+
+    import numpy as np
+
+    from paper_2606_00516_amd import analysis as AN
+    a = copy.copy(args)
+    a.shape, a.ctx16, a.dec_ctx, a.kv = "l8b", False, None, "bf16"
+    runs, pts_all = [], []
+    for _ in range(repeats):
+        out, pts = sweep(a, dev, budgets=[2048], w=w)
+        runs.append(out)
+        pts_all += pts
+        print(f"# sweep B=2048 kappa {out['fit']['kappa']:.4f}", file=sys.stderr, flush=True)
+    _, pts_other = sweep(a, dev, budgets=[512, 1024, 4096], w=w)
+    r = runs[0]["r"]
+    K = np.median(np.array([o["K_ms"] for o in runs]), axis=0)
+    kappas = [o["fit"]["kappa"] for o in runs]
+    rep = AN.sweep_report(r, K)
+    # per-share fits over the four budgets (the 2048 point: median of the repeats)
+    betas, alphas, r2s = [], [], []
+    for i, rr in enumerate(r):
+        ns = [2048] + [p["n_tok"] for p in pts_other if p["r"] == rr and p["mode"] == "mixed"]
+        ts = [float(K[i])] + [p["ms"] for p in pts_other if p["r"] == rr and p["mode"] == "mixed"]
+        al, be, r2 = AN.linear_fit(ns, ts)
+        alphas.append(round(al, 5))
+        betas.append(round(be * 1e3, 5))
+        r2s.append(round(r2, 5))
+    mixed0 = [p for p in pts_all if p["mode"] == "mixed"][:len(r)]
+    eb = {}
+    for mode in ("prefill", "decode"):
+        v = [p["ms"] for p in pts_all if p["mode"] == mode]
+        eb[mode] = round(float(np.median(v)), 5) if v else None
+    return {"workload": "llama3-8b-layer MB sweep: 2048-token steps at r = 0, 0.1, .., 1, decode ctx U[1024,8192], "
+                        "chunks U[256,1024] with prefix U[0,2048]; budgets 512/1024/4096 once for the fits",
+            "r": r, "K_ms": [round(float(k), 5) for k in K],
+            "K_ms_runs": [[round(k, 5) for k in o["K_ms"]] for o in runs],
+            "K_bar_ms": [round(float(k), 5) for k in AN.eb_line(r, K[0], K[-1])],
+            "eb_endpoints_ms": eb,
+            "attention_ms": [round(p["attention_ms"], 5) for p in mixed0],
+            "gemm_ms": [round(p["gemm_ms"], 5) for p in mixed0],
+            "attention_kernel_hbm_frac": [p["attention_kernel_hbm_frac"] for p in mixed0],
+            "kappa": round(float(np.median(kappas)), 4), "kappa_runs": [round(k, 4) for k in kappas],
+            "kappa_spread": round(float(max(kappas) - min(kappas)), 4), "fit_of_median": rep,
+            "alpha_ms": alphas, "beta_us_per_token": betas, "fit_r2": r2s,
+            "crossover_r": AN.crossover_primary(r, betas),
+            "eb_favoured_r": AN.eb_favoured(r, K, 0.02 * float(max(K))),
+            "paper_crossover_context": {"H200 (4.8 TB/s)": 0.8, "RTX PRO 6000 (1.792 TB/s)": 0.2,
+                                        "note": "the paper's crossovers were measured with every decode context "
+                                                "at 16 tokens (Sec. 1, Fig. marginal_cost); this sweep uses "
+                                                "contexts U[1024,8192]"}}
+
+
+def host_facts():
+    """The host the CPU oracle runs on: logical CPUs, model, BLAS."""
+    import platform
+    model = platform.processor() or ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')} ({info[0].get('num_threads')} threads)"
+    except Exception:  # pragma: no cover
+        pass
+    return {"os_cpu_count": os.cpu_count(), "cpu_model": model, "blas": blas,
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
 
 
 def main():
@@ -763,7 +931,7 @@ def main():
     h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
     ws = B.alloc_workspace(B.eb_workspace_bytes(h, batch.context_lens, batch.chunk_lens, mode), dev)
     timed_stage = "gate_up_gemm" if mode == "prefill" else "attention"
-    ms, stages, t_ms = measure(B, h, step_fn, w, pool, batch, x, y, ws, args.steps, args.warmup, kv_scales=kvs,
+    ms, stages, t_ms, tstats = measure(B, h, step_fn, w, pool, batch, x, y, ws, args.steps, args.warmup, kv_scales=kvs,
                                timed_stage=timed_stage)
 
     wk = step_work(shape, batch, 1 if args.kv == "fp8" else 2, args.weights)
@@ -828,6 +996,8 @@ def main():
                    "decode_share": round(batch.num_decode / max(wk["T"], 1), 4), "kv_cache": KV_LABEL[args.kv],
                    "parallelism": "single-gpu"},
         "tokens_per_s": round(wk["T"] / (ms / 1e3), 1),
+        "timing": {**tstats, "protocol": "per-step HIP events on the library's stream; a 512 MiB cache flush "
+                                         "before every step, outside its events; ms_per_step is the mean"},
         "step_bytes": step_bytes, "step_flops": step_flops,
         "stage_ms": {k: round(v, 5) for k, v in stages.items()},
         "gemm_ms": round(gemm_ms, 5), "attention_ms": round(attn_ms, 5),
@@ -835,6 +1005,16 @@ def main():
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(shape, batch, w, pool, x, mode, args.cpu_seconds, kvs)
+    if args.workload == "decode8b" and args.kv == "bf16" and args.weights == "bf16" and not args.no_extras:
+        # the metric's other two parts on the same line: the prefill EB step
+        # (MFMA TFLOP/s) and the MB sweep (step latency vs decode share)
+        del pool, ws, x, y
+        torch.cuda.empty_cache()
+        t1 = time.perf_counter()
+        line["prefill_8b"] = prefill_part(args, dev, w)
+        print(f"# prefill part {time.perf_counter() - t1:.1f} s", file=sys.stderr, flush=True)
+        line["mb_sweep_8b"] = sweep_part(args, dev, w)
+        print(f"# prefill + sweep parts {time.perf_counter() - t1:.1f} s", file=sys.stderr, flush=True)
     out = json.dumps(line)
     print(out)
     if args.json_out:

@@ -28,9 +28,27 @@
  *  - `stream` is a hipStream_t passed as void* (NULL = default stream).  Calls
  *    only enqueue work on it and return without waiting; buffers must stay
  *    alive until the stream has finished the work.
- *  - Every check runs before anything is enqueued: on a non-EB_OK return no
- *    work was launched and no byte of device memory was written.  The
- *    message for the last failure on the calling thread is eb_last_error().
+ *  - Every argument check runs before anything is enqueued: a return of
+ *    EB_ERR_NULL, EB_ERR_CONFIG, EB_ERR_BATCH, EB_ERR_MODE, EB_ERR_PAGES,
+ *    EB_ERR_WORKSPACE or EB_ERR_LIMITS means no work was launched and no byte
+ *    of device memory was written.  EB_ERR_HIP is different: a HIP call
+ *    failed after the checks, possibly after earlier stages (the metadata
+ *    copy, earlier kernels) were already enqueued on the stream; the
+ *    outputs, the workspace and the new cache slots are then undefined
+ *    (every other cache byte is still unchanged: no kernel writes outside
+ *    the new slots).  The message for the last failure on the calling thread
+ *    is eb_last_error().
+ *  - Device block tables are not read back on the host in normal operation:
+ *    eb_validate checks their contents from a host copy.  A handle created
+ *    while the environment variable EB_DEBUG_VALIDATE is set (to anything
+ *    but "0"), or by a library built with -DEB_DEBUG_VALIDATE, runs the
+ *    same check inside every call that takes a cache: it copies the needed
+ *    block-table rows to the host on the caller's stream, waits for them
+ *    (a host synchronisation: debugging only) and returns EB_ERR_PAGES
+ *    before enqueuing any work if an id is outside [0, num_pages) or a page
+ *    is used twice.  Without it a bad id reads as zeros (kernels bound every
+ *    page id by num_pages) and results are undefined, but no memory outside
+ *    the cache is touched.
  *  - Supported shapes: head_dim in {64, 128}; n_q_heads a multiple of
  *    n_kv_heads with n_q_heads / n_kv_heads in {1, 2, 4, 8}; page_size 16;
  *    hidden and ffn multiples of 8.  Anything else is EB_ERR_CONFIG.
@@ -171,6 +189,30 @@ void eb_destroy(eb_handle *h);
  * aligned base required).  Returns 0 if the batch is invalid for the mode. */
 size_t eb_workspace_bytes(const eb_handle *h, const eb_batch *batch, eb_mode mode);
 
+/* Intermediate buffers of a layer step inside its workspace.  After a
+ * step over `batch` in `mode` (or the last layer of a stack), the workspace
+ * holds, at the byte offset eb_workspace_offset() returns:
+ *   EB_WS_QKV  bf16 [num_tokens, (n_q + 2 n_kv) head_dim], the QKV projection
+ *              output with the q heads normalised (qk_norm) and rotated in
+ *              place, k and v as projected (the cache holds rotated k)
+ *   EB_WS_ATTN bf16 [num_tokens, n_q head_dim], the attention output
+ *   EB_WS_H1   bf16 [num_tokens, hidden], h1 = x + attn Wo^T
+ *   EB_WS_MLP  bf16 [num_tokens, ffn], m = SiLU(b Wg^T) * (b Wu^T) (dense
+ *              layers only)
+ *   EB_WS_NORM bf16 [num_tokens, hidden], b = RMSNorm(h1) g2
+ * The residual stream dominates y (|x| is far above |attn Wo^T| at these
+ * weight scales), so attention errors are visible only in these buffers;
+ * they exist for stage-level parity tests.  Returns (size_t)-1 for an
+ * invalid or empty batch, an unknown buffer, or EB_WS_MLP of an MoE layer. */
+typedef enum eb_ws_buffer {
+  EB_WS_QKV = 0,
+  EB_WS_ATTN = 1,
+  EB_WS_H1 = 2,
+  EB_WS_MLP = 3,
+  EB_WS_NORM = 4
+} eb_ws_buffer;
+size_t eb_workspace_offset(const eb_handle *h, const eb_batch *batch, eb_mode mode, int32_t which);
+
 /* The three step entry points.  x: bf16 [num_tokens, hidden] (input rows),
  * y: bf16 [num_tokens, hidden] (output; must not alias x).  Writes y, the
  * workspace and exactly the cache slots of positions c_i .. c_i + n_i - 1;
@@ -239,11 +281,16 @@ const char *eb_last_error(void); /* thread-local message of the last failure */
 
 /* ---- single operations of the step, same conventions (for parity tests) ---- */
 
-/* out[r] = bf16(x[r] / sqrt(mean(x[r]^2) + eps) * gamma), rows x hidden. */
+/* out[r] = bf16(x[r] / sqrt(mean(x[r]^2) + eps) * gamma), rows x hidden.
+ * The pre-attention and pre-MLP norms of the layer (the per-token "other"
+ * work of the step, App. A.2 "Kernel breakdown"). */
 eb_status eb_op_rmsnorm(const eb_handle *h, const void *x, const void *gamma, void *out, int32_t rows,
                         void *stream);
 
-/* out = epilogue(A W^T): A bf16 [M, K], W bf16 [N, K], out bf16 [M, N] (or
+/* The projection GEMMs of the step: the QKV, O, gate/up and down products
+ * that make up the 24 d^2 FLOPs per token of prefill (App. A.1) and do not
+ * change with the decode share or the context (App. A.2).
+ * out = epilogue(A W^T): A bf16 [M, K], W bf16 [N, K], out bf16 [M, N] (or
  * [M, N/2] for EB_EPI_SILU_MUL), residual bf16 [M, N] (EB_EPI_RESIDUAL only).
  * N and K must be multiples of 8 (EB_ERR_CONFIG otherwise).
  * ws: device scratch of at least eb_op_gemm_workspace_bytes(M, N, K). */
@@ -286,7 +333,10 @@ eb_status eb_op_moe_ffn(const void *b, const void *residual, const void *w_route
                         int32_t renormalize, void *out, int32_t *ids_out, float *weights_out, void *ws,
                         size_t ws_bytes, void *stream);
 
-/* RoPE on the q and k heads of qkv (bf16 [num_tokens, (n_q + 2 n_kv) head_dim],
+/* The cache append of the step: new keys and values join each request's
+ * paged KV cache, which the paper's engine keeps unchanged across
+ * iterations (Sec. 3.1 "System Model", Sec. 4.1 "Implementation").
+ * RoPE on the q and k heads of qkv (bf16 [num_tokens, (n_q + 2 n_kv) head_dim],
  * the QKV projection output) at pos = c_i + j; q is rotated in place, the
  * rotated k and the v heads are written to the cache.  A handle whose config
  * has qk_norm set gets EB_ERR_CONFIG: this entry has no norm gains (the layer
@@ -294,14 +344,22 @@ eb_status eb_op_moe_ffn(const void *b, const void *residual, const void *w_route
 eb_status eb_op_rope_kv_append(eb_handle *h, void *qkv, const eb_kv_cache *kv, const eb_batch *batch,
                                void *ws, size_t ws_bytes, void *stream);
 
-/* Attention of every row over keys 0..pos of its request, reading rotated q
+/* Attention of the step: decode rows stream their whole cached context
+ * (memory bound, App. A.2 "Effect of decode context length"), prefill rows
+ * are causal over their prefix and chunk (compute bound, App. A.1), and the
+ * mixed plan runs both kinds in one launch, the kernel in which the paper
+ * locates mixed-batch interference (Sec. 1, Fig. kernel_breakdown).
+ * Attention of every row over keys 0..pos of its request, reading rotated q
  * from qkv and keys/values from the cache (already appended); out bf16
  * [num_tokens, n_q head_dim].  mode selects the launch plan exactly as the
  * step entry points do. */
 eb_status eb_op_attention(eb_handle *h, const void *qkv, const eb_kv_cache *kv, const eb_batch *batch,
                           void *out, void *ws, size_t ws_bytes, eb_mode mode, void *stream);
 
-/* Dense copy of every request's cached positions 0 .. c_i + n_i - 1 through
+/* The paging of the cache (Sec. 4.1 "Implementation": paged attention left
+ * unchanged) as a plain copy, for bit-exact checks of the block-table
+ * addressing every attention kernel uses.
+ * Dense copy of every request's cached positions 0 .. c_i + n_i - 1 through
  * its block table: out_k, out_v [sum_i (c_i + n_i), n_kv_heads, head_dim]
  * elements of the cache's type (bf16, or the raw 8-bit codes), requests in
  * order.  Pure paging: bit-exact. */

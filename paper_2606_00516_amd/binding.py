@@ -29,7 +29,7 @@ SYMBOLS = ("eb_create", "eb_destroy", "eb_workspace_bytes", "eb_layer_step_decod
            "eb_layer_step_mixed", "eb_validate", "eb_status_str", "eb_last_error", "eb_op_rmsnorm",
            "eb_op_gemm_workspace_bytes", "eb_op_gemm", "eb_op_gemm_w8", "eb_op_moe_ffn_workspace_bytes", "eb_op_moe_ffn", "eb_op_rope_kv_append", "eb_op_attention",
            "eb_op_gather_kv", "eb_profile", "eb_profile_read", "eb_profile_stage_name", "eb_stack_workspace_bytes",
-           "eb_stack_step")
+           "eb_stack_step", "eb_workspace_offset")
 
 
 class EbError(RuntimeError):
@@ -86,6 +86,7 @@ def lib() -> ctypes.CDLL:
         "eb_create": (I32, [P(LayerConfig), I32, I32, P(VP)]),
         "eb_destroy": (None, [VP]),
         "eb_workspace_bytes": (SZ, [VP, P(Batch), I32]),
+        "eb_workspace_offset": (SZ, [VP, P(Batch), I32, I32]),
         "eb_validate": (I32, [P(LayerConfig), P(Batch), VP, I32, I32, I32]),
         "eb_status_str": (ctypes.c_char_p, [I32]),
         "eb_last_error": (ctypes.c_char_p, []),
@@ -211,6 +212,34 @@ class Handle:
 def eb_workspace_bytes(h: Handle, context_lens, chunk_lens, mode: str) -> int:
     hb = HostBatch(context_lens, chunk_lens)
     return int(lib().eb_workspace_bytes(h.h, ctypes.byref(hb.c), MODES[mode]))
+
+
+WS_BUFFERS = {"qkv": 0, "attn": 1, "h1": 2, "mlp": 3, "norm": 4}
+
+
+def eb_workspace_offset(h: Handle, context_lens, chunk_lens, mode: str, which: str) -> int:
+    """Byte offset of an intermediate buffer inside a step's workspace (-1:
+    none)."""
+    hb = HostBatch(context_lens, chunk_lens)
+    off = int(lib().eb_workspace_offset(h.h, ctypes.byref(hb.c), MODES[mode], WS_BUFFERS[which]))
+    return -1 if off == (1 << 64) - 1 else off
+
+
+def workspace_intermediates(h: Handle, ws: torch.Tensor, context_lens, chunk_lens, mode: str) -> dict:
+    """Views of the intermediate buffers a layer step left in ``ws``: bf16
+    qkv [T, (nq + 2 nkv) hd] (q normalised and rotated in place), attn
+    [T, nq hd], h1 [T, d], mlp [T, ffn] (dense layers), norm [T, d]."""
+    s = h.shape
+    T = int(np.asarray(chunk_lens).sum())
+    cols = {"qkv": (s.n_q_heads + 2 * s.n_kv_heads) * s.head_dim, "attn": s.n_q_heads * s.head_dim,
+            "h1": s.hidden, "mlp": s.ffn, "norm": s.hidden}
+    out = {}
+    for name, c in cols.items():
+        off = eb_workspace_offset(h, context_lens, chunk_lens, mode, name)
+        if off < 0:
+            continue
+        out[name] = ws[off:off + T * c * 2].view(torch.bfloat16).view(T, c)
+    return out
 
 
 def alloc_workspace(nbytes: int, device="cuda") -> torch.Tensor:

@@ -2,6 +2,7 @@
 // sequence of one decoder-layer step on the caller's stream.
 #include <cmath>
 #include <hip/hip_runtime.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -253,6 +254,9 @@ struct eb_handle {
   std::vector<std::vector<hipEvent_t>> pslot;
   std::vector<int> slot_layers;
   int max_layers;  // most layers a step on this handle has run
+  // debug validation: every step copies the device block tables back and
+  // checks them on the host before it enqueues anything (EB_DEBUG_VALIDATE)
+  bool debug_validate;
 };
 
 namespace {
@@ -306,6 +310,26 @@ eb_status check_ws(void *ws, size_t ws_bytes, size_t need) {
   if (ws_bytes < need)
     return fail(EB_ERR_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes, got " +
                                       std::to_string(ws_bytes));
+  return EB_OK;
+}
+
+// Debug validation of device block tables (handles created with
+// EB_DEBUG_VALIDATE set): copy the needed rows back on the caller's stream,
+// wait for them and run the host check.  Release handles skip this: they
+// never read device block tables on the host.
+eb_status debug_check_tables(const eb_handle *h, const eb_batch *b, const eb_kv_cache *kv, int n, hipStream_t st) {
+  if (!h->debug_validate || b->num_seqs == 0) return EB_OK;
+  std::vector<int32_t> host;
+  for (int l = 0; l < n; ++l) {
+    const size_t cnt = (size_t)b->num_seqs * kv[l].max_pages_per_seq;
+    host.resize(cnt);
+    hipError_t e = hipMemcpyAsync(host.data(), kv[l].block_tables, cnt * sizeof(int32_t), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) return fail(EB_ERR_HIP, std::string("debug validation copy: ") + hipGetErrorString(e));
+    std::string err;
+    const eb_status s = check_tables(h->cfg, *b, host.data(), kv[l].num_pages, kv[l].max_pages_per_seq, err);
+    if (s != EB_OK) return fail(s, (n > 1 ? "layer " + std::to_string(l) + ": " : std::string()) + err);
+  }
   return EB_OK;
 }
 
@@ -464,6 +488,8 @@ eb_status run_layers(eb_handle *h, int32_t n_layers, const eb_layer_weights *w, 
   if (n_layers > h->max_layers) h->max_layers = n_layers;
   if (!x || !y) return fail(EB_ERR_NULL, "x or y is NULL");
   if (x == y) return fail(EB_ERR_BATCH, "y must not alias x");
+  s = debug_check_tables(h, b, kv, n_layers, static_cast<hipStream_t>(stream));
+  if (s != EB_OK) return s;
   HostPlan p;
   build_plan(h->cfg, *b, mode, p);
   const bool stack = n_layers > 1;
@@ -541,6 +567,12 @@ eb_status eb_create(const eb_layer_config *cfg, int32_t max_seqs, int32_t max_to
   h->prof_mask = 0;
   h->prof_count = 0;
   h->max_layers = 1;
+#ifdef EB_DEBUG_VALIDATE
+  h->debug_validate = true;
+#else
+  const char *dv = getenv("EB_DEBUG_VALIDATE");
+  h->debug_validate = dv && dv[0] && strcmp(dv, "0") != 0;
+#endif
   for (int k = 0; k < kRing; ++k) {
     h->pinned[k] = nullptr;
     h->ev[k] = nullptr;
@@ -579,6 +611,24 @@ size_t eb_workspace_bytes(const eb_handle *h, const eb_batch *batch, eb_mode mod
   HostPlan p;
   build_plan(h->cfg, *batch, mode, p);
   return layout_for(h->shape, p, true).total;
+}
+
+size_t eb_workspace_offset(const eb_handle *h, const eb_batch *batch, eb_mode mode, int32_t which) {
+  const size_t none = (size_t)-1;
+  if (!h) return none;
+  std::string err;
+  if (check_batch(h->cfg, batch, -1, mode, err) != EB_OK || batch->num_tokens == 0) return none;
+  HostPlan p;
+  build_plan(h->cfg, *batch, mode, p);
+  const WsLayout L = layout_for(h->shape, p, true);
+  switch (which) {
+    case EB_WS_QKV: return L.qkv;
+    case EB_WS_ATTN: return L.attn;
+    case EB_WS_H1: return L.h1;
+    case EB_WS_MLP: return h->shape.moe() ? none : L.mlp;
+    case EB_WS_NORM: return L.act;
+  }
+  return none;
 }
 
 eb_status eb_layer_step_decode(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv, const eb_batch *batch,
@@ -778,6 +828,8 @@ eb_status eb_op_rope_kv_append(eb_handle *h, void *qkv, const eb_kv_cache *kv, c
   if (batch->num_tokens == 0) return EB_OK;
   if (!qkv) return fail(EB_ERR_NULL, "qkv is NULL");
   if (h->shape.qkn) return fail(EB_ERR_CONFIG, "qk_norm layers: the norm gains come with the layer step entry points");
+  s = debug_check_tables(h, batch, kv, 1, static_cast<hipStream_t>(stream));
+  if (s != EB_OK) return s;
   HostPlan p;
   build_plan(h->cfg, *batch, EB_MODE_MIXED, p);
   const WsLayout L = layout_for(h->shape, p, false);
@@ -799,6 +851,8 @@ eb_status eb_op_attention(eb_handle *h, const void *qkv, const eb_kv_cache *kv, 
   if (s != EB_OK) return s;
   if (batch->num_tokens == 0) return EB_OK;
   if (!qkv || !out) return fail(EB_ERR_NULL, "qkv or out is NULL");
+  s = debug_check_tables(h, batch, kv, 1, static_cast<hipStream_t>(stream));
+  if (s != EB_OK) return s;
   HostPlan p;
   build_plan(h->cfg, *batch, mode, p);
   const WsLayout L = layout_for(h->shape, p, false);
@@ -824,6 +878,8 @@ eb_status eb_op_gather_kv(eb_handle *h, const eb_kv_cache *kv, const eb_batch *b
   if (s != EB_OK) return s;
   if (batch->num_seqs == 0) return EB_OK;
   if (!out_k || !out_v) return fail(EB_ERR_NULL, "out_k or out_v is NULL");
+  s = debug_check_tables(h, batch, kv, 1, static_cast<hipStream_t>(stream));
+  if (s != EB_OK) return s;
   HostPlan p;
   build_plan(h->cfg, *batch, EB_MODE_MIXED, p);
   const WsLayout L = layout_for(h->shape, p, false);

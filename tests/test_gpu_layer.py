@@ -222,3 +222,38 @@ def test_8b_mixed_budget_sampled(w8b, r):
     pre = [int(i) for i in np.nonzero(batch.chunk_lens > 1)[0]]
     pre = [min(pre, key=lambda i: batch.chunk_lens[i])] if pre else []
     _sampled_parity(gen.L8B, batch, w, Wo, "mixed", dec + pre)
+
+
+def test_debug_validate_reports_bad_block_tables(monkeypatch):
+    # with EB_DEBUG_VALIDATE set when the handle is created, every step reads
+    # its device block tables back and refuses bad ids and shared pages
+    # before it enqueues anything; without it the same step runs
+    case = tiny_case("mixed")
+    d = DevCase(case)
+    b = case.batch
+    monkeypatch.setenv("EB_DEBUG_VALIDATE", "1")
+    h = B.Handle(case.shape, b.num_seqs, b.num_tokens)
+    monkeypatch.delenv("EB_DEBUG_VALIDATE")
+    y = torch.full_like(d.x, 3.0)
+    B.eb_layer_step_mixed(h, d.w, d.k, d.v, d.bt, b.context_lens, b.chunk_lens, d.x, y=y)
+    torch.cuda.synchronize()
+    assert not bool((y == 3.0).all())
+    for bad_value in ("out_of_range", "shared"):
+        bt = d.bt.clone()
+        if bad_value == "out_of_range":
+            bt[1, 0] = case.pool.num_pages
+        else:
+            bt[1, 0] = bt[0, 0]
+        y = torch.full_like(d.x, 3.0)
+        k_before = cache_bits(d.k)
+        with pytest.raises(B.EbError) as ei:
+            B.eb_layer_step_mixed(h, d.w, d.k, d.v, bt, b.context_lens, b.chunk_lens, d.x, y=y)
+        assert ei.value.status == -5, bad_value
+        torch.cuda.synchronize()
+        assert bool((y == 3.0).all()) and np.array_equal(cache_bits(d.k), k_before)
+    # a release handle does not read the tables back
+    h2 = B.Handle(case.shape, b.num_seqs, b.num_tokens)
+    bt = d.bt.clone()
+    bt[1, 0] = bt[0, 0]
+    B.eb_layer_step_mixed(h2, d.w, d.k.clone(), d.v.clone(), bt, b.context_lens, b.chunk_lens, d.x)
+    torch.cuda.synchronize()

@@ -473,3 +473,14 @@ def test_qk_norm_planted_mistakes_are_caught(monkeypatch):
     with monkeypatch.context() as mp:
         mp.setattr(L, "rmsnorm", whole_row)
         assert run(o0["cfg"], o0["w_bits"]) > 1e-3, "norm over the whole row"
+
+
+def test_attention_branch_is_a_few_percent_of_y():
+    # On the default weights (projections N(0, 0.02)) the attention branch
+    # attn Wo^T = h1 - x is a few percent of max|y|: a check of y alone at
+    # 2e-2 cannot see attention errors, which is why the GPU tests also
+    # compare the step's intermediate buffers (q, attention output, h1, m).
+    case = tiny_case("mixed")
+    (y, inter), _ = case.run_oracle(intermediates=True)
+    x = L.bf16_bits_to_f32(gen.bits(case.x))
+    assert np.max(np.abs(inter["h1"] - x)) < 0.1 * np.max(np.abs(y))
