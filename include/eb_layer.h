@@ -232,6 +232,27 @@ eb_status eb_layer_step_mixed(eb_handle *h, const eb_layer_weights *w, const eb_
                               const eb_batch *batch, const void *x, void *y, void *ws, size_t ws_bytes,
                               void *stream);
 
+/* eb_layer_step_mixed without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The step's intermediate buffers live
+ * in a fixed scratch array inside the library, eb_noalloc_scratch_bytes()
+ * = 64 MiB per GPU, held from the library's first use on a GPU until the
+ * process ends (its address is looked up once per device in eb_create).
+ * The call allocates no device or pinned memory (the handle's staging
+ * buffers come from eb_create; the host planner uses ordinary heap memory)
+ * and never profiles.  Same arguments, modes, checks and results as
+ * eb_layer_step_mixed, bitwise; EB_ERR_WORKSPACE when the batch needs more
+ * than the scratch holds (eb_workspace_bytes(h, batch, EB_MODE_MIXED) >
+ * eb_noalloc_scratch_bytes()), EB_ERR_HIP if the scratch's address could not
+ * be found.  Every call on one GPU shares that GPU's scratch and leaves its
+ * contents behind (no kernel of the step reads a scratch byte it did not
+ * write in the same call, so nothing needs clearing): calls that may overlap
+ * on one GPU (other streams, other handles or threads) race and must be
+ * serialised by the caller. */
+size_t eb_noalloc_scratch_bytes(void);
+eb_status eb_layer_step_mixed_noalloc(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv,
+                                      const eb_batch *batch, const void *x, void *y, void *stream);
+
 /* A model step: n_layers decoder layers over one batch.  The paper's
  * iteration time is that of the whole model over the batch (Sec. 1,
  * Sec. 3.1 "Timing Model"); every layer sees the same requests and rows.

@@ -29,7 +29,7 @@ SYMBOLS = ("eb_create", "eb_destroy", "eb_workspace_bytes", "eb_layer_step_decod
            "eb_layer_step_mixed", "eb_validate", "eb_status_str", "eb_last_error", "eb_op_rmsnorm",
            "eb_op_gemm_workspace_bytes", "eb_op_gemm", "eb_op_gemm_w8", "eb_op_moe_ffn_workspace_bytes", "eb_op_moe_ffn", "eb_op_rope_kv_append", "eb_op_attention",
            "eb_op_gather_kv", "eb_profile", "eb_profile_read", "eb_profile_stage_name", "eb_stack_workspace_bytes",
-           "eb_stack_step", "eb_workspace_offset")
+           "eb_stack_step", "eb_workspace_offset", "eb_noalloc_scratch_bytes", "eb_layer_step_mixed_noalloc")
 
 
 class EbError(RuntimeError):
@@ -87,6 +87,8 @@ def lib() -> ctypes.CDLL:
         "eb_destroy": (None, [VP]),
         "eb_workspace_bytes": (SZ, [VP, P(Batch), I32]),
         "eb_workspace_offset": (SZ, [VP, P(Batch), I32, I32]),
+        "eb_noalloc_scratch_bytes": (SZ, []),
+        "eb_layer_step_mixed_noalloc": (I32, [VP, P(LayerWeights), P(KvCache), P(Batch), VP, VP, VP]),
         "eb_validate": (I32, [P(LayerConfig), P(Batch), VP, I32, I32, I32]),
         "eb_status_str": (ctypes.c_char_p, [I32]),
         "eb_last_error": (ctypes.c_char_p, []),
@@ -280,6 +282,24 @@ def eb_layer_step_mixed(h, weights, k_cache, v_cache, block_tables, context_lens
                         stream=None, kv_scales=None):
     return _step("eb_layer_step_mixed", h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x,
                  y, ws, stream, kv_scales)
+
+
+def eb_noalloc_scratch_bytes() -> int:
+    return int(lib().eb_noalloc_scratch_bytes())
+
+
+def eb_layer_step_mixed_noalloc(h, weights, k_cache, v_cache, block_tables, context_lens, chunk_lens, x, y=None,
+                                stream=None, kv_scales=None):
+    """The mixed step on the library's fixed scratch (no workspace argument;
+    y must be given by callers that cannot allocate)."""
+    hb = HostBatch(context_lens, chunk_lens)
+    if y is None:
+        y = torch.empty_like(x)
+    kv = kv_struct(k_cache, v_cache, block_tables, kv_scales)
+    w = weights_struct(weights)
+    _check(lib().eb_layer_step_mixed_noalloc(h.h, ctypes.byref(w), ctypes.byref(kv), ctypes.byref(hb.c), _ptr(x),
+                                             _ptr(y), _stream(stream)))
+    return y
 
 
 def eb_stack_workspace_bytes(h: Handle, context_lens, chunk_lens, mode: str) -> int:

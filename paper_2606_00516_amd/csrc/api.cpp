@@ -257,6 +257,10 @@ struct eb_handle {
   // debug validation: every step copies the device block tables back and
   // checks them on the host before it enqueues anything (EB_DEBUG_VALIDATE)
   bool debug_validate;
+  // device address of this device's fixed scratch (eb_layer_step_mixed_noalloc);
+  // null with the lookup's error kept when it failed
+  void *scratch;
+  hipError_t scratch_err;
 };
 
 namespace {
@@ -470,7 +474,7 @@ eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, con
 // the last layer writes y.  Every check runs before anything is enqueued.
 eb_status run_layers(eb_handle *h, int32_t n_layers, const eb_layer_weights *w, const eb_kv_cache *kv,
                      const eb_batch *b, const void *x, void *y, void *ws, size_t ws_bytes, void *stream,
-                     eb_mode mode) {
+                     eb_mode mode, bool allow_prof = true) {
   if (!h) return fail(EB_ERR_NULL, "handle is NULL");
   if (n_layers < 1) return fail(EB_ERR_CONFIG, "n_layers must be >= 1");
   if (!w || !kv) return fail(EB_ERR_NULL, "weights or kv is NULL");
@@ -496,7 +500,7 @@ eb_status run_layers(eb_handle *h, int32_t n_layers, const eb_layer_weights *w, 
   const WsLayout L = layout_for(h->shape, p, true, stack);
   s = check_ws(ws, ws_bytes, L.total);
   if (s != EB_OK) return s;
-  const int slot = h->prof ? (int)(h->prof_count % h->prof_slots) : -1;
+  const int slot = h->prof && allow_prof ? (int)(h->prof_count % h->prof_slots) : -1;
   if (slot >= 0) {
     s = grow_events(h->pslot[slot], n_layers);
     if (s != EB_OK) return s;
@@ -578,6 +582,7 @@ eb_status eb_create(const eb_layer_config *cfg, int32_t max_seqs, int32_t max_to
     h->ev[k] = nullptr;
     h->used[k] = false;
   }
+  h->scratch_err = noalloc_scratch_setup(h->device, &h->scratch);
   for (int k = 0; k < kRing; ++k) {
     e = hipHostMalloc(reinterpret_cast<void **>(&h->pinned[k]), h->slot_cap * sizeof(int32_t), hipHostMallocDefault);
     if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev[k], hipEventDisableTiming);
@@ -644,6 +649,26 @@ eb_status eb_layer_step_prefill(eb_handle *h, const eb_layer_weights *w, const e
 eb_status eb_layer_step_mixed(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv, const eb_batch *batch,
                               const void *x, void *y, void *ws, size_t ws_bytes, void *stream) {
   return run_layers(h, 1, w, kv, batch, x, y, ws, ws_bytes, stream, EB_MODE_MIXED);
+}
+
+size_t eb_noalloc_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+eb_status eb_layer_step_mixed_noalloc(eb_handle *h, const eb_layer_weights *w, const eb_kv_cache *kv,
+                                      const eb_batch *batch, const void *x, void *y, void *stream) {
+  if (!h) return fail(EB_ERR_NULL, "handle is NULL");
+  std::string err;
+  eb_status s = check_batch(h->cfg, batch, -1, EB_MODE_MIXED, err);
+  if (s != EB_OK) return fail(s, err);
+  if (batch->num_tokens > 0) {
+    HostPlan p;
+    build_plan(h->cfg, *batch, EB_MODE_MIXED, p);
+    const size_t need = layout_for(h->shape, p, true).total;
+    if (need > kNoAllocScratchBytes)
+      return fail(EB_ERR_WORKSPACE, "batch needs " + std::to_string(need) + " bytes of workspace, the fixed scratch holds " +
+                                        std::to_string(kNoAllocScratchBytes));
+  }
+  if (!h->scratch) return hip_fail(h->scratch_err, "fixed scratch address (hipGetSymbolAddress)");
+  return run_layers(h, 1, w, kv, batch, x, y, h->scratch, kNoAllocScratchBytes, stream, EB_MODE_MIXED, false);
 }
 
 size_t eb_stack_workspace_bytes(const eb_handle *h, const eb_batch *batch, eb_mode mode) {

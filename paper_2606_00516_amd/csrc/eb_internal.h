@@ -66,6 +66,12 @@ struct Shape {
   int32_t group() const { return nq / nkv; }
 };
 
+// Fixed device scratch of the no-allocation step entry point: its size, and
+// the device address of the calling device's copy (looked up once per
+// device with that device current).
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+hipError_t noalloc_scratch_setup(int device, void **addr);
+
 // ---- launchers (each returns the launch error) ----
 hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gamma, uint16_t *out, int rows, int d, float eps,
                           hipStream_t st);
