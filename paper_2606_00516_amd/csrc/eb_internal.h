@@ -27,6 +27,22 @@ inline int prefill_bq(int group, bool mixed_launch) {
   return mixed_launch ? 64 / group : 128 / group;
 }
 
+// Work order of the single mixed attention launch.  Its P prefill items are
+// compute bound and its D decode units stream K/V from HBM; placing the
+// prefill items at every s-th block over the first kMixedPrefillSpan of the
+// grid (longest first) keeps both kinds running side by side on the CUs
+// instead of one phase after the other.  Block b runs prefill item b / s
+// when b % s == 0 and b / s < P, otherwise decode unit b - min(P, b / s + 1).
+#ifndef EB_MIX_SPAN
+#define EB_MIX_SPAN 70
+#endif
+constexpr int kMixedPrefillSpanPct = EB_MIX_SPAN;
+inline int mixed_prefill_stride(long P, long D) {
+  if (P <= 0 || D <= 0) return 1;
+  const long s = (long)kMixedPrefillSpanPct * (P + D) / (100 * P);
+  return s < 1 ? 1 : (s > (1L << 30) ? (1 << 30) : (int)s);
+}
+
 // Per-step metadata in device memory (all int32), produced by the planner.
 struct DevMeta {
   const int32_t *seq_ctx;       // [S] tokens cached before the step

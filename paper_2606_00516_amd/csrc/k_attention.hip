@@ -1163,39 +1163,52 @@ __global__ __launch_bounds__(64 * kPrefillWaves) void k_prefill(const uint16_t *
 // One grid for a mixed step: items [0, n_tiles) are prefill tiles (longest
 // first), the rest decode splits; every block (4 wavefronts) branches
 // uniformly on its kind.  Decode items run exactly the decode-only code.
+// Block b of a mixed launch: prefill item (>= 0) or decode unit (the
+// complement), from the interleaving stride s (see mixed_prefill_stride).
+__device__ __forceinline__ void mixed_slot(int b, int n_prefill, int s, int &pf, int &du) {
+  const int q = b / s;
+  if (b - q * s == 0 && q < n_prefill) {
+    pf = q;
+    du = -1;
+  } else {
+    pf = -1;
+    du = b - min(n_prefill, q + 1);
+  }
+}
+
 template <int HD, int G, bool F8>
 __global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
-                                               float *part_o, float *part_ml) {
+                                               float *part_o, float *part_ml, int stride) {
   constexpr int BQ = prefill_item_positions<G, true>();
   using Tr = PrefillTraits<HD, G, 4, BQ>;
   constexpr int PB = Tr::LDS_BYTES, DB = DecodeTraits<HD, G, 4>::LDS_BYTES;
   __shared__ __attribute__((aligned(16))) uint16_t lds[(PB > DB ? PB : DB) / 2];
-  const int b = blockIdx.x;
-  if (b < md.n_tiles * nkv)
-    prefill_item<HD, G, 4, BQ, F8>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, lds, lds + Tr::KS_BYTES / 2);
+  int pf, du;
+  mixed_slot(blockIdx.x, md.n_tiles * nkv, stride, pf, du);
+  if (pf >= 0)
+    prefill_item<HD, G, 4, BQ, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, lds, lds + Tr::KS_BYTES / 2);
   else
-    decode_item<HD, G, 4, F8>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml,
-                              reinterpret_cast<float *>(lds));
+    decode_item<HD, G, 4, F8>(qkv, nq, nkv, kv, md, du, out, part_o, part_ml, reinterpret_cast<float *>(lds));
 }
 
 // The same with matrix-core decode items; prefill tiles borrow two of the
 // page-slot arrays.
 template <int HD, int G, bool F8>
 __global__ __launch_bounds__(256) void k_mixed_mfma(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
-                                                    uint16_t *out, float *part_o, float *part_ml) {
+                                                    uint16_t *out, float *part_o, float *part_ml, int stride) {
   constexpr int BQ = prefill_item_positions<G, true>();
   using Tr = PrefillTraits<HD, G, 4, BQ>;
   constexpr int MS = 2;                           // ring depth of decode items in the mixed launch
   constexpr int SLOT = MdecTraits<HD>::SLOT;      // bf16-sized slots: prefill tiles stage bf16
   static_assert(Tr::KS_BYTES <= 4 * SLOT && Tr::VT_BYTES <= 4 * SLOT, "LDS");
   EB_MDEC_LDS(4 * SLOT, MS)
-  const int b = blockIdx.x;
-  if (b < md.n_tiles * nkv)
-    prefill_item<HD, G, 4, BQ, F8>(qkv, nq, nkv, kv, md, b / nkv, b % nkv, out, reinterpret_cast<uint16_t *>(l0),
+  int pf, du;
+  mixed_slot(blockIdx.x, md.n_tiles * nkv, stride, pf, du);
+  if (pf >= 0)
+    prefill_item<HD, G, 4, BQ, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, reinterpret_cast<uint16_t *>(l0),
                                    reinterpret_cast<uint16_t *>(l1));
   else
-    decode_item_mfma<HD, G, 4, MS, F8, SLOT>(qkv, nq, nkv, kv, md, b - md.n_tiles * nkv, out, part_o, part_ml, l0, l1,
-                                             l2, l3);
+    decode_item_mfma<HD, G, 4, MS, F8, SLOT>(qkv, nq, nkv, kv, md, du, out, part_o, part_ml, l0, l1, l2, l3);
 }
 #undef EB_MDEC_LDS
 
@@ -1208,12 +1221,13 @@ static hipError_t launch_attention_t(const Shape &s, const uint16_t *qkv, const 
   if (!(parts & 1)) {
     // combine only
   } else if (kind == 2 && has_dec && has_pf) {
+    const int stride = mixed_prefill_stride((long)m.n_tiles * nkv, m.total_units);
     if constexpr (kDecodeMfma<G>)
       hipLaunchKernelGGL((k_mixed_mfma<HD, G, F8>), dim3(m.n_tiles * nkv + m.total_units), dim3(256), 0, st, qkv, nq,
-                         nkv, kv, m, out, part_o, part_ml);
+                         nkv, kv, m, out, part_o, part_ml, stride);
     else
       hipLaunchKernelGGL((k_mixed<HD, G, F8>), dim3(m.n_tiles * nkv + m.total_units), dim3(256), 0, st, qkv, nq, nkv,
-                         kv, m, out, part_o, part_ml);
+                         kv, m, out, part_o, part_ml, stride);
   } else {
     if (has_pf)
       hipLaunchKernelGGL((k_prefill<HD, G, F8>), dim3(m.n_tiles * nkv), dim3(64 * kPrefillWaves), 0, st, qkv, nq, nkv,
