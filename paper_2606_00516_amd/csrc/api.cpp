@@ -157,8 +157,13 @@ hipError_t moe_second(const MoeArgs &a, hipStream_t st) {
 // Byte offsets of everything a step keeps in the caller's workspace.
 struct WsLayout {
   size_t meta = 0, act = 0, qkv = 0, attn = 0, h1 = 0, mlp = 0, part_o = 0, part_ml = 0, gemm = 0, alt = 0,
-         moe = 0, total = 0;
+         moe = 0, ssq = 0, total = 0;
 };
+
+// A decode-sized QKV projection (weight streaming with split K) takes the
+// first RMSNorm into its operand staging and its split-K sum into the RoPE /
+// append kernel: two launches fewer per layer.
+bool fused_qkv(const GemmPlan &qp) { return qp.kind == 0 && qp.splits >= 2; }
 
 // full_step: buffers of a whole layer; stack: plus the second activation
 // buffer that consecutive layers of a stack alternate with y.
@@ -195,6 +200,13 @@ WsLayout layout_for(const Shape &s, const HostPlan &p, bool full_step, bool stac
     }
     if (s.moe()) L.moe = take(moe_layout(p.T, s.hidden, s.ne, s.topk, s.effn).total);
     L.gemm = take(g);
+    // row sums of squares of the fused first RMSNorm (either weight type)
+    int ss_splits = 1;
+    for (int w8 = 0; w8 < 2; ++w8) {
+      const GemmPlan qp = plan_gemm(M, s.qkv_cols(), s.hidden, EPI_STORE, w8);
+      if (fused_qkv(qp) && qp.splits > ss_splits) ss_splits = qp.splits;
+    }
+    L.ssq = take((size_t)ss_splits * T * sizeof(float));
     if (stack) L.alt = take(T * s.hidden * 2);
   }
   L.total = off;
@@ -380,6 +392,7 @@ struct StepBufs {
   float *part_o, *part_ml;
   void *gws;
   char *moe;
+  float *ssq;
 };
 
 StepBufs bufs_at(char *base, const WsLayout &L) {
@@ -388,7 +401,7 @@ StepBufs bufs_at(char *base, const WsLayout &L) {
                   reinterpret_cast<uint16_t *>(base + L.mlp),  L.alt ? reinterpret_cast<uint16_t *>(base + L.alt)
                                                                       : nullptr,
                   reinterpret_cast<float *>(base + L.part_o), reinterpret_cast<float *>(base + L.part_ml),
-                  base + L.gemm, base + L.moe};
+                  base + L.gemm, base + L.moe, reinterpret_cast<float *>(base + L.ssq)};
 }
 
 // Make sure a profiling slot's events cover n layers.  They only time the
@@ -421,16 +434,27 @@ eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, con
   if ((e = mark(2 * (idx))) != hipSuccess) return hip_fail(e, "hipEventRecord"); \
   if ((e = (call)) != hipSuccess) return hip_fail(e, what);              \
   if ((e = mark(2 * (idx) + 1)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-  EB_STAGE(0, launch_rmsnorm(xin, static_cast<const uint16_t *>(w->attn_norm), B.act, T, sh.hidden, sh.eps, st),
-           "rmsnorm1");
-  EB_STAGE(1,
-           launch_gemm(plan_gemm(T, sh.qkv_cols(), sh.hidden, EPI_STORE, w8), B.act, w->w_qkv,
-                       w8 ? w->s_qkv : nullptr, B.qkv, nullptr, T, sh.qkv_cols(), sh.hidden, EPI_STORE, B.gws, st),
-           "qkv gemm");
-  EB_STAGE(2,
-           launch_rope_append(sh, B.qkv, kvd, m, st, static_cast<const uint16_t *>(w->q_norm),
-                              static_cast<const uint16_t *>(w->k_norm)),
-           "rope/kv append");
+  const GemmPlan qp = plan_gemm(T, sh.qkv_cols(), sh.hidden, EPI_STORE, w8);
+  const uint16_t *g1 = static_cast<const uint16_t *>(w->attn_norm);
+  const uint16_t *gq = static_cast<const uint16_t *>(w->q_norm), *gk = static_cast<const uint16_t *>(w->k_norm);
+  if (fused_qkv(qp)) {
+    // the first RMSNorm rides in the projection, the split-K sum in the RoPE
+    // kernel (stage 0 stays empty)
+    EB_STAGE(0, hipSuccess, "rmsnorm1");
+    EB_STAGE(1,
+             launch_gemm_prenorm(qp, xin, g1, w->w_qkv, w8 ? w->s_qkv : nullptr, T, sh.qkv_cols(), sh.hidden,
+                                 static_cast<float *>(B.gws), B.ssq, st),
+             "qkv gemm");
+    EB_STAGE(2, launch_qkv_rope_append(sh, static_cast<const float *>(B.gws), qp.splits, B.ssq, B.qkv, kvd, m, st, gq, gk),
+             "rope/kv append");
+  } else {
+    EB_STAGE(0, launch_rmsnorm(xin, g1, B.act, T, sh.hidden, sh.eps, st), "rmsnorm1");
+    EB_STAGE(1,
+             launch_gemm(qp, B.act, w->w_qkv, w8 ? w->s_qkv : nullptr, B.qkv, nullptr, T, sh.qkv_cols(), sh.hidden,
+                         EPI_STORE, B.gws, st),
+             "qkv gemm");
+    EB_STAGE(2, launch_rope_append(sh, B.qkv, kvd, m, st, gq, gk), "rope/kv append");
+  }
   const int kind = mode == EB_MODE_DECODE ? 0 : (mode == EB_MODE_PREFILL ? 1 : 2);
   EB_STAGE(3, launch_attention(sh, B.qkv, kvd, m, B.attn, B.part_o, B.part_ml, kind, st, 1), "attention");
   EB_STAGE(4, launch_attention(sh, B.qkv, kvd, m, B.attn, B.part_o, B.part_ml, kind, st, 2), "attention combine");

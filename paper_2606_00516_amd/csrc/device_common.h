@@ -24,6 +24,13 @@ EB_DEV uint32_t f32_to_bf16_bits(float f) {
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 EB_DEV uint32_t pack_bf16x2(float lo, float hi) { return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16); }
+// The same rounding (nearest even) by the hardware's packed conversion, one
+// instruction for the pair.
+EB_DEV uint32_t bf16_pair_rne(float lo, float hi) {
+  typedef float f32x2_v __attribute__((ext_vector_type(2)));
+  const f32x2_v f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
+}
 
 // DPP row controls (a "row" is 16 lanes).
 #define EB_DPP_QUAD_XOR1 0xB1   // quad_perm [1,0,3,2]

@@ -94,6 +94,13 @@ hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gamma, uint16_t *ou
 // gq, gk: the per-head norm gains, required when s.qkn
 hipError_t launch_rope_append(const Shape &s, uint16_t *qkv, const KV &kv, const DevMeta &m, hipStream_t st,
                               const uint16_t *gq = nullptr, const uint16_t *gk = nullptr);
+// The RoPE/append of a decode-sized step fused with the QKV projection's
+// split-K sum and the row scale of the RMSNorm before it: part holds the
+// projection's fp32 partials [splits][T][qkv_cols] of x * g1, ssq the rows'
+// partial sums of squares [splits][T] (launch_gemm_prenorm).
+hipError_t launch_qkv_rope_append(const Shape &s, const float *part, int splits, const float *ssq, uint16_t *qkv,
+                                  const KV &kv, const DevMeta &m, hipStream_t st, const uint16_t *gq = nullptr,
+                                  const uint16_t *gk = nullptr);
 hipError_t launch_gather_kv(const Shape &s, const KV &kv, const DevMeta &m, uint16_t *out_k, uint16_t *out_v,
                             hipStream_t st);
 
@@ -125,6 +132,13 @@ struct NormFuse {
 hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, const float *wscale, uint16_t *out,
                        const uint16_t *residual, int M, int N, int K, int epi, void *ws, hipStream_t st,
                        NormFuse *nf = nullptr);
+
+// The weight-streaming GEMM on the RMSNorm that precedes it: stages bf16(x *
+// gamma) as A and writes the split-K partials only (p.kind 0 with
+// p.splits >= 2), plus each row's partial sum of squares of x into ssq
+// [p.splits][M]; the consumer applies 1 / sqrt(mean(x^2) + eps) to the sum.
+hipError_t launch_gemm_prenorm(const GemmPlan &p, const uint16_t *x, const uint16_t *gamma, const void *W,
+                               const float *wscale, int M, int N, int K, float *part, float *ssq, hipStream_t st);
 
 // Mixture-of-experts block.  The grouped GEMM multiplies row tiles of
 // expert-sorted rows (tables [3][max_tiles]: expert, first sorted row, rows;

@@ -396,12 +396,6 @@ EB_DEV uint32_t bf16_pair_exact(float lo, float hi) {
   return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
 }
 
-// Round two fp32 values to bf16 (nearest even) and pack them.
-EB_DEV uint32_t bf16_pair_rne(float lo, float hi) {
-  typedef float f32x2_v __attribute__((ext_vector_type(2)));
-  const f32x2_v f = {lo, hi};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
-}
 
 // Online-softmax update with the page in a slot; the page holds at least one
 // key below k1, so the new running max is finite.

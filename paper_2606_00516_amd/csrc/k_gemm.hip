@@ -63,12 +63,19 @@ constexpr int SK_LDS = 2 * (SK_BN + SK_BM) * SK_ROWB;
 // and its up partner (32 apart) land in the same wave.
 __device__ __forceinline__ int sk_col(int w, int j) { return j < 8 ? 8 * w + j : 32 + 8 * w + (j - 8); }
 
-template <bool W8>
+// PRENORM (split-K partials only): A holds the rows x of an RMSNorm that
+// precedes the product.  The kernel stages bf16(x * gamma) instead of A and
+// the blocks of the first column tile write each row's partial sum of
+// squares over their K range to ssq[split][M]; the row scale
+// 1 / sqrt(mean(x^2) + eps) is applied to the summed partials by the
+// consumer (RMSNorm(x) g W^T = inv * ((x g) W^T)).
+template <bool W8, bool PRENORM = false>
 __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict__ A, const void *__restrict__ W,
                                                      const float *__restrict__ wscale, uint16_t *__restrict__ out,
                                                      const uint16_t *__restrict__ res, float *__restrict__ part, int M,
                                                      int N, int K, int epi, int ksteps_per_split, int tiles, int mt,
-                                                     int per_xcd) {
+                                                     int per_xcd, const uint16_t *__restrict__ gamma = nullptr,
+                                                     float *__restrict__ ssq = nullptr) {
   extern __shared__ __attribute__((aligned(16))) uint8_t sk_lds[];  // [2][64 W rows + 64 A rows][SK_ROWB]
   // block b takes tile (b % 8) * per_xcd + b / 8, so each XCD walks its own
   // contiguous tile range; the mt row blocks of one column tile are
@@ -102,7 +109,10 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
     aoff[j] = m < M ? ((uint32_t)m * (uint32_t)K + (uint32_t)(ch * 8)) * 2u : 0x80000000u;
   }
   u32x4_t wa[4], aa[4], wb[4], ab[4];
-  auto gload = [&](int s, u32x4_t (&wr)[4], u32x4_t (&ar)[4]) {
+  u32x4_t ga = {0u, 0u, 0u, 0u}, gb = {0u, 0u, 0u, 0u};  // PRENORM: gamma chunk of each stage
+  float ssacc[4] = {0.f, 0.f, 0.f, 0.f};                 // PRENORM: sum of squares of rows r0 + 16 j
+  const buf_rsrc_t rg = make_rsrc(PRENORM ? gamma : A, PRENORM ? K * 2 : 16);
+  auto gload = [&](int s, u32x4_t (&wr)[4], u32x4_t (&ar)[4], u32x4_t &gr) {
     const int k = kbeg + s * SK_KC + ch * 8;
     const bool ok = s < nst && k < kend;
     const uint32_t kb = (uint32_t)(kbeg + s * SK_KC) * 2u;
@@ -116,15 +126,30 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
       }
       ar[j] = buf_ld_u32x4<0>(ra, (int)(ok ? aoff[j] + kb : 0x80000000u));
     }
+    if constexpr (PRENORM) gr = buf_ld_u32x4<0>(rg, (int)(ok ? (uint32_t)(k * 2) : 0x80000000u));
   };
-  auto swrite = [&](int buf, const u32x4_t (&wr)[4], const u32x4_t (&ar)[4]) {
+  const bool first_col_tile = n0 == 0;
+  auto swrite = [&](int buf, const u32x4_t (&wr)[4], const u32x4_t (&ar)[4], const u32x4_t &gr) {
     uint8_t *b = sk_lds + buf * (SK_BN + SK_BM) * SK_ROWB;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       u32x4_t wv = wr[j];
       if constexpr (W8) wv = e4m3x8_to_bf16x8(u32x2_t{wr[j][0], wr[j][1]});
       *reinterpret_cast<u32x4_t *>(b + (r0 + 16 * j) * SK_ROWB + ch * 16) = wv;
-      *reinterpret_cast<u32x4_t *>(b + (SK_BN + r0 + 16 * j) * SK_ROWB + ch * 16) = ar[j];
+      u32x4_t av = ar[j];
+      if constexpr (PRENORM) {
+        if (first_col_tile) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float lo = bf16_lo(ar[j][e]), hi = bf16_hi(ar[j][e]);
+            ssacc[j] += lo * lo + hi * hi;
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          av[e] = bf16_pair_rne(bf16_lo(ar[j][e]) * bf16_lo(gr[e]), bf16_hi(ar[j][e]) * bf16_hi(gr[e]));
+      }
+      *reinterpret_cast<u32x4_t *>(b + (SK_BN + r0 + 16 * j) * SK_ROWB + ch * 16) = av;
     }
   };
   // Waves split the block's columns (16 each, see sk_col) and run the whole
@@ -149,21 +174,33 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
   };
   // Two stages in flight in registers, one in LDS: write stage s + 1 while
   // stage s is consumed, one barrier per stage.
-  gload(0, wa, aa);
-  swrite(0, wa, aa);
-  gload(1, wa, aa);
-  gload(2, wb, ab);
+  gload(0, wa, aa, ga);
+  swrite(0, wa, aa, ga);
+  gload(1, wa, aa, ga);
+  gload(2, wb, ab, gb);
   __syncthreads();
   for (int st = 0; st < nst; st += 2) {
     compute(0);
-    swrite(1, wa, aa);
-    gload(st + 3, wa, aa);
+    swrite(1, wa, aa, ga);
+    gload(st + 3, wa, aa, ga);
     __syncthreads();
     if (st + 1 >= nst) break;
     compute(1);
-    swrite(0, wb, ab);
-    gload(st + 4, wb, ab);
+    swrite(0, wb, ab, gb);
+    gload(st + 4, wb, ab, gb);
     __syncthreads();
+  }
+  if constexpr (PRENORM) {
+    // the 16 lanes of a row (chunks 0..15) hold its partial sums: one per
+    // row and split (stages past nst loaded zeros and added nothing)
+    if (first_col_tile) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float t = group_sum<16>(ssacc[j]);
+        const int m = m0 + r0 + 16 * j;
+        if (ch == 0 && m < M) ssq[(size_t)split * M + m] = t;
+      }
+    }
   }
 
   // lane: rows m = m0 + 16 i + lr, logical columns c .. c+3 of the block,
@@ -987,6 +1024,25 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, cons
   hipLaunchKernelGGL(k_gemm_tiled, dim3(tiles_m * tiles_n), dim3(256), 0, st, A,
                      static_cast<const uint16_t *>(W), out, res, M, N, K, epi, tiles_m,
                      tiles_n);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_prenorm(const GemmPlan &p, const uint16_t *x, const uint16_t *gamma, const void *W,
+                               const float *wscale, int M, int N, int K, float *part, float *ssq, hipStream_t st) {
+  if (M <= 0) return hipSuccess;
+  if (p.kind != 0 || p.splits < 2) return hipErrorInvalidValue;
+  const int nsteps = (K + 31) / 32;
+  const int per = (nsteps + p.splits - 1) / p.splits;
+  const int mt = (M + SK_BM - 1) / SK_BM;
+  const int tiles = ((N + SK_BN - 1) / SK_BN) * mt;
+  const int per_xcd = (tiles + 7) / 8;
+  dim3 grid(8 * per_xcd, p.splits);
+  if (wscale)
+    hipLaunchKernelGGL((k_gemm_skinny<true, true>), grid, dim3(256), SK_LDS, st, x, W, wscale, nullptr, nullptr, part,
+                       M, N, K, (int)EPI_STORE, per, tiles, mt, per_xcd, gamma, ssq);
+  else
+    hipLaunchKernelGGL((k_gemm_skinny<false, true>), grid, dim3(256), SK_LDS, st, x, W, wscale, nullptr, nullptr,
+                       part, M, N, K, (int)EPI_STORE, per, tiles, mt, per_xcd, gamma, ssq);
   return hipGetLastError();
 }
 

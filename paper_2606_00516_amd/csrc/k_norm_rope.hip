@@ -107,15 +107,46 @@ __device__ __forceinline__ u32x2_t e4m3x8_of_bf16x8(u32x4_t w, float scale) {
 // values divided by the scale (the division rounded in fp32).  With QKN each
 // q and k head is first RMS-normalised over its hd values and scaled by its
 // gain (gq for q heads, gk for k heads), in fp32, before the rotation.
-template <bool F8, bool QKN>
+// FUSED: the row first comes out of the QKV projection's split-K partials
+// (fp32 [splits][T][cols], summed in split order) times the row scale of the
+// RMSNorm that preceded the projection, 1 / sqrt(sum_s ssq[s][r] / d + eps)
+// (the projection ran on x * gamma, see the weight-streaming GEMM's
+// PRENORM form); it is rounded to bf16 into qkv and then rotated and
+// appended as in the plain form.
+struct QkvPartials {
+  const float *part, *ssq;
+  int splits, d;
+  float eps;
+};
+template <bool F8, bool QKN, bool FUSED = false>
 __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv, uint16_t *__restrict__ kc,
                                                      uint16_t *__restrict__ vc, const int32_t *__restrict__ bt,
                                                      int num_pages, int max_pages, DevMeta m, int nq, int nkv,
                                                      int hd, double log2_theta, float ks, float vs,
                                                      const uint16_t *__restrict__ gq,
-                                                     const uint16_t *__restrict__ gk, float eps) {
+                                                     const uint16_t *__restrict__ gk, float eps,
+                                                     QkvPartials qp = QkvPartials{}) {
   __shared__ float cs[64], sn[64];
   const int r = blockIdx.x;
+  // block y of the row takes heads [h_lo, h_hi) of the q, k, v heads
+  const int nh = nq + 2 * nkv;
+  const int hpb = (nh + gridDim.y - 1) / gridDim.y;
+  const int h_lo = blockIdx.y * hpb, h_hi = min(nh, h_lo + hpb);
+  if constexpr (FUSED) {
+    const int cols = nh * hd;
+    float ss = 0.f;
+    for (int s = 0; s < qp.splits; ++s) ss += qp.ssq[(size_t)s * m.T + r];
+    const float inv = 1.0f / sqrtf(ss / (float)qp.d + qp.eps);
+    const size_t stride = (size_t)m.T * cols;
+    const float *p0 = qp.part + (size_t)r * cols;
+    uint16_t *dst = qkv + (size_t)r * cols;
+    for (int c = h_lo * hd + threadIdx.x * 4; c < h_hi * hd; c += blockDim.x * 4) {
+      f32x4_t x = {0.f, 0.f, 0.f, 0.f};
+      for (int s = 0; s < qp.splits; ++s) x += *reinterpret_cast<const f32x4_t *>(p0 + s * stride + c);
+      *reinterpret_cast<u32x2_t *>(dst + c) = u32x2_t{pack_bf16x2(x[0] * inv, x[1] * inv), pack_bf16x2(x[2] * inv, x[3] * inv)};
+    }
+    __syncthreads();  // (the row's bf16 values are read back by other threads below)
+  }
   const int seq = m.row_seq[r];
   const int pos = m.row_pos[r];
   const int half = hd >> 1;
@@ -137,9 +168,10 @@ __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv,
   const int slot = pos % kPageSize;
   const int hch = half / 8;  // 8-dim chunks per half head
   // q and k heads: (head, chunk of the first half) per thread
-  const int items = (nq + nkv) * hch;
+  const int hk_hi = min(h_hi, nq + nkv);
+  const int items = h_lo < hk_hi ? (hk_hi - h_lo) * hch : 0;
   for (int i = threadIdx.x; i < items; i += blockDim.x) {
-    const int h = i / hch, t0 = (i - h * hch) * 8;
+    const int h = h_lo + i / hch, t0 = (i % hch) * 8;
     const u32x4_t a = ld_u32x4(row + h * hd + t0);
     const u32x4_t b = ld_u32x4(row + h * hd + t0 + half);
     float fa[8], fb[8];
@@ -193,11 +225,12 @@ __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv,
     }
   }
   // v: plain copy, 16 bytes per thread
-  if (page_ok) {
-    const uint16_t *vsrc = row + (nq + nkv) * hd;
-    const int vch = nkv * hd / 8;
+  const int v_lo = max(h_lo, nq + nkv) - (nq + nkv), v_hi = h_hi - (nq + nkv);
+  if (page_ok && v_lo < v_hi) {
+    const uint16_t *vsrc = row + (nq + nkv + v_lo) * hd;
+    const int vch = (v_hi - v_lo) * hd / 8;
     for (int i = threadIdx.x; i < vch; i += blockDim.x) {
-      const int kh = (i * 8) / hd, dd = i * 8 - kh * hd;
+      const int kh = v_lo + (i * 8) / hd, dd = (i * 8) % hd;
       const size_t e0 = (((size_t)page * nkv + kh) * kPageSize + slot) * hd + dd;
       if constexpr (F8)
         *reinterpret_cast<u32x2_t *>(reinterpret_cast<uint8_t *>(vc) + e0) = e4m3x8_of_bf16x8(ld_u32x4(vsrc + i * 8), vs);
@@ -205,6 +238,34 @@ __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv,
         st_u32x4(vc + e0, ld_u32x4(vsrc + i * 8));
     }
   }
+}
+
+hipError_t launch_qkv_rope_append(const Shape &s, const float *part, int splits, const float *ssq, uint16_t *qkv,
+                                  const KV &kv, const DevMeta &m, hipStream_t st, const uint16_t *gq,
+                                  const uint16_t *gk) {
+  if (m.T <= 0) return hipSuccess;
+  if (s.qkn && (!gq || !gk)) return hipErrorInvalidValue;
+  if (s.qkv_cols() % 4) return hipErrorInvalidValue;
+  const QkvPartials qp{part, ssq, splits, s.hidden, s.eps};
+  // four heads per block: a row's split-K sum is spread over several CUs
+  const int groups = (s.nq + 2 * s.nkv + 3) / 4;
+#define EB_ROPE_APPEND(F8_, QKN_)                                                                                   \
+  hipLaunchKernelGGL((k_rope_append<F8_, QKN_, true>), dim3(m.T, groups), dim3(256), 0, st, qkv, kv.k, kv.v, kv.bt, \
+                     kv.num_pages, kv.max_pages, m, s.nq, s.nkv, s.hd, log2((double)s.theta), kv.ks, kv.vs, gq, gk, \
+                     s.eps, qp)
+  if (kv.f8) {
+    if (s.qkn)
+      EB_ROPE_APPEND(true, true);
+    else
+      EB_ROPE_APPEND(true, false);
+  } else {
+    if (s.qkn)
+      EB_ROPE_APPEND(false, true);
+    else
+      EB_ROPE_APPEND(false, false);
+  }
+#undef EB_ROPE_APPEND
+  return hipGetLastError();
 }
 
 hipError_t launch_rope_append(const Shape &s, uint16_t *qkv, const KV &kv, const DevMeta &m, hipStream_t st,

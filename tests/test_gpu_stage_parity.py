@@ -199,3 +199,37 @@ def test_70b_decode_stages_full_size():
     batch = gen.batch_70b_decode()
     sample = [int(np.argmax(batch.context_lens)), 100]
     _sampled_stages(shape, batch, {k: v.cuda() for k, v in w.items()}, Wo, "decode", sample)
+
+
+# ------------------------------------------------- fused first RMSNorm + QKV
+
+# A layer whose decode-sized QKV projection splits K (hidden 1024: 24 column
+# tiles of 64, 32 k-steps -> 2 splits), so the step folds the first RMSNorm
+# into the projection's operand staging and the split-K sum into the RoPE /
+# append kernel; with and without the per-head q/k norms.
+MID = gen.LayerShape("mid-fused", 1024, 8, 2, 128, 2048, 5e5)
+MID_QKN = gen.LayerShape("mid-fused-qk-norm", 1024, 8, 2, 128, 2048, 1e6, qk_norm=True)
+
+
+@pytest.mark.parametrize("shape", [MID, MID_QKN], ids=lambda s: s.name)
+def test_fused_norm_qkv_decode_stages(shape):
+    rng = np.random.default_rng(11)
+    batch = gen.Batch(rng.integers(16, 700, 24).astype(np.int32), np.ones(24, np.int32), "mid-decode")
+    case = make_case(shape, batch)
+    d = DevCase(case)
+    h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
+    y, st = step_with_stages(h, "decode", d.w, d.k, d.v, d.bt, batch, d.x)
+    o = case.oracle_inputs()
+    W = oracle.prepare_weights(o["w_bits"], o["cfg"])
+    ref_y, inter = oracle.layer_step(o["cfg"], W, o["k_cache"], o["v_cache"], o["block_tables"], o["context_lens"],
+                                     o["chunk_lens"], o["x_bits"], intermediates=True)
+    ref = oracle_stages(inter, W, o["cfg"])
+    off = batch.row_offsets
+    for i in range(batch.num_seqs):
+        rows = slice(off[i], off[i + 1])
+        compare_stages(y, st, ref_y, ref, rows, rows, f"{shape.name} request {i}")
+    # the cached keys and values of the new rows (rotated k) against the oracle's
+    from tests._gpu import cache_bits, check_cache_update
+    bt = case.pool.block_tables.numpy()
+    check_cache_update(gen.bits(case.pool.k_cache), cache_bits(d.k), o["k_cache"], batch, bt)
+    check_cache_update(gen.bits(case.pool.v_cache), cache_bits(d.v), o["v_cache"], batch, bt)
