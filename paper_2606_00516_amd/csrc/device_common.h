@@ -131,6 +131,13 @@ EB_DEV f32x4_t mfma16x16x32(u32x4_t a, u32x4_t b, f32x4_t c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
 }
 
+// D = A B + C on one 32x32x16 bf16 tile.  Operand layout (lane l):
+//   A: row l % 32, k = 8 (l / 32) .. + 7      B: col l % 32, same k
+//   C/D (16 values): value i at row 8 (i / 4) + 4 (l / 32) + i % 4, col l % 32
+EB_DEV f32x16_t mfma32x32x16(u32x4_t a, u32x4_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+}
+
 // D = A B + C on one 16x16x16 bf16 tile.  Operand layout (lane l):
 //   A: row l % 16, k = 4 (l / 16) .. + 3      B: col l % 16, same k
 //   C/D: as for the 16x16x32 tile

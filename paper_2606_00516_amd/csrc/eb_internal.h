@@ -24,7 +24,7 @@ constexpr int kCombInfoInts = 4;
 // in the prefill-only launch and inside the mixed launch (must agree with
 // PrefillTraits in the attention kernels).
 inline int prefill_bq(int group, bool mixed_launch) {
-  return mixed_launch ? 64 / group : 128 / group;
+  return mixed_launch ? 128 / group : 128 / group;
 }
 
 // Work order of the single mixed attention launch.  Its P prefill items are

@@ -13,7 +13,7 @@ constexpr int kShortHeads = 4;      // must match kShortDecodeHeads
 
 // query positions per prefill item (must match the attention kernels)
 int prefill_bq_host(int group, bool mixed_launch) {
-  return mixed_launch ? 64 / group : 128 / group;
+  return mixed_launch ? 128 / group : 128 / group;
 }
 }  // namespace
 

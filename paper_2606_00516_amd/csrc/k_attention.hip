@@ -1104,6 +1104,251 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
   }
 }
 
+// Prefill item on 32x32x16 products: 128 query rows per item (G heads x
+// 128 / G positions) over 4 wavefronts, 32 rows (one 32-column block of the
+// products) per wave.  Against 16-row blocks every K and V^T fragment read
+// from LDS serves twice the rows, so a tile costs half the LDS reads per
+// FLOP.  Per 64-key tile a wave forms S^T = K Q^T as two 32-key blocks
+// (eight k-steps of 16 dims each), keeps its query's 32 scores in the lane
+// pair (l, l + 32), and feeds P^T straight from the score registers into
+// O^T += V^T P^T: k-step j of the P.V product takes score values 8 j' ..
+// 8 j' + 7 of key block j / 2 (j' = j % 2), i.e. keys 16 j' + {0..3, 8..11}
+// + 4 (l / 32) of the block, and the V^T operand reads the same keys.
+template <int HD, int G, int NW, bool F8>
+__device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
+                                               const DevMeta md, int tile, int kh, uint16_t *__restrict__ out,
+                                               uint16_t *Ks, uint16_t *Vt) {
+  constexpr int BQ = NW * 32 / G;          // query positions per item
+  static_assert(NW * 32 == G * BQ, "rows per item");
+  constexpr int KT = 64;                   // keys per tile
+  constexpr int KSS = HD + 8, VTS = KT + 4;
+  constexpr int KCH = KT * (HD / 8), VCH = (KT / 2) * (HD / 8);
+  constexpr int NT = NW * 64;
+  constexpr int KPT = (KCH + NT - 1) / NT, VPT = (VCH + NT - 1) / NT;
+  constexpr int NKS = HD / 16;  // k-steps of the QK^T product
+  constexpr int NOB = HD / 32;  // 32-dim output blocks
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int cols = (nq + 2 * nkv) * HD;
+  const int seq = md.tile_seq[tile];
+  const int qb = md.tile_qb[tile];
+  const int c = md.seq_ctx[seq];
+  const int n = md.seq_len[seq];
+  const int row0 = md.seq_row[seq];
+  const int q_lo = qb * BQ;
+  const int q_hi = min(n, q_lo + BQ);
+  const int kend = c + q_hi;
+  const int klen = c + n;
+  const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
+  const int npages = (klen + kPageSize - 1) / kPageSize;
+  const float qscale = F8 ? kLog2e / sqrtf((float)HD) * kv.ks : kLog2e / sqrtf((float)HD);
+  const int lq = lane & 31;  // query column of this lane
+  const int lh = lane >> 5;  // k half
+
+  // the wave's 32 rows: HPB heads x RPH positions
+  constexpr int RPH = BQ < 32 ? BQ : 32, HPB = 32 / RPH, HG = G / HPB;
+  static_assert(HPB * RPH == 32 && HG * HPB == G, "row block shape");
+  const int hb = wave % HG, sub = wave / HG;
+  const int hrow = hb * HPB + lq / RPH;
+  const int qrel = q_lo + sub * RPH + lq % RPH;
+  const bool qok = qrel < q_hi;
+  u32x4_t qreg[NKS];
+  {
+    const uint16_t *src = qkv + (size_t)(row0 + qrel) * cols + (kh * G + hrow) * HD + lh * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qreg[ks] = qok ? ld_u32x4(src + ks * 16) : u32x4_t{0, 0, 0, 0};
+  }
+  f32x16_t oacc[NOB];
+#pragma unroll
+  for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) oacc[ob][i] = 0.f;
+  float mrun = kNegInf, lrun = 0.f;
+
+  typedef int i32x4_t __attribute__((ext_vector_type(4)));
+  constexpr int PPT = KT / kPageSize;
+  static_assert(PPT == 4, "tile = 4 pages");
+  typedef const __attribute__((address_space(4))) int32_t *bt_ptr_t;
+  const bt_ptr_t btc = (bt_ptr_t)bt;
+  auto bt_tile = [&](int t) -> i32x4_t {
+    const int p0 = t * PPT;
+    i32x4_t r = {-1, -1, -1, -1};
+#pragma unroll
+    for (int j = 0; j < PPT; ++j)
+      if (p0 + j < npages) r[j] = btc[p0 + j];
+    return r;
+  };
+  static_assert(HD == 64 || HD == 128, "keys of one load within one page");
+  typedef typename std::conditional<F8, const uint8_t, const uint16_t>::type elem_t;
+  auto page_base = [&](elem_t *arr, const i32x4_t &btv, int j, bool &ok) -> elem_t * {
+    const int phys = j == 0 ? btv[0] : j == 1 ? btv[1] : j == 2 ? btv[2] : btv[3];
+    ok = phys >= 0 && phys < kv.num_pages;
+    return arr + (ok ? ((size_t)phys * nkv + kh) * (kPageSize * HD) : 0);
+  };
+  auto ld8 = [&](elem_t *p) -> RawT<F8> {
+    if constexpr (F8)
+      return *reinterpret_cast<const u32x2_t *>(p);
+    else
+      return ld_u32x4(p);
+  };
+  elem_t *const kbase = reinterpret_cast<elem_t *>(kv.k), *const vbase = reinterpret_cast<elem_t *>(kv.v);
+  RawT<F8> kreg[KPT], vreg[VPT][2];
+  uint32_t present = 0;
+  auto fetch = [&](int t, const i32x4_t &btv) {
+    const int k0 = t * KT;
+    present = 0;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int u = tid + i * NT;
+      const int key = u / (HD / 8), dc = u % (HD / 8);
+      const int j = __builtin_amdgcn_readfirstlane(key / kPageSize);
+      bool pok;
+      elem_t *pb = page_base(kbase, btv, j, pok);
+      kreg[i] = ld8(pb + (key % kPageSize) * HD + dc * 8);
+      present |= (u < KCH && pok && k0 + key < klen ? 1u : 0u) << i;
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int u = tid + i * NT;
+      const int kpair = u / (HD / 8), dc = u % (HD / 8);
+      const int j = __builtin_amdgcn_readfirstlane((2 * kpair) / kPageSize);
+      bool pok;
+      elem_t *pb = page_base(vbase, btv, j, pok);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int key = 2 * kpair + e;
+        vreg[i][e] = ld8(pb + (key % kPageSize) * HD + dc * 8);
+        present |= (u < VCH && pok && k0 + key < klen ? 1u : 0u) << (KPT + 2 * i + e);
+      }
+    }
+  };
+  auto stage = [&]() {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int u = tid + i * NT;
+      if (u < KCH)
+        st_u32x4(Ks + (u / (HD / 8)) * KSS + (u % (HD / 8)) * 8,
+                 (present >> i) & 1u ? raw_bf16<F8>(kreg[i]) : u32x4_t{0, 0, 0, 0});
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int u = tid + i * NT;
+      if (u < VCH) {
+        const int kpair = u / (HD / 8), dc = u % (HD / 8);
+        const int col = vt_col(dc * 8, 2 * kpair);
+        const bool p0 = (present >> (KPT + 2 * i)) & 1u, p1 = (present >> (KPT + 2 * i + 1)) & 1u;
+        const u32x4_t v0 = raw_bf16<F8>(vreg[i][0]), v1 = raw_bf16<F8>(vreg[i][1]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t a0 = p0 ? v0[j] : 0u, a1 = p1 ? v1[j] : 0u;
+          *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j) * VTS + col) = (a0 & 0xFFFFu) | (a1 << 16);
+          *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j + 1) * VTS + col) = (a0 >> 16) | (a1 & 0xFFFF0000u);
+        }
+      }
+    }
+  };
+
+  const int min_qpos = c + q_lo;
+  const int qpos = c + qrel;
+  const int ntiles = (kend + KT - 1) / KT;
+  i32x4_t bt_next = bt_tile(1);
+  fetch(0, bt_tile(0));
+  for (int t = 0; t < ntiles; ++t) {
+    const int k0 = t * KT;
+    stage();
+    __syncthreads();
+    if (t + 1 < ntiles) {  // in flight while this tile is consumed
+      const i32x4_t bt_cur = bt_next;
+      bt_next = bt_tile(t + 2);
+      fetch(t + 1, bt_cur);
+    }
+    // S^T: two 32-key blocks, lane value i at key 32 kb + 8 (i / 4) + 4 lh + i % 4
+    f32x16_t sc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const u32x4_t a = ld_u32x4(Ks + (kb * 32 + lq) * KSS + ks * 16 + lh * 8);
+        sc[kb] = mfma32x32x16(a, qreg[ks], sc[kb]);
+      }
+    // causal mask on the diagonal tiles (rows past the item's end are never
+    // stored and do not enter another row's arithmetic)
+    if (k0 + KT - 1 > min_qpos) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int kp = k0 + kb * 32 + 8 * (i >> 2) + 4 * lh + (i & 3);
+          sc[kb][i] = kp > qpos ? kNegInf : sc[kb][i];
+        }
+    }
+    float mraw = kNegInf;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mraw = fmaxf(mraw, sc[kb][i]);
+    mraw = fmaxf(mraw, shfl_xor_f32(mraw, 32));
+    const float mx = fmaxf(mrun, mraw * qscale);
+    const float alpha = (mrun == kNegInf) ? 0.f : fast_exp2(mrun - mx);
+    const float neg = mx != kNegInf ? -mx : 0.f;
+    float l = lrun * alpha;
+    uint32_t pk[2][8];  // [key block][pair]: bf16 pairs of values 2 p, 2 p + 1
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int pr = 0; pr < 8; ++pr) {
+        const float p0 = fast_exp2(fmaf(sc[kb][2 * pr], qscale, neg));
+        const float p1 = fast_exp2(fmaf(sc[kb][2 * pr + 1], qscale, neg));
+        l += p0;
+        l += p1;
+        pk[kb][pr] = bf16_pair_rne(p0, p1);
+      }
+    lrun = l;
+    mrun = mx;
+    const bool rescale = __builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0;
+    // O^T += V^T P^T: k-step j takes keys 16 (j % 2) + {0..3, 8..11} + 4 lh of key block j / 2
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) {
+      f32x16_t acc = oacc[ob];
+      if (rescale) acc = acc * alpha;
+      const int vr = ob * 32 + lq;
+      const uint16_t *vrow = Vt + vr * VTS;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int kb = j >> 1, jj = j & 1;
+        const int key0 = kb * 32 + 16 * jj + 4 * lh;
+        const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vrow + vt_col(vr, key0));
+        const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vrow + vt_col(vr, key0 + 8));
+        const u32x4_t a = {a0[0], a0[1], a1[0], a1[1]};
+        const u32x4_t b = {pk[kb][4 * jj], pk[kb][4 * jj + 1], pk[kb][4 * jj + 2], pk[kb][4 * jj + 3]};
+        acc = mfma32x32x16(a, b, acc);
+      }
+      oacc[ob] = acc;
+    }
+    __syncthreads();
+  }
+  // normalise and store: lane holds dims ob 32 + 8 g + 4 lh + e (e < 4) of its query
+  float l = lrun;
+  l += shfl_xor_f32(l, 32);
+  if (qok) {
+    const float inv = F8 ? kv.vs / l : 1.0f / l;
+    uint16_t *dst = out + (size_t)(row0 + qrel) * nq * HD + (kh * G + hrow) * HD + 4 * lh;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const u32x2_t w = {pack_bf16x2(oacc[ob][4 * g] * inv, oacc[ob][4 * g + 1] * inv),
+                           pack_bf16x2(oacc[ob][4 * g + 2] * inv, oacc[ob][4 * g + 3] * inv)};
+        *reinterpret_cast<u32x2_t *>(dst + ob * 32 + 8 * g) = w;
+      }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // kernels
 // ---------------------------------------------------------------------------
@@ -1138,20 +1383,21 @@ __global__ __launch_bounds__(64 * kDecWaves, F8 ? 4 : 1) void k_decode_mfma(cons
                                                    l2, l3);
 }
 
-// Prefill-only launch: 8 wavefronts per 128-row item, one 16-row block per
-// wave.  (Two blocks per wave in 4-wave items halve the LDS reads per MFMA
-// but measure slower: a wave's serial softmax -> product chain, not LDS
-// bandwidth, bounds the tile loop.)
-constexpr int kPrefillWaves = 8;
+// Prefill-only launch: 4 wavefronts per 128-row item, 32 rows per wave on
+// 32x32x16 products.
+constexpr int kPrefillWaves = 4;
+template <int HD>
+struct PrefillLds {
+  static constexpr int K_BYTES = 64 * (HD + 8) * 2;  // K tile, row-major
+  static constexpr int VT_BYTES = HD * (64 + 4) * 2;  // V^T tile
+};
 
 template <int HD, int G, bool F8>
-__global__ __launch_bounds__(64 * kPrefillWaves) void k_prefill(const uint16_t *qkv, int nq, int nkv, KV kv,
-                                                                   DevMeta md, uint16_t *out) {
-  constexpr int BQ = prefill_item_positions<G, false>();
-  using Tr = PrefillTraits<HD, G, kPrefillWaves, BQ>;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[Tr::LDS_BYTES / 2];
-  prefill_item<HD, G, kPrefillWaves, BQ, F8>(qkv, nq, nkv, kv, md, blockIdx.x / nkv, blockIdx.x % nkv, out, lds,
-                                             lds + Tr::KS_BYTES / 2);
+__global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_prefill(const uint16_t *qkv, int nq, int nkv, KV kv,
+                                                                      DevMeta md, uint16_t *out) {
+  __shared__ __attribute__((aligned(16))) uint16_t lds[(PrefillLds<HD>::K_BYTES + PrefillLds<HD>::VT_BYTES) / 2];
+  prefill_item32<HD, G, kPrefillWaves, F8>(qkv, nq, nkv, kv, md, blockIdx.x / nkv, blockIdx.x % nkv, out, lds,
+                                           lds + PrefillLds<HD>::K_BYTES / 2);
 }
 
 // One grid for a mixed step: items [0, n_tiles) are prefill tiles (longest
@@ -1171,16 +1417,15 @@ __device__ __forceinline__ void mixed_slot(int b, int n_prefill, int s, int &pf,
 }
 
 template <int HD, int G, bool F8>
-__global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
+__global__ __launch_bounds__(256, 2) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
                                                float *part_o, float *part_ml, int stride) {
-  constexpr int BQ = prefill_item_positions<G, true>();
-  using Tr = PrefillTraits<HD, G, 4, BQ>;
-  constexpr int PB = Tr::LDS_BYTES, DB = DecodeTraits<HD, G, 4>::LDS_BYTES;
+  constexpr int PB = PrefillLds<HD>::K_BYTES + PrefillLds<HD>::VT_BYTES, DB = DecodeTraits<HD, G, 4>::LDS_BYTES;
   __shared__ __attribute__((aligned(16))) uint16_t lds[(PB > DB ? PB : DB) / 2];
   int pf, du;
   mixed_slot(blockIdx.x, md.n_tiles * nkv, stride, pf, du);
   if (pf >= 0)
-    prefill_item<HD, G, 4, BQ, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, lds, lds + Tr::KS_BYTES / 2);
+    prefill_item32<HD, G, 4, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, lds,
+                                 lds + PrefillLds<HD>::K_BYTES / 2);
   else
     decode_item<HD, G, 4, F8>(qkv, nq, nkv, kv, md, du, out, part_o, part_ml, reinterpret_cast<float *>(lds));
 }
@@ -1188,19 +1433,17 @@ __global__ __launch_bounds__(256) void k_mixed(const uint16_t *qkv, int nq, int 
 // The same with matrix-core decode items; prefill tiles borrow two of the
 // page-slot arrays.
 template <int HD, int G, bool F8>
-__global__ __launch_bounds__(256) void k_mixed_mfma(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
+__global__ __launch_bounds__(256, 2) void k_mixed_mfma(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
                                                     uint16_t *out, float *part_o, float *part_ml, int stride) {
-  constexpr int BQ = prefill_item_positions<G, true>();
-  using Tr = PrefillTraits<HD, G, 4, BQ>;
   constexpr int MS = 2;                           // ring depth of decode items in the mixed launch
   constexpr int SLOT = MdecTraits<HD>::SLOT;      // bf16-sized slots: prefill tiles stage bf16
-  static_assert(Tr::KS_BYTES <= 4 * SLOT && Tr::VT_BYTES <= 4 * SLOT, "LDS");
+  static_assert(PrefillLds<HD>::K_BYTES <= 4 * SLOT && PrefillLds<HD>::VT_BYTES <= 4 * SLOT, "LDS");
   EB_MDEC_LDS(4 * SLOT, MS)
   int pf, du;
   mixed_slot(blockIdx.x, md.n_tiles * nkv, stride, pf, du);
   if (pf >= 0)
-    prefill_item<HD, G, 4, BQ, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, reinterpret_cast<uint16_t *>(l0),
-                                   reinterpret_cast<uint16_t *>(l1));
+    prefill_item32<HD, G, 4, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, reinterpret_cast<uint16_t *>(l0),
+                                 reinterpret_cast<uint16_t *>(l1));
   else
     decode_item_mfma<HD, G, 4, MS, F8, SLOT>(qkv, nq, nkv, kv, md, du, out, part_o, part_ml, l0, l1, l2, l3);
 }
