@@ -1104,6 +1104,8 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
   }
 }
 
+constexpr float kPrefillSlack = 8.0f;  // log2 units
+
 // Prefill item on 32x32x16 products: 128 query rows per item (G heads x
 // 128 / G positions) over 4 wavefronts, 32 rows (one 32-column block of the
 // products) per wave.  Against 16-row blocks every K and V^T fragment read
@@ -1131,11 +1133,13 @@ __device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv,
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int cols = (nq + 2 * nkv) * HD;
-  const int seq = md.tile_seq[tile];
-  const int qb = md.tile_qb[tile];
-  const int c = md.seq_ctx[seq];
-  const int n = md.seq_len[seq];
-  const int row0 = md.seq_row[seq];
+  // the item's metadata is uniform: held in scalar registers, so that the
+  // page arithmetic derived from it stays scalar too
+  const int seq = __builtin_amdgcn_readfirstlane(md.tile_seq[tile]);
+  const int qb = __builtin_amdgcn_readfirstlane(md.tile_qb[tile]);
+  const int c = __builtin_amdgcn_readfirstlane(md.seq_ctx[seq]);
+  const int n = __builtin_amdgcn_readfirstlane(md.seq_len[seq]);
+  const int row0 = __builtin_amdgcn_readfirstlane(md.seq_row[seq]);
   const int q_lo = qb * BQ;
   const int q_hi = min(n, q_lo + BQ);
   const int kend = c + q_hi;
@@ -1171,80 +1175,84 @@ __device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv,
   static_assert(PPT == 4, "tile = 4 pages");
   typedef const __attribute__((address_space(4))) int32_t *bt_ptr_t;
   const bt_ptr_t btc = (bt_ptr_t)bt;
+  // page ids of tile t; pages past the sequence repeat its last id (their
+  // ranges below are empty), so the loads need no branch and no select
   auto bt_tile = [&](int t) -> i32x4_t {
     const int p0 = t * PPT;
-    i32x4_t r = {-1, -1, -1, -1};
+    i32x4_t r;
 #pragma unroll
-    for (int j = 0; j < PPT; ++j)
-      if (p0 + j < npages) r[j] = btc[p0 + j];
+    for (int j = 0; j < PPT; ++j) r[j] = btc[min(p0 + j, npages - 1)];
     return r;
   };
   static_assert(HD == 64 || HD == 128, "keys of one load within one page");
   typedef typename std::conditional<F8, const uint8_t, const uint16_t>::type elem_t;
-  auto page_base = [&](elem_t *arr, const i32x4_t &btv, int j, bool &ok) -> elem_t * {
+  constexpr int ES = F8 ? 1 : 2;  // bytes per cache element
+  // Page j of tile t as a buffer range over its keys below klen (empty for an
+  // id outside the pool): loads past it return zeros without memory traffic,
+  // so keys past the sequence and bad ids stage as zeros with no selects.
+  constexpr uint32_t kPageHeadBytes = kPageSize * HD * ES;
+  const uint32_t page_bytes = (uint32_t)nkv * kPageHeadBytes;  // one page of all kv heads
+  auto page_rsrc = [&](const uint8_t *base, const i32x4_t &btv, int j, int first_key) -> buf_rsrc_t {
     const int phys = j == 0 ? btv[0] : j == 1 ? btv[1] : j == 2 ? btv[2] : btv[3];
-    ok = phys >= 0 && phys < kv.num_pages;
-    return arr + (ok ? ((size_t)phys * nkv + kh) * (kPageSize * HD) : 0);
+    const int rem = klen - first_key;  // keys of the sequence from the page's first on
+    const bool live = (unsigned)phys < (unsigned)kv.num_pages && rem > 0;
+    // (uniform; said so, or the compiler forms the range in vector registers
+    // and wraps every load in a loop over distinct descriptors)
+    const int range = __builtin_amdgcn_readfirstlane(live ? min(rem, kPageSize) * (HD * ES) : 0);
+    return make_rsrc(base + (uint64_t)(uint32_t)(live ? phys : 0) * page_bytes, range);
   };
-  auto ld8 = [&](elem_t *p) -> RawT<F8> {
+  auto ld8 = [&](buf_rsrc_t r, int off) -> RawT<F8> {
     if constexpr (F8)
-      return *reinterpret_cast<const u32x2_t *>(p);
+      return buf_ld_u32x2<0>(r, off);
     else
-      return ld_u32x4(p);
+      return buf_ld_u32x4<0>(r, off);
   };
-  elem_t *const kbase = reinterpret_cast<elem_t *>(kv.k), *const vbase = reinterpret_cast<elem_t *>(kv.v);
+  const uint8_t *const kbase = reinterpret_cast<const uint8_t *>(kv.k) + (size_t)kh * kPageHeadBytes;
+  const uint8_t *const vbase = reinterpret_cast<const uint8_t *>(kv.v) + (size_t)kh * kPageHeadBytes;
   RawT<F8> kreg[KPT], vreg[VPT][2];
-  uint32_t present = 0;
+  static_assert(KCH % NT == 0 && VCH % NT == 0, "whole load rounds");
+  // round i of the K loads covers keys i * NT / (HD / 8) .. (page fixed per
+  // wave); round i of the V loads covers key pairs likewise
+  constexpr int KPR = NT / (HD / 8), WPK = kPageSize * (HD / 8) / 64;  // keys per round, waves per page
+  static_assert(KPR % kPageSize == 0, "pages per round");
+  // the page of K load i: i KPR / 16 + wave / WPK (the second term is 0 when
+  // one round covers whole pages per wave group of NW)
+  const int kpw = NW <= WPK ? 0 : wave / WPK;
   auto fetch = [&](int t, const i32x4_t &btv) {
     const int k0 = t * KT;
-    present = 0;
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int u = tid + i * NT;
       const int key = u / (HD / 8), dc = u % (HD / 8);
-      const int j = __builtin_amdgcn_readfirstlane(key / kPageSize);
-      bool pok;
-      elem_t *pb = page_base(kbase, btv, j, pok);
-      kreg[i] = ld8(pb + (key % kPageSize) * HD + dc * 8);
-      present |= (u < KCH && pok && k0 + key < klen ? 1u : 0u) << i;
+      const int j = i * (KPR / kPageSize) + kpw;
+      kreg[i] = ld8(page_rsrc(kbase, btv, j, k0 + j * kPageSize), ((key % kPageSize) * HD + dc * 8) * ES);
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int u = tid + i * NT;
       const int kpair = u / (HD / 8), dc = u % (HD / 8);
-      const int j = __builtin_amdgcn_readfirstlane((2 * kpair) / kPageSize);
-      bool pok;
-      elem_t *pb = page_base(vbase, btv, j, pok);
+      const int j = i * (KPR / 8) + wave / (HD / 64);  // page of keys 2 kpair, 2 kpair + 1
+      const buf_rsrc_t r = page_rsrc(vbase, btv, j, k0 + j * kPageSize);
 #pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int key = 2 * kpair + e;
-        vreg[i][e] = ld8(pb + (key % kPageSize) * HD + dc * 8);
-        present |= (u < VCH && pok && k0 + key < klen ? 1u : 0u) << (KPT + 2 * i + e);
-      }
+      for (int e = 0; e < 2; ++e) vreg[i][e] = ld8(r, (((2 * kpair + e) % kPageSize) * HD + dc * 8) * ES);
     }
   };
   auto stage = [&]() {
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int u = tid + i * NT;
-      if (u < KCH)
-        st_u32x4(Ks + (u / (HD / 8)) * KSS + (u % (HD / 8)) * 8,
-                 (present >> i) & 1u ? raw_bf16<F8>(kreg[i]) : u32x4_t{0, 0, 0, 0});
+      st_u32x4(Ks + (u / (HD / 8)) * KSS + (u % (HD / 8)) * 8, raw_bf16<F8>(kreg[i]));
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int u = tid + i * NT;
-      if (u < VCH) {
-        const int kpair = u / (HD / 8), dc = u % (HD / 8);
-        const int col = vt_col(dc * 8, 2 * kpair);
-        const bool p0 = (present >> (KPT + 2 * i)) & 1u, p1 = (present >> (KPT + 2 * i + 1)) & 1u;
-        const u32x4_t v0 = raw_bf16<F8>(vreg[i][0]), v1 = raw_bf16<F8>(vreg[i][1]);
+      const int kpair = u / (HD / 8), dc = u % (HD / 8);
+      const int col = vt_col(dc * 8, 2 * kpair);
+      const u32x4_t v0 = raw_bf16<F8>(vreg[i][0]), v1 = raw_bf16<F8>(vreg[i][1]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t a0 = p0 ? v0[j] : 0u, a1 = p1 ? v1[j] : 0u;
-          *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j) * VTS + col) = (a0 & 0xFFFFu) | (a1 << 16);
-          *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j + 1) * VTS + col) = (a0 >> 16) | (a1 & 0xFFFF0000u);
-        }
+      for (int j = 0; j < 4; ++j) {  // dims 2 j, 2 j + 1 of keys 2 kpair, 2 kpair + 1
+        *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j) * VTS + col) = __builtin_amdgcn_perm(v1[j], v0[j], 0x05040100u);
+        *reinterpret_cast<uint32_t *>(Vt + (dc * 8 + 2 * j + 1) * VTS + col) = __builtin_amdgcn_perm(v1[j], v0[j], 0x07060302u);
       }
     }
   };
@@ -1258,11 +1266,6 @@ __device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv,
     const int k0 = t * KT;
     stage();
     __syncthreads();
-    if (t + 1 < ntiles) {  // in flight while this tile is consumed
-      const i32x4_t bt_cur = bt_next;
-      bt_next = bt_tile(t + 2);
-      fetch(t + 1, bt_cur);
-    }
     // S^T: two 32-key blocks, lane value i at key 32 kb + 8 (i / 4) + 4 lh + i % 4
     f32x16_t sc[2];
 #pragma unroll
@@ -1276,16 +1279,20 @@ __device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv,
         const u32x4_t a = ld_u32x4(Ks + (kb * 32 + lq) * KSS + ks * 16 + lh * 8);
         sc[kb] = mfma32x32x16(a, qreg[ks], sc[kb]);
       }
+    {  // the next tile's loads, issued while the products run and in flight
+       // while this tile is consumed (past the last tile: empty ranges, no traffic)
+      const i32x4_t bt_cur = bt_next;
+      bt_next = bt_tile(t + 2);
+      fetch(t + 1, bt_cur);
+    }
     // causal mask on the diagonal tiles (rows past the item's end are never
     // stored and do not enter another row's arithmetic)
     if (k0 + KT - 1 > min_qpos) {
+      const int d = qpos - k0 - 4 * lh;  // value i of block kb is visible iff its key offset is <= d
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int kp = k0 + kb * 32 + 8 * (i >> 2) + 4 * lh + (i & 3);
-          sc[kb][i] = kp > qpos ? kNegInf : sc[kb][i];
-        }
+        for (int i = 0; i < 16; ++i) sc[kb][i] = kb * 32 + 8 * (i >> 2) + (i & 3) > d ? kNegInf : sc[kb][i];
     }
     float mraw = kNegInf;
 #pragma unroll
@@ -1293,8 +1300,15 @@ __device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv,
 #pragma unroll
       for (int i = 0; i < 16; ++i) mraw = fmaxf(mraw, sc[kb][i]);
     mraw = fmaxf(mraw, shfl_xor_f32(mraw, 32));
-    const float mx = fmaxf(mrun, mraw * qscale);
-    const float alpha = (mrun == kNegInf) ? 0.f : fast_exp2(mrun - mx);
+    // The running max (log2 units) moves only when the tile's max exceeds it
+    // by more than kPrefillSlack; in between, probabilities stay below
+    // 2^kPrefillSlack, exact in fp32 and bf16 alike, and most tiles skip the
+    // rescaling of the accumulators.  The normaliser sums the bf16 values
+    // that enter the P.V product.
+    const float ms = mraw * qscale;
+    const bool bump = ms > mrun + kPrefillSlack;
+    const float mx = bump ? ms : mrun;
+    const float alpha = bump ? fast_exp2(mrun - mx) : 1.0f;  // 0 on the first tile
     const float neg = mx != kNegInf ? -mx : 0.f;
     float l = lrun * alpha;
     uint32_t pk[2][8];  // [key block][pair]: bf16 pairs of values 2 p, 2 p + 1
@@ -1304,18 +1318,21 @@ __device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv,
       for (int pr = 0; pr < 8; ++pr) {
         const float p0 = fast_exp2(fmaf(sc[kb][2 * pr], qscale, neg));
         const float p1 = fast_exp2(fmaf(sc[kb][2 * pr + 1], qscale, neg));
-        l += p0;
-        l += p1;
         pk[kb][pr] = bf16_pair_rne(p0, p1);
+        l = dot2_bf16(pk[kb][pr], 0x3F803F80u, l);  // + both values, (1, 1) in bf16
       }
+    // (a row whose max was still -inf has nothing accumulated to rescale)
+    const bool rescale = __builtin_amdgcn_ballot_w64(bump && mrun != kNegInf) != 0;
     lrun = l;
     mrun = mx;
-    const bool rescale = __builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0;
+    if (__builtin_expect(rescale, 0)) {
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) oacc[ob] = oacc[ob] * alpha;
+    }
     // O^T += V^T P^T: k-step j takes keys 16 (j % 2) + {0..3, 8..11} + 4 lh of key block j / 2
 #pragma unroll
     for (int ob = 0; ob < NOB; ++ob) {
       f32x16_t acc = oacc[ob];
-      if (rescale) acc = acc * alpha;
       const int vr = ob * 32 + lq;
       const uint16_t *vrow = Vt + vr * VTS;
 #pragma unroll

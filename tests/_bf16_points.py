@@ -24,7 +24,9 @@ def rb(x):
 
 def _attention_rounded_p(q, K, V, positions, group):
     """Causal attention with the probabilities rounded to bf16 for the P.V
-    product and the normaliser summed from the unrounded values."""
+    product and the normaliser summed from the unrounded values (the prefill
+    kernels sum the rounded ones; the two normalisers differ by far less
+    than the bounds the model is used for)."""
     n, nq, hd = q.shape
     L = K.shape[0]
     visible = np.arange(L)[None, :] <= np.asarray(positions)[:, None]
