@@ -1105,6 +1105,16 @@ __device__ __forceinline__ void prefill_item(const uint16_t *__restrict__ qkv, i
 }
 
 constexpr float kPrefillSlack = 8.0f;  // log2 units
+// V^T swizzle of the 32x32 item: 4-key group g of row r is stored at group
+// g ^ s(r), s(r) = bit 4 of r in bit 0 and bits 5-6 of r in bits 2-3.  Rows
+// of one 8-row store group share s; with rows of 68 elements the P.V reads
+// (row 32 ob + lq, keys 16 k' + 8 h + 4 lh) meet no bank twice, the stores
+// two-way at most, and each lane's two key halves h stay in address order,
+// so every pair of reads merges into one.
+__device__ __forceinline__ int vt32_col(int r, int key) {
+  return 4 * ((key >> 2) ^ (((r >> 4) & 1) | (((r >> 5) & 3) << 2))) + (key & 3);
+}
+
 
 // Prefill item on 32x32x16 products: 128 query rows per item (G heads x
 // 128 / G positions) over 4 wavefronts, 32 rows (one 32-column block of the
@@ -1247,7 +1257,7 @@ __device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv,
     for (int i = 0; i < VPT; ++i) {
       const int u = tid + i * NT;
       const int kpair = u / (HD / 8), dc = u % (HD / 8);
-      const int col = vt_col(dc * 8, 2 * kpair);
+      const int col = vt32_col(dc * 8, 2 * kpair);
       const u32x4_t v0 = raw_bf16<F8>(vreg[i][0]), v1 = raw_bf16<F8>(vreg[i][1]);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {  // dims 2 j, 2 j + 1 of keys 2 kpair, 2 kpair + 1
@@ -1260,6 +1270,15 @@ __device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv,
   const int min_qpos = c + q_lo;
   const int qpos = c + qrel;
   const int ntiles = (kend + KT - 1) / KT;
+  // V^T operand of the P.V product: row ob 32 + lq, keys kb 32 + 16 jj + 8 h
+  // + 4 lh .. + 3 at vt32_col(row, key), which splits into a lane part and a
+  // constant (the swizzle's lane bit lq / 16 meets only lh, its ob bits only
+  // kb and jj), so every read is one base register plus an immediate offset
+  static_assert(NOB <= 4, "ob bits of the swizzle");
+  const uint16_t *const vlane = Vt + lq * VTS + 4 * (lh ^ (lq >> 4));
+  auto vt_at = [&](int ob, int kb, int jj, int h) -> const uint16_t * {
+    return vlane + ob * 32 * VTS + 8 * h + 16 * ((2 * kb + jj) ^ ob);
+  };
   i32x4_t bt_next = bt_tile(1);
   fetch(0, bt_tile(0));
   for (int t = 0; t < ntiles; ++t) {
@@ -1299,7 +1318,10 @@ __device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv,
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i) mraw = fmaxf(mraw, sc[kb][i]);
-    mraw = fmaxf(mraw, shfl_xor_f32(mraw, 32));
+    {  // with the other half of the wave (lane l ^ 32 holds the same query)
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mraw), __float_as_uint(mraw), false, false);
+      mraw = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    }
     // The running max (log2 units) moves only when the tile's max exceeds it
     // by more than kPrefillSlack; in between, probabilities stay below
     // 2^kPrefillSlack, exact in fp32 and bf16 alike, and most tiles skip the
@@ -1333,14 +1355,11 @@ __device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv,
 #pragma unroll
     for (int ob = 0; ob < NOB; ++ob) {
       f32x16_t acc = oacc[ob];
-      const int vr = ob * 32 + lq;
-      const uint16_t *vrow = Vt + vr * VTS;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int kb = j >> 1, jj = j & 1;
-        const int key0 = kb * 32 + 16 * jj + 4 * lh;
-        const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vrow + vt_col(vr, key0));
-        const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vrow + vt_col(vr, key0 + 8));
+        const u32x2_t a0 = *reinterpret_cast<const u32x2_t *>(vt_at(ob, kb, jj, 0));
+        const u32x2_t a1 = *reinterpret_cast<const u32x2_t *>(vt_at(ob, kb, jj, 1));
         const u32x4_t a = {a0[0], a0[1], a1[0], a1[1]};
         const u32x4_t b = {pk[kb][4 * jj], pk[kb][4 * jj + 1], pk[kb][4 * jj + 2], pk[kb][4 * jj + 3]};
         acc = mfma32x32x16(a, b, acc);
