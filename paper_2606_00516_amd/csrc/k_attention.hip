@@ -1385,6 +1385,246 @@ __device__ __forceinline__ void prefill_item32(const uint16_t *__restrict__ qkv,
   }
 }
 
+// One 16-byte-per-lane load from a buffer range straight into LDS: lane l
+// fills bytes 16 l .. 16 l + 15 from dst (wave-uniform) with the bytes at its
+// offset (zeros past the range).
+__device__ __forceinline__ void lds_dma16(buf_rsrc_t r, uint8_t *dst, uint32_t off) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t *)dst, 16, off, 0, 0, 0);
+}
+
+// The 32x32 prefill item for bf16 caches with its tiles loaded straight
+// into LDS: two buffers of a K tile and a V tile (64 keys x HD, row-major,
+// 16-byte chunks swizzled), the next tile's loads issued at the top of a
+// tile and landed by the barrier that ends it, so there is no register
+// staging and one barrier per tile.  The scores read K chunks as in
+// prefill_item32; the P.V product reads its V^T operand with the transposing
+// LDS read (ds_read_b64_tr_b16: within 16 lanes, lane i receives element
+// i % 4 of the 8-byte pieces that lanes 4 e + i / 4 point at, e = 0..3), so
+// each lane gets one dim of four keys and V needs no transpose on its way in.
+// Chunk swizzles: K chunk c of key t sits at position c ^ (t & 7), so the 8
+// rows of one pass of a 16-byte read start in 8 bank groups; V chunk c of
+// key t at c ^ 2 (t & 3), so the 4 keys x 2 chunks of a transposed read's 16
+// lanes fall in 8 bank groups.
+template <int HD, int G, int NW>
+__device__ __forceinline__ void prefill_item32_dma(const uint16_t *__restrict__ qkv, int nq, int nkv, const KV kv,
+                                                   const DevMeta md, int tile, int kh, uint16_t *__restrict__ out,
+                                                   uint8_t *buf0, uint8_t *buf1) {
+  constexpr int BQ = NW * 32 / G;  // query positions per item
+  static_assert(NW * 32 == G * BQ, "rows per item");
+  constexpr int KT = 64;                 // keys per tile
+  constexpr int ROW = HD * 2;            // bytes per key row
+  constexpr int CPR = ROW / 16;          // 16-byte chunks per row
+  constexpr int TILE = KT * ROW;         // bytes of the K (and of the V) tile
+  constexpr int KPI = 1024 / ROW;        // keys per 1 KiB load instruction
+  constexpr int NI = KT / (KPI * NW);    // load instructions per wave per tile, each of K and V
+  static_assert(NI * KPI * NW == KT && KPI <= kPageSize, "whole load rounds within pages");
+  constexpr int NKS = HD / 16;  // k-steps of the QK^T product
+  constexpr int NOB = HD / 32;  // 32-dim output blocks
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int cols = (nq + 2 * nkv) * HD;
+  const int seq = __builtin_amdgcn_readfirstlane(md.tile_seq[tile]);
+  const int qb = __builtin_amdgcn_readfirstlane(md.tile_qb[tile]);
+  const int c = __builtin_amdgcn_readfirstlane(md.seq_ctx[seq]);
+  const int n = __builtin_amdgcn_readfirstlane(md.seq_len[seq]);
+  const int row0 = __builtin_amdgcn_readfirstlane(md.seq_row[seq]);
+  const int q_lo = qb * BQ;
+  const int q_hi = min(n, q_lo + BQ);
+  const int kend = c + q_hi;
+  const int klen = c + n;
+  const int32_t *bt = kv.bt + (size_t)seq * kv.max_pages;
+  const int npages = (klen + kPageSize - 1) / kPageSize;
+  const float qscale = kLog2e / sqrtf((float)HD);
+  const int lq = lane & 31;  // query column of this lane
+  const int lh = lane >> 5;  // k half
+
+  // the wave's 32 rows: HPB heads x RPH positions
+  constexpr int RPH = BQ < 32 ? BQ : 32, HPB = 32 / RPH, HG = G / HPB;
+  static_assert(HPB * RPH == 32 && HG * HPB == G, "row block shape");
+  const int hb = wave % HG, sub = wave / HG;
+  const int hrow = hb * HPB + lq / RPH;
+  const int qrel = q_lo + sub * RPH + lq % RPH;
+  const bool qok = qrel < q_hi;
+  u32x4_t qreg[NKS];
+  {
+    const uint16_t *src = qkv + (size_t)(row0 + qrel) * cols + (kh * G + hrow) * HD + lh * 8;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) qreg[ks] = qok ? ld_u32x4(src + ks * 16) : u32x4_t{0, 0, 0, 0};
+  }
+  f32x16_t oacc[NOB];
+#pragma unroll
+  for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) oacc[ob][i] = 0.f;
+  float mrun = kNegInf, lrun = 0.f;
+
+  typedef int i32x4_t __attribute__((ext_vector_type(4)));
+  constexpr int PPT = KT / kPageSize;
+  static_assert(PPT == 4, "tile = 4 pages");
+  typedef const __attribute__((address_space(4))) int32_t *bt_ptr_t;
+  const bt_ptr_t btc = (bt_ptr_t)bt;
+  auto bt_tile = [&](int t) -> i32x4_t {  // pages past the sequence repeat its last id (empty ranges below)
+    const int p0 = t * PPT;
+    i32x4_t r;
+#pragma unroll
+    for (int j = 0; j < PPT; ++j) r[j] = btc[min(p0 + j, npages - 1)];
+    return r;
+  };
+  constexpr uint32_t kPageHeadBytes = kPageSize * ROW;
+  const uint32_t page_bytes = (uint32_t)nkv * kPageHeadBytes;
+  const uint8_t *const kbase = reinterpret_cast<const uint8_t *>(kv.k) + (size_t)kh * kPageHeadBytes;
+  const uint8_t *const vbase = reinterpret_cast<const uint8_t *>(kv.v) + (size_t)kh * kPageHeadBytes;
+  // page j of a tile as a buffer range over its keys below klen (empty for
+  // an id outside the pool): loads past it land as zeros, without traffic
+  auto page_rsrc = [&](const uint8_t *base, const i32x4_t &btv, int j, int first_key) -> buf_rsrc_t {
+    const int phys = j == 0 ? btv[0] : j == 1 ? btv[1] : j == 2 ? btv[2] : btv[3];
+    const int rem = klen - first_key;
+    const bool live = (unsigned)phys < (unsigned)kv.num_pages && rem > 0;
+    const int range = __builtin_amdgcn_readfirstlane(live ? min(rem, kPageSize) * ROW : 0);
+    return make_rsrc(base + (uint64_t)(uint32_t)(live ? phys : 0) * page_bytes, range);
+  };
+  // load instruction i of wave w fills keys KPI (i NW + w) .. + KPI - 1 of a
+  // tile; lane l writes chunk position l % CPR of key KPI (i NW + w) + l / CPR
+  uint32_t koff[NI], voff[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int key = KPI * (i * NW + wave) + lane / CPR;  // within the tile
+    const int pos = lane % CPR;
+    koff[i] = (uint32_t)((key % kPageSize) * ROW + 16 * (pos ^ (key & 7)));
+    voff[i] = (uint32_t)((key % kPageSize) * ROW + 16 * (pos ^ (2 * (key & 3))));
+  }
+  auto dma = [&](int t, const i32x4_t &btv, uint8_t *buf) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int key0 = KPI * (i * NW + wave);
+      const int j = key0 / kPageSize;  // wave-uniform
+      const int first = t * KT + j * kPageSize;
+      lds_dma16(page_rsrc(kbase, btv, j, first), buf + key0 * ROW, koff[i]);
+      lds_dma16(page_rsrc(vbase, btv, j, first), buf + TILE + key0 * ROW, voff[i]);
+    }
+  };
+
+  // K operand of the scores: key kb 32 + lq, chunk 2 ks + lh at position
+  // (2 ks + lh) ^ (lq & 7) (bit 3 of the chunk, ks >> 2, is untouched)
+  int kaddr[4];
+#pragma unroll
+  for (int k4 = 0; k4 < 4; ++k4) kaddr[k4] = lq * ROW + 16 * ((2 * k4 + lh) ^ (lq & 7));
+  // V^T operand, the transposed read: lane 16 g + 4 e + q points at key
+  // kb 32 + 16 jj + 8 h + 4 (g / 2) + e, dims ob 32 + 16 (g & 1) + 4 q .. + 3,
+  // i.e. chunk 4 ob + 2 (g & 1) + q / 2 (half q & 1) at position
+  // chunk ^ 2 e; the lane part depends on ob & 1 only
+  const int tg = lane >> 4, te = (lane >> 2) & 3, tq = lane & 3;
+  int vaddr[2];
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+    vaddr[b] = (4 * (tg >> 1) + te) * ROW + 16 * ((4 * b + 2 * (tg & 1) + (tq >> 1)) ^ (2 * te)) + 8 * (tq & 1);
+  typedef short v4s_t __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
+  auto vt_read = [&](const uint8_t *vt, int ob, int kb, int jj, int h) -> u32x2_t {
+    const uint8_t *p = vt + vaddr[ob & 1] + (kb * 32 + 16 * jj + 8 * h) * ROW + 128 * (ob >> 1);
+    return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t *)p));
+  };
+
+  const int min_qpos = c + q_lo;
+  const int qpos = c + qrel;
+  const int ntiles = (kend + KT - 1) / KT;
+  dma(0, bt_tile(0), buf0);
+  i32x4_t bt_next = bt_tile(1);
+  __syncthreads();
+  for (int t = 0; t < ntiles; ++t) {
+    const int k0 = t * KT;
+    uint8_t *const cur = (t & 1) ? buf1 : buf0;
+    if (t + 1 < ntiles) {  // lands by the barrier that ends this tile
+      dma(t + 1, bt_next, (t & 1) ? buf0 : buf1);
+      bt_next = bt_tile(t + 2);
+    }
+    // S^T: two 32-key blocks, lane value i at key 32 kb + 8 (i / 4) + 4 lh + i % 4
+    f32x16_t sc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const u32x4_t a = *reinterpret_cast<const u32x4_t *>(cur + kaddr[ks & 3] + 128 * (ks >> 2) + kb * 32 * ROW);
+        sc[kb] = mfma32x32x16(a, qreg[ks], sc[kb]);
+      }
+    if (k0 + KT - 1 > min_qpos) {  // causal mask on the diagonal tiles
+      const int d = qpos - k0 - 4 * lh;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sc[kb][i] = kb * 32 + 8 * (i >> 2) + (i & 3) > d ? kNegInf : sc[kb][i];
+    }
+    float mraw = kNegInf;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mraw = fmaxf(mraw, sc[kb][i]);
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mraw), __float_as_uint(mraw), false, false);
+      mraw = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+    }
+    // lazy running max and bf16 normaliser, as in prefill_item32
+    const float ms = mraw * qscale;
+    const bool bump = ms > mrun + kPrefillSlack;
+    const float mx = bump ? ms : mrun;
+    const float alpha = bump ? fast_exp2(mrun - mx) : 1.0f;
+    const float neg = mx != kNegInf ? -mx : 0.f;
+    float l = lrun * alpha;
+    uint32_t pk[2][8];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int pr = 0; pr < 8; ++pr) {
+        const float p0 = fast_exp2(fmaf(sc[kb][2 * pr], qscale, neg));
+        const float p1 = fast_exp2(fmaf(sc[kb][2 * pr + 1], qscale, neg));
+        pk[kb][pr] = bf16_pair_rne(p0, p1);
+        l = dot2_bf16(pk[kb][pr], 0x3F803F80u, l);
+      }
+    const bool rescale = __builtin_amdgcn_ballot_w64(bump && mrun != kNegInf) != 0;
+    lrun = l;
+    mrun = mx;
+    if (__builtin_expect(rescale, 0)) {
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) oacc[ob] = oacc[ob] * alpha;
+    }
+    // O^T += V^T P^T: k-step j takes keys 16 (j % 2) + {0..3, 8..11} + 4 lh of key block j / 2
+    const uint8_t *const vt = cur + TILE;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) {
+      f32x16_t acc = oacc[ob];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int kb = j >> 1, jj = j & 1;
+        const u32x2_t a0 = vt_read(vt, ob, kb, jj, 0), a1 = vt_read(vt, ob, kb, jj, 1);
+        const u32x4_t a = {a0[0], a0[1], a1[0], a1[1]};
+        const u32x4_t b = {pk[kb][4 * jj], pk[kb][4 * jj + 1], pk[kb][4 * jj + 2], pk[kb][4 * jj + 3]};
+        acc = mfma32x32x16(a, b, acc);
+      }
+      oacc[ob] = acc;
+    }
+    __syncthreads();
+  }
+  float l = lrun;
+  l += shfl_xor_f32(l, 32);
+  if (qok) {
+    const float inv = 1.0f / l;
+    uint16_t *dst = out + (size_t)(row0 + qrel) * nq * HD + (kh * G + hrow) * HD + 4 * lh;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const u32x2_t w = {pack_bf16x2(oacc[ob][4 * g] * inv, oacc[ob][4 * g + 1] * inv),
+                           pack_bf16x2(oacc[ob][4 * g + 2] * inv, oacc[ob][4 * g + 3] * inv)};
+        *reinterpret_cast<u32x2_t *>(dst + ob * 32 + 8 * g) = w;
+      }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // kernels
 // ---------------------------------------------------------------------------
@@ -1426,14 +1666,22 @@ template <int HD>
 struct PrefillLds {
   static constexpr int K_BYTES = 64 * (HD + 8) * 2;  // K tile, row-major
   static constexpr int VT_BYTES = HD * (64 + 4) * 2;  // V^T tile
+  static constexpr int DMA_BYTES = 2 * 2 * 64 * HD * 2;  // bf16 caches: two buffers of a K and a V tile
 };
 
 template <int HD, int G, bool F8>
 __global__ __launch_bounds__(64 * kPrefillWaves, 2) void k_prefill(const uint16_t *qkv, int nq, int nkv, KV kv,
                                                                       DevMeta md, uint16_t *out) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds[(PrefillLds<HD>::K_BYTES + PrefillLds<HD>::VT_BYTES) / 2];
-  prefill_item32<HD, G, kPrefillWaves, F8>(qkv, nq, nkv, kv, md, blockIdx.x / nkv, blockIdx.x % nkv, out, lds,
-                                           lds + PrefillLds<HD>::K_BYTES / 2);
+  constexpr int LB = F8 ? PrefillLds<HD>::K_BYTES + PrefillLds<HD>::VT_BYTES : PrefillLds<HD>::DMA_BYTES;
+  __shared__ __attribute__((aligned(16))) uint16_t lds[LB / 2];
+  const int item = blockIdx.x / nkv, kh = blockIdx.x % nkv;
+  if constexpr (F8) {
+    prefill_item32<HD, G, kPrefillWaves, F8>(qkv, nq, nkv, kv, md, item, kh, out, lds, lds + PrefillLds<HD>::K_BYTES / 2);
+  } else {
+    uint8_t *const b0 = reinterpret_cast<uint8_t *>(lds);
+    prefill_item32_dma<HD, G, kPrefillWaves>(qkv, nq, nkv, kv, md, item, kh, out, b0,
+                                             b0 + PrefillLds<HD>::DMA_BYTES / 2);
+  }
 }
 
 // One grid for a mixed step: items [0, n_tiles) are prefill tiles (longest
@@ -1455,14 +1703,19 @@ __device__ __forceinline__ void mixed_slot(int b, int n_prefill, int s, int &pf,
 template <int HD, int G, bool F8>
 __global__ __launch_bounds__(256, 2) void k_mixed(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md, uint16_t *out,
                                                float *part_o, float *part_ml, int stride) {
-  constexpr int PB = PrefillLds<HD>::K_BYTES + PrefillLds<HD>::VT_BYTES, DB = DecodeTraits<HD, G, 4>::LDS_BYTES;
+  constexpr int PB = F8 ? PrefillLds<HD>::K_BYTES + PrefillLds<HD>::VT_BYTES : PrefillLds<HD>::DMA_BYTES;
+  constexpr int DB = DecodeTraits<HD, G, 4>::LDS_BYTES;
   __shared__ __attribute__((aligned(16))) uint16_t lds[(PB > DB ? PB : DB) / 2];
   int pf, du;
   mixed_slot(blockIdx.x, md.n_tiles * nkv, stride, pf, du);
-  if (pf >= 0)
-    prefill_item32<HD, G, 4, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, lds,
-                                 lds + PrefillLds<HD>::K_BYTES / 2);
-  else
+  if (pf >= 0) {
+    if constexpr (F8)
+      prefill_item32<HD, G, 4, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, lds,
+                                   lds + PrefillLds<HD>::K_BYTES / 2);
+    else
+      prefill_item32_dma<HD, G, 4>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, reinterpret_cast<uint8_t *>(lds),
+                                   reinterpret_cast<uint8_t *>(lds) + PrefillLds<HD>::DMA_BYTES / 2);
+  } else
     decode_item<HD, G, 4, F8>(qkv, nq, nkv, kv, md, du, out, part_o, part_ml, reinterpret_cast<float *>(lds));
 }
 
@@ -1473,14 +1726,18 @@ __global__ __launch_bounds__(256, 2) void k_mixed_mfma(const uint16_t *qkv, int 
                                                     uint16_t *out, float *part_o, float *part_ml, int stride) {
   constexpr int MS = 2;                           // ring depth of decode items in the mixed launch
   constexpr int SLOT = MdecTraits<HD>::SLOT;      // bf16-sized slots: prefill tiles stage bf16
-  static_assert(PrefillLds<HD>::K_BYTES <= 4 * SLOT && PrefillLds<HD>::VT_BYTES <= 4 * SLOT, "LDS");
+  static_assert(PrefillLds<HD>::K_BYTES <= 4 * SLOT && PrefillLds<HD>::VT_BYTES <= 4 * SLOT &&
+                    PrefillLds<HD>::DMA_BYTES / 2 <= 4 * SLOT, "LDS");
   EB_MDEC_LDS(4 * SLOT, MS)
   int pf, du;
   mixed_slot(blockIdx.x, md.n_tiles * nkv, stride, pf, du);
-  if (pf >= 0)
-    prefill_item32<HD, G, 4, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, reinterpret_cast<uint16_t *>(l0),
-                                 reinterpret_cast<uint16_t *>(l1));
-  else
+  if (pf >= 0) {
+    if constexpr (F8)
+      prefill_item32<HD, G, 4, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, reinterpret_cast<uint16_t *>(l0),
+                                   reinterpret_cast<uint16_t *>(l1));
+    else  // one tile buffer in each of the first two page-slot arrays
+      prefill_item32_dma<HD, G, 4>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, l0, l1);
+  } else
     decode_item_mfma<HD, G, 4, MS, F8, SLOT>(qkv, nq, nkv, kv, md, du, out, part_o, part_ml, l0, l1, l2, l3);
 }
 #undef EB_MDEC_LDS
