@@ -1494,14 +1494,14 @@ __device__ __forceinline__ void prefill_item32_dma(const uint16_t *__restrict__ 
     koff[i] = (uint32_t)((key % kPageSize) * ROW + 16 * (pos ^ (key & 7)));
     voff[i] = (uint32_t)((key % kPageSize) * ROW + 16 * (pos ^ (2 * (key & 3))));
   }
-  auto dma = [&](int t, const i32x4_t &btv, uint8_t *buf) {
+  // the K (or V) tile of tile t into dst
+  auto dma = [&](int t, const i32x4_t &btv, uint8_t *dst, bool is_v) {
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int key0 = KPI * (i * NW + wave);
       const int j = key0 / kPageSize;  // wave-uniform
       const int first = t * KT + j * kPageSize;
-      lds_dma16(page_rsrc(kbase, btv, j, first), buf + key0 * ROW, koff[i]);
-      lds_dma16(page_rsrc(vbase, btv, j, first), buf + TILE + key0 * ROW, voff[i]);
+      lds_dma16(page_rsrc(is_v ? vbase : kbase, btv, j, first), dst + key0 * ROW, is_v ? voff[i] : koff[i]);
     }
   };
 
@@ -1529,29 +1529,47 @@ __device__ __forceinline__ void prefill_item32_dma(const uint16_t *__restrict__ 
   const int min_qpos = c + q_lo;
   const int qpos = c + qrel;
   const int ntiles = (kend + KT - 1) / KT;
-  dma(0, bt_tile(0), buf0);
-  i32x4_t bt_next = bt_tile(1);
-  __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
-    const int k0 = t * KT;
-    uint8_t *const cur = (t & 1) ? buf1 : buf0;
-    if (t + 1 < ntiles) {  // lands by the barrier that ends this tile
-      dma(t + 1, bt_next, (t & 1) ? buf0 : buf1);
-      bt_next = bt_tile(t + 2);
-    }
-    // S^T: two 32-key blocks, lane value i at key 32 kb + 8 (i / 4) + 4 lh + i % 4
-    f32x16_t sc[2];
+  // S^T of the K tile at kt: two 32-key blocks, lane value i at key
+  // 32 kb + 8 (i / 4) + 4 lh + i % 4
+  auto scores = [&](const uint8_t *kt, f32x16_t (&s)[2]) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) sc[kb][i] = 0.f;
+      for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
 #pragma unroll
     for (int ks = 0; ks < NKS; ++ks)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const u32x4_t a = *reinterpret_cast<const u32x4_t *>(cur + kaddr[ks & 3] + 128 * (ks >> 2) + kb * 32 * ROW);
-        sc[kb] = mfma32x32x16(a, qreg[ks], sc[kb]);
+        const u32x4_t a = *reinterpret_cast<const u32x4_t *>(kt + kaddr[ks & 3] + 128 * (ks >> 2) + kb * 32 * ROW);
+        s[kb] = mfma32x32x16(a, qreg[ks], s[kb]);
       }
+  };
+  // Buffer b holds K tile and V tile of tiles b, b + 2, ...  K goes two tiles
+  // ahead and V one, so during tile t the scores of tile t + 1 (K landed by
+  // the barrier that ended tile t - 1) are formed while tile t's softmax
+  // runs: the two are independent and the matrix products overlap the
+  // exponentials.  One barrier per tile lands the loads issued at its top
+  // (K of t + 2, V of t + 1) and retires every read of the buffers they
+  // refill.
+  f32x16_t sc[2];
+  i32x4_t bt1 = bt_tile(1), bt2 = bt_tile(2);
+  dma(0, bt_tile(0), buf0, false);
+  dma(0, bt_tile(0), buf0 + TILE, true);
+  if (ntiles > 1) dma(1, bt1, buf1, false);
+  __syncthreads();
+  scores(buf0, sc);
+  __syncthreads();  // every wave past the scores of tile 0 before K of tile 2 refills buffer 0
+  auto step = [&](int t, auto lastconst) {
+    constexpr bool LAST = decltype(lastconst)::value;
+    uint8_t *const cur = (t & 1) ? buf1 : buf0, *const nxt = (t & 1) ? buf0 : buf1;
+    const int k0 = t * KT;
+    f32x16_t scn[2];
+    if constexpr (!LAST) {
+      if (t + 2 < ntiles) dma(t + 2, bt2, cur, false);  // K of tile t was read by its scores before the last barrier
+      dma(t + 1, bt1, nxt + TILE, true);                // V of tile t - 1 was read before the last barrier
+      bt1 = bt2;
+      bt2 = bt_tile(t + 3);
+    }
     if (k0 + KT - 1 > min_qpos) {  // causal mask on the diagonal tiles
       const int d = qpos - k0 - 4 * lh;
 #pragma unroll
@@ -1559,6 +1577,7 @@ __device__ __forceinline__ void prefill_item32_dma(const uint16_t *__restrict__ 
 #pragma unroll
         for (int i = 0; i < 16; ++i) sc[kb][i] = kb * 32 + 8 * (i >> 2) + (i & 3) > d ? kNegInf : sc[kb][i];
     }
+    if constexpr (!LAST) scores(nxt, scn);
     float mraw = kNegInf;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -1585,7 +1604,10 @@ __device__ __forceinline__ void prefill_item32_dma(const uint16_t *__restrict__ 
         pk[kb][pr] = bf16_pair_rne(p0, p1);
         l = dot2_bf16(pk[kb][pr], 0x3F803F80u, l);
       }
-    const bool rescale = __builtin_amdgcn_ballot_w64(bump && mrun != kNegInf) != 0;
+    // (the test on l, true for every finite sum, ties the branch below to
+    // the block above: decided earlier, it would split that block and keep
+    // the score products from running under the exponentials)
+    const bool rescale = __builtin_amdgcn_ballot_w64(bump && mrun != kNegInf && l >= 0.f) != 0;
     lrun = l;
     mrun = mx;
     if (__builtin_expect(rescale, 0)) {
@@ -1607,8 +1629,14 @@ __device__ __forceinline__ void prefill_item32_dma(const uint16_t *__restrict__ 
       }
       oacc[ob] = acc;
     }
-    __syncthreads();
-  }
+    if constexpr (!LAST) {
+      sc[0] = scn[0];
+      sc[1] = scn[1];
+      __syncthreads();
+    }
+  };
+  for (int t = 0; t + 1 < ntiles; ++t) step(t, std::false_type{});
+  step(ntiles - 1, std::true_type{});
   float l = lrun;
   l += shfl_xor_f32(l, 32);
   if (qok) {
