@@ -8,12 +8,12 @@ idle, then one prefill batch refills them while the other requests wait),
 linear iteration times, output lengths from a distribution with hazard h(t).
 MB runs chunked-prefill iterations of at most B rows, every decode request
 contributing one row (Sec. 3.5).  EB+ chooses EB or MB before every iteration
-with Eq. eb_plus_switch on online estimates.  The online controller of
-Alg. "Online Joint Adaptation of (k*, N*)" fits the hazard h(t) = p0 + eta t
-by weighted least squares over t in [1, t95] of a sliding window of output
-lengths (Sec. 3.4), solves Eq. theta_base, adds the IFR correction
-(Eq. delta_theta) with the previous batch size, clips, and sets
-N* (Eq. Nstar) and k* = floor(theta* N*).  A KV-aware gate defers a
+with Eq. eb_plus_switch on online estimates.  The online controller
+(Alg. "Online Joint Adaptation of (k*, N*)") keeps a window of completed
+requests, estimates the hazard h(t) = p0 + eta t from it by weighted least
+squares over t in [1, t95] (Sec. 3.4), and maps the estimates to a
+threshold (Eqs. theta_base and delta_theta), a batch size (Eq. Nstar) and
+k* = floor(theta* N*).  A KV-aware gate defers a
 decode -> prefill switch while fewer than f_KV of the cache blocks are free
 (App. "Runtime Refinement: KV-aware Feasibility Gate").
 """
@@ -117,48 +117,117 @@ class ControllerCfg:
     N_max: int = 8192
 
 
+@dataclasses.dataclass
+class LengthEstimates:
+    """What the controller knows of the workload: the linear hazard
+    h(t) = p0 + eta t of output lengths and the mean input length."""
+    p0: float
+    eta: float
+    mu_L: float
+
+
+class CompletionWindow:
+    """Input and output lengths of the most recently completed requests (a
+    bounded window) and the estimates taken from them (Sec. 3.4)."""
+
+    def __init__(self, size: int):
+        self._inputs: Deque[int] = deque(maxlen=size)
+        self._outputs: Deque[int] = deque(maxlen=size)
+
+    def add(self, L: int, O: int):
+        self._inputs.append(int(L))
+        self._outputs.append(int(O))
+
+    def __len__(self) -> int:
+        return len(self._outputs)
+
+    def mean_output(self) -> float:
+        return float(np.mean(self._outputs))
+
+    def estimates(self) -> LengthEstimates:
+        p0, eta = fit_linear_hazard(np.asarray(self._outputs))
+        # a hazard below zero or falling with t is outside the model's IFR /
+        # CFR family: clamp to the CFR boundary
+        return LengthEstimates(p0=max(p0, 1e-6), eta=max(eta, 0.0), mu_L=float(np.mean(self._inputs)))
+
+
+@dataclasses.dataclass
+class OperatingPoint:
+    """Threshold theta, batch size N and switch count k of EB(k, N)."""
+    theta0: float
+    theta: float
+    N: int
+    k: int
+
+
+def operating_point(costs: CM.StepCosts, est: LengthEstimates, N_prev: int, cfg: ControllerCfg) -> OperatingPoint:
+    """The operating point the estimates call for: the CFR threshold of
+    Eq. theta_base at the ratio p0 alpha_p / alpha_d, raised by the IFR
+    correction of Eq. delta_theta (taken at the batch size in use, N_prev),
+    kept within [theta_min, theta_max]; the largest batch Eq. Nstar allows at
+    that threshold under the KV capacity and risk level, within [1, N_max];
+    and k = floor(theta N)."""
+    th0 = CM.solve_theta0(est.p0 * costs.alpha_p / costs.alpha_d)
+    correction = CM.delta_theta(est.eta, est.p0, th0, costs.beta_d, N_prev, costs.alpha_d) if est.eta > 0 else 0.0
+    theta = min(cfg.theta_max, max(cfg.theta_min, th0 + correction))
+    N = int(min(cfg.N_max, max(1, CM.n_star(cfg.C, cfg.eps, theta, est.p0, est.mu_L))))
+    return OperatingPoint(theta0=th0, theta=theta, N=N, k=max(1, int(math.floor(theta * N))))
+
+
 class AdaptiveController:
-    """Alg. "Online Joint Adaptation of (k*, N*)": sliding windows of
-    completed requests' lengths, periodic re-estimation of (p0, eta, mu_L),
-    theta* = clip(theta_0 + Delta theta), N* from Eq. Nstar, k* =
-    floor(theta* N*)."""
+    """The online controller (Alg. "Online Joint Adaptation of (k*, N*)"):
+    a window of completions as the estimator, and the operating-point rule
+    above re-applied to its estimates every update_every completions once
+    the window holds at least min_window of them."""
 
     def __init__(self, costs: CM.StepCosts, cfg: ControllerCfg):
         self.c = costs
         self.cfg = cfg
-        self.WO: Deque[int] = deque(maxlen=cfg.window)
-        self.WL: Deque[int] = deque(maxlen=cfg.window)
-        self.j = 0
-        self.N = cfg.N_default
-        self.k = max(1, int(cfg.theta_default * cfg.N_default))
-        self.theta0 = cfg.theta_default
-        self.theta = cfg.theta_default
-        self.p0 = None
-        self.eta = 0.0
-        self.mu_L = None
+        self.window = CompletionWindow(cfg.window)
+        self.point = OperatingPoint(theta0=cfg.theta_default, theta=cfg.theta_default, N=cfg.N_default,
+                                    k=max(1, int(cfg.theta_default * cfg.N_default)))
+        self.est: Optional[LengthEstimates] = None
+        self._since_refresh = 0
         self.updates = 0
 
     def observe(self, L: int, O: int):
-        self.WO.append(int(O))
-        self.WL.append(int(L))
-        self.j += 1
-        if self.j >= self.cfg.update_every and len(self.WO) >= self.cfg.min_window:
-            self.update()
-            self.j = 0
+        """Record one completed request; refresh the operating point when due."""
+        self.window.add(L, O)
+        self._since_refresh += 1
+        if self._since_refresh >= self.cfg.update_every and len(self.window) >= self.cfg.min_window:
+            self.est = self.window.estimates()
+            self.point = operating_point(self.c, self.est, self.point.N, self.cfg)
+            self.updates += 1
+            self._since_refresh = 0
 
-    def update(self):
-        p0, eta = fit_linear_hazard(np.asarray(self.WO))
-        p0 = max(p0, 1e-6)
-        eta = max(eta, 0.0)
-        mu_L = float(np.mean(self.WL))
-        th0 = CM.solve_theta0(p0 * self.c.alpha_p / self.c.alpha_d)
-        dth = CM.delta_theta(eta, p0, th0, self.c.beta_d, self.N, self.c.alpha_d) if eta > 0 else 0.0
-        th = min(self.cfg.theta_max, max(self.cfg.theta_min, th0 + dth))
-        N = CM.n_star(self.cfg.C, self.cfg.eps, th, p0, mu_L)
-        N = int(min(self.cfg.N_max, max(1, N)))
-        self.p0, self.eta, self.mu_L, self.theta0, self.theta, self.N = p0, eta, mu_L, th0, th, N
-        self.k = max(1, int(math.floor(th * N)))
-        self.updates += 1
+    # the current operating point and estimates, as the simulator reads them
+    @property
+    def N(self) -> int:
+        return self.point.N
+
+    @property
+    def k(self) -> int:
+        return self.point.k
+
+    @property
+    def theta(self) -> float:
+        return self.point.theta
+
+    @property
+    def theta0(self) -> float:
+        return self.point.theta0
+
+    @property
+    def p0(self) -> Optional[float]:
+        return self.est.p0 if self.est else None
+
+    @property
+    def eta(self) -> float:
+        return self.est.eta if self.est else 0.0
+
+    @property
+    def mu_L(self) -> Optional[float]:
+        return self.est.mu_L if self.est else None
 
 
 # ----------------------------------------------------------------------------
@@ -341,7 +410,7 @@ class Simulator:
         total_blocks = cap // self.cfg.block
         used = int(np.ceil((self.pf[self.busy] + self.g[self.busy]) / self.cfg.block).sum())
         N, _ = self._limits()
-        mu_O = float(np.mean(self.ctrl.WO)) if (self.ctrl and len(self.ctrl.WO)) else float(np.mean(self.O[self.busy]))
+        mu_O = self.ctrl.window.mean_output() if (self.ctrl and len(self.ctrl.window)) else float(np.mean(self.O[self.busy]))
         f = CM.kv_gate_fraction(N, mu_O, self.cfg.block, total_blocks, self.cfg.s_kv, self.cfg.f0)
         return (total_blocks - used) >= f * total_blocks
 

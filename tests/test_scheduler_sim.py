@@ -134,3 +134,20 @@ def test_eb_plus_runs_the_better_discipline(mb_cost, expect):
     share_eb = ebp.eb_iterations / ebp.iterations
     assert (share_eb > 0.8) if expect == "eb" else (share_eb < 0.2)
     assert ebp.throughput >= 0.95 * max(eb.throughput, mb.throughput)
+
+
+def test_kv_gate_reads_the_controller_window():
+    # with the online controller on, the KV gate takes the mean output length
+    # from the controller's window of completions; the run completes, the
+    # controller refreshes, and the gate still lowers the memory peak
+    mu_O, mu_L = 200, 400
+    wl = S.Workload(S.fixed_inputs(mu_L), S.geometric_outputs(mu_O))
+    cap = 260_000
+    ctl = S.ControllerCfg(C=float(cap), window=1000, min_window=100, update_every=100, N_default=256, N_max=1024)
+    free = S.Simulator(COSTS, wl, S.SimCfg(N=256, policy="eb", adaptive=ctl, max_completions=2000), seed=1)
+    gated = S.Simulator(COSTS, wl, S.SimCfg(N=256, policy="eb", kv_capacity=cap, adaptive=ctl, max_completions=2000),
+                        seed=1)
+    rf, rg = free.run(), gated.run()
+    assert gated.ctrl.updates > 5 and gated.ctrl.window.mean_output() == pytest.approx(mu_O, rel=0.15)
+    assert min(rg.completed, rf.completed) >= 2000
+    assert rg.peak_kv_tokens <= rf.peak_kv_tokens
