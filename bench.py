@@ -276,7 +276,7 @@ def measure(B, h, step_fn, w, pool, batch, x, y, ws, steps, warmup, kv_scales=No
     return st["mean_ms"], stages, timed, st
 
 
-def sweep(args, dev, budgets=None, w=None):
+def sweep(args, dev, budgets=None, w=None, store=None):
     """Mixed step of the chosen layer (the 8B one by default) over decode
     shares 0, 0.1, .., 1 at several budgets (``budgets``, else --budgets)."""
     import numpy as np
@@ -298,7 +298,7 @@ def sweep(args, dev, budgets=None, w=None):
     pts = []
 
     def run(batch, mode):
-        pool, kvs = make_pool(gen, shape, batch, args.kv, device=dev, poison=False)
+        pool, kvs = make_pool(gen, shape, batch, args.kv, device=dev, poison=False, store=store)
         x = gen.make_x(shape, batch.num_tokens, device=dev)
         y = torch.empty_like(x)
         h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
@@ -338,7 +338,7 @@ def sweep(args, dev, budgets=None, w=None):
     big = max(budgets)
     mb = sorted([p for p in pts if p["budget"] == big and p["mode"] == "mixed"], key=lambda p: p["r"])
     r_arr = [p["r"] for p in mb]
-    K = [p["ms"] for p in mb]
+    K = [p["median_ms"] for p in mb]  # per share: the median step (one slow step does not bend the curve)
     Ka = [p["attention_ms"] for p in mb]
     rep = AN.sweep_report(r_arr, K)
     rep_attn = AN.sweep_report(r_arr, Ka)
@@ -686,7 +686,26 @@ def prefill_part(args, dev, w):
                                    "avg_launch_ms": round(a_ms, 5), "flops_per_launch": wk["attn_flops_prefill"]}}
 
 
-def sweep_part(args, dev, w, repeats=3):
+def sweep_store(shape, budgets, dec_ctx, kv, dev):
+    """One K and one V buffer sized for the largest pool of a sweep over
+    ``budgets``: every point lays its pool in them, so all points and repeats
+    read the same physical memory (separate allocations of a multi-GB pool
+    moved a point by up to 10 % between repeats)."""
+    import numpy as np
+    import torch
+
+    from paper_2606_00516_amd import inputs as gen
+    most = 0
+    for bud in budgets:
+        for i in range(11):
+            r = round(0.1 * i, 1)
+            rng = np.random.default_rng([gen.seeds()["batch"], int(round(r * 1000)), bud])
+            most = max(most, int(gen.pages_needed(gen.batch_mixed_budget(r, bud, rng, dec_ctx=dec_ctx)).sum()))
+    n = most * shape.n_kv_heads * shape.page_size * shape.head_dim * (1 if kv == "fp8" else 2)
+    return (torch.empty(n, dtype=torch.uint8, device=dev), torch.empty(n, dtype=torch.uint8, device=dev))
+
+
+def sweep_part(args, dev, w, repeats=5):
     """The 8B MB sweep at the 2048-token budget (decode ctx U[1024,8192],
     r = 0, 0.1, .., 1) ``repeats`` times, for K(r) and the spread of kappa,
     and once at budgets 512, 1024 and 4096 for the per-share linear fits
@@ -699,12 +718,14 @@ def sweep_part(args, dev, w, repeats=3):
     a = copy.copy(args)
     a.shape, a.ctx16, a.dec_ctx, a.kv = "l8b", False, None, "bf16"
     runs, pts_all = [], []
+    from paper_2606_00516_amd import inputs as gen
+    store = sweep_store(gen.L8B, [512, 1024, 2048, 4096], (1024, 8192), a.kv, dev)
     for _ in range(repeats):
-        out, pts = sweep(a, dev, budgets=[2048], w=w)
+        out, pts = sweep(a, dev, budgets=[2048], w=w, store=store)
         runs.append(out)
         pts_all += pts
         print(f"# sweep B=2048 kappa {out['fit']['kappa']:.4f}", file=sys.stderr, flush=True)
-    _, pts_other = sweep(a, dev, budgets=[512, 1024, 4096], w=w)
+    _, pts_other = sweep(a, dev, budgets=[512, 1024, 4096], w=w, store=store)
     r = runs[0]["r"]
     K = np.median(np.array([o["K_ms"] for o in runs]), axis=0)
     kappas = [o["fit"]["kappa"] for o in runs]

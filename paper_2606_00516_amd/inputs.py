@@ -440,15 +440,28 @@ def weight_arrays(w: dict) -> dict:
     return out
 
 
+def _pool_tensor(shape4, fill, dtype, device, store):
+    """A [pool, nkv, P, hd] tensor filled with ``fill``: fresh, or the leading
+    elements of the flat byte buffer ``store`` (so that a caller can keep one
+    allocation, and one physical placement, across many pools)."""
+    if store is None:
+        return torch.full(shape4, fill, dtype=dtype, device=device)
+    n = int(np.prod(shape4)) * torch.empty((), dtype=dtype).element_size()
+    if store.numel() < n or store.dtype != torch.uint8:
+        raise ValueError("pool storage too small")
+    return store[:n].view(dtype).view(shape4).fill_(fill)
+
+
 def make_kv_pool(shape: LayerShape, batch: Batch, seed: Optional[int] = None, device="cpu",
                  spare_pages: int = 0, poison: bool = True,
-                 max_pages_per_seq: Optional[int] = None) -> KVPool:
+                 max_pages_per_seq: Optional[int] = None, store=None) -> KVPool:
     """Paged bf16 K/V pool holding each request's prior context.
 
     Prior positions (< context_len) hold bf16 N(0, 1).  With ``poison`` every
     other slot (spare pages, the slots the step will append to, and slots past
     the end of each request) holds bf16 NaN, so any read outside the block
-    table or past a request's length shows up as NaN in the output.
+    table or past a request's length shows up as NaN in the output.  ``store``
+    (optional): two flat uint8 device buffers the K and V pools are laid in.
     """
     if seed is None:
         seed = seeds()["kv"]
@@ -456,8 +469,8 @@ def make_kv_pool(shape: LayerShape, batch: Batch, seed: Optional[int] = None, de
     nkv, P, hd = shape.n_kv_heads, shape.page_size, shape.head_dim
     g = _gen(device, seed)
     fill = float("nan") if poison else 0.0
-    kc = torch.full((pool, nkv, P, hd), fill, dtype=torch.bfloat16, device=device)
-    vc = torch.full((pool, nkv, P, hd), fill, dtype=torch.bfloat16, device=device)
+    kc = _pool_tensor((pool, nkv, P, hd), fill, torch.bfloat16, device, store[0] if store else None)
+    vc = _pool_tensor((pool, nkv, P, hd), fill, torch.bfloat16, device, store[1] if store else None)
     bt_t = torch.from_numpy(bt).to(device)
     for i in range(batch.num_seqs):
         c = int(batch.context_lens[i])
@@ -478,7 +491,7 @@ def make_kv_pool(shape: LayerShape, batch: Batch, seed: Optional[int] = None, de
 
 def make_kv_pool_codes(shape: LayerShape, batch: Batch, seed: Optional[int] = None, device="cpu",
                        spare_pages: int = 0, poison: bool = True,
-                       max_pages_per_seq: Optional[int] = None) -> KVPool:
+                       max_pages_per_seq: Optional[int] = None, store=None) -> KVPool:
     """Paged 8-bit K/V pool (uint8 E4M3 codes) holding each request's prior
     context: random bytes with a random sign bit, an exponent field in 4..9
     and a random 3-bit mantissa (code values 1/8 .. 7.5 in magnitude).  With
@@ -489,8 +502,8 @@ def make_kv_pool_codes(shape: LayerShape, batch: Batch, seed: Optional[int] = No
     nkv, P, hd = shape.n_kv_heads, shape.page_size, shape.head_dim
     g = _gen(device, seed)
     fill = 0x7F if poison else 0
-    kc = torch.full((pool, nkv, P, hd), fill, dtype=torch.uint8, device=device)
-    vc = torch.full((pool, nkv, P, hd), fill, dtype=torch.uint8, device=device)
+    kc = _pool_tensor((pool, nkv, P, hd), fill, torch.uint8, device, store[0] if store else None)
+    vc = _pool_tensor((pool, nkv, P, hd), fill, torch.uint8, device, store[1] if store else None)
     bt_t = torch.from_numpy(bt).to(device)
 
     def codes(n):
