@@ -33,6 +33,10 @@ def _bf(shape, seed, scale=1.0):
                                    # 256 x 256 tiles splitting K (few tiles): uneven splits, ragged M, N and F,
                                    # the 70B-shaped down projection
                                    (300, 1032, 2048), (256, 8192, 28672),
+                                   # odd counts of 64-wide K tiles per block, and blocks of one or two K
+                                   # tiles: one K range, and split K with uneven splits
+                                   (512, 1032, 576), (768, 2048, 192), (272, 1024, 1344), (512, 1024, 128),
+                                   (512, 1024, 64),
                                    # decode-sized row counts: one K stage, ragged N and F, split K, the
                                    # 8B-shaped down projection
                                    (63, 4104, 128), (17, 1032, 384), (1, 8200, 1152), (64, 4096, 14336)])
