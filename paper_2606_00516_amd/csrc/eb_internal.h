@@ -34,7 +34,7 @@ inline int prefill_bq(int group, bool mixed_launch) {
 // instead of one phase after the other.  Block b runs prefill item b / s
 // when b % s == 0 and b / s < P, otherwise decode unit b - min(P, b / s + 1).
 #ifndef EB_MIX_SPAN
-#define EB_MIX_SPAN 70
+#define EB_MIX_SPAN 80
 #endif
 constexpr int kMixedPrefillSpanPct = EB_MIX_SPAN;
 inline int mixed_prefill_stride(long P, long D) {
