@@ -1656,11 +1656,25 @@ __device__ __forceinline__ void prefill_item32_dma(const uint16_t *__restrict__ 
 // ---------------------------------------------------------------------------
 // kernels
 // ---------------------------------------------------------------------------
+// Work item of block b in a launch of n blocks (decode units, or the mixed
+// launch's interleaved items).  Consecutive decode units are the kv heads of
+// one split, which read the same pages (each page holds every
+// head's keys of its 16 positions), and blocks are dealt round-robin to the
+// 8 XCDs; so within each run of 64 blocks, block b takes item
+// 8 (b % 8) + (b % 64) / 8 of the run, which puts each 8 consecutive items
+// on one XCD, whose L2 and address translation then serve a page for all
+// its heads.  The order of the runs is kept; a last run shorter than 64
+// keeps the identity.
+__device__ __forceinline__ int xcd_grouped_unit(int b, int n) {
+  if (b >= (n & ~63)) return b;
+  return (b & ~63) + ((b & 7) << 3) + ((b & 63) >> 3);
+}
+
 template <int HD, int G, bool F8>
 __global__ __launch_bounds__(256, 2) void k_decode(const uint16_t *qkv, int nq, int nkv, KV kv, DevMeta md,
                                                    uint16_t *out, float *part_o, float *part_ml) {
   __shared__ float lds[DecodeTraits<HD, G, 4>::LDS_BYTES / 4];
-  decode_item<HD, G, 4, F8>(qkv, nq, nkv, kv, md, blockIdx.x, out, part_o, part_ml, lds);
+  decode_item<HD, G, 4, F8>(qkv, nq, nkv, kv, md, xcd_grouped_unit(blockIdx.x, gridDim.x), out, part_o, part_ml, lds);
 }
 
 // The matrix-core decode keeps its page slots in separate LDS arrays, so the
@@ -1683,8 +1697,8 @@ __global__ __launch_bounds__(64 * kDecWaves, F8 ? 4 : 1) void k_decode_mfma(cons
   constexpr int NS = F8 ? kDecSlotsF8 : kDecSlots;
   constexpr int SLOT = MdecTraits<HD, F8>::SLOT;
   EB_MDEC_LDS(kDecWaves * SLOT, NS)
-  decode_item_mfma<HD, G, kDecWaves, NS, F8, SLOT>(qkv, nq, nkv, kv, md, blockIdx.x, out, part_o, part_ml, l0, l1,
-                                                   l2, l3);
+  decode_item_mfma<HD, G, kDecWaves, NS, F8, SLOT>(qkv, nq, nkv, kv, md, xcd_grouped_unit(blockIdx.x, gridDim.x), out,
+                                                   part_o, part_ml, l0, l1, l2, l3);
 }
 
 // Prefill-only launch: 4 wavefronts per 128-row item, 32 rows per wave on
@@ -1735,7 +1749,7 @@ __global__ __launch_bounds__(256, 2) void k_mixed(const uint16_t *qkv, int nq, i
   constexpr int DB = DecodeTraits<HD, G, 4>::LDS_BYTES;
   __shared__ __attribute__((aligned(16))) uint16_t lds[(PB > DB ? PB : DB) / 2];
   int pf, du;
-  mixed_slot(blockIdx.x, md.n_tiles * nkv, stride, pf, du);
+  mixed_slot(xcd_grouped_unit(blockIdx.x, gridDim.x), md.n_tiles * nkv, stride, pf, du);
   if (pf >= 0) {
     if constexpr (F8)
       prefill_item32<HD, G, 4, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, lds,
@@ -1758,7 +1772,7 @@ __global__ __launch_bounds__(256, 2) void k_mixed_mfma(const uint16_t *qkv, int 
                     PrefillLds<HD>::DMA_BYTES / 2 <= 4 * SLOT, "LDS");
   EB_MDEC_LDS(4 * SLOT, MS)
   int pf, du;
-  mixed_slot(blockIdx.x, md.n_tiles * nkv, stride, pf, du);
+  mixed_slot(xcd_grouped_unit(blockIdx.x, gridDim.x), md.n_tiles * nkv, stride, pf, du);
   if (pf >= 0) {
     if constexpr (F8)
       prefill_item32<HD, G, 4, F8>(qkv, nq, nkv, kv, md, pf / nkv, pf % nkv, out, reinterpret_cast<uint16_t *>(l0),
