@@ -803,18 +803,20 @@ constexpr int kSkinnyMaxRows = 256;
 // The split-K sum of a residual GEMM and the RMSNorm of its rows in one
 // pass: h = bf16(sum_s part[s] + res) is stored (the splits summed in order,
 // as the split-K epilogue does), then out = bf16(h * inv * g) with inv from
-// the rounded h.  One block per row: thread t takes the 8-column chunks
-// t, t + 256, .. (rows up to 256 * 4 chunks wide), issues the loads of eight
-// splits before adding them, and the sum of squares is reduced across the
-// block.
-constexpr int kFuseMaxChunks = 4;
-__global__ __launch_bounds__(256) void k_splitk_residual_rmsnorm(const float *__restrict__ part, int splits,
+// the rounded h.  One block of kFuseThreads per row (a decode batch has few
+// rows, so the row's loads are spread over many waves): thread t takes the
+// 8-column chunks t, t + kFuseThreads, .. (rows up to kFuseThreads *
+// kFuseMaxChunks chunks wide), issues the loads of eight splits before
+// adding them, and the sum of squares is reduced across the block.
+constexpr int kFuseThreads = 512;
+constexpr int kFuseMaxChunks = 2;
+__global__ __launch_bounds__(kFuseThreads) void k_splitk_residual_rmsnorm(const float *__restrict__ part, int splits,
                                                                  const uint16_t *__restrict__ res,
                                                                  uint16_t *__restrict__ h,
                                                                  const uint16_t *__restrict__ g,
                                                                  uint16_t *__restrict__ out, int M, int N,
                                                                  float eps) {
-  __shared__ float red[4];
+  __shared__ float red[kFuseThreads / 64];
   const int row = blockIdx.x;
   const int tid = threadIdx.x;
   const int nch = N >> 3;
@@ -822,7 +824,7 @@ __global__ __launch_bounds__(256) void k_splitk_residual_rmsnorm(const float *__
   float ss = 0.f;
 #pragma unroll
   for (int j = 0; j < kFuseMaxChunks; ++j) {
-    const int c = tid + 256 * j;
+    const int c = tid + kFuseThreads * j;
     v[j] = u32x4_t{0u, 0u, 0u, 0u};
     if (c < nch) {
       f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
@@ -864,11 +866,13 @@ __global__ __launch_bounds__(256) void k_splitk_residual_rmsnorm(const float *__
   ss = wave_sum(ss);
   if ((tid & 63) == 0) red[tid >> 6] = ss;
   __syncthreads();
-  const float tot = red[0] + red[1] + red[2] + red[3];
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < kFuseThreads / 64; ++w) tot += red[w];
   const float inv = 1.0f / sqrtf(tot / (float)N + eps);
 #pragma unroll
   for (int j = 0; j < kFuseMaxChunks; ++j) {
-    const int c = tid + 256 * j;
+    const int c = tid + kFuseThreads * j;
     if (c < nch) {
       const u32x4_t gv = ld_u32x4(g + c * 8);
       u32x4_t o;
@@ -896,8 +900,8 @@ static hipError_t launch_splitk_epilogue(const float *part, int splits, uint16_t
 
 static hipError_t finish_splitk(const float *part, int splits, uint16_t *out, const uint16_t *res, int M, int N,
                                 int epi, NormFuse *nf, hipStream_t st) {
-  if (nf && nf->gamma && epi == EPI_RESIDUAL && N % 8 == 0 && N / 8 <= 256 * kFuseMaxChunks) {
-    hipLaunchKernelGGL(k_splitk_residual_rmsnorm, dim3(M), dim3(256), 0, st, part, splits, res, out, nf->gamma,
+  if (nf && nf->gamma && epi == EPI_RESIDUAL && N % 8 == 0 && N / 8 <= kFuseThreads * kFuseMaxChunks) {
+    hipLaunchKernelGGL(k_splitk_residual_rmsnorm, dim3(M), dim3(kFuseThreads), 0, st, part, splits, res, out, nf->gamma,
                        nf->out, M, N, nf->eps);
     nf->done = true;
     return hipGetLastError();
