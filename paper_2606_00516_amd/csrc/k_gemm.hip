@@ -264,28 +264,29 @@ __global__ __launch_bounds__(256) void k_gemm_splitk_epilogue(const float *__res
                                                               uint16_t *__restrict__ out,
                                                               const uint16_t *__restrict__ res, int M, int N,
                                                               int epi) {
-  // four consecutive output columns per thread and step (N and F are
-  // multiples of 4, and a SiLU group of 32 never splits a group of 4), the
+  // two consecutive output columns per thread and step (N and F are even,
+  // and a SiLU group of 32 never splits a pair; two rather than four columns
+  // so that a decode batch's few rows still give the chip many waves), the
   // loads of up to eight splits issued before they are added; each element
   // sums its splits in order, then adds the residual
+  typedef float f2_t __attribute__((ext_vector_type(2)));
   const int ncols = logical_cols(N, epi);
   const int outc = epi == EPI_SILU_MUL ? N / 2 : N;
-  const long total4 = (long)M * (outc / 4);
+  const long total2 = (long)M * (outc / 2);
   const size_t stride = (size_t)M * ncols;
-  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total4; idx += (long)gridDim.x * blockDim.x) {
-    const int m = (int)(idx / (outc / 4)), n = 4 * (int)(idx - (long)m * (outc / 4));
+  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < total2; idx += (long)gridDim.x * blockDim.x) {
+    const int m = (int)(idx / (outc / 2)), n = 2 * (int)(idx - (long)m * (outc / 2));
     const bool silu = epi == EPI_SILU_MUL;
     const int col = silu ? (n / 32) * 64 + (n & 31) : n;
     const float *p0 = part + (size_t)m * ncols + col;
-    f32x4_t x = {0.f, 0.f, 0.f, 0.f}, u = {0.f, 0.f, 0.f, 0.f};
+    f2_t x = {0.f, 0.f}, u = {0.f, 0.f};
     for (int s0 = 0; s0 < splits; s0 += 8) {
-      f32x4_t a[8], b[8];
+      f2_t a[8], b[8];
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         const bool ok = s0 + q < splits;
-        a[q] = ok ? *reinterpret_cast<const f32x4_t *>(p0 + (s0 + q) * stride) : f32x4_t{0.f, 0.f, 0.f, 0.f};
-        b[q] = ok && silu ? *reinterpret_cast<const f32x4_t *>(p0 + (s0 + q) * stride + 32)
-                          : f32x4_t{0.f, 0.f, 0.f, 0.f};
+        a[q] = ok ? *reinterpret_cast<const f2_t *>(p0 + (s0 + q) * stride) : f2_t{0.f, 0.f};
+        b[q] = ok && silu ? *reinterpret_cast<const f2_t *>(p0 + (s0 + q) * stride + 32) : f2_t{0.f, 0.f};
       }
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
@@ -293,21 +294,18 @@ __global__ __launch_bounds__(256) void k_gemm_splitk_epilogue(const float *__res
         u += b[q];
       }
     }
-    u32x2_t w;
+    uint32_t w;
     if (silu) {
-      w = u32x2_t{pack_bf16x2(silu_f(x[0]) * u[0], silu_f(x[1]) * u[1]),
-                  pack_bf16x2(silu_f(x[2]) * u[2], silu_f(x[3]) * u[3])};
+      w = pack_bf16x2(silu_f(x[0]) * u[0], silu_f(x[1]) * u[1]);
     } else {
       if (epi == EPI_RESIDUAL) {
-        const u32x2_t r = *reinterpret_cast<const u32x2_t *>(res + (size_t)m * N + n);
-        x[0] += bf16_lo(r[0]);
-        x[1] += bf16_hi(r[0]);
-        x[2] += bf16_lo(r[1]);
-        x[3] += bf16_hi(r[1]);
+        const uint32_t r = *reinterpret_cast<const uint32_t *>(res + (size_t)m * N + n);
+        x[0] += bf16_lo(r);
+        x[1] += bf16_hi(r);
       }
-      w = u32x2_t{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
+      w = pack_bf16x2(x[0], x[1]);
     }
-    *reinterpret_cast<u32x2_t *>(out + (size_t)m * outc + n) = w;
+    *reinterpret_cast<uint32_t *>(out + (size_t)m * outc + n) = w;
   }
 }
 
@@ -892,8 +890,8 @@ static hipError_t finish_splitk(const float *part, int splits, uint16_t *out, co
 static hipError_t launch_splitk_epilogue(const float *part, int splits, uint16_t *out, const uint16_t *res, int M,
                                          int N, int epi, hipStream_t st) {
   const int outc = epi == EPI_SILU_MUL ? N / 2 : N;
-  const long total = (long)M * (outc / 4);
-  const int blocks = (int)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
+  const long total = (long)M * (outc / 2);
+  const int blocks = (int)((total + 255) / 256 < 8192 ? (total + 255) / 256 : 8192);
   hipLaunchKernelGGL(k_gemm_splitk_epilogue, dim3(blocks), dim3(256), 0, st, part, splits, out, res, M, N, epi);
   return hipGetLastError();
 }
