@@ -132,24 +132,26 @@ __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv,
   const int nh = nq + 2 * nkv;
   const int hpb = (nh + gridDim.y - 1) / gridDim.y;
   const int h_lo = blockIdx.y * hpb, h_hi = min(nh, h_lo + hpb);
-  if constexpr (FUSED) {
-    const int cols = nh * hd;
-    float ss = 0.f;
-    for (int s = 0; s < qp.splits; ++s) ss += qp.ssq[(size_t)s * m.T + r];
-    const float inv = 1.0f / sqrtf(ss / (float)qp.d + qp.eps);
-    const size_t stride = (size_t)m.T * cols;
-    const float *p0 = qp.part + (size_t)r * cols;
-    uint16_t *dst = qkv + (size_t)r * cols;
-    for (int c = h_lo * hd + threadIdx.x * 4; c < h_hi * hd; c += blockDim.x * 4) {
-      f32x4_t x = {0.f, 0.f, 0.f, 0.f};
-      for (int s = 0; s < qp.splits; ++s) x += *reinterpret_cast<const f32x4_t *>(p0 + s * stride + c);
-      *reinterpret_cast<u32x2_t *>(dst + c) = u32x2_t{pack_bf16x2(x[0] * inv, x[1] * inv), pack_bf16x2(x[2] * inv, x[3] * inv)};
-    }
-    __syncthreads();  // (the row's bf16 values are read back by other threads below)
-  }
   const int seq = m.row_seq[r];
   const int pos = m.row_pos[r];
   const int half = hd >> 1;
+  // FUSED: the loads of the thread's first 4 columns (a block's heads fit
+  // in one pass at 256 threads) are issued before the angle table is
+  // formed, so the table's fp64 work runs under their latency; one barrier
+  // then publishes both the table and the row
+  const int cols_f = nh * hd;
+  const size_t stride_f = (size_t)m.T * cols_f;
+  const float *p0 = FUSED ? qp.part + (size_t)r * cols_f : nullptr;
+  const int c_first = h_lo * hd + threadIdx.x * 4;
+  f32x4_t x_first = {0.f, 0.f, 0.f, 0.f};
+  float inv = 1.f;
+  if constexpr (FUSED) {
+    float ss = 0.f;
+    for (int s = 0; s < qp.splits; ++s) ss += qp.ssq[(size_t)s * m.T + r];
+    if (c_first < h_hi * hd)
+      for (int s = 0; s < qp.splits; ++s) x_first += *reinterpret_cast<const f32x4_t *>(p0 + s * stride_f + c_first);
+    inv = 1.0f / sqrtf(ss / (float)qp.d + qp.eps);
+  }
   for (int t = threadIdx.x; t < half; t += blockDim.x) {
     const double inv_freq = exp2(-(2.0 * t / hd) * log2_theta);
     const double ang = (double)pos * inv_freq;
@@ -160,7 +162,18 @@ __global__ __launch_bounds__(256) void k_rope_append(uint16_t *__restrict__ qkv,
     cs[t] = c;
     sn[t] = s;
   }
-  __syncthreads();
+  if constexpr (FUSED) {
+    uint16_t *dst = qkv + (size_t)r * cols_f;
+    for (int c = c_first; c < h_hi * hd; c += blockDim.x * 4) {
+      f32x4_t x = x_first;
+      if (c != c_first) {
+        x = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int s = 0; s < qp.splits; ++s) x += *reinterpret_cast<const f32x4_t *>(p0 + s * stride_f + c);
+      }
+      *reinterpret_cast<u32x2_t *>(dst + c) = u32x2_t{pack_bf16x2(x[0] * inv, x[1] * inv), pack_bf16x2(x[2] * inv, x[3] * inv)};
+    }
+  }
+  __syncthreads();  // the angle table, and (FUSED) the row's bf16 values read back by other threads below
   const int cols = (nq + 2 * nkv) * hd;
   uint16_t *row = qkv + (size_t)r * cols;
   const int page = bt[(size_t)seq * max_pages + pos / kPageSize];
