@@ -10,8 +10,10 @@ namespace eb {
 // registers: every load of the row and of gamma is issued before the first
 // use, so the kernel waits for memory once; longer rows take a second pass.
 // ---------------------------------------------------------------------------
-constexpr int kNormMaxChunks = 16;  // 16-byte chunks per lane held in registers (rows up to 8192)
-
+// MC: 16-byte chunks per lane held in registers (rows up to 512 MC wide),
+// the smallest of 4, 8, 16 that holds the row, so that narrow rows leave
+// room for more waves
+template <int MC>
 __global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t *__restrict__ x, const uint16_t *__restrict__ g,
                                                  uint16_t *__restrict__ out, int rows, int d, float eps) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -20,21 +22,21 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t *__restrict__ x,
   const uint16_t *xr = x + (size_t)row * d;
   uint16_t *orow = out + (size_t)row * d;
   const int nch = d >> 3;
-  if (nch <= 64 * kNormMaxChunks) {
-    u32x4_t v[kNormMaxChunks], gv[kNormMaxChunks];
+  if (nch <= 64 * MC) {
+    u32x4_t v[MC], gv[MC];
 #pragma unroll
-    for (int j = 0; j < kNormMaxChunks; ++j) {
+    for (int j = 0; j < MC; ++j) {
       const int c = lane + 64 * j;
       v[j] = c < nch ? ld_u32x4(xr + c * 8) : u32x4_t{0u, 0u, 0u, 0u};
     }
 #pragma unroll
-    for (int j = 0; j < kNormMaxChunks; ++j) {
+    for (int j = 0; j < MC; ++j) {
       const int c = lane + 64 * j;
       gv[j] = c < nch ? ld_u32x4(g + c * 8) : u32x4_t{0u, 0u, 0u, 0u};  // shared by all rows: an L2 hit
     }
     float ss = 0.f;
 #pragma unroll
-    for (int j = 0; j < kNormMaxChunks; ++j)
+    for (int j = 0; j < MC; ++j)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float a = bf16_lo(v[j][i]), b = bf16_hi(v[j][i]);
@@ -43,7 +45,7 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t *__restrict__ x,
     ss = wave_sum(ss);
     const float inv = 1.0f / sqrtf(ss / (float)d + eps);
 #pragma unroll
-    for (int j = 0; j < kNormMaxChunks; ++j) {
+    for (int j = 0; j < MC; ++j) {
       const int c = lane + 64 * j;
       if (c < nch) {
         u32x4_t o;
@@ -80,7 +82,13 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const uint16_t *__restrict__ x,
 hipError_t launch_rmsnorm(const uint16_t *x, const uint16_t *gamma, uint16_t *out, int rows, int d, float eps,
                           hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_rmsnorm, dim3((rows + 3) / 4), dim3(256), 0, st, x, gamma, out, rows, d, eps);
+  const int nch = d >> 3;
+  if (nch <= 64 * 4)
+    hipLaunchKernelGGL(k_rmsnorm<4>, dim3((rows + 3) / 4), dim3(256), 0, st, x, gamma, out, rows, d, eps);
+  else if (nch <= 64 * 8)
+    hipLaunchKernelGGL(k_rmsnorm<8>, dim3((rows + 3) / 4), dim3(256), 0, st, x, gamma, out, rows, d, eps);
+  else
+    hipLaunchKernelGGL(k_rmsnorm<16>, dim3((rows + 3) / 4), dim3(256), 0, st, x, gamma, out, rows, d, eps);
   return hipGetLastError();
 }
 
