@@ -2,13 +2,13 @@
 // W [N, K] weights, both K-contiguous bf16, fp32 accumulation on the
 // 16x16x32 bf16 MFMA.
 //
-//  * skinny: decode-sized batches (up to 256 rows, 64-row x 64-column
-//    tiles).  The product is bound by streaming W from HBM once: tiles stage
-//    W and A through LDS in 128-wide K slices read as whole 256-byte rows,
-//    the 4 waves of a block split the tile's columns, the row blocks of a
-//    column tile run side by side on one XCD so W comes from HBM once, and
-//    blocks may further split K, with a small reduction kernel applying the
-//    epilogue.
+//  * skinny: decode-sized batches (up to 256 rows, 64-row x 128-column
+//    tiles, one block per CU).  The product is bound by streaming W from HBM
+//    once: tiles stage W and A through LDS in 128-wide K slices read as
+//    whole 256-byte rows, the 4 waves of a block own 32 columns each, the
+//    row blocks of a column tile run side by side on one XCD so W comes from
+//    HBM once, and blocks may further split K, with a small reduction kernel
+//    applying the epilogue.
 //  * tiled: larger M.  128x128 output tiles, K tiles of 64 double-buffered in
 //    LDS, 4 waves each owning a 64x64 sub-tile.
 //
@@ -63,6 +63,22 @@ constexpr int SK_LDS = 2 * (SK_BN + SK_BM) * SK_ROWB;
 // and its up partner (32 apart) land in the same wave.
 __device__ __forceinline__ int sk_col(int w, int j) { return j < 8 ? 8 * w + j : 32 + 8 * w + (j - 8); }
 
+// The weight-streaming kernel's block is 128 logical columns x 64 rows, one
+// block per CU.  W and A are staged through LDS in 128-wide K slices (each
+// load instruction reads 4 rows x 256 contiguous bytes, so a wave's loads
+// touch few pages), and each of the 4 waves owns 32 columns: per K step of
+// 32 it reads 2 W and 4 A fragments from LDS for 8 products, so the LDS
+// carries 3.5 bytes per weight byte (staging writes included) where a
+// 64-column block with 16 columns per wave carried 7.
+constexpr int SW_BN = 128;                                 // logical columns per block
+constexpr int SW_LDS = 2 * (SW_BN + SK_BM) * SK_ROWB;      // two stages of [128 W rows + 64 A rows]
+
+// Block-local logical column of row lr (0..15) of wave w's column fragment
+// f (0, 1): wave w takes half w % 2 of SiLU group w / 2, fragment 0 its 16
+// gate columns and fragment 1 their 16 up partners (32 further), so a lane
+// holds a gate sum and its partner.
+__device__ __forceinline__ int sw_col(int w, int f, int lr) { return (w >> 1) * 64 + f * 32 + (w & 1) * 16 + lr; }
+
 // PRENORM (split-K partials only): A holds the rows x of an RMSNorm that
 // precedes the product.  The kernel stages bf16(x * gamma) instead of A and
 // the blocks of the first column tile write each row's partial sum of
@@ -76,7 +92,7 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
                                                      int N, int K, int epi, int ksteps_per_split, int tiles, int mt,
                                                      int per_xcd, const uint16_t *__restrict__ gamma = nullptr,
                                                      float *__restrict__ ssq = nullptr) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t sk_lds[];  // [2][64 W rows + 64 A rows][SK_ROWB]
+  extern __shared__ __attribute__((aligned(16))) uint8_t sk_lds[];  // [2][128 W rows + 64 A rows][SK_ROWB]
   // block b takes tile (b % 8) * per_xcd + b / 8, so each XCD walks its own
   // contiguous tile range; the mt row blocks of one column tile are
   // neighbours there and share the W tile through that XCD's L2
@@ -85,57 +101,65 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n0 = (t / mt) * SK_BN;
+  const int n0 = (t / mt) * SW_BN;
   const int split = blockIdx.y;
   const int m0 = (t % mt) * SK_BM;
   const int kbeg = split * ksteps_per_split * 32;
   const int kend = min(K, kbeg + ksteps_per_split * 32);
-  const int nst = (kend - kbeg + SK_KC - 1) / SK_KC;
+  const int nst = kend > kbeg ? (kend - kbeg + SK_KC - 1) / SK_KC : 0;
   constexpr uint32_t WES = W8 ? 1u : 2u;  // bytes per W element
   const buf_rsrc_t ra = make_rsrc(A, (int)min((size_t)M * K * 2, (size_t)0x7FFFFFFF));
   const buf_rsrc_t rw = make_rsrc(W, (int)min((size_t)N * K * WES, (size_t)0x7FFFFFFF));
 
-  // Staging: thread t moves 16-byte chunk t % 16 of tile rows t / 16 + 16 j
-  // (each wave instruction reads 4 rows x 256 contiguous bytes); rows outside
-  // the operands, k past the block's range: offsets past the descriptor's
-  // range, loaded as zero without memory traffic.
+  // Staging: thread t moves 16-byte chunk t % 16 of W tile rows t / 16 + 16 j
+  // (j < 8) and A tile rows t / 16 + 16 j (j < 4); each wave instruction
+  // reads 4 rows x 256 contiguous bytes.  Rows outside the operands, k past
+  // the block's range: offsets past the descriptor's range, loaded as zero
+  // without memory traffic.
   const int ch = tid & 15, r0 = tid >> 4;
-  uint32_t woff[4], aoff[4];
+  uint32_t woff[8], aoff[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < 8; ++j) {
     const int wr = w_row_of(n0 + r0 + 16 * j, N, epi);
     woff[j] = wr >= 0 ? ((uint32_t)wr * (uint32_t)K + (uint32_t)(ch * 8)) * WES : 0x80000000u;
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
     const int m = m0 + r0 + 16 * j;
     aoff[j] = m < M ? ((uint32_t)m * (uint32_t)K + (uint32_t)(ch * 8)) * 2u : 0x80000000u;
   }
-  u32x4_t wa[4], aa[4], wb[4], ab[4];
+  u32x4_t wa[8], aa[4], wb[8], ab[4];
   u32x4_t ga = {0u, 0u, 0u, 0u}, gb = {0u, 0u, 0u, 0u};  // PRENORM: gamma chunk of each stage
   float ssacc[4] = {0.f, 0.f, 0.f, 0.f};                 // PRENORM: sum of squares of rows r0 + 16 j
   const buf_rsrc_t rg = make_rsrc(PRENORM ? gamma : A, PRENORM ? K * 2 : 16);
-  auto gload = [&](int s, u32x4_t (&wr)[4], u32x4_t (&ar)[4], u32x4_t &gr) {
+  auto gload = [&](int s, u32x4_t (&wr)[8], u32x4_t (&ar)[4], u32x4_t &gr) {
     const int k = kbeg + s * SK_KC + ch * 8;
     const bool ok = s < nst && k < kend;
     const uint32_t kb = (uint32_t)(kbeg + s * SK_KC) * 2u;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 8; ++j) {
       if constexpr (W8) {  // 8 codes in the low half; exact bf16 images when staged
         const u32x2_t c = buf_ld_u32x2<kAuxNT>(rw, (int)(ok ? woff[j] + kb / 2u : 0x80000000u));
         wr[j] = u32x4_t{c[0], c[1], 0u, 0u};
       } else {
         wr[j] = buf_ld_u32x4<kAuxNT>(rw, (int)(ok ? woff[j] + kb : 0x80000000u));
       }
-      ar[j] = buf_ld_u32x4<0>(ra, (int)(ok ? aoff[j] + kb : 0x80000000u));
     }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ar[j] = buf_ld_u32x4<0>(ra, (int)(ok ? aoff[j] + kb : 0x80000000u));
     if constexpr (PRENORM) gr = buf_ld_u32x4<0>(rg, (int)(ok ? (uint32_t)(k * 2) : 0x80000000u));
   };
   const bool first_col_tile = n0 == 0;
-  auto swrite = [&](int buf, const u32x4_t (&wr)[4], const u32x4_t (&ar)[4], const u32x4_t &gr) {
-    uint8_t *b = sk_lds + buf * (SK_BN + SK_BM) * SK_ROWB;
+  auto swrite = [&](int buf, const u32x4_t (&wr)[8], const u32x4_t (&ar)[4], const u32x4_t &gr) {
+    uint8_t *b = sk_lds + buf * (SW_BN + SK_BM) * SK_ROWB;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 8; ++j) {
       u32x4_t wv = wr[j];
       if constexpr (W8) wv = e4m3x8_to_bf16x8(u32x2_t{wr[j][0], wr[j][1]});
       *reinterpret_cast<u32x4_t *>(b + (r0 + 16 * j) * SK_ROWB + ch * 16) = wv;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
       u32x4_t av = ar[j];
       if constexpr (PRENORM) {
         if (first_col_tile) {
@@ -149,27 +173,33 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
         for (int e = 0; e < 4; ++e)
           av[e] = bf16_pair_rne(bf16_lo(ar[j][e]) * bf16_lo(gr[e]), bf16_hi(ar[j][e]) * bf16_hi(gr[e]));
       }
-      *reinterpret_cast<u32x4_t *>(b + (SK_BN + r0 + 16 * j) * SK_ROWB + ch * 16) = av;
+      *reinterpret_cast<u32x4_t *>(b + (SW_BN + r0 + 16 * j) * SK_ROWB + ch * 16) = av;
     }
   };
-  // Waves split the block's columns (16 each, see sk_col) and run the whole
-  // K range: the product is formed transposed, D[n][m] = W A^T, so a lane
-  // ends with 4 consecutive columns of one row.
-  f32x4_t acc[4];
+  // Each wave runs the whole K range on its 32 columns (two fragments, see
+  // sw_col); the product is formed transposed, D[n][m] = W A^T, so a lane
+  // ends with 4 consecutive columns of one row per fragment.
+  f32x4_t acc[2][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[f][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   const int lr = lane & 15, lg = lane >> 4;
-  const int my_wrow = sk_col(wave, lr);
   auto compute = [&](int buf) {
-    const uint8_t *b = sk_lds + buf * (SK_BN + SK_BM) * SK_ROWB;
+    const uint8_t *b = sk_lds + buf * (SW_BN + SK_BM) * SK_ROWB;
 #pragma unroll
     for (int ks = 0; ks < SK_KC / 32; ++ks) {
-      const u32x4_t wf = *reinterpret_cast<const u32x4_t *>(b + my_wrow * SK_ROWB + (ks * 4 + lg) * 16);
+      u32x4_t wf[2], af[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const u32x4_t af = *reinterpret_cast<const u32x4_t *>(b + (SK_BN + i * 16 + lr) * SK_ROWB + (ks * 4 + lg) * 16);
-        acc[i] = mfma16x16x32(wf, af, acc[i]);
-      }
+      for (int f = 0; f < 2; ++f)
+        wf[f] = *reinterpret_cast<const u32x4_t *>(b + sw_col(wave, f, lr) * SK_ROWB + (ks * 4 + lg) * 16);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[i] = *reinterpret_cast<const u32x4_t *>(b + (SW_BN + i * 16 + lr) * SK_ROWB + (ks * 4 + lg) * 16);
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[f][i] = mfma16x16x32(wf[f], af[i], acc[f][i]);
     }
   };
   // Two stages in flight in registers, one in LDS: write stage s + 1 while
@@ -196,65 +226,72 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
     if (first_col_tile) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float t = group_sum<16>(ssacc[j]);
+        const float s = group_sum<16>(ssacc[j]);
         const int m = m0 + r0 + 16 * j;
-        if (ch == 0 && m < M) ssq[(size_t)split * M + m] = t;
+        if (ch == 0 && m < M) ssq[(size_t)split * M + m] = s;
       }
     }
   }
 
-  // lane: rows m = m0 + 16 i + lr, logical columns c .. c+3 of the block,
-  // c = sk_col(wave, 4 lg)
-  const int c = sk_col(wave, 4 * lg);
+  // lane: rows m = m0 + 16 i + lr; fragment f holds logical columns
+  // c_f .. c_f + 3 with c_f = n0 + sw_col(wave, f, 4 lg)
   const int ncols = logical_cols(N, epi);
-  if constexpr (W8) {
-    if (n0 + c < ncols) {
+  int cf[2];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc[i] = row_scaled(acc[i], wscale, n0 + c, N, epi);
-    }
+  for (int f = 0; f < 2; ++f) cf[f] = n0 + sw_col(wave, f, 4 * lg);
+  if constexpr (W8) {
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+      if (cf[f] < ncols) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[f][i] = row_scaled(acc[f][i], wscale, cf[f], N, epi);
+      }
   }
   if (part) {  // split-K partial, logical column space
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int m = m0 + i * 16 + lr;
-      if (m < M && n0 + c < ncols)
-        *reinterpret_cast<f32x4_t *>(part + ((size_t)split * M + m) * ncols + n0 + c) = acc[i];
-    }
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = m0 + i * 16 + lr;
+        if (m < M && cf[f] < ncols)
+          *reinterpret_cast<f32x4_t *>(part + ((size_t)split * M + m) * ncols + cf[f]) = acc[f][i];
+      }
     return;
   }
   if (epi == EPI_SILU_MUL) {
-    // up partners sit 2 lane groups away (xor 32); lanes with lg < 2 finish
+    // fragment 0 holds gate sums, fragment 1 their up partners
     const int F = N >> 1;
-    const int f = (n0 >> 1) + 8 * wave + 4 * lg;
+    const int fo = ((n0 + (wave >> 1) * 64) >> 1) + (wave & 1) * 16 + 4 * lg;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      f32x4_t u;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) u[e] = shfl_xor_f32(acc[i][e], 32);
       const int m = m0 + i * 16 + lr;
-      if (lg < 2 && m < M && f < F) {
-        u32x2_t w = {pack_bf16x2(silu_f(acc[i][0]) * u[0], silu_f(acc[i][1]) * u[1]),
-                     pack_bf16x2(silu_f(acc[i][2]) * u[2], silu_f(acc[i][3]) * u[3])};
-        *reinterpret_cast<u32x2_t *>(out + (size_t)m * F + f) = w;
+      if (m < M && fo < F) {
+        const f32x4_t g = acc[0][i], u = acc[1][i];
+        const u32x2_t w = {pack_bf16x2(silu_f(g[0]) * u[0], silu_f(g[1]) * u[1]),
+                           pack_bf16x2(silu_f(g[2]) * u[2], silu_f(g[3]) * u[3])};
+        *reinterpret_cast<u32x2_t *>(out + (size_t)m * F + fo) = w;
       }
     }
     return;
   }
-  const int n = n0 + c;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int m = m0 + i * 16 + lr;
-    if (m < M && n < N) {
-      f32x4_t v = acc[i];
-      if (epi == EPI_RESIDUAL) {
-        const u32x2_t r = *reinterpret_cast<const u32x2_t *>(res + (size_t)m * N + n);
-        v[0] += bf16_lo(r[0]);
-        v[1] += bf16_hi(r[0]);
-        v[2] += bf16_lo(r[1]);
-        v[3] += bf16_hi(r[1]);
+  for (int f = 0; f < 2; ++f) {
+    const int n = cf[f];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + i * 16 + lr;
+      if (m < M && n < N) {
+        f32x4_t v = acc[f][i];
+        if (epi == EPI_RESIDUAL) {
+          const u32x2_t r = *reinterpret_cast<const u32x2_t *>(res + (size_t)m * N + n);
+          v[0] += bf16_lo(r[0]);
+          v[1] += bf16_hi(r[0]);
+          v[2] += bf16_lo(r[1]);
+          v[3] += bf16_hi(r[1]);
+        }
+        const u32x2_t w = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        *reinterpret_cast<u32x2_t *>(out + (size_t)m * N + n) = w;
       }
-      u32x2_t w = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-      *reinterpret_cast<u32x2_t *>(out + (size_t)m * N + n) = w;
     }
   }
 }
@@ -666,9 +703,9 @@ __global__ __launch_bounds__(BG_THREADS) void k_gemm_big(const uint16_t *__restr
 // tile b / col_tiles and column tile b % col_tiles of that expert's W, so the
 // column tiles of one row tile run side by side and share its A rows, and
 // the row tiles of one expert follow each other and share its W tiles in L2.
-// The main loop is the weight-streaming kernel's: W and A staged through LDS
-// in 128-wide K slices, the 4 waves split the tile's columns (transposed
-// product).  A rows are gathered through a_rows (null: the sorted row
+// The main loop stages W and A through LDS in 128-wide K slices as the
+// weight-streaming kernel does; here the 4 waves split the tile's 64 columns
+// (16 each, transposed product).  A rows are gathered through a_rows (null: the sorted row
 // itself).  SiLU: bf16 [rows, N / 2]; store: fp32 [rows, N].
 template <bool F32OUT>
 __global__ __launch_bounds__(256) void k_gemm_grouped(const uint16_t *__restrict__ A, int a_nrows,
@@ -908,14 +945,19 @@ static hipError_t finish_splitk(const float *part, int splits, uint16_t *out, co
 }
 
 static int skinny_splits(int M, int N, int K) {
-  const int ncol_tiles = (N + SK_BN - 1) / SK_BN;
-  const int mt = (M + SK_BM - 1) / SK_BM;
+  const int tiles = ((N + SW_BN - 1) / SW_BN) * ((M + SK_BM - 1) / SK_BM);
   const int nsteps = (K + 31) / 32;
-  int splits = 1;
-  // at least 384 blocks (the staging ring holds ~2 per CU) while each split
-  // keeps 4 or more stages of 128 in K
-  while (ncol_tiles * mt * splits < 384 && nsteps / (splits * 2) >= 16) splits *= 2;
-  return splits;
+  // one block per CU (256 CUs).  A grid that covers at least 3/4 of the CUs
+  // is not split; otherwise K is split into the count whose rounds of 256
+  // blocks take the least time per split (ceil(tiles s / 256) / s; fewer
+  // splits on ties), each split keeping 4 or more 128-wide K stages
+  if (tiles >= 192) return 1;
+  int best = 1;
+  for (int s = 2; s <= 16 && nsteps / s >= 16; ++s) {
+    const long rs = ((long)tiles * s + 255) / 256, rb = ((long)tiles * best + 255) / 256;
+    if (rs * best < rb * s) best = s;  // rs / s < rb / best
+  }
+  return best;
 }
 
 GemmPlan plan_gemm(int M, int N, int K, int epi, bool w8) {
@@ -971,14 +1013,14 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, cons
     const int per = (nsteps + splits - 1) / splits;
     float *part = splits > 1 ? reinterpret_cast<float *>(ws) : nullptr;
     const int mt = (M + SK_BM - 1) / SK_BM;
-    const int tiles = ((ncols + SK_BN - 1) / SK_BN) * mt;
+    const int tiles = ((ncols + SW_BN - 1) / SW_BN) * mt;
     const int per_xcd = (tiles + 7) / 8;
     dim3 grid(8 * per_xcd, splits);
     if (w8)
-      hipLaunchKernelGGL(k_gemm_skinny<true>, grid, dim3(256), SK_LDS, st, A, W, wscale, out, res, part, M, N, K, epi,
+      hipLaunchKernelGGL(k_gemm_skinny<true>, grid, dim3(256), SW_LDS, st, A, W, wscale, out, res, part, M, N, K, epi,
                          per, tiles, mt, per_xcd);
     else
-      hipLaunchKernelGGL(k_gemm_skinny<false>, grid, dim3(256), SK_LDS, st, A, W, wscale, out, res, part, M, N, K,
+      hipLaunchKernelGGL(k_gemm_skinny<false>, grid, dim3(256), SW_LDS, st, A, W, wscale, out, res, part, M, N, K,
                          epi, per, tiles, mt, per_xcd);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
@@ -1036,14 +1078,14 @@ hipError_t launch_gemm_prenorm(const GemmPlan &p, const uint16_t *x, const uint1
   const int nsteps = (K + 31) / 32;
   const int per = (nsteps + p.splits - 1) / p.splits;
   const int mt = (M + SK_BM - 1) / SK_BM;
-  const int tiles = ((N + SK_BN - 1) / SK_BN) * mt;
+  const int tiles = ((N + SW_BN - 1) / SW_BN) * mt;
   const int per_xcd = (tiles + 7) / 8;
   dim3 grid(8 * per_xcd, p.splits);
   if (wscale)
-    hipLaunchKernelGGL((k_gemm_skinny<true, true>), grid, dim3(256), SK_LDS, st, x, W, wscale, nullptr, nullptr, part,
+    hipLaunchKernelGGL((k_gemm_skinny<true, true>), grid, dim3(256), SW_LDS, st, x, W, wscale, nullptr, nullptr, part,
                        M, N, K, (int)EPI_STORE, per, tiles, mt, per_xcd, gamma, ssq);
   else
-    hipLaunchKernelGGL((k_gemm_skinny<false, true>), grid, dim3(256), SK_LDS, st, x, W, wscale, nullptr, nullptr,
+    hipLaunchKernelGGL((k_gemm_skinny<false, true>), grid, dim3(256), SW_LDS, st, x, W, wscale, nullptr, nullptr,
                        part, M, N, K, (int)EPI_STORE, per, tiles, mt, per_xcd, gamma, ssq);
   return hipGetLastError();
 }
