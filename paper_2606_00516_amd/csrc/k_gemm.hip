@@ -950,10 +950,11 @@ static int skinny_splits(int M, int N, int K) {
   // one block per CU (256 CUs).  A grid that covers at least 3/4 of the CUs
   // is not split; otherwise K is split into the count whose rounds of 256
   // blocks take the least time per split (ceil(tiles s / 256) / s; fewer
-  // splits on ties), each split keeping 4 or more 128-wide K stages
+  // splits on ties), at most 8 (the fp32 partials are written and read back
+  // once per split) and each split keeping 4 or more 128-wide K stages
   if (tiles >= 192) return 1;
   int best = 1;
-  for (int s = 2; s <= 16 && nsteps / s >= 16; ++s) {
+  for (int s = 2; s <= 8 && nsteps / s >= 16; ++s) {
     const long rs = ((long)tiles * s + 255) / 256, rb = ((long)tiles * best + 255) / 256;
     if (rs * best < rb * s) best = s;  // rs / s < rb / best
   }
