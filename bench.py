@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="decode8b",
                     choices=["decode8b", "prefill8b", "mixed8b", "sweep8b", "decode70b", "stack70b", "policy8b",
-                             "long8b", "moe30b", "q30b", "copy"])
+                             "long8b", "moe30b", "q30b", "copy", "oracle_cpu"])
     ap.add_argument("--calib-out", default=None, help="policy8b: write the calibrated step-cost profile here")
     ap.add_argument("--shape", default="l8b", choices=["l8b", "q30b"],
                     help="layer of the sweep8b / policy8b workloads: the llama3-8b layer, or the "
@@ -764,6 +764,43 @@ def sweep_part(args, dev, w, repeats=5):
                                                 "contexts U[1024,8192]"}}
 
 
+def oracle_cpu(args, dev, per_run_s=4.0, runs=3):
+    """The CPU oracle (as it stands, on this host's cores) on every workload it
+    can run: the tiny layer in its three modes, the 8B decode and prefill
+    steps and the 2048-token MB step at r = 0, 0.5 and 1, each as the median
+    of ``runs`` bounded runs of about ``per_run_s`` seconds of oracle time
+    (cheapest requests first, as in the default line's baseline)."""
+    import torch
+
+    from paper_2606_00516_amd import inputs as gen
+    cases = [("tiny decode EB (4 requests, ctx U[64,256])", gen.TINY, gen.batch_tiny(mode="decode"), "decode"),
+             ("tiny prefill EB (128-token chunk)", gen.TINY, gen.batch_tiny(mode="prefill"), "prefill"),
+             ("tiny MB (4 decode rows + a 128-token chunk)", gen.TINY, gen.batch_tiny(mode="mixed"), "mixed"),
+             ("llama3-8b decode EB (64 requests, ctx U[512,4096])", gen.L8B, gen.batch_8b_decode(), "decode"),
+             ("llama3-8b prefill EB (8 prompts U[256,2048])", gen.L8B, gen.batch_8b_prefill(), "prefill")]
+    for r in (0.0, 0.5, 1.0):
+        cases.append((f"llama3-8b MB, 2048 tokens, r = {r:.1f}", gen.L8B, gen.batch_8b_mixed(r), "mixed"))
+    out = []
+    weights = {}
+    for label, shape, batch, mode in cases:
+        if shape.name not in weights:
+            weights[shape.name] = gen.make_weights(shape, device=dev)
+        w = weights[shape.name]
+        pool, _ = make_pool(gen, shape, batch, "bf16", device=dev, poison=False)
+        x = gen.make_x(shape, batch.num_tokens, device=dev)
+        res = [cpu_baseline(shape, batch, w, pool, x, mode, per_run_s) for _ in range(runs)]
+        del pool, x
+        torch.cuda.empty_cache()
+        tps = sorted(r_["tokens_per_s"] for r_ in res)
+        gbps = sorted(r_["value"] for r_ in res)
+        med_tps = tps[len(tps) // 2]
+        out.append({"workload": label, "mode": mode, "tokens_per_s_median": med_tps, "tokens_per_s_runs": tps,
+                    "gbps_median": gbps[len(gbps) // 2],
+                    "sample": res[len(res) // 2]["sample"], "seconds_per_run": res[0]["seconds"]})
+        print(f"# {label}: {med_tps} tokens/s (runs {tps})", file=sys.stderr, flush=True)
+    return out
+
+
 def host_facts():
     """The host the CPU oracle runs on: logical CPUs, model, BLAS."""
     import platform
@@ -816,6 +853,22 @@ def main():
         dt = (time.perf_counter() - t0) / args.steps
         print(json.dumps({"workload": "copy", "bytes_read": n, "bytes_written": n, "ms": dt * 1e3,
                           "GBps": 2 * n / dt / 1e9}))
+        return
+
+    if args.workload == "oracle_cpu":
+        t0 = time.perf_counter()
+        pts = oracle_cpu(args, dev)
+        line = {"metric": "CPU oracle throughput", "value": pts[3]["tokens_per_s_median"], "unit": "tokens/s",
+                "n_gpus": 0, "steps": 3, "warmup": 0, "ms_per_step": None, "higher_is_better": True,
+                "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+                "config": {"workload": "the CPU oracle on the tiny, 8B decode / prefill and 8B MB (r = 0, 0.5, 1) "
+                                       "inputs; value: the 8B decode step's median tokens/s"},
+                "host": host_facts(), "points": pts, "wall_s": round(time.perf_counter() - t0, 1)}
+        js = json.dumps(line)
+        print(js)
+        if args.json_out:
+            with open(args.json_out, "w") as f:
+                f.write(js + "\n")
         return
 
     if args.workload == "sweep8b":
