@@ -9,7 +9,7 @@ of that quantity's own largest magnitude: q after RoPE, the attention
 output, h1, b = RMSNorm(h1) g2 and m, besides y.  Full-size 8B and 70B
 batches are checked on sampled requests (requests share no pages, so a
 subset is computed exactly as in the whole batch), including the longest 8B
-prompt and the largest chunk of the mixed batches.
+prompt and the largest chunk of the 8B and 70B-shaped mixed batches.
 
 The sharp-attention case (projections N(0, 0.2)) is checked against a CPU
 model of the step's bf16 rounding points (tests/_bf16_points.py) at 2e-2,
@@ -199,6 +199,24 @@ def test_70b_decode_stages_full_size():
     batch = gen.batch_70b_decode()
     sample = [int(np.argmax(batch.context_lens)), 100]
     _sampled_stages(shape, batch, {k: v.cuda() for k, v in w.items()}, Wo, "decode", sample)
+
+
+def test_70b_mixed_stages_largest_chunk():
+    # the 70B-shaped layer's 4096-token MB step at r = 0.2 (819 decode rows,
+    # contexts U[2048,16384], and prefill chunks over prefixes): the mixed
+    # launch with eight query heads per kv head and the 256 x 256 GEMMs at the
+    # 70B widths (qkv 10240, gate/up 57344, down over K = 28672); the largest
+    # chunk and two decode rows against the oracle
+    shape = gen.L70B
+    w = gen.make_weights(shape)
+    Wo = oracle.prepare_weights({k: gen.bits(v) for k, v in w.items()}, oracle_cfg(shape))
+    batch = gen.batch_70b_mixed(0.2)
+    dec = [int(i) for i in np.nonzero(batch.chunk_lens == 1)[0][[0, -1]]]
+    pre = np.nonzero(batch.chunk_lens > 1)[0]
+    largest = int(pre[np.argmax(batch.chunk_lens[pre])])
+    assert batch.num_tokens == 4096 and batch.chunk_lens[largest] >= 256
+    _sampled_stages(shape, batch, {k: v.cuda() for k, v in w.items()}, Wo, "mixed", dec + [largest])
+    torch.cuda.empty_cache()
 
 
 # ------------------------------------------------- fused first RMSNorm + QKV
