@@ -161,8 +161,9 @@ def w8b():
     return wd, Wo
 
 
-def sub_pool_for_oracle(pool: gen.KVPool, batch: gen.Batch, idx):
-    """The pages of requests ``idx`` copied to the host under compact ids."""
+def sub_pool_for_oracle(pool: gen.KVPool, batch: gen.Batch, idx, codes: bool = False):
+    """The pages of requests ``idx`` copied to the host under compact ids
+    (``codes``: an 8-bit pool, copied as its uint8 codes)."""
     need = gen.pages_needed(batch)
     bt_host = pool.block_tables.cpu().numpy()
     pages, rows = [], []
@@ -171,8 +172,9 @@ def sub_pool_for_oracle(pool: gen.KVPool, batch: gen.Batch, idx):
         rows.append(np.arange(len(pages), len(pages) + len(ids)))
         pages.extend(ids.tolist())
     sel = torch.as_tensor(pages, dtype=torch.long, device=pool.k_cache.device)
-    kb = gen.bits(pool.k_cache.index_select(0, sel))
-    vb = gen.bits(pool.v_cache.index_select(0, sel))
+    host = (lambda t: t.cpu().numpy()) if codes else gen.bits
+    kb = host(pool.k_cache.index_select(0, sel))
+    vb = host(pool.v_cache.index_select(0, sel))
     bt = np.full((len(idx), max(len(r) for r in rows)), -1, np.int32)
     for k, r in enumerate(rows):
         bt[k, :len(r)] = r

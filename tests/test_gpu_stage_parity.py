@@ -149,19 +149,27 @@ def w8b():
     return {k: v.cuda() for k, v in w.items()}, Wo
 
 
-def _sampled_stages(shape, batch, w, Wo, mode, sample):
-    pool = gen.make_kv_pool(shape, batch, device="cuda")
-    kb, vb, bt = sub_pool_for_oracle(pool, batch, sample)
+def _sampled_stages(shape, batch, w, Wo, mode, sample, kv_scales=None):
+    """Stages of the sampled requests against the oracle; ``kv_scales``: an
+    8-bit E4M3 cache with those scales (the oracle reads the same codes)."""
+    if kv_scales is None:
+        pool = gen.make_kv_pool(shape, batch, device="cuda")
+        kb, vb, bt = sub_pool_for_oracle(pool, batch, sample)
+    else:
+        pool = gen.make_kv_pool_codes(shape, batch, device="cuda", poison=False)
+        kb, vb, bt = sub_pool_for_oracle(pool, batch, sample, codes=True)
     x = gen.make_x(shape, batch.num_tokens)
     h = B.Handle(shape, batch.num_seqs, batch.num_tokens)
-    y, st = step_with_stages(h, mode, w, pool.k_cache, pool.v_cache, pool.block_tables, batch, x.cuda())
+    y, st = step_with_stages(h, mode, w, pool.k_cache, pool.v_cache, pool.block_tables, batch, x.cuda(),
+                             kv_scales=kv_scales)
     del pool
     assert np.isfinite(y).all()
     sub = batch.subset(sample)
     off = batch.row_offsets
     xs = np.concatenate([gen.bits(x)[off[i]:off[i + 1]] for i in sample])
     cfg = oracle_cfg(shape)
-    ref_y, inter = oracle.layer_step(cfg, Wo, kb, vb, bt, sub.context_lens, sub.chunk_lens, xs, intermediates=True)
+    ref_y, inter = oracle.layer_step(cfg, Wo, kb, vb, bt, sub.context_lens, sub.chunk_lens, xs, intermediates=True,
+                                     kv_scales=kv_scales)
     ref = oracle_stages(inter, Wo, cfg)
     so = sub.row_offsets
     for k, i in enumerate(sample):
@@ -199,6 +207,32 @@ def test_70b_decode_stages_full_size():
     batch = gen.batch_70b_decode()
     sample = [int(np.argmax(batch.context_lens)), 100]
     _sampled_stages(shape, batch, {k: v.cuda() for k, v in w.items()}, Wo, "decode", sample)
+
+
+def test_8b_decode_stages_fp8_cache(w8b):
+    # the 8B decode batch on an 8-bit E4M3 cache (scales that are not powers
+    # of two): the code-reading decode kernel and the code-writing append
+    w, Wo = w8b
+    _sampled_stages(gen.L8B, gen.batch_8b_decode(), w, Wo, "decode", [0, 17, 40, 63], kv_scales=(0.37, 0.61))
+
+
+@pytest.fixture(scope="module")
+def w8b_codes():
+    w = gen.make_weights_fp8(gen.L8B)
+    Wo = oracle.prepare_weights(gen.weight_arrays(w), oracle_cfg(gen.L8B))
+    return {k: v.cuda() for k, v in w.items()}, Wo
+
+
+def test_8b_decode_stages_fp8_weights(w8b_codes):
+    w, Wo = w8b_codes
+    _sampled_stages(gen.L8B, gen.batch_8b_decode(), w, Wo, "decode", [0, 17, 40, 63])
+
+
+def test_8b_prefill_stages_fp8_weights_longest(w8b_codes):
+    # every projection of the 8192-row step on the 256 x 256 tiles with 8-bit W
+    w, Wo = w8b_codes
+    batch = gen.batch_8b_prefill()
+    _sampled_stages(gen.L8B, batch, w, Wo, "prefill", [int(np.argmax(batch.chunk_lens))])
 
 
 def test_70b_mixed_stages_largest_chunk():
