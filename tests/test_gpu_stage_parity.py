@@ -56,8 +56,8 @@ def oracle_stages(inter, W, cfg):
     return ref
 
 
-def compare_stages(got_y, got, ref_y, ref, rows_got, rows_ref, label, tol=TOL):
-    errs = {"y": maxrel(got_y[rows_got], ref_y[rows_ref])}
+def compare_stages(got_y, got, ref_y, ref, rows_got, rows_ref, label, tol=TOL, with_y=True):
+    errs = {"y": maxrel(got_y[rows_got], ref_y[rows_ref])} if with_y else {}
     for name, r in ref.items():
         errs[name] = maxrel(got[name][rows_got], r[rows_ref])
     print(label, {k: f"{e:.2e}" for k, e in errs.items()})
@@ -149,9 +149,12 @@ def w8b():
     return {k: v.cuda() for k, v in w.items()}, Wo
 
 
-def _sampled_stages(shape, batch, w, Wo, mode, sample, kv_scales=None):
+def _sampled_stages(shape, batch, w, Wo, mode, sample, kv_scales=None, attention_only=False):
     """Stages of the sampled requests against the oracle; ``kv_scales``: an
-    8-bit E4M3 cache with those scales (the oracle reads the same codes)."""
+    8-bit E4M3 cache with those scales (the oracle reads the same codes);
+    ``attention_only``: the stages up to the feed-forward block's input
+    (q, attention output, h1, norm), for layers whose expert routing may
+    differ from the oracle's on near-tied logits."""
     if kv_scales is None:
         pool = gen.make_kv_pool(shape, batch, device="cuda")
         kb, vb, bt = sub_pool_for_oracle(pool, batch, sample)
@@ -171,10 +174,13 @@ def _sampled_stages(shape, batch, w, Wo, mode, sample, kv_scales=None):
     ref_y, inter = oracle.layer_step(cfg, Wo, kb, vb, bt, sub.context_lens, sub.chunk_lens, xs, intermediates=True,
                                      kv_scales=kv_scales)
     ref = oracle_stages(inter, Wo, cfg)
+    if attention_only:
+        ref = {k: ref[k] for k in ("q", "attn", "h1", "norm")}
     so = sub.row_offsets
     for k, i in enumerate(sample):
         compare_stages(y, st, ref_y, ref, slice(off[i], off[i + 1]), slice(so[k], so[k + 1]),
-                       f"{mode} {batch.label} request {i} (c={batch.context_lens[i]}, n={batch.chunk_lens[i]})")
+                       f"{mode} {batch.label} request {i} (c={batch.context_lens[i]}, n={batch.chunk_lens[i]})",
+                       with_y=not attention_only)
 
 
 def test_8b_decode_stages_full_size(w8b):
@@ -233,6 +239,22 @@ def test_8b_prefill_stages_fp8_weights_longest(w8b_codes):
     w, Wo = w8b_codes
     batch = gen.batch_8b_prefill()
     _sampled_stages(gen.L8B, batch, w, Wo, "prefill", [int(np.argmax(batch.chunk_lens))])
+
+
+@pytest.mark.parametrize("mode", ["decode", "prefill"])
+def test_q30b_attention_stages_full_size(mode):
+    # the Qwen3-30B-A3B-shaped layer (q/k norms, 32 q / 4 kv heads, G = 8):
+    # its attention half at full size; the expert block's output is checked
+    # under the routing reading by the MoE layer tests
+    shape = gen.Q30B
+    w = gen.make_weights(shape)
+    Wo = oracle.prepare_weights({k: gen.bits(v) for k, v in w.items()}, oracle_cfg(shape))
+    if mode == "decode":
+        batch, sample = gen.batch_8b_decode(), [0, 21, 63]
+    else:
+        batch = gen.batch_8b_prefill()
+        sample = [int(np.argmax(batch.chunk_lens))]
+    _sampled_stages(shape, batch, {k: v.cuda() for k, v in w.items()}, Wo, mode, sample, attention_only=True)
 
 
 def test_70b_mixed_stages_largest_chunk():
