@@ -65,6 +65,9 @@ def parse():
                     help="KV cache element: bf16, or 8-bit E4M3 codes with per-tensor k/v scales")
     ap.add_argument("--weights", default="bf16", choices=["bf16", "fp8"],
                     help="projection weights: bf16, or 8-bit E4M3 codes with one fp32 scale per output row")
+    ap.add_argument("--packed-weights", default="on", choices=["on", "off"],
+                    help="single-layer workloads: give the step fragment-packed copies of the bf16 projections "
+                         "(made once, before timing; read by the weight-streaming GEMMs of steps under 256 rows)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="decode8b: skip the prefill step and the MB sweep that the default line carries")
@@ -999,6 +1002,10 @@ def main():
                "mixed": B.eb_layer_step_mixed}[mode]
     # inputs generated on the GPU and left resident in HBM
     w = make_w(gen, shape, args.weights, device=dev)
+    packed = args.packed_weights == "on" and args.weights == "bf16"
+    if packed:
+        w = B.pack_layer_weights(w)
+        torch.cuda.synchronize()
     pool, kvs = make_pool(gen, shape, batch, args.kv, device=dev)
     x = gen.make_x(shape, batch.num_tokens, device=dev)
     y = torch.empty_like(x)
@@ -1065,6 +1072,7 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": label, "kv_cache": KV_LABEL[args.kv], "weights": W_LABEL[args.weights],
+                   "packed_weights": packed,
                    "num_tokens": wk["T"],
                    "num_requests": batch.num_seqs,
                    "decode_share": round(batch.num_decode / max(wk["T"], 1), 4), "kv_cache": KV_LABEL[args.kv],

@@ -135,6 +135,15 @@ typedef struct eb_layer_weights {
   /* per-head q and k norm gains, bf16 [head_dim] each (qk_norm layers;
    * unused otherwise) */
   const void *q_norm, *k_norm;
+  /* optional fragment-packed copies of the four bf16 projections
+   * (eb_pack_weight; NULL: none).  The weight-streaming GEMMs (steps of at
+   * most 256 rows) read a packed copy instead of the row-major matrix, the
+   * same values in the same order, so outputs are bitwise unchanged; the
+   * 256 x 256 tiled GEMMs always read the row-major matrices, which stay
+   * required.  Ignored for 8-bit weights and for a matrix whose shape
+   * eb_packed_weight_bytes rejects.  A packed copy must be made from the
+   * matrix it stands beside; the library cannot check that. */
+  const void *p_qkv, *p_o, *p_gate_up, *p_down;
 } eb_layer_weights;
 
 /* Element type of the KV cache. */
@@ -327,6 +336,23 @@ eb_status eb_op_gemm(const void *A, const void *W, void *out, const void *residu
  * operands through its 32-bit buffer ranges: W of 2^31 bytes or more, or A
  * of 2^31 bytes or more unless K is a multiple of 64, M >= 256 and W is
  * under 2^30 bytes.  A NaN code (0x7F, 0xFF) is the caller's to avoid. */
+/* Fragment-packed copy of a bf16 weight matrix W [rows, cols] (device, row
+ * major) for the weight-streaming GEMMs: each 16-row x 32-column block of W
+ * becomes one contiguous 1 KiB run in the lane order of the 16x16x32 bf16
+ * matrix-core operand (lane l: row 16 g + l % 16, columns 32 c + 8 (l / 16)
+ * .. + 7), block (g, c) at byte (g cols / 32 + c) 1024, so that one 16-byte
+ * load per lane fills an operand register from 1 KiB of contiguous memory.
+ * Made once per matrix (weights are fixed while serving, Sec. 4.1), outside
+ * the steps.  eb_packed_weight_bytes returns the size of the copy (rows cols
+ * 2), or 0 when the shape has no packed form (rows % 16, cols % 32 nonzero,
+ * or 2 rows cols >= 2^31).  eb_pack_weight writes it into `packed`
+ * (caller-owned device memory of that size, not overlapping W), enqueued on
+ * `stream`; EB_ERR_NULL for a null pointer, EB_ERR_CONFIG for a shape
+ * without a packed form, EB_ERR_HIP if the launch fails.  The split SwiGLU matrix [2 ffn, hidden]
+ * additionally needs ffn % 16 == 0 for its packed copy to be read. */
+size_t eb_packed_weight_bytes(int rows, int cols);
+eb_status eb_pack_weight(const void *w, void *packed, int rows, int cols, void *stream);
+
 eb_status eb_op_gemm_w8(const void *A, const void *W, const float *w_scale, void *out, const void *residual,
                         int32_t M, int32_t N, int32_t K, eb_epilogue epi, void *ws, size_t ws_bytes, void *stream);
 

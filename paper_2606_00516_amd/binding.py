@@ -29,7 +29,8 @@ SYMBOLS = ("eb_create", "eb_destroy", "eb_workspace_bytes", "eb_layer_step_decod
            "eb_layer_step_mixed", "eb_validate", "eb_status_str", "eb_last_error", "eb_op_rmsnorm",
            "eb_op_gemm_workspace_bytes", "eb_op_gemm", "eb_op_gemm_w8", "eb_op_moe_ffn_workspace_bytes", "eb_op_moe_ffn", "eb_op_rope_kv_append", "eb_op_attention",
            "eb_op_gather_kv", "eb_profile", "eb_profile_read", "eb_profile_stage_name", "eb_stack_workspace_bytes",
-           "eb_stack_step", "eb_workspace_offset", "eb_noalloc_scratch_bytes", "eb_layer_step_mixed_noalloc")
+           "eb_stack_step", "eb_workspace_offset", "eb_noalloc_scratch_bytes", "eb_layer_step_mixed_noalloc",
+           "eb_packed_weight_bytes", "eb_pack_weight")
 
 
 class EbError(RuntimeError):
@@ -49,7 +50,8 @@ class LayerConfig(ctypes.Structure):
 class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")] + \
         [("w_dtype", ctypes.c_int32)] + [(n, ctypes.c_void_p) for n in ("s_qkv", "s_o", "s_gate_up", "s_down")] + \
-        [(n, ctypes.c_void_p) for n in ("w_router", "w_experts_gate_up", "w_experts_down", "q_norm", "k_norm")]
+        [(n, ctypes.c_void_p) for n in ("w_router", "w_experts_gate_up", "w_experts_down", "q_norm", "k_norm")] + \
+        [(n, ctypes.c_void_p) for n in ("p_qkv", "p_o", "p_gate_up", "p_down")]
 
 
 W_BF16, W_FP8_E4M3 = 0, 1
@@ -96,6 +98,8 @@ def lib() -> ctypes.CDLL:
         "eb_op_gemm_workspace_bytes": (SZ, [I32, I32, I32]),
         "eb_op_gemm": (I32, [VP, VP, VP, VP, I32, I32, I32, I32, VP, SZ, VP]),
         "eb_op_gemm_w8": (I32, [VP, VP, VP, VP, VP, I32, I32, I32, I32, VP, SZ, VP]),
+        "eb_packed_weight_bytes": (SZ, [ctypes.c_int, ctypes.c_int]),
+        "eb_pack_weight": (I32, [VP, VP, ctypes.c_int, ctypes.c_int, VP]),
         "eb_op_moe_ffn_workspace_bytes": (SZ, [I32, I32, I32, I32, I32]),
         "eb_op_moe_ffn": (I32, [VP, VP, VP, VP, VP, I32, I32, I32, I32, I32, I32, VP, VP, VP, VP, SZ, VP]),
         "eb_op_rope_kv_append": (I32, [VP, VP, P(KvCache), P(Batch), VP, SZ, VP]),
@@ -175,9 +179,12 @@ def weights_struct(w: dict) -> LayerWeights:
     codes with float32 row scales under s_qkv, s_o, s_gate_up, s_down;
     a mixture-of-experts layer brings w_router, w_experts_gate_up and
     w_experts_down instead of w_gate_up and w_down; a layer with q/k norms
-    brings their gains under q_norm and k_norm."""
+    brings their gains under q_norm and k_norm; fragment-packed copies of
+    the bf16 projections (eb_pack_weight) go under p_qkv, p_o, p_gate_up,
+    p_down."""
     lw = LayerWeights(*[_ptr(w.get(k)) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")])
-    for k in ("w_router", "w_experts_gate_up", "w_experts_down", "q_norm", "k_norm"):
+    for k in ("w_router", "w_experts_gate_up", "w_experts_down", "q_norm", "k_norm", "p_qkv", "p_o", "p_gate_up",
+              "p_down"):
         if k in w:
             setattr(lw, k, _ptr(w[k]))
     if w["w_qkv"].dtype in _CODE_DTYPES:
@@ -361,6 +368,36 @@ def eb_op_gemm(A: torch.Tensor, W: torch.Tensor, epilogue: str = "store", residu
     ws = alloc_workspace(nb, A.device)
     _check(lib().eb_op_gemm(_ptr(A), _ptr(W), _ptr(out), _ptr(residual), M, N, K, EPILOGUES[epilogue], _ptr(ws),
                             ws.numel(), _stream(stream)))
+    return out
+
+
+def eb_packed_weight_bytes(rows: int, cols: int) -> int:
+    return int(lib().eb_packed_weight_bytes(rows, cols))
+
+
+def eb_pack_weight(W: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Fragment-packed copy of a bf16 [rows, cols] weight matrix (a flat
+    bf16 tensor of rows * cols elements)."""
+    if W.dtype != torch.bfloat16 or W.dim() != 2:
+        raise ValueError("W must be a 2-D bf16 tensor")
+    rows, cols = W.shape
+    out = torch.empty(rows * cols, dtype=torch.bfloat16, device=W.device) if out is None else out
+    if out.numel() * 2 < eb_packed_weight_bytes(rows, cols):
+        raise ValueError("out is smaller than the packed copy")
+    _check(lib().eb_pack_weight(_ptr(W), _ptr(out), rows, cols, _stream(stream)))
+    return out
+
+
+def pack_layer_weights(w: dict, stream=None) -> dict:
+    """The weights dict plus packed copies of its bf16 projections (those
+    whose shape has a packed form)."""
+    out = dict(w)
+    if w.get("w_qkv") is None or w["w_qkv"].dtype != torch.bfloat16:
+        return out
+    for src, dst in (("w_qkv", "p_qkv"), ("w_o", "p_o"), ("w_gate_up", "p_gate_up"), ("w_down", "p_down")):
+        t = w.get(src)
+        if t is not None and eb_packed_weight_bytes(*t.shape) > 0:
+            out[dst] = eb_pack_weight(t, stream=stream)
     return out
 
 

@@ -420,6 +420,8 @@ eb_status grow_events(std::vector<hipEvent_t> &pev, int layers) {
 
 // The nine stages of one layer on the stream: x -> y with weights w and
 // cache kvd; the batch metadata m is already in the workspace.
+static inline const uint16_t *pk(const void *p) { return static_cast<const uint16_t *>(p); }
+
 eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, const DevMeta &m, const StepBufs &B,
                      const uint16_t *xin, uint16_t *yout, int T, eb_mode mode, int layer, hipEvent_t *pev,
                      hipStream_t st) {
@@ -443,7 +445,7 @@ eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, con
     EB_STAGE(0, hipSuccess, "rmsnorm1");
     EB_STAGE(1,
              launch_gemm_prenorm(qp, xin, g1, w->w_qkv, w8 ? w->s_qkv : nullptr, T, sh.qkv_cols(), sh.hidden,
-                                 static_cast<float *>(B.gws), B.ssq, st),
+                                 static_cast<float *>(B.gws), B.ssq, st, w8 ? nullptr : pk(w->p_qkv)),
              "qkv gemm");
     EB_STAGE(2, launch_qkv_rope_append(sh, static_cast<const float *>(B.gws), qp.splits, B.ssq, B.qkv, kvd, m, st, gq, gk),
              "rope/kv append");
@@ -451,7 +453,7 @@ eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, con
     EB_STAGE(0, launch_rmsnorm(xin, g1, B.act, T, sh.hidden, sh.eps, st), "rmsnorm1");
     EB_STAGE(1,
              launch_gemm(qp, B.act, w->w_qkv, w8 ? w->s_qkv : nullptr, B.qkv, nullptr, T, sh.qkv_cols(), sh.hidden,
-                         EPI_STORE, B.gws, st),
+                         EPI_STORE, B.gws, st, nullptr, w8 ? nullptr : pk(w->p_qkv)),
              "qkv gemm");
     EB_STAGE(2, launch_rope_append(sh, B.qkv, kvd, m, st, gq, gk), "rope/kv append");
   }
@@ -463,7 +465,8 @@ eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, con
   NormFuse nf{static_cast<const uint16_t *>(w->mlp_norm), B.act, sh.eps, false};
   EB_STAGE(5,
            launch_gemm(plan_gemm(T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, w8), B.attn, w->w_o,
-                       w8 ? w->s_o : nullptr, B.h1, xin, T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, B.gws, st, &nf),
+                       w8 ? w->s_o : nullptr, B.h1, xin, T, sh.hidden, sh.nq * sh.hd, EPI_RESIDUAL, B.gws, st, &nf,
+                       w8 ? nullptr : pk(w->p_o)),
            "o gemm");
   EB_STAGE(6,
            nf.done ? hipSuccess
@@ -483,11 +486,12 @@ eb_status layer_body(eb_handle *h, const eb_layer_weights *w, const KV &kvd, con
   EB_STAGE(7,
            launch_gemm(plan_gemm(T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL, w8), B.act, w->w_gate_up,
                        w8 ? w->s_gate_up : nullptr, B.mlp, nullptr, T, 2 * sh.ffn, sh.hidden, EPI_SILU_MUL, B.gws,
-                       st),
+                       st, nullptr, w8 ? nullptr : pk(w->p_gate_up)),
            "gate/up gemm");
   EB_STAGE(8,
            launch_gemm(plan_gemm(T, sh.hidden, sh.ffn, EPI_RESIDUAL, w8), B.mlp, w->w_down,
-                       w8 ? w->s_down : nullptr, yout, B.h1, T, sh.hidden, sh.ffn, EPI_RESIDUAL, B.gws, st),
+                       w8 ? w->s_down : nullptr, yout, B.h1, T, sh.hidden, sh.ffn, EPI_RESIDUAL, B.gws, st, nullptr,
+                       w8 ? nullptr : pk(w->p_down)),
            "down gemm");
 #undef EB_STAGE
   return EB_OK;
@@ -830,6 +834,20 @@ eb_status op_gemm(const void *A, const void *W, const float *wscale, void *out, 
 eb_status eb_op_gemm(const void *A, const void *W, void *out, const void *residual, int32_t M, int32_t N, int32_t K,
                      eb_epilogue epi, void *ws, size_t ws_bytes, void *stream) {
   return op_gemm(A, W, nullptr, out, residual, M, N, K, epi, ws, ws_bytes, stream);
+}
+
+size_t eb_packed_weight_bytes(int rows, int cols) {
+  if (rows <= 0 || cols <= 0 || rows % 16 || cols % 32) return 0;
+  if ((size_t)rows * cols * 2 >= ((size_t)1 << 31)) return 0;
+  return packed_weight_bytes(rows, cols);
+}
+
+eb_status eb_pack_weight(const void *w, void *packed, int rows, int cols, void *stream) {
+  if (!w || !packed) return fail(EB_ERR_NULL, "w or packed is NULL");
+  if (eb_packed_weight_bytes(rows, cols) == 0) return fail(EB_ERR_CONFIG, "shape has no packed form");
+  const hipError_t e = pack_weight(static_cast<const uint16_t *>(w), static_cast<uint16_t *>(packed), rows, cols,
+                                   static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? EB_OK : fail(EB_ERR_HIP, hipGetErrorString(e));
 }
 
 eb_status eb_op_gemm_w8(const void *A, const void *W, const float *w_scale, void *out, const void *residual,

@@ -131,14 +131,20 @@ struct NormFuse {
 };
 hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, const float *wscale, uint16_t *out,
                        const uint16_t *residual, int M, int N, int K, int epi, void *ws, hipStream_t st,
-                       NormFuse *nf = nullptr);
+                       NormFuse *nf = nullptr, const uint16_t *Wp = nullptr);
+// Wp: optional fragment-packed copy of a bf16 W (pack_weight); the
+// weight-streaming plans read it instead of W when packed_ok(N, K, epi).
+bool packed_ok(int N, int K, int epi);
+size_t packed_weight_bytes(int N, int K);
+hipError_t pack_weight(const uint16_t *W, uint16_t *P, int N, int K, hipStream_t st);
 
 // The weight-streaming GEMM on the RMSNorm that precedes it: stages bf16(x *
 // gamma) as A and writes the split-K partials only (p.kind 0 with
 // p.splits >= 2), plus each row's partial sum of squares of x into ssq
 // [p.splits][M]; the consumer applies 1 / sqrt(mean(x^2) + eps) to the sum.
 hipError_t launch_gemm_prenorm(const GemmPlan &p, const uint16_t *x, const uint16_t *gamma, const void *W,
-                               const float *wscale, int M, int N, int K, float *part, float *ssq, hipStream_t st);
+                               const float *wscale, int M, int N, int K, float *part, float *ssq, hipStream_t st,
+                               const uint16_t *Wp = nullptr);
 
 // Mixture-of-experts block.  The grouped GEMM multiplies row tiles of
 // expert-sorted rows (tables [3][max_tiles]: expert, first sorted row, rows;

@@ -296,6 +296,234 @@ __global__ __launch_bounds__(256) void k_gemm_skinny(const uint16_t *__restrict_
   }
 }
 
+// Fragment-packed weights.  A packed copy of W [N][K] (N % 16 == 0,
+// K % 32 == 0) stores each 16-row x 32-column block as one contiguous
+// 1 KiB run in the lane order of the MFMA's 16x16x32 operand: lane l holds
+// row 16 g + l % 16, columns 32 c + 8 (l / 16) .. + 7, and block (g, c) sits
+// at byte ((g * K / 32) + c) * 1024.  One 16-byte load per lane then fills an
+// operand register with 1 KiB of contiguous memory.
+__global__ __launch_bounds__(256) void k_pack_weight(const uint16_t *__restrict__ W, uint16_t *__restrict__ P, int N,
+                                                     int K) {
+  const size_t q = (size_t)blockIdx.x * 256 + threadIdx.x;  // 16-byte chunk of P
+  const size_t nchunks = (size_t)N * K / 8;
+  if (q >= nchunks) return;
+  const int kc32 = K / 32;
+  const size_t frag = q >> 6;
+  const int l = (int)(q & 63);
+  const size_t g = frag / kc32;
+  const int c = (int)(frag - g * kc32);
+  const size_t row = g * 16 + (l & 15);
+  const size_t k = (size_t)c * 32 + (l >> 4) * 8;
+  *reinterpret_cast<u32x4_t *>(P + q * 8) = *reinterpret_cast<const u32x4_t *>(W + row * K + k);
+}
+
+// The weight-streaming kernel on packed bf16 weights.  Same block, columns,
+// split ranges, products and epilogues as k_gemm_skinny<false>, but each
+// wave loads its W operands straight into registers from the packed copy
+// (every element of W is used by one wave only, so W needs no LDS), three
+// 128-wide K stages ahead in a ring of three register sets; only A passes
+// through LDS (three buffers).  The products take the same operands in the
+// same order, so the sums are bitwise those of k_gemm_skinny<false>.
+constexpr int SP_LDS = 3 * SK_BM * SK_ROWB;
+template <bool PRENORM = false>
+__global__ __launch_bounds__(256) void k_gemm_skinny_packed(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Wp,
+                                                            uint16_t *__restrict__ out, const uint16_t *__restrict__ res,
+                                                            float *__restrict__ part, int M, int N, int K, int epi,
+                                                            int ksteps_per_split, int tiles, int mt, int per_xcd,
+                                                            const uint16_t *__restrict__ gamma = nullptr,
+                                                            float *__restrict__ ssq = nullptr) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t sp_lds[];  // [3][64 A rows][SK_ROWB]
+  const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (t >= tiles) return;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n0 = (t / mt) * SW_BN;
+  const int split = blockIdx.y;
+  const int m0 = (t % mt) * SK_BM;
+  const int kbeg = split * ksteps_per_split * 32;
+  const int kend = min(K, kbeg + ksteps_per_split * 32);
+  const int nst = kend > kbeg ? (kend - kbeg + SK_KC - 1) / SK_KC : 0;
+  const buf_rsrc_t ra = make_rsrc(A, (int)min((size_t)M * K * 2, (size_t)0x7FFFFFFF));
+  const buf_rsrc_t rw = make_rsrc(Wp, (int)min((size_t)N * K * 2, (size_t)0x7FFFFFFF));
+
+  // W: fragment f of this wave covers W rows wr_f .. wr_f + 15 (a 16-aligned
+  // run, or none); its 32-wide K step kc is the 1 KiB run at
+  // (wr_f / 16 * K / 32 + kc) * 1024, of which this lane reads 16 bytes.
+  uint32_t wbase[2];
+  bool wok[2];
+#pragma unroll
+  for (int f = 0; f < 2; ++f) {
+    const int wr = w_row_of(n0 + sw_col(wave, f, 0), N, epi);
+    wok[f] = wr >= 0;
+    wbase[f] = wok[f] ? ((uint32_t)(wr >> 4) * (uint32_t)(K >> 5)) * 1024u + (uint32_t)lane * 16u : 0u;
+  }
+  const int kc0 = kbeg >> 5, kc_end = kend >> 5;
+  u32x4_t w0[2][4], w1[2][4], w2[2][4];
+  auto wload = [&](int s, u32x4_t (&wr)[2][4]) {
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int kc = kc0 + s * 4 + ks;
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+        wr[f][ks] = buf_ld_u32x4<kAuxNT>(
+            rw, (int)(wok[f] && s < nst && kc < kc_end ? wbase[f] + (uint32_t)kc * 1024u : 0x80000000u));
+    }
+  };
+
+  // A: thread t moves 16-byte chunk t % 16 of tile rows t / 16 + 16 j (j < 4)
+  const int ch = tid & 15, r0 = tid >> 4;
+  uint32_t aoff[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int m = m0 + r0 + 16 * j;
+    aoff[j] = m < M ? ((uint32_t)m * (uint32_t)K + (uint32_t)(ch * 8)) * 2u : 0x80000000u;
+  }
+  u32x4_t aa[4];
+  u32x4_t ga = {0u, 0u, 0u, 0u};
+  float ssacc[4] = {0.f, 0.f, 0.f, 0.f};
+  const buf_rsrc_t rg = make_rsrc(PRENORM ? gamma : A, PRENORM ? K * 2 : 16);
+  auto aload = [&](int s) {
+    const int k = kbeg + s * SK_KC + ch * 8;
+    const bool ok = s < nst && k < kend;
+    const uint32_t kb = (uint32_t)(kbeg + s * SK_KC) * 2u;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) aa[j] = buf_ld_u32x4<0>(ra, (int)(ok ? aoff[j] + kb : 0x80000000u));
+    if constexpr (PRENORM) ga = buf_ld_u32x4<0>(rg, (int)(ok ? (uint32_t)(k * 2) : 0x80000000u));
+  };
+  const bool first_col_tile = n0 == 0;
+  auto awrite = [&](int buf) {
+    uint8_t *b = sp_lds + buf * SK_BM * SK_ROWB;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      u32x4_t av = aa[j];
+      if constexpr (PRENORM) {
+        if (first_col_tile) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float lo = bf16_lo(aa[j][e]), hi = bf16_hi(aa[j][e]);
+            ssacc[j] += lo * lo + hi * hi;
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          av[e] = bf16_pair_rne(bf16_lo(aa[j][e]) * bf16_lo(ga[e]), bf16_hi(aa[j][e]) * bf16_hi(ga[e]));
+      }
+      *reinterpret_cast<u32x4_t *>(b + (r0 + 16 * j) * SK_ROWB + ch * 16) = av;
+    }
+  };
+  f32x4_t acc[2][4];
+#pragma unroll
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[f][i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int lr = lane & 15, lg = lane >> 4;
+  auto compute = [&](int buf, const u32x4_t (&wr)[2][4]) {
+    const uint8_t *b = sp_lds + buf * SK_BM * SK_ROWB;
+#pragma unroll
+    for (int ks = 0; ks < SK_KC / 32; ++ks) {
+      u32x4_t af[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        af[i] = *reinterpret_cast<const u32x4_t *>(b + (i * 16 + lr) * SK_ROWB + (ks * 4 + lg) * 16);
+#pragma unroll
+      for (int f = 0; f < 2; ++f)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[f][i] = mfma16x16x32(wr[f][ks], af[i], acc[f][i]);
+    }
+  };
+  // Stage s: compute(s) from A buffer s % 3 and W set s % 3; write A(s + 2)
+  // (loaded during stage s - 1) into buffer (s + 2) % 3; load A(s + 3), then
+  // W(s + 3) into the set just consumed; one barrier.  A's loads go out
+  // before W's so that waiting for A(s + 2) never waits for W(s + 2).
+  aload(0);
+  wload(0, w0);
+  awrite(0);
+  aload(1);
+  wload(1, w1);
+  awrite(1);
+  aload(2);
+  wload(2, w2);
+  __syncthreads();
+  auto stage = [&](int s, int buf, u32x4_t (&wr)[2][4]) {
+    compute(buf, wr);
+    awrite(buf == 0 ? 2 : buf - 1);
+    aload(s + 3);
+    wload(s + 3, wr);
+    __syncthreads();
+  };
+  int s = 0;
+  for (; s + 3 <= nst; s += 3) {
+    stage(s, 0, w0);
+    stage(s + 1, 1, w1);
+    stage(s + 2, 2, w2);
+  }
+  // one or two stages left: A(s) and A(s + 1) already sit in buffers 0 and 1
+  if (s < nst) compute(0, w0);
+  if (s + 1 < nst) compute(1, w1);
+  if constexpr (PRENORM) {
+    if (first_col_tile) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float v = group_sum<16>(ssacc[j]);
+        const int m = m0 + r0 + 16 * j;
+        if (ch == 0 && m < M) ssq[(size_t)split * M + m] = v;
+      }
+    }
+  }
+
+  const int ncols = logical_cols(N, epi);
+  int cf[2];
+#pragma unroll
+  for (int f = 0; f < 2; ++f) cf[f] = n0 + sw_col(wave, f, 4 * lg);
+  if (part) {
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = m0 + i * 16 + lr;
+        if (m < M && cf[f] < ncols)
+          *reinterpret_cast<f32x4_t *>(part + ((size_t)split * M + m) * ncols + cf[f]) = acc[f][i];
+      }
+    return;
+  }
+  if (epi == EPI_SILU_MUL) {
+    const int F = N >> 1;
+    const int fo = ((n0 + (wave >> 1) * 64) >> 1) + (wave & 1) * 16 + 4 * lg;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + i * 16 + lr;
+      if (m < M && fo < F) {
+        const f32x4_t g = acc[0][i], u = acc[1][i];
+        const u32x2_t w = {pack_bf16x2(silu_f(g[0]) * u[0], silu_f(g[1]) * u[1]),
+                           pack_bf16x2(silu_f(g[2]) * u[2], silu_f(g[3]) * u[3])};
+        *reinterpret_cast<u32x2_t *>(out + (size_t)m * F + fo) = w;
+      }
+    }
+    return;
+  }
+#pragma unroll
+  for (int f = 0; f < 2; ++f) {
+    const int n = cf[f];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + i * 16 + lr;
+      if (m < M && n < N) {
+        f32x4_t v = acc[f][i];
+        if (epi == EPI_RESIDUAL) {
+          const u32x2_t r = *reinterpret_cast<const u32x2_t *>(res + (size_t)m * N + n);
+          v[0] += bf16_lo(r[0]);
+          v[1] += bf16_hi(r[0]);
+          v[2] += bf16_lo(r[1]);
+          v[3] += bf16_hi(r[1]);
+        }
+        const u32x2_t w = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+        *reinterpret_cast<u32x2_t *>(out + (size_t)m * N + n) = w;
+      }
+    }
+  }
+}
+
 // Sum split-K partials (logical column space) and apply the epilogue.
 __global__ __launch_bounds__(256) void k_gemm_splitk_epilogue(const float *__restrict__ part, int splits,
                                                               uint16_t *__restrict__ out,
@@ -1001,8 +1229,26 @@ GemmPlan plan_gemm(int M, int N, int K, int epi, bool w8) {
   return p;
 }
 
+bool packed_ok(int N, int K, int epi) {
+  if (N <= 0 || K <= 0 || N % 16 || K % 32) return false;
+  if (epi == EPI_SILU_MUL && (N / 2) % 16) return false;  // gate and up runs must stay 16-aligned
+  return (size_t)N * K * 2 < ((size_t)1 << 31);
+}
+
+size_t packed_weight_bytes(int N, int K) { return (size_t)N * K * 2; }
+
+hipError_t pack_weight(const uint16_t *W, uint16_t *P, int N, int K, hipStream_t st) {
+  if (!W || !P || N <= 0 || K <= 0 || N % 16 || K % 32) return hipErrorInvalidValue;
+  const size_t chunks = (size_t)N * K / 8;
+  const size_t blocks = (chunks + 255) / 256;
+  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_pack_weight, dim3((unsigned)blocks), dim3(256), 0, st, W, P, N, K);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, const float *wscale, uint16_t *out,
-                       const uint16_t *res, int M, int N, int K, int epi, void *ws, hipStream_t st, NormFuse *nf) {
+                       const uint16_t *res, int M, int N, int K, int epi, void *ws, hipStream_t st, NormFuse *nf,
+                       const uint16_t *Wp) {
   if (nf) nf->done = false;
   if (M <= 0) return hipSuccess;
   const bool w8 = wscale != nullptr;
@@ -1020,6 +1266,9 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, cons
     if (w8)
       hipLaunchKernelGGL(k_gemm_skinny<true>, grid, dim3(256), SW_LDS, st, A, W, wscale, out, res, part, M, N, K, epi,
                          per, tiles, mt, per_xcd);
+    else if (Wp && packed_ok(N, K, epi))  // (SW_LDS of LDS keeps one block per CU)
+      hipLaunchKernelGGL(k_gemm_skinny_packed<false>, grid, dim3(256), SW_LDS, st, A, Wp, out, res, part, M, N, K,
+                         epi, per, tiles, mt, per_xcd);
     else
       hipLaunchKernelGGL(k_gemm_skinny<false>, grid, dim3(256), SW_LDS, st, A, W, wscale, out, res, part, M, N, K,
                          epi, per, tiles, mt, per_xcd);
@@ -1073,7 +1322,8 @@ hipError_t launch_gemm(const GemmPlan &p, const uint16_t *A, const void *W, cons
 }
 
 hipError_t launch_gemm_prenorm(const GemmPlan &p, const uint16_t *x, const uint16_t *gamma, const void *W,
-                               const float *wscale, int M, int N, int K, float *part, float *ssq, hipStream_t st) {
+                               const float *wscale, int M, int N, int K, float *part, float *ssq, hipStream_t st,
+                               const uint16_t *Wp) {
   if (M <= 0) return hipSuccess;
   if (p.kind != 0 || p.splits < 2) return hipErrorInvalidValue;
   const int nsteps = (K + 31) / 32;
@@ -1085,6 +1335,9 @@ hipError_t launch_gemm_prenorm(const GemmPlan &p, const uint16_t *x, const uint1
   if (wscale)
     hipLaunchKernelGGL((k_gemm_skinny<true, true>), grid, dim3(256), SW_LDS, st, x, W, wscale, nullptr, nullptr, part,
                        M, N, K, (int)EPI_STORE, per, tiles, mt, per_xcd, gamma, ssq);
+  else if (Wp && packed_ok(N, K, EPI_STORE))
+    hipLaunchKernelGGL((k_gemm_skinny_packed<true>), grid, dim3(256), SW_LDS, st, x, Wp, nullptr, nullptr, part, M, N,
+                       K, (int)EPI_STORE, per, tiles, mt, per_xcd, gamma, ssq);
   else
     hipLaunchKernelGGL((k_gemm_skinny<false, true>), grid, dim3(256), SW_LDS, st, x, W, wscale, nullptr, nullptr,
                        part, M, N, K, (int)EPI_STORE, per, tiles, mt, per_xcd, gamma, ssq);

@@ -155,3 +155,17 @@ def test_create_rejects_bad_config_before_touching_the_gpu():
     cfg = B.config_of(gen.TINY)
     assert B.lib().eb_create(ctypes.byref(cfg), 0, 64, ctypes.byref(h)) == -7
     assert B.lib().eb_create(ctypes.byref(cfg), 4, 64, None) == -1
+
+
+def test_packed_weight_shapes_host_only():
+    # the size of a packed copy and the shapes without one; a rejected shape
+    # returns before any device call
+    L = B.lib()
+    assert L.eb_packed_weight_bytes(16, 32) == 16 * 32 * 2
+    assert L.eb_packed_weight_bytes(28672, 4096) == 28672 * 4096 * 2
+    for rows, cols in [(0, 32), (16, 0), (17, 32), (16, 48), (8, 32), (-16, 32), (32768, 32768)]:
+        assert L.eb_packed_weight_bytes(rows, cols) == 0, (rows, cols)
+    fake = ctypes.c_void_p(0x1000)
+    code = {name: c for c, name in B.STATUS.items()}
+    assert L.eb_pack_weight(fake, fake, 16, 48, None) == code["EB_ERR_CONFIG"]
+    assert L.eb_pack_weight(None, fake, 16, 32, None) == code["EB_ERR_NULL"]
